@@ -1,0 +1,336 @@
+"""CPU oracle of the MiniMax Sparse Attention (MSA) inference hot path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, the package entry's ``smoke()``
+check and the benchmark's CPU-baseline leg may import or run this module.  It
+shares no code with the HIP path (no kernels, helpers, tables or constants)
+and imports nothing from the library package; the inputs it receives are bf16
+bit patterns (numpy ``uint16``) that it decodes itself.
+
+What it computes, in the paper's order and notation:
+
+* Index Branch (Sec. 3.1, index-projection / index-score / top-k equations):
+  token index scores S = q_idx . k_idx / sqrt(d_idx) over the visible tokens
+  j <= i, causal block max-pooling M_b = max_{j in B_b, j <= i} S_j (blocks
+  with no visible token score -inf), and Top-k block selection with the local
+  block always included (Sec. 3.1 last paragraph of "Index Branch"; Sec. 3.2
+  "Local Block"; Appendix C.2 final recipe: only the incomplete self block is
+  forced, no sink).
+* Main Branch (Sec. 3.1, sparse-attention equation): exact softmax attention of
+  each query head of group r over the causally visible tokens of the selected
+  blocks, using key/value head r; also the natural-log log-sum-exp.
+* Split combine (Sec. 4.2 "Two-phase forward"): merge of locally normalised
+  partials through their log-sum-exps.
+* Dense causal attention (Sec. 2.1, softmax-attention equation) and the FLOP
+  model of Sec. 3.3.
+
+Precision: float64 everywhere, with one deliberate exception.  Block
+selection is an integer decision taken from floating point; it is taken on
+each index dot product rounded once to float32 (the precision in which the GPU
+kernels take it), before the positive 1/sqrt(d_idx) scale, which cannot change
+the order (Sec. 4.1 "Exp-free selection": order-preserving maps leave Top-k
+unchanged).  Score gaps used by the tie rule are reported in float64 on the
+scaled scores S.
+
+Readings of passages the paper leaves open (all used below):
+
+ R1  Local block + Top-k: the local block lb = floor(p / B_k) takes one of the k
+     slots and the other k-1 slots go to the best other causal blocks
+     (Sec. 3.2 "Local Block": one slot is reserved, the remaining slots are
+     chosen by the Index Branch; Sec. 3.1: budget at most k*B_k tokens).
+ R2  Fewer causal blocks than k: all of them are selected; the row's id list is
+     padded with -1 (blocks without a visible token score -inf, Sec. 3.1).
+ R3  Ties: higher score first, then the lower block id.  Ids are returned in
+     ascending order (Sec. 4.1 reports unsorted outputs and identical index
+     sets across implementations; the order of the output is a convention).
+ R4  Score gap g of a row: scaled score of the last selected non-local block
+     minus that of the best unselected candidate; +inf when every candidate
+     is selected.
+ R5  No sink block is forced (Appendix C.2).
+ R6  Softmax scale 1/sqrt(d_h); log-sum-exp uses the natural log (Sec. 4.2
+     combine uses log/exp).
+ R7  A partial last block holds min(b*B_k, N) - (b-1)*B_k tokens (Sec. 2.3).
+ R8  Position convention: query row t of a sequence with kv_len keys and
+     q_rows query rows sits at absolute position kv_len - q_rows + t; its own
+     key is already in the cache (decode: p = kv_len - 1; chunked prefill is
+     right-aligned).  The paper does not discuss decode or chunked prefill.
+ R9  Index scores take the projected q_idx / k_idx as given (no RoPE on the
+     Index Branch is described).
+"""
+from __future__ import annotations
+
+import math
+from typing import Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+
+# --------------------------------------------------------------------------
+# representation
+# --------------------------------------------------------------------------
+def decode_bf16(bits: np.ndarray) -> np.ndarray:
+    """bf16 bit patterns (uint16) -> float64 values (exact)."""
+    u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+    return u32.view(np.float32).astype(np.float64)
+
+
+class Layout:
+    """Sequence layout: query rows of sequence s are q_offsets[s]..q_offsets[s+1];
+    its keys are rows kv_starts[s] .. kv_starts[s]+kv_lens[s] of the key side."""
+
+    def __init__(self, q_rows: Sequence[int], kv_lens: Sequence[int], kv_starts: Sequence[int]):
+        self.q_rows = [int(x) for x in q_rows]
+        self.kv_lens = [int(x) for x in kv_lens]
+        self.kv_starts = [int(x) for x in kv_starts]
+        self.q_offsets = [0]
+        for r in self.q_rows:
+            self.q_offsets.append(self.q_offsets[-1] + r)
+
+    @property
+    def total_q_rows(self) -> int:
+        return self.q_offsets[-1]
+
+    def locate(self, row: int) -> Tuple[int, int]:
+        """(sequence, absolute position) of packed query row ``row`` (R8)."""
+        s = int(np.searchsorted(self.q_offsets, row, side="right")) - 1
+        t = row - self.q_offsets[s]
+        return s, self.kv_lens[s] - self.q_rows[s] + t
+
+
+def layout_of(problem) -> Layout:
+    return Layout(problem.q_rows, problem.kv_lens, problem.kv_starts)
+
+
+# --------------------------------------------------------------------------
+# Index Branch (Sec. 3.1)
+# --------------------------------------------------------------------------
+def index_dots(iq_row: np.ndarray, ik: np.ndarray) -> np.ndarray:
+    """Unscaled index dot products q_idx^(r)_i . k_idx_j for every group r.
+
+    iq_row: (H_kv, d_idx) float64, ik: (n, d_idx) float64 -> (H_kv, n) float64.
+    bf16 x bf16 products are exact in float64; the sum is float64."""
+    return iq_row @ ik.T
+
+
+def block_maxima(dots_row: np.ndarray, pos: int, block_size: int) -> np.ndarray:
+    """Causal block max-pool of one (row, group): M_b over blocks
+    b = 0 .. ceil(n / B_k) - 1 of the visible prefix j <= pos; blocks whose
+    tokens are all in the future are -inf (Sec. 3.1, index-score equation)."""
+    n = dots_row.shape[0]
+    nblk = (n + block_size - 1) // block_size
+    out = np.full(nblk, -np.inf, dtype=dots_row.dtype)
+    vis = dots_row[:pos + 1]
+    full = (pos + 1) // block_size
+    if full:
+        out[:full] = vis[:full * block_size].reshape(full, block_size).max(axis=1)
+    if (pos + 1) % block_size:
+        out[full] = vis[full * block_size:].max()
+    return out
+
+
+def select_row(m_rank: np.ndarray, m_scaled: np.ndarray, pos: int, block_size: int,
+               topk: int) -> Tuple[np.ndarray, float]:
+    """Top-k with the local block forced (R1-R5) for one (row, group).
+
+    m_rank: block maxima used for ranking (float32-rounded unscaled dots),
+    m_scaled: the same maxima in float64 on the scaled score S (for the gap).
+    Returns (ids ascending, padded with -1 to ``topk``; gap g)."""
+    lb = pos // block_size
+    others = topk - 1                          # one slot is the local block's (R1)
+    ids = np.full(topk, -1, dtype=np.int32)
+    gap = math.inf
+    chosen = np.zeros(0, dtype=np.int64)
+    if lb > 0 and others > 0:
+        cand = np.arange(lb)                   # every other causal block is fully visible
+        # rank: higher score first, then the lower block id (R3)
+        order = np.lexsort((cand, -m_rank[:lb].astype(np.float64)))
+        chosen = cand[order[:others]]
+        if lb > others:
+            gap = float(m_scaled[order[others - 1]] - m_scaled[order[others]])
+    sel = np.sort(np.concatenate([chosen, [lb]]).astype(np.int64))
+    ids[:sel.shape[0]] = sel
+    return ids, gap
+
+
+def select_blocks(index_q_bits: np.ndarray, index_k_bits: np.ndarray, layout: Layout,
+                  block_size: int, topk: int, rows: Optional[Iterable[int]] = None,
+                  batch_rows: int = 256) -> Tuple[np.ndarray, np.ndarray]:
+    """Index Branch for the given packed query rows (all rows by default).
+
+    index_q_bits: (Tq, H_kv, d_idx) uint16; index_k_bits: (Tk, d_idx) uint16.
+    Returns block_ids (R, H_kv, topk) int32 and gaps (R, H_kv) float64."""
+    Tq, H_kv, d_idx = index_q_bits.shape
+    rows = list(range(Tq)) if rows is None else [int(r) for r in rows]
+    inv_sqrt = 1.0 / math.sqrt(d_idx)
+    ids = np.full((len(rows), H_kv, topk), -1, dtype=np.int32)
+    gaps = np.full((len(rows), H_kv), math.inf)
+    # group the requested rows by sequence so each batch shares its keys
+    by_seq = {}
+    for i, r in enumerate(rows):
+        s, pos = layout.locate(r)
+        by_seq.setdefault(s, []).append((i, r, pos))
+    for s, items in by_seq.items():
+        kv0, kvl = layout.kv_starts[s], layout.kv_lens[s]
+        for b0 in range(0, len(items), batch_rows):
+            batch = items[b0:b0 + batch_rows]
+            pmax = max(pos for _, _, pos in batch)
+            ik = decode_bf16(index_k_bits[kv0:kv0 + min(kvl, pmax + 1)])
+            iq = decode_bf16(index_q_bits[[r for _, r, _ in batch]])      # (B, H_kv, d)
+            dots = np.einsum("bhd,nd->bhn", iq, ik, optimize=True)        # float64
+            for j, (i, r, pos) in enumerate(batch):
+                for g in range(H_kv):
+                    d = dots[j, g]
+                    m_rank = block_maxima(d.astype(np.float32), pos, block_size)
+                    m_scaled = block_maxima(d, pos, block_size) * inv_sqrt
+                    ids[i, g], gaps[i, g] = select_row(m_rank, m_scaled, pos, block_size, topk)
+    return ids, gaps
+
+
+def row_block_scores(index_q_bits, index_k_bits, layout: Layout, row: int, group: int,
+                     block_size: int) -> np.ndarray:
+    """Scaled float64 block maxima M_b (Sec. 3.1) of one (row, group); used by
+    the tie rule to judge a selection that differs from the oracle's."""
+    s, pos = layout.locate(row)
+    kv0 = layout.kv_starts[s]
+    ik = decode_bf16(index_k_bits[kv0:kv0 + pos + 1])
+    iq = decode_bf16(index_q_bits[row, group])
+    d = ik @ iq
+    return block_maxima(d, pos, block_size) / math.sqrt(iq.shape[0])
+
+
+def selection_is_valid(ids: np.ndarray, block_scores: np.ndarray, pos: int, block_size: int,
+                       topk: int, tol: float) -> bool:
+    """A selection other than the oracle's is acceptable when it keeps the
+    local block, has min(k, lb+1) distinct causal blocks, and every selected
+    non-local block scores within ``tol`` of every unselected candidate."""
+    lb = pos // block_size
+    sel = [int(b) for b in ids if b >= 0]
+    if len(sel) != len(set(sel)) or len(sel) != min(topk, lb + 1) or lb not in sel:
+        return False
+    if any(b < 0 or b > lb for b in sel):
+        return False
+    if list(ids[:len(sel)]) != sorted(sel) or any(int(b) != -1 for b in ids[len(sel):]):
+        return False
+    nonlocal_sel = [b for b in sel if b != lb]
+    unsel = [b for b in range(lb) if b not in set(sel)]
+    if not nonlocal_sel or not unsel:
+        return True
+    return min(block_scores[b] for b in nonlocal_sel) >= max(block_scores[b] for b in unsel) - tol
+
+
+# --------------------------------------------------------------------------
+# Main Branch (Sec. 3.1, sparse-attention equation)
+# --------------------------------------------------------------------------
+def _attend(qh: np.ndarray, keys: np.ndarray, vals: np.ndarray, scale: float):
+    """Softmax attention of query heads qh (G, d) over keys/vals (n, d)."""
+    z = (qh @ keys.T) * scale                    # (G, n)
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    l = e.sum(axis=1, keepdims=True)
+    o = (e @ vals) / l
+    lse = (m + np.log(l))[:, 0]
+    return o, lse
+
+
+def selected_tokens(block_ids_row: Sequence[int], pos: int, block_size: int) -> np.ndarray:
+    """Causally visible tokens of the selected blocks (ids < 0 are padding)."""
+    parts = [np.arange(b * block_size, min((b + 1) * block_size, pos + 1))
+             for b in block_ids_row if b >= 0 and b * block_size <= pos]
+    return np.concatenate(parts) if parts else np.zeros(0, dtype=np.int64)
+
+
+def sparse_attention(q_bits, k_bits, v_bits, block_ids: np.ndarray, layout: Layout,
+                     block_size: int, scale: Optional[float] = None,
+                     rows: Optional[Iterable[int]] = None,
+                     block_ids_are_for_rows: bool = False):
+    """O (R, H_q, d_h) and LSE (R, H_q), float64, for the given packed rows.
+
+    q_bits: (Tq, H_q, d_h); k_bits, v_bits: (Tk, H_kv, d_h) uint16.
+    block_ids: (Tq, H_kv, k) for all rows, or (R, H_kv, k) aligned with
+    ``rows`` when ``block_ids_are_for_rows``.  Head h uses group h // G."""
+    Tq, H_q, d_h = q_bits.shape
+    H_kv = k_bits.shape[1]
+    G = H_q // H_kv
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_h)
+    rows = list(range(Tq)) if rows is None else [int(r) for r in rows]
+    O = np.zeros((len(rows), H_q, d_h))
+    L = np.zeros((len(rows), H_q))
+    for i, r in enumerate(rows):
+        s, pos = layout.locate(r)
+        kv0 = layout.kv_starts[s]
+        qf = decode_bf16(q_bits[r])
+        ids_row = block_ids[i] if block_ids_are_for_rows else block_ids[r]
+        for g in range(H_kv):
+            toks = selected_tokens(ids_row[g], pos, block_size)
+            keys = decode_bf16(k_bits[kv0 + toks, g])
+            vals = decode_bf16(v_bits[kv0 + toks, g])
+            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(
+                qf[g * G:(g + 1) * G], keys, vals, scale)
+    return O, L
+
+
+def dense_causal_attention(q_bits, k_bits, v_bits, layout: Layout, scale: Optional[float] = None,
+                           rows: Optional[Iterable[int]] = None):
+    """Causal GQA softmax attention over all tokens j <= p (Sec. 2.1)."""
+    Tq, H_q, d_h = q_bits.shape
+    H_kv = k_bits.shape[1]
+    G = H_q // H_kv
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_h)
+    rows = list(range(Tq)) if rows is None else [int(r) for r in rows]
+    O = np.zeros((len(rows), H_q, d_h))
+    L = np.zeros((len(rows), H_q))
+    for i, r in enumerate(rows):
+        s, pos = layout.locate(r)
+        kv0 = layout.kv_starts[s]
+        qf = decode_bf16(q_bits[r])
+        for g in range(H_kv):
+            keys = decode_bf16(k_bits[kv0:kv0 + pos + 1, g])
+            vals = decode_bf16(v_bits[kv0:kv0 + pos + 1, g])
+            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(
+                qf[g * G:(g + 1) * G], keys, vals, scale)
+    return O, L
+
+
+# --------------------------------------------------------------------------
+# Split combine (Sec. 4.2, "Two-phase forward")
+# --------------------------------------------------------------------------
+def combine_partials(lse_parts: np.ndarray, o_parts: np.ndarray):
+    """Merge S locally normalised partials: a = max_s LSE_s,
+    LSE = a + log sum_s exp(LSE_s - a), w_s = exp(LSE_s - LSE), O = sum_s w_s O_s.
+
+    lse_parts: (S,), o_parts: (S, d) -> (O (d,), LSE scalar)."""
+    lse_parts = np.asarray(lse_parts, dtype=np.float64)
+    a = lse_parts.max()
+    lse = a + math.log(np.exp(lse_parts - a).sum())
+    w = np.exp(lse_parts - lse)
+    return (w[:, None] * np.asarray(o_parts, dtype=np.float64)).sum(axis=0), lse
+
+
+# --------------------------------------------------------------------------
+# FLOP model (Sec. 3.3) and effective work
+# --------------------------------------------------------------------------
+def flops_gqa(N: int, H_q: int, d_h: int) -> float:
+    """Causal GQA attention FLOPs, F_GQA(N) = 2 H_q d_h N^2 (Sec. 3.3)."""
+    return 2.0 * H_q * d_h * N * N
+
+
+def flops_msa(N: int, H_q: int, H_kv: int, d_h: int, d_idx: int, block_size: int, k: int) -> float:
+    """F_MSA(N) = H_kv d_idx N^2 (Index Branch) + 4 H_q d_h N k B_k (Main Branch)."""
+    return float(H_kv) * d_idx * N * N + 4.0 * H_q * d_h * N * k * block_size
+
+
+def effective_main_flops(block_ids: np.ndarray, positions: np.ndarray, H_q: int, d_h: int,
+                         block_size: int) -> float:
+    """4 d_h x (sum over rows and query heads of the number of attended
+    tokens): QK^T and PV each cost 2 d_h FLOPs per (query head, token)."""
+    H_kv = block_ids.shape[1]
+    G = H_q // H_kv
+    total = 0
+    for i in range(block_ids.shape[0]):
+        p = int(positions[i])
+        for g in range(H_kv):
+            for b in block_ids[i, g]:
+                if b >= 0 and b * block_size <= p:
+                    total += min((b + 1) * block_size, p + 1) - b * block_size
+    return 4.0 * d_h * G * total

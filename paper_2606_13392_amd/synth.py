@@ -1,0 +1,308 @@
+"""Seeded synthetic inputs for the MSA inference hot path.
+
+This module draws the inputs that both the HIP path (tests, bench) and the CPU
+oracle consume.  It holds none of the method's arithmetic: it draws N(0,1)
+values, optionally plants "relevant" index-key blocks, rounds each tensor once
+to bf16 (round to nearest even) and describes the sequence layout.
+
+Layout conventions (shared by every entry point of the library):
+
+* a batch is ``num_seqs`` sequences; sequence ``s`` owns query rows
+  ``q_offsets[s] .. q_offsets[s+1]`` of the packed query-side tensors and key
+  rows ``kv_starts[s] .. kv_starts[s] + kv_lens[s]`` of the key-side tensors;
+* query row ``t`` (0-based inside its sequence) sits at absolute position
+  ``kv_lens[s] - q_rows[s] + t``: its own key/value (and index key) are already
+  in the cache.  Prefill has ``q_rows == kv_len``; decode has ``q_rows == 1``.
+
+Two backends: ``numpy`` (row-addressable chunks, used by CPU tests and small
+GPU cases) and ``torch`` (draws directly on a device, used for the large
+workloads whose host-side generation would take minutes).
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, List, Optional
+
+import numpy as np
+
+CHUNK_ROWS = 65536
+
+# tensor ids used to derive independent streams from one seed
+TID_INDEX_Q, TID_INDEX_K, TID_Q, TID_K, TID_V, TID_PLANT, TID_LENS = range(7)
+
+
+# --------------------------------------------------------------------------
+# bf16 helpers (representation only)
+# --------------------------------------------------------------------------
+def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to bf16 (nearest, ties to even); return uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounding = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
+    return ((u + rounding) >> np.uint32(16)).astype(np.uint16)
+
+
+def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+# --------------------------------------------------------------------------
+# problem description
+# --------------------------------------------------------------------------
+@dataclasses.dataclass
+class Problem:
+    """Shapes, hyper-parameters and sequence layout of one workload."""
+
+    name: str
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    d_idx: int
+    block_size: int
+    topk: int
+    q_rows: List[int]
+    kv_lens: List[int]
+    kv_starts: List[int]
+    total_kv_rows: int
+    seed: int
+    planted_blocks_per_group: int = 0
+    plant_alpha: Optional[float] = None   # default 2*sqrt(d_idx)
+    description: str = ""
+
+    @property
+    def num_seqs(self) -> int:
+        return len(self.q_rows)
+
+    @property
+    def q_offsets(self) -> List[int]:
+        out = [0]
+        for r in self.q_rows:
+            out.append(out[-1] + r)
+        return out
+
+    @property
+    def total_q_rows(self) -> int:
+        return sum(self.q_rows)
+
+    @property
+    def max_q_rows(self) -> int:
+        return max(self.q_rows) if self.q_rows else 0
+
+    @property
+    def max_kv_len(self) -> int:
+        return max(self.kv_lens) if self.kv_lens else 0
+
+    @property
+    def group_size(self) -> int:
+        return self.num_q_heads // self.num_kv_heads
+
+    def positions(self) -> np.ndarray:
+        """Absolute position of every packed query row (int64)."""
+        pos = np.empty(self.total_q_rows, dtype=np.int64)
+        off = 0
+        for s, qr in enumerate(self.q_rows):
+            pos[off:off + qr] = self.kv_lens[s] - qr + np.arange(qr)
+            off += qr
+        return pos
+
+    def seq_of_row(self) -> np.ndarray:
+        out = np.empty(self.total_q_rows, dtype=np.int64)
+        off = 0
+        for s, qr in enumerate(self.q_rows):
+            out[off:off + qr] = s
+            off += qr
+        return out
+
+
+def packed_problem(name, q_rows, kv_lens, *, num_q_heads, num_kv_heads, head_dim=128,
+                   d_idx=64, block_size=64, topk=8, seed=0, planted=0, description="",
+                   kv_pad_to: Optional[int] = None) -> Problem:
+    """Sequences packed back to back in the key-side tensors.
+
+    ``kv_pad_to`` places sequence ``s`` at key row ``s * kv_pad_to`` instead
+    (a padded cache, as decode uses)."""
+    assert len(q_rows) == len(kv_lens)
+    for qr, kl in zip(q_rows, kv_lens):
+        assert 0 <= qr <= kl
+    starts = []
+    if kv_pad_to is None:
+        acc = 0
+        for kl in kv_lens:
+            starts.append(acc)
+            acc += kl
+        total = acc
+    else:
+        assert all(kl <= kv_pad_to for kl in kv_lens)
+        starts = [s * kv_pad_to for s in range(len(kv_lens))]
+        total = kv_pad_to * len(kv_lens)
+    return Problem(name=name, num_q_heads=num_q_heads, num_kv_heads=num_kv_heads,
+                   head_dim=head_dim, d_idx=d_idx, block_size=block_size, topk=topk,
+                   q_rows=list(q_rows), kv_lens=list(kv_lens), kv_starts=starts,
+                   total_kv_rows=total, seed=seed, planted_blocks_per_group=planted,
+                   description=description)
+
+
+def chunked_contexts(seed: int, num_seqs: int, lo: int, hi: int) -> List[int]:
+    """Cached context lengths drawn log-uniformly in [lo, hi]."""
+    rng = np.random.default_rng([seed, TID_LENS])
+    u = rng.uniform(math.log(lo), math.log(hi), size=num_seqs)
+    return [int(math.floor(math.exp(x))) for x in u]
+
+
+# The five workloads the library is measured on.
+def workload(name: str) -> Problem:
+    if name == "prefill_4k":
+        return packed_problem(name, [4096], [4096], num_q_heads=8, num_kv_heads=2, topk=8,
+                              seed=1001, description="prefill T=4096, 8q/2kv, k=8, i.i.d. N(0,1)")
+    if name == "prefill_32k":
+        return packed_problem(name, [32768], [32768], num_q_heads=64, num_kv_heads=8, topk=32,
+                              seed=1002, planted=16,
+                              description="prefill T=32768, 64q/8kv, k=32, 16 planted blocks/group")
+    if name == "decode_128k":
+        return packed_problem(name, [1] * 64, [131072] * 64, num_q_heads=64, num_kv_heads=8,
+                              topk=32, seed=1003, kv_pad_to=131072,
+                              description="decode 64 seqs x 1 token, context 131072, 64q/8kv, k=32")
+    if name == "prefill_1m":
+        return packed_problem(name, [1 << 20], [1 << 20], num_q_heads=64, num_kv_heads=8, topk=64,
+                              seed=1004, planted=32,
+                              description="prefill T=1048576, 64q/8kv, k=64, 32 planted blocks/group")
+    if name == "chunked_8x8k":
+        ctx = chunked_contexts(1005, 8, 16384, 524288)
+        return packed_problem(name, [8192] * 8, [c + 8192 for c in ctx], num_q_heads=64,
+                              num_kv_heads=8, topk=48, seed=1005,
+                              description="chunked prefill, 8 seqs x 8192 new rows on 16K-512K contexts, k=48")
+    raise KeyError(name)
+
+
+WORKLOADS = ["prefill_4k", "prefill_32k", "decode_128k", "prefill_1m", "chunked_8x8k"]
+
+
+# --------------------------------------------------------------------------
+# numpy backend (row addressable)
+# --------------------------------------------------------------------------
+def _normal_rows(seed: int, tid: int, rows: int, row_width: int, row0: int = 0,
+                 nrows: Optional[int] = None) -> np.ndarray:
+    """N(0,1) float32 rows [row0, row0+nrows) of a (rows, row_width) tensor.
+
+    Rows are drawn in chunks of CHUNK_ROWS from default_rng([seed, tid, chunk]),
+    so any row range is reproducible without drawing the rows before it."""
+    if nrows is None:
+        nrows = rows - row0
+    out = np.empty((nrows, row_width), dtype=np.float32)
+    r = row0
+    while r < row0 + nrows:
+        c = r // CHUNK_ROWS
+        c0 = c * CHUNK_ROWS
+        c1 = min(c0 + CHUNK_ROWS, rows)
+        rng = np.random.default_rng([seed, tid, c])
+        chunk = rng.standard_normal((c1 - c0, row_width), dtype=np.float32)
+        a = r - c0
+        b = min(c1, row0 + nrows) - c0
+        out[r - row0:r - row0 + (b - a)] = chunk[a:b]
+        r = c0 + b
+    return out
+
+
+def plant_plan(p: Problem) -> Dict[int, List[int]]:
+    """Per group r: the key blocks (block index inside sequence 0) that get
+    shifted toward group r's random index query.  Blocks are disjoint across
+    groups (the index key head is shared)."""
+    if p.planted_blocks_per_group <= 0:
+        return {}
+    nblk = p.kv_lens[0] // p.block_size
+    need = p.planted_blocks_per_group * p.num_kv_heads
+    assert nblk > need
+    rng = np.random.default_rng([p.seed, TID_PLANT])
+    blocks = rng.choice(nblk - 1, size=need, replace=False)  # never the last block
+    plan = {}
+    for r in range(p.num_kv_heads):
+        plan[r] = sorted(int(b) for b in blocks[r * p.planted_blocks_per_group:
+                                                   (r + 1) * p.planted_blocks_per_group])
+    return plan
+
+
+def plant_anchor_rows(p: Problem) -> List[int]:
+    rng = np.random.default_rng([p.seed, TID_PLANT, 1])
+    return [int(x) for x in rng.integers(0, p.total_q_rows, size=p.num_kv_heads)]
+
+
+def _plant_alpha(p: Problem) -> float:
+    return p.plant_alpha if p.plant_alpha is not None else 2.0 * math.sqrt(p.d_idx)
+
+
+def generate_numpy(p: Problem) -> Dict[str, np.ndarray]:
+    """All five input tensors as uint16 bf16 bit patterns (numpy)."""
+    Tq, Tk = p.total_q_rows, p.total_kv_rows
+    out = {}
+    iq = _normal_rows(p.seed, TID_INDEX_Q, Tq, p.num_kv_heads * p.d_idx)
+    out["index_q"] = bf16_bits_from_f32(iq).reshape(Tq, p.num_kv_heads, p.d_idx)
+    ik = _normal_rows(p.seed, TID_INDEX_K, Tk, p.d_idx)
+    if p.planted_blocks_per_group:
+        iqf = f32_from_bf16_bits(out["index_q"])
+        anchors = plant_anchor_rows(p)
+        alpha = _plant_alpha(p)
+        base = p.kv_starts[0]
+        for r, blocks in plant_plan(p).items():
+            u = iqf[anchors[r], r].astype(np.float64)
+            u = (u / np.linalg.norm(u)).astype(np.float32)
+            for b in blocks:
+                ik[base + b * p.block_size: base + (b + 1) * p.block_size] += alpha * u
+    out["index_k"] = bf16_bits_from_f32(ik)
+    out["q"] = bf16_bits_from_f32(_normal_rows(p.seed, TID_Q, Tq, p.num_q_heads * p.head_dim)
+                                  ).reshape(Tq, p.num_q_heads, p.head_dim)
+    out["k"] = bf16_bits_from_f32(_normal_rows(p.seed, TID_K, Tk, p.num_kv_heads * p.head_dim)
+                                  ).reshape(Tk, p.num_kv_heads, p.head_dim)
+    out["v"] = bf16_bits_from_f32(_normal_rows(p.seed, TID_V, Tk, p.num_kv_heads * p.head_dim)
+                                  ).reshape(Tk, p.num_kv_heads, p.head_dim)
+    return out
+
+
+# --------------------------------------------------------------------------
+# torch backend (draws on the device; for the large workloads)
+# --------------------------------------------------------------------------
+def generate_torch(p: Problem, device, tensors=("index_q", "index_k", "q", "k", "v")):
+    """Same distributions and planting recipe, drawn with torch's generator on
+    ``device``.  Returns bf16 torch tensors.  (Values differ from the numpy
+    backend; the oracle reads whatever rows it needs back from these inputs.)"""
+    import torch
+
+    def draw(tid, shape):
+        g = torch.Generator(device=device)
+        g.manual_seed(int(p.seed) * 1000003 + tid)
+        out = torch.empty(shape, dtype=torch.bfloat16, device=device)
+        flat = out.view(shape[0], -1)
+        step = max(1, (1 << 27) // max(1, flat.shape[1]))
+        for r0 in range(0, shape[0], step):
+            r1 = min(shape[0], r0 + step)
+            flat[r0:r1] = torch.randn((r1 - r0, flat.shape[1]), generator=g, device=device,
+                                      dtype=torch.float32).to(torch.bfloat16)
+        return out
+
+    Tq, Tk = p.total_q_rows, p.total_kv_rows
+    out = {}
+    if "index_q" in tensors or p.planted_blocks_per_group:
+        out["index_q"] = draw(TID_INDEX_Q, (Tq, p.num_kv_heads, p.d_idx))
+    if "index_k" in tensors:
+        g = torch.Generator(device=device)
+        g.manual_seed(int(p.seed) * 1000003 + TID_INDEX_K)
+        ik = torch.randn((Tk, p.d_idx), generator=g, device=device, dtype=torch.float32)
+        if p.planted_blocks_per_group:
+            anchors = plant_anchor_rows(p)
+            alpha = _plant_alpha(p)
+            base = p.kv_starts[0]
+            for r, blocks in plant_plan(p).items():
+                u = out["index_q"][anchors[r], r].float()
+                u = u / torch.linalg.vector_norm(u.double()).float()
+                for b in blocks:
+                    ik[base + b * p.block_size: base + (b + 1) * p.block_size] += alpha * u
+        out["index_k"] = ik.to(torch.bfloat16)
+        del ik
+    if "q" in tensors:
+        out["q"] = draw(TID_Q, (Tq, p.num_q_heads, p.head_dim))
+    if "k" in tensors:
+        out["k"] = draw(TID_K, (Tk, p.num_kv_heads, p.head_dim))
+    if "v" in tensors:
+        out["v"] = draw(TID_V, (Tk, p.num_kv_heads, p.head_dim))
+    if "index_q" not in tensors:
+        out.pop("index_q", None)
+    return out

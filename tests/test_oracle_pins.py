@@ -1,0 +1,60 @@
+"""The CPU oracle against what the paper and the mathematics fix (no GPU)."""
+import importlib.util
+import os
+
+import pytest
+
+import oracle.msa_oracle as O
+from tests import pins
+
+ORACLE_SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                          "oracle", "msa_oracle.py")
+
+
+@pytest.mark.parametrize("pin", pins.ALL_PINS, ids=lambda f: f.__name__)
+def test_oracle_pin(pin):
+    pin(O)
+
+
+# Plausible mistakes planted in a copy of the oracle; each must trip a pin.
+MUTATIONS = {
+    "rank_ascending": ("order = np.lexsort((cand, -m_rank[:lb].astype(np.float64)))",
+                       "order = np.lexsort((cand, m_rank[:lb].astype(np.float64)))"),
+    "tie_higher_id": ("order = np.lexsort((cand, -m_rank[:lb].astype(np.float64)))",
+                      "order = np.lexsort((-cand, -m_rank[:lb].astype(np.float64)))"),
+    "local_not_reserved": ("others = topk - 1                          # one slot",
+                           "others = topk                              # one slot"),
+    "causal_cut_off_by_one": ("vis = dots_row[:pos + 1]", "vis = dots_row[:pos]"),
+    "own_token_dropped": ("np.arange(b * block_size, min((b + 1) * block_size, pos + 1))",
+                          "np.arange(b * block_size, min((b + 1) * block_size, pos))"),
+    "no_softmax_scale": ("z = (qh @ keys.T) * scale", "z = (qh @ keys.T)"),
+    "lse_log2": ("lse = (m + np.log(l))[:, 0]", "lse = (m + np.log2(l))[:, 0]"),
+    "combine_weight_sign": ("w = np.exp(lse_parts - lse)", "w = np.exp(lse - lse_parts)"),
+    "flops_main_factor": ("4.0 * H_q * d_h * N * k * block_size", "2.0 * H_q * d_h * N * k * block_size"),
+    "left_aligned_positions": ("return s, self.kv_lens[s] - self.q_rows[s] + t", "return s, t"),
+    "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
+                             "O[i, g::H_kv], L[i, g::H_kv] = _attend(\n                qf[g::H_kv], keys, vals, scale)"),
+}
+
+
+def _mutant(name, old, new):
+    src = open(ORACLE_SRC).read()
+    assert src.count(old) >= 1, f"mutation {name} does not apply"
+    src = src.replace(old, new)
+    spec = importlib.util.spec_from_loader(f"oracle_mutant_{name}", loader=None)
+    mod = importlib.util.module_from_spec(spec)
+    exec(compile(src, f"<mutant {name}>", "exec"), mod.__dict__)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_oracle_mutations_are_caught(name):
+    old, new = MUTATIONS[name]
+    mod = _mutant(name, old, new)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(mod)
+        except Exception:
+            failed.append(pin.__name__)
+    assert failed, f"no pin catches mutation {name}"
