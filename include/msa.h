@@ -1,0 +1,157 @@
+/*
+ * msa.h -- C ABI of libmsa.so, the MI355X (gfx950) inference hot path of
+ * MiniMax Sparse Attention (MSA).
+ *
+ * The paper factors sparse attention into an indexer that picks which keys a
+ * query attends to and an exact attention over the picked keys (Sec. 2.2,
+ * two-stage equation).  MSA's indexer is block- and GQA-group-granular
+ * (Sec. 2.3; Sec. 3.1 "Index Branch"); its attention runs only over the
+ * selected blocks (Sec. 3.1 "Main Branch").  The library exports one call per
+ * stage and per inference phase:
+ *
+ *   msa_index_topk           Index Branch: block scores + Top-k (prefill and decode)
+ *   msa_sparse_attn_prefill  Main Branch for many query rows per sequence
+ *   msa_sparse_attn_decode   Main Branch for one query row per sequence
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every tensor argument is a DEVICE pointer to contiguous row-major memory
+ *   that the caller allocates, owns and keeps alive until the stream has
+ *   executed the call.  bf16 tensors hold IEEE bfloat16 bit patterns.
+ * - Calls are asynchronous on `stream` (0 = the null stream): they validate
+ *   their arguments on the host, launch kernels and return.  Results are
+ *   valid once the stream has reached them.  Nothing is launched when a call
+ *   returns an error.  No call synchronises the host with the device.
+ * - The library allocates no device memory.  Calls that need scratch space take
+ *   a caller-provided `workspace` of at least the size returned by the
+ *   matching *_workspace_size() query; the workspace is free again once the
+ *   stream has executed the call.  Calls that share a workspace must be ordered
+ *   on one stream.
+ * - The library keeps no global state; concurrent calls from several host
+ *   threads are safe when they use distinct outputs and workspaces.
+ * - NaN or Inf inputs give unspecified (but memory-safe) results.
+ *
+ * Sequence layout (struct msa_seqs)
+ * ---------------------------------
+ * A batch holds `num_seqs` sequences.  Sequence s owns the packed query rows
+ * q_offsets[s] .. q_offsets[s+1]-1 of the query-side tensors (index_q, q, o,
+ * lse, block_ids) and key rows kv_starts[s] .. kv_starts[s]+kv_lens[s]-1 of
+ * the key-side tensors (index_k, k, v).  Query row t of sequence s (t counted
+ * from 0 inside the sequence) sits at absolute position
+ *     p = kv_lens[s] - (q_offsets[s+1] - q_offsets[s]) + t,
+ * i.e. its own key is already in the cache.  This covers prefill
+ * (q rows == kv_len), chunked prefill (rows appended to a cached context) and
+ * decode (one row per sequence; kv_starts may then point into a padded cache,
+ * e.g. s * max_len).  Key block b of a sequence holds its keys
+ * b*block_size .. min((b+1)*block_size, kv_len)-1 (Sec. 2.3, block equation);
+ * the local block of position p is p / block_size.
+ */
+#ifndef MSA_H_
+#define MSA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes returned by every int-valued call. */
+#define MSA_OK 0
+#define MSA_ERR_INVALID (-1)     /* null pointer, negative or inconsistent size, H_q % H_kv != 0 ... */
+#define MSA_ERR_UNSUPPORTED (-2) /* a valid shape this build has no kernel for */
+#define MSA_ERR_WORKSPACE (-3)   /* workspace smaller than the *_workspace_size() value */
+#define MSA_ERR_HIP (-4)         /* a HIP launch failed (the HIP error is consumed) */
+
+typedef struct msa_seqs {
+  int32_t num_seqs;          /* host: number of sequences, >= 1 */
+  int64_t total_q_rows;      /* host: rows of the query-side tensors (= q_offsets[num_seqs]) */
+  int64_t total_kv_rows;     /* host: rows of the key-side tensors; every key access is
+                                kept below this bound */
+  int32_t max_q_rows;        /* host: upper bound of q_offsets[s+1]-q_offsets[s] */
+  int32_t max_kv_len;        /* host: upper bound of kv_lens[s] */
+  const int32_t* q_offsets;  /* device [num_seqs+1], non-decreasing, q_offsets[0] == 0 */
+  const int64_t* kv_starts;  /* device [num_seqs], >= 0 */
+  const int32_t* kv_lens;    /* device [num_seqs], >= the sequence's query rows */
+} msa_seqs;
+
+/* Human-readable text of a status code (static storage). */
+const char* msa_strerror(int status);
+
+/* ------------------------------------------------------------------------
+ * Index Branch: msa_index_topk
+ *
+ * Sec. 3.1, index-score equation: for query position i of group r and key j,
+ * S_ij = q_idx[i, r, :] . k_idx[j, :] / sqrt(d_idx); a key block scores the
+ * maximum of S over its causally visible tokens (j <= i).  Sec. 3.1, top-k
+ * equation and Sec. 3.2 "Local Block": each (query row, group) keeps the
+ * local block i / block_size plus the top-k-1 other causal blocks.  Selection
+ * ranks the raw dot products (Sec. 4.1 "Exp-free selection": neither the
+ * softmax nor the positive scale changes the order); equal scores keep the
+ * lower block id.
+ *
+ *   index_q   bf16 [total_q_rows, num_kv_heads, d_idx]   one index-query head per group
+ *   index_k   bf16 [total_kv_rows, d_idx]                the single shared index-key head
+ *   block_ids int32 [total_q_rows, num_kv_heads, topk]   OUTPUT: the min(topk, lb+1) selected
+ *             block ids of each (row, group) in ascending order, then -1 padding.
+ *
+ * Supported: d_idx in {64, 128}; block_size in {64, 128}; 1 <= topk <= 64;
+ * num_kv_heads a power of two <= 64.
+ * ------------------------------------------------------------------------ */
+size_t msa_index_topk_workspace_size(const msa_seqs* seqs, int num_kv_heads, int d_idx,
+                                     int block_size, int topk);
+int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seqs,
+                   int num_kv_heads, int d_idx, int block_size, int topk, int32_t* block_ids,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Main Branch: msa_sparse_attn_prefill / msa_sparse_attn_decode
+ *
+ * Sec. 3.1, sparse-attention equation: for query row i and query head h of
+ * group r = h / (num_q_heads / num_kv_heads), softmax attention with scale
+ * `softmax_scale` (the paper uses 1/sqrt(head_dim)) over the causally visible
+ * tokens (j <= i) of the blocks listed in block_ids[i, r, :], using key/value
+ * head r.  Entries < 0 are padding; the ids of a row must be distinct; ids
+ * past the local block select no token.  Every row must list a block with a
+ * visible token (its local block, as msa_index_topk guarantees); a row without
+ * one gets O = 0 and LSE = -inf.
+ *
+ *   q          bf16 [total_q_rows, num_q_heads, head_dim]
+ *   k, v       bf16 [total_kv_rows, num_kv_heads, head_dim]
+ *   block_ids  int32 [total_q_rows, num_kv_heads, topk]   (msa_index_topk's output)
+ *   o          bf16 [total_q_rows, num_q_heads, head_dim]  OUTPUT
+ *   lse        fp32 [total_q_rows, num_q_heads]            OUTPUT, natural log of the
+ *              softmax denominator including the scale (Sec. 4.2 combine)
+ *
+ * The prefill call is built for many query rows per sequence; the decode call
+ * for one query row per sequence (it accepts any layout, and gives the same
+ * result as the prefill call up to rounding).
+ *
+ * Supported: head_dim == 128; block_size in {64, 128}; 1 <= topk <= 64;
+ * 1 <= num_q_heads / num_kv_heads <= 16; num_kv_heads <= 64.
+ * ------------------------------------------------------------------------ */
+size_t msa_sparse_attn_prefill_workspace_size(const msa_seqs* seqs, int num_q_heads,
+                                              int num_kv_heads, int head_dim, int block_size,
+                                              int topk);
+int msa_sparse_attn_prefill(const void* q, const void* k, const void* v,
+                            const int32_t* block_ids, const msa_seqs* seqs, int num_q_heads,
+                            int num_kv_heads, int head_dim, int block_size, int topk,
+                            float softmax_scale, void* o, float* lse, void* workspace,
+                            size_t workspace_bytes, hipStream_t stream);
+
+size_t msa_sparse_attn_decode_workspace_size(const msa_seqs* seqs, int num_q_heads,
+                                             int num_kv_heads, int head_dim, int block_size,
+                                             int topk);
+int msa_sparse_attn_decode(const void* q, const void* k, const void* v,
+                           const int32_t* block_ids, const msa_seqs* seqs, int num_q_heads,
+                           int num_kv_heads, int head_dim, int block_size, int topk,
+                           float softmax_scale, void* o, float* lse, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MSA_H_ */

@@ -220,8 +220,9 @@ def selection_is_valid(ids: np.ndarray, block_scores: np.ndarray, pos: int, bloc
 # --------------------------------------------------------------------------
 # Main Branch (Sec. 3.1, sparse-attention equation)
 # --------------------------------------------------------------------------
-def _attend(qh: np.ndarray, keys: np.ndarray, vals: np.ndarray, scale: float):
-    """Softmax attention of query heads qh (G, d) over keys/vals (n, d)."""
+def attend(qh: np.ndarray, keys: np.ndarray, vals: np.ndarray, scale: float):
+    """Softmax attention of query heads qh (G, d) over keys/vals (n, d);
+    returns O (G, d) and the natural-log LSE (G,)."""
     z = (qh @ keys.T) * scale                    # (G, n)
     m = z.max(axis=1, keepdims=True)
     e = np.exp(z - m)
@@ -264,7 +265,7 @@ def sparse_attention(q_bits, k_bits, v_bits, block_ids: np.ndarray, layout: Layo
             toks = selected_tokens(ids_row[g], pos, block_size)
             keys = decode_bf16(k_bits[kv0 + toks, g])
             vals = decode_bf16(v_bits[kv0 + toks, g])
-            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(
+            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(
                 qf[g * G:(g + 1) * G], keys, vals, scale)
     return O, L
 
@@ -287,7 +288,7 @@ def dense_causal_attention(q_bits, k_bits, v_bits, layout: Layout, scale: Option
         for g in range(H_kv):
             keys = decode_bf16(k_bits[kv0:kv0 + pos + 1, g])
             vals = decode_bf16(v_bits[kv0:kv0 + pos + 1, g])
-            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(
+            O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(
                 qf[g * G:(g + 1) * G], keys, vals, scale)
     return O, L
 

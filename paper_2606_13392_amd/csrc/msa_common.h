@@ -1,0 +1,184 @@
+// Shared device and host helpers of libmsa (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "msa.h"
+
+namespace msa {
+
+// ---------------------------------------------------------------- vector types
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t* p) {
+  return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
+}
+__device__ __forceinline__ bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0)); }
+
+// MFMA 32x32x16 bf16 -> f32.  Lane l supplies row (A) / column (B) l%32 and
+// eight consecutive k of the half l/32; C lane l holds column l%32, rows
+// 8*(r/4) + 4*(l/32) + r%4 for r = 0..15.
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// MFMA 16x16x32 bf16 -> f32.  Lane l supplies row/column l%16 and eight k of
+// the quarter l/16; C lane l holds column l%16, rows 4*(l/16) + r, r = 0..3.
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// float -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16_bits(lo)) | (static_cast<uint32_t>(f32_to_bf16_bits(hi)) << 16);
+}
+
+// ---------------------------------------------------------------- ranking keys
+// Order-preserving map of a float score to uint32 (-0 and +0 compare equal).
+__device__ __forceinline__ uint32_t ordered_u32(float x) {
+  uint32_t u = __float_as_uint(x);
+  if (u == 0x80000000u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+// 64-bit ranking key: larger score first, then the smaller block id.  Every
+// real key is non-zero, so 0 serves as the empty slot.
+__device__ __forceinline__ uint64_t rank_key(float score, uint32_t block) {
+  return (static_cast<uint64_t>(ordered_u32(score)) << 32) | static_cast<uint64_t>(0xFFFFFFFFu - block);
+}
+__device__ __forceinline__ uint32_t key_block(uint64_t key) {
+  return 0xFFFFFFFFu - static_cast<uint32_t>(key);
+}
+
+// ---------------------------------------------------------------- wave helpers
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
+  int lo = __shfl_xor(static_cast<int>(static_cast<uint32_t>(v)), mask);
+  int hi = __shfl_xor(static_cast<int>(static_cast<uint32_t>(v >> 32)), mask);
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+}
+__device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
+  int lo = __shfl(static_cast<int>(static_cast<uint32_t>(v)), src);
+  int hi = __shfl(static_cast<int>(static_cast<uint32_t>(v >> 32)), src);
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v)), lane);
+  uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(static_cast<uint32_t>(v >> 32)), lane);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// Bitonic sort of one 64-bit key per lane across the wave, descending
+// (lane 0 receives the largest key).
+__device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      uint64_t o = shfl_xor_u64(v, j);
+      bool desc_block = (lane & k) == 0;
+      bool lower = (lane & j) == 0;
+      bool take_max = (desc_block == lower);
+      v = take_max ? (v > o ? v : o) : (v < o ? v : o);
+    }
+  }
+  return v;
+}
+// Sorts a bitonic sequence (one key per lane) descending.
+__device__ __forceinline__ uint64_t wave_bitonic_merge_desc_u64(uint64_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int j = kWave >> 1; j > 0; j >>= 1) {
+    uint64_t o = shfl_xor_u64(v, j);
+    bool lower = (lane & j) == 0;
+    v = lower ? (v > o ? v : o) : (v < o ? v : o);
+  }
+  return v;
+}
+// Bitonic sort of one uint32 per lane, ascending.
+__device__ __forceinline__ uint32_t wave_sort_asc_u32(uint32_t v) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), j));
+      bool asc_block = (lane & k) == 0;
+      bool lower = (lane & j) == 0;
+      bool take_min = (asc_block == lower);
+      v = take_min ? (v < o ? v : o) : (v > o ? v : o);
+    }
+  }
+  return v;
+}
+
+// Sequence of a packed query row: largest s with q_offsets[s] <= row.
+__device__ __forceinline__ int find_seq(const int32_t* __restrict__ q_offsets, int num_seqs, int64_t row) {
+  int lo = 0, hi = num_seqs - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (static_cast<int64_t>(q_offsets[mid]) <= row) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Per-sequence geometry read from the device layout arrays, with the key
+// range clamped to the key-side tensor so no access can leave it.
+struct SeqGeom {
+  int64_t kv_start;   // first key row of the sequence
+  int32_t kv_len;     // keys visible to the sequence's last query row
+  int32_t q_begin;    // first packed query row
+  int32_t q_rows;     // query rows of the sequence
+};
+__device__ __forceinline__ SeqGeom seq_geom(const msa_seqs& sq, int s) {
+  SeqGeom g;
+  g.q_begin = sq.q_offsets[s];
+  g.q_rows = sq.q_offsets[s + 1] - g.q_begin;
+  int64_t st = sq.kv_starts[s];
+  int64_t len = sq.kv_lens[s];
+  if (st < 0) st = 0;
+  if (st > sq.total_kv_rows) st = sq.total_kv_rows;
+  if (len > sq.total_kv_rows - st) len = sq.total_kv_rows - st;
+  if (len < 0) len = 0;
+  g.kv_start = st;
+  g.kv_len = static_cast<int32_t>(len);
+  return g;
+}
+
+}  // namespace msa
+
+// ---------------------------------------------------------------- host helpers
+namespace msa_host {
+
+inline bool is_pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+inline int validate_seqs(const msa_seqs* s) {
+  if (!s) return MSA_ERR_INVALID;
+  if (s->num_seqs < 1 || s->total_q_rows < 0 || s->total_kv_rows < 0 || s->max_q_rows < 0 ||
+      s->max_kv_len < 0)
+    return MSA_ERR_INVALID;
+  if (!s->q_offsets || !s->kv_starts || !s->kv_lens) return MSA_ERR_INVALID;
+  if (s->max_q_rows > s->max_kv_len) return MSA_ERR_INVALID;
+  if (s->total_q_rows > (int64_t)s->num_seqs * s->max_q_rows) return MSA_ERR_INVALID;
+  if (s->total_q_rows >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  return MSA_OK;
+}
+
+inline int launch_status() {
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? MSA_OK : MSA_ERR_HIP;
+}
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace msa_host

@@ -1,0 +1,370 @@
+// Main Branch of MSA on gfx950: exact softmax attention over the causally
+// visible tokens of the selected key blocks (Sec. 3.1, sparse-attention
+// equation), returning O and the natural-log LSE.
+//
+// attn_rows_kernel: one wave per (query row, group, split).  The G query heads
+// of the group share the group's block list (Sec. 2.3, group-shared index
+// set), so one wave computes S^T = K Q^T for all of them with MFMA 16x16x32
+// (keys as M, heads as N, head_dim as K), keeps an online softmax per head in
+// registers (each lane owns one head's column) and accumulates O^T = V^T P^T
+// with V staged transposed in LDS.  With several splits per row it writes
+// locally normalised partials that combine_kernel merges with the log-sum-exp
+// rule of Sec. 4.2 ("Two-phase forward").
+#include "msa_common.h"
+
+namespace {
+
+using namespace msa;
+
+constexpr int kHeadDim = 128;
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+template <int BK>
+struct AttnSmem {
+  // V of one block, transposed: vt[d][key]; +4 keys of padding per row.
+  uint16_t vt[kHeadDim][BK + 4];
+};
+
+// Stage V[b*BK .. b*BK+BK) of group r into LDS as vt[d][key] (keys past the
+// sequence's end read as zero).
+template <int BK>
+__device__ __forceinline__ void stage_v_transposed(AttnSmem<BK>& sm, const uint16_t* __restrict__ vbase,
+                                                   int64_t row_stride, int key0, int kv_len) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int it = 0; it < BK / 16; ++it) {
+    const int q = lane + kWave * it;        // (4-key group, 8-dim group)
+    const int key4 = q >> 4, dg = q & 15;
+    uint4 rows[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key = key0 + 4 * key4 + j;
+      rows[j] = key < kv_len ? *reinterpret_cast<const uint4*>(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
+                             : make_uint4(0, 0, 0, 0);
+    }
+    const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
+    const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&rows[1]);
+    const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&rows[2]);
+    const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&rows[3]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint2 w;
+      w.x = static_cast<uint32_t>(e0[e]) | (static_cast<uint32_t>(e1[e]) << 16);
+      w.y = static_cast<uint32_t>(e2[e]) | (static_cast<uint32_t>(e3[e]) << 16);
+      *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = w;
+    }
+  }
+}
+
+template <int BK>
+__global__ __launch_bounds__(64) void attn_rows_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int topk,
+    int slots_per_split, float scale_log2, uint16_t* __restrict__ o, float* __restrict__ lse,
+    float* __restrict__ o_part, float* __restrict__ lse_part) {
+  __shared__ AttnSmem<BK> sm;
+  const int lane = lane_id();
+  const int G = H_q / H_kv;
+  const int64_t row = blockIdx.x / H_kv;
+  const int r = blockIdx.x % H_kv;
+  const int sp = blockIdx.y;
+  const int nsplit = gridDim.y;
+  if (row >= sq.total_q_rows) return;
+  const int s = find_seq(sq.q_offsets, sq.num_seqs, row);
+  const SeqGeom g = seq_geom(sq, s);
+  int p = g.kv_len - g.q_rows + static_cast<int>(row - g.q_begin);
+  if (p >= g.kv_len) p = -1;                        // inconsistent layout: attend to nothing
+
+  const int n = lane & 15, q4 = lane >> 4;
+  // B operand of S^T = K Q^T: head n of the group, dims 32*ks + 8*q4 .. +8.
+  bf16x8 bq[kHeadDim / 32];
+  const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + n) * kHeadDim + 8 * q4;
+#pragma unroll
+  for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = n < G ? ld_bf16x8(qrow + 32 * ks) : zero_bf16x8();
+
+  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  const uint16_t* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
+  const uint16_t* vbase = v + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x4 acc[kHeadDim / 16];
+#pragma unroll
+  for (int t = 0; t < kHeadDim / 16; ++t) acc[t] = f32x4{};
+
+  const int slot0 = sp * slots_per_split;
+  const int slot1 = min(topk, slot0 + slots_per_split);
+  for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
+    const int b = ids[slot];
+    if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
+    const int key0 = b * BK;
+    __syncthreads();                                  // previous block's V reads are done
+    stage_v_transposed<BK>(sm, vbase, kv_stride, key0, g.kv_len);
+
+    // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
+    f32x4 st[BK / 16];
+#pragma unroll
+    for (int i = 0; i < BK / 16; ++i) {
+      const int key = key0 + 16 * i + n;
+      st[i] = f32x4{};
+      const uint16_t* kp = kbase + static_cast<int64_t>(key) * kv_stride;
+#pragma unroll
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) {
+        bf16x8 a = key < g.kv_len ? ld_bf16x8(kp + 32 * ks) : zero_bf16x8();
+        st[i] = mfma16x16x32(a, bq[ks], st[i]);
+      }
+    }
+    // lane (n, q4) holds keys 16i + 4*q4 + e of head n
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < BK / 16; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int key = key0 + 16 * i + 4 * q4 + e;
+        float z = st[i][e] * scale_log2;
+        z = key <= p ? z : -INFINITY;
+        st[i][e] = z;
+        bmax = fmaxf(bmax, z);
+      }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+    const float m_new = fmaxf(m_run, bmax);
+    const float alpha = exp2f(m_run - m_new);
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < BK / 16; ++i)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float pe = exp2f(st[i][e] - m_new);
+        st[i][e] = pe;
+        lsum += pe;
+      }
+    lsum += __shfl_xor(lsum, 16);
+    lsum += __shfl_xor(lsum, 32);
+    l_run = l_run * alpha + lsum;
+    m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < kHeadDim / 16; ++t) acc[t] *= alpha;
+
+    // P^T as the B operand: k-step u covers keys 32u..32u+31; lane (n, q4)
+    // supplies logical k = 8*q4 + e <-> key 32u + 4*q4 + e (e < 4) and
+    // 32u + 16 + 4*q4 + e - 4 (e >= 4), exactly the keys its S^T tiles hold.
+    __syncthreads();                                  // V staged
+#pragma unroll
+    for (int u = 0; u < BK / 32; ++u) {
+      bf16x8 bp;
+      {
+        uint4 w;
+        w.x = pack_bf16x2(st[2 * u][0], st[2 * u][1]);
+        w.y = pack_bf16x2(st[2 * u][2], st[2 * u][3]);
+        w.z = pack_bf16x2(st[2 * u + 1][0], st[2 * u + 1][1]);
+        w.w = pack_bf16x2(st[2 * u + 1][2], st[2 * u + 1][3]);
+        bp = __builtin_bit_cast(bf16x8, w);
+      }
+#pragma unroll
+      for (int t = 0; t < kHeadDim / 16; ++t) {
+        // A operand V^T: row d = 16t + n (lane's m), the same key mapping.
+        const uint16_t* vr = &sm.vt[16 * t + n][32 * u + 4 * q4];
+        uint4 w;
+        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+        w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
+        acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, w), bp, acc[t]);
+      }
+    }
+  }
+
+  // O^T tiles: lane (n, q4) holds d = 16t + 4*q4 + e of head n.
+  if (n >= G) return;
+  const int64_t head_row = row * H_q + static_cast<int64_t>(r) * G + n;
+  const bool empty = !(l_run > 0.f);
+  const float inv_l = empty ? 0.f : 1.f / l_run;
+  const float lse_v = empty ? -INFINITY : (m_run + __log2f(l_run)) * kLn2;
+  if (nsplit == 1) {
+    uint16_t* orow = o + head_row * kHeadDim + 4 * q4;
+#pragma unroll
+    for (int t = 0; t < kHeadDim / 16; ++t) {
+      uint2 w;
+      w.x = pack_bf16x2(acc[t][0] * inv_l, acc[t][1] * inv_l);
+      w.y = pack_bf16x2(acc[t][2] * inv_l, acc[t][3] * inv_l);
+      *reinterpret_cast<uint2*>(orow + 16 * t) = w;
+    }
+    if (q4 == 0) lse[head_row] = lse_v;
+  } else {
+    const int64_t part_row = static_cast<int64_t>(sp) * sq.total_q_rows * H_q + head_row;
+    float* orow = o_part + part_row * kHeadDim + 4 * q4;
+#pragma unroll
+    for (int t = 0; t < kHeadDim / 16; ++t)
+      *reinterpret_cast<float4*>(orow + 16 * t) =
+          make_float4(acc[t][0] * inv_l, acc[t][1] * inv_l, acc[t][2] * inv_l, acc[t][3] * inv_l);
+    if (q4 == 0) lse_part[part_row] = lse_v;
+  }
+}
+
+// Merge `nsplit` partials per (row, head): a = max LSE_s,
+// LSE = a + log sum exp(LSE_s - a), O = sum exp(LSE_s - LSE) O_s (Sec. 4.2).
+// One thread per (row, head, 8 dims).
+__global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ o_part,
+                                                      const float* __restrict__ lse_part, int nsplit,
+                                                      int64_t head_rows, uint16_t* __restrict__ o,
+                                                      float* __restrict__ lse) {
+  const int64_t tid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t hr = tid >> 4;
+  const int d0 = static_cast<int>(tid & 15) * 8;
+  if (hr >= head_rows) return;
+  float a = -INFINITY;
+  for (int s = 0; s < nsplit; ++s) a = fmaxf(a, lse_part[s * head_rows + hr]);
+  float out[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  float total = -INFINITY;
+  if (a > -INFINITY) {
+    float sum = 0.f;
+    for (int s = 0; s < nsplit; ++s) sum += exp2f((lse_part[s * head_rows + hr] - a) * kLog2e);
+    total = a + __logf(sum);
+    for (int s = 0; s < nsplit; ++s) {
+      const float ls = lse_part[s * head_rows + hr];
+      if (!(ls > -INFINITY)) continue;
+      const float w = exp2f((ls - total) * kLog2e);
+      const float4* src = reinterpret_cast<const float4*>(o_part + (s * head_rows + hr) * kHeadDim + d0);
+      const float4 x0 = src[0], x1 = src[1];
+      out[0] += w * x0.x; out[1] += w * x0.y; out[2] += w * x0.z; out[3] += w * x0.w;
+      out[4] += w * x1.x; out[5] += w * x1.y; out[6] += w * x1.z; out[7] += w * x1.w;
+    }
+  }
+  uint4 wv;
+  wv.x = pack_bf16x2(out[0], out[1]);
+  wv.y = pack_bf16x2(out[2], out[3]);
+  wv.z = pack_bf16x2(out[4], out[5]);
+  wv.w = pack_bf16x2(out[6], out[7]);
+  *reinterpret_cast<uint4*>(o + hr * kHeadDim + d0) = wv;
+  if (d0 == 0) lse[hr] = total;
+}
+
+// ---------------------------------------------------------------- host side
+int validate_attn(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, int topk) {
+  int st = msa_host::validate_seqs(seqs);
+  if (st != MSA_OK) return st;
+  if (H_q < 1 || H_kv < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
+  if (H_q % H_kv != 0) return MSA_ERR_INVALID;
+  if (head_dim != kHeadDim) return MSA_ERR_UNSUPPORTED;
+  if (BK != 64 && BK != 128) return MSA_ERR_UNSUPPORTED;
+  if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
+  if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  return MSA_OK;
+}
+
+struct SplitPlan {
+  int nsplit;
+  int slots_per_split;
+};
+
+// Split the k slots of each (row, group) over enough waves to fill the chip.
+SplitPlan split_plan(const msa_seqs* seqs, int H_kv, int topk) {
+  SplitPlan sp;
+  const int64_t pairs = seqs->total_q_rows * H_kv;
+  int want = pairs > 0 ? static_cast<int>((4096 + pairs - 1) / pairs) : 1;
+  if (want < 1) want = 1;
+  if (want > topk) want = topk;
+  sp.slots_per_split = (topk + want - 1) / want;
+  sp.nsplit = (topk + sp.slots_per_split - 1) / sp.slots_per_split;
+  return sp;
+}
+
+size_t split_workspace(const msa_seqs* seqs, int H_q, const SplitPlan& sp) {
+  if (sp.nsplit <= 1) return 0;
+  const size_t hr = static_cast<size_t>(seqs->total_q_rows) * H_q;
+  return msa_host::align_up(sp.nsplit * hr * kHeadDim * sizeof(float), 256) + sp.nsplit * hr * sizeof(float);
+}
+
+int run_rows(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
+             int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, const SplitPlan& sp,
+             void* workspace, hipStream_t stream) {
+  const int64_t hr = seqs->total_q_rows * H_q;
+  float* o_part = nullptr;
+  float* lse_part = nullptr;
+  if (sp.nsplit > 1) {
+    o_part = static_cast<float*>(workspace);
+    lse_part = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                        msa_host::align_up(sp.nsplit * static_cast<size_t>(hr) * kHeadDim * sizeof(float), 256));
+  }
+  const dim3 grid(static_cast<unsigned>(seqs->total_q_rows * H_kv), static_cast<unsigned>(sp.nsplit));
+  const float sl2 = scale * kLog2e;
+  const msa_seqs sq = *seqs;
+  auto* qp = static_cast<const uint16_t*>(q);
+  auto* kp = static_cast<const uint16_t*>(k);
+  auto* vp = static_cast<const uint16_t*>(v);
+  auto* op = static_cast<uint16_t*>(o);
+  if (BK == 64)
+    hipLaunchKernelGGL(attn_rows_kernel<64>, grid, dim3(64), 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv,
+                       topk, sp.slots_per_split, sl2, op, lse, o_part, lse_part);
+  else
+    hipLaunchKernelGGL(attn_rows_kernel<128>, grid, dim3(64), 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv,
+                       topk, sp.slots_per_split, sl2, op, lse, o_part, lse_part);
+  if (sp.nsplit > 1) {
+    const int64_t threads = hr * 16;
+    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,
+                       o_part, lse_part, sp.nsplit, hr, op, lse);
+  }
+  return msa_host::launch_status();
+}
+
+int check_ptrs(const void* q, const void* k, const void* v, const int32_t* ids, const void* o, const float* lse) {
+  return (q && k && v && ids && o && lse) ? MSA_OK : MSA_ERR_INVALID;
+}
+
+}  // namespace
+
+extern "C" size_t msa_sparse_attn_decode_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                                       int head_dim, int block_size, int topk) {
+  if (validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
+  return split_workspace(seqs, num_q_heads, split_plan(seqs, num_kv_heads, topk));
+}
+
+extern "C" int msa_sparse_attn_decode(const void* q, const void* k, const void* v, const int32_t* block_ids,
+                                      const msa_seqs* seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                                      int block_size, int topk, float softmax_scale, void* o, float* lse,
+                                      void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
+  const SplitPlan sp = split_plan(seqs, num_kv_heads, topk);
+  const size_t need = split_workspace(seqs, num_q_heads, sp);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return MSA_ERR_WORKSPACE;
+  return run_rows(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o, lse,
+                  sp, workspace, stream);
+}
+
+extern "C" size_t msa_sparse_attn_prefill_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                                        int head_dim, int block_size, int topk) {
+  if (validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
+  return 0;
+}
+
+extern "C" int msa_sparse_attn_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids,
+                                       const msa_seqs* seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                                       int block_size, int topk, float softmax_scale, void* o, float* lse,
+                                       void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  (void)workspace;
+  (void)workspace_bytes;
+  int st = validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
+  SplitPlan sp;
+  sp.nsplit = 1;
+  sp.slots_per_split = topk;
+  return run_rows(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o, lse,
+                  sp, nullptr, stream);
+}
+
+extern "C" const char* msa_strerror(int status) {
+  switch (status) {
+    case MSA_OK: return "ok";
+    case MSA_ERR_INVALID: return "invalid argument";
+    case MSA_ERR_UNSUPPORTED: return "unsupported shape or parameter";
+    case MSA_ERR_WORKSPACE: return "workspace too small";
+    case MSA_ERR_HIP: return "HIP launch failure";
+    default: return "unknown status";
+  }
+}

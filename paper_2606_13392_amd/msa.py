@@ -1,0 +1,205 @@
+"""Python binding of libmsa.so (argument marshalling only).
+
+Each function checks dtypes, shapes and devices, takes device pointers and the
+current torch stream, and calls the C ABI of ``include/msa.h`` under the same
+name.  All work runs in the library's HIP kernels; there is no fallback: when
+the library is not built, or a call returns an error, a RuntimeError is raised.
+torch provides device memory (outputs, workspaces) and the stream.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmsa.so")
+
+MSA_OK, MSA_ERR_INVALID, MSA_ERR_UNSUPPORTED, MSA_ERR_WORKSPACE, MSA_ERR_HIP = 0, -1, -2, -3, -4
+
+EXPORTS = [
+    "msa_strerror",
+    "msa_index_topk_workspace_size", "msa_index_topk",
+    "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
+    "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
+]
+
+
+class MsaSeqsC(ctypes.Structure):
+    _fields_ = [
+        ("num_seqs", ctypes.c_int32),
+        ("total_q_rows", ctypes.c_int64),
+        ("total_kv_rows", ctypes.c_int64),
+        ("max_q_rows", ctypes.c_int32),
+        ("max_kv_len", ctypes.c_int32),
+        ("q_offsets", ctypes.c_void_p),
+        ("kv_starts", ctypes.c_void_p),
+        ("kv_lens", ctypes.c_void_p),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libmsa.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB_PATH)
+        P, S, I, Z, F = ctypes.c_void_p, ctypes.POINTER(MsaSeqsC), ctypes.c_int, ctypes.c_size_t, ctypes.c_float
+        L.msa_strerror.argtypes = [I]
+        L.msa_strerror.restype = ctypes.c_char_p
+        L.msa_index_topk_workspace_size.argtypes = [S, I, I, I, I]
+        L.msa_index_topk_workspace_size.restype = Z
+        L.msa_index_topk.argtypes = [P, P, S, I, I, I, I, P, P, Z, P]
+        L.msa_index_topk.restype = I
+        for name in ("prefill", "decode"):
+            ws = getattr(L, f"msa_sparse_attn_{name}_workspace_size")
+            ws.argtypes = [S, I, I, I, I, I]
+            ws.restype = Z
+            fn = getattr(L, f"msa_sparse_attn_{name}")
+            fn.argtypes = [P, P, P, P, S, I, I, I, I, I, F, P, P, P, Z, P]
+            fn.restype = I
+        _lib = L
+    return _lib
+
+
+def _check(status: int, what: str):
+    if status != MSA_OK:
+        raise RuntimeError(f"{what} failed: {lib().msa_strerror(status).decode()} ({status})")
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: Sequence[int], device):
+    if t.dtype != dtype:
+        raise TypeError(f"{name}: expected {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous")
+    if t.device != device:
+        raise ValueError(f"{name}: expected device {device}, got {t.device}")
+
+
+class Seqs:
+    """Sequence layout (see include/msa.h): device arrays plus host totals."""
+
+    def __init__(self, q_rows: Sequence[int], kv_lens: Sequence[int], kv_starts: Sequence[int],
+                 total_kv_rows: int, device):
+        assert len(q_rows) == len(kv_lens) == len(kv_starts) and len(q_rows) >= 1
+        offs = [0]
+        for r in q_rows:
+            offs.append(offs[-1] + int(r))
+        dev = torch.device(device)
+        if dev.type == "cuda" and dev.index is None:
+            dev = torch.device("cuda", torch.cuda.current_device())
+        self.device = dev
+        self.q_offsets = torch.tensor(offs, dtype=torch.int32, device=self.device)
+        self.kv_starts = torch.tensor([int(x) for x in kv_starts], dtype=torch.int64, device=self.device)
+        self.kv_lens = torch.tensor([int(x) for x in kv_lens], dtype=torch.int32, device=self.device)
+        self.num_seqs = len(q_rows)
+        self.total_q_rows = offs[-1]
+        self.total_kv_rows = int(total_kv_rows)
+        self.max_q_rows = max(int(r) for r in q_rows)
+        self.max_kv_len = max(int(x) for x in kv_lens)
+        self.c = MsaSeqsC(self.num_seqs, self.total_q_rows, self.total_kv_rows, self.max_q_rows,
+                          self.max_kv_len, self.q_offsets.data_ptr(), self.kv_starts.data_ptr(),
+                          self.kv_lens.data_ptr())
+
+    @classmethod
+    def from_problem(cls, p, device) -> "Seqs":
+        return cls(p.q_rows, p.kv_lens, p.kv_starts, p.total_kv_rows, device)
+
+    def ref(self):
+        return ctypes.byref(self.c)
+
+
+def _workspace(nbytes: int, device, ws: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
+    if nbytes == 0:
+        return ws
+    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+        return ws
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+# ---------------------------------------------------------------- Index Branch
+def index_topk_workspace_size(seqs: Seqs, num_kv_heads: int, d_idx: int, block_size: int, topk: int) -> int:
+    return int(lib().msa_index_topk_workspace_size(seqs.ref(), num_kv_heads, d_idx, block_size, topk))
+
+
+def index_topk(index_q: torch.Tensor, index_k: torch.Tensor, seqs: Seqs, block_size: int, topk: int,
+               out: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Block ids [total_q_rows, H_kv, topk] (int32, ascending, -1 padded)."""
+    Tq, H_kv, d_idx = index_q.shape
+    dev = seqs.device
+    _need(index_q, "index_q", torch.bfloat16, (seqs.total_q_rows, H_kv, d_idx), dev)
+    _need(index_k, "index_k", torch.bfloat16, (seqs.total_kv_rows, d_idx), dev)
+    if out is None:
+        out = torch.empty((Tq, H_kv, topk), dtype=torch.int32, device=dev)
+    _need(out, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    nbytes = index_topk_workspace_size(seqs, H_kv, d_idx, block_size, topk)
+    ws = _workspace(nbytes, dev, workspace)
+    st = lib().msa_index_topk(_ptr(index_q), _ptr(index_k), seqs.ref(), H_kv, d_idx, block_size, topk,
+                              _ptr(out), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, "msa_index_topk")
+    return out
+
+
+# ---------------------------------------------------------------- Main Branch
+def _attn(kind: str, q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_scale, out, lse, workspace):
+    Tq, H_q, d_h = q.shape
+    H_kv = k.shape[1]
+    topk = block_ids.shape[2]
+    dev = seqs.device
+    _need(q, "q", torch.bfloat16, (seqs.total_q_rows, H_q, d_h), dev)
+    _need(k, "k", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(v, "v", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(block_ids, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    if out is None:
+        out = torch.empty((Tq, H_q, d_h), dtype=torch.bfloat16, device=dev)
+    if lse is None:
+        lse = torch.empty((Tq, H_q), dtype=torch.float32, device=dev)
+    _need(out, "o", torch.bfloat16, (Tq, H_q, d_h), dev)
+    _need(lse, "lse", torch.float32, (Tq, H_q), dev)
+    scale = 1.0 / math.sqrt(d_h) if softmax_scale is None else float(softmax_scale)
+    L = lib()
+    nbytes = int(getattr(L, f"msa_sparse_attn_{kind}_workspace_size")(seqs.ref(), H_q, H_kv, d_h, block_size, topk))
+    ws = _workspace(nbytes, dev, workspace)
+    st = getattr(L, f"msa_sparse_attn_{kind}")(
+        _ptr(q), _ptr(k), _ptr(v), _ptr(block_ids), seqs.ref(), H_q, H_kv, d_h, block_size, topk, scale,
+        _ptr(out), _ptr(lse), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, f"msa_sparse_attn_{kind}")
+    return out, lse
+
+
+def sparse_attn_prefill_workspace_size(seqs: Seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) -> int:
+    return int(lib().msa_sparse_attn_prefill_workspace_size(seqs.ref(), num_q_heads, num_kv_heads, head_dim,
+                                                             block_size, topk))
+
+
+def sparse_attn_decode_workspace_size(seqs: Seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) -> int:
+    return int(lib().msa_sparse_attn_decode_workspace_size(seqs.ref(), num_q_heads, num_kv_heads, head_dim,
+                                                            block_size, topk))
+
+
+def sparse_attn_prefill(q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_scale=None,
+                        out=None, lse=None, workspace=None):
+    """O [Tq, H_q, d_h] bf16 and LSE [Tq, H_q] fp32 over the selected blocks."""
+    return _attn("prefill", q, k, v, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
+
+
+def sparse_attn_decode(q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_scale=None,
+                       out=None, lse=None, workspace=None):
+    """Decode-shaped variant of sparse_attn_prefill (one query row per sequence)."""
+    return _attn("decode", q, k, v, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)

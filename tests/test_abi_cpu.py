@@ -1,0 +1,104 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects invalid arguments on the host before launching."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2606_13392_amd import msa
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "msa.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(msa_[a-z_]+)\s*\(", src)))
+
+
+def test_header_matches_binding():
+    assert _declared() == sorted(msa.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = msa.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", msa.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (msa_\w+)", out))
+    assert set(_declared()) <= exported
+
+
+def test_strerror():
+    L = msa.lib()
+    assert L.msa_strerror(0) == b"ok"
+    assert L.msa_strerror(msa.MSA_ERR_WORKSPACE) == b"workspace too small"
+
+
+def _seqs(**kw):
+    base = dict(num_seqs=1, total_q_rows=100, total_kv_rows=100, max_q_rows=100, max_kv_len=100,
+                q_offsets=8, kv_starts=8, kv_lens=8)   # fake non-null pointers, never dereferenced
+    base.update(kw)
+    return msa.MsaSeqsC(**base)
+
+
+def test_workspace_queries_are_host_only():
+    L = msa.lib()
+    s = _seqs()
+    n = L.msa_index_topk_workspace_size(ctypes.byref(s), 2, 64, 64, 8)
+    # 64 index rows per group, ceil(100/64)=2 blocks rounded to 4, fp32; plus the group table
+    groups = 100 // 32 + 1
+    assert n == 256 + groups * 64 * 4 * 4
+    assert L.msa_sparse_attn_prefill_workspace_size(ctypes.byref(s), 8, 2, 128, 64, 8) == 0
+    assert L.msa_index_topk_workspace_size(ctypes.byref(s), 3, 64, 64, 8) == 0      # H_kv not a power of 2
+
+
+BAD_INDEX = [
+    (dict(), dict(H_kv=3), msa.MSA_ERR_UNSUPPORTED),
+    (dict(), dict(d_idx=96), msa.MSA_ERR_UNSUPPORTED),
+    (dict(), dict(bk=32), msa.MSA_ERR_UNSUPPORTED),
+    (dict(), dict(topk=65), msa.MSA_ERR_UNSUPPORTED),
+    (dict(), dict(topk=0), msa.MSA_ERR_INVALID),
+    (dict(num_seqs=0), dict(), msa.MSA_ERR_INVALID),
+    (dict(max_q_rows=200), dict(), msa.MSA_ERR_INVALID),      # more query rows than keys
+    (dict(q_offsets=0), dict(), msa.MSA_ERR_INVALID),
+    (dict(), dict(null_out=True), msa.MSA_ERR_INVALID),
+    (dict(), dict(ws_bytes=8), msa.MSA_ERR_WORKSPACE),
+]
+
+
+@pytest.mark.parametrize("seq_kw,arg_kw,want", BAD_INDEX)
+def test_index_topk_rejects(seq_kw, arg_kw, want):
+    L = msa.lib()
+    s = _seqs(**seq_kw)
+    a = dict(H_kv=2, d_idx=64, bk=64, topk=8, null_out=False, ws_bytes=1 << 20)
+    a.update(arg_kw)
+    st = L.msa_index_topk(8, 8, ctypes.byref(s), a["H_kv"], a["d_idx"], a["bk"], a["topk"],
+                          None if a["null_out"] else 8, 8, a["ws_bytes"], None)
+    assert st == want
+
+
+BAD_ATTN = [
+    (dict(H_q=6, H_kv=4), msa.MSA_ERR_INVALID),
+    (dict(d_h=64), msa.MSA_ERR_UNSUPPORTED),
+    (dict(H_q=64, H_kv=2), msa.MSA_ERR_UNSUPPORTED),           # group of 32 heads
+    (dict(bk=256), msa.MSA_ERR_UNSUPPORTED),
+    (dict(topk=0), msa.MSA_ERR_INVALID),
+    (dict(null_q=True), msa.MSA_ERR_INVALID),
+]
+
+
+@pytest.mark.parametrize("kind", ["prefill", "decode"])
+@pytest.mark.parametrize("arg_kw,want", BAD_ATTN)
+def test_sparse_attn_rejects(kind, arg_kw, want):
+    L = msa.lib()
+    s = _seqs()
+    a = dict(H_q=8, H_kv=2, d_h=128, bk=64, topk=8, null_q=False)
+    a.update(arg_kw)
+    fn = getattr(L, f"msa_sparse_attn_{kind}")
+    st = fn(None if a["null_q"] else 8, 8, 8, 8, ctypes.byref(s), a["H_q"], a["H_kv"], a["d_h"], a["bk"],
+            a["topk"], 0.1, 8, 8, 8, 1 << 30, None)
+    assert st == want

@@ -1,0 +1,221 @@
+"""HIP path vs the CPU oracle through the C ABI (needs an MI355X).
+
+Block ids: bit-exact wherever the oracle's score gap exceeds 1e-3, otherwise
+a valid selection within that gap.  O / LSE: within 1e-2 max-abs and 5e-3
+relative L2 of the float64 oracle, computed on the same block ids.
+"""
+from __future__ import annotations
+
+import math
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.msa_oracle as O
+from paper_2606_13392_amd import msa, synth
+from tests.util import check_block_ids, check_outputs, from_dev_bits, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    msa.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+# name, q_rows, kv_lens, H_q, H_kv, d_idx, block, topk, kv_pad_to, planted
+SMALL = [
+    ("ragged_T200_k3", [200], [200], 8, 2, 64, 64, 3, None, 0),
+    ("prefill_T1000_k8", [1000], [1000], 16, 2, 64, 64, 8, None, 0),
+    ("k1_local_only", [300], [300], 8, 2, 64, 64, 1, None, 0),
+    ("k_covers_all", [700], [700], 8, 4, 64, 64, 64, None, 0),
+    ("chunked_varlen", [130, 64, 1, 257], [700, 64, 900, 1500], 16, 4, 64, 64, 6, None, 0),
+    ("empty_seq_in_batch", [50, 0, 70], [50, 300, 500], 8, 2, 64, 64, 4, None, 0),
+    ("decode_padded", [1, 1, 1, 1, 1], [3000, 64, 65, 4097, 1], 16, 4, 64, 64, 6, 4160, 0),
+    ("bk128_didx128_g16", [600], [600], 32, 2, 128, 128, 5, None, 0),
+    ("bk64_didx128_g8", [900], [900], 32, 4, 128, 64, 7, None, 0),
+    ("bk128_didx64_g1", [520], [520], 8, 8, 64, 128, 4, None, 0),
+    ("many_blocks_k32", [5000], [5000], 16, 2, 64, 64, 32, None, 0),
+    ("planted_k16", [4096], [4096], 16, 8, 64, 64, 16, None, 6),
+]
+
+
+def _problem(case):
+    name, q_rows, kv_lens, H_q, H_kv, d_idx, bk, topk, pad, planted = case
+    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, d_idx=d_idx,
+                             block_size=bk, topk=topk, seed=zlib.crc32(name.encode()) % 10000, planted=planted,
+                             kv_pad_to=pad)
+    return p
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_end_to_end(case):
+    p = _problem(case)
+    _say(f"[case] {p.name}")
+    x = synth.generate_numpy(p)
+    lay = O.layout_of(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+
+    ids_gpu = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    torch.cuda.synchronize()
+    ids_gpu = ids_gpu.cpu().numpy()
+    ids_ora, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
+    exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, x, lay, p.block_size, p.topk)
+    _say(f"  ids exact={exact} ties={ties}")
+
+    # Main branch on the oracle's ids (both entry points) and on the GPU's ids.
+    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_ora, lay, p.block_size)
+    ids_dev = torch.from_numpy(ids_ora).to(dev)
+    for fn in (msa.sparse_attn_prefill, msa.sparse_attn_decode):
+        o, l = fn(d["q"], d["k"], d["v"], ids_dev, seqs, p.block_size)
+        torch.cuda.synchronize()
+        stats = check_outputs(o.float().cpu().numpy(), l.cpu().numpy(), o_ref, l_ref, f"{p.name}/{fn.__name__}")
+        _say(f"  {fn.__name__}: max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e} lse {stats[2]:.2e}")
+    if ties:
+        o_ref2, l_ref2 = O.sparse_attention(x["q"], x["k"], x["v"], ids_gpu, lay, p.block_size)
+        o, l = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], torch.from_numpy(ids_gpu).to(dev), seqs,
+                                       p.block_size)
+        check_outputs(o.float().cpu().numpy(), l.cpu().numpy(), o_ref2, l_ref2, p.name + "/gpu-ids")
+
+
+def test_deterministic():
+    p = _problem(SMALL[1])
+    x = synth.generate_numpy(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    a = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    b = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    oa, la = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], a, seqs, p.block_size)
+    ob, lb = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], b, seqs, p.block_size)
+    od, ld = msa.sparse_attn_decode(d["q"], d["k"], d["v"], a, seqs, p.block_size)
+    od2, ld2 = msa.sparse_attn_decode(d["q"], d["k"], d["v"], a, seqs, p.block_size)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert torch.equal(oa.view(torch.int16), ob.view(torch.int16)) and torch.equal(la, lb)
+    assert torch.equal(od.view(torch.int16), od2.view(torch.int16)) and torch.equal(ld, ld2)
+
+
+def test_workspace_rejected_when_small():
+    p = _problem(SMALL[1])
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    x = synth.generate_numpy(p)
+    d = {k: to_dev(v) for k, v in x.items()}
+    small = torch.empty(16, dtype=torch.uint8, device=dev)
+    out = torch.full((p.total_q_rows, p.num_kv_heads, p.topk), 7, dtype=torch.int32, device=dev)
+    st = msa.lib().msa_index_topk(d["index_q"].data_ptr(), d["index_k"].data_ptr(), seqs.ref(), p.num_kv_heads,
+                                  p.d_idx, p.block_size, p.topk, out.data_ptr(), small.data_ptr(), 16,
+                                  msa._stream())
+    assert st == msa.MSA_ERR_WORKSPACE
+    torch.cuda.synchronize()
+    assert bool((out == 7).all())          # nothing was launched
+
+
+# ---------------------------------------------------------------- workloads
+def _sample_rows(p, n, seed):
+    rng = np.random.default_rng(seed)
+    T = p.total_q_rows
+    rows = set(int(r) for r in rng.integers(0, T, size=n))
+    for s in range(p.num_seqs):
+        a, b = p.q_offsets[s], p.q_offsets[s + 1]
+        if b > a:
+            rows |= {a, b - 1, min(b - 1, a + 63), min(b - 1, a + 64)}
+    return sorted(rows)
+
+
+def test_workload_prefill_4k():
+    p = synth.workload("prefill_4k")
+    _say(f"[case] {p.name}")
+    x = synth.generate_numpy(p)
+    lay = O.layout_of(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    o, l = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    torch.cuda.synchronize()
+    ids_gpu = ids.cpu().numpy()
+    ids_ora, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
+    exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, x, lay, p.block_size, p.topk)
+    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_gpu, lay, p.block_size)
+    stats = check_outputs(o.float().cpu().numpy(), l.cpu().numpy(), o_ref, l_ref, p.name)
+    _say(f"  ids exact={exact} ties={ties}; O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+
+
+def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
+    p = synth.workload(name)
+    _say(f"[case] {p.name} rows={p.total_q_rows} kv_rows={p.total_kv_rows}")
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    if gen == "numpy":
+        x = synth.generate_numpy(p)
+        d = {k: to_dev(v) for k, v in x.items()}
+    else:
+        d = synth.generate_torch(p, dev)
+        x = None
+    lay = O.layout_of(p)
+    decode = p.max_q_rows == 1
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    fn = msa.sparse_attn_decode if decode else msa.sparse_attn_prefill
+    o, l = fn(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    torch.cuda.synchronize()
+    rows = list(range(p.total_q_rows)) if decode else _sample_rows(p, n_rows, seed=p.seed)
+    # the oracle reads the input rows it needs back from the (generated) inputs
+    iq_h = x["index_q"] if x is not None else from_dev_bits(d["index_q"])
+    ik_h = x["index_k"] if x is not None else from_dev_bits(d["index_k"])
+    ids_all = ids.cpu().numpy()
+    ids_gpu = ids_all[rows]
+    ids_ora, gaps = O.select_blocks(iq_h, ik_h, lay, p.block_size, p.topk, rows=rows)
+    inputs = {"index_q": iq_h, "index_k": ik_h}
+    exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, inputs, lay, p.block_size, p.topk, rows=rows)
+    _say(f"  ids exact={exact} ties={ties} over {len(rows)} rows")
+    # Main branch on sampled rows, oracle fed with the GPU's (validated) ids
+    arows = rows if check_attn_rows is None else rows[::max(1, len(rows) // check_attn_rows)]
+    o_h = o.float().cpu().numpy()
+    l_h = l.cpu().numpy()
+    G = p.group_size
+    o_ref = np.zeros((len(arows), p.num_q_heads, p.head_dim))
+    l_ref = np.zeros((len(arows), p.num_q_heads))
+    for i, r in enumerate(arows):
+        s, pos = lay.locate(r)
+        kv0 = p.kv_starts[s]
+        qb = from_dev_bits(d["q"][r])
+        for g in range(p.num_kv_heads):
+            idr = ids_all[r, g]
+            toks = O.selected_tokens(idr, pos, p.block_size)
+            tt = torch.from_numpy(kv0 + toks).to(dev)
+            kb = from_dev_bits(d["k"][tt, g])
+            vb = from_dev_bits(d["v"][tt, g])
+            oo, ll = O.attend(O.decode_bf16(qb[g * G:(g + 1) * G]), O.decode_bf16(kb), O.decode_bf16(vb),
+                              1.0 / math.sqrt(p.head_dim))
+            o_ref[i, g * G:(g + 1) * G] = oo
+            l_ref[i, g * G:(g + 1) * G] = ll
+    stats = check_outputs(o_h[arows], l_h[arows], o_ref, l_ref, p.name)
+    _say(f"  O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e} lse {stats[2]:.2e} over {len(arows)} rows")
+
+
+def test_workload_prefill_32k_sampled():
+    _sampled_workload("prefill_32k", 160, check_attn_rows=64)
+
+
+def test_workload_decode_128k():
+    _sampled_workload("decode_128k", 64, gen="torch")
+
+
+def test_workload_chunked_8x8k_sampled():
+    _sampled_workload("chunked_8x8k", 96, gen="torch", check_attn_rows=48)

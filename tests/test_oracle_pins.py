@@ -32,8 +32,8 @@ MUTATIONS = {
     "combine_weight_sign": ("w = np.exp(lse_parts - lse)", "w = np.exp(lse - lse_parts)"),
     "flops_main_factor": ("4.0 * H_q * d_h * N * k * block_size", "2.0 * H_q * d_h * N * k * block_size"),
     "left_aligned_positions": ("return s, self.kv_lens[s] - self.q_rows[s] + t", "return s, t"),
-    "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = _attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
-                             "O[i, g::H_kv], L[i, g::H_kv] = _attend(\n                qf[g::H_kv], keys, vals, scale)"),
+    "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
+                             "O[i, g::H_kv], L[i, g::H_kv] = attend(\n                qf[g::H_kv], keys, vals, scale)"),
 }
 
 

@@ -1,0 +1,60 @@
+"""Helpers shared by the GPU parity tests: upload of generated inputs and the
+comparison rules (block ids: bit-exact where the oracle's score gap exceeds
+the tolerance, otherwise a valid selection within that gap; outputs: max-abs
+and relative-L2 bounds against the float64 oracle)."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import oracle.msa_oracle as O
+
+GAP_TOL = 1e-3          # score gap below which several selections are correct
+O_MAX_ABS = 1e-2        # outputs vs the fp64 oracle, on top of the output format's rounding
+O_REL_L2 = 5e-3
+# O is returned in bf16, which keeps 8 significant bits: rounding the exact
+# result to the output format alone moves it by up to 2^-9 |O| (0.0078 at
+# |O| = 4), so the element-wise bound is O_MAX_ABS + 2^-9 |O_ref|.
+BF16_HALF_ULP_REL = 2.0 ** -9
+
+
+def to_dev(bits: np.ndarray, device="cuda") -> torch.Tensor:
+    """uint16 bf16 bit patterns -> bf16 tensor on the device."""
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(device).view(torch.bfloat16)
+
+
+def from_dev_bits(t: torch.Tensor) -> np.ndarray:
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def check_block_ids(gpu_ids, ora_ids, gaps, inputs, layout, block_size, topk, rows=None, tol=GAP_TOL):
+    """Returns (exact rows, tie rows). Raises AssertionError on a violation."""
+    rows = list(range(gpu_ids.shape[0])) if rows is None else list(rows)
+    exact = ties = 0
+    for i, r in enumerate(rows):
+        for g in range(gpu_ids.shape[1]):
+            a, b = gpu_ids[i, g], ora_ids[i, g]
+            if np.array_equal(a, b):
+                exact += 1
+                continue
+            assert gaps[i, g] <= tol, f"row {r} group {g}: ids differ with gap {gaps[i, g]}: {a} vs {b}"
+            _, pos = layout.locate(r)
+            sc = O.row_block_scores(inputs["index_q"], inputs["index_k"], layout, r, g, block_size)
+            assert O.selection_is_valid(a, sc, pos, block_size, topk, tol), \
+                f"row {r} group {g}: invalid tie selection {a} (oracle {b})"
+            ties += 1
+    return exact, ties
+
+
+def check_outputs(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse_ref: np.ndarray, what=""):
+    o_gpu = o_gpu.astype(np.float64)
+    err = np.abs(o_gpu - o_ref)
+    rel = np.linalg.norm(o_gpu - o_ref) / max(np.linalg.norm(o_ref), 1e-30)
+    lerr = np.abs(lse_gpu.astype(np.float64) - lse_ref)
+    bound = O_MAX_ABS + BF16_HALF_ULP_REL * np.abs(o_ref)
+    worst = np.unravel_index(np.argmax(err - bound), err.shape)
+    assert (err <= bound).all(), \
+        f"{what} O error {err[worst]:.3e} > bound {bound[worst]:.3e} at {worst} (max-abs {err.max():.3e})"
+    assert rel <= O_REL_L2, f"{what} O rel-L2 {rel:.3e}"
+    assert lerr.max() <= O_MAX_ABS, f"{what} LSE max-abs {lerr.max():.3e}"
+    return float(err.max()), float(rel), float(lerr.max())
