@@ -241,6 +241,16 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 }
 
 // ---------------------------------------------------------------- host side
+}  // namespace
+
+// key-block-outer prefill (sparse_attn_prefill.hip)
+size_t msa_kvo_workspace_size(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk);
+int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
+                    int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream);
+
+namespace {
+
 int validate_attn(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, int topk) {
   int st = msa_host::validate_seqs(seqs);
   if (st != MSA_OK) return st;
@@ -338,24 +348,19 @@ extern "C" int msa_sparse_attn_decode(const void* q, const void* k, const void* 
 extern "C" size_t msa_sparse_attn_prefill_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
                                                         int head_dim, int block_size, int topk) {
   if (validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
-  return 0;
+  return msa_kvo_workspace_size(seqs, num_q_heads, num_kv_heads, block_size, topk);
 }
 
 extern "C" int msa_sparse_attn_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids,
                                        const msa_seqs* seqs, int num_q_heads, int num_kv_heads, int head_dim,
                                        int block_size, int topk, float softmax_scale, void* o, float* lse,
                                        void* workspace, size_t workspace_bytes, hipStream_t stream) {
-  (void)workspace;
-  (void)workspace_bytes;
   int st = validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk);
   if (st != MSA_OK) return st;
   if (seqs->total_q_rows == 0) return MSA_OK;
   if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
-  SplitPlan sp;
-  sp.nsplit = 1;
-  sp.slots_per_split = topk;
-  return run_rows(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o, lse,
-                  sp, nullptr, stream);
+  return msa_kvo_prefill(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o,
+                         lse, workspace, workspace_bytes, stream);
 }
 
 extern "C" const char* msa_strerror(int status) {

@@ -1,0 +1,656 @@
+// Prefill Main Branch of MSA on gfx950, key-block-outer.
+//
+// The sparse-attention equation of Sec. 3.1 restricted to one selected block
+// is an ordinary softmax attention over <= B_k keys.  Iterating queries on the
+// outside would fetch a 2 x B_k x d_h K/V block per (query, group, block)
+// incidence; iterating key blocks on the outside fetches every block once and
+// gathers the queries that picked it, so each incidence costs a Q gather, a
+// partial write and a partial read instead (Sec. 4.2, the Q-outer / KV-outer
+// IO comparison).  The partial of each incidence is normalised locally and
+// merged afterwards with the log-sum-exp rule of Sec. 4.2 ("Two-phase
+// forward"), so no atomics touch O.
+//
+// Per chunk of query rows (the partial buffer is k x rows x H_q x d_h):
+//   kvo_count    incidences per tile (group r, key block), device atomics
+//   kvo_scan*    exclusive offsets of handles and of work items per tile
+//   kvo_fill     handle (row in chunk << 6 | slot) lists per tile
+//   kvo_attn     persistent CTAs; a work item is <= kItemQueries queries of one
+//                tile.  K and V^T of the block are staged in LDS once per tile,
+//                each wave gathers 32 (query, head) rows, computes S^T = K Q^T
+//                and O^T = V^T P^T with MFMA 32x32x16 and writes the bf16
+//                partial and its LSE into the incidence's slot.
+//   kvo_combine  O and LSE per (row, head) from the valid slots.
+#include <algorithm>
+
+#include "msa_common.h"
+
+namespace {
+
+using namespace msa;
+
+constexpr int kHeadDim = 128;
+constexpr int kItemQueries = 256;      // queries of one tile per work item
+constexpr int kAttnThreads = 256;      // 4 waves
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bool slot_valid(int b, int p, int BK) { return b >= 0 && p >= 0 && b <= p / BK; }
+
+__device__ __forceinline__ int row_position(const msa_seqs& sq, int64_t row, int* seq_out) {
+  const int s = find_seq(sq.q_offsets, sq.num_seqs, row);
+  const SeqGeom g = seq_geom(sq, s);
+  int p = g.kv_len - g.q_rows + static_cast<int>(row - g.q_begin);
+  if (p >= g.kv_len) p = -1;
+  *seq_out = s;
+  return p;
+}
+
+// ---------------------------------------------------------------- setup
+// blk_base[s] = key blocks of the sequences before s (kv_len clamped to max_kv_len).
+__global__ __launch_bounds__(256) void kvo_block_base_kernel(msa_seqs sq, int BK, int64_t* __restrict__ blk_base) {
+  __shared__ int64_t part[256];
+  const int t = threadIdx.x;
+  const int S = sq.num_seqs;
+  const int per = (S + 255) / 256;
+  const int s0 = t * per, s1 = min(S, s0 + per);
+  auto nblk = [&](int s) -> int64_t {
+    int64_t len = seq_geom(sq, s).kv_len;
+    if (len > sq.max_kv_len) len = sq.max_kv_len;
+    return (len + BK - 1) / BK;
+  };
+  int64_t acc = 0;
+  for (int s = s0; s < s1; ++s) acc += nblk(s);
+  part[t] = acc;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 256; ++i) { int64_t x = part[i]; part[i] = run; run += x; }
+    blk_base[S] = run;
+  }
+  __syncthreads();
+  acc = part[t];
+  for (int s = s0; s < s1; ++s) { blk_base[s] = acc; acc += nblk(s); }
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+// ---------------------------------------------------------------- reverse index
+// One thread per (row, group) of the chunk.
+__global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
+                                                        const int64_t* __restrict__ blk_base, int H_kv, int BK,
+                                                        int topk, int64_t nbcap, int64_t row0, int64_t nrows,
+                                                        int32_t* __restrict__ cnt) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= nrows * H_kv) return;
+  const int64_t row = row0 + i / H_kv;
+  const int r = static_cast<int>(i % H_kv);
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
+  for (int j = 0; j < topk; ++j) {
+    const int b = ids[j];
+    if (!slot_valid(b, p, BK)) continue;
+    if (blk_base[s] + b >= nbcap) continue;
+    atomicAdd(&cnt[base + b], 1);
+  }
+}
+
+__global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
+                                                       const int64_t* __restrict__ blk_base, int H_kv, int BK,
+                                                       int topk, int64_t nbcap, int64_t row0, int64_t nrows,
+                                                       const int32_t* __restrict__ tile_off,
+                                                       int32_t* __restrict__ cursor, uint32_t* __restrict__ handles) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= nrows * H_kv) return;
+  const int64_t rl = i / H_kv;
+  const int64_t row = row0 + rl;
+  const int r = static_cast<int>(i % H_kv);
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
+  for (int j = 0; j < topk; ++j) {
+    const int b = ids[j];
+    if (!slot_valid(b, p, BK)) continue;
+    if (blk_base[s] + b >= nbcap) continue;
+    const int64_t tile = base + b;
+    const int pos = atomicSub(&cursor[tile], 1) - 1;     // cursor starts at the tile's count
+    handles[tile_off[tile] + pos] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(j);
+  }
+}
+
+// Two-array exclusive scan (handles per tile, work items per tile) in three
+// kernels: per-block scan, scan of block totals, add.
+constexpr int kScanPerBlock = 2048;   // 256 threads x 8
+
+__global__ __launch_bounds__(256) void kvo_scan_block_kernel(const int32_t* __restrict__ cnt, int64_t n,
+                                                             int32_t* __restrict__ tile_off,
+                                                             int32_t* __restrict__ item_off,
+                                                             int32_t* __restrict__ blk_tot) {
+  __shared__ int32_t sa[256], sb[256];
+  const int t = threadIdx.x;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanPerBlock + t * 8;
+  int32_t a[8], b[8];
+  int32_t ta = 0, tb = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int32_t c = base + e < n ? cnt[base + e] : 0;
+    a[e] = ta; b[e] = tb;
+    ta += c;
+    tb += (c + kItemQueries - 1) / kItemQueries;
+  }
+  sa[t] = ta; sb[t] = tb;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int32_t xa = t >= off ? sa[t - off] : 0;
+    const int32_t xb = t >= off ? sb[t - off] : 0;
+    __syncthreads();
+    sa[t] += xa; sb[t] += xb;
+    __syncthreads();
+  }
+  const int32_t pa = sa[t] - ta, pb = sb[t] - tb;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (base + e < n) { tile_off[base + e] = a[e] + pa; item_off[base + e] = b[e] + pb; }
+  if (t == 255) { blk_tot[2 * blockIdx.x] = sa[255]; blk_tot[2 * blockIdx.x + 1] = sb[255]; }
+}
+
+__global__ __launch_bounds__(1024) void kvo_scan_top_kernel(int32_t* __restrict__ blk_tot, int nblk,
+                                                            int32_t* __restrict__ tile_off,
+                                                            int32_t* __restrict__ item_off, int64_t n) {
+  __shared__ int32_t sa[1024], sb[1024];
+  const int t = threadIdx.x;
+  const int per = (nblk + 1023) / 1024;
+  const int b0 = t * per, b1 = min(nblk, b0 + per);
+  int32_t ta = 0, tb = 0;
+  for (int b = b0; b < b1; ++b) { ta += blk_tot[2 * b]; tb += blk_tot[2 * b + 1]; }
+  sa[t] = ta; sb[t] = tb;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t xa = t >= off ? sa[t - off] : 0;
+    const int32_t xb = t >= off ? sb[t - off] : 0;
+    __syncthreads();
+    sa[t] += xa; sb[t] += xb;
+    __syncthreads();
+  }
+  int32_t ra = sa[t] - ta, rb = sb[t] - tb;
+  for (int b = b0; b < b1; ++b) {
+    const int32_t xa = blk_tot[2 * b], xb = blk_tot[2 * b + 1];
+    blk_tot[2 * b] = ra; blk_tot[2 * b + 1] = rb;
+    ra += xa; rb += xb;
+  }
+  if (t == 1023) { tile_off[n] = sa[1023]; item_off[n] = sb[1023]; }
+}
+
+__global__ __launch_bounds__(256) void kvo_scan_add_kernel(const int32_t* __restrict__ blk_tot, int64_t n,
+                                                           int32_t* __restrict__ tile_off,
+                                                           int32_t* __restrict__ item_off) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t b = i / kScanPerBlock;
+  tile_off[i] += blk_tot[2 * b];
+  item_off[i] += blk_tot[2 * b + 1];
+}
+
+// ---------------------------------------------------------------- attention
+template <int BK>
+struct KvoSmem {
+  uint16_t k[BK][kHeadDim + 8];     // K block, row-major (+16 B pad per row)
+  uint16_t vt[kHeadDim][BK + 4];    // V block transposed (+8 B pad per row)
+};
+
+// Largest i with arr[i] <= x, for arr non-decreasing with arr[0] <= x.
+template <typename T>
+__device__ __forceinline__ int64_t upper_index(const T* __restrict__ arr, int64_t n, int64_t x) {
+  int64_t lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (static_cast<int64_t>(arr[mid]) <= x) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <int BK>
+__global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, msa_seqs sq,
+    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk,
+    int64_t nbcap, int64_t row0, float scale_log2, uint16_t* __restrict__ o_buf, float* __restrict__ lse_buf) {
+  __shared__ KvoSmem<BK> sm;
+  __shared__ int32_t s_row[kItemQueries];     // query row inside the chunk
+  __shared__ int32_t s_pos[kItemQueries];     // its absolute position
+  __shared__ int32_t s_slot[kItemQueries];    // slot of this block in the row's id list
+  constexpr int MT = BK / 32;                 // 32-key tiles of S^T
+  constexpr int KS = kHeadDim / 16;           // k-steps of S^T = K Q^T
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int n = lane & 31, h = lane >> 5;
+  const int G = H_q / H_kv;
+  const int qpw = 32 / G;                     // queries per wave pass
+  const int jq = n / G, hh = n % G;           // this lane's (query within pass, head)
+  const bool lane_row = n < qpw * G;
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  int64_t staged = -1;
+
+  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int64_t gb = tile % nbcap;
+    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+    const SeqGeom g = seq_geom(sq, s);
+    const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
+
+    __syncthreads();                          // the previous item is finished with LDS
+    if (static_cast<int>(threadIdx.x) < nq) {
+      const uint32_t hd = handles[h0 + threadIdx.x];
+      const int32_t rl = static_cast<int32_t>(hd >> 6);
+      s_row[threadIdx.x] = rl;
+      s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
+      // every query of the tile belongs to sequence s
+      s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
+    }
+    if (tile != staged) {
+      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kAttnThreads) {
+        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        const uint4 x = key0 + key < g.kv_len
+                            ? *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg)
+                            : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = x;
+      }
+      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += kAttnThreads) {
+        const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        uint4 rows[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int key = 4 * key4 + j;
+          rows[j] = key0 + key < g.kv_len
+                        ? *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg)
+                        : make_uint4(0, 0, 0, 0);
+        }
+        const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
+        const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&rows[1]);
+        const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&rows[2]);
+        const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&rows[3]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          uint2 w;
+          w.x = static_cast<uint32_t>(e0[e]) | (static_cast<uint32_t>(e1[e]) << 16);
+          w.y = static_cast<uint32_t>(e2[e]) | (static_cast<uint32_t>(e3[e]) << 16);
+          *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = w;
+        }
+      }
+      staged = tile;
+    }
+    __syncthreads();
+
+    // passes of qpw queries x G heads = 32 rows per wave; Q of the next pass is
+    // requested before the current pass computes.
+    const int stride = 4 * qpw;
+    int c = wave * qpw;
+    bf16x8 bq[KS];
+    auto load_q = [&](int cc, bf16x8* dst) {
+      const int qi = cc + jq;
+      const bool ok = lane_row && qi < nq;
+      const int64_t row = row0 + (ok ? s_row[qi] : 0);
+      const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + h * (kHeadDim / 2);
+#pragma unroll
+      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld_bf16x8(qrow + 8 * st) : zero_bf16x8();
+    };
+    if (c < nq) load_q(c, bq);
+    for (; c < nq; c += stride) {
+      bf16x8 bq_next[KS];
+      if (c + stride < nq) load_q(c + stride, bq_next);
+      const int qi = c + jq;
+      const bool valid = lane_row && qi < nq;
+      const int p = valid ? s_pos[qi] : -1;
+
+      // S^T = K Q^T: lane (n, h) holds keys 32i + 8(e/4) + 4h + e%4 of row n
+      f32x16 acc_s[MT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) {
+        acc_s[i] = f32x16{};
+        const uint16_t* kr = &sm.k[32 * i + n][h * (kHeadDim / 2)];
+#pragma unroll
+        for (int st = 0; st < KS; ++st)
+          acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st)),
+                                  bq[st], acc_s[i]);
+        __builtin_amdgcn_sched_barrier(0);    // bound how far LDS operand reads are hoisted
+      }
+      float m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = key0 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+          float z = acc_s[i][e] * scale_log2;
+          z = key <= p ? z : -INFINITY;
+          acc_s[i][e] = z;
+          m = fmaxf(m, z);
+        }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      const float mm = m == -INFINITY ? 0.f : m;
+      float l = 0.f;
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float pe = exp2f(acc_s[i][e] - mm);
+          acc_s[i][e] = pe;
+          l += pe;
+        }
+      l += __shfl_xor(l, 32);
+
+      // P in bf16 as the B operand of O^T = V^T P^T: k-step u covers keys
+      // 32(u/2) + 16(u%2) + {4h + e, 8 + 4h + e}; the lane's P values for it
+      // are acc_s[u/2][8(u%2) .. 8(u%2)+7].
+      bf16x8 bp[BK / 16];
+#pragma unroll
+      for (int u = 0; u < BK / 16; ++u) {
+        uint4 pw;
+        const int i = u >> 1, e0 = 8 * (u & 1);
+        pw.x = pack_bf16x2(acc_s[i][e0 + 0], acc_s[i][e0 + 1]);
+        pw.y = pack_bf16x2(acc_s[i][e0 + 2], acc_s[i][e0 + 3]);
+        pw.z = pack_bf16x2(acc_s[i][e0 + 4], acc_s[i][e0 + 5]);
+        pw.w = pack_bf16x2(acc_s[i][e0 + 6], acc_s[i][e0 + 7]);
+        bp[u] = __builtin_bit_cast(bf16x8, pw);
+      }
+      const bool empty = !(l > 0.f);
+      const float inv_l = empty ? 0.f : 1.f / l;
+      // partial slot of this incidence: [row][group][slot][head][d]
+      const int64_t prow = valid ? ((static_cast<int64_t>(s_row[qi]) * H_kv + r) * topk + s_slot[qi]) * G + hh : 0;
+      uint16_t* orow = o_buf + prow * kHeadDim + 4 * h;
+      // two halves of d (64 dims = 2 tiles each) keep 32 accumulators live
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        __builtin_amdgcn_sched_barrier(0);
+        f32x16 acc_o[2];
+        acc_o[0] = f32x16{};
+        acc_o[1] = f32x16{};
+#pragma unroll
+        for (int u = 0; u < BK / 16; ++u) {
+          const int kbase = 32 * (u >> 1) + 16 * (u & 1) + 4 * h;
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2) {
+            const uint16_t* vr = &sm.vt[32 * (2 * half + t2) + n][kbase];
+            const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+            const uint2 hi2 = *reinterpret_cast<const uint2*>(vr + 8);
+            uint4 w;
+            w.x = lo.x; w.y = lo.y; w.z = hi2.x; w.w = hi2.y;
+            acc_o[t2] = mfma32x32x16(__builtin_bit_cast(bf16x8, w), bp[u], acc_o[t2]);
+          }
+        }
+        if (valid) {
+          // O^T tile t: lane (n, h) holds d = 32t + 8(e/4) + 4h + e%4
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+            for (int e4 = 0; e4 < 4; ++e4) {
+              uint2 w;
+              w.x = pack_bf16x2(acc_o[t2][4 * e4 + 0] * inv_l, acc_o[t2][4 * e4 + 1] * inv_l);
+              w.y = pack_bf16x2(acc_o[t2][4 * e4 + 2] * inv_l, acc_o[t2][4 * e4 + 3] * inv_l);
+              *reinterpret_cast<uint2*>(orow + 32 * (2 * half + t2) + 8 * e4) = w;
+            }
+        }
+      }
+      if (valid && h == 0) lse_buf[prow] = empty ? -INFINITY : (mm + __log2f(l)) * kLn2;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) bq[st] = bq_next[st];
+    }
+  }
+}
+
+// ---------------------------------------------------------------- combine
+// One wave per (row, group) of the chunk: lane j reads slot j's LSEs, the
+// per-head weights go through LDS, and each lane accumulates 2G of the 128
+// dims of one of the group's G heads over the valid slots.
+constexpr int kCombineWaves = 4;
+
+__global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
+    const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int BK, int topk, int64_t row0,
+    int64_t nrows, const uint16_t* __restrict__ o_buf, const float* __restrict__ lse_buf, uint16_t* __restrict__ o,
+    float* __restrict__ lse) {
+  __shared__ float s_w[kCombineWaves][64][17];        // weight of slot j for head hh (G <= 16)
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  int64_t pr = static_cast<int64_t>(blockIdx.x) * kCombineWaves + wave;   // (row, group) pair
+  const bool active = pr < nrows * H_kv;
+  if (!active) pr = 0;                               // computes a row it does not store
+  const int64_t rl = pr / H_kv;
+  const int r = static_cast<int>(pr % H_kv);
+  const int G = H_q / H_kv;
+  const int64_t row = row0 + rl;
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const bool valid = lane < topk && slot_valid(ids[lane], p, BK);
+  const float* lrow = lse_buf + (rl * H_kv + r) * static_cast<int64_t>(topk) * G;
+  // per head: max and sum over the valid slots (lane j = slot j)
+  float tot[16];
+#pragma unroll
+  for (int hh = 0; hh < 16; ++hh) {
+    if (hh >= G) break;
+    const float x = valid ? lrow[lane * G + hh] : -INFINITY;
+    float a = x;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) a = fmaxf(a, __shfl_xor(a, off));
+    float e = (valid && a > -INFINITY && x > -INFINITY) ? exp2f((x - a) * kLog2e) : 0.f;
+    float sum = e;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) sum += __shfl_xor(sum, off);
+    const float t = a > -INFINITY ? a + __logf(sum) : -INFINITY;
+    tot[hh] = t;
+    s_w[wave][lane][hh] = (valid && x > -INFINITY && t > -INFINITY) ? exp2f((x - t) * kLog2e) : 0.f;
+  }
+  __syncthreads();
+  // dims per lane: 8 for G <= 4, 16 for G <= 8, 32 for G <= 16 (a multiple of
+  // the 16-byte loads); lane covers head hh, dims [dd, dd + per); lanes past
+  // G * 128 / per idle.
+  const int per = G <= 4 ? 8 : (G <= 8 ? 16 : 32);
+  const int lanes_per_head = kHeadDim / per;
+  const bool lane_on = lane < G * lanes_per_head;
+  const int hh = lane_on ? lane / lanes_per_head : 0;
+  const int dd = (lane % lanes_per_head) * per;
+  float acc[32];
+#pragma unroll
+  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
+  const uint16_t* obase = o_buf + ((rl * H_kv + r) * static_cast<int64_t>(topk)) * G * kHeadDim +
+                          static_cast<int64_t>(hh) * kHeadDim + dd;
+  const uint64_t vmask = __ballot(valid);
+  for (int j = 0; j < topk && lane_on; ++j) {
+    if (!((vmask >> j) & 1ull)) continue;
+    const float w = s_w[wave][j][hh];
+    const uint16_t* src = obase + static_cast<int64_t>(j) * G * kHeadDim;
+#pragma unroll
+    for (int e8 = 0; e8 < 4; ++e8) {
+      if (8 * e8 >= per) break;
+      const uint4 x = *reinterpret_cast<const uint4*>(src + 8 * e8);
+      const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[8 * e8 + 2 * e] += w * __uint_as_float(xs[e] << 16);
+        acc[8 * e8 + 2 * e + 1] += w * __uint_as_float(xs[e] & 0xFFFF0000u);
+      }
+    }
+  }
+  if (!active || !lane_on) return;
+  const int head = r * G + hh;
+  uint16_t* dst = o + (row * H_q + head) * kHeadDim + dd;
+#pragma unroll
+  for (int e8 = 0; e8 < 4; ++e8) {
+    if (8 * e8 >= per) break;
+    uint4 wv;
+    wv.x = pack_bf16x2(acc[8 * e8 + 0], acc[8 * e8 + 1]);
+    wv.y = pack_bf16x2(acc[8 * e8 + 2], acc[8 * e8 + 3]);
+    wv.z = pack_bf16x2(acc[8 * e8 + 4], acc[8 * e8 + 5]);
+    wv.w = pack_bf16x2(acc[8 * e8 + 6], acc[8 * e8 + 7]);
+    *reinterpret_cast<uint4*>(dst + 8 * e8) = wv;
+  }
+  if (lane % lanes_per_head == 0) {
+    float t = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < 16; ++x)
+      if (x == hh) t = tot[x];
+    lse[row * H_q + head] = t;
+  }
+}
+
+// ---------------------------------------------------------------- host plan
+struct KvoPlan {
+  int64_t nbcap;        // key blocks over all sequences (upper bound)
+  int64_t ntile;        // H_kv * nbcap
+  int64_t chunk_rows;   // query rows per chunk
+  int nscan;            // scan blocks
+  // workspace offsets
+  size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_handles, off_obuf, off_lse, total;
+};
+
+size_t fixed_bytes(KvoPlan& pl, const msa_seqs* seqs) {
+  using msa_host::align_up;
+  size_t o = 0;
+  pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
+  return o;
+}
+
+size_t per_row_bytes(int H_q, int H_kv, int topk) {
+  return sizeof(uint32_t) * H_kv * topk + static_cast<size_t>(topk) * H_q * (kHeadDim * 2 + sizeof(float));
+}
+
+void layout_rows(KvoPlan& pl, size_t fixed, int H_q, int H_kv, int topk) {
+  using msa_host::align_up;
+  size_t o = fixed;
+  pl.off_handles = o; o = align_up(o + sizeof(uint32_t) * pl.chunk_rows * H_kv * topk, 256);
+  pl.off_obuf = o;    o = align_up(o + sizeof(uint16_t) * static_cast<size_t>(topk) * pl.chunk_rows * H_q * kHeadDim, 256);
+  pl.off_lse = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(topk) * pl.chunk_rows * H_q, 256);
+  pl.total = o;
+}
+
+constexpr size_t kDefaultPartialBytes = size_t(32) << 30;
+
+int make_kvo_plan(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk, size_t budget, KvoPlan* pl) {
+  const int64_t nb = (seqs->max_kv_len + BK - 1) / BK;
+  pl->nbcap = static_cast<int64_t>(seqs->num_seqs) * (nb > 0 ? nb : 1);
+  pl->ntile = static_cast<int64_t>(H_kv) * pl->nbcap;
+  if (pl->ntile >= (int64_t(1) << 31) - 1) return MSA_ERR_UNSUPPORTED;
+  pl->nscan = static_cast<int>((pl->ntile + kScanPerBlock - 1) / kScanPerBlock);
+  if (pl->nscan > 1024 * 64) return MSA_ERR_UNSUPPORTED;
+  const size_t fixed = fixed_bytes(*pl, seqs);
+  const size_t prb = per_row_bytes(H_q, H_kv, topk);
+  int64_t rows = seqs->total_q_rows > 0 ? seqs->total_q_rows : 1;
+  pl->chunk_rows = rows;
+  layout_rows(*pl, fixed, H_q, H_kv, topk);
+  if (pl->total <= budget) {
+    // everything in one chunk
+  } else if (budget > fixed) {
+    const int64_t fit = static_cast<int64_t>((budget - fixed - 3 * 256) / prb);
+    if (fit < rows) rows = fit;
+  } else {
+    rows = 0;
+  }
+  // incidences of a chunk must fit the int32 offsets
+  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  if (rows > max_rows) rows = max_rows;
+  if (rows < 1) return MSA_ERR_WORKSPACE;
+  pl->chunk_rows = rows;
+  layout_rows(*pl, fixed, H_q, H_kv, topk);
+  return MSA_OK;
+}
+
+// CTAs of a persistent kernel: every CU filled to the kernel's occupancy.
+template <typename K>
+int persistent_ctas(K kernel, int threads, int* cache) {
+  if (*cache == 0) {
+    int dev = 0, cus = 256, per_cu = 1;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu < 1)
+      per_cu = 1;
+    *cache = cus * per_cu;
+  }
+  return *cache;
+}
+
+}  // namespace
+
+// Used by the prefill entry points in sparse_attn.hip.
+size_t msa_kvo_workspace_size(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk) {
+  KvoPlan pl;
+  if (make_kvo_plan(seqs, H_q, H_kv, BK, topk, kDefaultPartialBytes, &pl) != MSA_OK) {
+    // the default budget is too small for one row: ask for exactly one row
+    if (make_kvo_plan(seqs, H_q, H_kv, BK, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+    pl.chunk_rows = 1;
+    layout_rows(pl, fixed_bytes(pl, seqs), H_q, H_kv, topk);
+  }
+  return pl.total;
+}
+
+int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
+                    int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, void* workspace,
+                    size_t workspace_bytes, hipStream_t stream) {
+  KvoPlan pl;
+  int st = make_kvo_plan(seqs, H_q, H_kv, BK, topk, workspace_bytes, &pl);
+  if (st != MSA_OK) return st;
+  if (!workspace || workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  auto* blk_base = reinterpret_cast<int64_t*>(ws + pl.off_blk_base);
+  auto* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
+  auto* tile_off = reinterpret_cast<int32_t*>(ws + pl.off_tile_off);
+  auto* item_off = reinterpret_cast<int32_t*>(ws + pl.off_item_off);
+  auto* blk_tot = reinterpret_cast<int32_t*>(ws + pl.off_blk_tot);
+  auto* handles = reinterpret_cast<uint32_t*>(ws + pl.off_handles);
+  auto* o_buf = reinterpret_cast<uint16_t*>(ws + pl.off_obuf);
+  auto* lse_buf = reinterpret_cast<float*>(ws + pl.off_lse);
+  const msa_seqs sq = *seqs;
+  auto* qp = static_cast<const uint16_t*>(q);
+  auto* kp = static_cast<const uint16_t*>(k);
+  auto* vp = static_cast<const uint16_t*>(v);
+  auto* op = static_cast<uint16_t*>(o);
+  const float sl2 = scale * kLog2e;
+
+  hipLaunchKernelGGL(kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK, blk_base);
+  const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((pl.ntile + 255) / 256, 4096));
+  for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
+    const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
+    const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, pl.ntile, 0);
+    hipLaunchKernelGGL(kvo_count_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
+                       topk, pl.nbcap, r0, nr, cnt);
+    hipLaunchKernelGGL(kvo_scan_block_kernel, dim3(pl.nscan), dim3(256), 0, stream, cnt, pl.ntile, tile_off,
+                       item_off, blk_tot);
+    hipLaunchKernelGGL(kvo_scan_top_kernel, dim3(1), dim3(1024), 0, stream, blk_tot, pl.nscan, tile_off, item_off,
+                       pl.ntile);
+    hipLaunchKernelGGL(kvo_scan_add_kernel, dim3(static_cast<unsigned>((pl.ntile + 255) / 256)), dim3(256), 0,
+                       stream, blk_tot, pl.ntile, tile_off, item_off);
+    hipLaunchKernelGGL(kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
+                       topk, pl.nbcap, r0, nr, tile_off, cnt, handles);
+    static int ctas64 = 0, ctas128 = 0;
+    if (BK == 64)
+      hipLaunchKernelGGL(kvo_attn_kernel<64>, dim3(persistent_ctas(kvo_attn_kernel<64>, kAttnThreads, &ctas64)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
+                         sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
+                         lse_buf);
+    else
+      hipLaunchKernelGGL(kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, kAttnThreads, &ctas128)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
+                         sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
+                         lse_buf);
+    const int64_t pairs = nr * H_kv;
+    hipLaunchKernelGGL(kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
+                       dim3(64 * kCombineWaves), 0, stream, block_ids, sq, H_q, H_kv, BK, topk, r0, nr, o_buf,
+                       lse_buf, op, lse);
+  }
+  return msa_host::launch_status();
+}
