@@ -9,71 +9,74 @@
 // the local block is forced and never scored.  Selection ranks raw fp32 dot
 // products (Sec. 4.1 "Exp-free selection": monotone maps keep the order).
 //
-// Two kernels per chunk of query rows:
-//   index_block_max  MFMA 32x32x16 (keys as M, index rows as N) over one key
-//                    block at a time; the block max is reduced in registers and
-//                    one permlane32 swap, then written as M[row][block] (fp32).
-//   index_topk       one wave per index row streams M[row][0..lb) 64 blocks at a
-//                    time, filters against the current k-1-th best key and keeps
-//                    a sorted 64-entry list (one 64-bit key per lane).
+// Work units: a row group is qr = 64 / H_kv consecutive query rows of one
+// sequence (64 index rows: query row x group, contiguous in index_q); a unit is
+// U consecutive row groups of one sequence.  Per chunk of units:
+//   index_block_max_lds   (U = 4, prefill) one CTA = 4 waves = 256 index rows
+//                         sharing each K_idx block through a double-buffered LDS
+//                         ring fed by register prefetch two blocks ahead;
+//   index_block_max_wave  (U = 1, few rows per sequence, e.g. decode) one wave
+//                         per row group and slice of key blocks;
+// both run MFMA 32x32x16 with keys as M and index rows as N, reduce the block
+// max in registers plus one permlane32 swap and write M[row][block] (fp32);
+//   index_topk            one wave per index row streams M[row][0..lb) 64
+//                         blocks at a time, filters against the current k-1-th
+//                         best key and keeps a sorted list (one key per lane).
 #include "msa_common.h"
 
 namespace {
 
 using namespace msa;
 
-constexpr int kWavesPerBlock = 4;
-constexpr int kBlocksPerWave = 16;     // key blocks one wave scores per launch slice
+constexpr int kWaves = 4;
+constexpr int kBlocksPerCta = 64;      // key blocks per CTA slice, LDS kernel
 constexpr int kSmallInsert = 6;        // survivors per 64-block step inserted one by one
 
 // ---------------------------------------------------------------- setup
-// group_off[s] = number of row groups before sequence s; a row group is `qr`
-// consecutive query rows of one sequence (qr * H_kv = 64 index rows).
-__global__ __launch_bounds__(256) void row_group_offsets_kernel(msa_seqs sq, int qr,
-                                                                int32_t* __restrict__ group_off) {
+// unit_off[s] = units before sequence s.
+__global__ __launch_bounds__(256) void unit_offsets_kernel(msa_seqs sq, int qr, int U,
+                                                           int32_t* __restrict__ unit_off) {
   __shared__ int32_t part[256];
   const int t = threadIdx.x;
   const int S = sq.num_seqs;
   const int per = (S + 255) / 256;
   const int s0 = t * per, s1 = min(S, s0 + per);
+  auto units = [&](int s) -> int32_t {
+    const int rows = sq.q_offsets[s + 1] - sq.q_offsets[s];
+    const int groups = rows > 0 ? (rows + qr - 1) / qr : 0;
+    return (groups + U - 1) / U;
+  };
   int32_t acc = 0;
-  for (int s = s0; s < s1; ++s) {
-    int rows = sq.q_offsets[s + 1] - sq.q_offsets[s];
-    acc += rows > 0 ? (rows + qr - 1) / qr : 0;
-  }
+  for (int s = s0; s < s1; ++s) acc += units(s);
   part[t] = acc;
   __syncthreads();
   if (t == 0) {
     int32_t run = 0;
     for (int i = 0; i < 256; ++i) { int32_t x = part[i]; part[i] = run; run += x; }
-    group_off[S] = run;
+    unit_off[S] = run;
   }
   __syncthreads();
   acc = part[t];
-  for (int s = s0; s < s1; ++s) {
-    group_off[s] = acc;
-    int rows = sq.q_offsets[s + 1] - sq.q_offsets[s];
-    acc += rows > 0 ? (rows + qr - 1) / qr : 0;
-  }
+  for (int s = s0; s < s1; ++s) { unit_off[s] = acc; acc += units(s); }
 }
 
-struct GroupRows {
+struct UnitRows {
   bool ok;
   int s;
   SeqGeom g;
-  int t0;       // first query row (inside the sequence) of the group
-  int nq;       // valid query rows in the group
+  int t0;       // first query row (inside the sequence) of the unit
+  int nq;       // valid query rows in the unit
 };
 
-__device__ __forceinline__ GroupRows locate_group(const msa_seqs& sq, const int32_t* __restrict__ group_off,
-                                                  int64_t gidx, int qr) {
-  GroupRows r;
+__device__ __forceinline__ UnitRows locate_unit(const msa_seqs& sq, const int32_t* __restrict__ unit_off,
+                                                int64_t uidx, int qr, int U) {
+  UnitRows r;
   r.ok = false;
-  if (gidx >= group_off[sq.num_seqs]) return r;
-  r.s = find_seq(group_off, sq.num_seqs, gidx);
+  if (uidx >= unit_off[sq.num_seqs]) return r;
+  r.s = find_seq(unit_off, sq.num_seqs, uidx);
   r.g = seq_geom(sq, r.s);
-  r.t0 = static_cast<int>(gidx - group_off[r.s]) * qr;
-  r.nq = min(qr, r.g.q_rows - r.t0);
+  r.t0 = static_cast<int>(uidx - unit_off[r.s]) * qr * U;
+  r.nq = min(qr * U, r.g.q_rows - r.t0);
   // never touch query rows past the query-side tensors
   const int64_t left = sq.total_q_rows - (static_cast<int64_t>(r.g.q_begin) + r.t0);
   if (left < r.nq) r.nq = static_cast<int>(left > 0 ? left : 0);
@@ -81,94 +84,230 @@ __device__ __forceinline__ GroupRows locate_group(const msa_seqs& sq, const int3
   return r;
 }
 
-// ---------------------------------------------------------------- scores
-// One wave: 64 index rows (qr query rows x H_kv groups, contiguous in index_q)
-// against key blocks [kb0, kb0 + kBlocksPerWave) of its sequence.
-template <int D_IDX, int BK>
-__global__ __launch_bounds__(256) void index_block_max_kernel(
-    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
-    const int32_t* __restrict__ group_off, int H_kv, int qr, int64_t g0, int64_t g1,
-    float* __restrict__ M, int64_t ldm) {
-  constexpr int KS = D_IDX / 16;        // k-steps of the MFMA
-  constexpr int HALF = D_IDX / 2;       // dims a lane half supplies
-  constexpr int MT = BK / 32;           // 32-key M tiles per block
-  const int lane = lane_id();
-  const int64_t gidx = g0 + static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
-  if (gidx >= g1) return;
-  GroupRows gr = locate_group(sq, group_off, gidx, qr);
-  if (!gr.ok) return;
-  const int p_last = gr.g.kv_len - gr.g.q_rows + gr.t0 + gr.nq - 1;
-  if (p_last < 0) return;
-  const int lb_max = p_last / BK;                    // candidates are blocks < lb
-  const int kb0 = blockIdx.y * kBlocksPerWave;
-  const int kb1 = min(min(kb0 + kBlocksPerWave, lb_max), static_cast<int>(ldm));
-  if (kb0 >= kb1) return;
-
-  const int n = lane & 31, h = lane >> 5;
-  const int nvalid = gr.nq * H_kv;
-  // B operand: the wave's 64 index rows (two 32-column N tiles), kept in registers.
-  const uint16_t* qbase = index_q + (static_cast<int64_t>(gr.g.q_begin + gr.t0) * H_kv) * D_IDX;
-  bf16x8 bq[2][KS];
+// B operand of S^T = K Q^T for the wave's 64 index rows (two 32-column tiles);
+// lane (n, h) supplies dims h*D/2 + 8*st .. +8 of row 32j + n.
+template <int D_IDX>
+__device__ __forceinline__ void load_index_rows(const uint16_t* __restrict__ qbase, int nvalid, int n, int h,
+                                                bf16x8 (&bq)[2][D_IDX / 16]) {
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
     const int row = 32 * j + n;
 #pragma unroll
-    for (int s = 0; s < KS; ++s)
-      bq[j][s] = row < nvalid ? ld_bf16x8(qbase + static_cast<int64_t>(row) * D_IDX + h * HALF + 8 * s)
-                              : zero_bf16x8();
+    for (int st = 0; st < D_IDX / 16; ++st)
+      bq[j][st] = row < nvalid ? ld_bf16x8(qbase + static_cast<int64_t>(row) * D_IDX + h * (D_IDX / 2) + 8 * st)
+                               : zero_bf16x8();
   }
-  const uint16_t* kbase = index_k + gr.g.kv_start * D_IDX + h * HALF;
-  float* mrow = M + ((gidx - g0) * kWave + lane) * ldm;
-  const bool store = lane < nvalid;
+}
 
-  for (int kb = kb0; kb < kb1; ++kb) {
+// Block max of one key block for the wave's 64 rows from the S^T tiles: each
+// lane holds half of the block's keys for its column; lanes 0-31 then own rows
+// 0-31 and lanes 32-63 rows 32-63.
+template <int MT>
+__device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][2]) {
+  float pm[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    float m = acc[0][j][0];
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, acc[i][j][e]);
+    pm[j] = m;
+  }
+  auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(pm[0]), __float_as_uint(pm[1]), false, false);
+  return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+}
+
+// ---------------------------------------------------------------- scores, LDS
+constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
+
+template <int D_IDX, int BK>
+struct IdxSmem {
+  uint16_t k[2][BK][D_IDX + 8];                   // K_idx blocks, row-major, +16 B pad per row
+  float stage[kWaves][kWave][kStageBlocks + 1];    // per wave: 64 rows x 16 block maxima
+};
+
+template <int D_IDX, int BK>
+__global__ __launch_bounds__(256, 4) void index_block_max_lds_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
+    int64_t ldm) {
+  constexpr int KS = D_IDX / 16;                        // k-steps of the MFMA
+  constexpr int MT = BK / 32;                           // 32-key M tiles per block
+  constexpr int SEGS = D_IDX / 8;                       // 16-byte segments per key row
+  constexpr int CH = BK * SEGS / 256;                   // 16-byte loads per thread per block
+  __shared__ IdxSmem<D_IDX, BK> sm;
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int64_t uidx = u0 + blockIdx.x;
+  if (uidx >= u1) return;
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, kWaves);
+  if (!ur.ok) return;
+  const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
+  if (p_last < 0) return;
+  const int kb0 = blockIdx.y * kBlocksPerCta;
+  const int kb1 = min(min(kb0 + kBlocksPerCta, p_last / BK), static_cast<int>(ldm));
+  if (kb0 >= kb1) return;                               // uniform over the CTA
+
+  const int n = lane & 31, h = lane >> 5;
+  const int wq0 = w * qr;                               // this wave's first query row in the unit
+  const int nvalid = max(0, min(qr, ur.nq - wq0)) * H_kv;
+  bf16x8 bq[2][KS];
+  load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0 + wq0) * H_kv) * D_IDX, nvalid, n,
+                         h, bq);
+  // this wave's 64 rows of M; the block maxima of a 16-block group are staged
+  // in LDS and stored as 64-byte row segments (blocks past kb1 in the last
+  // group hold stale values that no row reads: they are >= its local block)
+  float* mrow0 = M + ((uidx - u0) * (kWaves * kWave) + w * kWave) * ldm;
+
+  const uint16_t* kseq = index_k + ur.g.kv_start * D_IDX;
+  auto load_block = [&](int kb, uint4 (&dst)[CH]) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int idx = threadIdx.x + 256 * c;
+      const int key = idx / SEGS, seg = idx % SEGS;
+      dst[c] = *reinterpret_cast<const uint4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
+    }
+  };
+  auto store_block = [&](int buf, const uint4 (&src)[CH]) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int idx = threadIdx.x + 256 * c;
+      const int key = idx / SEGS, seg = idx % SEGS;
+      *reinterpret_cast<uint4*>(&sm.k[buf][key][8 * seg]) = src[c];
+    }
+  };
+  auto compute = [&](int buf, int kb) {
+    if (nvalid == 0) return;
     f32x16 acc[MT][2];
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
-      bf16x8 a[KS];
+      const uint16_t* kr = &sm.k[buf][32 * i + n][h * (D_IDX / 2)];
+      acc[i][0] = f32x16{};
+      acc[i][1] = f32x16{};
 #pragma unroll
-      for (int s = 0; s < KS; ++s) a[s] = ld_bf16x8(kp + 8 * s);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        acc[i][j] = f32x16{};
-#pragma unroll
-        for (int s = 0; s < KS; ++s) acc[i][j] = mfma32x32x16(a[s], bq[j][s], acc[i][j]);
+      for (int st = 0; st < KS; ++st) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st));
+        acc[i][0] = mfma32x32x16(a, bq[0][st], acc[i][0]);
+        acc[i][1] = mfma32x32x16(a, bq[1][st], acc[i][1]);
       }
     }
-    // block max: each lane holds half of the block's keys for its column
-    float pm[2];
+    const float bm = block_max_rows<MT>(acc);
+    sm.stage[w][lane][kb & (kStageBlocks - 1)] = bm;
+    if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
+      // the wave writes 16 rows x 64 B per store pass (4 lanes per row, 16 B each)
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      const int kbase = kb & ~(kStageBlocks - 1);
+      const int qd = lane & 3;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      float m = acc[0][j][0];
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) m = fmaxf(m, acc[i][j][r]);
-      pm[j] = m;
+      for (int pass = 0; pass < 4; ++pass) {
+        const int row = 16 * pass + (lane >> 2);
+        const int b = kbase + 4 * qd;
+        if (row < nvalid && b < ldm) {
+          const float* src = &sm.stage[w][row][4 * qd];
+          *reinterpret_cast<float4*>(mrow0 + static_cast<int64_t>(row) * ldm + b) =
+              make_float4(src[0], src[1], src[2], src[3]);
+        }
+      }
     }
-    // lanes 0-31 gather column tile 0 (rows 0-31), lanes 32-63 tile 1 (rows 32-63)
-    auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(pm[0]), __float_as_uint(pm[1]), false, false);
-    const float bm = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));
+  };
+
+  uint4 ra[CH], rb[CH];
+  load_block(kb0, ra);
+  if (kb0 + 1 < kb1) load_block(kb0 + 1, rb);
+  store_block(0, ra);
+  __syncthreads();
+  // iteration i: LDS buffer i%2 holds block kb, the other register set holds kb+1
+  for (int kb = kb0; kb < kb1; kb += 2) {
+    if (kb + 2 < kb1) load_block(kb + 2, ra);
+    compute(0, kb);
+    if (kb + 1 < kb1) store_block(1, rb);
+    __syncthreads();
+    if (kb + 1 >= kb1) break;
+    if (kb + 3 < kb1) load_block(kb + 3, rb);
+    compute(1, kb + 1);
+    if (kb + 2 < kb1) store_block(0, ra);
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------- scores, per wave
+// One wave: one row group (U = 1) against key blocks [kb0, kb0 + nbw).
+template <int D_IDX, int BK>
+__global__ __launch_bounds__(256) void index_block_max_wave_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, int nbw,
+    float* __restrict__ M, int64_t ldm) {
+  constexpr int KS = D_IDX / 16;
+  constexpr int MT = BK / 32;
+  const int lane = lane_id();
+  const int64_t uidx = u0 + static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
+  if (uidx >= u1) return;
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, 1);
+  if (!ur.ok) return;
+  const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
+  if (p_last < 0) return;
+  const int kb0 = blockIdx.y * nbw;
+  const int kb1 = min(min(kb0 + nbw, p_last / BK), static_cast<int>(ldm));
+  if (kb0 >= kb1) return;
+
+  const int n = lane & 31, h = lane >> 5;
+  const int nvalid = ur.nq * H_kv;
+  bf16x8 bq[2][KS];
+  load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv) * D_IDX, nvalid, n, h, bq);
+  const uint16_t* kbase = index_k + ur.g.kv_start * D_IDX + h * (D_IDX / 2);
+  float* mrow = M + ((uidx - u0) * kWave + lane) * ldm;
+  const bool store = lane < nvalid;
+
+  auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const uint16_t* kp = kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
+#pragma unroll
+      for (int st = 0; st < KS; ++st) a[i][st] = ld_bf16x8(kp + 8 * st);
+    }
+  };
+  bf16x8 a[MT][KS], an[MT][KS];
+  load_a(kb0, a);
+  for (int kb = kb0; kb < kb1; ++kb) {
+    if (kb + 1 < kb1) load_a(kb + 1, an);              // next block in flight during this one
+    f32x16 acc[MT][2];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc[i][0] = f32x16{};
+      acc[i][1] = f32x16{};
+#pragma unroll
+      for (int st = 0; st < KS; ++st) {
+        acc[i][0] = mfma32x32x16(a[i][st], bq[0][st], acc[i][0]);
+        acc[i][1] = mfma32x32x16(a[i][st], bq[1][st], acc[i][1]);
+      }
+    }
+    const float bm = block_max_rows<MT>(acc);
     if (store) mrow[kb] = bm;
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int st = 0; st < KS; ++st) a[i][st] = an[i][st];
   }
 }
 
 // ---------------------------------------------------------------- top-k
 __global__ __launch_bounds__(256) void index_topk_kernel(
-    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ group_off,
-    int H_kv, int qr, int64_t g0, int64_t g1, int BK, int topk, int32_t* __restrict__ block_ids) {
+    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
+    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
   const int lane = lane_id();
-  const int64_t slot = static_cast<int64_t>(blockIdx.x) * kWavesPerBlock + threadIdx.x / kWave;
-  if (slot >= (g1 - g0) * kWave) return;
-  const int64_t gidx = g0 + slot / kWave;
-  const int L = static_cast<int>(slot % kWave);
-  GroupRows gr = locate_group(sq, group_off, gidx, qr);
-  if (!gr.ok || L >= gr.nq * H_kv) return;
-  const int t = gr.t0 + L / H_kv;
+  const int64_t slot = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
+  const int64_t per_unit = static_cast<int64_t>(U) * kWave;
+  if (slot >= (u1 - u0) * per_unit) return;
+  const int64_t uidx = u0 + slot / per_unit;
+  const int L = static_cast<int>(slot % per_unit);     // index row inside the unit
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, U);
+  if (!ur.ok || L >= ur.nq * H_kv) return;
+  const int t = ur.t0 + L / H_kv;
   const int r = L % H_kv;
-  int32_t* out = block_ids + (static_cast<int64_t>(gr.g.q_begin + t) * H_kv + r) * topk;
-  const int p = gr.g.kv_len - gr.g.q_rows + t;
+  int32_t* out = block_ids + (static_cast<int64_t>(ur.g.q_begin + t) * H_kv + r) * topk;
+  const int p = ur.g.kv_len - ur.g.q_rows + t;
   if (p < 0) {
     if (lane < topk) out[lane] = -1;
     return;
@@ -214,10 +353,11 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
 // ---------------------------------------------------------------- host side
 struct IndexPlan {
   int qr;
-  int64_t max_groups;
-  int bcap;
+  int U;                // row groups per unit
+  int64_t max_units;    // upper bound of the units over all sequences
+  int bcap;             // M row length (key blocks, multiple of 4)
   size_t hdr_bytes;
-  size_t group_bytes;
+  size_t unit_bytes;    // M bytes per unit
 };
 
 int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, IndexPlan* pl) {
@@ -229,15 +369,30 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   if (BK != 64 && BK != 128) return MSA_ERR_UNSUPPORTED;
   if (topk > 64) return MSA_ERR_UNSUPPORTED;
   pl->qr = 64 / H_kv;
-  pl->max_groups = seqs->total_q_rows / pl->qr + seqs->num_seqs;
+  // sequences longer than two row groups take the LDS-shared kernel
+  pl->U = static_cast<int64_t>(seqs->max_q_rows) > 2 * pl->qr ? kWaves : 1;
+  const int64_t max_groups = seqs->total_q_rows / pl->qr + seqs->num_seqs;
+  pl->max_units = max_groups / pl->U + seqs->num_seqs;
   int nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
-  pl->group_bytes = static_cast<size_t>(kWave) * pl->bcap * sizeof(float);
+  pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * pl->bcap * sizeof(float);
   return MSA_OK;
 }
 
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
+
+template <int D, int B>
+void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
+                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, int nbw,
+                   float* M) {
+  if (pl.U == kWaves)
+    hipLaunchKernelGGL((index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
+                       pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+  else
+    hipLaunchKernelGGL((index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
+                       pl.qr, u0, u1, nbw, M, static_cast<int64_t>(pl.bcap));
+}
 
 }  // namespace
 
@@ -245,10 +400,10 @@ extern "C" size_t msa_index_topk_workspace_size(const msa_seqs* seqs, int num_kv
                                                 int block_size, int topk) {
   IndexPlan pl;
   if (make_plan(seqs, num_kv_heads, d_idx, block_size, topk, &pl) != MSA_OK) return 0;
-  int64_t groups = static_cast<int64_t>(kDefaultScoreBytes / pl.group_bytes);
-  if (groups < 1) groups = 1;
-  if (groups > pl.max_groups) groups = pl.max_groups;
-  return pl.hdr_bytes + static_cast<size_t>(groups) * pl.group_bytes;
+  int64_t units = static_cast<int64_t>(kDefaultScoreBytes / pl.unit_bytes);
+  if (units < 1) units = 1;
+  if (units > pl.max_units) units = pl.max_units;
+  return pl.hdr_bytes + static_cast<size_t>(units) * pl.unit_bytes;
 }
 
 extern "C" int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seqs,
@@ -260,36 +415,43 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   if (st != MSA_OK) return st;
   if (seqs->total_q_rows == 0) return MSA_OK;
   if (!index_q || !index_k || !block_ids || !workspace) return MSA_ERR_INVALID;
-  if (workspace_bytes < pl.hdr_bytes + pl.group_bytes) return MSA_ERR_WORKSPACE;
-  int64_t chunk = static_cast<int64_t>((workspace_bytes - pl.hdr_bytes) / pl.group_bytes);
-  if (chunk > pl.max_groups) chunk = pl.max_groups;
+  if (workspace_bytes < pl.hdr_bytes + pl.unit_bytes) return MSA_ERR_WORKSPACE;
+  int64_t chunk = static_cast<int64_t>((workspace_bytes - pl.hdr_bytes) / pl.unit_bytes);
+  if (chunk > pl.max_units) chunk = pl.max_units;
 
-  int32_t* group_off = static_cast<int32_t*>(workspace);
+  int32_t* unit_off = static_cast<int32_t*>(workspace);
   float* M = reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.hdr_bytes);
   const msa_seqs sq = *seqs;
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
 
-  hipLaunchKernelGGL(row_group_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, group_off);
-  const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerWave - 1) / kBlocksPerWave);
-  for (int64_t g0 = 0; g0 < pl.max_groups; g0 += chunk) {
-    const int64_t g1 = g0 + chunk < pl.max_groups ? g0 + chunk : pl.max_groups;
-    const unsigned nx = static_cast<unsigned>((g1 - g0 + kWavesPerBlock - 1) / kWavesPerBlock);
+  hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
+  // per-wave kernel: enough block slices to give ~16K waves in total
+  int nbw = kBlocksPerCta;
+  if (pl.U == 1) {
+    const int64_t target = 16384;
+    int64_t slices = (target + pl.max_units - 1) / pl.max_units;
+    nbw = static_cast<int>((pl.bcap + slices - 1) / slices);
+    if (nbw < 4) nbw = 4;
+    if (nbw > 64) nbw = 64;
+  }
+  const unsigned ny = static_cast<unsigned>((pl.bcap + nbw - 1) / nbw);
+  for (int64_t u0 = 0; u0 < pl.max_units; u0 += chunk) {
+    const int64_t u1 = u0 + chunk < pl.max_units ? u0 + chunk : pl.max_units;
+    const unsigned nx = pl.U == kWaves ? static_cast<unsigned>(u1 - u0)
+                                       : static_cast<unsigned>((u1 - u0 + kWaves - 1) / kWaves);
+    const dim3 grid(nx, ny);
     if (d_idx == 64 && block_size == 64)
-      hipLaunchKernelGGL((index_block_max_kernel<64, 64>), dim3(nx, ny), dim3(256), 0, stream, iq, ik, sq,
-                         group_off, num_kv_heads, pl.qr, g0, g1, M, static_cast<int64_t>(pl.bcap));
+      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
     else if (d_idx == 64)
-      hipLaunchKernelGGL((index_block_max_kernel<64, 128>), dim3(nx, ny), dim3(256), 0, stream, iq, ik, sq,
-                         group_off, num_kv_heads, pl.qr, g0, g1, M, static_cast<int64_t>(pl.bcap));
+      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
     else if (block_size == 64)
-      hipLaunchKernelGGL((index_block_max_kernel<128, 64>), dim3(nx, ny), dim3(256), 0, stream, iq, ik, sq,
-                         group_off, num_kv_heads, pl.qr, g0, g1, M, static_cast<int64_t>(pl.bcap));
+      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
     else
-      hipLaunchKernelGGL((index_block_max_kernel<128, 128>), dim3(nx, ny), dim3(256), 0, stream, iq, ik, sq,
-                         group_off, num_kv_heads, pl.qr, g0, g1, M, static_cast<int64_t>(pl.bcap));
-    const unsigned nt = static_cast<unsigned>((g1 - g0) * kWave / kWavesPerBlock);
+      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
+    const unsigned nt = static_cast<unsigned>((u1 - u0) * pl.U * kWave / kWaves);
     hipLaunchKernelGGL(index_topk_kernel, dim3(nt), dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), sq,
-                       group_off, num_kv_heads, pl.qr, g0, g1, block_size, topk, block_ids);
+                       unit_off, num_kv_heads, pl.qr, pl.U, u0, u1, block_size, topk, block_ids);
   }
   return msa_host::launch_status();
 }

@@ -439,7 +439,8 @@ __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
   float tot[16];
 #pragma unroll
   for (int hh = 0; hh < 16; ++hh) {
-    if (hh >= G) break;
+    tot[hh] = -INFINITY;
+    if (hh >= G) continue;
     const float x = valid ? lrow[lane * G + hh] : -INFINITY;
     float a = x;
 #pragma unroll
