@@ -202,6 +202,8 @@ template <int BK>
 struct KvoSmem {
   uint16_t k[BK][kHeadDim + 8];     // K block, row-major (+16 B pad per row)
   uint16_t vt[kHeadDim][BK + 4];    // V block transposed (+8 B pad per row)
+  uint16_t ost[4][32][64];          // per wave: one 64-dim half of 32 partial rows (bf16),
+                                    // 16-byte units XOR-swizzled by row & 7
 };
 
 // Largest i with arr[i] <= x, for arr non-decreasing with arr[0] <= x.
@@ -303,9 +305,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
       const int qi = cc + jq;
       const bool ok = lane_row && qi < nq;
       const int64_t row = row0 + (ok ? s_row[qi] : 0);
-      const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + h * (kHeadDim / 2);
+      // k-step st: lane half h supplies dims 16*st + 8h .. +8 (32 contiguous bytes per row per load)
+      const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + 8 * h;
 #pragma unroll
-      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld_bf16x8(qrow + 8 * st) : zero_bf16x8();
+      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld_bf16x8(qrow + 16 * st) : zero_bf16x8();
     };
     if (c < nq) load_q(c, bq);
     for (; c < nq; c += stride) {
@@ -320,10 +323,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
 #pragma unroll
       for (int i = 0; i < MT; ++i) {
         acc_s[i] = f32x16{};
-        const uint16_t* kr = &sm.k[32 * i + n][h * (kHeadDim / 2)];
+        const uint16_t* kr = &sm.k[32 * i + n][8 * h];
 #pragma unroll
         for (int st = 0; st < KS; ++st)
-          acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st)),
+          acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 16 * st)),
                                   bq[st], acc_s[i]);
         __builtin_amdgcn_sched_barrier(0);    // bound how far LDS operand reads are hoisted
       }
@@ -369,7 +372,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
       const float inv_l = empty ? 0.f : 1.f / l;
       // partial slot of this incidence: [row][group][slot][head][d]
       const int64_t prow = valid ? ((static_cast<int64_t>(s_row[qi]) * H_kv + r) * topk + s_slot[qi]) * G + hh : 0;
-      uint16_t* orow = o_buf + prow * kHeadDim + 4 * h;
       // two halves of d (64 dims = 2 tiles each) keep 32 accumulators live
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
@@ -390,18 +392,33 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
             acc_o[t2] = mfma32x32x16(__builtin_bit_cast(bf16x8, w), bp[u], acc_o[t2]);
           }
         }
-        if (valid) {
-          // O^T tile t: lane (n, h) holds d = 32t + 8(e/4) + 4h + e%4
+        // O^T tile t: lane (n, h) holds d = 32t + 8(e/4) + 4h + e%4 of row n.
+        // Stage the half in LDS, then each store writes 8 rows x 128 B.
 #pragma unroll
-          for (int t2 = 0; t2 < 2; ++t2)
+        for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-            for (int e4 = 0; e4 < 4; ++e4) {
-              uint2 w;
-              w.x = pack_bf16x2(acc_o[t2][4 * e4 + 0] * inv_l, acc_o[t2][4 * e4 + 1] * inv_l);
-              w.y = pack_bf16x2(acc_o[t2][4 * e4 + 2] * inv_l, acc_o[t2][4 * e4 + 3] * inv_l);
-              *reinterpret_cast<uint2*>(orow + 32 * (2 * half + t2) + 8 * e4) = w;
-            }
+          for (int e4 = 0; e4 < 4; ++e4) {
+            uint2 w;
+            w.x = pack_bf16x2(acc_o[t2][4 * e4 + 0] * inv_l, acc_o[t2][4 * e4 + 1] * inv_l);
+            w.y = pack_bf16x2(acc_o[t2][4 * e4 + 2] * inv_l, acc_o[t2][4 * e4 + 3] * inv_l);
+            *reinterpret_cast<uint2*>(&sm.ost[wave][n][(32 * t2 + 8 * e4 + 4 * h) ^ ((n & 7) << 3)]) = w;
+          }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int pass = 0; pass < 4; ++pass) {
+          const int srow = 8 * pass + (lane >> 3);        // staged row = lane column n of its pass
+          const int seg = lane & 7;                       // 16-byte segment of the 128-byte half row
+          const int sq_i = c + srow / G;
+          if (srow < qpw * G && sq_i < nq) {
+            const int64_t prow_s =
+                ((static_cast<int64_t>(s_row[sq_i]) * H_kv + r) * topk + s_slot[sq_i]) * G + (srow % G);
+            *reinterpret_cast<uint4*>(o_buf + prow_s * kHeadDim + 64 * half + 8 * seg) =
+                *reinterpret_cast<const uint4*>(&sm.ost[wave][srow][(8 * seg) ^ ((srow & 7) << 3)]);
+          }
         }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
       if (valid && h == 0) lse_buf[prow] = empty ? -INFINITY : (mm + __log2f(l)) * kLn2;
 #pragma unroll
