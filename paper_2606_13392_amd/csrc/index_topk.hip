@@ -127,8 +127,33 @@ struct IdxSmem {
   float stage[kWaves][kWave][kStageBlocks + 1];    // per wave: 64 rows x 16 block maxima
 };
 
+// Cooperative copy of one K_idx block (BK keys x D_IDX dims) through
+// registers: 256 threads x CH 16-byte pieces.
+template <int D_IDX, int BK, int CH>
+__device__ __forceinline__ void idx_load_block(const uint16_t* __restrict__ kseq, int kb, int tid,
+                                               u32x4 (&dst)[CH]) {
+  constexpr int SEGS = D_IDX / 8;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int idx = tid + 256 * c;
+    const int key = idx / SEGS, seg = idx % SEGS;
+    dst[c] = *reinterpret_cast<const u32x4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
+  }
+}
+template <int D_IDX, int BK, int CH>
+__device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_IDX + 8], int tid,
+                                                const u32x4 (&src)[CH]) {
+  constexpr int SEGS = D_IDX / 8;
+#pragma unroll
+  for (int c = 0; c < CH; ++c) {
+    const int idx = tid + 256 * c;
+    const int key = idx / SEGS, seg = idx % SEGS;
+    *reinterpret_cast<u32x4*>(&dstk[key][8 * seg]) = src[c];
+  }
+}
+
 template <int D_IDX, int BK>
-__global__ __launch_bounds__(256, 4) void index_block_max_lds_kernel(
+__global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
     int64_t ldm) {
@@ -161,22 +186,7 @@ __global__ __launch_bounds__(256, 4) void index_block_max_lds_kernel(
   float* mrow0 = M + ((uidx - u0) * (kWaves * kWave) + w * kWave) * ldm;
 
   const uint16_t* kseq = index_k + ur.g.kv_start * D_IDX;
-  auto load_block = [&](int kb, uint4 (&dst)[CH]) {
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      const int idx = threadIdx.x + 256 * c;
-      const int key = idx / SEGS, seg = idx % SEGS;
-      dst[c] = *reinterpret_cast<const uint4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
-    }
-  };
-  auto store_block = [&](int buf, const uint4 (&src)[CH]) {
-#pragma unroll
-    for (int c = 0; c < CH; ++c) {
-      const int idx = threadIdx.x + 256 * c;
-      const int key = idx / SEGS, seg = idx % SEGS;
-      *reinterpret_cast<uint4*>(&sm.k[buf][key][8 * seg]) = src[c];
-    }
-  };
+  const int tid = threadIdx.x;
   auto compute = [&](int buf, int kb) {
     if (nvalid == 0) return;
     f32x16 acc[MT][2];
@@ -213,43 +223,50 @@ __global__ __launch_bounds__(256, 4) void index_block_max_lds_kernel(
     }
   };
 
-  uint4 ra[CH], rb[CH];
-  load_block(kb0, ra);
-  if (kb0 + 1 < kb1) load_block(kb0 + 1, rb);
-  store_block(0, ra);
+  // Loads are issued unconditionally (the index is clamped to the last block)
+  // so no branch forces the compiler to wait on a prefetch it just issued.
+  u32x4 ra[CH], rb[CH];
+  const int klast = kb1 - 1;
+  idx_load_block<D_IDX, BK, CH>(kseq, kb0, tid, ra);
+  idx_load_block<D_IDX, BK, CH>(kseq, min(kb0 + 1, klast), tid, rb);
+  idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
   __syncthreads();
-  // iteration i: LDS buffer i%2 holds block kb, the other register set holds kb+1
+  // LDS buffer 0 holds block kb, register set rb holds kb+1
   for (int kb = kb0; kb < kb1; kb += 2) {
-    if (kb + 2 < kb1) load_block(kb + 2, ra);
+    idx_load_block<D_IDX, BK, CH>(kseq, min(kb + 2, klast), tid, ra);
     compute(0, kb);
-    if (kb + 1 < kb1) store_block(1, rb);
+    if (kb + 1 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[1], tid, rb);
     __syncthreads();
     if (kb + 1 >= kb1) break;
-    if (kb + 3 < kb1) load_block(kb + 3, rb);
+    idx_load_block<D_IDX, BK, CH>(kseq, min(kb + 3, klast), tid, rb);
     compute(1, kb + 1);
-    if (kb + 2 < kb1) store_block(0, ra);
+    if (kb + 2 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
     __syncthreads();
   }
 }
 
 // ---------------------------------------------------------------- scores, per wave
-// One wave: one row group (U = 1) against key blocks [kb0, kb0 + nbw).
+// One wave: one row group (U = 1) against key blocks slice, slice + nslice,
+// slice + 2 nslice, ...: the waves of a sequence sweep its index keys together,
+// so concurrently running waves read neighbouring memory.
 template <int D_IDX, int BK>
 __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
-    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, int nbw,
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, int nslice,
     float* __restrict__ M, int64_t ldm) {
   constexpr int KS = D_IDX / 16;
   constexpr int MT = BK / 32;
   const int lane = lane_id();
-  const int64_t uidx = u0 + static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
-  if (uidx >= u1) return;
+  // blockIdx.x: 4 consecutive slices of one unit; blockIdx.y: unit
+  const int64_t uidx = u0 + blockIdx.y;
+  const int slice = blockIdx.x * kWaves + threadIdx.x / kWave;
+  if (uidx >= u1 || slice >= nslice) return;
   UnitRows ur = locate_unit(sq, unit_off, uidx, qr, 1);
   if (!ur.ok) return;
   const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
   if (p_last < 0) return;
-  const int kb0 = blockIdx.y * nbw;
-  const int kb1 = min(min(kb0 + nbw, p_last / BK), static_cast<int>(ldm));
+  const int kb1 = min(p_last / BK, static_cast<int>(ldm));
+  const int kb0 = slice;
   if (kb0 >= kb1) return;
 
   const int n = lane & 31, h = lane >> 5;
@@ -270,8 +287,9 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
   };
   bf16x8 a[MT][KS], an[MT][KS];
   load_a(kb0, a);
-  for (int kb = kb0; kb < kb1; ++kb) {
-    if (kb + 1 < kb1) load_a(kb + 1, an);              // next block in flight during this one
+  for (int kb = kb0; kb < kb1; kb += nslice) {
+    // next block in flight during this one (clamped, unconditional: see above)
+    load_a(kb + nslice < kb1 ? kb + nslice : kb, an);
     f32x16 acc[MT][2];
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
@@ -320,9 +338,24 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   uint64_t list = 0;   // sorted descending across lanes; 0 marks an empty slot
   uint64_t tau = 0;    // key of the K1-th best so far (0 while fewer are known)
   if (K1 > 0) {
-    for (int c0 = 0; c0 < nscan; c0 += kWave) {
+    // block scores of the next kAhead chunks are in flight while one is ranked
+    constexpr int kAhead = 4;
+    float pf[kAhead];
+#pragma unroll
+    for (int a = 0; a < kAhead; ++a) {
+      const int b = a * kWave + lane;
+      pf[a] = b < nscan ? mrow[b] : 0.f;
+    }
+    for (int c0 = 0, ci = 0; c0 < nscan; c0 += kWave, ++ci) {
       const int b = c0 + lane;
-      const uint64_t v = b < nscan ? rank_key(mrow[b], static_cast<uint32_t>(b)) : 0ull;
+      float x = pf[0];
+#pragma unroll
+      for (int a = 0; a + 1 < kAhead; ++a) pf[a] = pf[a + 1];
+      {
+        const int bn = c0 + kAhead * kWave + lane;
+        pf[kAhead - 1] = bn < nscan ? mrow[bn] : 0.f;
+      }
+      const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
       uint64_t pass = __ballot(v > tau);
       if (pass == 0) continue;
       if (__popcll(pass) <= kSmallInsert) {
@@ -384,14 +417,14 @@ constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging 
 
 template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
-                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, int nbw,
+                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, int nslice,
                    float* M) {
   if (pl.U == kWaves)
     hipLaunchKernelGGL((index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
   else
     hipLaunchKernelGGL((index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
-                       pl.qr, u0, u1, nbw, M, static_cast<int64_t>(pl.bcap));
+                       pl.qr, u0, u1, nslice, M, static_cast<int64_t>(pl.bcap));
 }
 
 }  // namespace
@@ -426,29 +459,28 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
 
   hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
-  // per-wave kernel: enough block slices to give ~16K waves in total
-  int nbw = kBlocksPerCta;
+  // per-wave kernel: interleaved slices, ~8 blocks per wave and >= 16K waves
+  int nslice = 0;
   if (pl.U == 1) {
-    const int64_t target = 16384;
-    int64_t slices = (target + pl.max_units - 1) / pl.max_units;
-    nbw = static_cast<int>((pl.bcap + slices - 1) / slices);
-    if (nbw < 4) nbw = 4;
-    if (nbw > 64) nbw = 64;
+    int64_t sl = (pl.bcap + 7) / 8;
+    const int64_t want = (16384 + pl.max_units - 1) / pl.max_units;
+    if (sl < want) sl = want;
+    if (sl > pl.bcap) sl = pl.bcap;
+    nslice = static_cast<int>(msa_host::align_up(static_cast<size_t>(sl), kWaves));
   }
-  const unsigned ny = static_cast<unsigned>((pl.bcap + nbw - 1) / nbw);
+  const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerCta - 1) / kBlocksPerCta);
   for (int64_t u0 = 0; u0 < pl.max_units; u0 += chunk) {
     const int64_t u1 = u0 + chunk < pl.max_units ? u0 + chunk : pl.max_units;
-    const unsigned nx = pl.U == kWaves ? static_cast<unsigned>(u1 - u0)
-                                       : static_cast<unsigned>((u1 - u0 + kWaves - 1) / kWaves);
-    const dim3 grid(nx, ny);
+    const dim3 grid = pl.U == kWaves ? dim3(static_cast<unsigned>(u1 - u0), ny)
+                                     : dim3(static_cast<unsigned>(nslice / kWaves), static_cast<unsigned>(u1 - u0));
     if (d_idx == 64 && block_size == 64)
-      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
+      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
     else if (d_idx == 64)
-      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
+      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
     else if (block_size == 64)
-      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
+      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
     else
-      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nbw, M);
+      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
     const unsigned nt = static_cast<unsigned>((u1 - u0) * pl.U * kWave / kWaves);
     hipLaunchKernelGGL(index_topk_kernel, dim3(nt), dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), sq,
                        unit_off, num_kv_heads, pl.qr, pl.U, u0, u1, block_size, topk, block_ids);

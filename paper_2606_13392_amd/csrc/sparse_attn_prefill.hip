@@ -313,7 +313,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
     if (c < nq) load_q(c, bq);
     for (; c < nq; c += stride) {
       bf16x8 bq_next[KS];
-      if (c + stride < nq) load_q(c + stride, bq_next);
+      load_q(c + stride < nq ? c + stride : c, bq_next);   // unconditional: no wait on it below
       const int qi = c + jq;
       const bool valid = lane_row && qi < nq;
       const int p = valid ? s_pos[qi] : -1;
