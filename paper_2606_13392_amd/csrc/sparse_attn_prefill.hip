@@ -35,6 +35,13 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 __device__ __forceinline__ bool slot_valid(int b, int p, int BK) { return b >= 0 && p >= 0 && b <= p / BK; }
+// An incidence takes part in the reverse index, the attention and the combine
+// iff its slot is valid and the block exists in the sequence's block range
+// (always true for consistent layouts; the second test keeps every index in
+// bounds when kv_lens exceed max_kv_len).
+__device__ __forceinline__ bool incidence_ok(int b, int p, int BK, const int64_t* __restrict__ blk_base, int s) {
+  return slot_valid(b, p, BK) && static_cast<int64_t>(b) < blk_base[s + 1] - blk_base[s];
+}
 
 __device__ __forceinline__ int row_position(const msa_seqs& sq, int64_t row, int* seq_out) {
   const int s = find_seq(sq.q_offsets, sq.num_seqs, row);
@@ -79,32 +86,81 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, 
 }
 
 // ---------------------------------------------------------------- reverse index
-// One thread per (row, group) of the chunk.
+// Positions of every incidence inside its tile's handle list, with few device
+// atomics: a CTA takes kHistRows query rows of one group, histograms their
+// incidences over the key blocks of its sequences in LDS, claims one segment
+// of each touched tile with a single device atomic (the returned count is the
+// segment's start) and hands out positions inside its segments with LDS
+// atomics.  A CTA whose sequences span more than kHistBins key blocks falls
+// back to one device atomic per incidence.  Positions are relative to the
+// tile; kvo_fill adds the tile offsets once the scan has run.
+constexpr int kHistRows = 4096;
+constexpr int kHistBins = 16384;
+
 __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
                                                         const int64_t* __restrict__ blk_base, int H_kv, int BK,
                                                         int topk, int64_t nbcap, int64_t row0, int64_t nrows,
-                                                        int32_t* __restrict__ cnt) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  if (i >= nrows * H_kv) return;
-  const int64_t row = row0 + i / H_kv;
-  const int r = static_cast<int>(i % H_kv);
-  int s;
-  const int p = row_position(sq, row, &s);
-  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
-  const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
-  for (int j = 0; j < topk; ++j) {
-    const int b = ids[j];
-    if (!slot_valid(b, p, BK)) continue;
-    if (blk_base[s] + b >= nbcap) continue;
-    atomicAdd(&cnt[base + b], 1);
+                                                        int32_t* __restrict__ cnt, int32_t* __restrict__ tpos) {
+  __shared__ int32_t hist[kHistBins];
+  const int r = blockIdx.y;
+  const int64_t rb0 = row0 + static_cast<int64_t>(blockIdx.x) * kHistRows;
+  const int64_t rb1 = min(rb0 + kHistRows, row0 + nrows);
+  const int s_first = find_seq(sq.q_offsets, sq.num_seqs, rb0);
+  const int s_last = find_seq(sq.q_offsets, sq.num_seqs, rb1 - 1);
+  const int64_t g_lo = blk_base[s_first];
+  const int64_t g_hi = blk_base[s_last + 1];
+  const bool in_lds = g_hi - g_lo <= kHistBins;           // uniform over the CTA
+  const int64_t tile_base = static_cast<int64_t>(r) * nbcap;
+
+  if (in_lds) {
+    for (int i = threadIdx.x; i < kHistBins; i += 256) hist[i] = 0;
+    __syncthreads();
+  }
+  // pass 1: histogram (or, without LDS room, claim each position directly)
+  for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
+    int s;
+    const int p = row_position(sq, row, &s);
+    const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+    int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
+    const int64_t gb0 = blk_base[s];
+    for (int j = 0; j < topk; ++j) {
+      const int b = ids[j];
+      if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+      if (in_lds) atomicAdd(&hist[gb0 + b - g_lo], 1);
+      else tp[j] = atomicAdd(&cnt[tile_base + gb0 + b], 1);
+    }
+  }
+  if (!in_lds) return;
+  __syncthreads();
+  // claim one segment per touched tile; hist becomes the segment cursor
+  const int nbin = static_cast<int>(g_hi - g_lo);
+  for (int i = threadIdx.x; i < nbin; i += 256) {
+    const int c = hist[i];
+    if (c > 0) hist[i] = atomicAdd(&cnt[tile_base + g_lo + i], c);
+  }
+  __syncthreads();
+  // pass 2: positions inside the claimed segments
+  for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
+    int s;
+    const int p = row_position(sq, row, &s);
+    const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+    int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
+    const int64_t gb0 = blk_base[s];
+    for (int j = 0; j < topk; ++j) {
+      const int b = ids[j];
+      if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+      tp[j] = atomicAdd(&hist[gb0 + b - g_lo], 1);
+    }
   }
 }
 
+// One thread per (row, group) of the chunk: handle = (row in chunk << 6 | slot).
 __global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
                                                        const int64_t* __restrict__ blk_base, int H_kv, int BK,
                                                        int topk, int64_t nbcap, int64_t row0, int64_t nrows,
                                                        const int32_t* __restrict__ tile_off,
-                                                       int32_t* __restrict__ cursor, uint32_t* __restrict__ handles) {
+                                                       const int32_t* __restrict__ tpos,
+                                                       uint32_t* __restrict__ handles) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= nrows * H_kv) return;
   const int64_t rl = i / H_kv;
@@ -113,14 +169,12 @@ __global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict
   int s;
   const int p = row_position(sq, row, &s);
   const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const int32_t* tp = tpos + i * topk;
   const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
   for (int j = 0; j < topk; ++j) {
     const int b = ids[j];
-    if (!slot_valid(b, p, BK)) continue;
-    if (blk_base[s] + b >= nbcap) continue;
-    const int64_t tile = base + b;
-    const int pos = atomicSub(&cursor[tile], 1) - 1;     // cursor starts at the tile's count
-    handles[tile_off[tile] + pos] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(j);
+    if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+    handles[tile_off[base + b] + tp[j]] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(j);
   }
 }
 
@@ -434,9 +488,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
 constexpr int kCombineWaves = 4;
 
 __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
-    const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int BK, int topk, int64_t row0,
-    int64_t nrows, const uint16_t* __restrict__ o_buf, const float* __restrict__ lse_buf, uint16_t* __restrict__ o,
-    float* __restrict__ lse) {
+    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_q, int H_kv,
+    int BK, int topk, int64_t row0, int64_t nrows, const uint16_t* __restrict__ o_buf,
+    const float* __restrict__ lse_buf, uint16_t* __restrict__ o, float* __restrict__ lse) {
   __shared__ float s_w[kCombineWaves][64][17];        // weight of slot j for head hh (G <= 16)
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
@@ -450,7 +504,7 @@ __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
   int s;
   const int p = row_position(sq, row, &s);
   const int32_t* ids = block_ids + (row * H_kv + r) * topk;
-  const bool valid = lane < topk && slot_valid(ids[lane], p, BK);
+  const bool valid = lane < topk && incidence_ok(ids[lane], p, BK, blk_base, s);
   const float* lrow = lse_buf + (rl * H_kv + r) * static_cast<int64_t>(topk) * G;
   // per head: max and sum over the valid slots (lane j = slot j)
   float tot[16];
@@ -530,7 +584,8 @@ struct KvoPlan {
   int64_t chunk_rows;   // query rows per chunk
   int nscan;            // scan blocks
   // workspace offsets
-  size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_handles, off_obuf, off_lse, total;
+  size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_handles, off_tpos, off_obuf, off_lse,
+      total;
 };
 
 size_t fixed_bytes(KvoPlan& pl, const msa_seqs* seqs) {
@@ -545,13 +600,14 @@ size_t fixed_bytes(KvoPlan& pl, const msa_seqs* seqs) {
 }
 
 size_t per_row_bytes(int H_q, int H_kv, int topk) {
-  return sizeof(uint32_t) * H_kv * topk + static_cast<size_t>(topk) * H_q * (kHeadDim * 2 + sizeof(float));
+  return 2 * sizeof(uint32_t) * H_kv * topk + static_cast<size_t>(topk) * H_q * (kHeadDim * 2 + sizeof(float));
 }
 
 void layout_rows(KvoPlan& pl, size_t fixed, int H_q, int H_kv, int topk) {
   using msa_host::align_up;
   size_t o = fixed;
   pl.off_handles = o; o = align_up(o + sizeof(uint32_t) * pl.chunk_rows * H_kv * topk, 256);
+  pl.off_tpos = o;    o = align_up(o + sizeof(int32_t) * pl.chunk_rows * H_kv * topk, 256);
   pl.off_obuf = o;    o = align_up(o + sizeof(uint16_t) * static_cast<size_t>(topk) * pl.chunk_rows * H_q * kHeadDim, 256);
   pl.off_lse = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(topk) * pl.chunk_rows * H_q, 256);
   pl.total = o;
@@ -574,7 +630,7 @@ int make_kvo_plan(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk, siz
   if (pl->total <= budget) {
     // everything in one chunk
   } else if (budget > fixed) {
-    const int64_t fit = static_cast<int64_t>((budget - fixed - 3 * 256) / prb);
+    const int64_t fit = static_cast<int64_t>((budget - fixed - 4 * 256) / prb);
     if (fit < rows) rows = fit;
   } else {
     rows = 0;
@@ -631,6 +687,7 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
   auto* item_off = reinterpret_cast<int32_t*>(ws + pl.off_item_off);
   auto* blk_tot = reinterpret_cast<int32_t*>(ws + pl.off_blk_tot);
   auto* handles = reinterpret_cast<uint32_t*>(ws + pl.off_handles);
+  auto* tpos = reinterpret_cast<int32_t*>(ws + pl.off_tpos);
   auto* o_buf = reinterpret_cast<uint16_t*>(ws + pl.off_obuf);
   auto* lse_buf = reinterpret_cast<float*>(ws + pl.off_lse);
   const msa_seqs sq = *seqs;
@@ -646,8 +703,9 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
     const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
     hipLaunchKernelGGL(fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, pl.ntile, 0);
-    hipLaunchKernelGGL(kvo_count_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
-                       topk, pl.nbcap, r0, nr, cnt);
+    const dim3 hgrid(static_cast<unsigned>((nr + kHistRows - 1) / kHistRows), static_cast<unsigned>(H_kv));
+    hipLaunchKernelGGL(kvo_count_kernel, hgrid, dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK, topk,
+                       pl.nbcap, r0, nr, cnt, tpos);
     hipLaunchKernelGGL(kvo_scan_block_kernel, dim3(pl.nscan), dim3(256), 0, stream, cnt, pl.ntile, tile_off,
                        item_off, blk_tot);
     hipLaunchKernelGGL(kvo_scan_top_kernel, dim3(1), dim3(1024), 0, stream, blk_tot, pl.nscan, tile_off, item_off,
@@ -655,7 +713,7 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
     hipLaunchKernelGGL(kvo_scan_add_kernel, dim3(static_cast<unsigned>((pl.ntile + 255) / 256)), dim3(256), 0,
                        stream, blk_tot, pl.ntile, tile_off, item_off);
     hipLaunchKernelGGL(kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
-                       topk, pl.nbcap, r0, nr, tile_off, cnt, handles);
+                       topk, pl.nbcap, r0, nr, tile_off, tpos, handles);
     static int ctas64 = 0, ctas128 = 0;
     if (BK == 64)
       hipLaunchKernelGGL(kvo_attn_kernel<64>, dim3(persistent_ctas(kvo_attn_kernel<64>, kAttnThreads, &ctas64)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
@@ -667,8 +725,8 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
                          lse_buf);
     const int64_t pairs = nr * H_kv;
     hipLaunchKernelGGL(kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
-                       dim3(64 * kCombineWaves), 0, stream, block_ids, sq, H_q, H_kv, BK, topk, r0, nr, o_buf,
-                       lse_buf, op, lse);
+                       dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,
+                       o_buf, lse_buf, op, lse);
   }
   return msa_host::launch_status();
 }

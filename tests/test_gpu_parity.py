@@ -49,6 +49,8 @@ SMALL = [
     ("bk128_didx64_g1", [520], [520], 8, 8, 64, 128, 4, None, 0),
     ("many_blocks_k32", [5000], [5000], 16, 2, 64, 64, 32, None, 0),
     ("planted_k16", [4096], [4096], 16, 8, 64, 64, 16, None, 6),
+    # one reverse-index CTA covers 3 x 6250 key blocks: more than its LDS histogram holds
+    ("wide_block_range", [100, 100, 100], [400000, 400000, 400000], 4, 1, 64, 64, 8, None, 0),
 ]
 
 
