@@ -246,27 +246,29 @@ __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
 }
 
 // ---------------------------------------------------------------- scores, per wave
-// One wave: one row group (U = 1) against key blocks slice, slice + nslice,
-// slice + 2 nslice, ...: the waves of a sequence sweep its index keys together,
-// so concurrently running waves read neighbouring memory.
+// One wave: one row group (U = 1) against kSliceBlocks consecutive key blocks;
+// the 4 waves of a CTA take 4 consecutive slices of one unit, so a CTA streams
+// 4 x kSliceBlocks contiguous blocks.  Each row's block maxima are kept in
+// registers and written as two 16-byte stores.
+constexpr int kSliceBlocks = 8;
+
 template <int D_IDX, int BK>
 __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
-    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, int nslice,
-    float* __restrict__ M, int64_t ldm) {
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
+    int64_t ldm) {
   constexpr int KS = D_IDX / 16;
   constexpr int MT = BK / 32;
   const int lane = lane_id();
-  // blockIdx.x: 4 consecutive slices of one unit; blockIdx.y: unit
   const int64_t uidx = u0 + blockIdx.y;
   const int slice = blockIdx.x * kWaves + threadIdx.x / kWave;
-  if (uidx >= u1 || slice >= nslice) return;
+  if (uidx >= u1) return;
   UnitRows ur = locate_unit(sq, unit_off, uidx, qr, 1);
   if (!ur.ok) return;
   const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
   if (p_last < 0) return;
   const int kb1 = min(p_last / BK, static_cast<int>(ldm));
-  const int kb0 = slice;
+  const int kb0 = slice * kSliceBlocks;
   if (kb0 >= kb1) return;
 
   const int n = lane & 31, h = lane >> 5;
@@ -274,8 +276,6 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
   bf16x8 bq[2][KS];
   load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv) * D_IDX, nvalid, n, h, bq);
   const uint16_t* kbase = index_k + ur.g.kv_start * D_IDX + h * (D_IDX / 2);
-  float* mrow = M + ((uidx - u0) * kWave + lane) * ldm;
-  const bool store = lane < nvalid;
 
   auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
 #pragma unroll
@@ -286,101 +286,183 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
     }
   };
   bf16x8 a[MT][KS], an[MT][KS];
+  float mb[kSliceBlocks];
   load_a(kb0, a);
-  for (int kb = kb0; kb < kb1; kb += nslice) {
-    // next block in flight during this one (clamped, unconditional: see above)
-    load_a(kb + nslice < kb1 ? kb + nslice : kb, an);
-    f32x16 acc[MT][2];
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      acc[i][0] = f32x16{};
-      acc[i][1] = f32x16{};
+  for (int i = 0; i < kSliceBlocks; ++i) {
+    const int kb = kb0 + i;
+    mb[i] = 0.f;
+    if (kb < kb1) {                                   // uniform
+      // next block in flight during this one (clamped, unconditional load)
+      load_a(kb + 1 < kb1 ? kb + 1 : kb, an);
+      f32x16 acc[MT][2];
 #pragma unroll
-      for (int st = 0; st < KS; ++st) {
-        acc[i][0] = mfma32x32x16(a[i][st], bq[0][st], acc[i][0]);
-        acc[i][1] = mfma32x32x16(a[i][st], bq[1][st], acc[i][1]);
+      for (int t = 0; t < MT; ++t) {
+        acc[t][0] = f32x16{};
+        acc[t][1] = f32x16{};
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          acc[t][0] = mfma32x32x16(a[t][st], bq[0][st], acc[t][0]);
+          acc[t][1] = mfma32x32x16(a[t][st], bq[1][st], acc[t][1]);
+        }
       }
+      mb[i] = block_max_rows<MT>(acc);
+#pragma unroll
+      for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int st = 0; st < KS; ++st) a[t][st] = an[t][st];
     }
-    const float bm = block_max_rows<MT>(acc);
-    if (store) mrow[kb] = bm;
+  }
+  // values past kb1 are never read (they are >= every row's local block) and
+  // stay inside this slice; quads start below ldm (a multiple of 4)
+  if (lane < nvalid) {
+    float* mrow = M + ((uidx - u0) * kWave + lane) * ldm + kb0;
 #pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int st = 0; st < KS; ++st) a[i][st] = an[i][st];
+    for (int q4 = 0; q4 < kSliceBlocks / 4; ++q4)
+      if (kb0 + 4 * q4 < ldm)
+        *reinterpret_cast<float4*>(mrow + 4 * q4) = make_float4(mb[4 * q4], mb[4 * q4 + 1], mb[4 * q4 + 2], mb[4 * q4 + 3]);
   }
 }
 
 // ---------------------------------------------------------------- top-k
-__global__ __launch_bounds__(256) void index_topk_kernel(
-    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
-    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+// Streams chunks c_begin, c_begin + c_step, ... (64 blocks each) of one row's
+// block scores; returns the row's best keys of those chunks, sorted
+// descending across the lanes (at least the best K1 are exact).
+__device__ __forceinline__ uint64_t scan_row_chunks(const float* __restrict__ mrow, int nscan, int K1, int c_begin,
+                                                    int c_step) {
   const int lane = lane_id();
-  const int64_t slot = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
-  const int64_t per_unit = static_cast<int64_t>(U) * kWave;
-  if (slot >= (u1 - u0) * per_unit) return;
-  const int64_t uidx = u0 + slot / per_unit;
-  const int L = static_cast<int>(slot % per_unit);     // index row inside the unit
-  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, U);
-  if (!ur.ok || L >= ur.nq * H_kv) return;
-  const int t = ur.t0 + L / H_kv;
-  const int r = L % H_kv;
-  int32_t* out = block_ids + (static_cast<int64_t>(ur.g.q_begin + t) * H_kv + r) * topk;
-  const int p = ur.g.kv_len - ur.g.q_rows + t;
-  if (p < 0) {
-    if (lane < topk) out[lane] = -1;
-    return;
-  }
-  const int lb = p / BK;
-  const int nscan = min(lb, static_cast<int>(ldm));   // == lb whenever kv_lens respect max_kv_len
-  const int K1 = topk - 1;
-  const float* mrow = M + slot * ldm;
-
   uint64_t list = 0;   // sorted descending across lanes; 0 marks an empty slot
   uint64_t tau = 0;    // key of the K1-th best so far (0 while fewer are known)
-  if (K1 > 0) {
-    // block scores of the next kAhead chunks are in flight while one is ranked
-    constexpr int kAhead = 4;
-    float pf[kAhead];
+  if (K1 <= 0) return list;
+  // block scores of the next kAhead chunks are in flight while one is ranked
+  constexpr int kAhead = 4;
+  float pf[kAhead];
 #pragma unroll
-    for (int a = 0; a < kAhead; ++a) {
-      const int b = a * kWave + lane;
-      pf[a] = b < nscan ? mrow[b] : 0.f;
-    }
-    for (int c0 = 0, ci = 0; c0 < nscan; c0 += kWave, ++ci) {
-      const int b = c0 + lane;
-      float x = pf[0];
-#pragma unroll
-      for (int a = 0; a + 1 < kAhead; ++a) pf[a] = pf[a + 1];
-      {
-        const int bn = c0 + kAhead * kWave + lane;
-        pf[kAhead - 1] = bn < nscan ? mrow[bn] : 0.f;
-      }
-      const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
-      uint64_t pass = __ballot(v > tau);
-      if (pass == 0) continue;
-      if (__popcll(pass) <= kSmallInsert) {
-        while (pass) {
-          const int src = __ffsll(static_cast<unsigned long long>(pass)) - 1;
-          pass &= pass - 1;
-          const uint64_t x = readlane_u64(v, src);
-          const int rnk = __popcll(__ballot(list > x));
-          const uint64_t prev = shfl_u64(list, lane - 1);
-          list = lane < rnk ? list : (lane == rnk ? x : prev);
-        }
-      } else {
-        const uint64_t vs = wave_sort_desc_u64(v);
-        const uint64_t rev = shfl_u64(vs, kWave - 1 - lane);
-        list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
-      }
-      tau = readlane_u64(list, K1 - 1);
-    }
+  for (int a = 0; a < kAhead; ++a) {
+    const int b = (c_begin + a * c_step) * kWave + lane;
+    pf[a] = b < nscan ? mrow[b] : 0.f;
   }
+  for (int c = c_begin; c * kWave < nscan; c += c_step) {
+    const int b = c * kWave + lane;
+    const float x = pf[0];
+#pragma unroll
+    for (int a = 0; a + 1 < kAhead; ++a) pf[a] = pf[a + 1];
+    {
+      const int bn = (c + kAhead * c_step) * kWave + lane;
+      pf[kAhead - 1] = bn < nscan ? mrow[bn] : 0.f;
+    }
+    const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
+    uint64_t pass = __ballot(v > tau);
+    if (pass == 0) continue;
+    if (__popcll(pass) <= kSmallInsert) {
+      while (pass) {
+        const int src = __ffsll(static_cast<unsigned long long>(pass)) - 1;
+        pass &= pass - 1;
+        const uint64_t xk = readlane_u64(v, src);
+        const int rnk = __popcll(__ballot(list > xk));
+        const uint64_t prev = lane_shr1_u64(list, list);
+        list = lane < rnk ? list : (lane == rnk ? xk : prev);
+      }
+    } else {
+      const uint64_t vs = wave_sort_desc_u64(v);
+      const uint64_t rev = shfl_u64(vs, kWave - 1 - lane);
+      list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+    }
+    tau = readlane_u64(list, K1 - 1);
+  }
+  return list;
+}
+
+// Local block + the K1 best keys of `list`, ids ascending, -1 padded.
+__device__ __forceinline__ void finish_row(uint64_t list, int K1, int lb, int topk, int32_t* __restrict__ out) {
+  const int lane = lane_id();
   const int cnt = K1 > 0 ? __popcll(__ballot(lane < K1 && list != 0ull)) : 0;
   uint32_t id = 0xFFFFFFFFu;
   if (lane < cnt) id = key_block(list);
   else if (lane == cnt) id = static_cast<uint32_t>(lb);
   id = wave_sort_asc_u32(id);
   if (lane < topk) out[lane] = lane <= cnt ? static_cast<int32_t>(id) : -1;
+}
+
+struct RowTask {
+  bool ok;
+  int lb, nscan;
+  int32_t* out;
+  const float* mrow;
+  bool no_position;
+};
+
+__device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64_t ldm, const msa_seqs& sq,
+                                              const int32_t* __restrict__ unit_off, int H_kv, int qr, int U,
+                                              int64_t u0, int64_t slot, int BK, int topk,
+                                              int32_t* __restrict__ block_ids) {
+  RowTask t;
+  t.ok = false;
+  t.no_position = false;
+  const int64_t per_unit = static_cast<int64_t>(U) * kWave;
+  const int64_t uidx = u0 + slot / per_unit;
+  const int L = static_cast<int>(slot % per_unit);     // index row inside the unit
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, U);
+  if (!ur.ok || L >= ur.nq * H_kv) return t;
+  const int row = ur.t0 + L / H_kv;
+  const int r = L % H_kv;
+  t.out = block_ids + (static_cast<int64_t>(ur.g.q_begin + row) * H_kv + r) * topk;
+  const int p = ur.g.kv_len - ur.g.q_rows + row;
+  t.ok = true;
+  if (p < 0) {
+    t.no_position = true;
+    return t;
+  }
+  t.lb = p / BK;
+  t.nscan = min(t.lb, static_cast<int>(ldm));      // == lb whenever kv_lens respect max_kv_len
+  t.mrow = M + slot * ldm;
+  return t;
+}
+
+// One wave per index row.
+__global__ __launch_bounds__(256) void index_topk_kernel(
+    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
+    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+  const int lane = lane_id();
+  const int64_t slot = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
+  if (slot >= (u1 - u0) * U * kWave) return;
+  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, u0, slot, BK, topk, block_ids);
+  if (!t.ok) return;
+  if (t.no_position) {
+    if (lane < topk) t.out[lane] = -1;
+    return;
+  }
+  const uint64_t list = scan_row_chunks(t.mrow, t.nscan, topk - 1, 0, 1);
+  finish_row(list, topk - 1, t.lb, topk, t.out);
+}
+
+// Four waves per index row (for few rows): wave w scans chunks w, w+4, ...;
+// the partial lists are merged through LDS.
+__global__ __launch_bounds__(256) void index_topk_split_kernel(
+    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
+    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+  __shared__ uint64_t lists[kWaves][kWave];
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int64_t slot = blockIdx.x;
+  if (slot >= (u1 - u0) * U * kWave) return;        // uniform over the CTA
+  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, u0, slot, BK, topk, block_ids);
+  if (!t.ok) return;
+  if (t.no_position) {
+    if (w == 0 && lane < topk) t.out[lane] = -1;
+    return;
+  }
+  const int K1 = topk - 1;
+  lists[w][lane] = scan_row_chunks(t.mrow, t.nscan, K1, w, kWaves);
+  __syncthreads();
+  if (w != 0) return;
+  uint64_t list = lists[0][lane];
+#pragma unroll
+  for (int ww = 1; ww < kWaves; ++ww) {
+    const uint64_t rev = lists[ww][kWave - 1 - lane];   // ascending: bitonic with `list`
+    list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+  }
+  finish_row(list, K1, t.lb, topk, t.out);
 }
 
 // ---------------------------------------------------------------- host side
@@ -414,17 +496,17 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
 }
 
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
+constexpr int64_t kSplitTopkRows = 16384;                // fewer index rows: 4 waves per row
 
 template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
-                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, int nslice,
-                   float* M) {
+                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M) {
   if (pl.U == kWaves)
     hipLaunchKernelGGL((index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
   else
     hipLaunchKernelGGL((index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
-                       pl.qr, u0, u1, nslice, M, static_cast<int64_t>(pl.bcap));
+                       pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
 }
 
 }  // namespace
@@ -459,31 +541,31 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
 
   hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
-  // per-wave kernel: interleaved slices, ~8 blocks per wave and >= 16K waves
-  int nslice = 0;
-  if (pl.U == 1) {
-    int64_t sl = (pl.bcap + 7) / 8;
-    const int64_t want = (16384 + pl.max_units - 1) / pl.max_units;
-    if (sl < want) sl = want;
-    if (sl > pl.bcap) sl = pl.bcap;
-    nslice = static_cast<int>(msa_host::align_up(static_cast<size_t>(sl), kWaves));
-  }
+  // per-wave kernel: slices of kSliceBlocks consecutive blocks, 4 per CTA
+  const int nslice = (pl.bcap + kSliceBlocks - 1) / kSliceBlocks;
   const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerCta - 1) / kBlocksPerCta);
   for (int64_t u0 = 0; u0 < pl.max_units; u0 += chunk) {
     const int64_t u1 = u0 + chunk < pl.max_units ? u0 + chunk : pl.max_units;
     const dim3 grid = pl.U == kWaves ? dim3(static_cast<unsigned>(u1 - u0), ny)
-                                     : dim3(static_cast<unsigned>(nslice / kWaves), static_cast<unsigned>(u1 - u0));
+                                     : dim3(static_cast<unsigned>((nslice + kWaves - 1) / kWaves),
+                                            static_cast<unsigned>(u1 - u0));
     if (d_idx == 64 && block_size == 64)
-      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
+      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
     else if (d_idx == 64)
-      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
+      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
     else if (block_size == 64)
-      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
+      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
     else
-      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, nslice, M);
-    const unsigned nt = static_cast<unsigned>((u1 - u0) * pl.U * kWave / kWaves);
-    hipLaunchKernelGGL(index_topk_kernel, dim3(nt), dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), sq,
-                       unit_off, num_kv_heads, pl.qr, pl.U, u0, u1, block_size, topk, block_ids);
+      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
+    const int64_t rows = (u1 - u0) * pl.U * kWave;
+    if (rows <= kSplitTopkRows)
+      hipLaunchKernelGGL(index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, M,
+                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, u0, u1,
+                         block_size, topk, block_ids);
+    else
+      hipLaunchKernelGGL(index_topk_kernel, dim3(static_cast<unsigned>(rows / kWaves)), dim3(256), 0, stream, M,
+                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, u0, u1,
+                         block_size, topk, block_ids);
   }
   return msa_host::launch_status();
 }

@@ -78,33 +78,69 @@ __device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// Value of lane (lane ^ J): DPP quad permutes for J = 1, 2, ds_swizzle
+// (bit-mask mode, within 32 lanes) for J = 4, 8, 16, permlane32 swap for 32.
+template <int J>
+__device__ __forceinline__ uint32_t xor_lane_u32(uint32_t v) {
+  if constexpr (J == 1) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0xB1, 0xF, 0xF, false));
+  } else if constexpr (J == 2) {
+    return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(v), 0x4E, 0xF, 0xF, false));
+  } else if constexpr (J < 32) {
+    return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(v), 0x1F | (J << 10)));
+  } else {
+    auto sw = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return __lane_id() < 32 ? sw[1] : sw[0];
+  }
+}
+template <int J>
+__device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v) {
+  const uint32_t lo = xor_lane_u32<J>(static_cast<uint32_t>(v));
+  const uint32_t hi = xor_lane_u32<J>(static_cast<uint32_t>(v >> 32));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+// Value of lane - 1 (lane 0 receives `fill`): DPP wave shift right by one.
+__device__ __forceinline__ uint64_t lane_shr1_u64(uint64_t v, uint64_t fill) {
+  const int lo = __builtin_amdgcn_update_dpp(static_cast<int>(static_cast<uint32_t>(fill)),
+                                             static_cast<int>(static_cast<uint32_t>(v)), 0x138, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(static_cast<int>(static_cast<uint32_t>(fill >> 32)),
+                                             static_cast<int>(static_cast<uint32_t>(v >> 32)), 0x138, 0xF, 0xF, false);
+  return (static_cast<uint64_t>(static_cast<uint32_t>(hi)) << 32) | static_cast<uint32_t>(lo);
+}
+
+// One compare-exchange step of a bitonic network: lanes with (lane & J) == 0
+// keep the max when `desc` else the min; their partners the other one.
+template <int J>
+__device__ __forceinline__ uint64_t bitonic_step_u64(uint64_t v, bool desc) {
+  const uint64_t o = xor_lane_u64<J>(v);
+  const bool lower = (__lane_id() & J) == 0;
+  return (desc == lower) ? (v > o ? v : o) : (v < o ? v : o);
+}
+template <int K, int J>
+__device__ __forceinline__ uint64_t bitonic_stage_desc_u64(uint64_t v) {
+  if constexpr (J == 0) {
+    return v;
+  } else {
+    v = bitonic_step_u64<J>(v, (__lane_id() & K) == 0);
+    return bitonic_stage_desc_u64<K, J / 2>(v);
+  }
+}
+template <int K>
+__device__ __forceinline__ uint64_t bitonic_sort_desc_u64(uint64_t v) {
+  if constexpr (K > kWave) {
+    return v;
+  } else {
+    v = bitonic_stage_desc_u64<K, K / 2>(v);
+    return bitonic_sort_desc_u64<K * 2>(v);
+  }
+}
 // Bitonic sort of one 64-bit key per lane across the wave, descending
 // (lane 0 receives the largest key).
-__device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int k = 2; k <= kWave; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      uint64_t o = shfl_xor_u64(v, j);
-      bool desc_block = (lane & k) == 0;
-      bool lower = (lane & j) == 0;
-      bool take_max = (desc_block == lower);
-      v = take_max ? (v > o ? v : o) : (v < o ? v : o);
-    }
-  }
-  return v;
-}
+__device__ __forceinline__ uint64_t wave_sort_desc_u64(uint64_t v) { return bitonic_sort_desc_u64<2>(v); }
 // Sorts a bitonic sequence (one key per lane) descending.
 __device__ __forceinline__ uint64_t wave_bitonic_merge_desc_u64(uint64_t v) {
-  const int lane = lane_id();
-#pragma unroll
-  for (int j = kWave >> 1; j > 0; j >>= 1) {
-    uint64_t o = shfl_xor_u64(v, j);
-    bool lower = (lane & j) == 0;
-    v = lower ? (v > o ? v : o) : (v < o ? v : o);
-  }
-  return v;
+  // K = 128 > every lane index: all lanes sort descending
+  return bitonic_stage_desc_u64<128, kWave / 2>(v);
 }
 // Bitonic sort of one uint32 per lane, ascending.
 __device__ __forceinline__ uint32_t wave_sort_asc_u32(uint32_t v) {

@@ -538,22 +538,37 @@ __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
   for (int e = 0; e < 32; ++e) acc[e] = 0.f;
   const uint16_t* obase = o_buf + ((rl * H_kv + r) * static_cast<int64_t>(topk)) * G * kHeadDim +
                           static_cast<int64_t>(hh) * kHeadDim + dd;
-  const uint64_t vmask = __ballot(valid);
-  for (int j = 0; j < topk && lane_on; ++j) {
-    if (!((vmask >> j) & 1ull)) continue;
-    const float w = s_w[wave][j][hh];
-    const uint16_t* src = obase + static_cast<int64_t>(j) * G * kHeadDim;
+  // valid slots, 4 at a time: their partial loads are in flight together
+  uint64_t vmask = __ballot(valid);
+  while (vmask != 0ull && lane_on) {
+    int js[4];
 #pragma unroll
-    for (int e8 = 0; e8 < 4; ++e8) {
-      if (8 * e8 >= per) break;
-      const uint4 x = *reinterpret_cast<const uint4*>(src + 8 * e8);
-      const uint32_t xs[4] = {x.x, x.y, x.z, x.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[8 * e8 + 2 * e] += w * __uint_as_float(xs[e] << 16);
-        acc[8 * e8 + 2 * e + 1] += w * __uint_as_float(xs[e] & 0xFFFF0000u);
-      }
+    for (int u = 0; u < 4; ++u) {
+      js[u] = vmask != 0ull ? __ffsll(static_cast<unsigned long long>(vmask)) - 1 : -1;
+      vmask &= vmask - 1;
     }
+    u32x4 x[4][4];
+    float w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int j = js[u] >= 0 ? js[u] : js[0];
+      w[u] = js[u] >= 0 ? s_w[wave][j][hh] : 0.f;
+      const uint16_t* src = obase + static_cast<int64_t>(j) * G * kHeadDim;
+#pragma unroll
+      for (int e8 = 0; e8 < 4; ++e8)
+        if (8 * e8 < per) x[u][e8] = *reinterpret_cast<const u32x4*>(src + 8 * e8);
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int e8 = 0; e8 < 4; ++e8) {
+        if (8 * e8 >= per) break;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[8 * e8 + 2 * e] += w[u] * __uint_as_float(x[u][e8][e] << 16);
+          acc[8 * e8 + 2 * e + 1] += w[u] * __uint_as_float(x[u][e8][e] & 0xFFFF0000u);
+        }
+      }
   }
   if (!active || !lane_on) return;
   const int head = r * G + hh;
