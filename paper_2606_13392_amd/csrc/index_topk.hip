@@ -22,6 +22,8 @@
 //   index_topk            one wave per index row streams M[row][0..lb) 64
 //                         blocks at a time, filters against the current k-1-th
 //                         best key and keeps a sorted list (one key per lane).
+#include <algorithm>
+
 #include "msa_common.h"
 
 namespace {
@@ -392,16 +394,18 @@ struct RowTask {
   bool no_position;
 };
 
+// Task `task` of a chunk: index row L = task % rpu of unit u0 + task / rpu,
+// where rpu (<= U * 64) bounds the index rows a unit can hold.
 __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64_t ldm, const msa_seqs& sq,
                                               const int32_t* __restrict__ unit_off, int H_kv, int qr, int U,
-                                              int64_t u0, int64_t slot, int BK, int topk,
+                                              int rpu, int64_t u0, int64_t task, int BK, int topk,
                                               int32_t* __restrict__ block_ids) {
   RowTask t;
   t.ok = false;
   t.no_position = false;
-  const int64_t per_unit = static_cast<int64_t>(U) * kWave;
-  const int64_t uidx = u0 + slot / per_unit;
-  const int L = static_cast<int>(slot % per_unit);     // index row inside the unit
+  const int64_t uidx = u0 + task / rpu;
+  const int L = static_cast<int>(task % rpu);          // index row inside the unit
+  const int64_t slot = (uidx - u0) * (static_cast<int64_t>(U) * kWave) + L;
   UnitRows ur = locate_unit(sq, unit_off, uidx, qr, U);
   if (!ur.ok || L >= ur.nq * H_kv) return t;
   const int row = ur.t0 + L / H_kv;
@@ -422,11 +426,11 @@ __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64
 // One wave per index row.
 __global__ __launch_bounds__(256) void index_topk_kernel(
     const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
-    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+    int qr, int U, int rpu, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
   const int lane = lane_id();
-  const int64_t slot = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
-  if (slot >= (u1 - u0) * U * kWave) return;
-  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, u0, slot, BK, topk, block_ids);
+  const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
+  if (task >= (u1 - u0) * rpu) return;
+  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, rpu, u0, task, BK, topk, block_ids);
   if (!t.ok) return;
   if (t.no_position) {
     if (lane < topk) t.out[lane] = -1;
@@ -440,13 +444,13 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
 // the partial lists are merged through LDS.
 __global__ __launch_bounds__(256) void index_topk_split_kernel(
     const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
-    int qr, int U, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+    int qr, int U, int rpu, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
   __shared__ uint64_t lists[kWaves][kWave];
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
-  const int64_t slot = blockIdx.x;
-  if (slot >= (u1 - u0) * U * kWave) return;        // uniform over the CTA
-  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, u0, slot, BK, topk, block_ids);
+  const int64_t task = blockIdx.x;
+  if (task >= (u1 - u0) * rpu) return;              // uniform over the CTA
+  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, rpu, u0, task, BK, topk, block_ids);
   if (!t.ok) return;
   if (t.no_position) {
     if (w == 0 && lane < topk) t.out[lane] = -1;
@@ -557,15 +561,18 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
       launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
     else
       launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
-    const int64_t rows = (u1 - u0) * pl.U * kWave;
+    // index rows a unit can hold: its query rows (<= U * qr, <= max_q_rows) x H_kv
+    const int rpu = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(pl.U) * pl.qr, seqs->max_q_rows)) *
+                    num_kv_heads;
+    const int64_t rows = (u1 - u0) * rpu;
     if (rows <= kSplitTopkRows)
       hipLaunchKernelGGL(index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, M,
-                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, u0, u1,
+                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
                          block_size, topk, block_ids);
     else
-      hipLaunchKernelGGL(index_topk_kernel, dim3(static_cast<unsigned>(rows / kWaves)), dim3(256), 0, stream, M,
-                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, u0, u1,
-                         block_size, topk, block_ids);
+      hipLaunchKernelGGL(index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)), dim3(256), 0,
+                         stream, M, static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0,
+                         u1, block_size, topk, block_ids);
   }
   return msa_host::launch_status();
 }

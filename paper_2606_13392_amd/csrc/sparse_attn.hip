@@ -26,33 +26,39 @@ struct AttnSmem {
   uint16_t vt[kHeadDim][BK + 4];
 };
 
-// Stage V[b*BK .. b*BK+BK) of group r into LDS as vt[d][key] (keys past the
-// sequence's end read as zero).
+// V[b*BK .. b*BK+BK) of group r: each lane loads 4 keys x 8 dims per
+// (4-key group, 8-dim group) pair; keys past the sequence's end read as zero.
 template <int BK>
-__device__ __forceinline__ void stage_v_transposed(AttnSmem<BK>& sm, const uint16_t* __restrict__ vbase,
-                                                   int64_t row_stride, int key0, int kv_len) {
+__device__ __forceinline__ void load_v_raw(const uint16_t* __restrict__ vbase, int64_t row_stride, int key0,
+                                           int kv_len, u32x4 (&raw)[BK / 16][4]) {
   const int lane = lane_id();
 #pragma unroll
   for (int it = 0; it < BK / 16; ++it) {
     const int q = lane + kWave * it;        // (4-key group, 8-dim group)
     const int key4 = q >> 4, dg = q & 15;
-    uint4 rows[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int key = key0 + 4 * key4 + j;
-      rows[j] = key < kv_len ? *reinterpret_cast<const uint4*>(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
-                             : make_uint4(0, 0, 0, 0);
+      raw[it][j] = key < kv_len ? *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
+                                : u32x4{0, 0, 0, 0};
     }
-    const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
-    const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&rows[1]);
-    const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&rows[2]);
-    const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&rows[3]);
+  }
+}
+// ... and stores them transposed into LDS as vt[d][key].
+template <int BK>
+__device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const u32x4 (&raw)[BK / 16][4]) {
+  const int lane = lane_id();
+#pragma unroll
+  for (int it = 0; it < BK / 16; ++it) {
+    const int q = lane + kWave * it;
+    const int key4 = q >> 4, dg = q & 15;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      uint2 w;
-      w.x = static_cast<uint32_t>(e0[e]) | (static_cast<uint32_t>(e1[e]) << 16);
-      w.y = static_cast<uint32_t>(e2[e]) | (static_cast<uint32_t>(e3[e]) << 16);
-      *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = w;
+      const int w = e >> 1, sh = (e & 1) * 16;
+      uint2 x;
+      x.x = ((raw[it][0][w] >> sh) & 0xFFFFu) | (((raw[it][1][w] >> sh) & 0xFFFFu) << 16);
+      x.y = ((raw[it][2][w] >> sh) & 0xFFFFu) | (((raw[it][3][w] >> sh) & 0xFFFFu) << 16);
+      *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = x;
     }
   }
 }
@@ -99,21 +105,26 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
     const int b = ids[slot];
     if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
     const int key0 = b * BK;
-    __syncthreads();                                  // previous block's V reads are done
-    stage_v_transposed<BK>(sm, vbase, kv_stride, key0, g.kv_len);
+    // K (A operands of S^T) and raw V of this block are requested together;
+    // S^T and the softmax run while V is still in flight.
+    bf16x8 ka[BK / 16][kHeadDim / 32];
+#pragma unroll
+    for (int i = 0; i < BK / 16; ++i) {
+      const int key = key0 + 16 * i + n;
+      const uint16_t* kp = kbase + static_cast<int64_t>(key) * kv_stride;
+#pragma unroll
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? ld_bf16x8(kp + 32 * ks) : zero_bf16x8();
+    }
+    u32x4 vraw[BK / 16][4];
+    load_v_raw<BK>(vbase, kv_stride, key0, g.kv_len, vraw);
 
     // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
     f32x4 st[BK / 16];
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i) {
-      const int key = key0 + 16 * i + n;
       st[i] = f32x4{};
-      const uint16_t* kp = kbase + static_cast<int64_t>(key) * kv_stride;
 #pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) {
-        bf16x8 a = key < g.kv_len ? ld_bf16x8(kp + 32 * ks) : zero_bf16x8();
-        st[i] = mfma16x16x32(a, bq[ks], st[i]);
-      }
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) st[i] = mfma16x16x32(ka[i][ks], bq[ks], st[i]);
     }
     // lane (n, q4) holds keys 16i + 4*q4 + e of head n
     float bmax = -INFINITY;
@@ -147,6 +158,8 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
 #pragma unroll
     for (int t = 0; t < kHeadDim / 16; ++t) acc[t] *= alpha;
 
+    __syncthreads();                                  // the previous block's V^T reads are done
+    store_v_transposed<BK>(sm, vraw);
     // P^T as the B operand: k-step u covers keys 32u..32u+31; lane (n, q4)
     // supplies logical k = 8*q4 + e <-> key 32u + 4*q4 + e (e < 4) and
     // 32u + 16 + 4*q4 + e - 4 (e >= 4), exactly the keys its S^T tiles hold.
