@@ -75,7 +75,7 @@ __device__ __forceinline__ UnitRows locate_unit(const msa_seqs& sq, const int32_
   UnitRows r;
   r.ok = false;
   if (uidx >= unit_off[sq.num_seqs]) return r;
-  r.s = find_seq(unit_off, sq.num_seqs, uidx);
+  r.s = find_seq_wave(unit_off, sq.num_seqs, uidx);
   r.g = seq_geom(sq, r.s);
   r.t0 = static_cast<int>(uidx - unit_off[r.s]) * qr * U;
   r.nq = min(qr * U, r.g.q_rows - r.t0);
@@ -326,6 +326,85 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
   }
 }
 
+// Narrow variant for row groups of at most 16 index rows (decode: one query
+// row x H_kv <= 16 groups): MFMA 16x16x32 with keys as M and the rows as N
+// needs a quarter of the registers, so DEPTH blocks stream through registers
+// per wave (clamped, unconditional loads) and more waves share each CU.
+// Lane (n, q4) supplies key 16i + n / row n and dims 32ks + 8q4 .. +8; C lane
+// (n, q4) holds row n, keys 16i + 4q4 + e.
+template <int D_IDX, int BK, int DEPTH>
+__global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
+    int64_t ldm) {
+  constexpr int KS = D_IDX / 32;
+  constexpr int MT = BK / 16;
+  const int lane = lane_id();
+  const int64_t uidx = u0 + blockIdx.y;
+  const int slice = blockIdx.x * kWaves + threadIdx.x / kWave;
+  if (uidx >= u1) return;
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, 1);
+  if (!ur.ok) return;
+  const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
+  if (p_last < 0) return;
+  const int kb1 = min(p_last / BK, static_cast<int>(ldm));
+  const int kb0 = slice * kSliceBlocks;
+  if (kb0 >= kb1) return;
+
+  const int n = lane & 15, q4 = lane >> 4;
+  const int nvalid = min(ur.nq * H_kv, 16);
+  bf16x8 bq[KS];
+  const uint16_t* qrow = index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv + n) * D_IDX + 8 * q4;
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) bq[ks] = n < nvalid ? ld_bf16x8(qrow + 32 * ks) : zero_bf16x8();
+  const uint16_t* kbase = index_k + (ur.g.kv_start + n) * D_IDX + 8 * q4;
+
+  // blocks kb0 .. kb1-1 are entirely before every row's local block, hence
+  // inside the sequence; loads past kb1 re-read block kb1-1
+  auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
+    kb = min(kb, kb1 - 1);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      const uint16_t* kp = kbase + static_cast<int64_t>(kb * BK + 16 * i) * D_IDX;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) a[i][ks] = ld_bf16x8(kp + 32 * ks);
+    }
+  };
+  bf16x8 buf[DEPTH][MT][KS];
+#pragma unroll
+  for (int d = 0; d < DEPTH; ++d) load_a(kb0 + d, buf[d]);
+  float mb[kSliceBlocks];
+#pragma unroll
+  for (int i = 0; i < kSliceBlocks; ++i) {
+    bf16x8 (&a)[MT][KS] = buf[i % DEPTH];
+    f32x4 acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      acc[t] = f32x4{};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) acc[t] = mfma16x16x32(a[t][ks], bq[ks], acc[t]);
+    }
+    float m = acc[0][0];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) m = fmaxf(m, acc[t][e]);
+    m = fmaxf(m, __uint_as_float(xor_lane_u32<16>(__float_as_uint(m))));
+    m = fmaxf(m, __uint_as_float(xor_lane_u32<32>(__float_as_uint(m))));
+    mb[i] = m;
+    if (i + DEPTH < kSliceBlocks) load_a(kb0 + i + DEPTH, a);
+  }
+  // values past kb1 are never read (they are >= every row's local block) and
+  // stay inside this slice; quads start below ldm (a multiple of 4)
+  if (lane < nvalid) {
+    float* mrow = M + ((uidx - u0) * kWave + lane) * ldm + kb0;
+#pragma unroll
+    for (int q = 0; q < kSliceBlocks / 4; ++q)
+      if (kb0 + 4 * q < ldm)
+        *reinterpret_cast<float4*>(mrow + 4 * q) = make_float4(mb[4 * q], mb[4 * q + 1], mb[4 * q + 2], mb[4 * q + 3]);
+  }
+}
+
 // ---------------------------------------------------------------- top-k
 // Streams chunks c_begin, c_begin + c_step, ... (64 blocks each) of one row's
 // block scores; returns the row's best keys of those chunks, sorted
@@ -473,6 +552,7 @@ __global__ __launch_bounds__(256) void index_topk_split_kernel(
 struct IndexPlan {
   int qr;
   int U;                // row groups per unit
+  bool narrow;          // U = 1 with at most 16 index rows per row group
   int64_t max_units;    // upper bound of the units over all sequences
   int bcap;             // M row length (key blocks, multiple of 4)
   size_t hdr_bytes;
@@ -490,6 +570,7 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   pl->qr = 64 / H_kv;
   // sequences longer than two row groups take the LDS-shared kernel
   pl->U = static_cast<int64_t>(seqs->max_q_rows) > 2 * pl->qr ? kWaves : 1;
+  pl->narrow = pl->U == 1 && std::min(pl->qr, seqs->max_q_rows) * H_kv <= 16 && !(d_idx == 128 && BK == 128);
   const int64_t max_groups = seqs->total_q_rows / pl->qr + seqs->num_seqs;
   pl->max_units = max_groups / pl->U + seqs->num_seqs;
   int nb = (seqs->max_kv_len + BK - 1) / BK;
@@ -502,12 +583,19 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
 constexpr int64_t kSplitTopkRows = 16384;                // fewer index rows: 4 waves per row
 
+// Blocks in flight per wave of the narrow kernel: about 128 VGPRs of K_idx.
+template <int D, int B>
+constexpr int kNarrowDepth = D * B <= 64 * 64 ? 4 : 2;
+
 template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
                    const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M) {
   if (pl.U == kWaves)
     hipLaunchKernelGGL((index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+  else if (pl.narrow)
+    hipLaunchKernelGGL((index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
+                       ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
   else
     hipLaunchKernelGGL((index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));

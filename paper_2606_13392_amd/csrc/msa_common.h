@@ -169,6 +169,25 @@ __device__ __forceinline__ int find_seq(const int32_t* __restrict__ q_offsets, i
   return lo;
 }
 
+// The same search for a wave-uniform row: each level samples 64 evenly spaced
+// offsets (one load per lane) and keeps the last one <= row, so one level
+// covers 64 sequences and two cover 4096.  Every lane of the wave must call it
+// with the same row; offsets[0] <= row is assumed (offsets start at zero).
+__device__ __forceinline__ int find_seq_wave(const int32_t* __restrict__ offsets, int num_seqs, int64_t row) {
+  int lo = 0, n = num_seqs;                  // the answer lies in [lo, lo + n)
+  while (n > 1) {
+    const int stride = (n + kWave - 1) / kWave;
+    const int idx = lo + __lane_id() * stride;
+    const bool ok = idx < lo + n && static_cast<int64_t>(offsets[idx]) <= row;
+    const uint64_t mask = __ballot(ok);      // a prefix of the lanes: offsets are non-decreasing
+    const int j = 63 - __clzll(static_cast<long long>(mask | 1ull));
+    const int lo_new = lo + j * stride;
+    n = min(stride, lo + n - lo_new);
+    lo = lo_new;
+  }
+  return lo;
+}
+
 // Per-sequence geometry read from the device layout arrays, with the key
 // range clamped to the key-side tensor so no access can leave it.
 struct SeqGeom {

@@ -77,7 +77,7 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
   const int sp = blockIdx.y;
   const int nsplit = gridDim.y;
   if (row >= sq.total_q_rows) return;
-  const int s = find_seq(sq.q_offsets, sq.num_seqs, row);
+  const int s = find_seq_wave(sq.q_offsets, sq.num_seqs, row);
   const SeqGeom g = seq_geom(sq, s);
   int p = g.kv_len - g.q_rows + static_cast<int>(row - g.q_begin);
   if (p >= g.kv_len) p = -1;                        // inconsistent layout: attend to nothing
@@ -101,8 +101,10 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
 
   const int slot0 = sp * slots_per_split;
   const int slot1 = min(topk, slot0 + slots_per_split);
+  // the split's block ids, one per lane, fetched at once (slots_per_split <= 64)
+  const int my_b = slot0 + lane < slot1 ? ids[slot0 + lane] : -1;
   for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
-    const int b = ids[slot];
+    const int b = __builtin_amdgcn_readlane(my_b, slot - slot0);
     if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
     const int key0 = b * BK;
     // K (A operands of S^T) and raw V of this block are requested together;

@@ -105,8 +105,8 @@ __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restric
   const int r = blockIdx.y;
   const int64_t rb0 = row0 + static_cast<int64_t>(blockIdx.x) * kHistRows;
   const int64_t rb1 = min(rb0 + kHistRows, row0 + nrows);
-  const int s_first = find_seq(sq.q_offsets, sq.num_seqs, rb0);
-  const int s_last = find_seq(sq.q_offsets, sq.num_seqs, rb1 - 1);
+  const int s_first = find_seq_wave(sq.q_offsets, sq.num_seqs, rb0);
+  const int s_last = find_seq_wave(sq.q_offsets, sq.num_seqs, rb1 - 1);
   const int64_t g_lo = blk_base[s_first];
   const int64_t g_hi = blk_base[s_last + 1];
   const bool in_lds = g_hi - g_lo <= kHistBins;           // uniform over the CTA

@@ -49,9 +49,17 @@ def test_workspace_queries_are_host_only():
     L = msa.lib()
     s = _seqs()
     n = L.msa_index_topk_workspace_size(ctypes.byref(s), 2, 64, 64, 8)
-    # 64 index rows per group, ceil(100/64)=2 blocks rounded to 4, fp32; plus the group table
+    # row groups of 64 / H_kv = 32 query rows; sequences longer than two groups
+    # take units of 4 groups.  Each unit holds 4 x 64 index rows of
+    # ceil(100/64) = 2 block scores rounded up to 4, fp32; plus the unit table.
     groups = 100 // 32 + 1
-    assert n == 256 + groups * 64 * 4 * 4
+    units = groups // 4 + 1
+    assert n == 256 + units * 4 * 64 * 4 * 4
+    # a single row group per sequence: units of one group
+    s1 = _seqs(num_seqs=4, total_q_rows=4, max_q_rows=1)
+    n1 = L.msa_index_topk_workspace_size(ctypes.byref(s1), 2, 64, 64, 8)
+    groups1 = 4 // 32 + 4
+    assert n1 == 256 + (groups1 + 4) * 64 * 4 * 4
     # partials (bf16 O + fp32 LSE per slot, row, head) and the (row, group, slot) handles
     n = L.msa_sparse_attn_prefill_workspace_size(ctypes.byref(s), 8, 2, 128, 64, 8)
     assert n >= 8 * 100 * 8 * (128 * 2 + 4) + 100 * 2 * 8 * 4
