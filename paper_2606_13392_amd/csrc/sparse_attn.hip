@@ -2,14 +2,16 @@
 // visible tokens of the selected key blocks (Sec. 3.1, sparse-attention
 // equation), returning O and the natural-log LSE.
 //
-// attn_rows_kernel: one wave per (query row, group, split).  The G query heads
+// attn_rows_kernel: one CTA of four waves per (query row, group, split); each
+// wave takes its own share of the group's selected blocks.  The G query heads
 // of the group share the group's block list (Sec. 2.3, group-shared index
 // set), so one wave computes S^T = K Q^T for all of them with MFMA 16x16x32
 // (keys as M, heads as N, head_dim as K), keeps an online softmax per head in
 // registers (each lane owns one head's column) and accumulates O^T = V^T P^T
-// with V staged transposed in LDS.  With several splits per row it writes
-// locally normalised partials that combine_kernel merges with the log-sum-exp
-// rule of Sec. 4.2 ("Two-phase forward").
+// with V staged transposed in its own LDS area.  The four waves then merge
+// their states through LDS with the log-sum-exp rule of Sec. 4.2 ("Two-phase
+// forward").  With several splits per row the CTA writes a locally normalised
+// partial that combine_kernel merges by the same rule.
 #include "msa_common.h"
 
 namespace {
@@ -20,11 +22,23 @@ constexpr int kHeadDim = 128;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+constexpr int kAttnWaves = 4;                 // waves per CTA, each with its own block share
+constexpr int kRedStride = kHeadDim + 4;      // fp32 row stride of the merge buffer
+
 template <int BK>
 struct AttnSmem {
-  // V of one block, transposed: vt[d][key]; +4 keys of padding per row.
+  // V of one block, transposed: vt[d][key]; +4 keys of padding per row.  After
+  // the block loop the same bytes hold the wave's scaled O (16 x kRedStride fp32).
   uint16_t vt[kHeadDim][BK + 4];
 };
+static_assert(sizeof(AttnSmem<64>) >= 16 * kRedStride * sizeof(float), "merge buffer does not fit");
+
+// Orders a wave's own LDS accesses (a wave's LDS operations complete in issue
+// order; this keeps the compiler from moving them across).
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
 
 // V[b*BK .. b*BK+BK) of group r: each lane loads 4 keys x 8 dims per
 // (4-key group, 8-dim group) pair; keys past the sequence's end read as zero.
@@ -64,19 +78,22 @@ __device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const u32x4
 }
 
 template <int BK>
-__global__ __launch_bounds__(64) void attn_rows_kernel(
+__global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int topk,
-    int slots_per_split, float scale_log2, uint16_t* __restrict__ o, float* __restrict__ lse,
+    int slots_per_wave, float scale_log2, uint16_t* __restrict__ o, float* __restrict__ lse,
     float* __restrict__ o_part, float* __restrict__ lse_part) {
-  __shared__ AttnSmem<BK> sm;
+  __shared__ __align__(16) AttnSmem<BK> smw[kAttnWaves];
+  __shared__ float mls[kAttnWaves][2][16];
   const int lane = lane_id();
+  const int wv = threadIdx.x / kWave;
+  AttnSmem<BK>& sm = smw[wv];
   const int G = H_q / H_kv;
   const int64_t row = blockIdx.x / H_kv;
   const int r = blockIdx.x % H_kv;
   const int sp = blockIdx.y;
   const int nsplit = gridDim.y;
-  if (row >= sq.total_q_rows) return;
+  if (row >= sq.total_q_rows) return;                // uniform over the CTA
   const int s = find_seq_wave(sq.q_offsets, sq.num_seqs, row);
   const SeqGeom g = seq_geom(sq, s);
   int p = g.kv_len - g.q_rows + static_cast<int>(row - g.q_begin);
@@ -99,9 +116,9 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
 #pragma unroll
   for (int t = 0; t < kHeadDim / 16; ++t) acc[t] = f32x4{};
 
-  const int slot0 = sp * slots_per_split;
-  const int slot1 = min(topk, slot0 + slots_per_split);
-  // the split's block ids, one per lane, fetched at once (slots_per_split <= 64)
+  const int slot0 = min(topk, (sp * kAttnWaves + wv) * slots_per_wave);
+  const int slot1 = min(topk, slot0 + slots_per_wave);
+  // the wave's block ids, one per lane, fetched at once (slots_per_wave <= 64)
   const int my_b = slot0 + lane < slot1 ? ids[slot0 + lane] : -1;
   for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
     const int b = __builtin_amdgcn_readlane(my_b, slot - slot0);
@@ -160,12 +177,12 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
 #pragma unroll
     for (int t = 0; t < kHeadDim / 16; ++t) acc[t] *= alpha;
 
-    __syncthreads();                                  // the previous block's V^T reads are done
+    wave_lds_order();                                 // the previous block's V^T reads are done
     store_v_transposed<BK>(sm, vraw);
     // P^T as the B operand: k-step u covers keys 32u..32u+31; lane (n, q4)
     // supplies logical k = 8*q4 + e <-> key 32u + 4*q4 + e (e < 4) and
     // 32u + 16 + 4*q4 + e - 4 (e >= 4), exactly the keys its S^T tiles hold.
-    __syncthreads();                                  // V staged
+    wave_lds_order();                                 // V staged
 #pragma unroll
     for (int u = 0; u < BK / 32; ++u) {
       bf16x8 bp;
@@ -190,30 +207,70 @@ __global__ __launch_bounds__(64) void attn_rows_kernel(
     }
   }
 
-  // O^T tiles: lane (n, q4) holds d = 16t + 4*q4 + e of head n.
-  if (n >= G) return;
-  const int64_t head_row = row * H_q + static_cast<int64_t>(r) * G + n;
-  const bool empty = !(l_run > 0.f);
-  const float inv_l = empty ? 0.f : 1.f / l_run;
-  const float lse_v = empty ? -INFINITY : (m_run + __log2f(l_run)) * kLn2;
-  if (nsplit == 1) {
-    uint16_t* orow = o + head_row * kHeadDim + 4 * q4;
+  // Merge the waves' states (Sec. 4.2): M = max_w m_w, L = sum_w l_w 2^(m_w - M),
+  // O = sum_w 2^(m_w - M) acc_w / L.  O^T tiles: lane (n, q4) holds
+  // d = 16t + 4*q4 + e of head n.
+  __syncthreads();                                    // every wave is done with its V^T area
+  if (q4 == 0) {
+    mls[wv][0][n] = m_run;
+    mls[wv][1][n] = l_run;
+  }
+  __syncthreads();
+  auto merged = [&](int h, float& M, float& L) {
+    M = -INFINITY;
 #pragma unroll
-    for (int t = 0; t < kHeadDim / 16; ++t) {
-      uint2 w;
-      w.x = pack_bf16x2(acc[t][0] * inv_l, acc[t][1] * inv_l);
-      w.y = pack_bf16x2(acc[t][2] * inv_l, acc[t][3] * inv_l);
-      *reinterpret_cast<uint2*>(orow + 16 * t) = w;
+    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, mls[w][0][h]);
+    L = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const float mw = mls[w][0][h];
+      L += mw > -INFINITY ? mls[w][1][h] * exp2f(mw - M) : 0.f;
     }
-    if (q4 == 0) lse[head_row] = lse_v;
+  };
+  {
+    float M, L;
+    merged(n, M, L);
+    const float f = m_run > -INFINITY ? exp2f(m_run - M) : 0.f;
+    float* red = reinterpret_cast<float*>(&sm.vt[0][0]) + n * kRedStride + 4 * q4;
+#pragma unroll
+    for (int t = 0; t < kHeadDim / 16; ++t) *reinterpret_cast<f32x4*>(red + 16 * t) = acc[t] * f;
+  }
+  __syncthreads();
+  // thread (head hn, dims d0 .. d0+8) sums the waves' scaled rows
+  const int hn = threadIdx.x / 16, d0 = 8 * (threadIdx.x % 16);
+  if (hn >= G) return;
+  float M, L;
+  merged(hn, M, L);
+  float out[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+  for (int w = 0; w < kAttnWaves; ++w) {
+    const float* red = reinterpret_cast<const float*>(&smw[w].vt[0][0]) + hn * kRedStride + d0;
+    const f32x4 x0 = *reinterpret_cast<const f32x4*>(red);
+    const f32x4 x1 = *reinterpret_cast<const f32x4*>(red + 4);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[e] += x0[e];
+      out[4 + e] += x1[e];
+    }
+  }
+  const int64_t head_row = row * H_q + static_cast<int64_t>(r) * G + hn;
+  const bool empty = !(L > 0.f);
+  const float inv_l = empty ? 0.f : 1.f / L;
+  const float lse_v = empty ? -INFINITY : (M + __log2f(L)) * kLn2;
+  if (nsplit == 1) {
+    uint4 wq;
+    wq.x = pack_bf16x2(out[0] * inv_l, out[1] * inv_l);
+    wq.y = pack_bf16x2(out[2] * inv_l, out[3] * inv_l);
+    wq.z = pack_bf16x2(out[4] * inv_l, out[5] * inv_l);
+    wq.w = pack_bf16x2(out[6] * inv_l, out[7] * inv_l);
+    *reinterpret_cast<uint4*>(o + head_row * kHeadDim + d0) = wq;
+    if (d0 == 0) lse[head_row] = lse_v;
   } else {
     const int64_t part_row = static_cast<int64_t>(sp) * sq.total_q_rows * H_q + head_row;
-    float* orow = o_part + part_row * kHeadDim + 4 * q4;
-#pragma unroll
-    for (int t = 0; t < kHeadDim / 16; ++t)
-      *reinterpret_cast<float4*>(orow + 16 * t) =
-          make_float4(acc[t][0] * inv_l, acc[t][1] * inv_l, acc[t][2] * inv_l, acc[t][3] * inv_l);
-    if (q4 == 0) lse_part[part_row] = lse_v;
+    float4* dst = reinterpret_cast<float4*>(o_part + part_row * kHeadDim + d0);
+    dst[0] = make_float4(out[0] * inv_l, out[1] * inv_l, out[2] * inv_l, out[3] * inv_l);
+    dst[1] = make_float4(out[4] * inv_l, out[5] * inv_l, out[6] * inv_l, out[7] * inv_l);
+    if (d0 == 0) lse_part[part_row] = lse_v;
   }
 }
 
@@ -279,19 +336,22 @@ int validate_attn(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK,
 }
 
 struct SplitPlan {
-  int nsplit;
-  int slots_per_split;
+  int nsplit;           // CTAs per (row, group); above one, partials go through combine_kernel
+  int slots_per_wave;
 };
 
-// Split the k slots of each (row, group) over enough waves to fill the chip.
+// Spread the k slots of each (row, group) over kAttnWaves waves per CTA and
+// over enough CTAs to give the chip about 2048 waves.
 SplitPlan split_plan(const msa_seqs* seqs, int H_kv, int topk) {
   SplitPlan sp;
   const int64_t pairs = seqs->total_q_rows * H_kv;
-  int want = pairs > 0 ? static_cast<int>((4096 + pairs - 1) / pairs) : 1;
+  const int max_ctas = (topk + kAttnWaves - 1) / kAttnWaves;
+  int64_t want = pairs > 0 ? (2048 + pairs * kAttnWaves - 1) / (pairs * kAttnWaves) : 1;
   if (want < 1) want = 1;
-  if (want > topk) want = topk;
-  sp.slots_per_split = (topk + want - 1) / want;
-  sp.nsplit = (topk + sp.slots_per_split - 1) / sp.slots_per_split;
+  if (want > max_ctas) want = max_ctas;
+  const int waves = static_cast<int>(want) * kAttnWaves;
+  sp.slots_per_wave = (topk + waves - 1) / waves;
+  sp.nsplit = (topk + sp.slots_per_wave * kAttnWaves - 1) / (sp.slots_per_wave * kAttnWaves);
   return sp;
 }
 
@@ -319,12 +379,13 @@ int run_rows(const void* q, const void* k, const void* v, const int32_t* block_i
   auto* kp = static_cast<const uint16_t*>(k);
   auto* vp = static_cast<const uint16_t*>(v);
   auto* op = static_cast<uint16_t*>(o);
+  const dim3 block(64 * kAttnWaves);
   if (BK == 64)
-    hipLaunchKernelGGL(attn_rows_kernel<64>, grid, dim3(64), 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv,
-                       topk, sp.slots_per_split, sl2, op, lse, o_part, lse_part);
+    hipLaunchKernelGGL(attn_rows_kernel<64>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
+                       sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
   else
-    hipLaunchKernelGGL(attn_rows_kernel<128>, grid, dim3(64), 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv,
-                       topk, sp.slots_per_split, sl2, op, lse, o_part, lse_part);
+    hipLaunchKernelGGL(attn_rows_kernel<128>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
+                       sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
   if (sp.nsplit > 1) {
     const int64_t threads = hr * 16;
     hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,
