@@ -12,9 +12,14 @@ reported under "decode".
 
 Inputs are drawn on the device before timing (synthetic, seeded) and stay
 resident in HBM.  Each library call is bracketed by HIP events on the stream
-it runs on; ``roofline`` uses the attention call's average duration and its
-effective FLOPs (selected tokens only).  ``cpu_baseline`` times the CPU oracle
-on a bounded sample of query rows of the same workload.
+it runs on, and the library's kernel timing (msa_profile_*) brackets each of
+its kernels with events on that same stream during the timed steps.
+``roofline`` describes the kernel with the largest time per step: its
+algorithmic bytes or FLOPs per launch (models below) over its average launch
+duration.  ``calls`` gives both calls' times; the attention call's effective
+FLOPs (selected tokens only) over its time is the MFMA utilisation of the
+Main Branch.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
+query rows of the same workload.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -105,11 +110,15 @@ def run_prefill(args, dev):
         torch.cuda.synchronize()
         log(f"[bench] warmup {i + 1}/{args.warmup} done")
     torch.cuda.synchronize()
+    msa.profile_reset()
+    msa.profile_enable(True)
     t0 = time.perf_counter()
     for i in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    msa.profile_enable(False)
+    kernels = msa.profile_read()
     log(f"[bench] timed {args.steps} prefill steps in {t1 - t0:.3f} s")
     sec = (t1 - t0) / args.steps
     ms_idx = t_idx.mean_ms(skip=args.warmup)
@@ -117,8 +126,11 @@ def run_prefill(args, dev):
 
     positions = torch.from_numpy(p.positions()).to(dev)
     toks = attended_tokens(ids, positions, p.block_size)
+    pos3 = positions.view(-1, 1, 1)
+    incidences = float(((ids >= 0) & (ids.to(torch.int64) * p.block_size <= pos3)).sum().item())
+    scored_keys = float(index_scored_keys(positions, p.block_size).sum().item())
     eff_flops = 4.0 * dh * (H_q // H_kv) * float(toks.sum().item())
-    idx_flops = 2.0 * p.d_idx * H_kv * float(index_scored_keys(positions, p.block_size).sum().item())
+    idx_flops = 2.0 * p.d_idx * H_kv * scored_keys
     paper_main = 4.0 * H_q * dh * p.total_q_rows * p.topk * p.block_size
     res = {
         "workload": p,
@@ -128,10 +140,65 @@ def run_prefill(args, dev):
         "eff_flops": eff_flops,
         "idx_flops": idx_flops,
         "paper_main_flops": paper_main,
+        "kernels": {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
+                        "ms_per_launch": ms / n} for k, (n, ms) in kernels.items()},
+        "models": kernel_models(p, incidences, scored_keys, eff_flops, idx_flops),
         "inputs": d,
         "ids": ids,
     }
     return res
+
+
+def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
+    """Algorithmic work per step of the prefill kernels: (bound, amount, unit).
+
+    An incidence is one valid (query row, group, selected block).  The
+    key-block-outer attention reads each key block's K and V once per group and,
+    per incidence, gathers the G query rows and writes a bf16 partial O plus its
+    fp32 LSE (Sec. 4.2 IO analysis, KV-outer): its intensity, about 2/3 B_k
+    FLOP/B, sits far below MI355X's bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312), so
+    it is HBM-bound.  The combine reads every partial and writes O and LSE.
+    Index scoring is an MFMA contraction; Top-k streams the block scores."""
+    G = p.num_q_heads // p.num_kv_heads
+    d, T, H_kv, H_q = p.head_dim, p.total_q_rows, p.num_kv_heads, p.num_q_heads
+    kv_bytes = 4.0 * H_kv * float(sum(p.kv_lens)) * d
+    attn_bytes = kv_bytes + incidences * (4.0 * G * d + 4.0 * G + 4.0)
+    comb_bytes = incidences * (2.0 * G * d + 4.0 * G) + T * H_q * (2.0 * d + 4.0) + T * H_kv * p.topk * 4.0
+    score_blocks = scored_keys / p.block_size * H_kv          # block scores written and read back
+    return {
+        "kvo_attn_kernel": ("hbm", attn_bytes, "bytes"),
+        "kvo_combine_kernel": ("hbm", comb_bytes, "bytes"),
+        "index_block_max_lds_kernel": ("mfma", idx_flops, "flops"),
+        "index_block_max_wave_kernel": ("mfma", idx_flops, "flops"),
+        "index_topk_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
+        "index_topk_split_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
+    }
+
+
+def roofline_of(pre):
+    """Roofline object of the kernel with the largest time per step."""
+    kern = pre["kernels"]
+    if not kern:
+        return None
+    name = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    k = kern[name]
+    out = {"kernel": name, "ms_per_launch": k["ms_per_launch"], "launches_per_step": k["launches_per_step"],
+           "traffic": None}
+    model = pre["models"].get(name)
+    if model is None:
+        out.update({"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None})
+        return out
+    bound, amount, what = model
+    per_launch = amount / k["launches_per_step"]
+    if bound == "hbm":
+        achieved = per_launch / (k["ms_per_launch"] * 1e-3) / 1e9
+        out.update({"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": achieved / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": per_launch})
+    else:
+        achieved = per_launch / (k["ms_per_launch"] * 1e-3) / 1e12
+        out.update({"bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / PEAK_BF16_TFLOPS, "algorithmic_flops_per_launch": per_launch})
+    return out
 
 
 def run_decode(args, dev):
@@ -287,12 +354,14 @@ def main():
         "config": {"workload": p.name, "description": p.description, "T": p.total_q_rows,
                    "num_q_heads": p.num_q_heads, "num_kv_heads": p.num_kv_heads, "head_dim": p.head_dim,
                    "d_idx": p.d_idx, "block_size": p.block_size, "topk": p.topk},
-        "roofline": {"kernel": "msa_sparse_attn_prefill", "bound": "mfma", "achieved": att_tflops,
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": att_tflops / PEAK_BF16_TFLOPS,
-                     "traffic": None, "algorithmic_flops_per_launch": pre["eff_flops"],
-                     "ms_per_launch": pre["ms_att"]},
-        "index_topk": {"ms_per_launch": pre["ms_idx"], "algorithmic_flops_per_launch": pre["idx_flops"],
-                       "achieved_tflops": idx_tflops, "frac_of_bf16_peak": idx_tflops / PEAK_BF16_TFLOPS},
+        "roofline": roofline_of(pre),
+        "calls": {
+            "msa_index_topk": {"ms_per_call": pre["ms_idx"], "algorithmic_flops": pre["idx_flops"],
+                               "tflops": idx_tflops, "frac_of_bf16_peak": idx_tflops / PEAK_BF16_TFLOPS},
+            "msa_sparse_attn_prefill": {"ms_per_call": pre["ms_att"], "effective_flops": pre["eff_flops"],
+                                        "tflops": att_tflops, "frac_of_bf16_peak": att_tflops / PEAK_BF16_TFLOPS},
+        },
+        "kernels": pre["kernels"],
         "main_branch_flops": {"effective": pre["eff_flops"], "paper_formula_4HqdhNkBk": pre["paper_main_flops"]},
     }
     ids = pre.pop("ids")

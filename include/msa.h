@@ -27,8 +27,9 @@
  *   matching *_workspace_size() query; the workspace is free again once the
  *   stream has executed the call.  Calls that share a workspace must be ordered
  *   on one stream.
- * - The library keeps no global state; concurrent calls from several host
- *   threads are safe when they use distinct outputs and workspaces.
+ * - Apart from the opt-in kernel timing at the end of this header, the
+ *   library keeps no global state; concurrent calls from several host threads
+ *   are safe when they use distinct outputs and workspaces.
  * - NaN or Inf inputs give unspecified (but memory-safe) results.
  *
  * Sequence layout (struct msa_seqs)
@@ -149,6 +150,32 @@ int msa_sparse_attn_decode(const void* q, const void* k, const void* v,
                            int num_kv_heads, int head_dim, int block_size, int topk,
                            float softmax_scale, void* o, float* lse, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing (a measurement aid; no part of the attention path)
+ *
+ * While enabled, every kernel a call launches is bracketed by a pair of HIP
+ * events recorded on the call's stream, filed under the kernel's name (e.g.
+ * "kvo_attn_kernel", "index_block_max_lds_kernel").  The events are created
+ * on first use and kept for reuse; they are the library's only global state.
+ *
+ *   msa_profile_enable(on)   on != 0 starts recording for later calls, 0 stops.
+ *   msa_profile_reset()      forgets the launches recorded so far.
+ *   msa_profile_kernel_name(i)  name of the i-th kernel seen since load, or
+ *                            NULL past the last one (static until unload).
+ *   msa_profile_read(name, &launches, &total_ms)  launches of `name` since the
+ *                            last reset and their summed event-to-event time;
+ *                            waits for those events; unknown names read 0.
+ *
+ * Timing adds two event records per launch, so enable it only for runs that
+ * read it.  Calls on several host threads must not interleave with reset or
+ * read.  Errors: MSA_ERR_INVALID for null output pointers, MSA_ERR_HIP when
+ * an event cannot be read.
+ * ------------------------------------------------------------------------ */
+int msa_profile_enable(int on);
+int msa_profile_reset(void);
+const char* msa_profile_kernel_name(int i);
+int msa_profile_read(const char* kernel, int64_t* launches, double* total_ms);
 
 #ifdef __cplusplus
 }

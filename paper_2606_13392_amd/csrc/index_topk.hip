@@ -25,6 +25,7 @@
 #include <algorithm>
 
 #include "msa_common.h"
+#include "msa_profile.h"
 
 namespace {
 
@@ -591,13 +592,13 @@ template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
                    const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M) {
   if (pl.U == kWaves)
-    hipLaunchKernelGGL((index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
+    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
   else if (pl.narrow)
-    hipLaunchKernelGGL((index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
+    msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
                        ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
   else
-    hipLaunchKernelGGL((index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
+    msa_prof::launch("index_block_max_wave_kernel", (index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
                        pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
 }
 
@@ -632,7 +633,7 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
 
-  hipLaunchKernelGGL(unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
+  msa_prof::launch("unit_offsets_kernel", unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
   // per-wave kernel: slices of kSliceBlocks consecutive blocks, 4 per CTA
   const int nslice = (pl.bcap + kSliceBlocks - 1) / kSliceBlocks;
   const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerCta - 1) / kBlocksPerCta);
@@ -654,11 +655,11 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
                     num_kv_heads;
     const int64_t rows = (u1 - u0) * rpu;
     if (rows <= kSplitTopkRows)
-      hipLaunchKernelGGL(index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, M,
+      msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, M,
                          static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
                          block_size, topk, block_ids);
     else
-      hipLaunchKernelGGL(index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)), dim3(256), 0,
+      msa_prof::launch("index_topk_kernel", index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)), dim3(256), 0,
                          stream, M, static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0,
                          u1, block_size, topk, block_ids);
   }

@@ -13,6 +13,7 @@
 // forward").  With several splits per row the CTA writes a locally normalised
 // partial that combine_kernel merges by the same rule.
 #include "msa_common.h"
+#include "msa_profile.h"
 
 namespace {
 
@@ -381,14 +382,14 @@ int run_rows(const void* q, const void* k, const void* v, const int32_t* block_i
   auto* op = static_cast<uint16_t*>(o);
   const dim3 block(64 * kAttnWaves);
   if (BK == 64)
-    hipLaunchKernelGGL(attn_rows_kernel<64>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
+    msa_prof::launch("attn_rows_kernel", attn_rows_kernel<64>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
                        sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
   else
-    hipLaunchKernelGGL(attn_rows_kernel<128>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
+    msa_prof::launch("attn_rows_kernel", attn_rows_kernel<128>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
                        sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
   if (sp.nsplit > 1) {
     const int64_t threads = hr * 16;
-    hipLaunchKernelGGL(combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,
+    msa_prof::launch("combine_kernel", combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,
                        o_part, lse_part, sp.nsplit, hr, op, lse);
   }
   return msa_host::launch_status();

@@ -23,6 +23,7 @@
 #include <algorithm>
 
 #include "msa_common.h"
+#include "msa_profile.h"
 
 namespace {
 
@@ -712,34 +713,34 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
   auto* op = static_cast<uint16_t*>(o);
   const float sl2 = scale * kLog2e;
 
-  hipLaunchKernelGGL(kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK, blk_base);
+  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK, blk_base);
   const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((pl.ntile + 255) / 256, 4096));
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
     const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, pl.ntile, 0);
+    msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, pl.ntile, 0);
     const dim3 hgrid(static_cast<unsigned>((nr + kHistRows - 1) / kHistRows), static_cast<unsigned>(H_kv));
-    hipLaunchKernelGGL(kvo_count_kernel, hgrid, dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK, topk,
+    msa_prof::launch("kvo_count_kernel", kvo_count_kernel, hgrid, dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK, topk,
                        pl.nbcap, r0, nr, cnt, tpos);
-    hipLaunchKernelGGL(kvo_scan_block_kernel, dim3(pl.nscan), dim3(256), 0, stream, cnt, pl.ntile, tile_off,
+    msa_prof::launch("kvo_scan_block_kernel", kvo_scan_block_kernel, dim3(pl.nscan), dim3(256), 0, stream, cnt, pl.ntile, tile_off,
                        item_off, blk_tot);
-    hipLaunchKernelGGL(kvo_scan_top_kernel, dim3(1), dim3(1024), 0, stream, blk_tot, pl.nscan, tile_off, item_off,
+    msa_prof::launch("kvo_scan_top_kernel", kvo_scan_top_kernel, dim3(1), dim3(1024), 0, stream, blk_tot, pl.nscan, tile_off, item_off,
                        pl.ntile);
-    hipLaunchKernelGGL(kvo_scan_add_kernel, dim3(static_cast<unsigned>((pl.ntile + 255) / 256)), dim3(256), 0,
+    msa_prof::launch("kvo_scan_add_kernel", kvo_scan_add_kernel, dim3(static_cast<unsigned>((pl.ntile + 255) / 256)), dim3(256), 0,
                        stream, blk_tot, pl.ntile, tile_off, item_off);
-    hipLaunchKernelGGL(kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
+    msa_prof::launch("kvo_fill_kernel", kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
                        topk, pl.nbcap, r0, nr, tile_off, tpos, handles);
     static int ctas64 = 0, ctas128 = 0;
     if (BK == 64)
-      hipLaunchKernelGGL(kvo_attn_kernel<64>, dim3(persistent_ctas(kvo_attn_kernel<64>, kAttnThreads, &ctas64)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
+      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<64>, dim3(persistent_ctas(kvo_attn_kernel<64>, kAttnThreads, &ctas64)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
                          sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
                          lse_buf);
     else
-      hipLaunchKernelGGL(kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, kAttnThreads, &ctas128)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
+      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, kAttnThreads, &ctas128)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
                          sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
                          lse_buf);
     const int64_t pairs = nr * H_kv;
-    hipLaunchKernelGGL(kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
+    msa_prof::launch("kvo_combine_kernel", kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
                        dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,
                        o_buf, lse_buf, op, lse);
   }

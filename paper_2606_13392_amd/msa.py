@@ -24,6 +24,7 @@ EXPORTS = [
     "msa_index_topk_workspace_size", "msa_index_topk",
     "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
+    "msa_profile_enable", "msa_profile_reset", "msa_profile_kernel_name", "msa_profile_read",
 ]
 
 
@@ -64,6 +65,15 @@ def lib() -> ctypes.CDLL:
             fn = getattr(L, f"msa_sparse_attn_{name}")
             fn.argtypes = [P, P, P, P, S, I, I, I, I, I, F, P, P, P, Z, P]
             fn.restype = I
+        L.msa_profile_enable.argtypes = [I]
+        L.msa_profile_enable.restype = I
+        L.msa_profile_reset.argtypes = []
+        L.msa_profile_reset.restype = I
+        L.msa_profile_kernel_name.argtypes = [I]
+        L.msa_profile_kernel_name.restype = ctypes.c_char_p
+        L.msa_profile_read.argtypes = [ctypes.c_char_p, ctypes.POINTER(ctypes.c_int64),
+                                       ctypes.POINTER(ctypes.c_double)]
+        L.msa_profile_read.restype = I
         _lib = L
     return _lib
 
@@ -203,3 +213,31 @@ def sparse_attn_decode(q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_
                        out=None, lse=None, workspace=None):
     """Decode-shaped variant of sparse_attn_prefill (one query row per sequence)."""
     return _attn("decode", q, k, v, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
+
+
+# ---------------------------------------------------------------- kernel timing
+def profile_enable(on: bool = True) -> None:
+    """Bracket every kernel of later calls with HIP events on its stream."""
+    _check(lib().msa_profile_enable(1 if on else 0), "msa_profile_enable")
+
+
+def profile_reset() -> None:
+    _check(lib().msa_profile_reset(), "msa_profile_reset")
+
+
+def profile_read() -> dict:
+    """{kernel name: (launches, summed ms)} since the last reset (waits for the events)."""
+    L = lib()
+    out = {}
+    i = 0
+    while True:
+        name = L.msa_profile_kernel_name(i)
+        if name is None:
+            break
+        n = ctypes.c_int64(0)
+        ms = ctypes.c_double(0.0)
+        _check(L.msa_profile_read(name, ctypes.byref(n), ctypes.byref(ms)), "msa_profile_read")
+        if n.value > 0:
+            out[name.decode()] = (int(n.value), float(ms.value))
+        i += 1
+    return out

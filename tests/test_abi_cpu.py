@@ -113,3 +113,17 @@ def test_sparse_attn_rejects(kind, arg_kw, want):
     st = fn(None if a["null_q"] else 8, 8, 8, 8, ctypes.byref(s), a["H_q"], a["H_kv"], a["d_h"], a["bk"],
             a["topk"], 0.1, 8, 8, 8, 1 << 30, None)
     assert st == want
+
+
+def test_profile_api_without_launches():
+    # enabling, resetting and reading touch no device while nothing was launched
+    L = msa.lib()
+    assert L.msa_profile_enable(1) == 0
+    assert L.msa_profile_reset() == 0
+    n = ctypes.c_int64(-1)
+    ms = ctypes.c_double(-1.0)
+    assert L.msa_profile_read(b"no_such_kernel", ctypes.byref(n), ctypes.byref(ms)) == 0
+    assert n.value == 0 and ms.value == 0.0
+    assert L.msa_profile_read(b"no_such_kernel", None, ctypes.byref(ms)) != 0
+    assert L.msa_profile_enable(0) == 0
+    assert msa.profile_read() == {} or all(v[0] > 0 for v in msa.profile_read().values())

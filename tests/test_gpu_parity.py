@@ -112,6 +112,34 @@ def test_deterministic():
     assert torch.equal(od.view(torch.int16), od2.view(torch.int16)) and torch.equal(ld, ld2)
 
 
+def test_kernel_timing_records_launches():
+    p = _problem(SMALL[1])
+    x = synth.generate_numpy(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    ids0 = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    o0, _ = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids0, seqs, p.block_size)
+    torch.cuda.synchronize()
+    msa.profile_reset()
+    msa.profile_enable(True)
+    try:
+        ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+        o, _ = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+        torch.cuda.synchronize()
+    finally:
+        msa.profile_enable(False)
+    rec = msa.profile_read()
+    assert rec.get("kvo_attn_kernel", (0, 0.0))[0] >= 1
+    assert rec.get("kvo_combine_kernel", (0, 0.0))[0] >= 1
+    assert any(k.startswith("index_block_max") for k in rec)
+    assert all(n >= 1 and ms > 0.0 for n, ms in rec.values())
+    # timing changes nothing in the results
+    assert torch.equal(ids, ids0) and torch.equal(o.view(torch.int16), o0.view(torch.int16))
+    msa.profile_reset()
+    assert msa.profile_read() == {}
+
+
 def test_workspace_rejected_when_small():
     p = _problem(SMALL[1])
     dev = torch.device("cuda")
