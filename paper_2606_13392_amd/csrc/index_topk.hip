@@ -155,11 +155,15 @@ __device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_
   }
 }
 
+// Besides M, each CTA writes its 64-block slice's maximum per row (over the
+// row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
+// prunes with.
 template <int D_IDX, int BK>
 __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
-    int64_t ldm) {
+    int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
+  static_assert(kBlocksPerCta == kWave, "a CTA slice is one Top-k chunk");
   constexpr int KS = D_IDX / 16;                        // k-steps of the MFMA
   constexpr int MT = BK / 32;                           // 32-key M tiles per block
   constexpr int SEGS = D_IDX / 8;                       // 16-byte segments per key row
@@ -186,7 +190,11 @@ __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
   // this wave's 64 rows of M; the block maxima of a 16-block group are staged
   // in LDS and stored as 64-byte row segments (blocks past kb1 in the last
   // group hold stale values that no row reads: they are >= its local block)
-  float* mrow0 = M + ((uidx - u0) * (kWaves * kWave) + w * kWave) * ldm;
+  const int64_t slot0 = (uidx - u0) * (kWaves * kWave) + w * kWave;   // this wave's first row of M
+  float* mrow0 = M + slot0 * ldm;
+  // candidate blocks of row `lane` end at its local block
+  const int lb_lane = (ur.g.kv_len - ur.g.q_rows + ur.t0 + wq0 + lane / H_kv) / BK;
+  float cmax = -INFINITY;
 
   const uint16_t* kseq = index_k + ur.g.kv_start * D_IDX;
   const int tid = threadIdx.x;
@@ -206,6 +214,7 @@ __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
       }
     }
     const float bm = block_max_rows<MT>(acc);
+    if (kb < lb_lane) cmax = fmaxf(cmax, bm);
     sm.stage[w][lane][kb & (kStageBlocks - 1)] = bm;
     if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
       // the wave writes 16 rows x 64 B per store pass (4 lanes per row, 16 B each)
@@ -246,6 +255,8 @@ __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
     if (kb + 2 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
     __syncthreads();
   }
+  // rows whose local block is at or below kb0 never read this entry
+  if (lane < nvalid) CM[static_cast<int64_t>(blockIdx.y) * cm_stride + slot0 + lane] = cmax;
 }
 
 // ---------------------------------------------------------------- scores, per wave
@@ -407,11 +418,34 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
 }
 
 // ---------------------------------------------------------------- top-k
-// Streams chunks c_begin, c_begin + c_step, ... (64 blocks each) of one row's
-// block scores; returns the row's best keys of those chunks, sorted
-// descending across the lanes (at least the best K1 are exact).
-__device__ __forceinline__ uint64_t scan_row_chunks(const float* __restrict__ mrow, int nscan, int K1, int c_begin,
-                                                    int c_step) {
+// Inserts the keys v (one per lane; 0 = none) that beat `thr` into `list`
+// (sorted descending across lanes) and returns the new K1-th best key.
+__device__ __forceinline__ uint64_t insert_keys(uint64_t v, uint64_t thr, int K1, uint64_t& list) {
+  const int lane = lane_id();
+  uint64_t pass = __ballot(v > thr);
+  if (pass == 0) return readlane_u64(list, K1 - 1);
+  if (__popcll(pass) <= kSmallInsert) {
+    while (pass) {
+      const int src = __ffsll(static_cast<unsigned long long>(pass)) - 1;
+      pass &= pass - 1;
+      const uint64_t xk = readlane_u64(v, src);
+      const int rnk = __popcll(__ballot(list > xk));
+      const uint64_t prev = lane_shr1_u64(list, list);
+      list = lane < rnk ? list : (lane == rnk ? xk : prev);
+    }
+  } else {
+    const uint64_t vs = wave_sort_desc_u64(v > thr ? v : 0ull);
+    const uint64_t rev = shfl_u64(vs, kWave - 1 - lane);
+    list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+  }
+  return readlane_u64(list, K1 - 1);
+}
+
+// Streams chunks c_begin, c_begin + c_step, ... (64 scores each) of one row,
+// score b read as load(b); returns the row's best keys of those chunks,
+// sorted descending across the lanes (at least the best K1 are exact).
+template <typename Load>
+__device__ __forceinline__ uint64_t scan_row_chunks(Load load, int nscan, int K1, int c_begin, int c_step) {
   const int lane = lane_id();
   uint64_t list = 0;   // sorted descending across lanes; 0 marks an empty slot
   uint64_t tau = 0;    // key of the K1-th best so far (0 while fewer are known)
@@ -422,7 +456,7 @@ __device__ __forceinline__ uint64_t scan_row_chunks(const float* __restrict__ mr
 #pragma unroll
   for (int a = 0; a < kAhead; ++a) {
     const int b = (c_begin + a * c_step) * kWave + lane;
-    pf[a] = b < nscan ? mrow[b] : 0.f;
+    pf[a] = b < nscan ? load(b) : 0.f;
   }
   for (int c = c_begin; c * kWave < nscan; c += c_step) {
     const int b = c * kWave + lane;
@@ -431,26 +465,72 @@ __device__ __forceinline__ uint64_t scan_row_chunks(const float* __restrict__ mr
     for (int a = 0; a + 1 < kAhead; ++a) pf[a] = pf[a + 1];
     {
       const int bn = (c + kAhead * c_step) * kWave + lane;
-      pf[kAhead - 1] = bn < nscan ? mrow[bn] : 0.f;
+      pf[kAhead - 1] = bn < nscan ? load(bn) : 0.f;
     }
     const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
-    uint64_t pass = __ballot(v > tau);
-    if (pass == 0) continue;
-    if (__popcll(pass) <= kSmallInsert) {
-      while (pass) {
-        const int src = __ffsll(static_cast<unsigned long long>(pass)) - 1;
-        pass &= pass - 1;
-        const uint64_t xk = readlane_u64(v, src);
-        const int rnk = __popcll(__ballot(list > xk));
-        const uint64_t prev = lane_shr1_u64(list, list);
-        list = lane < rnk ? list : (lane == rnk ? xk : prev);
-      }
-    } else {
-      const uint64_t vs = wave_sort_desc_u64(v);
-      const uint64_t rev = shfl_u64(vs, kWave - 1 - lane);
-      list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+    tau = insert_keys(v, tau, K1, list);
+  }
+  return list;
+}
+
+// The same selection with chunk maxima: chunk c of the row (scores
+// 64c .. 64c+63) has maximum cm(c).  The K1-th largest chunk maximum t0 is a
+// lower bound of the row's K1-th best score (K1 distinct chunks each hold a
+// score >= t0), so chunks with maximum below t0 are skipped and scores below
+// t0 are never ranked.
+template <typename Load, typename LoadCm>
+__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int nscan, int K1) {
+  const int lane = lane_id();
+  const int nchunk = (nscan + kWave - 1) / kWave;
+  if (K1 <= 0 || nchunk <= K1) return scan_row_chunks(load, nscan, K1, 0, 1);
+  const uint64_t t0key = readlane_u64(scan_row_chunks(cm, nchunk, K1, 0, 1), K1 - 1);
+  const uint32_t o0 = static_cast<uint32_t>(t0key >> 32);     // ordered score of t0
+  // keys above floor_key have scores >= t0 (o0 > 0 for every non-NaN score)
+  const uint64_t floor_key = o0 > 0 ? (static_cast<uint64_t>(o0) << 32) - 1 : 0ull;
+
+  int g = 0;
+  uint64_t mask = 0;
+  bool more = true;
+  // next chunk whose maximum reaches t0 (wave-uniform), or -1
+  auto next_chunk = [&]() -> int {
+    while (mask == 0) {
+      if (!more) return -1;
+      const int c = kWave * g + lane;
+      mask = __ballot(c < nchunk && ordered_u32(cm(c)) >= o0);
+      ++g;
+      more = kWave * g < nchunk;
     }
-    tau = readlane_u64(list, K1 - 1);
+    const int j = __ffsll(static_cast<unsigned long long>(mask)) - 1;
+    mask &= mask - 1;
+    return kWave * (g - 1) + j;
+  };
+  uint64_t list = 0;
+  uint64_t tau = floor_key;
+  constexpr int kAhead = 4;
+  int cs[kAhead];
+  float pf[kAhead];
+#pragma unroll
+  for (int a = 0; a < kAhead; ++a) {
+    cs[a] = next_chunk();
+    const int b = cs[a] * kWave + lane;
+    pf[a] = (cs[a] >= 0 && b < nscan) ? load(b) : 0.f;
+  }
+  while (cs[0] >= 0) {
+    const int b = cs[0] * kWave + lane;
+    const float x = pf[0];
+#pragma unroll
+    for (int a = 0; a + 1 < kAhead; ++a) {
+      cs[a] = cs[a + 1];
+      pf[a] = pf[a + 1];
+    }
+    cs[kAhead - 1] = next_chunk();
+    {
+      const int bn = cs[kAhead - 1] * kWave + lane;
+      pf[kAhead - 1] = (cs[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
+    }
+    const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
+    tau = insert_keys(v, tau, K1, list);
+    if (tau < floor_key) tau = floor_key;
   }
   return list;
 }
@@ -471,6 +551,7 @@ struct RowTask {
   int lb, nscan;
   int32_t* out;
   const float* mrow;
+  int64_t slot;         // the row's index in the chunk's score rows
   bool no_position;
 };
 
@@ -500,13 +581,16 @@ __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64
   t.lb = p / BK;
   t.nscan = min(t.lb, static_cast<int>(ldm));      // == lb whenever kv_lens respect max_kv_len
   t.mrow = M + slot * ldm;
+  t.slot = slot;
   return t;
 }
 
-// One wave per index row.
+// One wave per index row.  With chunk maxima (CM[chunk][row], row stride
+// cm_stride) the row is ranked by the pruned scan.
 __global__ __launch_bounds__(256) void index_topk_kernel(
-    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
-    int qr, int U, int rpu, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+    const float* __restrict__ M, int64_t ldm, const float* __restrict__ CM, int64_t cm_stride, msa_seqs sq,
+    const int32_t* __restrict__ unit_off, int H_kv, int qr, int U, int rpu, int64_t u0, int64_t u1, int BK,
+    int topk, int32_t* __restrict__ block_ids) {
   const int lane = lane_id();
   const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
   if (task >= (u1 - u0) * rpu) return;
@@ -516,7 +600,16 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
     if (lane < topk) t.out[lane] = -1;
     return;
   }
-  const uint64_t list = scan_row_chunks(t.mrow, t.nscan, topk - 1, 0, 1);
+  const float* mrow = t.mrow;
+  auto load = [=](int b) { return mrow[b]; };
+  uint64_t list;
+  if (CM) {
+    const float* cmrow = CM + t.slot;
+    auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
+    list = scan_row_pruned(load, cm, t.nscan, topk - 1);
+  } else {
+    list = scan_row_chunks(load, t.nscan, topk - 1, 0, 1);
+  }
   finish_row(list, topk - 1, t.lb, topk, t.out);
 }
 
@@ -537,7 +630,8 @@ __global__ __launch_bounds__(256) void index_topk_split_kernel(
     return;
   }
   const int K1 = topk - 1;
-  lists[w][lane] = scan_row_chunks(t.mrow, t.nscan, K1, w, kWaves);
+  const float* mrow = t.mrow;
+  lists[w][lane] = scan_row_chunks([=](int b) { return mrow[b]; }, t.nscan, K1, w, kWaves);
   __syncthreads();
   if (w != 0) return;
   uint64_t list = lists[0][lane];
@@ -556,8 +650,9 @@ struct IndexPlan {
   bool narrow;          // U = 1 with at most 16 index rows per row group
   int64_t max_units;    // upper bound of the units over all sequences
   int bcap;             // M row length (key blocks, multiple of 4)
+  int cmcap;            // chunk maxima per row (64-block Top-k chunks; U = 4 only, else 0)
   size_t hdr_bytes;
-  size_t unit_bytes;    // M bytes per unit
+  size_t unit_bytes;    // M and chunk-maximum bytes per unit
 };
 
 int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, IndexPlan* pl) {
@@ -577,12 +672,13 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   int nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
-  pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * pl->bcap * sizeof(float);
+  pl->cmcap = pl->U == kWaves ? (pl->bcap + kWave - 1) / kWave : 0;
+  pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * (pl->bcap + pl->cmcap) * sizeof(float);
   return MSA_OK;
 }
 
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
-constexpr int64_t kSplitTopkRows = 16384;                // fewer index rows: 4 waves per row
+constexpr int64_t kSplitTopkRows = 4096;                 // fewer index rows: 4 waves per row
 
 // Blocks in flight per wave of the narrow kernel: about 128 VGPRs of K_idx.
 template <int D, int B>
@@ -590,10 +686,11 @@ constexpr int kNarrowDepth = D * B <= 64 * 64 ? 4 : 2;
 
 template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
-                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M) {
+                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
+                   float* CM, int64_t cm_stride) {
   if (pl.U == kWaves)
-    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
-                       pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream,
+                     iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM, cm_stride);
   else if (pl.narrow)
     msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
                        ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
@@ -629,6 +726,9 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
 
   int32_t* unit_off = static_cast<int32_t*>(workspace);
   float* M = reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.hdr_bytes);
+  // chunk maxima CM[chunk][row] follow the chunk's score rows
+  const int64_t cm_stride = chunk * pl.U * kWave;
+  float* CM = pl.cmcap > 0 ? M + cm_stride * pl.bcap : nullptr;
   const msa_seqs sq = *seqs;
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
@@ -643,13 +743,13 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
                                      : dim3(static_cast<unsigned>((nslice + kWaves - 1) / kWaves),
                                             static_cast<unsigned>(u1 - u0));
     if (d_idx == 64 && block_size == 64)
-      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
+      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
     else if (d_idx == 64)
-      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
+      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
     else if (block_size == 64)
-      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
+      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
     else
-      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M);
+      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
     // index rows a unit can hold: its query rows (<= U * qr, <= max_q_rows) x H_kv
     const int rpu = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(pl.U) * pl.qr, seqs->max_q_rows)) *
                     num_kv_heads;
@@ -659,9 +759,9 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
                          static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
                          block_size, topk, block_ids);
     else
-      msa_prof::launch("index_topk_kernel", index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)), dim3(256), 0,
-                         stream, M, static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0,
-                         u1, block_size, topk, block_ids);
+      msa_prof::launch("index_topk_kernel", index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)),
+                       dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), static_cast<const float*>(CM), cm_stride,
+                       sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1, block_size, topk, block_ids);
   }
   return msa_host::launch_status();
 }

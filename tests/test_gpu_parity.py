@@ -51,6 +51,11 @@ SMALL = [
     ("planted_k16", [4096], [4096], 16, 8, 64, 64, 16, None, 6),
     # one reverse-index CTA covers 3 x 6250 key blocks: more than its LDS histogram holds
     ("wide_block_range", [100, 100, 100], [400000, 400000, 400000], 4, 1, 64, 64, 8, None, 0),
+    # rows with more 64-block chunks than k-1: Top-k skips chunks below the
+    # (k-1)-th largest chunk maximum
+    ("pruned_topk_long_ctx", [300, 200], [100000, 60000], 4, 2, 64, 64, 8, None, 0),
+    ("pruned_topk_k2", [150], [40000], 4, 2, 64, 64, 2, None, 0),
+    ("pruned_topk_planted", [300], [70000], 8, 2, 64, 64, 12, None, 4),
 ]
 
 
