@@ -12,6 +12,7 @@
  *   msa_index_topk           Index Branch: block scores + Top-k (prefill and decode)
  *   msa_sparse_attn_prefill  Main Branch for many query rows per sequence
  *   msa_sparse_attn_decode   Main Branch for one query row per sequence
+ *   msa_dense_attn           dense causal GQA attention (the comparison baseline)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -150,6 +151,32 @@ int msa_sparse_attn_decode(const void* q, const void* k, const void* v,
                            int num_kv_heads, int head_dim, int block_size, int topk,
                            float softmax_scale, void* o, float* lse, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * msa_dense_attn -- dense causal GQA attention, the baseline MSA is measured
+ * against (no block selection).
+ *
+ * Every query row attends to all keys of its sequence at positions <= p: the
+ * softmax attention that the sparse-attention equation of Sec. 3.1 becomes
+ * when the selected set covers every causal block (Sec. 2.2, full attention
+ * with GQA sharing of K and V across the G query heads of a group).
+ *
+ * Arguments, layouts, ownership, outputs and errors are those of
+ * msa_sparse_attn_prefill without block ids: q [total_q_rows, H_q, 128],
+ * k and v [total_kv_rows, H_kv, 128] (bf16), o [total_q_rows, H_q, 128] bf16,
+ * lse [total_q_rows, H_q] fp32 natural log (-inf for rows with no visible
+ * key).  Sequences with at most 4 query rows (decode) run a split row kernel
+ * whose partials need the workspace; longer ones run a FlashAttention-style
+ * tiled kernel that needs only a small table.
+ *
+ * Supported: head_dim == 128; 1 <= num_q_heads / num_kv_heads <= 16;
+ * num_kv_heads <= 64.
+ * ------------------------------------------------------------------------ */
+size_t msa_dense_attn_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                     int head_dim);
+int msa_dense_attn(const void* q, const void* k, const void* v, const msa_seqs* seqs,
+                   int num_q_heads, int num_kv_heads, int head_dim, float softmax_scale, void* o,
+                   float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (a measurement aid; no part of the attention path)

@@ -110,7 +110,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   const uint16_t* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
   const uint16_t* vbase = v + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  // without block ids (dense mode) slot b is key block b
+  const int32_t* ids = block_ids ? block_ids + (row * H_kv + r) * topk : nullptr;
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 acc[kHeadDim / 16];
@@ -119,10 +120,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
 
   const int slot0 = min(topk, (sp * kAttnWaves + wv) * slots_per_wave);
   const int slot1 = min(topk, slot0 + slots_per_wave);
-  // the wave's block ids, one per lane, fetched at once (slots_per_wave <= 64)
-  const int my_b = slot0 + lane < slot1 ? ids[slot0 + lane] : -1;
+  // the wave's block ids, one per lane, fetched at once (slots_per_wave <= 64 with ids)
+  const int my_b = ids && slot0 + lane < slot1 ? ids[slot0 + lane] : -1;
   for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
-    const int b = __builtin_amdgcn_readlane(my_b, slot - slot0);
+    const int b = ids ? __builtin_amdgcn_readlane(my_b, slot - slot0) : slot;
     if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
     const int key0 = b * BK;
     // K (A operands of S^T) and raw V of this block are requested together;
@@ -395,11 +396,41 @@ int run_rows(const void* q, const void* k, const void* v, const int32_t* block_i
   return msa_host::launch_status();
 }
 
+// Dense mode: every key block of the longest sequence is a slot.
+SplitPlan dense_plan(const msa_seqs* seqs, int H_kv) {
+  SplitPlan sp;
+  const int nblk = (seqs->max_kv_len + 63) / 64 > 0 ? (seqs->max_kv_len + 63) / 64 : 1;
+  const int64_t pairs = seqs->total_q_rows * H_kv;
+  const int max_ctas = (nblk + kAttnWaves - 1) / kAttnWaves;
+  int64_t want = pairs > 0 ? (8192 + pairs * kAttnWaves - 1) / (pairs * kAttnWaves) : 1;
+  if (want < 1) want = 1;
+  if (want > max_ctas) want = max_ctas;
+  const int waves = static_cast<int>(want) * kAttnWaves;
+  sp.slots_per_wave = (nblk + waves - 1) / waves;
+  sp.nsplit = (nblk + sp.slots_per_wave * kAttnWaves - 1) / (sp.slots_per_wave * kAttnWaves);
+  return sp;
+}
+
 int check_ptrs(const void* q, const void* k, const void* v, const int32_t* ids, const void* o, const float* lse) {
   return (q && k && v && ids && o && lse) ? MSA_OK : MSA_ERR_INVALID;
 }
 
 }  // namespace
+
+// Dense causal attention of few-row sequences (the baseline call in
+// dense_attn.hip): the row kernel over every key block, B_k = 64.
+size_t msa_rows_dense_workspace_size(const msa_seqs* seqs, int H_q, int H_kv) {
+  return split_workspace(seqs, H_q, dense_plan(seqs, H_kv));
+}
+
+int msa_rows_dense(const void* q, const void* k, const void* v, const msa_seqs* seqs, int H_q, int H_kv,
+                   float scale, void* o, float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const SplitPlan sp = dense_plan(seqs, H_kv);
+  const size_t need = split_workspace(seqs, H_q, sp);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return MSA_ERR_WORKSPACE;
+  const int nblk = (seqs->max_kv_len + 63) / 64 > 0 ? (seqs->max_kv_len + 63) / 64 : 1;
+  return run_rows(q, k, v, nullptr, seqs, H_q, H_kv, 64, nblk, scale, o, lse, sp, workspace, stream);
+}
 
 extern "C" size_t msa_sparse_attn_decode_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
                                                        int head_dim, int block_size, int topk) {

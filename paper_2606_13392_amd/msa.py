@@ -24,6 +24,7 @@ EXPORTS = [
     "msa_index_topk_workspace_size", "msa_index_topk",
     "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
+    "msa_dense_attn_workspace_size", "msa_dense_attn",
     "msa_profile_enable", "msa_profile_reset", "msa_profile_kernel_name", "msa_profile_read",
 ]
 
@@ -65,6 +66,10 @@ def lib() -> ctypes.CDLL:
             fn = getattr(L, f"msa_sparse_attn_{name}")
             fn.argtypes = [P, P, P, P, S, I, I, I, I, I, F, P, P, P, Z, P]
             fn.restype = I
+        L.msa_dense_attn_workspace_size.argtypes = [S, I, I, I]
+        L.msa_dense_attn_workspace_size.restype = Z
+        L.msa_dense_attn.argtypes = [P, P, P, S, I, I, I, F, P, P, P, Z, P]
+        L.msa_dense_attn.restype = I
         L.msa_profile_enable.argtypes = [I]
         L.msa_profile_enable.restype = I
         L.msa_profile_reset.argtypes = []
@@ -213,6 +218,34 @@ def sparse_attn_decode(q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_
                        out=None, lse=None, workspace=None):
     """Decode-shaped variant of sparse_attn_prefill (one query row per sequence)."""
     return _attn("decode", q, k, v, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
+
+
+# ---------------------------------------------------------------- dense baseline
+def dense_attn_workspace_size(seqs: Seqs, num_q_heads: int, num_kv_heads: int, head_dim: int = 128) -> int:
+    return int(lib().msa_dense_attn_workspace_size(seqs.ref(), num_q_heads, num_kv_heads, head_dim))
+
+
+def dense_attn(q, k, v, seqs: Seqs, softmax_scale=None, out=None, lse=None, workspace=None):
+    """Dense causal GQA attention (the baseline): (O bf16 [Tq, H_q, d], LSE fp32 [Tq, H_q])."""
+    Tq, H_q, d_h = q.shape
+    H_kv = k.shape[1]
+    dev = seqs.device
+    _need(q, "q", torch.bfloat16, (seqs.total_q_rows, H_q, d_h), dev)
+    _need(k, "k", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(v, "v", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    if out is None:
+        out = torch.empty((Tq, H_q, d_h), dtype=torch.bfloat16, device=dev)
+    if lse is None:
+        lse = torch.empty((Tq, H_q), dtype=torch.float32, device=dev)
+    _need(out, "o", torch.bfloat16, (Tq, H_q, d_h), dev)
+    _need(lse, "lse", torch.float32, (Tq, H_q), dev)
+    scale = 1.0 / math.sqrt(d_h) if softmax_scale is None else float(softmax_scale)
+    nbytes = dense_attn_workspace_size(seqs, H_q, H_kv, d_h)
+    ws = _workspace(nbytes, dev, workspace)
+    st = lib().msa_dense_attn(_ptr(q), _ptr(k), _ptr(v), seqs.ref(), H_q, H_kv, d_h, scale, _ptr(out), _ptr(lse),
+                              _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, "msa_dense_attn")
+    return out, lse
 
 
 # ---------------------------------------------------------------- kernel timing
