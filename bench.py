@@ -19,7 +19,9 @@ algorithmic bytes or FLOPs per launch (models below) over its average launch
 duration.  ``calls`` gives both calls' times; the attention call's effective
 FLOPs (selected tokens only) over its time is the MFMA utilisation of the
 Main Branch.  ``cpu_baseline`` times the CPU oracle on a bounded sample of
-query rows of the same workload.
+query rows of the same workload.  ``dense_baseline`` times our dense causal
+GQA kernel (msa_dense_attn) on the same inputs: the last rows of the prefill
+(extrapolated to all rows at the measured rate) and the whole decode step.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -132,7 +134,9 @@ def run_prefill(args, dev):
     eff_flops = 4.0 * dh * (H_q // H_kv) * float(toks.sum().item())
     idx_flops = 2.0 * p.d_idx * H_kv * scored_keys
     paper_main = 4.0 * H_q * dh * p.total_q_rows * p.topk * p.block_size
+    dense = dense_prefill_baseline(args, p, d, dev) if not args.no_dense else None
     res = {
+        "dense": dense,
         "workload": p,
         "sec": sec,
         "ms_idx": ms_idx,
@@ -147,6 +151,46 @@ def run_prefill(args, dev):
         "ids": ids,
     }
     return res
+
+
+def dense_prefill_baseline(args, p, d, dev):
+    """Our dense causal GQA kernel (msa_dense_attn) on the same inputs.
+
+    The full causal pass at T = 1M is ~1.8e16 FLOP, so by default only the last
+    ``--dense-rows`` query rows are run (a chunked-prefill layout over the whole
+    context: the most expensive rows) and the full time is extrapolated at the
+    measured TFLOP/s; ``--dense-rows 0`` runs every row."""
+    import torch
+    from paper_2606_13392_amd import msa
+    T = p.total_q_rows
+    S = T if args.dense_rows <= 0 else min(args.dense_rows, T)
+    seqs = msa.Seqs([S], [p.kv_lens[0]], [p.kv_starts[0]], p.total_kv_rows, dev) if p.num_seqs == 1 else None
+    if seqs is None:
+        return None
+    q = d["q"][T - S:]
+    o = torch.empty_like(q)
+    lse = torch.empty((S, p.num_q_heads), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(1, msa.dense_attn_workspace_size(seqs, p.num_q_heads, p.num_kv_heads, p.head_dim)),
+                     dtype=torch.uint8, device=dev)
+    msa.dense_attn(q, d["k"], d["v"], seqs, out=o, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    msa.dense_attn(q, d["k"], d["v"], seqs, out=o, lse=lse, workspace=ws)
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b)
+    L = p.kv_lens[0]
+    pos_sum = lambda lo, hi: (hi - lo) * (lo + hi + 1) / 2.0        # sum of (position + 1) over [lo, hi)
+    slice_flops = 4.0 * p.num_q_heads * p.head_dim * pos_sum(L - S, L)
+    full_flops = 4.0 * p.num_q_heads * p.head_dim * pos_sum(L - T, L)
+    tflops = slice_flops / (ms * 1e-3) / 1e12
+    del o, lse, ws
+    log(f"[bench] dense baseline: {S} rows in {ms:.1f} ms ({tflops:.0f} TFLOP/s)")
+    return {"rows_timed": S, "ms_timed": ms, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS,
+            "flops_full": full_flops, "ms_full": ms * full_flops / slice_flops,
+            "full_is": "measured" if S == T else "extrapolated from the timed rows at the same TFLOP/s"}
 
 
 def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
@@ -175,6 +219,26 @@ def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
     }
 
 
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 counter summary
+    (profiles/hbm_traffic_*.md), or None when there is none for this kernel and
+    workload or the kernel's source has changed since the counters were taken."""
+    import glob
+    import hashlib
+    for f in sorted(glob.glob(os.path.join(ROOT, "profiles", "hbm_traffic_*.md"))):
+        for line in open(f):
+            if not line.startswith("<!-- traffic: "):
+                continue
+            rec = json.loads(line[len("<!-- traffic: "):].rsplit("-->", 1)[0])
+            if rec.get("kernel") != kernel or rec.get("workload") != workload:
+                continue
+            src = os.path.join(ROOT, rec["source"])
+            if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+                return None
+            return float(rec["bytes_per_launch"])
+    return None
+
+
 def roofline_of(pre):
     """Roofline object of the kernel with the largest time per step."""
     kern = pre["kernels"]
@@ -183,7 +247,7 @@ def roofline_of(pre):
     name = max(kern, key=lambda k: kern[k]["ms_per_step"])
     k = kern[name]
     out = {"kernel": name, "ms_per_launch": k["ms_per_launch"], "launches_per_step": k["launches_per_step"],
-           "traffic": None}
+           "traffic": measured_traffic(name, pre["workload"].name)}
     model = pre["models"].get(name)
     if model is None:
         out.update({"bound": None, "achieved": None, "peak": None, "unit": None, "frac": None})
@@ -241,6 +305,20 @@ def run_decode(args, dev):
         t_idx.time(call_index)
         t_att.time(call_attn)
     torch.cuda.synchronize()
+    dense = None
+    if not args.no_dense:
+        ws_d = torch.empty(max(1, msa.dense_attn_workspace_size(seqs, H_q, H_kv, dh)), dtype=torch.uint8, device=dev)
+        msa.dense_attn(d["q"], d["k"], d["v"], seqs, out=o, lse=lse, workspace=ws_d)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.decode_steps):
+            msa.dense_attn(d["q"], d["k"], d["v"], seqs, out=o, lse=lse, workspace=ws_d)
+        torch.cuda.synchronize()
+        dms = (time.perf_counter() - t0) / args.decode_steps * 1e3
+        kv_bytes = 2.0 * float(sum(p.kv_lens)) * H_kv * dh * 2
+        dense = {"ms_per_step": dms, "kv_bytes": kv_bytes, "hbm_gbs": kv_bytes / (dms * 1e-3) / 1e9,
+                 "msa_speedup": dms / (sec * 1e3)}
+        del ws_d
     positions = torch.from_numpy(p.positions()).to(dev)
     toks = attended_tokens(ids, positions, p.block_size)
     scored = index_scored_keys(positions, p.block_size)
@@ -262,6 +340,8 @@ def run_decode(args, dev):
         "hbm_frac": (idx_bytes + att_bytes) / sec / 1e9 / PEAK_HBM_GBS,
         "index_gbs": idx_bytes / (t_idx.mean_ms() * 1e-3) / 1e9,
         "attn_gbs": att_bytes / (t_att.mean_ms() * 1e-3) / 1e9,
+        "dense_baseline": dense,
+        "paper_decode_speedup_h800": 7.6,
     }
     del d
     return out
@@ -317,8 +397,14 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=20)
     ap.add_argument("--decode-warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
-    ap.add_argument("--cpu-sample-rows", type=int, default=48)
+    ap.add_argument("--cpu-sample-rows", type=int, default=160)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
+    ap.add_argument("--calib-copy-gib", type=float, default=0.0,
+                    help="first run one in-place int32 add over this many GiB (reads and writes exactly "
+                         "that much): the reference kernel for scaling HBM byte counters")
+    ap.add_argument("--dense-rows", type=int, default=8192,
+                    help="prefill rows the dense baseline runs (the last ones; 0 = all)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py: this build runs the MSA hot path on one GPU only; --gpus must be 1 "
@@ -333,6 +419,13 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
 
+    if args.calib_copy_gib > 0:
+        x = torch.zeros(int(args.calib_copy_gib * (1 << 30)) // 4, dtype=torch.int32, device=dev)
+        x.add_(1)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration: int32 add_ over {x.numel() * 4} bytes")
+        del x
+        torch.cuda.empty_cache()
     pre = run_prefill(args, dev)
     p = pre["workload"]
     sec = pre["sec"]
@@ -362,6 +455,9 @@ def main():
                                         "tflops": att_tflops, "frac_of_bf16_peak": att_tflops / PEAK_BF16_TFLOPS},
         },
         "kernels": pre["kernels"],
+        "dense_baseline": None if pre["dense"] is None else dict(
+            pre["dense"], msa_attention_speedup=pre["dense"]["ms_full"] / pre["ms_att"],
+            msa_step_speedup=pre["dense"]["ms_full"] / (sec * 1e3), paper_prefill_speedup_h800=14.2),
         "main_branch_flops": {"effective": pre["eff_flops"], "paper_formula_4HqdhNkBk": pre["paper_main_flops"]},
     }
     ids = pre.pop("ids")
