@@ -65,6 +65,16 @@ __global__ __launch_bounds__(256) void dense_tile_offsets_kernel(msa_seqs sq, in
   for (int s = s0; s < s1; ++s) { tile_off[s] = acc; acc += tiles(s); }
 }
 
+// V staging map: thread tid takes 4-key group tid & 15 and 8-dim group
+// 4 (tid / 64) + {0, 2, 1, 3}[(tid / 16) & 3], so each 32-lane half of a wave
+// writes dim groups d and d + 2 of Vt, whose rows start 32 banks apart: the
+// 8-byte transposed stores hit 64 distinct banks.
+__device__ __forceinline__ void dense_v_map(int tid, int& key4, int& dg) {
+  key4 = tid & 15;
+  const int q = (tid >> 4) & 3;
+  dg = 4 * (tid >> 6) + ((q & 1) << 1) + (q >> 1);
+}
+
 // One key block of group r: thread tid loads 4 K pieces (key, 16-byte
 // segment) and 4 V rows of one (4-key group, 8-dim group); keys at or past
 // kv_len read as zero.
@@ -78,7 +88,8 @@ __device__ __forceinline__ void dense_load_block(const uint16_t* __restrict__ kb
     rk[c] = key0 + key < kv_len ? *reinterpret_cast<const u32x4*>(kb + static_cast<int64_t>(key0 + key) * stride + 8 * seg)
                                 : u32x4{0, 0, 0, 0};
   }
-  const int key4 = tid / (kHeadDim / 8), dg = tid % (kHeadDim / 8);
+  int key4, dg;
+  dense_v_map(tid, key4, dg);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int key = key0 + 4 * key4 + j;
@@ -94,7 +105,8 @@ __device__ __forceinline__ void dense_store_block(DenseSmem& sm, int buf, int ti
     const int key = idx / (kHeadDim / 8), seg = idx % (kHeadDim / 8);
     *reinterpret_cast<u32x4*>(&sm.k[buf][key][8 * seg]) = rk[c];
   }
-  const int key4 = tid / (kHeadDim / 8), dg = tid % (kHeadDim / 8);
+  int key4, dg;
+  dense_v_map(tid, key4, dg);
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int w = e >> 1, sh = (e & 1) * 16;
@@ -136,6 +148,8 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
   const int t = t0 + wave * qpw + jq;                     // this lane's query row in the sequence
   const bool valid = n < qpw * G && t < t_end;
   const int p = valid ? g.kv_len - g.q_rows + t : -1;
+  // smallest position among the wave's rows (invalid lanes see every key masked anyway)
+  const int p_wave = g.kv_len - g.q_rows + min(t0 + wave * qpw, t_end - 1);
   const int64_t head_row = (static_cast<int64_t>(g.q_begin) + (valid ? t : t0)) * H_q + static_cast<int64_t>(r) * G + hh;
 
   bf16x8 bq[KS];
@@ -177,35 +191,43 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
                                 acc_s[i]);
     }
     const int key0 = b * kBK;
+    // running max in raw score units (scale_log2 > 0 keeps the order);
+    // only blocks reaching past the wave's first row need the causal mask
+    if (key0 + kBK - 1 > p_wave) {
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int key = key0 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+          acc_s[i][e] = key <= p ? acc_s[i][e] : -INFINITY;
+        }
+    }
     float bmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int key = key0 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
-        float z = acc_s[i][e] * scale_log2;
-        z = key <= p ? z : -INFINITY;
-        acc_s[i][e] = z;
-        bmax = fmaxf(bmax, z);
-      }
+      for (int e = 0; e < 16; ++e) bmax = fmaxf(bmax, acc_s[i][e]);
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
     const float m_new = fmaxf(m_run, bmax);
     const float mm = m_new == -INFINITY ? 0.f : m_new;     // rows with nothing visible yet
-    const float alpha = exp2f(m_run - mm);
+    const float alpha = exp2f((m_run - mm) * scale_log2);
+    const float neg = -mm * scale_log2;
     float lsum = 0.f;
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float pe = exp2f(acc_s[i][e] - mm);
+        const float pe = exp2f(fmaf(acc_s[i][e], scale_log2, neg));
         acc_s[i][e] = pe;
         lsum += pe;
       }
     lsum += __shfl_xor(lsum, 32);
     l_run = l_run * alpha + lsum;
     m_run = m_new;
+    if (__ballot(alpha != 1.f)) {                        // some row's maximum moved
 #pragma unroll
-    for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] *= alpha;
+      for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] *= alpha;
+    }
 
     // P in bf16 as the B operand of O^T = V^T P^T: k-step u covers keys
     // 32(u/2) + 16(u%2) + {4h + e, 8 + 4h + e}, the lane's acc_s[u/2][8(u%2) ..].
@@ -246,7 +268,7 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
       w.y = pack_bf16x2(acc_o[td][4 * e4 + 2] * inv_l, acc_o[td][4 * e4 + 3] * inv_l);
       *reinterpret_cast<uint2*>(orow + 32 * td + 8 * e4) = w;
     }
-  if (h == 0) lse[head_row] = empty ? -INFINITY : (m_run + __log2f(l_run)) * kLn2;
+  if (h == 0) lse[head_row] = empty ? -INFINITY : (m_run * scale_log2 + __log2f(l_run)) * kLn2;
 }
 
 int validate_dense(const msa_seqs* seqs, int H_q, int H_kv, int head_dim) {
