@@ -232,8 +232,13 @@ def measured_traffic(kernel, workload):
             rec = json.loads(line[len("<!-- traffic: "):].rsplit("-->", 1)[0])
             if rec.get("kernel") != kernel or rec.get("workload") != workload:
                 continue
-            src = os.path.join(ROOT, rec["source"])
-            if not os.path.exists(src) or hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+            h = hashlib.sha256()
+            for rel in rec["sources"]:
+                src = os.path.join(ROOT, rel)
+                if not os.path.exists(src):
+                    return None
+                h.update(open(src, "rb").read())
+            if h.hexdigest() != rec["sources_sha256"]:
                 return None
             return float(rec["bytes_per_launch"])
     return None

@@ -71,14 +71,23 @@ struct UnitRows {
   int nq;       // valid query rows in the unit
 };
 
+// Without a unit table (every sequence has at most one row group and U = 1)
+// unit s is sequence s.
 __device__ __forceinline__ UnitRows locate_unit(const msa_seqs& sq, const int32_t* __restrict__ unit_off,
                                                 int64_t uidx, int qr, int U) {
   UnitRows r;
   r.ok = false;
-  if (uidx >= unit_off[sq.num_seqs]) return r;
-  r.s = find_seq_wave(unit_off, sq.num_seqs, uidx);
-  r.g = seq_geom(sq, r.s);
-  r.t0 = static_cast<int>(uidx - unit_off[r.s]) * qr * U;
+  if (!unit_off) {
+    if (uidx >= sq.num_seqs) return r;
+    r.s = static_cast<int>(uidx);
+    r.g = seq_geom(sq, r.s);
+    r.t0 = 0;
+  } else {
+    if (uidx >= unit_off[sq.num_seqs]) return r;
+    r.s = find_seq_wave(unit_off, sq.num_seqs, uidx);
+    r.g = seq_geom(sq, r.s);
+    r.t0 = static_cast<int>(uidx - unit_off[r.s]) * qr * U;
+  }
   r.nq = min(qr * U, r.g.q_rows - r.t0);
   // never touch query rows past the query-side tensors
   const int64_t left = sq.total_q_rows - (static_cast<int64_t>(r.g.q_begin) + r.t0);
@@ -613,34 +622,41 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   finish_row(list, topk - 1, t.lb, topk, t.out);
 }
 
-// Four waves per index row (for few rows): wave w scans chunks w, w+4, ...;
-// the partial lists are merged through LDS.
-__global__ __launch_bounds__(256) void index_topk_split_kernel(
+// kSplitWaves waves per index row (for few rows): wave w scans chunks w,
+// w + kSplitWaves, ...; the partial lists are merged pairwise through LDS in
+// log2(kSplitWaves) steps.
+constexpr int kSplitWaves = 16;
+
+__global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
     const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv,
     int qr, int U, int rpu, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
-  __shared__ uint64_t lists[kWaves][kWave];
+  __shared__ uint64_t lists[kSplitWaves][kWave];
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int64_t task = blockIdx.x;
   if (task >= (u1 - u0) * rpu) return;              // uniform over the CTA
   const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, rpu, u0, task, BK, topk, block_ids);
-  if (!t.ok) return;
+  if (!t.ok) return;                                 // uniform
   if (t.no_position) {
     if (w == 0 && lane < topk) t.out[lane] = -1;
     return;
   }
   const int K1 = topk - 1;
   const float* mrow = t.mrow;
-  lists[w][lane] = scan_row_chunks([=](int b) { return mrow[b]; }, t.nscan, K1, w, kWaves);
-  __syncthreads();
-  if (w != 0) return;
-  uint64_t list = lists[0][lane];
+  uint64_t list = scan_row_chunks([=](int b) { return mrow[b]; }, t.nscan, K1, w, kSplitWaves);
+  lists[w][lane] = list;
+  // step s: wave w (a multiple of 2s) merges in wave w + s's list, written at
+  // the previous step; the barrier orders the steps
 #pragma unroll
-  for (int ww = 1; ww < kWaves; ++ww) {
-    const uint64_t rev = lists[ww][kWave - 1 - lane];   // ascending: bitonic with `list`
-    list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+  for (int s = 1; s < kSplitWaves; s <<= 1) {
+    __syncthreads();
+    if ((w & (2 * s - 1)) == 0) {
+      const uint64_t rev = lists[w + s][kWave - 1 - lane];   // ascending: bitonic with `list`
+      list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+      lists[w][lane] = list;
+    }
   }
-  finish_row(list, K1, t.lb, topk, t.out);
+  if (w == 0) finish_row(list, K1, t.lb, topk, t.out);
 }
 
 // ---------------------------------------------------------------- host side
@@ -648,6 +664,7 @@ struct IndexPlan {
   int qr;
   int U;                // row groups per unit
   bool narrow;          // U = 1 with at most 16 index rows per row group
+  bool seq_units;       // U = 1 and no sequence longer than one row group
   int64_t max_units;    // upper bound of the units over all sequences
   int bcap;             // M row length (key blocks, multiple of 4)
   int cmcap;            // chunk maxima per row (64-block Top-k chunks; U = 4 only, else 0)
@@ -667,8 +684,10 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   // sequences longer than two row groups take the LDS-shared kernel
   pl->U = static_cast<int64_t>(seqs->max_q_rows) > 2 * pl->qr ? kWaves : 1;
   pl->narrow = pl->U == 1 && std::min(pl->qr, seqs->max_q_rows) * H_kv <= 16 && !(d_idx == 128 && BK == 128);
+  // at most one row group per sequence: unit s is sequence s, no unit table
+  pl->seq_units = pl->U == 1 && seqs->max_q_rows <= pl->qr;
   const int64_t max_groups = seqs->total_q_rows / pl->qr + seqs->num_seqs;
-  pl->max_units = max_groups / pl->U + seqs->num_seqs;
+  pl->max_units = pl->seq_units ? seqs->num_seqs : max_groups / pl->U + seqs->num_seqs;
   int nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
@@ -724,7 +743,7 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   int64_t chunk = static_cast<int64_t>((workspace_bytes - pl.hdr_bytes) / pl.unit_bytes);
   if (chunk > pl.max_units) chunk = pl.max_units;
 
-  int32_t* unit_off = static_cast<int32_t*>(workspace);
+  int32_t* unit_off = pl.seq_units ? nullptr : static_cast<int32_t*>(workspace);
   float* M = reinterpret_cast<float*>(static_cast<char*>(workspace) + pl.hdr_bytes);
   // chunk maxima CM[chunk][row] follow the chunk's score rows
   const int64_t cm_stride = chunk * pl.U * kWave;
@@ -733,7 +752,9 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
 
-  msa_prof::launch("unit_offsets_kernel", unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U, unit_off);
+  if (unit_off)
+    msa_prof::launch("unit_offsets_kernel", unit_offsets_kernel, dim3(1), dim3(256), 0, stream, sq, pl.qr, pl.U,
+                     unit_off);
   // per-wave kernel: slices of kSliceBlocks consecutive blocks, 4 per CTA
   const int nslice = (pl.bcap + kSliceBlocks - 1) / kSliceBlocks;
   const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerCta - 1) / kBlocksPerCta);
@@ -755,7 +776,7 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
                     num_kv_heads;
     const int64_t rows = (u1 - u0) * rpu;
     if (rows <= kSplitTopkRows)
-      msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(256), 0, stream, M,
+      msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(64 * kSplitWaves), 0, stream, M,
                          static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
                          block_size, topk, block_ids);
     else

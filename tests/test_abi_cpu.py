@@ -56,11 +56,14 @@ def test_workspace_queries_are_host_only():
     groups = 100 // 32 + 1
     units = groups // 4 + 1
     assert n == 256 + units * 4 * 64 * (4 + 1) * 4
-    # a single row group per sequence: units of one group
+    # at most one row group per sequence: one unit per sequence, no chunk maxima
     s1 = _seqs(num_seqs=4, total_q_rows=4, max_q_rows=1)
     n1 = L.msa_index_topk_workspace_size(ctypes.byref(s1), 2, 64, 64, 8)
-    groups1 = 4 // 32 + 4
-    assert n1 == 256 + (groups1 + 4) * 64 * 4 * 4
+    assert n1 == 256 + 4 * 64 * 4 * 4
+    # two row groups per sequence: units of one group, bounded by the groups
+    s2 = _seqs(num_seqs=2, total_q_rows=100, max_q_rows=50)
+    n2 = L.msa_index_topk_workspace_size(ctypes.byref(s2), 2, 64, 64, 8)
+    assert n2 == 256 + (100 // 32 + 2 + 2) * 64 * 4 * 4
     # partials (bf16 O + fp32 LSE per slot, row, head) and the (row, group, slot) handles
     n = L.msa_sparse_attn_prefill_workspace_size(ctypes.byref(s), 8, 2, 128, 64, 8)
     assert n >= 8 * 100 * 8 * (128 * 2 + 4) + 100 * 2 * 8 * 4

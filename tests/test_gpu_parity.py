@@ -56,6 +56,10 @@ SMALL = [
     ("pruned_topk_long_ctx", [300, 200], [100000, 60000], 4, 2, 64, 64, 8, None, 0),
     ("pruned_topk_k2", [150], [40000], 4, 2, 64, 64, 2, None, 0),
     ("pruned_topk_planted", [300], [70000], 8, 2, 64, 64, 12, None, 4),
+    # at most one row group per sequence: units are sequences (an empty one
+    # included), 16-wave Top-k per row
+    ("seq_units_empty_and_multirow", [1, 0, 1, 3, 2], [500, 300, 4097, 64, 9000], 16, 4, 64, 64, 6, None, 0),
+    ("seq_units_k32_long", [1, 1, 2], [131072, 70000, 20000], 8, 8, 64, 64, 32, 131072, 0),
 ]
 
 
