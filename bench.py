@@ -273,7 +273,7 @@ def roofline_of(pre):
 def run_decode(args, dev):
     import torch
     from paper_2606_13392_amd import msa, synth
-    p = synth.workload("decode_128k")
+    p = synth.workload(args.decode_workload)
     log(f"[bench] generating {p.name}: {p.description}")
     d = synth.generate_torch(p, dev)
     seqs = msa.Seqs.from_problem(p, dev)
@@ -399,6 +399,7 @@ def main():
     ap.add_argument("--steps", type=int, default=3)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="prefill_1m")
+    ap.add_argument("--decode-workload", default="decode_128k")
     ap.add_argument("--decode-steps", type=int, default=20)
     ap.add_argument("--decode-warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")

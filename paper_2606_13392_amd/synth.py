@@ -166,6 +166,16 @@ def workload(name: str) -> Problem:
         return packed_problem(name, [1 << 20], [1 << 20], num_q_heads=64, num_kv_heads=8, topk=64,
                               seed=1004, planted=32,
                               description="prefill T=1048576, 64q/8kv, k=64, 32 planted blocks/group")
+    if name == "prefill_1m_bk128":
+        return packed_problem(name, [1 << 20], [1 << 20], num_q_heads=64, num_kv_heads=4, d_idx=128,
+                              block_size=128, topk=16, seed=1006, planted=8,
+                              description="prefill T=1048576, 64q/4kv, d_idx 128, B_k 128, k=16, "
+                                          "8 planted blocks/group (the paper's deployed shape)")
+    if name == "decode_128k_bk128":
+        return packed_problem(name, [1] * 64, [131072] * 64, num_q_heads=64, num_kv_heads=4, d_idx=128,
+                              block_size=128, topk=16, seed=1007, kv_pad_to=131072,
+                              description="decode 64 seqs x 1 token, context 131072, 64q/4kv, d_idx 128, "
+                                          "B_k 128, k=16 (the paper's deployed shape)")
     if name == "chunked_8x8k":
         ctx = chunked_contexts(1005, 8, 16384, 524288)
         return packed_problem(name, [8192] * 8, [c + 8192 for c in ctx], num_q_heads=64,
@@ -175,6 +185,8 @@ def workload(name: str) -> Problem:
 
 
 WORKLOADS = ["prefill_4k", "prefill_32k", "decode_128k", "prefill_1m", "chunked_8x8k"]
+# the paper's deployed shape (B_k 128, k 16, GQA 16, d_idx 128)
+WORKLOADS_BK128 = ["prefill_1m_bk128", "decode_128k_bk128"]
 
 
 # --------------------------------------------------------------------------

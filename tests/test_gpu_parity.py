@@ -214,19 +214,26 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
     o, l = fn(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
     torch.cuda.synchronize()
     rows = list(range(p.total_q_rows)) if decode else _sample_rows(p, n_rows, seed=p.seed)
-    # the oracle reads the input rows it needs back from the (generated) inputs
-    iq_h = x["index_q"] if x is not None else from_dev_bits(d["index_q"])
-    ik_h = x["index_k"] if x is not None else from_dev_bits(d["index_k"])
-    ids_all = ids.cpu().numpy()
-    ids_gpu = ids_all[rows]
+    # the oracle reads the input rows it needs back from the (generated) inputs;
+    # only sampled rows of the query-side tensors and outputs leave the device
+    rows_t = torch.tensor(rows, dtype=torch.int64, device=dev)
+    if x is not None:
+        iq_h, ik_h = x["index_q"], x["index_k"]
+    else:
+        iq_h = np.zeros(tuple(d["index_q"].shape), dtype=np.uint16)
+        iq_h[rows] = from_dev_bits(d["index_q"][rows_t])
+        ik_h = from_dev_bits(d["index_k"])
+    ids_gpu = ids[rows_t].cpu().numpy()
     ids_ora, gaps = O.select_blocks(iq_h, ik_h, lay, p.block_size, p.topk, rows=rows)
     inputs = {"index_q": iq_h, "index_k": ik_h}
     exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, inputs, lay, p.block_size, p.topk, rows=rows)
     _say(f"  ids exact={exact} ties={ties} over {len(rows)} rows")
     # Main branch on sampled rows, oracle fed with the GPU's (validated) ids
     arows = rows if check_attn_rows is None else rows[::max(1, len(rows) // check_attn_rows)]
-    o_h = o.float().cpu().numpy()
-    l_h = l.cpu().numpy()
+    arows_t = torch.tensor(arows, dtype=torch.int64, device=dev)
+    o_h = o[arows_t].float().cpu().numpy()
+    l_h = l[arows_t].cpu().numpy()
+    ids_a = ids[arows_t].cpu().numpy()
     G = p.group_size
     o_ref = np.zeros((len(arows), p.num_q_heads, p.head_dim))
     l_ref = np.zeros((len(arows), p.num_q_heads))
@@ -235,7 +242,7 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
         kv0 = p.kv_starts[s]
         qb = from_dev_bits(d["q"][r])
         for g in range(p.num_kv_heads):
-            idr = ids_all[r, g]
+            idr = ids_a[i, g]
             toks = O.selected_tokens(idr, pos, p.block_size)
             tt = torch.from_numpy(kv0 + toks).to(dev)
             kb = from_dev_bits(d["k"][tt, g])
@@ -244,8 +251,10 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
                               1.0 / math.sqrt(p.head_dim))
             o_ref[i, g * G:(g + 1) * G] = oo
             l_ref[i, g * G:(g + 1) * G] = ll
-    stats = check_outputs(o_h[arows], l_h[arows], o_ref, l_ref, p.name)
+    stats = check_outputs(o_h, l_h, o_ref, l_ref, p.name)
     _say(f"  O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e} lse {stats[2]:.2e} over {len(arows)} rows")
+    del d, o, l, ids
+    torch.cuda.empty_cache()
 
 
 def test_workload_prefill_32k_sampled():
@@ -258,3 +267,17 @@ def test_workload_decode_128k():
 
 def test_workload_chunked_8x8k_sampled():
     _sampled_workload("chunked_8x8k", 96, gen="torch", check_attn_rows=48)
+
+
+def test_workload_prefill_1m_sampled():
+    # the full 1M-token prefill in the launch configuration bench.py times;
+    # ids and outputs checked on sampled rows (first/last rows and block edges included)
+    _sampled_workload("prefill_1m", 40, gen="torch", check_attn_rows=20)
+
+
+def test_workload_prefill_1m_bk128_sampled():
+    _sampled_workload("prefill_1m_bk128", 40, gen="torch", check_attn_rows=20)
+
+
+def test_workload_decode_128k_bk128():
+    _sampled_workload("decode_128k_bk128", 64, gen="torch")
