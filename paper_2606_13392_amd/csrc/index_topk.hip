@@ -168,7 +168,7 @@ __device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_
 // row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
 // prunes with.
 template <int D_IDX, int BK>
-__global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
+__global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
     int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
@@ -209,20 +209,25 @@ __global__ __launch_bounds__(256, 3) void index_block_max_lds_kernel(
   const int tid = threadIdx.x;
   auto compute = [&](int buf, int kb) {
     if (nvalid == 0) return;
-    f32x16 acc[MT][2];
+    // 64 keys (two 32-key tiles) at a time keep 64 accumulators live for any B_k
+    float bm = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const uint16_t* kr = &sm.k[buf][32 * i + n][h * (D_IDX / 2)];
-      acc[i][0] = f32x16{};
-      acc[i][1] = f32x16{};
+    for (int hk = 0; hk < MT / 2; ++hk) {
+      f32x16 acc[2][2];
 #pragma unroll
-      for (int st = 0; st < KS; ++st) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st));
-        acc[i][0] = mfma32x32x16(a, bq[0][st], acc[i][0]);
-        acc[i][1] = mfma32x32x16(a, bq[1][st], acc[i][1]);
+      for (int i = 0; i < 2; ++i) {
+        const uint16_t* kr = &sm.k[buf][64 * hk + 32 * i + n][h * (D_IDX / 2)];
+        acc[i][0] = f32x16{};
+        acc[i][1] = f32x16{};
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st));
+          acc[i][0] = mfma32x32x16(a, bq[0][st], acc[i][0]);
+          acc[i][1] = mfma32x32x16(a, bq[1][st], acc[i][1]);
+        }
       }
+      bm = fmaxf(bm, block_max_rows<2>(acc));
     }
-    const float bm = block_max_rows<MT>(acc);
     if (kb < lb_lane) cmax = fmaxf(cmax, bm);
     sm.stage[w][lane][kb & (kStageBlocks - 1)] = bm;
     if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
