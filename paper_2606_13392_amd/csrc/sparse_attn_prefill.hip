@@ -31,7 +31,11 @@ using namespace msa;
 
 constexpr int kHeadDim = 128;
 constexpr int kItemQueries = 256;      // queries of one tile per work item
-constexpr int kAttnThreads = 256;      // 4 waves
+constexpr int kAttnThreads = 256;      // 4 waves (B_k 64)
+// waves per attention CTA: B_k 128 stages 88 KB of K / Vt per CTA, so one CTA
+// fills a CU and 8 waves keep 2 per SIMD
+template <int BK>
+constexpr int kvo_waves() { return BK == 128 ? 8 : 4; }
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -257,7 +261,7 @@ template <int BK>
 struct KvoSmem {
   uint16_t k[BK][kHeadDim + 8];     // K block, row-major (+16 B pad per row)
   uint16_t vt[kHeadDim][BK + 4];    // V block transposed (+8 B pad per row)
-  uint16_t ost[4][32][64];          // per wave: one 64-dim half of 32 partial rows (bf16),
+  uint16_t ost[kvo_waves<BK>()][32][64];   // per wave: one 64-dim half of 32 partial rows (bf16),
                                     // 16-byte units XOR-swizzled by row & 7
 };
 
@@ -273,7 +277,7 @@ __device__ __forceinline__ int64_t upper_index(const T* __restrict__ arr, int64_
 }
 
 template <int BK>
-__global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
+__global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_attn_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off,
     const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk,
@@ -318,14 +322,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
     if (tile != staged) {
       const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kAttnThreads) {
+      for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const uint4 x = key0 + key < g.kv_len
                             ? *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg)
                             : make_uint4(0, 0, 0, 0);
         *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = x;
       }
-      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += kAttnThreads) {
+      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
         const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         uint4 rows[4];
 #pragma unroll
@@ -353,7 +357,7 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
 
     // passes of qpw queries x G heads = 32 rows per wave; Q of the next pass is
     // requested before the current pass computes.
-    const int stride = 4 * qpw;
+    const int stride = kvo_waves<BK>() * qpw;
     int c = wave * qpw;
     bf16x8 bq[KS];
     auto load_q = [&](int cc, bf16x8* dst) {
@@ -367,8 +371,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
     };
     if (c < nq) load_q(c, bq);
     for (; c < nq; c += stride) {
+      // B_k 64: the next pass's Q is requested now (unconditional: no wait on it
+      // below); B_k 128 leaves latency to the second wave on the SIMD
       bf16x8 bq_next[KS];
-      load_q(c + stride < nq ? c + stride : c, bq_next);   // unconditional: no wait on it below
+      if constexpr (BK == 64) load_q(c + stride < nq ? c + stride : c, bq_next);
       const int qi = c + jq;
       const bool valid = lane_row && qi < nq;
       const int p = valid ? s_pos[qi] : -1;
@@ -476,8 +482,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void kvo_attn_kernel(
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
       if (valid && h == 0) lse_buf[prow] = empty ? -INFINITY : (mm + __log2f(l)) * kLn2;
+      if constexpr (BK == 64) {
 #pragma unroll
-      for (int st = 0; st < KS; ++st) bq[st] = bq_next[st];
+        for (int st = 0; st < KS; ++st) bq[st] = bq_next[st];
+      } else if (c + stride < nq) {
+        load_q(c + stride, bq);
+      }
     }
   }
 }
@@ -736,7 +746,7 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
                          sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
                          lse_buf);
     else
-      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, kAttnThreads, &ctas128)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
+      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, 64 * kvo_waves<128>(), &ctas128)), dim3(64 * kvo_waves<128>()), 0, stream, qp, kp, vp,
                          sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
                          lse_buf);
     const int64_t pairs = nr * H_kv;
