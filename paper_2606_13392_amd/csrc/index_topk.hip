@@ -96,13 +96,13 @@ __device__ __forceinline__ UnitRows locate_unit(const msa_seqs& sq, const int32_
   return r;
 }
 
-// B operand of S^T = K Q^T for the wave's 64 index rows (two 32-column tiles);
-// lane (n, h) supplies dims h*D/2 + 8*st .. +8 of row 32j + n.
-template <int D_IDX>
+// B operand of S^T = K Q^T for the wave's 32 NJ index rows (NJ 32-column
+// tiles); lane (n, h) supplies dims h*D/2 + 8*st .. +8 of row 32j + n.
+template <int D_IDX, int NJ = 2>
 __device__ __forceinline__ void load_index_rows(const uint16_t* __restrict__ qbase, int nvalid, int n, int h,
-                                                bf16x8 (&bq)[2][D_IDX / 16]) {
+                                                bf16x8 (&bq)[NJ][D_IDX / 16]) {
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < NJ; ++j) {
     const int row = 32 * j + n;
 #pragma unroll
     for (int st = 0; st < D_IDX / 16; ++st)
@@ -114,16 +114,17 @@ __device__ __forceinline__ void load_index_rows(const uint16_t* __restrict__ qba
 // Block max of one key block for the wave's 64 rows from the S^T tiles: each
 // lane holds half of the block's keys for its column; lanes 0-31 then own rows
 // 0-31 and lanes 32-63 rows 32-63.
-template <int MT>
-__device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][2]) {
+// (Column tiles j0, j0 + 1 of wider accumulators: rows 64 (j0 / 2) + lane.)
+template <int MT, int NJ = 2>
+__device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][NJ], int j0 = 0) {
   float pm[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j) {
-    float m = acc[0][j][0];
+    float m = acc[0][j0 + j][0];
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) m = fmaxf(m, acc[i][j][e]);
+      for (int e = 0; e < 16; ++e) m = fmaxf(m, acc[i][j0 + j][e]);
     pm[j] = m;
   }
   auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(pm[0]), __float_as_uint(pm[1]), false, false);
@@ -133,10 +134,10 @@ __device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][2]) {
 // ---------------------------------------------------------------- scores, LDS
 constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
 
-template <int D_IDX, int BK>
+template <int D_IDX, int BK, int RW>
 struct IdxSmem {
   uint16_t k[2][BK][D_IDX + 8];                   // K_idx blocks, row-major, +16 B pad per row
-  float stage[kWaves][kWave][kStageBlocks + 1];    // per wave: 64 rows x 16 block maxima
+  float stage[kWaves][RW][kStageBlocks + 1];       // per wave: RW rows x 16 block maxima
 };
 
 // Cooperative copy of one K_idx block (BK keys x D_IDX dims) through
@@ -166,9 +167,10 @@ __device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_
 
 // Besides M, each CTA writes its 64-block slice's maximum per row (over the
 // row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
-// prunes with.
-template <int D_IDX, int BK>
-__global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_kernel(
+// prunes with.  RW index rows per wave (64 or 128; a unit is 4 RW / 64 row
+// groups): with 128 every K_idx operand read from LDS feeds four MFMAs.
+template <int D_IDX, int BK, int RW>
+__global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
     int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
@@ -177,12 +179,14 @@ __global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_
   constexpr int MT = BK / 32;                           // 32-key M tiles per block
   constexpr int SEGS = D_IDX / 8;                       // 16-byte segments per key row
   constexpr int CH = BK * SEGS / 256;                   // 16-byte loads per thread per block
-  __shared__ IdxSmem<D_IDX, BK> sm;
+  constexpr int NJ = RW / 32;                           // 32-row column tiles per wave
+  constexpr int NP = RW / 64;                           // row groups per wave
+  __shared__ IdxSmem<D_IDX, BK, RW> sm;
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int64_t uidx = u0 + blockIdx.x;
   if (uidx >= u1) return;
-  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, kWaves);
+  UnitRows ur = locate_unit(sq, unit_off, uidx, qr, kWaves * NP);
   if (!ur.ok) return;
   const int p_last = ur.g.kv_len - ur.g.q_rows + ur.t0 + ur.nq - 1;
   if (p_last < 0) return;
@@ -191,45 +195,56 @@ __global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_
   if (kb0 >= kb1) return;                               // uniform over the CTA
 
   const int n = lane & 31, h = lane >> 5;
-  const int wq0 = w * qr;                               // this wave's first query row in the unit
-  const int nvalid = max(0, min(qr, ur.nq - wq0)) * H_kv;
-  bf16x8 bq[2][KS];
-  load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0 + wq0) * H_kv) * D_IDX, nvalid, n,
-                         h, bq);
-  // this wave's 64 rows of M; the block maxima of a 16-block group are staged
+  const int wq0 = w * NP * qr;                          // this wave's first query row in the unit
+  const int nvalid = max(0, min(NP * qr, ur.nq - wq0)) * H_kv;
+  bf16x8 bq[NJ][KS];
+  load_index_rows<D_IDX, NJ>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0 + wq0) * H_kv) * D_IDX, nvalid,
+                             n, h, bq);
+  // this wave's RW rows of M; the block maxima of a 16-block group are staged
   // in LDS and stored as 64-byte row segments (blocks past kb1 in the last
   // group hold stale values that no row reads: they are >= its local block)
-  const int64_t slot0 = (uidx - u0) * (kWaves * kWave) + w * kWave;   // this wave's first row of M
+  const int64_t slot0 = (uidx - u0) * (kWaves * RW) + w * RW;   // this wave's first row of M
   float* mrow0 = M + slot0 * ldm;
-  // candidate blocks of row `lane` end at its local block
-  const int lb_lane = (ur.g.kv_len - ur.g.q_rows + ur.t0 + wq0 + lane / H_kv) / BK;
-  float cmax = -INFINITY;
+  // lane holds rows 64 s + lane; their candidate blocks end at their local blocks
+  int lb_lane[NP];
+  float cmax[NP];
+#pragma unroll
+  for (int sp = 0; sp < NP; ++sp) {
+    lb_lane[sp] = (ur.g.kv_len - ur.g.q_rows + ur.t0 + wq0 + (64 * sp + lane) / H_kv) / BK;
+    cmax[sp] = -INFINITY;
+  }
 
   const uint16_t* kseq = index_k + ur.g.kv_start * D_IDX;
   const int tid = threadIdx.x;
   auto compute = [&](int buf, int kb) {
     if (nvalid == 0) return;
-    // 64 keys (two 32-key tiles) at a time keep 64 accumulators live for any B_k
-    float bm = -INFINITY;
+    // 64 keys (two 32-key tiles) at a time keep 32 NJ accumulators live for any B_k
+    float bm[NP];
+#pragma unroll
+    for (int sp = 0; sp < NP; ++sp) bm[sp] = -INFINITY;
 #pragma unroll
     for (int hk = 0; hk < MT / 2; ++hk) {
-      f32x16 acc[2][2];
+      f32x16 acc[2][NJ];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
         const uint16_t* kr = &sm.k[buf][64 * hk + 32 * i + n][h * (D_IDX / 2)];
-        acc[i][0] = f32x16{};
-        acc[i][1] = f32x16{};
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16{};
 #pragma unroll
         for (int st = 0; st < KS; ++st) {
           const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st));
-          acc[i][0] = mfma32x32x16(a, bq[0][st], acc[i][0]);
-          acc[i][1] = mfma32x32x16(a, bq[1][st], acc[i][1]);
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32x32x16(a, bq[j][st], acc[i][j]);
         }
       }
-      bm = fmaxf(bm, block_max_rows<2>(acc));
+#pragma unroll
+      for (int sp = 0; sp < NP; ++sp) bm[sp] = fmaxf(bm[sp], block_max_rows<2, NJ>(acc, 2 * sp));
     }
-    if (kb < lb_lane) cmax = fmaxf(cmax, bm);
-    sm.stage[w][lane][kb & (kStageBlocks - 1)] = bm;
+#pragma unroll
+    for (int sp = 0; sp < NP; ++sp) {
+      if (kb < lb_lane[sp]) cmax[sp] = fmaxf(cmax[sp], bm[sp]);
+      sm.stage[w][64 * sp + lane][kb & (kStageBlocks - 1)] = bm[sp];
+    }
     if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
       // the wave writes 16 rows x 64 B per store pass (4 lanes per row, 16 B each)
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -237,7 +252,7 @@ __global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_
       const int kbase = kb & ~(kStageBlocks - 1);
       const int qd = lane & 3;
 #pragma unroll
-      for (int pass = 0; pass < 4; ++pass) {
+      for (int pass = 0; pass < RW / 16; ++pass) {
         const int row = 16 * pass + (lane >> 2);
         const int b = kbase + 4 * qd;
         if (row < nvalid && b < ldm) {
@@ -270,7 +285,9 @@ __global__ __launch_bounds__(256, D_IDX == 64 ? 3 : 2) void index_block_max_lds_
     __syncthreads();
   }
   // rows whose local block is at or below kb0 never read this entry
-  if (lane < nvalid) CM[static_cast<int64_t>(blockIdx.y) * cm_stride + slot0 + lane] = cmax;
+#pragma unroll
+  for (int sp = 0; sp < NP; ++sp)
+    if (64 * sp + lane < nvalid) CM[static_cast<int64_t>(blockIdx.y) * cm_stride + slot0 + 64 * sp + lane] = cmax[sp];
 }
 
 // ---------------------------------------------------------------- scores, per wave
@@ -686,8 +703,11 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   if (BK != 64 && BK != 128) return MSA_ERR_UNSUPPORTED;
   if (topk > 64) return MSA_ERR_UNSUPPORTED;
   pl->qr = 64 / H_kv;
-  // sequences longer than two row groups take the LDS-shared kernel
-  pl->U = static_cast<int64_t>(seqs->max_q_rows) > 2 * pl->qr ? kWaves : 1;
+  // sequences longer than two row groups take the LDS-shared kernel: units of
+  // 4 row groups (one per wave), or 8 (two per wave) for d_idx 64 and
+  // sequences longer than four row groups
+  const int64_t mq = seqs->max_q_rows;
+  pl->U = mq > 4 * pl->qr && d_idx == 64 && BK == 64 ? 2 * kWaves : (mq > 2 * pl->qr ? kWaves : 1);
   pl->narrow = pl->U == 1 && std::min(pl->qr, seqs->max_q_rows) * H_kv <= 16 && !(d_idx == 128 && BK == 128);
   // at most one row group per sequence: unit s is sequence s, no unit table
   pl->seq_units = pl->U == 1 && seqs->max_q_rows <= pl->qr;
@@ -696,7 +716,7 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   int nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
-  pl->cmcap = pl->U == kWaves ? (pl->bcap + kWave - 1) / kWave : 0;
+  pl->cmcap = pl->U >= kWaves ? (pl->bcap + kWave - 1) / kWave : 0;
   pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * (pl->bcap + pl->cmcap) * sizeof(float);
   return MSA_OK;
 }
@@ -712,8 +732,16 @@ template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
                    const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
                    float* CM, int64_t cm_stride) {
+  if constexpr (D == 64 && B == 64) {
+    if (pl.U == 2 * kWaves) {
+      msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 128>), grid, dim3(256), 0,
+                       stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
+                       cm_stride);
+      return;
+    }
+  }
   if (pl.U == kWaves)
-    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B>), grid, dim3(256), 0, stream,
+    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 64>), grid, dim3(256), 0, stream,
                      iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM, cm_stride);
   else if (pl.narrow)
     msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
@@ -765,7 +793,7 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   const unsigned ny = static_cast<unsigned>((pl.bcap + kBlocksPerCta - 1) / kBlocksPerCta);
   for (int64_t u0 = 0; u0 < pl.max_units; u0 += chunk) {
     const int64_t u1 = u0 + chunk < pl.max_units ? u0 + chunk : pl.max_units;
-    const dim3 grid = pl.U == kWaves ? dim3(static_cast<unsigned>(u1 - u0), ny)
+    const dim3 grid = pl.U >= kWaves ? dim3(static_cast<unsigned>(u1 - u0), ny)
                                      : dim3(static_cast<unsigned>((nslice + kWaves - 1) / kWaves),
                                             static_cast<unsigned>(u1 - u0));
     if (d_idx == 64 && block_size == 64)
