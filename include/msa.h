@@ -12,6 +12,7 @@
  *   msa_index_topk           Index Branch: block scores + Top-k (prefill and decode)
  *   msa_sparse_attn_prefill  Main Branch for many query rows per sequence
  *   msa_sparse_attn_decode   Main Branch for one query row per sequence
+ *   msa_sparse_attn_*_fp8    Main Branch on e4m3 queries and KV cache
  *   msa_dense_attn           dense causal GQA attention (the comparison baseline)
  *
  * Conventions shared by every call
@@ -151,6 +152,36 @@ int msa_sparse_attn_decode(const void* q, const void* k, const void* v,
                            int num_kv_heads, int head_dim, int block_size, int topk,
                            float softmax_scale, void* o, float* lse, void* workspace,
                            size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * msa_sparse_attn_prefill_fp8 / msa_sparse_attn_decode_fp8 -- the Main Branch
+ * on 8-bit queries and KV cache.
+ *
+ * Sec. 4.2 notes that the kernels also take fp8 inputs, which rescales the IO
+ * volume of the Main Branch.  q, k and v hold OCP 8-bit floating point E4M3
+ * ("e4m3fn": sign, 4 exponent bits with bias 7, 3 mantissa bits; no
+ * infinities; S.1111.111 is NaN) codes, one byte per element, in the layouts
+ * of the bf16 calls.  Element values are code * q_scale, code * k_scale and
+ * code * v_scale (per-tensor fp32 scales, finite and > 0).  The result is the
+ * attention of those values: logits use softmax_scale * q_scale * k_scale and
+ * O is scaled by v_scale.  Block ids, the bf16 O and fp32 LSE outputs, the
+ * workspace (the *_workspace_size queries of the bf16 calls apply), stream and
+ * error behaviour are those of msa_sparse_attn_prefill / _decode; a scale that
+ * is not finite and positive returns MSA_ERR_INVALID.  The kernels widen e4m3
+ * to bf16 exactly on load and compute as the bf16 calls do.
+ * ------------------------------------------------------------------------ */
+int msa_sparse_attn_prefill_fp8(const void* q, const void* k, const void* v, float q_scale,
+                                float k_scale, float v_scale, const int32_t* block_ids,
+                                const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                int head_dim, int block_size, int topk, float softmax_scale,
+                                void* o, float* lse, void* workspace, size_t workspace_bytes,
+                                hipStream_t stream);
+int msa_sparse_attn_decode_fp8(const void* q, const void* k, const void* v, float q_scale,
+                               float k_scale, float v_scale, const int32_t* block_ids,
+                               const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                               int head_dim, int block_size, int topk, float softmax_scale,
+                               void* o, float* lse, void* workspace, size_t workspace_bytes,
+                               hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * msa_dense_attn -- dense causal GQA attention, the baseline MSA is measured

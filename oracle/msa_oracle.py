@@ -4,7 +4,8 @@ TEST INFRASTRUCTURE ONLY.  Only ``tests/``, the package entry's ``smoke()``
 check and the benchmark's CPU-baseline leg may import or run this module.  It
 shares no code with the HIP path (no kernels, helpers, tables or constants)
 and imports nothing from the library package; the inputs it receives are bf16
-bit patterns (numpy ``uint16``) that it decodes itself.
+bit patterns (numpy ``uint16``) or 8-bit E4M3 codes (numpy ``uint8``, Main
+Branch only) that it decodes itself.
 
 What it computes, in the paper's order and notation:
 
@@ -71,6 +72,30 @@ def decode_bf16(bits: np.ndarray) -> np.ndarray:
     """bf16 bit patterns (uint16) -> float64 values (exact)."""
     u32 = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
     return u32.view(np.float32).astype(np.float64)
+
+
+def decode_fp8_e4m3(codes: np.ndarray) -> np.ndarray:
+    """OCP 8-bit floating point E4M3 codes (uint8) -> float64 values (exact).
+
+    Bit 7 is the sign, bits 6..3 the exponent E (bias 7), bits 2..0 the
+    mantissa M: E > 0 gives (-1)^s 2^(E-7) (1 + M/8), E = 0 the subnormals
+    (-1)^s 2^-6 (M/8); the format has no infinities and E = 15, M = 7 is NaN.
+    (Sec. 4.2 notes that the kernels also take fp8 inputs.)"""
+    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+    sign = np.where(c & 0x80, -1.0, 1.0)
+    e = (c >> 3) & 0xF
+    m = (c & 0x7).astype(np.float64)
+    v = np.where(e > 0, np.ldexp(1.0 + m / 8.0, e - 7), np.ldexp(m / 8.0, -6))
+    v = np.where((e == 15) & ((c & 0x7) == 7), np.nan, v)
+    return sign * v
+
+
+def _decoder(fmt: str):
+    if fmt == "bf16":
+        return decode_bf16
+    if fmt == "e4m3":
+        return decode_fp8_e4m3
+    raise ValueError(f"unknown input format {fmt}")
 
 
 class Layout:
@@ -242,12 +267,17 @@ def selected_tokens(block_ids_row: Sequence[int], pos: int, block_size: int) -> 
 def sparse_attention(q_bits, k_bits, v_bits, block_ids: np.ndarray, layout: Layout,
                      block_size: int, scale: Optional[float] = None,
                      rows: Optional[Iterable[int]] = None,
-                     block_ids_are_for_rows: bool = False):
+                     block_ids_are_for_rows: bool = False, fmt: str = "bf16",
+                     input_scales: Tuple[float, float, float] = (1.0, 1.0, 1.0)):
     """O (R, H_q, d_h) and LSE (R, H_q), float64, for the given packed rows.
 
-    q_bits: (Tq, H_q, d_h); k_bits, v_bits: (Tk, H_kv, d_h) uint16.
+    q_bits: (Tq, H_q, d_h); k_bits, v_bits: (Tk, H_kv, d_h): bf16 bit patterns
+    (uint16), or E4M3 codes (uint8) with fmt="e4m3", whose values are the
+    decoded codes times the per-tensor ``input_scales`` (q, k, v).
     block_ids: (Tq, H_kv, k) for all rows, or (R, H_kv, k) aligned with
     ``rows`` when ``block_ids_are_for_rows``.  Head h uses group h // G."""
+    dec = _decoder(fmt)
+    qs, ks, vs = (float(x) for x in input_scales)
     Tq, H_q, d_h = q_bits.shape
     H_kv = k_bits.shape[1]
     G = H_q // H_kv
@@ -259,12 +289,12 @@ def sparse_attention(q_bits, k_bits, v_bits, block_ids: np.ndarray, layout: Layo
     for i, r in enumerate(rows):
         s, pos = layout.locate(r)
         kv0 = layout.kv_starts[s]
-        qf = decode_bf16(q_bits[r])
+        qf = dec(q_bits[r]) * qs
         ids_row = block_ids[i] if block_ids_are_for_rows else block_ids[r]
         for g in range(H_kv):
             toks = selected_tokens(ids_row[g], pos, block_size)
-            keys = decode_bf16(k_bits[kv0 + toks, g])
-            vals = decode_bf16(v_bits[kv0 + toks, g])
+            keys = dec(k_bits[kv0 + toks, g]) * ks
+            vals = dec(v_bits[kv0 + toks, g]) * vs
             O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(
                 qf[g * G:(g + 1) * G], keys, vals, scale)
     return O, L

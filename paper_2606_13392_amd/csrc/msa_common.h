@@ -21,6 +21,22 @@ __device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t* p) {
 }
 __device__ __forceinline__ bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0)); }
 
+// Eight consecutive elements of a bf16 tensor, or of an OCP 8-bit E4M3
+// ("e4m3fn") tensor widened to bf16 (exact: every e4m3 value is a bf16 value;
+// gfx950's v_cvt_scalef32_pk_bf16_fp8 at scale 1 converts two per instruction).
+__device__ __forceinline__ u32x4 ld8_bits(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ u32x4 ld8_bits(const uint8_t* p) {
+  const uint2 r = *reinterpret_cast<const uint2*>(p);
+  u32x4 o;
+  o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, false));
+  o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, true));
+  o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, false));
+  o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, true));
+  return o;
+}
+template <typename T>
+__device__ __forceinline__ bf16x8 ld8(const T* p) { return __builtin_bit_cast(bf16x8, ld8_bits(p)); }
+
 // MFMA 32x32x16 bf16 -> f32.  Lane l supplies row (A) / column (B) l%32 and
 // eight consecutive k of the half l/32; C lane l holds column l%32, rows
 // 8*(r/4) + 4*(l/32) + r%4 for r = 0..15.

@@ -43,8 +43,8 @@ __device__ __forceinline__ void wave_lds_order() {
 
 // V[b*BK .. b*BK+BK) of group r: each lane loads 4 keys x 8 dims per
 // (4-key group, 8-dim group) pair; keys past the sequence's end read as zero.
-template <int BK>
-__device__ __forceinline__ void load_v_raw(const uint16_t* __restrict__ vbase, int64_t row_stride, int key0,
+template <int BK, typename T>
+__device__ __forceinline__ void load_v_raw(const T* __restrict__ vbase, int64_t row_stride, int key0,
                                            int kv_len, u32x4 (&raw)[BK / 16][4]) {
   const int lane = lane_id();
 #pragma unroll
@@ -54,7 +54,7 @@ __device__ __forceinline__ void load_v_raw(const uint16_t* __restrict__ vbase, i
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int key = key0 + 4 * key4 + j;
-      raw[it][j] = key < kv_len ? *reinterpret_cast<const u32x4*>(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
+      raw[it][j] = key < kv_len ? ld8_bits(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
                                 : u32x4{0, 0, 0, 0};
     }
   }
@@ -78,11 +78,13 @@ __device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const u32x4
   }
 }
 
-template <int BK>
+// T: element type of Q, K and V (uint16_t = bf16 bits, uint8_t = e4m3 bits);
+// o_scale multiplies O (the V dequantisation scale for e4m3).
+template <int BK, typename T>
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int topk,
-    int slots_per_wave, float scale_log2, uint16_t* __restrict__ o, float* __restrict__ lse,
+    int slots_per_wave, float scale_log2, float o_scale, uint16_t* __restrict__ o, float* __restrict__ lse,
     float* __restrict__ o_part, float* __restrict__ lse_part) {
   __shared__ __align__(16) AttnSmem<BK> smw[kAttnWaves];
   __shared__ float mls[kAttnWaves][2][16];
@@ -103,13 +105,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   const int n = lane & 15, q4 = lane >> 4;
   // B operand of S^T = K Q^T: head n of the group, dims 32*ks + 8*q4 .. +8.
   bf16x8 bq[kHeadDim / 32];
-  const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + n) * kHeadDim + 8 * q4;
+  const T* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + n) * kHeadDim + 8 * q4;
 #pragma unroll
-  for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = n < G ? ld_bf16x8(qrow + 32 * ks) : zero_bf16x8();
+  for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = n < G ? ld8(qrow + 32 * ks) : zero_bf16x8();
 
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
-  const uint16_t* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
-  const uint16_t* vbase = v + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+  const T* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
+  const T* vbase = v + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim;
   // without block ids (dense mode) slot b is key block b
   const int32_t* ids = block_ids ? block_ids + (row * H_kv + r) * topk : nullptr;
 
@@ -132,12 +134,12 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i) {
       const int key = key0 + 16 * i + n;
-      const uint16_t* kp = kbase + static_cast<int64_t>(key) * kv_stride;
+      const T* kp = kbase + static_cast<int64_t>(key) * kv_stride;
 #pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? ld_bf16x8(kp + 32 * ks) : zero_bf16x8();
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? ld8(kp + 32 * ks) : zero_bf16x8();
     }
     u32x4 vraw[BK / 16][4];
-    load_v_raw<BK>(vbase, kv_stride, key0, g.kv_len, vraw);
+    load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
 
     // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
     f32x4 st[BK / 16];
@@ -257,7 +259,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   }
   const int64_t head_row = row * H_q + static_cast<int64_t>(r) * G + hn;
   const bool empty = !(L > 0.f);
-  const float inv_l = empty ? 0.f : 1.f / L;
+  const float inv_l = empty ? 0.f : o_scale / L;
   const float lse_v = empty ? -INFINITY : (M + __log2f(L)) * kLn2;
   if (nsplit == 1) {
     uint4 wq;
@@ -321,7 +323,8 @@ __global__ __launch_bounds__(256) void combine_kernel(const float* __restrict__ 
 size_t msa_kvo_workspace_size(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk);
 int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
                     int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream);
+                    size_t workspace_bytes, hipStream_t stream, bool fp8, float q_scale, float k_scale,
+                    float v_scale);
 
 namespace {
 
@@ -363,9 +366,12 @@ size_t split_workspace(const msa_seqs* seqs, int H_q, const SplitPlan& sp) {
   return msa_host::align_up(sp.nsplit * hr * kHeadDim * sizeof(float), 256) + sp.nsplit * hr * sizeof(float);
 }
 
+// fp8: Q, K and V are OCP e4m3 with per-tensor scales (logits use
+// scale * q_scale * k_scale, O is multiplied by v_scale); else bf16 (scales 1).
 int run_rows(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
              int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, const SplitPlan& sp,
-             void* workspace, hipStream_t stream) {
+             void* workspace, hipStream_t stream, bool fp8 = false, float q_scale = 1.f, float k_scale = 1.f,
+             float v_scale = 1.f) {
   const int64_t hr = seqs->total_q_rows * H_q;
   float* o_part = nullptr;
   float* lse_part = nullptr;
@@ -375,19 +381,20 @@ int run_rows(const void* q, const void* k, const void* v, const int32_t* block_i
                                         msa_host::align_up(sp.nsplit * static_cast<size_t>(hr) * kHeadDim * sizeof(float), 256));
   }
   const dim3 grid(static_cast<unsigned>(seqs->total_q_rows * H_kv), static_cast<unsigned>(sp.nsplit));
-  const float sl2 = scale * kLog2e;
+  const float sl2 = scale * q_scale * k_scale * kLog2e;
   const msa_seqs sq = *seqs;
-  auto* qp = static_cast<const uint16_t*>(q);
-  auto* kp = static_cast<const uint16_t*>(k);
-  auto* vp = static_cast<const uint16_t*>(v);
   auto* op = static_cast<uint16_t*>(o);
   const dim3 block(64 * kAttnWaves);
-  if (BK == 64)
-    msa_prof::launch("attn_rows_kernel", attn_rows_kernel<64>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
-                       sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
-  else
-    msa_prof::launch("attn_rows_kernel", attn_rows_kernel<128>, grid, block, 0, stream, qp, kp, vp, block_ids, sq, H_q, H_kv, topk,
-                       sp.slots_per_wave, sl2, op, lse, o_part, lse_part);
+  auto launch = [&](auto kernel, auto elem) {
+    using T = decltype(elem);
+    msa_prof::launch("attn_rows_kernel", kernel, grid, block, 0, stream, static_cast<const T*>(q),
+                     static_cast<const T*>(k), static_cast<const T*>(v), block_ids, sq, H_q, H_kv, topk,
+                     sp.slots_per_wave, sl2, v_scale, op, lse, o_part, lse_part);
+  };
+  if (BK == 64 && !fp8) launch(attn_rows_kernel<64, uint16_t>, uint16_t{});
+  else if (BK == 64) launch(attn_rows_kernel<64, uint8_t>, uint8_t{});
+  else if (!fp8) launch(attn_rows_kernel<128, uint16_t>, uint16_t{});
+  else launch(attn_rows_kernel<128, uint8_t>, uint8_t{});
   if (sp.nsplit > 1) {
     const int64_t threads = hr * 16;
     msa_prof::launch("combine_kernel", combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,
@@ -468,7 +475,42 @@ extern "C" int msa_sparse_attn_prefill(const void* q, const void* k, const void*
   if (seqs->total_q_rows == 0) return MSA_OK;
   if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
   return msa_kvo_prefill(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o,
-                         lse, workspace, workspace_bytes, stream);
+                         lse, workspace, workspace_bytes, stream, false, 1.f, 1.f, 1.f);
+}
+
+namespace {
+bool scale_ok(float x) { return x > 0.f && x < 3.0e38f; }   // finite and positive
+}  // namespace
+
+extern "C" int msa_sparse_attn_prefill_fp8(const void* q, const void* k, const void* v, float q_scale,
+                                           float k_scale, float v_scale, const int32_t* block_ids,
+                                           const msa_seqs* seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                                           int block_size, int topk, float softmax_scale, void* o, float* lse,
+                                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (!scale_ok(q_scale) || !scale_ok(k_scale) || !scale_ok(v_scale)) return MSA_ERR_INVALID;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
+  return msa_kvo_prefill(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o,
+                         lse, workspace, workspace_bytes, stream, true, q_scale, k_scale, v_scale);
+}
+
+extern "C" int msa_sparse_attn_decode_fp8(const void* q, const void* k, const void* v, float q_scale,
+                                          float k_scale, float v_scale, const int32_t* block_ids,
+                                          const msa_seqs* seqs, int num_q_heads, int num_kv_heads, int head_dim,
+                                          int block_size, int topk, float softmax_scale, void* o, float* lse,
+                                          void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st = validate_attn(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (!scale_ok(q_scale) || !scale_ok(k_scale) || !scale_ok(v_scale)) return MSA_ERR_INVALID;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if ((st = check_ptrs(q, k, v, block_ids, o, lse)) != MSA_OK) return st;
+  const SplitPlan sp = split_plan(seqs, num_kv_heads, topk);
+  const size_t need = split_workspace(seqs, num_q_heads, sp);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return MSA_ERR_WORKSPACE;
+  return run_rows(q, k, v, block_ids, seqs, num_q_heads, num_kv_heads, block_size, topk, softmax_scale, o, lse,
+                  sp, workspace, stream, true, q_scale, k_scale, v_scale);
 }
 
 extern "C" const char* msa_strerror(int status) {

@@ -31,9 +31,8 @@ using namespace msa;
 
 constexpr int kHeadDim = 128;
 constexpr int kItemQueries = 256;      // queries of one tile per work item
-constexpr int kAttnThreads = 256;      // 4 waves (B_k 64)
-// waves per attention CTA: B_k 128 stages 88 KB of K / Vt per CTA, so one CTA
-// fills a CU and 8 waves keep 2 per SIMD
+// waves per attention CTA: 4 for B_k 64; B_k 128 stages 88 KB of K / Vt per
+// CTA, so one CTA fills a CU and 8 waves keep 2 per SIMD
 template <int BK>
 constexpr int kvo_waves() { return BK == 128 ? 8 : 4; }
 constexpr float kLog2e = 1.4426950408889634f;
@@ -276,12 +275,15 @@ __device__ __forceinline__ int64_t upper_index(const T* __restrict__ arr, int64_
   return lo;
 }
 
-template <int BK>
+// T: element type of Q, K and V (uint16_t = bf16 bits, uint8_t = e4m3 bits);
+// o_scale multiplies the partial O (the V dequantisation scale for e4m3).
+template <int BK, typename T>
 __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_attn_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, msa_seqs sq,
+    const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off,
     const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk,
-    int64_t nbcap, int64_t row0, float scale_log2, uint16_t* __restrict__ o_buf, float* __restrict__ lse_buf) {
+    int64_t nbcap, int64_t row0, float scale_log2, float o_scale, uint16_t* __restrict__ o_buf,
+    float* __restrict__ lse_buf) {
   __shared__ KvoSmem<BK> sm;
   __shared__ int32_t s_row[kItemQueries];     // query row inside the chunk
   __shared__ int32_t s_pos[kItemQueries];     // its absolute position
@@ -320,12 +322,12 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
     }
     if (tile != staged) {
-      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const T* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const T* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const uint4 x = key0 + key < g.kv_len
-                            ? *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg)
+                            ? __builtin_bit_cast(uint4, ld8_bits(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg))
                             : make_uint4(0, 0, 0, 0);
         *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = x;
       }
@@ -336,7 +338,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
         for (int j = 0; j < 4; ++j) {
           const int key = 4 * key4 + j;
           rows[j] = key0 + key < g.kv_len
-                        ? *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg)
+                        ? __builtin_bit_cast(uint4, ld8_bits(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg))
                         : make_uint4(0, 0, 0, 0);
         }
         const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
@@ -365,9 +367,9 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       const bool ok = lane_row && qi < nq;
       const int64_t row = row0 + (ok ? s_row[qi] : 0);
       // k-step st: lane half h supplies dims 16*st + 8h .. +8 (32 contiguous bytes per row per load)
-      const uint16_t* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + 8 * h;
+      const T* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + 8 * h;
 #pragma unroll
-      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld_bf16x8(qrow + 16 * st) : zero_bf16x8();
+      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld8(qrow + 16 * st) : zero_bf16x8();
     };
     if (c < nq) load_q(c, bq);
     for (; c < nq; c += stride) {
@@ -430,7 +432,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
         bp[u] = __builtin_bit_cast(bf16x8, pw);
       }
       const bool empty = !(l > 0.f);
-      const float inv_l = empty ? 0.f : 1.f / l;
+      const float inv_l = empty ? 0.f : o_scale / l;
       // partial slot of this incidence: [row][group][slot][head][d]
       const int64_t prow = valid ? ((static_cast<int64_t>(s_row[qi]) * H_kv + r) * topk + s_slot[qi]) * G + hh : 0;
       // two halves of d (64 dims = 2 tiles each) keep 32 accumulators live
@@ -699,9 +701,29 @@ size_t msa_kvo_workspace_size(const msa_seqs* seqs, int H_q, int H_kv, int BK, i
   return pl.total;
 }
 
+namespace {
+
+template <int BK, typename T>
+void launch_kvo_attn(const void* q, const void* k, const void* v, const msa_seqs& sq, const int64_t* blk_base,
+                     const int32_t* tile_off, const int32_t* item_off, const uint32_t* handles, int H_q, int H_kv,
+                     int topk, int64_t nbcap, int64_t r0, float sl2, float o_scale, uint16_t* o_buf, float* lse_buf,
+                     hipStream_t stream) {
+  static int ctas = 0;
+  constexpr int threads = 64 * kvo_waves<BK>();
+  msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<BK, T>,
+                   dim3(persistent_ctas(kvo_attn_kernel<BK, T>, threads, &ctas)), dim3(threads), 0, stream,
+                   static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), sq, blk_base,
+                   tile_off, item_off, handles, H_q, H_kv, topk, nbcap, r0, sl2, o_scale, o_buf, lse_buf);
+}
+
+}  // namespace
+
+// fp8: Q, K and V are OCP e4m3 with per-tensor scales (logits use
+// scale * q_scale * k_scale, O is multiplied by v_scale); else bf16 (scales 1).
 int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* block_ids, const msa_seqs* seqs,
                     int H_q, int H_kv, int BK, int topk, float scale, void* o, float* lse, void* workspace,
-                    size_t workspace_bytes, hipStream_t stream) {
+                    size_t workspace_bytes, hipStream_t stream, bool fp8, float q_scale, float k_scale,
+                    float v_scale) {
   KvoPlan pl;
   int st = make_kvo_plan(seqs, H_q, H_kv, BK, topk, workspace_bytes, &pl);
   if (st != MSA_OK) return st;
@@ -717,11 +739,8 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
   auto* o_buf = reinterpret_cast<uint16_t*>(ws + pl.off_obuf);
   auto* lse_buf = reinterpret_cast<float*>(ws + pl.off_lse);
   const msa_seqs sq = *seqs;
-  auto* qp = static_cast<const uint16_t*>(q);
-  auto* kp = static_cast<const uint16_t*>(k);
-  auto* vp = static_cast<const uint16_t*>(v);
   auto* op = static_cast<uint16_t*>(o);
-  const float sl2 = scale * kLog2e;
+  const float sl2 = scale * q_scale * k_scale * kLog2e;
 
   msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK, blk_base);
   const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((pl.ntile + 255) / 256, 4096));
@@ -740,15 +759,18 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
                        stream, blk_tot, pl.ntile, tile_off, item_off);
     msa_prof::launch("kvo_fill_kernel", kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base, H_kv, BK,
                        topk, pl.nbcap, r0, nr, tile_off, tpos, handles);
-    static int ctas64 = 0, ctas128 = 0;
-    if (BK == 64)
-      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<64>, dim3(persistent_ctas(kvo_attn_kernel<64>, kAttnThreads, &ctas64)), dim3(kAttnThreads), 0, stream, qp, kp, vp,
-                         sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
-                         lse_buf);
+    if (BK == 64 && !fp8)
+      launch_kvo_attn<64, uint16_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0,
+                                    sl2, v_scale, o_buf, lse_buf, stream);
+    else if (BK == 64)
+      launch_kvo_attn<64, uint8_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0,
+                                   sl2, v_scale, o_buf, lse_buf, stream);
+    else if (!fp8)
+      launch_kvo_attn<128, uint16_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap,
+                                     r0, sl2, v_scale, o_buf, lse_buf, stream);
     else
-      msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<128>, dim3(persistent_ctas(kvo_attn_kernel<128>, 64 * kvo_waves<128>(), &ctas128)), dim3(64 * kvo_waves<128>()), 0, stream, qp, kp, vp,
-                         sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0, sl2, o_buf,
-                         lse_buf);
+      launch_kvo_attn<128, uint8_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap,
+                                    r0, sl2, v_scale, o_buf, lse_buf, stream);
     const int64_t pairs = nr * H_kv;
     msa_prof::launch("kvo_combine_kernel", kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
                        dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,

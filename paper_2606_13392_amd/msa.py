@@ -24,6 +24,7 @@ EXPORTS = [
     "msa_index_topk_workspace_size", "msa_index_topk",
     "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
+    "msa_sparse_attn_prefill_fp8", "msa_sparse_attn_decode_fp8",
     "msa_dense_attn_workspace_size", "msa_dense_attn",
     "msa_profile_enable", "msa_profile_reset", "msa_profile_kernel_name", "msa_profile_read",
 ]
@@ -65,6 +66,10 @@ def lib() -> ctypes.CDLL:
             ws.restype = Z
             fn = getattr(L, f"msa_sparse_attn_{name}")
             fn.argtypes = [P, P, P, P, S, I, I, I, I, I, F, P, P, P, Z, P]
+            fn.restype = I
+        for name in ("prefill", "decode"):
+            fn = getattr(L, f"msa_sparse_attn_{name}_fp8")
+            fn.argtypes = [P, P, P, F, F, F, P, S, I, I, I, I, I, F, P, P, P, Z, P]
             fn.restype = I
         L.msa_dense_attn_workspace_size.argtypes = [S, I, I, I]
         L.msa_dense_attn_workspace_size.restype = Z
@@ -218,6 +223,45 @@ def sparse_attn_decode(q, k, v, block_ids, seqs: Seqs, block_size: int, softmax_
                        out=None, lse=None, workspace=None):
     """Decode-shaped variant of sparse_attn_prefill (one query row per sequence)."""
     return _attn("decode", q, k, v, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
+
+
+def _attn_fp8(kind: str, q, k, v, scales, block_ids, seqs: Seqs, block_size: int, softmax_scale, out, lse,
+              workspace):
+    Tq, H_q, d_h = q.shape
+    H_kv = k.shape[1]
+    topk = block_ids.shape[2]
+    dev = seqs.device
+    _need(q, "q", torch.uint8, (seqs.total_q_rows, H_q, d_h), dev)
+    _need(k, "k", torch.uint8, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(v, "v", torch.uint8, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(block_ids, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    if out is None:
+        out = torch.empty((Tq, H_q, d_h), dtype=torch.bfloat16, device=dev)
+    if lse is None:
+        lse = torch.empty((Tq, H_q), dtype=torch.float32, device=dev)
+    _need(out, "o", torch.bfloat16, (Tq, H_q, d_h), dev)
+    _need(lse, "lse", torch.float32, (Tq, H_q), dev)
+    scale = 1.0 / math.sqrt(d_h) if softmax_scale is None else float(softmax_scale)
+    L = lib()
+    nbytes = int(getattr(L, f"msa_sparse_attn_{kind}_workspace_size")(seqs.ref(), H_q, H_kv, d_h, block_size, topk))
+    ws = _workspace(nbytes, dev, workspace)
+    qs, ks, vs = (float(x) for x in scales)
+    st = getattr(L, f"msa_sparse_attn_{kind}_fp8")(
+        _ptr(q), _ptr(k), _ptr(v), qs, ks, vs, _ptr(block_ids), seqs.ref(), H_q, H_kv, d_h, block_size, topk, scale,
+        _ptr(out), _ptr(lse), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, f"msa_sparse_attn_{kind}_fp8")
+    return out, lse
+
+
+def sparse_attn_prefill_fp8(q, k, v, scales, block_ids, seqs: Seqs, block_size: int, softmax_scale=None,
+                            out=None, lse=None, workspace=None):
+    """Main Branch on e4m3 codes (uint8 tensors) with per-tensor scales (q, k, v)."""
+    return _attn_fp8("prefill", q, k, v, scales, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
+
+
+def sparse_attn_decode_fp8(q, k, v, scales, block_ids, seqs: Seqs, block_size: int, softmax_scale=None,
+                           out=None, lse=None, workspace=None):
+    return _attn_fp8("decode", q, k, v, scales, block_ids, seqs, block_size, softmax_scale, out, lse, workspace)
 
 
 # ---------------------------------------------------------------- dense baseline

@@ -270,24 +270,58 @@ def generate_numpy(p: Problem) -> Dict[str, np.ndarray]:
 
 
 # --------------------------------------------------------------------------
+# 8-bit E4M3 inputs for the Main Branch
+# --------------------------------------------------------------------------
+# Per-tensor scales of the e4m3 workloads: N(0,1) / 2^-4 keeps |code value| <=
+# ~100, well inside e4m3's +-448 range.
+FP8_SCALES = (2.0 ** -4, 2.0 ** -4, 2.0 ** -4)
+
+
+def e4m3_codes(x, scale: float):
+    """float32 values (numpy or torch) -> OCP E4M3 codes of x / scale, rounded
+    to nearest even (torch's float8_e4m3fn cast), as uint8 of the same kind."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)) if isinstance(x, np.ndarray) else x
+    codes = (t.float() / scale).to(torch.float8_e4m3fn).view(torch.uint8)
+    return codes.numpy() if isinstance(x, np.ndarray) else codes
+
+
+def generate_fp8_numpy(p: Problem, scales=FP8_SCALES) -> Dict[str, np.ndarray]:
+    """Index tensors as bf16 patterns (as generate_numpy) and q, k, v as E4M3
+    codes (uint8) of the same N(0,1) draws divided by ``scales``."""
+    Tq, Tk = p.total_q_rows, p.total_kv_rows
+    out = {k: v for k, v in generate_numpy(p).items() if k in ("index_q", "index_k")}
+    out["q"] = e4m3_codes(_normal_rows(p.seed, TID_Q, Tq, p.num_q_heads * p.head_dim), scales[0]
+                          ).reshape(Tq, p.num_q_heads, p.head_dim)
+    out["k"] = e4m3_codes(_normal_rows(p.seed, TID_K, Tk, p.num_kv_heads * p.head_dim), scales[1]
+                          ).reshape(Tk, p.num_kv_heads, p.head_dim)
+    out["v"] = e4m3_codes(_normal_rows(p.seed, TID_V, Tk, p.num_kv_heads * p.head_dim), scales[2]
+                          ).reshape(Tk, p.num_kv_heads, p.head_dim)
+    return out
+
+
+# --------------------------------------------------------------------------
 # torch backend (draws on the device; for the large workloads)
 # --------------------------------------------------------------------------
-def generate_torch(p: Problem, device, tensors=("index_q", "index_k", "q", "k", "v")):
+def generate_torch(p: Problem, device, tensors=("index_q", "index_k", "q", "k", "v"), fp8_scales=None):
     """Same distributions and planting recipe, drawn with torch's generator on
-    ``device``.  Returns bf16 torch tensors.  (Values differ from the numpy
-    backend; the oracle reads whatever rows it needs back from these inputs.)"""
+    ``device``.  Returns bf16 torch tensors; with ``fp8_scales`` (q, k, v), q, k
+    and v are E4M3 codes (uint8) of the draws divided by those scales.  (Values
+    differ from the numpy backend; the oracle reads whatever rows it needs back
+    from these inputs.)"""
     import torch
 
-    def draw(tid, shape):
+    def draw(tid, shape, fp8_scale=None):
         g = torch.Generator(device=device)
         g.manual_seed(int(p.seed) * 1000003 + tid)
-        out = torch.empty(shape, dtype=torch.bfloat16, device=device)
+        dtype = torch.bfloat16 if fp8_scale is None else torch.uint8
+        out = torch.empty(shape, dtype=dtype, device=device)
         flat = out.view(shape[0], -1)
         step = max(1, (1 << 27) // max(1, flat.shape[1]))
         for r0 in range(0, shape[0], step):
             r1 = min(shape[0], r0 + step)
-            flat[r0:r1] = torch.randn((r1 - r0, flat.shape[1]), generator=g, device=device,
-                                      dtype=torch.float32).to(torch.bfloat16)
+            x = torch.randn((r1 - r0, flat.shape[1]), generator=g, device=device, dtype=torch.float32)
+            flat[r0:r1] = x.to(torch.bfloat16) if fp8_scale is None else e4m3_codes(x, fp8_scale)
         return out
 
     Tq, Tk = p.total_q_rows, p.total_kv_rows
@@ -309,12 +343,13 @@ def generate_torch(p: Problem, device, tensors=("index_q", "index_k", "q", "k", 
                     ik[base + b * p.block_size: base + (b + 1) * p.block_size] += alpha * u
         out["index_k"] = ik.to(torch.bfloat16)
         del ik
+    fs = (None, None, None) if fp8_scales is None else tuple(fp8_scales)
     if "q" in tensors:
-        out["q"] = draw(TID_Q, (Tq, p.num_q_heads, p.head_dim))
+        out["q"] = draw(TID_Q, (Tq, p.num_q_heads, p.head_dim), fs[0])
     if "k" in tensors:
-        out["k"] = draw(TID_K, (Tk, p.num_kv_heads, p.head_dim))
+        out["k"] = draw(TID_K, (Tk, p.num_kv_heads, p.head_dim), fs[1])
     if "v" in tensors:
-        out["v"] = draw(TID_V, (Tk, p.num_kv_heads, p.head_dim))
+        out["v"] = draw(TID_V, (Tk, p.num_kv_heads, p.head_dim), fs[2])
     if "index_q" not in tensors:
         out.pop("index_q", None)
     return out

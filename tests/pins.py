@@ -308,7 +308,61 @@ def pin_head_permutation(O, seed=19):
     assert np.array_equal(o2, o[:, perm]) and np.array_equal(l2, l[:, perm])
 
 
+def pin_fp8_e4m3_codes(O):
+    """E4M3 decoding against the format's definition (OCP 8-bit floating point:
+    sign, 4 exponent bits with bias 7, 3 mantissa bits, no infinities), and
+    every code against torch's independent float8_e4m3fn decoder."""
+    known = {0x00: 0.0, 0x38: 1.0, 0x40: 2.0, 0xC0: -2.0, 0x30: 0.5, 0x3C: 1.5, 0x34: 0.75,
+             0x7E: 448.0, 0xFE: -448.0, 0x08: 2.0 ** -6, 0x01: 2.0 ** -9, 0x07: 7 * 2.0 ** -9,
+             0x79: 288.0, 0x78: 256.0}
+    codes = np.array(sorted(known), dtype=np.uint8)
+    got = O.decode_fp8_e4m3(codes)
+    assert np.array_equal(got, np.array([known[int(c)] for c in codes]))
+    assert np.isnan(O.decode_fp8_e4m3(np.array([0x7F, 0xFF], dtype=np.uint8))).all()
+    pos = O.decode_fp8_e4m3(np.arange(0x00, 0x7F, dtype=np.uint8))
+    assert (np.diff(pos) > 0).all()                               # codes 0x00..0x7E ascend
+    neg = O.decode_fp8_e4m3(np.arange(0x80, 0xFF, dtype=np.uint8))
+    assert np.array_equal(neg, -pos)                              # sign-magnitude
+    try:
+        import torch
+    except ImportError:
+        return
+    all_codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(all_codes).view(torch.float8_e4m3fn).double().numpy()
+    mine = O.decode_fp8_e4m3(all_codes)
+    assert np.array_equal(np.isnan(ref), np.isnan(mine))
+    ok = ~np.isnan(ref)
+    assert np.array_equal(ref[ok], mine[ok])
+
+
+def pin_fp8_attention_scales(O, seed=23):
+    """Attention on E4M3 inputs with per-tensor scales equals attention on the
+    bf16 patterns of the same values (every scaled E4M3 value below is exact
+    in bf16), and O is linear in the V scale."""
+    rng = np.random.default_rng(seed)
+    T, B, H_q, H_kv, d = 48, 8, 4, 2, 16
+    q8 = rng.integers(0, 0x7F, size=(T, H_q, d)).astype(np.uint8) | (rng.integers(0, 2, (T, H_q, d)) << 7).astype(np.uint8)
+    k8 = rng.integers(0x20, 0x50, size=(T, H_kv, d)).astype(np.uint8) | (rng.integers(0, 2, (T, H_kv, d)) << 7).astype(np.uint8)
+    v8 = rng.integers(0x20, 0x50, size=(T, H_kv, d)).astype(np.uint8) | (rng.integers(0, 2, (T, H_kv, d)) << 7).astype(np.uint8)
+    q8 = np.where((q8 & 0x7F) == 0x7F, q8 & 0xF0, q8).astype(np.uint8)   # no NaN codes
+    scales = (2.0 ** -9, 2.0 ** -3, 2.0 ** 2)
+    ids = np.full((T, H_kv, 3), -1, dtype=np.int32)
+    for p in range(T):
+        ids[p, :, :min(3, p // B + 1)] = np.arange(min(3, p // B + 1))[::-1][:3] if p // B < 3 else [0, 1, p // B]
+    lay = _prefill_layout(O, T)
+    o8, l8 = O.sparse_attention(q8, k8, v8, ids, lay, B, fmt="e4m3", input_scales=scales)
+    qb = _bits(O.decode_fp8_e4m3(q8) * scales[0])
+    kb = _bits(O.decode_fp8_e4m3(k8) * scales[1])
+    vb = _bits(O.decode_fp8_e4m3(v8) * scales[2])
+    assert np.array_equal(_vals(qb), O.decode_fp8_e4m3(q8) * scales[0])   # exact in bf16
+    ob, lb = O.sparse_attention(qb, kb, vb, ids, lay, B)
+    assert np.array_equal(o8, ob) and np.array_equal(l8, lb)
+    o2, l2 = O.sparse_attention(q8, k8, v8, ids, lay, B, fmt="e4m3", input_scales=(scales[0], scales[1], 2 * scales[2]))
+    assert np.allclose(o2, 2 * o8, rtol=1e-14, atol=0) and np.array_equal(l2, l8)
+
+
 ALL_PINS = [pin_flops_ratio, pin_effective_flops_dense, pin_brute_force_selection,
             pin_planted_closed_form, pin_selection_invariants, pin_block_maxima_partial,
             pin_dense_equality, pin_closed_forms, pin_combine,
-            pin_decode_and_chunked_consistency, pin_head_permutation]
+            pin_decode_and_chunked_consistency, pin_head_permutation,
+            pin_fp8_e4m3_codes, pin_fp8_attention_scales]

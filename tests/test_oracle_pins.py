@@ -32,6 +32,11 @@ MUTATIONS = {
     "combine_weight_sign": ("w = np.exp(lse_parts - lse)", "w = np.exp(lse - lse_parts)"),
     "flops_main_factor": ("4.0 * H_q * d_h * N * k * block_size", "2.0 * H_q * d_h * N * k * block_size"),
     "left_aligned_positions": ("return s, self.kv_lens[s] - self.q_rows[s] + t", "return s, t"),
+    "fp8_exponent_bias": ("np.ldexp(1.0 + m / 8.0, e - 7)", "np.ldexp(1.0 + m / 8.0, e - 8)"),
+    "fp8_subnormal_scale": ("np.ldexp(m / 8.0, -6)", "np.ldexp(m / 8.0, -7)"),
+    "fp8_nan_all_top_exponent": ("v = np.where((e == 15) & ((c & 0x7) == 7), np.nan, v)",
+                                 "v = np.where(e == 15, np.nan, v)"),
+    "fp8_v_scale_dropped": ("vals = dec(v_bits[kv0 + toks, g]) * vs", "vals = dec(v_bits[kv0 + toks, g])"),
     "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
                              "O[i, g::H_kv], L[i, g::H_kv] = attend(\n                qf[g::H_kv], keys, vals, scale)"),
 }
