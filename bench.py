@@ -135,7 +135,9 @@ def run_prefill(args, dev):
     idx_flops = 2.0 * p.d_idx * H_kv * scored_keys
     paper_main = 4.0 * H_q * dh * p.total_q_rows * p.topk * p.block_size
     dense = dense_prefill_baseline(args, p, d, dev) if not args.no_dense else None
+    fp8 = prefill_fp8(args, p, seqs, ids, dev) if args.fp8 else None
     res = {
+        "fp8": fp8,
         "dense": dense,
         "workload": p,
         "sec": sec,
@@ -151,6 +153,35 @@ def run_prefill(args, dev):
         "ids": ids,
     }
     return res
+
+
+def prefill_fp8(args, p, seqs, ids, dev):
+    """msa_sparse_attn_prefill_fp8 on E4M3 codes of fresh N(0,1) draws (same
+    shapes, same block ids): the attention call's time and kernels."""
+    import torch
+    from paper_2606_13392_amd import msa, synth
+    x = synth.generate_torch(p, dev, tensors=("q", "k", "v"), fp8_scales=synth.FP8_SCALES)
+    ws = torch.empty(max(1, msa.sparse_attn_prefill_workspace_size(seqs, p.num_q_heads, p.num_kv_heads, p.head_dim,
+                                                                   p.block_size, p.topk)), dtype=torch.uint8, device=dev)
+    o = torch.empty((p.total_q_rows, p.num_q_heads, p.head_dim), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((p.total_q_rows, p.num_q_heads), dtype=torch.float32, device=dev)
+    call = lambda: msa.sparse_attn_prefill_fp8(x["q"], x["k"], x["v"], synth.FP8_SCALES, ids, seqs, p.block_size,
+                                               out=o, lse=lse, workspace=ws)
+    call()
+    torch.cuda.synchronize()
+    msa.profile_reset()
+    msa.profile_enable(True)
+    t = CallTimer()
+    for _ in range(2):
+        t.time(call)
+    torch.cuda.synchronize()
+    msa.profile_enable(False)
+    kern = msa.profile_read()
+    ms = t.mean_ms()
+    del x, ws, o, lse
+    torch.cuda.empty_cache()
+    log(f"[bench] fp8 attention call {ms:.1f} ms")
+    return {"ms_per_call": ms, "kernels_ms_per_call": {k: v[1] / 2 for k, v in kern.items()}}
 
 
 def dense_prefill_baseline(args, p, d, dev):
@@ -310,6 +341,27 @@ def run_decode(args, dev):
         t_idx.time(call_index)
         t_att.time(call_attn)
     torch.cuda.synchronize()
+    fp8 = None
+    if args.fp8:
+        x8 = synth.generate_torch(p, dev, tensors=("q", "k", "v"), fp8_scales=synth.FP8_SCALES)
+
+        def call_attn8():
+            msa.sparse_attn_decode_fp8(x8["q"], x8["k"], x8["v"], synth.FP8_SCALES, ids, seqs, p.block_size,
+                                       out=o, lse=lse, workspace=ws_a)
+
+        for _ in range(args.decode_warmup):
+            call_index()
+            call_attn8()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.decode_steps):
+            call_index()
+            call_attn8()
+        torch.cuda.synchronize()
+        sec8 = (time.perf_counter() - t0) / args.decode_steps
+        del x8
+        torch.cuda.empty_cache()
+        fp8 = {"ms_per_step": sec8 * 1e3, "value": p.total_q_rows / sec8, "unit": "tok/s"}
     dense = None
     if not args.no_dense:
         ws_d = torch.empty(max(1, msa.dense_attn_workspace_size(seqs, H_q, H_kv, dh)), dtype=torch.uint8, device=dev)
@@ -348,6 +400,13 @@ def run_decode(args, dev):
         "dense_baseline": dense,
         "paper_decode_speedup_h800": 7.6,
     }
+    if fp8 is not None:
+        # bytes of the step with 1-byte Q, K, V (index tensors stay bf16)
+        att8 = (float(toks.sum().item()) * dh * 2 + rows * H_q * dh * (1 + 2) + rows * H_q * 4
+                + rows * H_kv * p.topk * 4)
+        fp8.update({"algorithmic_bytes_per_step": idx_bytes + att8,
+                    "hbm_gbs": (idx_bytes + att8) / (fp8["ms_per_step"] * 1e-3) / 1e9})
+        out["fp8"] = fp8
     del d
     return out
 
@@ -406,6 +465,8 @@ def main():
     ap.add_argument("--cpu-sample-rows", type=int, default=160)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
+    ap.add_argument("--fp8", action="store_true",
+                    help="also time the Main Branch on E4M3 Q/K/V (msa_sparse_attn_*_fp8)")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="first run one in-place int32 add over this many GiB (reads and writes exactly "
                          "that much): the reference kernel for scaling HBM byte counters")
@@ -461,6 +522,9 @@ def main():
                                         "tflops": att_tflops, "frac_of_bf16_peak": att_tflops / PEAK_BF16_TFLOPS},
         },
         "kernels": pre["kernels"],
+        "fp8_attention": None if pre["fp8"] is None else dict(
+            pre["fp8"], tflops=pre["eff_flops"] / (pre["fp8"]["ms_per_call"] * 1e-3) / 1e12,
+            frac_of_bf16_peak=pre["eff_flops"] / (pre["fp8"]["ms_per_call"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS),
         "dense_baseline": None if pre["dense"] is None else dict(
             pre["dense"], msa_attention_speedup=pre["dense"]["ms_full"] / pre["ms_att"],
             msa_step_speedup=pre["dense"]["ms_full"] / (sec * 1e3), paper_prefill_speedup_h800=14.2),

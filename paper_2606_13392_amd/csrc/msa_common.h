@@ -21,21 +21,32 @@ __device__ __forceinline__ bf16x8 ld_bf16x8(const uint16_t* p) {
 }
 __device__ __forceinline__ bf16x8 zero_bf16x8() { return __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0)); }
 
-// Eight consecutive elements of a bf16 tensor, or of an OCP 8-bit E4M3
-// ("e4m3fn") tensor widened to bf16 (exact: every e4m3 value is a bf16 value;
-// gfx950's v_cvt_scalef32_pk_bf16_fp8 at scale 1 converts two per instruction).
-__device__ __forceinline__ u32x4 ld8_bits(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ u32x4 ld8_bits(const uint8_t* p) {
-  const uint2 r = *reinterpret_cast<const uint2*>(p);
+// Eight consecutive elements of a bf16 tensor (T = uint16_t) or of an OCP
+// 8-bit E4M3 ("e4m3fn") tensor (T = uint8_t).  Raw<T> holds them as loaded;
+// widen() gives 8 bf16 values (exact for e4m3: every e4m3 value is a bf16
+// value; gfx950's v_cvt_scalef32_pk_bf16_fp8 at scale 1 converts two per
+// instruction).  Kernels load raw under their bounds conditions and widen at
+// the point of use, so no conversion sits inside a branch and forces a wait
+// on the load right after issuing it.
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+template <typename T> struct RawOf;
+template <> struct RawOf<uint16_t> { using type = u32x4; };
+template <> struct RawOf<uint8_t> { using type = u32x2; };
+template <typename T> using Raw = typename RawOf<T>::type;
+
+__device__ __forceinline__ u32x4 load_raw(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ u32x2 load_raw(const uint8_t* p) { return *reinterpret_cast<const u32x2*>(p); }
+__device__ __forceinline__ u32x4 widen(u32x4 r) { return r; }
+__device__ __forceinline__ u32x4 widen(u32x2 r) {
   u32x4 o;
-  o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, false));
-  o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.x, 1.0f, true));
-  o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, false));
-  o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r.y, 1.0f, true));
+  o[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r[0], 1.0f, false));
+  o[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r[0], 1.0f, true));
+  o[2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r[1], 1.0f, false));
+  o[3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(r[1], 1.0f, true));
   return o;
 }
-template <typename T>
-__device__ __forceinline__ bf16x8 ld8(const T* p) { return __builtin_bit_cast(bf16x8, ld8_bits(p)); }
+template <typename R>
+__device__ __forceinline__ bf16x8 widen_bf16x8(R r) { return __builtin_bit_cast(bf16x8, widen(r)); }
 
 // MFMA 32x32x16 bf16 -> f32.  Lane l supplies row (A) / column (B) l%32 and
 // eight consecutive k of the half l/32; C lane l holds column l%32, rows

@@ -45,7 +45,7 @@ __device__ __forceinline__ void wave_lds_order() {
 // (4-key group, 8-dim group) pair; keys past the sequence's end read as zero.
 template <int BK, typename T>
 __device__ __forceinline__ void load_v_raw(const T* __restrict__ vbase, int64_t row_stride, int key0,
-                                           int kv_len, u32x4 (&raw)[BK / 16][4]) {
+                                           int kv_len, Raw<T> (&raw)[BK / 16][4]) {
   const int lane = lane_id();
 #pragma unroll
   for (int it = 0; it < BK / 16; ++it) {
@@ -54,25 +54,27 @@ __device__ __forceinline__ void load_v_raw(const T* __restrict__ vbase, int64_t 
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int key = key0 + 4 * key4 + j;
-      raw[it][j] = key < kv_len ? ld8_bits(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg)
-                                : u32x4{0, 0, 0, 0};
+      raw[it][j] = key < kv_len ? load_raw(vbase + static_cast<int64_t>(key) * row_stride + 8 * dg) : Raw<T>{};
     }
   }
 }
-// ... and stores them transposed into LDS as vt[d][key].
-template <int BK>
-__device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const u32x4 (&raw)[BK / 16][4]) {
+// ... and stores them (widened to bf16) transposed into LDS as vt[d][key].
+template <int BK, typename R>
+__device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const R (&raw_in)[BK / 16][4]) {
   const int lane = lane_id();
 #pragma unroll
   for (int it = 0; it < BK / 16; ++it) {
     const int q = lane + kWave * it;
     const int key4 = q >> 4, dg = q & 15;
+    u32x4 raw[1][4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) raw[0][j] = widen(raw_in[it][j]);
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int w = e >> 1, sh = (e & 1) * 16;
       uint2 x;
-      x.x = ((raw[it][0][w] >> sh) & 0xFFFFu) | (((raw[it][1][w] >> sh) & 0xFFFFu) << 16);
-      x.y = ((raw[it][2][w] >> sh) & 0xFFFFu) | (((raw[it][3][w] >> sh) & 0xFFFFu) << 16);
+      x.x = ((raw[0][0][w] >> sh) & 0xFFFFu) | (((raw[0][1][w] >> sh) & 0xFFFFu) << 16);
+      x.y = ((raw[0][2][w] >> sh) & 0xFFFFu) | (((raw[0][3][w] >> sh) & 0xFFFFu) << 16);
       *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = x;
     }
   }
@@ -107,7 +109,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   bf16x8 bq[kHeadDim / 32];
   const T* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + n) * kHeadDim + 8 * q4;
 #pragma unroll
-  for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = n < G ? ld8(qrow + 32 * ks) : zero_bf16x8();
+  for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = widen_bf16x8(n < G ? load_raw(qrow + 32 * ks) : Raw<T>{});
 
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   const T* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
@@ -130,15 +132,15 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     const int key0 = b * BK;
     // K (A operands of S^T) and raw V of this block are requested together;
     // S^T and the softmax run while V is still in flight.
-    bf16x8 ka[BK / 16][kHeadDim / 32];
+    Raw<T> ka[BK / 16][kHeadDim / 32];
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i) {
       const int key = key0 + 16 * i + n;
       const T* kp = kbase + static_cast<int64_t>(key) * kv_stride;
 #pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? ld8(kp + 32 * ks) : zero_bf16x8();
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? load_raw(kp + 32 * ks) : Raw<T>{};
     }
-    u32x4 vraw[BK / 16][4];
+    Raw<T> vraw[BK / 16][4];
     load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
 
     // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     for (int i = 0; i < BK / 16; ++i) {
       st[i] = f32x4{};
 #pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) st[i] = mfma16x16x32(ka[i][ks], bq[ks], st[i]);
+      for (int ks = 0; ks < kHeadDim / 32; ++ks) st[i] = mfma16x16x32(widen_bf16x8(ka[i][ks]), bq[ks], st[i]);
     }
     // lane (n, q4) holds keys 16i + 4*q4 + e of head n
     float bmax = -INFINITY;

@@ -327,7 +327,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const uint4 x = key0 + key < g.kv_len
-                            ? __builtin_bit_cast(uint4, ld8_bits(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg))
+                            ? __builtin_bit_cast(uint4, widen(load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg)))
                             : make_uint4(0, 0, 0, 0);
         *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = x;
       }
@@ -338,7 +338,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
         for (int j = 0; j < 4; ++j) {
           const int key = 4 * key4 + j;
           rows[j] = key0 + key < g.kv_len
-                        ? __builtin_bit_cast(uint4, ld8_bits(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg))
+                        ? __builtin_bit_cast(uint4, widen(load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg)))
                         : make_uint4(0, 0, 0, 0);
         }
         const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
@@ -361,21 +361,21 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
     // requested before the current pass computes.
     const int stride = kvo_waves<BK>() * qpw;
     int c = wave * qpw;
-    bf16x8 bq[KS];
-    auto load_q = [&](int cc, bf16x8* dst) {
+    Raw<T> bq[KS];                            // raw Q elements, widened at the MFMA
+    auto load_q = [&](int cc, Raw<T>* dst) {
       const int qi = cc + jq;
       const bool ok = lane_row && qi < nq;
       const int64_t row = row0 + (ok ? s_row[qi] : 0);
       // k-step st: lane half h supplies dims 16*st + 8h .. +8 (32 contiguous bytes per row per load)
       const T* qrow = q + (row * H_q + static_cast<int64_t>(r) * G + hh) * kHeadDim + 8 * h;
 #pragma unroll
-      for (int st = 0; st < KS; ++st) dst[st] = ok ? ld8(qrow + 16 * st) : zero_bf16x8();
+      for (int st = 0; st < KS; ++st) dst[st] = ok ? load_raw(qrow + 16 * st) : Raw<T>{};
     };
     if (c < nq) load_q(c, bq);
     for (; c < nq; c += stride) {
       // B_k 64: the next pass's Q is requested now (unconditional: no wait on it
       // below); B_k 128 leaves latency to the second wave on the SIMD
-      bf16x8 bq_next[KS];
+      Raw<T> bq_next[KS];
       if constexpr (BK == 64) load_q(c + stride < nq ? c + stride : c, bq_next);
       const int qi = c + jq;
       const bool valid = lane_row && qi < nq;
@@ -390,7 +390,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
 #pragma unroll
         for (int st = 0; st < KS; ++st)
           acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 16 * st)),
-                                  bq[st], acc_s[i]);
+                                  widen_bf16x8(bq[st]), acc_s[i]);
         __builtin_amdgcn_sched_barrier(0);    // bound how far LDS operand reads are hoisted
       }
       float m = -INFINITY;
