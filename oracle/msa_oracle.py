@@ -23,6 +23,10 @@ What it computes, in the paper's order and notation:
   partials through their log-sum-exps.
 * Dense causal attention (Sec. 2.1, softmax-attention equation) and the FLOP
   model of Sec. 3.3.
+* Training backward (Sec. 3.2 "KL Loss" and "Gradient Detach"; Alg. 1):
+  gradients of the Main Branch output with respect to Q, K and V for a given
+  upstream dO, and the sparse KL loss KL(sg(P) || P_idx) per (query, group)
+  with its gradients with respect to the index query and index key.
 
 Precision: float64 everywhere, with one deliberate exception.  Block
 selection is an integer decision taken from floating point; it is taken on
@@ -56,6 +60,14 @@ Readings of passages the paper leaves open (all used below):
      right-aligned).  The paper does not discuss decode or chunked prefill.
  R9  Index scores take the projected q_idx / k_idx as given (no RoPE on the
      Index Branch is described).
+ R10 KL loss: the teacher P averages the heads' softmax distributions over
+     the same selected-token set the Main Branch attends (its normaliser is
+     the forward's LSE); the loss is the mean over rows and groups of the
+     per-(row, group) KL, so the gradients returned here are those of the sum
+     and a caller scales them by lambda / (N H_kv).  Detach (Sec. 3.2): no
+     gradient reaches Q, K or the teacher.
+ R11 A key row that no query selects gets a zero gradient; so does a (row,
+     group) without visible tokens.
 """
 from __future__ import annotations
 
@@ -365,3 +377,116 @@ def effective_main_flops(block_ids: np.ndarray, positions: np.ndarray, H_q: int,
                 if b >= 0 and b * block_size <= p:
                     total += min((b + 1) * block_size, p + 1) - b * block_size
     return 4.0 * d_h * G * total
+
+
+# --------------------------------------------------------------------------
+# Training backward (Sec. 3.2 "KL Loss", "Gradient Detach"; Alg. 1; Sec. 4.3)
+# --------------------------------------------------------------------------
+def softmax_rows(z: np.ndarray) -> np.ndarray:
+    """Row-wise softmax, float64."""
+    e = np.exp(z - z.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
+
+
+def attend_backward(qh: np.ndarray, keys: np.ndarray, vals: np.ndarray, d_o: np.ndarray, scale: float):
+    """Gradients of sum(d_o * O) for O = softmax(scale qh keys^T) vals.
+
+    qh, d_o: (G, d); keys, vals: (n, d).  Returns dq (G, d), dk (n, d), dv (n, d).
+    The softmax Jacobian applied to dP = d_o vals^T gives, per row,
+    dz_j = p_j (dP_j - sum_u p_u dP_u); z = scale q.k passes scale on."""
+    p = softmax_rows((qh @ keys.T) * scale)      # (G, n)
+    dv = p.T @ d_o
+    dp = d_o @ vals.T                            # (G, n)
+    dz = p * (dp - (p * dp).sum(axis=1, keepdims=True))
+    dq = (dz @ keys) * scale
+    dk = (dz.T @ qh) * scale
+    return dq, dk, dv
+
+
+def sparse_attention_backward(q_bits, k_bits, v_bits, d_o_bits, block_ids: np.ndarray, layout: Layout,
+                              block_size: int, scale: Optional[float] = None):
+    """dQ (Tq, H_q, d_h), dK and dV (Tk, H_kv, d_h), float64: gradients of
+    sum(dO * O) for the Main Branch output O of every packed row (the
+    sparse-attention equation of Sec. 3.1; Alg. 1 trains through it).
+
+    All inputs are bf16 bit patterns; dO (Tq, H_q, d_h).  Key rows that no
+    query attends receive zero gradient."""
+    Tq, H_q, d_h = q_bits.shape
+    H_kv = k_bits.shape[1]
+    G = H_q // H_kv
+    if scale is None:
+        scale = 1.0 / math.sqrt(d_h)
+    dQ = np.zeros((Tq, H_q, d_h))
+    dK = np.zeros((k_bits.shape[0], H_kv, d_h))
+    dV = np.zeros_like(dK)
+    for r in range(Tq):
+        s, pos = layout.locate(r)
+        kv0 = layout.kv_starts[s]
+        qf = decode_bf16(q_bits[r])
+        gf = decode_bf16(d_o_bits[r])
+        for g in range(H_kv):
+            toks = selected_tokens(block_ids[r, g], pos, block_size)
+            if toks.shape[0] == 0:
+                continue
+            heads = slice(g * G, (g + 1) * G)
+            dq, dk, dv = attend_backward(qf[heads], decode_bf16(k_bits[kv0 + toks, g]),
+                                         decode_bf16(v_bits[kv0 + toks, g]), gf[heads], scale)
+            dQ[r, heads] += dq
+            dK[kv0 + toks, g] += dk
+            dV[kv0 + toks, g] += dv
+    return dQ, dK, dV
+
+
+def kl_row(iq_r: np.ndarray, ik_toks: np.ndarray, q_heads: np.ndarray, k_toks: np.ndarray,
+           scale_idx: float, scale_main: float):
+    """KL(sg(P) || P_idx) of one (query, group) over its token set, and the
+    gradients of that value with respect to S_idx, q_idx and the k_idx rows.
+
+    P_idx = softmax(scale_idx q_idx . k_idx) over the tokens; the teacher P is
+    the mean over the group's heads of the per-head Main Branch softmax
+    distributions over the same tokens (the P / P_idx equation of Sec. 3.2).
+    With P detached, d KL / d S_idx_j = P_idx_j - P_j."""
+    s_idx = (ik_toks @ iq_r) * scale_idx                      # (n,)
+    p_idx = softmax_rows(s_idx[None, :])[0]
+    p = softmax_rows((q_heads @ k_toks.T) * scale_main).mean(axis=0)
+    kl = float(np.sum(p * (np.log(p) - np.log(p_idx))))
+    ds = p_idx - p
+    d_iq = (ds @ ik_toks) * scale_idx
+    d_ik = np.outer(ds, iq_r) * scale_idx
+    return kl, d_iq, d_ik
+
+
+def sparse_kl(index_q_bits, index_k_bits, q_bits, k_bits, block_ids: np.ndarray, layout: Layout,
+              block_size: int, scale_idx: Optional[float] = None, scale_main: Optional[float] = None):
+    """Sparse KL loss terms and their gradients for every packed row.
+
+    Returns kl (Tq, H_kv): KL(sg(P^(r)_i) || P_idx^(r)_i) over the causally
+    visible tokens of the selected blocks (Sec. 3.2, KL-loss equation; the
+    loss is their mean over rows and groups), and the gradients of
+    sum_{i,r} kl[i, r] with respect to index_q (Tq, H_kv, d_idx) and
+    index_k (Tk, d_idx).  Under the gradient detach of Sec. 3.2 nothing flows
+    into Q or K.  A (row, group) without visible tokens contributes 0."""
+    Tq, H_kv, d_idx = index_q_bits.shape
+    H_q, d_h = q_bits.shape[1], q_bits.shape[2]
+    G = H_q // H_kv
+    if scale_idx is None:
+        scale_idx = 1.0 / math.sqrt(d_idx)
+    if scale_main is None:
+        scale_main = 1.0 / math.sqrt(d_h)
+    kl = np.zeros((Tq, H_kv))
+    d_iq = np.zeros((Tq, H_kv, d_idx))
+    d_ik = np.zeros((index_k_bits.shape[0], d_idx))
+    for r in range(Tq):
+        s, pos = layout.locate(r)
+        kv0 = layout.kv_starts[s]
+        iq = decode_bf16(index_q_bits[r])
+        qf = decode_bf16(q_bits[r])
+        for g in range(H_kv):
+            toks = selected_tokens(block_ids[r, g], pos, block_size)
+            if toks.shape[0] == 0:
+                continue
+            kl[r, g], d_iq[r, g], dk = kl_row(iq[g], decode_bf16(index_k_bits[kv0 + toks]),
+                                              qf[g * G:(g + 1) * G], decode_bf16(k_bits[kv0 + toks, g]),
+                                              scale_idx, scale_main)
+            d_ik[kv0 + toks] += dk
+    return kl, d_iq, d_ik

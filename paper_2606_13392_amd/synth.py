@@ -29,7 +29,7 @@ import numpy as np
 CHUNK_ROWS = 65536
 
 # tensor ids used to derive independent streams from one seed
-TID_INDEX_Q, TID_INDEX_K, TID_Q, TID_K, TID_V, TID_PLANT, TID_LENS = range(7)
+TID_INDEX_Q, TID_INDEX_K, TID_Q, TID_K, TID_V, TID_PLANT, TID_LENS, TID_DO, TID_BLOCKS = range(9)
 
 
 # --------------------------------------------------------------------------
@@ -350,6 +350,43 @@ def generate_torch(p: Problem, device, tensors=("index_q", "index_k", "q", "k", 
         out["k"] = draw(TID_K, (Tk, p.num_kv_heads, p.head_dim), fs[1])
     if "v" in tensors:
         out["v"] = draw(TID_V, (Tk, p.num_kv_heads, p.head_dim), fs[2])
+    if "d_o" in tensors:
+        out["d_o"] = draw(TID_DO, (Tq, p.num_q_heads, p.head_dim))
     if "index_q" not in tensors:
         out.pop("index_q", None)
     return out
+
+
+# --------------------------------------------------------------------------
+# training-backward inputs
+# --------------------------------------------------------------------------
+def generate_grad_numpy(p: Problem) -> np.ndarray:
+    """Upstream gradient dO of the Main Branch output: N(0,1) rounded to bf16,
+    (Tq, H_q, d_h) uint16 bit patterns.  (Real upstream gradients are smaller;
+    every bar on the backward is relative, and bf16 keeps its relative
+    precision over the whole range used.)"""
+    Tq = p.total_q_rows
+    return bf16_bits_from_f32(_normal_rows(p.seed, TID_DO, Tq, p.num_q_heads * p.head_dim)
+                              ).reshape(Tq, p.num_q_heads, p.head_dim)
+
+
+def random_block_ids(p: Problem, pad_slots: int = 0) -> np.ndarray:
+    """A seeded block selection with the structure of a Top-k output, drawn
+    without looking at any score: per (row, group) the block holding the row's
+    own position plus min(k - 1, lb) distinct earlier blocks chosen uniformly,
+    ascending, padded with -1 to k (+ ``pad_slots`` extra -1 slots).  Rows
+    at a position < 0 get only -1."""
+    rng = np.random.default_rng([p.seed, TID_BLOCKS])
+    k = p.topk
+    ids = np.full((p.total_q_rows, p.num_kv_heads, k + pad_slots), -1, dtype=np.int32)
+    pos = p.positions()
+    for row in range(p.total_q_rows):
+        if pos[row] < 0:
+            continue
+        lb = int(pos[row]) // p.block_size
+        take = min(k - 1, lb)
+        for g in range(p.num_kv_heads):
+            others = rng.choice(lb, size=take, replace=False) if take else np.zeros(0, dtype=np.int64)
+            sel = np.sort(np.concatenate([others, [lb]]))
+            ids[row, g, :sel.shape[0]] = sel
+    return ids

@@ -361,8 +361,194 @@ def pin_fp8_attention_scales(O, seed=23):
     assert np.allclose(o2, 2 * o8, rtol=1e-14, atol=0) and np.array_equal(l2, l8)
 
 
+
+# ---------------------------------------------------------------- training backward
+def _central_diff(f, x, h=1e-6):
+    """Central differences of the scalar f at x (float64 array), elementwise."""
+    g = np.zeros_like(x)
+    it = np.nditer(x, flags=["multi_index"])
+    for _ in it:
+        i = it.multi_index
+        old = x[i]
+        x[i] = old + h
+        fp = f()
+        x[i] = old - h
+        fm = f()
+        x[i] = old
+        g[i] = (fp - fm) / (2 * h)
+    return g
+
+
+def pin_attention_backward_fd(O, seed=29):
+    """attend_backward against central differences of sum(dO * O) computed
+    with the oracle's forward ``attend`` (float64)."""
+    rng = np.random.default_rng(seed)
+    G, n, d, scale = 3, 7, 5, 0.61
+    q = rng.standard_normal((G, d))
+    k = rng.standard_normal((n, d))
+    v = rng.standard_normal((n, d))
+    do = rng.standard_normal((G, d))
+    dq, dk, dv = O.attend_backward(q, k, v, do, scale)
+    loss = lambda: float((O.attend(q, k, v, scale)[0] * do).sum())
+    for got, x in ((dq, q), (dk, k), (dv, v)):
+        want = _central_diff(loss, x)
+        assert np.abs(got - want).max() < 1e-7 * max(1.0, np.abs(want).max()), (got, want)
+
+
+def _masked_sparse_torch(qv, kv, vv, ids, lay, B, scale):
+    """Main Branch via a dense score matrix over each sequence's keys with an
+    explicit selected-and-visible mask and torch.softmax (float64 tensors with
+    autograd).  Returns the (Tq, H_q, d) output."""
+    Tq, H_q, d = qv.shape
+    H_kv = kv.shape[1]
+    G = H_q // H_kv
+    outs = []
+    for r in range(Tq):
+        s, pos = lay.locate(r)
+        kv0, n = lay.kv_starts[s], lay.kv_lens[s]
+        heads = []
+        for h in range(H_q):
+            g = h // G
+            mask = torch.zeros(n, dtype=torch.bool)
+            for b in ids[r, g]:
+                if b >= 0:
+                    mask[b * B:(b + 1) * B] = True
+            mask[pos + 1:] = False
+            z = (kv[kv0:kv0 + n, g] @ qv[r, h]) * scale
+            p = torch.softmax(z.masked_fill(~mask, -math.inf), dim=0)
+            heads.append(p @ vv[kv0:kv0 + n, g])
+        outs.append(torch.stack(heads))
+    return torch.stack(outs)
+
+
+def pin_attention_backward_autograd(O, seed=31):
+    """sparse_attention_backward against torch autograd (float64, CPU) of the
+    masked dense formulation, on chunked and decode rows with GQA and -1
+    padding; key rows nobody selects must get exactly zero."""
+    rng = np.random.default_rng(seed)
+    B, H_q, H_kv, d = 4, 4, 2, 8
+    lay = O.Layout([9, 1, 3], [9, 22, 17], [0, 9, 31])
+    Tq, Tk = 13, 48
+    q = _bits(rng.standard_normal((Tq, H_q, d)))
+    k = _bits(rng.standard_normal((Tk, H_kv, d)))
+    v = _bits(rng.standard_normal((Tk, H_kv, d)))
+    do = _bits(rng.standard_normal((Tq, H_q, d)))
+    ids = np.full((Tq, H_kv, 3), -1, dtype=np.int32)
+    for r in range(Tq):
+        _, pos = lay.locate(r)
+        lb = pos // B
+        for g in range(H_kv):
+            others = rng.choice(lb, size=min(1, lb), replace=False) if lb else []
+            sel = sorted(set(int(x) for x in others) | {lb})
+            ids[r, g, :len(sel)] = sel
+    scale = 1.0 / math.sqrt(d)
+    dQ, dK, dV = O.sparse_attention_backward(q, k, v, do, ids, lay, B, scale)
+    qt, kt, vt = (torch.tensor(_vals(x), requires_grad=True) for x in (q, k, v))
+    out = _masked_sparse_torch(qt, kt, vt, ids, lay, B, scale)
+    (out * torch.from_numpy(_vals(do))).sum().backward()
+    for got, t in ((dQ, qt), (dK, kt), (dV, vt)):
+        assert np.abs(got - t.grad.numpy()).max() < 1e-12, np.abs(got - t.grad.numpy()).max()
+    used = np.zeros((Tk, H_kv), dtype=bool)
+    for r in range(Tq):
+        s, pos = lay.locate(r)
+        for g in range(H_kv):
+            used[lay.kv_starts[s] + O.selected_tokens(ids[r, g], pos, B), g] = True
+    assert np.all(dK[~used] == 0) and np.all(dV[~used] == 0)
+
+
+def pin_kl_fd(O, seed=37):
+    """kl_row's gradients against central differences of its own KL value."""
+    rng = np.random.default_rng(seed)
+    n, d_idx, G, d = 6, 4, 3, 5
+    iq = rng.standard_normal(d_idx)
+    ik = rng.standard_normal((n, d_idx))
+    qh = rng.standard_normal((G, d))
+    kt = rng.standard_normal((n, d))
+    kl, d_iq, d_ik = O.kl_row(iq, ik, qh, kt, 0.5, 0.45)
+    assert kl >= 0
+    f = lambda: O.kl_row(iq, ik, qh, kt, 0.5, 0.45)[0]
+    for got, x in ((d_iq, iq), (d_ik, ik)):
+        want = _central_diff(f, x)
+        assert np.abs(got - want).max() < 1e-7, (got, want)
+
+
+def pin_kl_autograd(O, seed=41):
+    """sparse_kl against torch.nn.functional.kl_div with autograd (float64,
+    CPU): teacher = per-head masked softmax averaged over the group's heads and
+    detached; student = masked log_softmax of the index scores."""
+    rng = np.random.default_rng(seed)
+    B, H_q, H_kv, d, d_idx = 4, 6, 2, 8, 4
+    lay = O.Layout([10, 1], [10, 19], [0, 10])
+    Tq, Tk = 11, 29
+    G = H_q // H_kv
+    iq = _bits(rng.standard_normal((Tq, H_kv, d_idx)))
+    ik = _bits(rng.standard_normal((Tk, d_idx)))
+    q = _bits(rng.standard_normal((Tq, H_q, d)))
+    k = _bits(rng.standard_normal((Tk, H_kv, d)))
+    ids = np.full((Tq, H_kv, 3), -1, dtype=np.int32)
+    for r in range(Tq):
+        _, pos = lay.locate(r)
+        lb = pos // B
+        for g in range(H_kv):
+            others = rng.choice(lb, size=min(2, lb), replace=False) if lb else []
+            sel = sorted(set(int(x) for x in others) | {lb})
+            ids[r, g, :len(sel)] = sel
+    kl, d_iq, d_ik = O.sparse_kl(iq, ik, q, k, ids, lay, B)
+    iqt = torch.tensor(_vals(iq), requires_grad=True)
+    ikt = torch.tensor(_vals(ik), requires_grad=True)
+    qv, kv = torch.from_numpy(_vals(q)), torch.from_numpy(_vals(k))
+    total = 0
+    for r in range(Tq):
+        s, pos = lay.locate(r)
+        kv0, n = lay.kv_starts[s], lay.kv_lens[s]
+        for g in range(H_kv):
+            mask = torch.zeros(n, dtype=torch.bool)
+            for b in ids[r, g]:
+                if b >= 0:
+                    mask[b * B:(b + 1) * B] = True
+            mask[pos + 1:] = False
+            zi = (ikt[kv0:kv0 + n] @ iqt[r, g]) / math.sqrt(d_idx)
+            logp_idx = torch.log_softmax(zi.masked_fill(~mask, -math.inf), dim=0)[mask]
+            zm = (kv[kv0:kv0 + n, g] @ qv[r, g * G:(g + 1) * G].T).T / math.sqrt(d)
+            teacher = torch.softmax(zm.masked_fill(~mask, -math.inf), dim=1).mean(dim=0)[mask].detach()
+            term = torch.nn.functional.kl_div(logp_idx, teacher, reduction="sum")
+            assert abs(float(term.detach()) - kl[r, g]) < 1e-12, (r, g, float(term.detach()), kl[r, g])
+            total = total + term
+    total.backward()
+    assert np.abs(iqt.grad.numpy() - d_iq).max() < 1e-12
+    assert np.abs(ikt.grad.numpy() - d_ik).max() < 1e-12
+
+
+def pin_kl_mixture_closed_form(O):
+    """Teacher averaged at the probability level (Sec. 3.2): with one head at
+    q = 0 (uniform over the n visible tokens) and one head whose score on token
+    j* is so large that its softmax is one-hot, P = 1/(2n) + [j = j*]/2.  A zero
+    index query makes P_idx uniform, so KL = sum_j P_j log(n P_j) and
+    d KL / d q_idx = scale_idx (sum_j k_j / (2n) - k_j* / 2)."""
+    B, d, d_idx, n, jstar = 8, 8, 4, 8, 5
+    lay = O.Layout([8], [8], [0])
+    q = np.zeros((8, 2, d), dtype=np.uint16)
+    k = np.zeros((8, 1, d), dtype=np.uint16)
+    q[7, 1, 0] = _bits([64.0])[0]
+    k[jstar, 0, 0] = _bits([64.0])[0]
+    iq = np.zeros((8, 1, d_idx), dtype=np.uint16)
+    ik = _bits(np.arange(8 * d_idx, dtype=np.float32).reshape(8, d_idx) / 16.0 - 0.9)
+    ids = np.zeros((8, 1, 1), dtype=np.int32)
+    kl, d_iq, _ = O.sparse_kl(iq, ik, q, k, ids, lay, B)
+    P = np.full(n, 1.0 / (2 * n))
+    P[jstar] += 0.5
+    assert abs(kl[7, 0] - float(np.sum(P * np.log(n * P)))) < 1e-12, kl[7, 0]
+    kv = _vals(ik)
+    want = (kv.sum(axis=0) / (2 * n) - kv[jstar] / 2) / math.sqrt(d_idx)
+    assert np.abs(d_iq[7, 0] - want).max() < 1e-12
+    # row 0 sees one token: both distributions are that token, KL = 0, no gradient
+    assert kl[0, 0] == 0 and np.all(d_iq[0, 0] == 0)
+
+
 ALL_PINS = [pin_flops_ratio, pin_effective_flops_dense, pin_brute_force_selection,
             pin_planted_closed_form, pin_selection_invariants, pin_block_maxima_partial,
             pin_dense_equality, pin_closed_forms, pin_combine,
             pin_decode_and_chunked_consistency, pin_head_permutation,
-            pin_fp8_e4m3_codes, pin_fp8_attention_scales]
+            pin_fp8_e4m3_codes, pin_fp8_attention_scales,
+            pin_attention_backward_fd, pin_attention_backward_autograd, pin_kl_fd,
+            pin_kl_autograd, pin_kl_mixture_closed_form]

@@ -37,6 +37,16 @@ MUTATIONS = {
     "fp8_nan_all_top_exponent": ("v = np.where((e == 15) & ((c & 0x7) == 7), np.nan, v)",
                                  "v = np.where(e == 15, np.nan, v)"),
     "fp8_v_scale_dropped": ("vals = dec(v_bits[kv0 + toks, g]) * vs", "vals = dec(v_bits[kv0 + toks, g])"),
+    "bwd_softmax_jacobian_no_mean": ("dz = p * (dp - (p * dp).sum(axis=1, keepdims=True))", "dz = p * dp"),
+    "bwd_dk_unscaled": ("dk = (dz.T @ qh) * scale", "dk = (dz.T @ qh)"),
+    "bwd_dv_scaled": ("dv = p.T @ d_o", "dv = (p.T @ d_o) * scale"),
+    "bwd_dk_into_group0": ("dK[kv0 + toks, g] += dk", "dK[kv0 + toks, 0] += dk"),
+    "kl_teacher_logit_mean": ("p = softmax_rows((q_heads @ k_toks.T) * scale_main).mean(axis=0)",
+                              "p = softmax_rows(((q_heads @ k_toks.T) * scale_main).mean(axis=0)[None, :])[0]"),
+    "kl_grad_sign": ("ds = p_idx - p", "ds = p - p_idx"),
+    "kl_reverse_direction": ("kl = float(np.sum(p * (np.log(p) - np.log(p_idx))))",
+                             "kl = float(np.sum(p_idx * (np.log(p_idx) - np.log(p))))"),
+    "kl_dq_unscaled": ("d_iq = (ds @ ik_toks) * scale_idx", "d_iq = (ds @ ik_toks)"),
     "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
                              "O[i, g::H_kv], L[i, g::H_kv] = attend(\n                qf[g::H_kv], keys, vals, scale)"),
 }
