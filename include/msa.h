@@ -14,6 +14,7 @@
  *   msa_sparse_attn_decode   Main Branch for one query row per sequence
  *   msa_sparse_attn_*_fp8    Main Branch on e4m3 queries and KV cache
  *   msa_dense_attn           dense causal GQA attention (the comparison baseline)
+ *   msa_sparse_attn_backward training: Main Branch gradients dQ, dK, dV
  *
  * Conventions shared by every call
  * --------------------------------
@@ -208,6 +209,43 @@ size_t msa_dense_attn_workspace_size(const msa_seqs* seqs, int num_q_heads, int 
 int msa_dense_attn(const void* q, const void* k, const void* v, const msa_seqs* seqs,
                    int num_q_heads, int num_kv_heads, int head_dim, float softmax_scale, void* o,
                    float* lse, void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * msa_sparse_attn_backward -- training backward of the Main Branch.
+ *
+ * Alg. 1 trains through the sparse attention of Sec. 3.1.  For an upstream
+ * gradient dO of the output O, with P_ij = exp(softmax_scale q_i.k_j - LSE_i)
+ * over the tokens row i attended and D_i = dO_i . O_i:
+ *   dV_j = sum_i P_ij dO_i,  dS_ij = P_ij (dO_i . v_j - D_i),
+ *   dQ_i = softmax_scale sum_j dS_ij k_j,  dK_j = softmax_scale sum_i dS_ij q_i,
+ * each sum running over the (row, head, token) triples of the forward.
+ *
+ *   q, k, v, block_ids, seqs, heads, block_size, topk, softmax_scale: exactly
+ *              as passed to the forward call (msa_sparse_attn_prefill/_decode)
+ *   o          bf16 [total_q_rows, num_q_heads, head_dim]   the forward's O
+ *   lse        fp32 [total_q_rows, num_q_heads]             the forward's LSE
+ *   d_o        bf16 [total_q_rows, num_q_heads, head_dim]   upstream gradient
+ *   d_q        bf16 [total_q_rows, num_q_heads, head_dim]   OUTPUT
+ *   d_k, d_v   bf16 [total_kv_rows, num_kv_heads, head_dim] OUTPUT; every row is
+ *              written, key rows no query attended get 0
+ *
+ * Work runs key-block-outer with fp32 accumulation.  d_q is bit-reproducible
+ * (its partials are added in slot order); d_k and d_v add the contributions of
+ * a key block in an order fixed at run time, so their last bits can differ
+ * between calls.  Workspace, stream and
+ * error behaviour as for msa_sparse_attn_prefill.  Supported: head_dim == 128;
+ * block_size == 64; 1 <= topk <= 64; 1 <= num_q_heads / num_kv_heads <= 16;
+ * num_kv_heads <= 64 (block_size 128 returns MSA_ERR_UNSUPPORTED).
+ * ------------------------------------------------------------------------ */
+size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,
+                                               int num_kv_heads, int head_dim, int block_size,
+                                               int topk);
+int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const void* o,
+                             const float* lse, const void* d_o, const int32_t* block_ids,
+                             const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                             int head_dim, int block_size, int topk, float softmax_scale,
+                             void* d_q, void* d_k, void* d_v, void* workspace,
+                             size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (a measurement aid; no part of the attention path)

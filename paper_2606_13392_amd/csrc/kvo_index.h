@@ -1,0 +1,295 @@
+// Reverse index of a block selection for key-block-outer kernels.
+//
+// A block selection lists, per (query row, group), the key blocks the row
+// attends (Sec. 3.1, top-k equation).  Kernels that iterate key blocks on the
+// outside need the transpose: per tile (group r, key block) the list of
+// (query row, slot) handles that selected it, cut into work items of at most
+// kItemQueries queries (Sec. 4.2 on the KV-outer order; Sec. 4.3 on work
+// partitioned along the gathered-query dimension).  Built per chunk of query
+// rows:
+//   kvo_count    incidences per tile and each incidence's position in its tile
+//   kvo_scan*    exclusive offsets of handles and of work items per tile
+//   kvo_fill     handle (row in chunk << 6 | slot) lists per tile
+// Included by the forward and backward Main Branch sources; everything here
+// has internal linkage.
+#pragma once
+
+#include <algorithm>
+
+#include "msa_common.h"
+#include "msa_profile.h"
+
+namespace {
+
+using namespace msa;
+
+constexpr int kHeadDim = 128;
+constexpr int kItemQueries = 256;      // queries of one tile per work item
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ bool slot_valid(int b, int p, int BK) { return b >= 0 && p >= 0 && b <= p / BK; }
+// An incidence takes part in the reverse index, the attention and the combine
+// iff its slot is valid and the block exists in the sequence's block range
+// (always true for consistent layouts; the second test keeps every index in
+// bounds when kv_lens exceed max_kv_len).
+__device__ __forceinline__ bool incidence_ok(int b, int p, int BK, const int64_t* __restrict__ blk_base, int s) {
+  return slot_valid(b, p, BK) && static_cast<int64_t>(b) < blk_base[s + 1] - blk_base[s];
+}
+
+__device__ __forceinline__ int row_position(const msa_seqs& sq, int64_t row, int* seq_out) {
+  const int s = find_seq(sq.q_offsets, sq.num_seqs, row);
+  const SeqGeom g = seq_geom(sq, s);
+  int p = g.kv_len - g.q_rows + static_cast<int>(row - g.q_begin);
+  if (p >= g.kv_len) p = -1;
+  *seq_out = s;
+  return p;
+}
+
+// ---------------------------------------------------------------- setup
+// blk_base[s] = key blocks of the sequences before s (kv_len clamped to max_kv_len).
+__global__ __launch_bounds__(256) void kvo_block_base_kernel(msa_seqs sq, int BK, int64_t* __restrict__ blk_base) {
+  __shared__ int64_t part[256];
+  const int t = threadIdx.x;
+  const int S = sq.num_seqs;
+  const int per = (S + 255) / 256;
+  const int s0 = t * per, s1 = min(S, s0 + per);
+  auto nblk = [&](int s) -> int64_t {
+    int64_t len = seq_geom(sq, s).kv_len;
+    if (len > sq.max_kv_len) len = sq.max_kv_len;
+    return (len + BK - 1) / BK;
+  };
+  int64_t acc = 0;
+  for (int s = s0; s < s1; ++s) acc += nblk(s);
+  part[t] = acc;
+  __syncthreads();
+  if (t == 0) {
+    int64_t run = 0;
+    for (int i = 0; i < 256; ++i) { int64_t x = part[i]; part[i] = run; run += x; }
+    blk_base[S] = run;
+  }
+  __syncthreads();
+  acc = part[t];
+  for (int s = s0; s < s1; ++s) { blk_base[s] = acc; acc += nblk(s); }
+}
+
+__global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, int64_t n, int32_t v) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+// ---------------------------------------------------------------- reverse index
+// Positions of every incidence inside its tile's handle list, with few device
+// atomics: a CTA takes kHistRows query rows of one group, histograms their
+// incidences over the key blocks of its sequences in LDS, claims one segment
+// of each touched tile with a single device atomic (the returned count is the
+// segment's start) and hands out positions inside its segments with LDS
+// atomics.  A CTA whose sequences span more than kHistBins key blocks falls
+// back to one device atomic per incidence.  Positions are relative to the
+// tile; kvo_fill adds the tile offsets once the scan has run.
+constexpr int kHistRows = 4096;
+constexpr int kHistBins = 16384;
+
+__global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
+                                                        const int64_t* __restrict__ blk_base, int H_kv, int BK,
+                                                        int topk, int64_t nbcap, int64_t row0, int64_t nrows,
+                                                        int32_t* __restrict__ cnt, int32_t* __restrict__ tpos) {
+  __shared__ int32_t hist[kHistBins];
+  const int r = blockIdx.y;
+  const int64_t rb0 = row0 + static_cast<int64_t>(blockIdx.x) * kHistRows;
+  const int64_t rb1 = min(rb0 + kHistRows, row0 + nrows);
+  const int s_first = find_seq_wave(sq.q_offsets, sq.num_seqs, rb0);
+  const int s_last = find_seq_wave(sq.q_offsets, sq.num_seqs, rb1 - 1);
+  const int64_t g_lo = blk_base[s_first];
+  const int64_t g_hi = blk_base[s_last + 1];
+  const bool in_lds = g_hi - g_lo <= kHistBins;           // uniform over the CTA
+  const int64_t tile_base = static_cast<int64_t>(r) * nbcap;
+
+  if (in_lds) {
+    for (int i = threadIdx.x; i < kHistBins; i += 256) hist[i] = 0;
+    __syncthreads();
+  }
+  // pass 1: histogram (or, without LDS room, claim each position directly)
+  for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
+    int s;
+    const int p = row_position(sq, row, &s);
+    const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+    int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
+    const int64_t gb0 = blk_base[s];
+    for (int j = 0; j < topk; ++j) {
+      const int b = ids[j];
+      if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+      if (in_lds) atomicAdd(&hist[gb0 + b - g_lo], 1);
+      else tp[j] = atomicAdd(&cnt[tile_base + gb0 + b], 1);
+    }
+  }
+  if (!in_lds) return;
+  __syncthreads();
+  // claim one segment per touched tile; hist becomes the segment cursor
+  const int nbin = static_cast<int>(g_hi - g_lo);
+  for (int i = threadIdx.x; i < nbin; i += 256) {
+    const int c = hist[i];
+    if (c > 0) hist[i] = atomicAdd(&cnt[tile_base + g_lo + i], c);
+  }
+  __syncthreads();
+  // pass 2: positions inside the claimed segments
+  for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
+    int s;
+    const int p = row_position(sq, row, &s);
+    const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+    int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
+    const int64_t gb0 = blk_base[s];
+    for (int j = 0; j < topk; ++j) {
+      const int b = ids[j];
+      if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+      tp[j] = atomicAdd(&hist[gb0 + b - g_lo], 1);
+    }
+  }
+}
+
+// One thread per (row, group) of the chunk: handle = (row in chunk << 6 | slot).
+__global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
+                                                       const int64_t* __restrict__ blk_base, int H_kv, int BK,
+                                                       int topk, int64_t nbcap, int64_t row0, int64_t nrows,
+                                                       const int32_t* __restrict__ tile_off,
+                                                       const int32_t* __restrict__ tpos,
+                                                       uint32_t* __restrict__ handles) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= nrows * H_kv) return;
+  const int64_t rl = i / H_kv;
+  const int64_t row = row0 + rl;
+  const int r = static_cast<int>(i % H_kv);
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const int32_t* tp = tpos + i * topk;
+  const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
+  for (int j = 0; j < topk; ++j) {
+    const int b = ids[j];
+    if (!incidence_ok(b, p, BK, blk_base, s)) continue;
+    handles[tile_off[base + b] + tp[j]] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(j);
+  }
+}
+
+// Two-array exclusive scan (handles per tile, work items per tile) in three
+// kernels: per-block scan, scan of block totals, add.
+constexpr int kScanPerBlock = 2048;   // 256 threads x 8
+
+__global__ __launch_bounds__(256) void kvo_scan_block_kernel(const int32_t* __restrict__ cnt, int64_t n,
+                                                             int32_t* __restrict__ tile_off,
+                                                             int32_t* __restrict__ item_off,
+                                                             int32_t* __restrict__ blk_tot) {
+  __shared__ int32_t sa[256], sb[256];
+  const int t = threadIdx.x;
+  const int64_t base = static_cast<int64_t>(blockIdx.x) * kScanPerBlock + t * 8;
+  int32_t a[8], b[8];
+  int32_t ta = 0, tb = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int32_t c = base + e < n ? cnt[base + e] : 0;
+    a[e] = ta; b[e] = tb;
+    ta += c;
+    tb += (c + kItemQueries - 1) / kItemQueries;
+  }
+  sa[t] = ta; sb[t] = tb;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int32_t xa = t >= off ? sa[t - off] : 0;
+    const int32_t xb = t >= off ? sb[t - off] : 0;
+    __syncthreads();
+    sa[t] += xa; sb[t] += xb;
+    __syncthreads();
+  }
+  const int32_t pa = sa[t] - ta, pb = sb[t] - tb;
+#pragma unroll
+  for (int e = 0; e < 8; ++e)
+    if (base + e < n) { tile_off[base + e] = a[e] + pa; item_off[base + e] = b[e] + pb; }
+  if (t == 255) { blk_tot[2 * blockIdx.x] = sa[255]; blk_tot[2 * blockIdx.x + 1] = sb[255]; }
+}
+
+__global__ __launch_bounds__(1024) void kvo_scan_top_kernel(int32_t* __restrict__ blk_tot, int nblk,
+                                                            int32_t* __restrict__ tile_off,
+                                                            int32_t* __restrict__ item_off, int64_t n) {
+  __shared__ int32_t sa[1024], sb[1024];
+  const int t = threadIdx.x;
+  const int per = (nblk + 1023) / 1024;
+  const int b0 = t * per, b1 = min(nblk, b0 + per);
+  int32_t ta = 0, tb = 0;
+  for (int b = b0; b < b1; ++b) { ta += blk_tot[2 * b]; tb += blk_tot[2 * b + 1]; }
+  sa[t] = ta; sb[t] = tb;
+  __syncthreads();
+  for (int off = 1; off < 1024; off <<= 1) {
+    const int32_t xa = t >= off ? sa[t - off] : 0;
+    const int32_t xb = t >= off ? sb[t - off] : 0;
+    __syncthreads();
+    sa[t] += xa; sb[t] += xb;
+    __syncthreads();
+  }
+  int32_t ra = sa[t] - ta, rb = sb[t] - tb;
+  for (int b = b0; b < b1; ++b) {
+    const int32_t xa = blk_tot[2 * b], xb = blk_tot[2 * b + 1];
+    blk_tot[2 * b] = ra; blk_tot[2 * b + 1] = rb;
+    ra += xa; rb += xb;
+  }
+  if (t == 1023) { tile_off[n] = sa[1023]; item_off[n] = sb[1023]; }
+}
+
+__global__ __launch_bounds__(256) void kvo_scan_add_kernel(const int32_t* __restrict__ blk_tot, int64_t n,
+                                                           int32_t* __restrict__ tile_off,
+                                                           int32_t* __restrict__ item_off) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int64_t b = i / kScanPerBlock;
+  tile_off[i] += blk_tot[2 * b];
+  item_off[i] += blk_tot[2 * b + 1];
+}
+
+// Largest i with arr[i] <= x, for arr non-decreasing with arr[0] <= x.
+template <typename T>
+__device__ __forceinline__ int64_t upper_index(const T* __restrict__ arr, int64_t n, int64_t x) {
+  int64_t lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (static_cast<int64_t>(arr[mid]) <= x) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// CTAs of a persistent kernel: every CU filled to the kernel's occupancy.
+template <typename K>
+int persistent_ctas(K kernel, int threads, int* cache) {
+  if (*cache == 0) {
+    int dev = 0, cus = 256, per_cu = 1;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu < 1)
+      per_cu = 1;
+    *cache = cus * per_cu;
+  }
+  return *cache;
+}
+// Reverse index of query rows r0 .. r0 + nr - 1 (one chunk): counts, scans
+// and handle lists for every tile of H_kv x nbcap.
+void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int64_t* blk_base, int H_kv, int BK,
+                         int topk, int64_t nbcap, int64_t ntile, int nscan, int64_t r0, int64_t nr, int32_t* cnt,
+                         int32_t* tile_off, int32_t* item_off, int32_t* blk_tot, int32_t* tpos, uint32_t* handles,
+                         hipStream_t stream) {
+  const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((ntile + 255) / 256, 4096));
+  const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, ntile, 0);
+  const dim3 hgrid(static_cast<unsigned>((nr + kHistRows - 1) / kHistRows), static_cast<unsigned>(H_kv));
+  msa_prof::launch("kvo_count_kernel", kvo_count_kernel, hgrid, dim3(256), 0, stream, block_ids, sq, blk_base, H_kv,
+                   BK, topk, nbcap, r0, nr, cnt, tpos);
+  msa_prof::launch("kvo_scan_block_kernel", kvo_scan_block_kernel, dim3(nscan), dim3(256), 0, stream, cnt, ntile,
+                   tile_off, item_off, blk_tot);
+  msa_prof::launch("kvo_scan_top_kernel", kvo_scan_top_kernel, dim3(1), dim3(1024), 0, stream, blk_tot, nscan,
+                   tile_off, item_off, ntile);
+  msa_prof::launch("kvo_scan_add_kernel", kvo_scan_add_kernel, dim3(static_cast<unsigned>((ntile + 255) / 256)),
+                   dim3(256), 0, stream, blk_tot, ntile, tile_off, item_off);
+  msa_prof::launch("kvo_fill_kernel", kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base,
+                   H_kv, BK, topk, nbcap, r0, nr, tile_off, tpos, handles);
+}
+
+}  // namespace

@@ -1,0 +1,562 @@
+// Training backward of the MSA Main Branch on gfx950, key-block-outer.
+//
+// Alg. 1 trains through the sparse attention of Sec. 3.1: O_i = sum_j P_ij V_j
+// with P_i = softmax(scale Q_i K_j^T) over the causally visible tokens of the
+// blocks row i selected.  For an upstream gradient dO, with P recomputed from
+// the forward's log-sum-exp and D_i = dO_i . O_i (the softmax Jacobian's
+// row term),
+//   dV_j += P_ij dO_i,   dP_ij = dO_i . V_j,   dS_ij = P_ij (dP_ij - D_i),
+//   dQ_i += scale dS_ij K_j,   dK_j += scale dS_ij Q_i.
+// Key blocks are iterated on the outside (the reverse index of kvo_index.h):
+// dK and dV of a block stay in registers while the queries that selected it
+// stream past, each incidence costs a gather of its Q and dO rows, and its dQ
+// contribution goes as an fp32 partial into the incidence's slot.  No
+// atomics touch a gradient: dQ sums its slot partials in slot order (bit-
+// reproducible); dK and dV sum a block's queries in the order of its handle
+// list, which the reverse index fills with atomics, so their last bits can
+// differ between runs.
+//
+//   bwd_delta        D per (row, head)
+//   per chunk of query rows:
+//     reverse index  (kvo_index.h)
+//     bwd_kvo        persistent CTAs of 8 waves over the work items (<= 256
+//                    queries of one tile).  K, V and K^T of the block sit in
+//                    LDS.  A CTA pass takes 64 gathered (query, head) rows;
+//                    wave (kq, rg) owns keys 16kq .. 16kq+15 and rows
+//                    32rg .. 32rg+31 of the pass: S = Q K^T and dP = dO V^T
+//                    (MFMA 16x16x32, one key per lane column), then
+//                    dV += P^T dO and dK += dS^T Q from transposed copies of
+//                    the pass's Q and dO rows, then dQ over all 64 keys for
+//                    dims 32kq .. 32kq+31 from dS staged in LDS.  At the end
+//                    of an item the 2 row groups' dK / dV are summed in LDS
+//                    and written as the item's partial.
+//     bwd_tile_reduce  per tile: its items' partials, in order, added to fp32
+//                    dK / dV accumulators
+//     bwd_dq_combine per (row, group): the valid slots' partials in slot order,
+//                    times scale, to bf16 dQ
+//   bwd_kv_convert   accumulators (dK times scale) to bf16 dK, dV
+#include "kvo_index.h"
+
+namespace {
+
+constexpr int kBwdBK = 64;
+constexpr int kBwdRowGroups = 2;
+constexpr int kBwdWaves = 4 * kBwdRowGroups;          // 4 key quarters x 2 row groups
+constexpr int kBwdThreads = 64 * kBwdWaves;
+constexpr int kBwdPassRows = 32 * kBwdRowGroups;      // gathered (query, head) rows per CTA pass
+constexpr int kPartFloats = 2 * kBwdBK * kHeadDim;    // dK and dV of one work item
+
+struct BwdSmem {
+  uint16_t k[kBwdBK][kHeadDim + 8];                   // K block, row-major
+  uint16_t v[kBwdBK][kHeadDim + 8];                   // V block, row-major
+  uint16_t kt[kHeadDim][kBwdBK + 8];                  // K block transposed
+  uint16_t qt[kHeadDim][kBwdPassRows + 8];            // Q rows of the pass, transposed
+  uint16_t dot[kHeadDim][kBwdPassRows + 8];           // dO rows of the pass, transposed
+  uint16_t ds[kBwdRowGroups][32][kBwdBK + 8];         // dS of the pass, [row][key] per row group
+  float lse2[kBwdPassRows];                           // LSE * log2(e) per pass row (+inf: no row)
+  float dlt[kBwdPassRows];                            // D per pass row
+  int32_t rpos[kBwdPassRows];                         // absolute position per pass row (-1: no row)
+  int64_t dqoff[kBwdPassRows];                        // float offset of the row's dQ partial (-1: no row)
+  int32_t s_row[kItemQueries];                        // query row inside the chunk
+  int32_t s_slot[kItemQueries];                       // slot of this block in the row's id list
+  int32_t s_pos[kItemQueries];                        // absolute position of the query
+};
+// the item-end reduction reuses qt and dot: 4 key quarters x 32 registers x 64 lanes
+static_assert(sizeof(uint16_t) * 2 * kHeadDim * (kBwdPassRows + 8) >= 4 * 32 * 64 * sizeof(float),
+              "reduction scratch");
+
+__device__ __forceinline__ uint16_t raw_elem(const u32x4& w, int j) {
+  return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
+}
+__device__ __forceinline__ bf16x8 lds_pair_bf16x8(const uint16_t* lo, const uint16_t* hi) {
+  const uint2 a = *reinterpret_cast<const uint2*>(lo), b = *reinterpret_cast<const uint2*>(hi);
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+
+// D[row, head] = sum_d dO . O; 16 lanes per (row, head), 8 dims each.
+__global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restrict__ o, const uint16_t* __restrict__ d_o,
+                                                        int64_t pairs, float* __restrict__ delta) {
+  const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  const int64_t pair = t >> 4;
+  const int part = static_cast<int>(t & 15);
+  float acc = 0.f;
+  if (pair < pairs) {
+    const u32x4 a = load_raw(o + pair * kHeadDim + 8 * part);
+    const u32x4 b = load_raw(d_o + pair * kHeadDim + 8 * part);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc += __uint_as_float(a[j] << 16) * __uint_as_float(b[j] << 16);
+      acc += __uint_as_float(a[j] & 0xFFFF0000u) * __uint_as_float(b[j] & 0xFFFF0000u);
+    }
+  }
+#pragma unroll
+  for (int off = 8; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+  if (pair < pairs && part == 0) delta[pair] = acc;
+}
+
+// Wave (kq, rg): keys 16kq .. 16kq+15 of the block, rows 32rg .. 32rg+31 of
+// each CTA pass.  MFMA 16x16x32: lane l = (c = l % 16, quarter qd = l / 16).
+// In S = Q K^T and dP = dO V^T the lane holds key 16kq + c and, of row tile
+// t, rows 16t + 4qd + i (i = 0..3).  Those 8 rows are the k-slice the lane
+// supplies to dV += P^T dO and dK += dS^T Q (k index 8qd + 4t + i), and
+// the B operands read the same rows from the transposed Q / dO copies.
+__global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const uint16_t* __restrict__ d_o, const float* __restrict__ lse, const float* __restrict__ delta, msa_seqs sq,
+    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
+    const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0, float scale_log2,
+    float* __restrict__ dq_buf, float* __restrict__ part) {
+  __shared__ BwdSmem sm;
+  constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int kq = wave & 3, rg = wave >> 2;
+  const int c16 = lane & 15, qd = lane >> 4;
+  const int G = H_q / H_kv;
+  const int qpw = 32 / G;                             // queries per row group and pass
+  const int rows_g = qpw * G;                         // used rows of a row group
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  int64_t staged = -1;
+
+  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int64_t gb = tile % nbcap;
+    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+    const SeqGeom g = seq_geom(sq, s);
+    const int key0 = static_cast<int>(gb - blk_base[s]) * kBwdBK;
+
+    __syncthreads();                                  // the previous item is done with LDS
+    if (static_cast<int>(threadIdx.x) < nq) {
+      const uint32_t hd = handles[h0 + threadIdx.x];
+      const int32_t rl = static_cast<int32_t>(hd >> 6);
+      sm.s_row[threadIdx.x] = rl;
+      sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
+      sm.s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
+    }
+    if (tile != staged) {
+      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      // K row-major and transposed: a thread takes 4 keys x 8 dims
+      for (int c = threadIdx.x; c < (kBwdBK / 4) * (kHeadDim / 8); c += kBwdThreads) {
+        const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        u32x4 rows[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int key = 4 * key4 + j;
+          rows[j] = key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
+          *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) = rows[j];
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          uint2 w;
+          w.x = static_cast<uint32_t>(raw_elem(rows[0], e)) | (static_cast<uint32_t>(raw_elem(rows[1], e)) << 16);
+          w.y = static_cast<uint32_t>(raw_elem(rows[2], e)) | (static_cast<uint32_t>(raw_elem(rows[3], e)) << 16);
+          *reinterpret_cast<uint2*>(&sm.kt[8 * dg + e][4 * key4]) = w;
+        }
+      }
+      for (int c = threadIdx.x; c < kBwdBK * (kHeadDim / 8); c += kBwdThreads) {
+        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        *reinterpret_cast<u32x4*>(&sm.v[key][8 * dg]) =
+            key0 + key < g.kv_len ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
+      }
+      staged = tile;
+    }
+    __syncthreads();
+
+    f32x4 acc_dv[8], acc_dk[8];                       // [dim tile]: lane column = dim, rows = keys 4qd + i
+#pragma unroll
+    for (int t = 0; t < 8; ++t) { acc_dv[t] = f32x4{}; acc_dk[t] = f32x4{}; }
+    const int key = key0 + 16 * kq + c16;             // this lane's key in the C layout of S
+
+    for (int c = 0; c < nq; c += kBwdRowGroups * qpw) {
+      // A operands: Q and dO of rows 16t + c16 of this row group, dims 32ks + 8qd .. +8
+      u32x4 bq[2][KS], bdo[2][KS];
+      int64_t hrow[2];
+      bool arow[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int ra = 16 * t + c16;
+        const int qa = c + rg * qpw + ra / G;
+        arow[t] = ra < rows_g && qa < nq;
+        const int64_t grow = row0 + (arow[t] ? sm.s_row[qa] : 0);
+        hrow[t] = grow * H_q + static_cast<int64_t>(r) * G + ra % G;
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          bq[t][st] = arow[t] ? load_raw(q + hrow[t] * kHeadDim + 32 * st + 8 * qd) : u32x4{};
+          bdo[t][st] = arow[t] ? load_raw(d_o + hrow[t] * kHeadDim + 32 * st + 8 * qd) : u32x4{};
+        }
+      }
+      __syncthreads();                                // the previous pass is done with qt, dot, ds, row scalars
+      // transposed copies: key quarter kq writes the dims of k-step kq
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int col = 32 * rg + 16 * t + c16;
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          if (st != kq) continue;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            sm.qt[32 * st + 8 * qd + j][col] = raw_elem(bq[t][st], j);
+            sm.dot[32 * st + 8 * qd + j][col] = raw_elem(bdo[t][st], j);
+          }
+        }
+        if (qd == 0 && kq == 0) {
+          const int ra = 16 * t + c16;
+          const int qa = c + rg * qpw + ra / G;
+          sm.lse2[col] = arow[t] ? lse[hrow[t]] * kLog2e : INFINITY;
+          sm.dlt[col] = arow[t] ? delta[hrow[t]] : 0.f;
+          sm.rpos[col] = arow[t] ? sm.s_pos[qa] : -1;
+          sm.dqoff[col] = arow[t] ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G +
+                                     ra % G) * kHeadDim
+                                  : -1;
+        }
+      }
+      __syncthreads();
+
+      // S = Q K^T, dP = dO V^T for this row group x this key quarter
+      f32x4 acc_s[2], acc_dp[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        acc_s[t] = f32x4{};
+        acc_dp[t] = f32x4{};
+#pragma unroll
+        for (int st = 0; st < KS; ++st) {
+          acc_s[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
+                                  ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
+          acc_dp[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bdo[t][st]),
+                                   ld_bf16x8(&sm.v[16 * kq + c16][32 * st + 8 * qd]), acc_dp[t]);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      // P and dS in place: lane holds rows 16t + 4qd + i
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int prow = 32 * rg + 16 * t + 4 * qd + i;
+          const float l2 = sm.lse2[prow];
+          const bool vis = key <= sm.rpos[prow] && l2 > -INFINITY;
+          const float p = vis ? exp2f(acc_s[t][i] * scale_log2 - l2) : 0.f;
+          acc_s[t][i] = p;
+          acc_dp[t][i] = p * (acc_dp[t][i] - sm.dlt[prow]);
+        }
+      // A operands of dV and dK: k index 8qd + 4t + i = row 16t + 4qd + i
+      uint4 pw, sw;
+      pw.x = pack_bf16x2(acc_s[0][0], acc_s[0][1]);
+      pw.y = pack_bf16x2(acc_s[0][2], acc_s[0][3]);
+      pw.z = pack_bf16x2(acc_s[1][0], acc_s[1][1]);
+      pw.w = pack_bf16x2(acc_s[1][2], acc_s[1][3]);
+      sw.x = pack_bf16x2(acc_dp[0][0], acc_dp[0][1]);
+      sw.y = pack_bf16x2(acc_dp[0][2], acc_dp[0][3]);
+      sw.z = pack_bf16x2(acc_dp[1][0], acc_dp[1][1]);
+      sw.w = pack_bf16x2(acc_dp[1][2], acc_dp[1][3]);
+      const bf16x8 pa = __builtin_bit_cast(bf16x8, pw);
+      const bf16x8 sa = __builtin_bit_cast(bf16x8, sw);
+      // dS to LDS as [row][key] for dQ
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          sm.ds[rg][16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(sw[2 * t + (i >> 1)] >> (16 * (i & 1)));
+      __builtin_amdgcn_sched_barrier(0);
+      // dV += P^T dO, dK += dS^T Q over the 32 rows (one k-step), 8 dim tiles
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const uint16_t* dr = &sm.dot[16 * t + c16][32 * rg + 4 * qd];
+        const uint16_t* qr = &sm.qt[16 * t + c16][32 * rg + 4 * qd];
+        acc_dv[t] = mfma16x16x32(pa, lds_pair_bf16x8(dr, dr + 16), acc_dv[t]);
+        acc_dk[t] = mfma16x16x32(sa, lds_pair_bf16x8(qr, qr + 16), acc_dk[t]);
+      }
+      __syncthreads();                                // dS of all 4 key quarters in LDS
+
+      // dQ of this row group, dims 32kq + 16u + c16, over the 64 keys
+      f32x4 acc_q[2][2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          acc_q[t][u] = f32x4{};
+#pragma unroll
+          for (int ks = 0; ks < kBwdBK / 32; ++ks)
+            acc_q[t][u] = mfma16x16x32(ld_bf16x8(&sm.ds[rg][16 * t + c16][32 * ks + 8 * qd]),
+                                       ld_bf16x8(&sm.kt[32 * kq + 16 * u + c16][32 * ks + 8 * qd]), acc_q[t][u]);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+      // fp32 partial of each valid row into its incidence's slot
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t off = sm.dqoff[32 * rg + 16 * t + 4 * qd + i];
+          if (off >= 0) {
+            float* dst = dq_buf + off + 32 * kq + c16;
+            dst[0] = acc_q[t][0][i];
+            dst[16] = acc_q[t][1][i];
+          }
+        }
+    }
+
+    // item end: rg 1 hands its dV / dK to rg 0 through LDS; rg 0 writes the
+    // item's partial [tensor][kq][reg][lane]
+    float* red = reinterpret_cast<float*>(&sm.qt[0][0]);
+#pragma unroll
+    for (int tensor = 0; tensor < 2; ++tensor) {
+      f32x4* acc = tensor == 0 ? acc_dv : acc_dk;
+      __syncthreads();
+      if (rg == 1)
+#pragma unroll
+        for (int reg = 0; reg < 32; ++reg) red[(kq * 32 + reg) * 64 + lane] = acc[reg >> 2][reg & 3];
+      __syncthreads();
+      if (rg == 0) {
+        float* dst = part + (static_cast<int64_t>(item) * 2 + tensor) * (4 * 32 * 64) + kq * (32 * 64) + lane;
+#pragma unroll
+        for (int reg = 0; reg < 32; ++reg) dst[reg * 64] = acc[reg >> 2][reg & 3] + red[(kq * 32 + reg) * 64 + lane];
+      }
+    }
+  }
+}
+
+// One CTA per tile: sum of the tile's item partials (in item order) added to
+// the fp32 accumulators of the block's keys.
+__global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
+                                                              const int32_t* __restrict__ item_off, int H_kv,
+                                                              int64_t nbcap, const float* __restrict__ part,
+                                                              float* __restrict__ dk_acc, float* __restrict__ dv_acc) {
+  const int64_t tile = blockIdx.x;
+  const int32_t i0 = item_off[tile], i1 = item_off[tile + 1];
+  if (i0 == i1) return;
+  const int r = static_cast<int>(tile / nbcap);
+  const int64_t gb = tile % nbcap;
+  const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+  const SeqGeom g = seq_geom(sq, s);
+  const int key0 = static_cast<int>(gb - blk_base[s]) * kBwdBK;
+  for (int idx = threadIdx.x; idx < kPartFloats; idx += 256) {
+    float acc = 0.f;
+    for (int32_t it = i0; it < i1; ++it) acc += part[static_cast<int64_t>(it) * kPartFloats + idx];
+    const int tensor = idx / (4 * 32 * 64);
+    const int kq = (idx / (32 * 64)) & 3;
+    const int reg = (idx / 64) & 31;
+    const int ln = idx & 63;
+    const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
+    const int dim = 16 * (reg >> 2) + (ln & 15);
+    if (key0 + key >= g.kv_len) continue;
+    float* dst = (tensor == 0 ? dv_acc : dk_acc) +
+                 ((g.kv_start + key0 + key) * H_kv + r) * static_cast<int64_t>(kHeadDim) + dim;
+    *dst += acc;
+  }
+}
+
+// One wave per (row, group) of the chunk: dQ = scale x sum of the valid slots'
+// partials, in slot order.
+constexpr int kCombWaves = 4;
+
+__global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
+    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_q, int H_kv,
+    int topk, int64_t row0, int64_t nrows, const float* __restrict__ dq_buf, float scale, uint16_t* __restrict__ dq) {
+  const int lane = lane_id();
+  const int64_t pr = static_cast<int64_t>(blockIdx.x) * kCombWaves + threadIdx.x / kWave;
+  if (pr >= nrows * H_kv) return;
+  const int64_t rl = pr / H_kv;
+  const int r = static_cast<int>(pr % H_kv);
+  const int G = H_q / H_kv;
+  const int64_t row = row0 + rl;
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const int E = G * kHeadDim;                         // floats of one slot
+  const float* src = dq_buf + pr * topk * static_cast<int64_t>(E);
+  uint16_t* dst = dq + (row * H_q + static_cast<int64_t>(r) * G) * kHeadDim;
+  for (int c4 = lane; c4 < E / 4; c4 += kWave) {
+    f32x4 acc = f32x4{};
+    for (int j = 0; j < topk; ++j) {
+      if (!incidence_ok(ids[j], p, kBwdBK, blk_base, s)) continue;
+      acc += *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(j) * E + 4 * c4);
+    }
+    uint2 w;
+    w.x = pack_bf16x2(acc[0] * scale, acc[1] * scale);
+    w.y = pack_bf16x2(acc[2] * scale, acc[3] * scale);
+    *reinterpret_cast<uint2*>(dst + 4 * c4) = w;
+  }
+}
+
+__global__ __launch_bounds__(256) void bwd_kv_convert_kernel(const float* __restrict__ dk_acc,
+                                                             const float* __restrict__ dv_acc, int64_t n4, float scale,
+                                                             uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n4;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const f32x4 a = reinterpret_cast<const f32x4*>(dk_acc)[i];
+    const f32x4 b = reinterpret_cast<const f32x4*>(dv_acc)[i];
+    uint2 wa, wb;
+    wa.x = pack_bf16x2(a[0] * scale, a[1] * scale);
+    wa.y = pack_bf16x2(a[2] * scale, a[3] * scale);
+    wb.x = pack_bf16x2(b[0], b[1]);
+    wb.y = pack_bf16x2(b[2], b[3]);
+    reinterpret_cast<uint2*>(dk)[i] = wa;
+    reinterpret_cast<uint2*>(dv)[i] = wb;
+  }
+}
+
+// ---------------------------------------------------------------- host plan
+struct BwdPlan {
+  int64_t nbcap, ntile, chunk_rows, max_items;
+  int nscan;
+  size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_delta, off_dk, off_dv, off_handles,
+      off_tpos, off_dq, off_part, total;
+};
+
+constexpr size_t kDefaultBwdBytes = size_t(64) << 30;
+
+void bwd_layout(BwdPlan& pl, const msa_seqs* seqs, int H_q, int H_kv, int topk) {
+  using msa_host::align_up;
+  size_t o = 0;
+  pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
+  pl.off_delta = o;    o = align_up(o + sizeof(float) * static_cast<size_t>(seqs->total_q_rows) * H_q, 256);
+  const size_t kv_floats = static_cast<size_t>(seqs->total_kv_rows) * H_kv * kHeadDim;
+  pl.off_dk = o;       o = align_up(o + sizeof(float) * kv_floats, 256);
+  pl.off_dv = o;       o = align_up(o + sizeof(float) * kv_floats, 256);
+  const size_t inc = static_cast<size_t>(pl.chunk_rows) * H_kv * topk;
+  pl.max_items = pl.ntile + static_cast<int64_t>((inc + kItemQueries - 1) / kItemQueries);
+  pl.off_handles = o;  o = align_up(o + sizeof(uint32_t) * inc, 256);
+  pl.off_tpos = o;     o = align_up(o + sizeof(int32_t) * inc, 256);
+  pl.off_dq = o;       o = align_up(o + sizeof(float) * inc * (H_q / H_kv) * kHeadDim, 256);
+  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * kPartFloats, 256);
+  pl.total = o;
+}
+
+int make_bwd_plan(const msa_seqs* seqs, int H_q, int H_kv, int topk, size_t budget, BwdPlan* pl) {
+  const int64_t nb = (seqs->max_kv_len + kBwdBK - 1) / kBwdBK;
+  pl->nbcap = static_cast<int64_t>(seqs->num_seqs) * (nb > 0 ? nb : 1);
+  pl->ntile = static_cast<int64_t>(H_kv) * pl->nbcap;
+  if (pl->ntile >= (int64_t(1) << 31) - 1) return MSA_ERR_UNSUPPORTED;
+  pl->nscan = static_cast<int>((pl->ntile + kScanPerBlock - 1) / kScanPerBlock);
+  if (pl->nscan > 1024 * 64) return MSA_ERR_UNSUPPORTED;
+  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  int64_t rows = std::max<int64_t>(1, seqs->total_q_rows);
+  rows = std::min(rows, max_rows);
+  pl->chunk_rows = rows;
+  bwd_layout(*pl, seqs, H_q, H_kv, topk);
+  if (pl->total > budget) {
+    // bytes per chunk row, from the layout at one row and at two rows
+    pl->chunk_rows = 1;
+    bwd_layout(*pl, seqs, H_q, H_kv, topk);
+    const size_t one = pl->total;
+    if (one > budget) return MSA_ERR_WORKSPACE;
+    pl->chunk_rows = 2;
+    bwd_layout(*pl, seqs, H_q, H_kv, topk);
+    const size_t per_row = pl->total - one + 1024;
+    rows = 1 + static_cast<int64_t>((budget - one) / per_row);
+    pl->chunk_rows = std::min(rows, std::min<int64_t>(max_rows, std::max<int64_t>(1, seqs->total_q_rows)));
+    bwd_layout(*pl, seqs, H_q, H_kv, topk);
+    while (pl->total > budget && pl->chunk_rows > 1) {
+      pl->chunk_rows = std::max<int64_t>(1, pl->chunk_rows * 7 / 8);
+      bwd_layout(*pl, seqs, H_q, H_kv, topk);
+    }
+    if (pl->total > budget) return MSA_ERR_WORKSPACE;
+  }
+  return MSA_OK;
+}
+
+int validate_bwd(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, int topk) {
+  int st = msa_host::validate_seqs(seqs);
+  if (st != MSA_OK) return st;
+  if (H_q < 1 || H_kv < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
+  if (H_q % H_kv != 0) return MSA_ERR_INVALID;
+  if (head_dim != kHeadDim || BK != kBwdBK) return MSA_ERR_UNSUPPORTED;
+  if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
+  if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  return MSA_OK;
+}
+
+}  // namespace
+
+extern "C" size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                                         int head_dim, int block_size, int topk) {
+  if (validate_bwd(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
+  BwdPlan pl;
+  if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk, kDefaultBwdBytes, &pl) != MSA_OK) {
+    if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+    pl.chunk_rows = 1;
+    bwd_layout(pl, seqs, num_q_heads, num_kv_heads, topk);
+  }
+  return pl.total;
+}
+
+extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                                        const void* d_o, const int32_t* block_ids, const msa_seqs* seqs,
+                                        int num_q_heads, int num_kv_heads, int head_dim, int block_size, int topk,
+                                        float softmax_scale, void* d_q, void* d_k, void* d_v, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  const int H_q = num_q_heads, H_kv = num_kv_heads;
+  int st = validate_bwd(seqs, H_q, H_kv, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (!q || !k || !v || !o || !lse || !d_o || !block_ids || !d_q || !d_k || !d_v) return MSA_ERR_INVALID;
+  if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
+  BwdPlan pl;
+  st = make_bwd_plan(seqs, H_q, H_kv, topk, workspace_bytes, &pl);
+  if (st != MSA_OK) return st;
+  if (!workspace || workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  auto* blk_base = reinterpret_cast<int64_t*>(ws + pl.off_blk_base);
+  auto* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
+  auto* tile_off = reinterpret_cast<int32_t*>(ws + pl.off_tile_off);
+  auto* item_off = reinterpret_cast<int32_t*>(ws + pl.off_item_off);
+  auto* blk_tot = reinterpret_cast<int32_t*>(ws + pl.off_blk_tot);
+  auto* delta = reinterpret_cast<float*>(ws + pl.off_delta);
+  auto* dk_acc = reinterpret_cast<float*>(ws + pl.off_dk);
+  auto* dv_acc = reinterpret_cast<float*>(ws + pl.off_dv);
+  auto* handles = reinterpret_cast<uint32_t*>(ws + pl.off_handles);
+  auto* tpos = reinterpret_cast<int32_t*>(ws + pl.off_tpos);
+  auto* dq_buf = reinterpret_cast<float*>(ws + pl.off_dq);
+  auto* part = reinterpret_cast<float*>(ws + pl.off_part);
+  const msa_seqs sq = *seqs;
+  const int64_t kv_floats = seqs->total_kv_rows * H_kv * static_cast<int64_t>(kHeadDim);
+  const unsigned zero_blocks = static_cast<unsigned>(std::min<int64_t>((kv_floats + 255) / 256, 8192));
+
+  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, kBwdBK,
+                   blk_base);
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
+                   reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
+                   reinterpret_cast<int32_t*>(dv_acc), kv_floats, 0);
+  const int64_t pairs = seqs->total_q_rows * H_q;
+  if (pairs > 0)
+    msa_prof::launch("bwd_delta_kernel", bwd_delta_kernel, dim3(static_cast<unsigned>((pairs * 16 + 255) / 256)),
+                     dim3(256), 0, stream, static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(d_o), pairs,
+                     delta);
+  static int ctas = 0;
+  const int nctas = persistent_ctas(bwd_kvo_kernel, kBwdThreads, &ctas);
+  const float sl2 = softmax_scale * kLog2e;
+  for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
+    const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
+    build_reverse_index(block_ids, sq, blk_base, H_kv, kBwdBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
+                        tile_off, item_off, blk_tot, tpos, handles, stream);
+    msa_prof::launch("bwd_kvo_kernel", bwd_kvo_kernel, dim3(nctas), dim3(kBwdThreads), 0, stream,
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                     static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(d_o), lse,
+                     static_cast<const float*>(delta), sq, static_cast<const int64_t*>(blk_base),
+                     static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
+                     static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf, part);
+    msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile)),
+                     dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
+                     static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc,
+                     dv_acc);
+    msa_prof::launch("bwd_dq_combine_kernel", bwd_dq_combine_kernel,
+                     dim3(static_cast<unsigned>((nr * H_kv + kCombWaves - 1) / kCombWaves)), dim3(64 * kCombWaves),
+                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_q, H_kv, topk, r0, nr,
+                     static_cast<const float*>(dq_buf), softmax_scale, static_cast<uint16_t*>(d_q));
+  }
+  if (kv_floats > 0)
+    msa_prof::launch("bwd_kv_convert_kernel", bwd_kv_convert_kernel, dim3(zero_blocks), dim3(256), 0, stream,
+                     static_cast<const float*>(dk_acc), static_cast<const float*>(dv_acc), kv_floats / 4,
+                     softmax_scale, static_cast<uint16_t*>(d_k), static_cast<uint16_t*>(d_v));
+  return msa_host::launch_status();
+}

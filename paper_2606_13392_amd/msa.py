@@ -26,6 +26,7 @@ EXPORTS = [
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
     "msa_sparse_attn_prefill_fp8", "msa_sparse_attn_decode_fp8",
     "msa_dense_attn_workspace_size", "msa_dense_attn",
+    "msa_sparse_attn_backward_workspace_size", "msa_sparse_attn_backward",
     "msa_profile_enable", "msa_profile_reset", "msa_profile_kernel_name", "msa_profile_read",
 ]
 
@@ -75,6 +76,10 @@ def lib() -> ctypes.CDLL:
         L.msa_dense_attn_workspace_size.restype = Z
         L.msa_dense_attn.argtypes = [P, P, P, S, I, I, I, F, P, P, P, Z, P]
         L.msa_dense_attn.restype = I
+        L.msa_sparse_attn_backward_workspace_size.argtypes = [S, I, I, I, I, I]
+        L.msa_sparse_attn_backward_workspace_size.restype = Z
+        L.msa_sparse_attn_backward.argtypes = [P, P, P, P, P, P, P, S, I, I, I, I, I, F, P, P, P, P, Z, P]
+        L.msa_sparse_attn_backward.restype = I
         L.msa_profile_enable.argtypes = [I]
         L.msa_profile_enable.restype = I
         L.msa_profile_reset.argtypes = []
@@ -293,6 +298,48 @@ def dense_attn(q, k, v, seqs: Seqs, softmax_scale=None, out=None, lse=None, work
 
 
 # ---------------------------------------------------------------- kernel timing
+# ---------------------------------------------------------------- training backward
+def sparse_attn_backward_workspace_size(seqs: Seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) -> int:
+    return int(lib().msa_sparse_attn_backward_workspace_size(seqs.ref(), num_q_heads, num_kv_heads, head_dim,
+                                                              block_size, topk))
+
+
+def sparse_attn_backward(q, k, v, o, lse, d_o, block_ids, seqs: Seqs, block_size: int, softmax_scale=None,
+                         d_q=None, d_k=None, d_v=None, workspace=None):
+    """dQ [Tq, H_q, d_h], dK and dV [Tkv, H_kv, d_h] (bf16) of the Main Branch for
+    the upstream gradient d_o, given the forward's O and LSE."""
+    Tq, H_q, d_h = q.shape
+    H_kv = k.shape[1]
+    topk = block_ids.shape[2]
+    dev = seqs.device
+    _need(q, "q", torch.bfloat16, (seqs.total_q_rows, H_q, d_h), dev)
+    _need(k, "k", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(v, "v", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(o, "o", torch.bfloat16, (Tq, H_q, d_h), dev)
+    _need(lse, "lse", torch.float32, (Tq, H_q), dev)
+    _need(d_o, "d_o", torch.bfloat16, (Tq, H_q, d_h), dev)
+    _need(block_ids, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    if d_q is None:
+        d_q = torch.empty_like(q)
+    if d_k is None:
+        d_k = torch.empty_like(k)
+    if d_v is None:
+        d_v = torch.empty_like(v)
+    _need(d_q, "d_q", torch.bfloat16, tuple(q.shape), dev)
+    _need(d_k, "d_k", torch.bfloat16, tuple(k.shape), dev)
+    _need(d_v, "d_v", torch.bfloat16, tuple(v.shape), dev)
+    scale = 1.0 / math.sqrt(d_h) if softmax_scale is None else float(softmax_scale)
+    L = lib()
+    nbytes = int(L.msa_sparse_attn_backward_workspace_size(seqs.ref(), H_q, H_kv, d_h, block_size, topk))
+    ws = _workspace(nbytes, dev, workspace)
+    st = L.msa_sparse_attn_backward(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(d_o), _ptr(block_ids),
+                                    seqs.ref(), H_q, H_kv, d_h, block_size, topk, scale, _ptr(d_q), _ptr(d_k),
+                                    _ptr(d_v), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(),
+                                    _stream())
+    _check(st, "msa_sparse_attn_backward")
+    return d_q, d_k, d_v
+
+
 def profile_enable(on: bool = True) -> None:
     """Bracket every kernel of later calls with HIP events on its stream."""
     _check(lib().msa_profile_enable(1 if on else 0), "msa_profile_enable")

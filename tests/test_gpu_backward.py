@@ -1,0 +1,206 @@
+"""Training backward of the Main Branch (msa_sparse_attn_backward) against the
+oracle's float64 gradients.
+
+Block selections come from the seeded score-free generator (the structure of
+a Top-k output), so these cases test the backward alone; O and LSE are the
+library's own forward outputs, as in training.  Bar: check_grad (tests/util).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.msa_oracle as O
+from paper_2606_13392_amd import msa, synth
+from tests.util import check_grad, from_dev_bits, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    msa.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+# name, q_rows, kv_lens, H_q, H_kv, topk, kv_pad_to
+CASES = [
+    ("bwd_T1000_g8", [1000], [1000], 16, 2, 8, None),
+    ("bwd_ragged_T333_g4", [333], [333], 8, 2, 5, None),
+    ("bwd_g16", [300], [300], 32, 2, 4, None),
+    ("bwd_g1", [200], [200], 4, 4, 3, None),
+    ("bwd_g3", [150], [150], 6, 2, 4, None),
+    ("bwd_chunked_varlen", [130, 0, 64, 1, 257], [700, 300, 64, 900, 1500], 16, 4, 6, None),
+    ("bwd_decode_padded", [1, 1, 1, 1, 1], [3000, 64, 65, 4097, 1], 16, 4, 6, 4160),
+    ("bwd_many_items_k32", [2048], [2048], 16, 2, 32, None),
+]
+
+
+def _setup(name, q_rows, kv_lens, H_q, H_kv, topk, pad):
+    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, topk=topk,
+                             seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
+    x = {k: v for k, v in synth.generate_numpy(p).items() if k in ("q", "k", "v")}
+    x["d_o"] = synth.generate_grad_numpy(p)
+    ids = synth.random_block_ids(p)
+    return p, x, ids
+
+
+def _run(p, x, ids, workspace_bytes=None):
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    ids_d = torch.from_numpy(ids).to(dev)
+    fwd = msa.sparse_attn_decode if p.max_q_rows == 1 else msa.sparse_attn_prefill
+    o, lse = fwd(d["q"], d["k"], d["v"], ids_d, seqs, p.block_size)
+    if workspace_bytes is None:
+        dq, dk, dv = msa.sparse_attn_backward(d["q"], d["k"], d["v"], o, lse, d["d_o"], ids_d, seqs, p.block_size)
+    else:
+        dq, dk, dv = (torch.empty_like(d[t]) for t in ("q", "k", "v"))
+        ws = torch.empty(workspace_bytes, dtype=torch.uint8, device=dev)
+        st = msa.lib().msa_sparse_attn_backward(
+            d["q"].data_ptr(), d["k"].data_ptr(), d["v"].data_ptr(), o.data_ptr(), lse.data_ptr(),
+            d["d_o"].data_ptr(), ids_d.data_ptr(), seqs.ref(), p.num_q_heads, p.num_kv_heads, p.head_dim,
+            p.block_size, ids.shape[2], 1.0 / math.sqrt(p.head_dim), dq.data_ptr(), dk.data_ptr(), dv.data_ptr(),
+            ws.data_ptr(), workspace_bytes, msa._stream())
+        assert st == 0, msa.lib().msa_strerror(st)
+    torch.cuda.synchronize()
+    return (t.float().cpu().numpy() for t in (dq, dk, dv))
+
+
+def _check_all(name, got, ref):
+    for t, g, r in zip(("dQ", "dK", "dV"), got, ref):
+        stats = check_grad(g, r, f"{name} {t}")
+        _say(f"  {t} max-err/max|ref| {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_backward_small(case):
+    name = case[0]
+    _say(f"[case] {name}")
+    p, x, ids = _setup(*case)
+    got = list(_run(p, x, ids))
+    ref = O.sparse_attention_backward(x["q"], x["k"], x["v"], x["d_o"], ids, O.layout_of(p), p.block_size)
+    _check_all(name, got, ref)
+    # key rows outside every sequence (cache padding) and keys nobody attends are exactly zero
+    lay = O.layout_of(p)
+    used = np.zeros(got[1].shape[:2], dtype=bool)
+    for r in range(p.total_q_rows):
+        s, pos = lay.locate(r)
+        for g in range(p.num_kv_heads):
+            used[p.kv_starts[s] + O.selected_tokens(ids[r, g], pos, p.block_size), g] = True
+    assert np.all(got[1][~used] == 0) and np.all(got[2][~used] == 0)
+
+
+def test_backward_chunked_workspace_and_reproducibility():
+    """A workspace below the one-chunk size runs several row chunks and meets
+    the same bar.  dQ sums its slot partials in slot order, so it is equal bit
+    for bit across runs and chunkings; dK and dV add a block's queries in the
+    run-time order of the reverse index, so only the bar applies to them."""
+    case = ("bwd_chunks", [700, 900], [700, 1200], 16, 2, 6, None)
+    _say("[case] bwd_chunks")
+    p, x, ids = _setup(*case)
+    seqs_h = msa.Seqs.from_problem(p, torch.device("cuda"))
+    full = msa.sparse_attn_backward_workspace_size(seqs_h, p.num_q_heads, p.num_kv_heads, p.head_dim,
+                                                   p.block_size, p.topk)
+    one = list(_run(p, x, ids))
+    again = list(_run(p, x, ids))
+    assert np.array_equal(one[0], again[0]), "dQ is not reproducible"
+    small = list(_run(p, x, ids, workspace_bytes=int(full * 0.4)))
+    ref = O.sparse_attention_backward(x["q"], x["k"], x["v"], x["d_o"], ids, O.layout_of(p), p.block_size)
+    _check_all("bwd_chunks (one chunk)", one, ref)
+    _check_all("bwd_chunks (small workspace)", small, ref)
+    assert np.array_equal(one[0], small[0]), "chunked dQ differs from the one-chunk dQ"
+
+
+def test_backward_rejects_block_128():
+    p = synth.packed_problem("bwd_bk128", [10], [10], num_q_heads=8, num_kv_heads=2, topk=2, seed=1)
+    seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 2) == 0
+
+
+def test_backward_workload_sampled():
+    """Full-size 32K prefill (64 query / 8 KV heads, k 32, B_k 64; block ids
+    from msa_index_topk): dQ of sampled rows and dK / dV of the last two key
+    blocks against the oracle (every row that selected those blocks is
+    recomputed), and two identities over all keys: sum_j dV_j = sum_i dO_i per
+    group (each row's P sums to 1) and sum_j dK_j = 0 (each row's dS sums to 0)."""
+    p = synth.workload("prefill_32k")
+    _say("[case] backward prefill_32k sampled")
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = synth.generate_torch(p, dev, tensors=("index_q", "index_k", "q", "k", "v", "d_o"))
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    del d["index_q"], d["index_k"]
+    o, lse = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    dq, dk, dv = msa.sparse_attn_backward(d["q"], d["k"], d["v"], o, lse, d["d_o"], ids, seqs, p.block_size)
+    torch.cuda.synchronize()
+    lay = O.layout_of(p)
+    G, H_kv, B = p.group_size, p.num_kv_heads, p.block_size
+    scale = 1.0 / math.sqrt(p.head_dim)
+    ids_h = ids.cpu().numpy()
+
+    def row_grads(r, g):
+        s, pos = lay.locate(r)
+        toks = O.selected_tokens(ids_h[r, g], pos, B)
+        tt = torch.from_numpy(p.kv_starts[s] + toks).to(dev)
+        hs = slice(g * G, (g + 1) * G)
+        qh = O.decode_bf16(from_dev_bits(d["q"][r, hs]))
+        gh = O.decode_bf16(from_dev_bits(d["d_o"][r, hs]))
+        kk = O.decode_bf16(from_dev_bits(d["k"][tt, g]))
+        vv = O.decode_bf16(from_dev_bits(d["v"][tt, g]))
+        return toks, O.attend_backward(qh, kk, vv, gh, scale)
+
+    # dQ of sampled rows
+    rng = np.random.default_rng(p.seed)
+    rows = sorted(set(int(r) for r in rng.integers(0, p.total_q_rows, size=12)) | {0, p.total_q_rows - 1})
+    dq_ref = np.zeros((len(rows), p.num_q_heads, p.head_dim))
+    for i, r in enumerate(rows):
+        for g in range(H_kv):
+            dq_ref[i, g * G:(g + 1) * G] = row_grads(r, g)[1][0]
+    rows_t = torch.tensor(rows, dtype=torch.int64, device=dev)
+    stats = check_grad(dq[rows_t].float().cpu().numpy(), dq_ref, "dQ sampled rows")
+    _say(f"  dQ ({len(rows)} rows) max-err/max|ref| {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+
+    # dK / dV of the last two key blocks: every (row, group) that selected them
+    nblk = p.kv_lens[0] // B
+    for b in (nblk - 2, nblk - 1):
+        k_ref = np.zeros((B, H_kv, p.head_dim))
+        v_ref = np.zeros_like(k_ref)
+        for g in range(H_kv):
+            sel_rows = np.nonzero((ids_h[:, g, :] == b).any(axis=1))[0]
+            for r in sel_rows:
+                toks, (_, dkr, dvr) = row_grads(int(r), g)
+                m = (toks >= b * B) & (toks < (b + 1) * B)
+                k_ref[toks[m] - b * B, g] += dkr[m]
+                v_ref[toks[m] - b * B, g] += dvr[m]
+        sl = slice(b * B, (b + 1) * B)
+        sk = check_grad(dk[sl].float().cpu().numpy(), k_ref, f"dK block {b}")
+        sv = check_grad(dv[sl].float().cpu().numpy(), v_ref, f"dV block {b}")
+        _say(f"  block {b}: dK {sk[0]:.2e}/{sk[1]:.2e} dV {sv[0]:.2e}/{sv[1]:.2e} (max-err/max|ref|, rel-L2)")
+
+    # identities over every key
+    sum_dv = dv.double().sum(dim=0)                                   # (H_kv, d)
+    sum_do = d["d_o"].double().view(p.total_q_rows, H_kv, G, p.head_dim).sum(dim=(0, 2))
+    rel = float((sum_dv - sum_do).norm() / sum_do.norm())
+    _say(f"  sum dV vs sum dO rel {rel:.2e}")
+    assert rel < 1e-2
+    sum_dk = dk.double().sum(dim=0)
+    ratio = float(sum_dk.norm() / dk.double().abs().sum(dim=0).norm())
+    _say(f"  |sum dK| / |sum |dK|| {ratio:.2e}")
+    assert ratio < 1e-2
+    del d, o, lse, dq, dk, dv, ids
+    torch.cuda.empty_cache()

@@ -58,3 +58,27 @@ def check_outputs(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse
     assert rel <= O_REL_L2, f"{what} O rel-L2 {rel:.3e}"
     assert lerr.max() <= O_MAX_ABS, f"{what} LSE max-abs {lerr.max():.3e}"
     return float(err.max()), float(rel), float(lerr.max())
+
+
+# Gradients of the training backward: each element is a sum of products in
+# which one factor (P or dS) is rounded to bf16 for the MFMA (relative 2^-9),
+# accumulated in fp32 and rounded once to bf16 on output (2^-9).  dQ and dK
+# sum terms of both signs (the dS of a row sums to zero), so the error is
+# bounded relative to the tensor's scale rather than to each element:
+# |err| <= GRAD_MAX_ABS_REL * max|ref| + 2^-9 |ref| element-wise and
+# relative L2 <= GRAD_REL_L2 per tensor.
+GRAD_MAX_ABS_REL = 1e-2
+GRAD_REL_L2 = 1e-2
+
+
+def check_grad(got: np.ndarray, ref: np.ndarray, what=""):
+    got = got.astype(np.float64)
+    err = np.abs(got - ref)
+    scale = max(float(np.abs(ref).max()), 1e-30)
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+    bound = GRAD_MAX_ABS_REL * scale + BF16_HALF_ULP_REL * np.abs(ref)
+    worst = np.unravel_index(np.argmax(err - bound), err.shape)
+    assert (err <= bound).all(), \
+        f"{what} error {err[worst]:.3e} > bound {bound[worst]:.3e} at {worst} (max|ref| {scale:.3e})"
+    assert rel <= GRAD_REL_L2, f"{what} rel-L2 {rel:.3e}"
+    return float(err.max() / scale), float(rel)
