@@ -10,7 +10,7 @@
 // Key blocks are iterated on the outside (the reverse index of kvo_index.h):
 // dK and dV of a block stay in registers while the queries that selected it
 // stream past, each incidence costs a gather of its Q and dO rows, and its dQ
-// contribution goes as an fp32 partial into the incidence's slot.  No
+// contribution goes as a bf16 partial into the incidence's slot.  No
 // atomics touch a gradient: dQ sums its slot partials in slot order (bit-
 // reproducible); dK and dV sum a block's queries in the order of its handle
 // list, which the reverse index fills with atomics, so their last bits can
@@ -19,17 +19,16 @@
 //   bwd_delta        D per (row, head)
 //   per chunk of query rows:
 //     reverse index  (kvo_index.h)
-//     bwd_kvo        persistent CTAs of 8 waves over the work items (<= 256
-//                    queries of one tile).  K, V and K^T of the block sit in
-//                    LDS.  A CTA pass takes 64 gathered (query, head) rows;
-//                    wave (kq, rg) owns keys 16kq .. 16kq+15 and rows
-//                    32rg .. 32rg+31 of the pass: S = Q K^T and dP = dO V^T
-//                    (MFMA 16x16x32, one key per lane column), then
-//                    dV += P^T dO and dK += dS^T Q from transposed copies of
-//                    the pass's Q and dO rows, then dQ over all 64 keys for
-//                    dims 32kq .. 32kq+31 from dS staged in LDS.  At the end
-//                    of an item the 2 row groups' dK / dV are summed in LDS
-//                    and written as the item's partial.
+//     bwd_kvo        persistent CTAs of 4 waves, two per CU, over the work
+//                    items (<= 256 queries of one tile).  K, V and K^T of the
+//                    block sit in LDS.  A CTA pass takes 32 gathered (query,
+//                    head) rows; wave kq owns keys 16kq .. 16kq+15: S = Q K^T
+//                    and dP = dO V^T (MFMA 16x16x32, one key per lane column),
+//                    then dV += P^T dO and dK += dS^T Q from transposed copies
+//                    of the pass's Q and dO rows, then dQ over all 64 keys
+//                    for dims 32kq .. 32kq+31 from dS staged in LDS.  At the
+//                    end of an item each wave writes its keys' dK / dV as the
+//                    item's partial.
 //     bwd_tile_reduce  per tile: its items' partials, in order, added to fp32
 //                    dK / dV accumulators
 //     bwd_dq_combine per (row, group): the valid slots' partials in slot order,
@@ -40,10 +39,11 @@
 namespace {
 
 constexpr int kBwdBK = 64;
-constexpr int kBwdRowGroups = 2;
-constexpr int kBwdWaves = 4 * kBwdRowGroups;          // 4 key quarters x 2 row groups
+constexpr int kBwdRowGroups = 1;                      // 32-row groups per CTA pass
+constexpr int kBwdWaves = 4 * kBwdRowGroups;          // 4 key quarters
 constexpr int kBwdThreads = 64 * kBwdWaves;
 constexpr int kBwdPassRows = 32 * kBwdRowGroups;      // gathered (query, head) rows per CTA pass
+static_assert(kBwdRowGroups == 1, "dK / dV of a key quarter live in one wave");
 constexpr int kPartFloats = 2 * kBwdBK * kHeadDim;    // dK and dV of one work item
 
 struct BwdSmem {
@@ -56,14 +56,12 @@ struct BwdSmem {
   float lse2[kBwdPassRows];                           // LSE * log2(e) per pass row (+inf: no row)
   float dlt[kBwdPassRows];                            // D per pass row
   int32_t rpos[kBwdPassRows];                         // absolute position per pass row (-1: no row)
-  int64_t dqoff[kBwdPassRows];                        // float offset of the row's dQ partial (-1: no row)
+  int64_t dqoff[kBwdPassRows];                        // element offset of the row's dQ partial (the trash row: no row)
   int32_t s_row[kItemQueries];                        // query row inside the chunk
   int32_t s_slot[kItemQueries];                       // slot of this block in the row's id list
-  int32_t s_pos[kItemQueries];                        // absolute position of the query
 };
-// the item-end reduction reuses qt and dot: 4 key quarters x 32 registers x 64 lanes
-static_assert(sizeof(uint16_t) * 2 * kHeadDim * (kBwdPassRows + 8) >= 4 * 32 * 64 * sizeof(float),
-              "reduction scratch");
+// two CTAs per CU
+static_assert(sizeof(BwdSmem) <= 80 * 1024, "LDS of a backward CTA");
 
 __device__ __forceinline__ uint16_t raw_elem(const u32x4& w, int j) {
   return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
@@ -100,12 +98,12 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restri
 // t, rows 16t + 4qd + i (i = 0..3).  Those 8 rows are the k-slice the lane
 // supplies to dV += P^T dO and dK += dS^T Q (k index 8qd + 4t + i), and
 // the B operands read the same rows from the transposed Q / dO copies.
-__global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
+__global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ d_o, const float* __restrict__ lse, const float* __restrict__ delta, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0, float scale_log2,
-    float* __restrict__ dq_buf, float* __restrict__ part) {
+    uint16_t* __restrict__ dq_buf, int64_t dq_trash, float* __restrict__ part) {
   __shared__ BwdSmem sm;
   constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension
   const int lane = lane_id();
@@ -114,6 +112,8 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
   const int c16 = lane & 15, qd = lane >> 4;
   const int G = H_q / H_kv;
   const int qpw = 32 / G;                             // queries per row group and pass
+  // this lane's A-operand rows 16t + c16: (query within the pass, head)
+  const int jq0 = c16 / G, hh0 = c16 % G, jq1 = (16 + c16) / G, hh1 = (16 + c16) % G;
   const int rows_g = qpw * G;                         // used rows of a row group
   const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
   const int32_t total_items = item_off[ntile];
@@ -136,8 +136,8 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
       const int32_t rl = static_cast<int32_t>(hd >> 6);
       sm.s_row[threadIdx.x] = rl;
       sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
-      sm.s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
     }
+    const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);   // + row in chunk
     if (tile != staged) {
       const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
@@ -173,47 +173,55 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
     for (int t = 0; t < 8; ++t) { acc_dv[t] = f32x4{}; acc_dk[t] = f32x4{}; }
     const int key = key0 + 16 * kq + c16;             // this lane's key in the C layout of S
 
-    for (int c = 0; c < nq; c += kBwdRowGroups * qpw) {
-      // A operands: Q and dO of rows 16t + c16 of this row group, dims 32ks + 8qd .. +8
-      u32x4 bq[2][KS], bdo[2][KS];
-      int64_t hrow[2];
-      bool arow[2];
+    // A operands of a pass: Q and dO of rows 16t + c16 of this row group, dims
+    // 32ks + 8qd .. +8, plus the rows' LSE and D.  The next pass's are
+    // requested as soon as S and dP have consumed the current ones.
+    u32x4 bq[2][KS], bdo[2][KS];
+    int64_t hrow[2];
+    bool arow[2];
+    float lse_v[2], dlt_v[2];
+    auto load_pass = [&](int cc) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const int ra = 16 * t + c16;
-        const int qa = c + rg * qpw + ra / G;
+        const int qa = cc + rg * qpw + (t ? jq1 : jq0);
         arow[t] = ra < rows_g && qa < nq;
-        const int64_t grow = row0 + (arow[t] ? sm.s_row[qa] : 0);
-        hrow[t] = grow * H_q + static_cast<int64_t>(r) * G + ra % G;
+        // rows without a query load a valid row of the item: their P and dS
+        // are zero, so any finite operand values give zero contributions
+        const int64_t grow = row0 + sm.s_row[min(qa, nq - 1)];
+        hrow[t] = grow * H_q + static_cast<int64_t>(r) * G + (t ? hh1 : hh0);
 #pragma unroll
         for (int st = 0; st < KS; ++st) {
-          bq[t][st] = arow[t] ? load_raw(q + hrow[t] * kHeadDim + 32 * st + 8 * qd) : u32x4{};
-          bdo[t][st] = arow[t] ? load_raw(d_o + hrow[t] * kHeadDim + 32 * st + 8 * qd) : u32x4{};
+          bq[t][st] = load_raw(q + hrow[t] * kHeadDim + 32 * st + 8 * qd);
+          bdo[t][st] = load_raw(d_o + hrow[t] * kHeadDim + 32 * st + 8 * qd);
         }
+        lse_v[t] = lse[hrow[t]];
+        dlt_v[t] = delta[hrow[t]];
       }
+    };
+    load_pass(0);
+
+    for (int c = 0; c < nq; c += kBwdRowGroups * qpw) {
       __syncthreads();                                // the previous pass is done with qt, dot, ds, row scalars
       // transposed copies: key quarter kq writes the dims of k-step kq
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const int col = 32 * rg + 16 * t + c16;
+        const u32x4 wq = kq == 0 ? bq[t][0] : kq == 1 ? bq[t][1] : kq == 2 ? bq[t][2] : bq[t][3];
+        const u32x4 wd = kq == 0 ? bdo[t][0] : kq == 1 ? bdo[t][1] : kq == 2 ? bdo[t][2] : bdo[t][3];
 #pragma unroll
-        for (int st = 0; st < KS; ++st) {
-          if (st != kq) continue;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            sm.qt[32 * st + 8 * qd + j][col] = raw_elem(bq[t][st], j);
-            sm.dot[32 * st + 8 * qd + j][col] = raw_elem(bdo[t][st], j);
-          }
+        for (int j = 0; j < 8; ++j) {
+          sm.qt[32 * kq + 8 * qd + j][col] = raw_elem(wq, j);
+          sm.dot[32 * kq + 8 * qd + j][col] = raw_elem(wd, j);
         }
         if (qd == 0 && kq == 0) {
-          const int ra = 16 * t + c16;
-          const int qa = c + rg * qpw + ra / G;
-          sm.lse2[col] = arow[t] ? lse[hrow[t]] * kLog2e : INFINITY;
-          sm.dlt[col] = arow[t] ? delta[hrow[t]] : 0.f;
-          sm.rpos[col] = arow[t] ? sm.s_pos[qa] : -1;
+          const int qa = c + rg * qpw + (t ? jq1 : jq0);
+          sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
+          sm.dlt[col] = arow[t] ? dlt_v[t] : 0.f;
+          sm.rpos[col] = arow[t] ? pos_base + sm.s_row[qa] : -1;
           sm.dqoff[col] = arow[t] ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G +
-                                     ra % G) * kHeadDim
-                                  : -1;
+                                     (t ? hh1 : hh0)) * kHeadDim
+                                  : dq_trash;
         }
       }
       __syncthreads();
@@ -233,6 +241,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
         }
       }
       __builtin_amdgcn_sched_barrier(0);
+      if (c + kBwdRowGroups * qpw < nq) load_pass(c + kBwdRowGroups * qpw);
       // P and dS in place: lane holds rows 16t + 4qd + i
 #pragma unroll
       for (int t = 0; t < 2; ++t)
@@ -271,6 +280,7 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
         const uint16_t* qr = &sm.qt[16 * t + c16][32 * rg + 4 * qd];
         acc_dv[t] = mfma16x16x32(pa, lds_pair_bf16x8(dr, dr + 16), acc_dv[t]);
         acc_dk[t] = mfma16x16x32(sa, lds_pair_bf16x8(qr, qr + 16), acc_dk[t]);
+        if (t & 1) __builtin_amdgcn_sched_barrier(0);   // bound the operand reads in flight
       }
       __syncthreads();                                // dS of all 4 key quarters in LDS
 
@@ -287,36 +297,31 @@ __global__ __launch_bounds__(kBwdThreads, 1) void bwd_kvo_kernel(
                                        ld_bf16x8(&sm.kt[32 * kq + 16 * u + c16][32 * ks + 8 * qd]), acc_q[t][u]);
         }
       __builtin_amdgcn_sched_barrier(0);
-      // fp32 partial of each valid row into its incidence's slot
+      // bf16 partial of each row into its incidence's slot: lanes c16 and
+      // c16 ^ 1 swap values so that each stores one bf16 pair (even lanes
+      // dims c16, c16 + 1; odd lanes dims 15 + c16, 16 + c16); rows without a
+      // query write the trash row (no branch around the stores)
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int64_t off = sm.dqoff[32 * rg + 16 * t + 4 * qd + i];
-          if (off >= 0) {
-            float* dst = dq_buf + off + 32 * kq + c16;
-            dst[0] = acc_q[t][0][i];
-            dst[16] = acc_q[t][1][i];
-          }
+          const float v0 = acc_q[t][0][i], v1 = acc_q[t][1][i];
+          const bool odd = c16 & 1;
+          const float mine = odd ? v1 : v0;
+          const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(odd ? v0 : v1)));
+          const uint32_t pair = odd ? pack_bf16x2(other, mine) : pack_bf16x2(mine, other);
+          uint16_t* dst = dq_buf + sm.dqoff[32 * rg + 16 * t + 4 * qd + i] + 32 * kq + (odd ? 15 + c16 : c16);
+          *reinterpret_cast<uint32_t*>(dst) = pair;
         }
     }
 
-    // item end: rg 1 hands its dV / dK to rg 0 through LDS; rg 0 writes the
-    // item's partial [tensor][kq][reg][lane]
-    float* red = reinterpret_cast<float*>(&sm.qt[0][0]);
+    // item end: the item's dV / dK partial, [tensor][kq][reg][lane]
 #pragma unroll
     for (int tensor = 0; tensor < 2; ++tensor) {
-      f32x4* acc = tensor == 0 ? acc_dv : acc_dk;
-      __syncthreads();
-      if (rg == 1)
+      const f32x4* acc = tensor == 0 ? acc_dv : acc_dk;
+      float* dst = part + (static_cast<int64_t>(item) * 2 + tensor) * (4 * 32 * 64) + kq * (32 * 64) + lane;
 #pragma unroll
-        for (int reg = 0; reg < 32; ++reg) red[(kq * 32 + reg) * 64 + lane] = acc[reg >> 2][reg & 3];
-      __syncthreads();
-      if (rg == 0) {
-        float* dst = part + (static_cast<int64_t>(item) * 2 + tensor) * (4 * 32 * 64) + kq * (32 * 64) + lane;
-#pragma unroll
-        for (int reg = 0; reg < 32; ++reg) dst[reg * 64] = acc[reg >> 2][reg & 3] + red[(kq * 32 + reg) * 64 + lane];
-      }
+      for (int reg = 0; reg < 32; ++reg) dst[reg * 64] = acc[reg >> 2][reg & 3];
     }
   }
 }
@@ -357,7 +362,8 @@ constexpr int kCombWaves = 4;
 
 __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
     const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_q, int H_kv,
-    int topk, int64_t row0, int64_t nrows, const float* __restrict__ dq_buf, float scale, uint16_t* __restrict__ dq) {
+    int topk, int64_t row0, int64_t nrows, const uint16_t* __restrict__ dq_buf, float scale,
+    uint16_t* __restrict__ dq) {
   const int lane = lane_id();
   const int64_t pr = static_cast<int64_t>(blockIdx.x) * kCombWaves + threadIdx.x / kWave;
   if (pr >= nrows * H_kv) return;
@@ -368,19 +374,26 @@ __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
   int s;
   const int p = row_position(sq, row, &s);
   const int32_t* ids = block_ids + (row * H_kv + r) * topk;
-  const int E = G * kHeadDim;                         // floats of one slot
-  const float* src = dq_buf + pr * topk * static_cast<int64_t>(E);
+  const int E = G * kHeadDim;                         // elements of one slot
+  const uint16_t* src = dq_buf + pr * topk * static_cast<int64_t>(E);
   uint16_t* dst = dq + (row * H_q + static_cast<int64_t>(r) * G) * kHeadDim;
-  for (int c4 = lane; c4 < E / 4; c4 += kWave) {
-    f32x4 acc = f32x4{};
+  for (int c8 = lane; c8 < E / 8; c8 += kWave) {
+    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     for (int j = 0; j < topk; ++j) {
       if (!incidence_ok(ids[j], p, kBwdBK, blk_base, s)) continue;
-      acc += *reinterpret_cast<const f32x4*>(src + static_cast<int64_t>(j) * E + 4 * c4);
+      const u32x4 w = load_raw(src + static_cast<int64_t>(j) * E + 8 * c8);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] += __uint_as_float(w[e] << 16);
+        acc[2 * e + 1] += __uint_as_float(w[e] & 0xFFFF0000u);
+      }
     }
-    uint2 w;
-    w.x = pack_bf16x2(acc[0] * scale, acc[1] * scale);
-    w.y = pack_bf16x2(acc[2] * scale, acc[3] * scale);
-    *reinterpret_cast<uint2*>(dst + 4 * c4) = w;
+    uint4 o;
+    o.x = pack_bf16x2(acc[0] * scale, acc[1] * scale);
+    o.y = pack_bf16x2(acc[2] * scale, acc[3] * scale);
+    o.z = pack_bf16x2(acc[4] * scale, acc[5] * scale);
+    o.w = pack_bf16x2(acc[6] * scale, acc[7] * scale);
+    *reinterpret_cast<uint4*>(dst + 8 * c8) = o;
   }
 }
 
@@ -427,7 +440,7 @@ void bwd_layout(BwdPlan& pl, const msa_seqs* seqs, int H_q, int H_kv, int topk) 
   pl.max_items = pl.ntile + static_cast<int64_t>((inc + kItemQueries - 1) / kItemQueries);
   pl.off_handles = o;  o = align_up(o + sizeof(uint32_t) * inc, 256);
   pl.off_tpos = o;     o = align_up(o + sizeof(int32_t) * inc, 256);
-  pl.off_dq = o;       o = align_up(o + sizeof(float) * inc * (H_q / H_kv) * kHeadDim, 256);
+  pl.off_dq = o;       o = align_up(o + sizeof(uint16_t) * (inc * (H_q / H_kv) + 1) * kHeadDim, 256);   // + trash row
   pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * kPartFloats, 256);
   pl.total = o;
 }
@@ -515,7 +528,7 @@ extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void
   auto* dv_acc = reinterpret_cast<float*>(ws + pl.off_dv);
   auto* handles = reinterpret_cast<uint32_t*>(ws + pl.off_handles);
   auto* tpos = reinterpret_cast<int32_t*>(ws + pl.off_tpos);
-  auto* dq_buf = reinterpret_cast<float*>(ws + pl.off_dq);
+  auto* dq_buf = reinterpret_cast<uint16_t*>(ws + pl.off_dq);
   auto* part = reinterpret_cast<float*>(ws + pl.off_part);
   const msa_seqs sq = *seqs;
   const int64_t kv_floats = seqs->total_kv_rows * H_kv * static_cast<int64_t>(kHeadDim);
@@ -544,7 +557,8 @@ extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void
                      static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(d_o), lse,
                      static_cast<const float*>(delta), sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
-                     static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf, part);
+                     static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf,
+                     static_cast<int64_t>(pl.chunk_rows) * H_kv * topk * (H_q / H_kv) * kHeadDim, part);
     msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc,
@@ -552,7 +566,7 @@ extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void
     msa_prof::launch("bwd_dq_combine_kernel", bwd_dq_combine_kernel,
                      dim3(static_cast<unsigned>((nr * H_kv + kCombWaves - 1) / kCombWaves)), dim3(64 * kCombWaves),
                      0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_q, H_kv, topk, r0, nr,
-                     static_cast<const float*>(dq_buf), softmax_scale, static_cast<uint16_t*>(d_q));
+                     static_cast<const uint16_t*>(dq_buf), softmax_scale, static_cast<uint16_t*>(d_q));
   }
   if (kv_floats > 0)
     msa_prof::launch("bwd_kv_convert_kernel", bwd_kv_convert_kernel, dim3(zero_blocks), dim3(256), 0, stream,
