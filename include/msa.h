@@ -15,6 +15,7 @@
  *   msa_sparse_attn_*_fp8    Main Branch on e4m3 queries and KV cache
  *   msa_dense_attn           dense causal GQA attention (the comparison baseline)
  *   msa_sparse_attn_backward training: Main Branch gradients dQ, dK, dV
+ *   msa_sparse_kl_backward   training: sparse KL loss and its index-projection gradients
  *
  * Conventions shared by every call
  * --------------------------------
@@ -246,6 +247,48 @@ int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const 
                              int head_dim, int block_size, int topk, float softmax_scale,
                              void* d_q, void* d_k, void* d_v, void* workspace,
                              size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * msa_sparse_kl_backward -- the sparse KL loss that trains the Index Branch.
+ *
+ * Sec. 3.2 ("KL Loss"), per query row i and group r, over the causally
+ * visible tokens T of the selected blocks: the student
+ * P_idx_j = softmax_j(q_idx[i,r] . k_idx[j] / sqrt(d_idx)) and the detached
+ * teacher P_j = (1/G) sum over the group's query heads h of
+ * exp(softmax_scale q[i,h] . k[j,r] - lse[i,h]) (Alg. 1: the Main Branch
+ * attention over the same tokens; lse is the forward's LSE, Sec. 4.3 "LSE
+ * fusion").  Outputs, with Delta_j = P_idx_j - P_j:
+ *   kl[i, r]        = sum_j P_j (ln P_j - ln P_idx_j)          (optional)
+ *   d_index_q[i, r] = grad_scale / sqrt(d_idx) sum_j Delta_j k_idx[j]
+ *   d_index_k[j]    = grad_scale / sqrt(d_idx) sum_{i,r} Delta_ij q_idx[i, r]
+ * i.e. grad_scale times the gradients of sum_{i,r} kl[i, r]; the paper's
+ * per-layer loss is the mean over rows and groups, so a training loop passes
+ * grad_scale = lambda / (total_q_rows * num_kv_heads).  Nothing flows into q
+ * or k (the gradient detach of Sec. 3.2).
+ *
+ *   index_q    bf16 [total_q_rows, num_kv_heads, d_idx]
+ *   index_k    bf16 [total_kv_rows, d_idx]
+ *   q, k       bf16 as for msa_sparse_attn_prefill; lse fp32 [total_q_rows, num_q_heads]
+ *   block_ids  int32 [total_q_rows, num_kv_heads, topk]   the selection the forward used
+ *   d_index_q  bf16 [total_q_rows, num_kv_heads, d_idx]   OUTPUT
+ *   d_index_k  bf16 [total_kv_rows, d_idx]                OUTPUT; every row written
+ *   kl         fp32 [total_q_rows, num_kv_heads]          OUTPUT, or NULL to skip
+ *
+ * Workspace, stream and error behaviour as for msa_sparse_attn_prefill.
+ * d_index_q and kl are bit-reproducible; d_index_k adds a key block's queries
+ * in an order fixed at run time.  Supported: d_idx in {64, 128};
+ * head_dim == 128; block_size == 64; 1 <= topk <= 64;
+ * 1 <= num_q_heads / num_kv_heads <= 16; num_kv_heads <= 64.
+ * ------------------------------------------------------------------------ */
+size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,
+                                             int num_kv_heads, int d_idx, int head_dim,
+                                             int block_size, int topk);
+int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void* q, const void* k,
+                           const float* lse, const int32_t* block_ids, const msa_seqs* seqs,
+                           int num_q_heads, int num_kv_heads, int d_idx, int head_dim,
+                           int block_size, int topk, float softmax_scale, float grad_scale,
+                           void* d_index_q, void* d_index_k, float* kl, void* workspace,
+                           size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing (a measurement aid; no part of the attention path)

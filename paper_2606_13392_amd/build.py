@@ -11,7 +11,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libmsa.so")
-SOURCES = ["index_topk.hip", "sparse_attn.hip", "sparse_attn_prefill.hip", "sparse_attn_backward.hip", "dense_attn.hip",
+SOURCES = ["index_topk.hip", "sparse_attn.hip", "sparse_attn_prefill.hip", "sparse_attn_backward.hip",
+           "sparse_kl_backward.hip", "dense_attn.hip",
            "msa_profile.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

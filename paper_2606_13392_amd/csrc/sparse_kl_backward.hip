@@ -1,0 +1,678 @@
+// Sparse KL loss of the Index Branch on gfx950: gradients and loss terms.
+//
+// Sec. 3.2 ("KL Loss"): for query row i and group r, over the causally
+// visible tokens T of the selected blocks, the student is
+// P_idx = softmax(s_idx q_idx . k_idx_j) and the teacher is the mean over the
+// group's G heads of the Main Branch softmax distributions,
+// P = (1/G) sum_h softmax(s q_h . k_j).  The teacher is detached and, by the
+// gradient detach of Sec. 3.2, no gradient reaches Q or K; with
+// Delta_j = P_idx_j - P_j (the derivative of the KL with respect to the
+// student's logit j):
+//   d q_idx_i = s_idx sum_j Delta_j k_idx_j,
+//   d k_idx_j = s_idx sum_{i, r} Delta_ij q_idx_ir,
+//   KL_ir     = sum_j P_j (ln P_j - ln P_idx_j).
+// The teacher's per-head normalisers are the forward's LSE (Sec. 4.3, "LSE
+// fusion"); the student's LSE_idx is reduced over the selected blocks from
+// per-block log-sum-exps (Sec. 4.3) computed in a first key-block-outer
+// sweep.  Both sweeps use the reverse index of kvo_index.h, per chunk of
+// query rows:
+//   kl_lse           per incidence: ln sum_j exp(s_idx S_idx_j) over the block's visible keys
+//   kl_lse_combine   per (row, group): LSE_idx over the valid slots
+//   kl_grad          per work item (<= 256 queries of one tile): P, P_idx and
+//                    Delta on MFMA 16x16x32; d k_idx of the block in registers
+//                    (an fp32 partial per item), d q_idx and the KL term of
+//                    every incidence as fp32 partials
+//   kl_tile_reduce   per key block: the items of every group's tile, in
+//                    order, added to the fp32 d k_idx accumulator
+//   kl_combine       per (row, group): d q_idx and KL over the valid slots, in
+//                    slot order
+// and at the end kl_convert (accumulator times grad_scale to bf16).  No
+// atomics touch a result except the reverse index's handle order, which
+// fixes the order in which a block's queries add into d k_idx.
+#include "kvo_index.h"
+
+namespace {
+
+constexpr int kKlBK = 64;
+constexpr int kKlThreads = 256;                       // 4 waves: key quarters
+constexpr int kKlRows = 32;                           // gathered (query, head) rows per pass
+
+template <int D>
+struct KlSmem {
+  uint16_t k[kKlBK][kHeadDim + 8];                    // K block (Main Branch head r), row-major
+  uint16_t ki[kKlBK][D + 8];                          // index-key block, row-major
+  uint16_t kit[D][kKlBK + 8];                         // index-key block transposed
+  uint16_t qit[D][32 + 8];                            // index queries of the pass, transposed
+  float pl[kKlBK][kKlRows + 4];                       // P of the pass, [key][row]
+  uint16_t dl[32][kKlBK + 8];                         // Delta of the pass (bf16), [query][key]
+  float kls[4][32];                                   // KL term per (key quarter, query)
+  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row
+  float lsei2[32];                                    // LSE_idx * log2(e) per query (+inf: none)
+  int32_t qpos[32];                                   // position per query (-1: none)
+  int64_t incoff[32];                                 // incidence index per query (the trash slot: none)
+  int32_t s_row[kItemQueries];
+  int32_t s_slot[kItemQueries];
+};
+
+__device__ __forceinline__ uint16_t raw_elem16(const u32x4& w, int j) {
+  return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
+}
+
+// Stage the index-key block (row-major and transposed) of keys key0 .. key0+63.
+template <int D, typename Smem>
+__device__ __forceinline__ void stage_index_keys(Smem& sm, const uint16_t* __restrict__ ikb, int nkeys) {
+  for (int c = threadIdx.x; c < (kKlBK / 4) * (D / 8); c += kKlThreads) {
+    const int key4 = c / (D / 8), dg = c % (D / 8);
+    u32x4 rows[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key = 4 * key4 + j;
+      rows[j] = key < nkeys ? load_raw(ikb + static_cast<int64_t>(key) * D + 8 * dg) : u32x4{};
+      *reinterpret_cast<u32x4*>(&sm.ki[key][8 * dg]) = rows[j];
+    }
+    if constexpr (sizeof(sm.kit) > 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        uint2 w;
+        w.x = static_cast<uint32_t>(raw_elem16(rows[0], e)) | (static_cast<uint32_t>(raw_elem16(rows[1], e)) << 16);
+        w.y = static_cast<uint32_t>(raw_elem16(rows[2], e)) | (static_cast<uint32_t>(raw_elem16(rows[3], e)) << 16);
+        *reinterpret_cast<uint2*>(&sm.kit[8 * dg + e][4 * key4]) = w;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- LSE_idx
+template <int D>
+struct KlLseSmem {
+  uint16_t ki[kKlBK][D + 8];
+  int32_t s_row[kItemQueries];
+  int32_t s_slot[kItemQueries];
+};
+
+// Per work item: each wave takes 16 queries at a time; S_idx (16 queries x 64
+// keys) on MFMA 16x16x32, masked to the visible keys, reduced to the block's
+// log-sum-exp per query.
+template <int D>
+__global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
+    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
+    const uint32_t* __restrict__ handles, int H_kv, int topk, int64_t nbcap, int64_t row0, float sidx_log2,
+    float* __restrict__ lse_part) {
+  __shared__ KlLseSmem<D> sm;
+  constexpr int KS = D / 32;
+  const int lane = lane_id();
+  const int wave = threadIdx.x / kWave;
+  const int c16 = lane & 15, qd = lane >> 4;
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  int64_t staged = -1;
+  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int64_t gb = tile % nbcap;
+    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+    const SeqGeom g = seq_geom(sq, s);
+    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+    const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
+    __syncthreads();
+    if (static_cast<int>(threadIdx.x) < nq) {
+      const uint32_t hd = handles[h0 + threadIdx.x];
+      sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
+      sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
+    }
+    if (tile != staged) {
+      const uint16_t* ikb = index_k + (g.kv_start + key0) * static_cast<int64_t>(D);
+      for (int c = threadIdx.x; c < kKlBK * (D / 8); c += kKlThreads) {
+        const int key = c / (D / 8), dg = c % (D / 8);
+        *reinterpret_cast<u32x4*>(&sm.ki[key][8 * dg]) =
+            key0 + key < g.kv_len ? load_raw(ikb + static_cast<int64_t>(key) * D + 8 * dg) : u32x4{};
+      }
+      staged = tile;
+    }
+    __syncthreads();
+    for (int c = 16 * wave; c < nq; c += 64) {
+      const int qa = min(c + c16, nq - 1);            // A-operand query of this lane (clamped)
+      const int64_t grow = row0 + sm.s_row[qa];
+      u32x4 a[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) a[ks] = load_raw(index_q + (grow * H_kv + r) * D + 32 * ks + 8 * qd);
+      f32x4 acc[4];
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        acc[kt] = f32x4{};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          acc[kt] = mfma16x16x32(__builtin_bit_cast(bf16x8, a[ks]), ld_bf16x8(&sm.ki[16 * kt + c16][32 * ks + 8 * qd]),
+                                 acc[kt]);
+      }
+      // lane (key 16kt + c16, queries c + 4qd + i)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int qi = c + 4 * qd + i;
+        const int pos = qi < nq ? pos_base + sm.s_row[qi] : -1;
+        float m = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) {
+          const float z = key0 + 16 * kt + c16 <= pos ? acc[kt][i] * sidx_log2 : -INFINITY;
+          acc[kt][i] = z;
+          m = fmaxf(m, z);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
+        const float mm = m == -INFINITY ? 0.f : m;
+        float l = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt) l += exp2f(acc[kt][i] - mm);
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) l += __shfl_xor(l, off);
+        if (c16 == 0 && qi < nq) {
+          const int64_t inc = (static_cast<int64_t>(sm.s_row[qi]) * H_kv + r) * topk + sm.s_slot[qi];
+          lse_part[inc] = l > 0.f ? (mm + __log2f(l)) * kLn2 : -INFINITY;
+        }
+      }
+    }
+  }
+}
+
+// One thread per (row, group) of the chunk: LSE_idx = ln sum over the valid
+// slots of exp(partial).
+__global__ __launch_bounds__(256) void kl_lse_combine_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
+                                                             const int64_t* __restrict__ blk_base, int H_kv, int topk,
+                                                             int64_t row0, int64_t nrows,
+                                                             const float* __restrict__ lse_part,
+                                                             float* __restrict__ lse_idx) {
+  const int64_t pr = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (pr >= nrows * H_kv) return;
+  const int64_t row = row0 + pr / H_kv;
+  const int r = static_cast<int>(pr % H_kv);
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  const float* lp = lse_part + pr * topk;
+  float m = -INFINITY;
+  for (int j = 0; j < topk; ++j)
+    if (incidence_ok(ids[j], p, kKlBK, blk_base, s)) m = fmaxf(m, lp[j]);
+  float l = 0.f;
+  if (m > -INFINITY)
+    for (int j = 0; j < topk; ++j)
+      if (incidence_ok(ids[j], p, kKlBK, blk_base, s)) l += __expf(lp[j] - m);
+  lse_idx[pr] = m > -INFINITY ? m + __logf(l) : -INFINITY;
+}
+
+// ---------------------------------------------------------------- gradients
+// Wave kq owns keys 16kq .. 16kq+15 of the block.  MFMA 16x16x32 lane l =
+// (c16 = l % 16, qd = l / 16).  A pass takes qpw = 32 / G queries x G heads =
+// 32 rows (row 16t + c16 of the A operands; C rows 16t + 4qd + i) and the
+// same qpw queries of the index branch (query tiles of 16).
+template <int D>
+__global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
+    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
+    const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
+    float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
+    float* __restrict__ part) {
+  __shared__ KlSmem<D> sm;
+  constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
+  constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
+  constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
+  const int lane = lane_id();
+  const int kq = threadIdx.x / kWave;
+  const int c16 = lane & 15, qd = lane >> 4;
+  const int G = H_q / H_kv;
+  const int qpw = 32 / G;
+  const int rows_g = qpw * G;
+  const int jq0 = c16 / G, hh0 = c16 % G, jq1 = (16 + c16) / G, hh1 = (16 + c16) % G;
+  const float inv_g = 1.f / static_cast<float>(G);
+  const float sidx_log2 = sidx * kLog2e;
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  int64_t staged = -1;
+
+  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int64_t gb = tile % nbcap;
+    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+    const SeqGeom g = seq_geom(sq, s);
+    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+    const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
+
+    __syncthreads();                                  // the previous item is done with LDS
+    if (static_cast<int>(threadIdx.x) < nq) {
+      const uint32_t hd = handles[h0 + threadIdx.x];
+      sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
+      sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
+    }
+    if (tile != staged) {
+      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      for (int c = threadIdx.x; c < kKlBK * (kHeadDim / 8); c += kKlThreads) {
+        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) =
+            key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
+      }
+      stage_index_keys<D>(sm, index_k + (g.kv_start + key0) * static_cast<int64_t>(D), g.kv_len - key0);
+      staged = tile;
+    }
+    __syncthreads();
+
+    f32x4 acc_dk[NT];                                 // d k_idx: lane column = dim, rows = keys 4qd + i
+#pragma unroll
+    for (int t = 0; t < NT; ++t) acc_dk[t] = f32x4{};
+    const int key = key0 + 16 * kq + c16;             // this lane's key in the C layouts
+
+    for (int c = 0; c < nq; c += qpw) {
+      // Main Branch A operands (rows 16t + c16) and index A operands (queries 16t + c16)
+      u32x4 bq[2][KSM], bi[2][KSI];
+      float lse_v[2];
+      bool arow[2], aq[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int qa = c + (t ? jq1 : jq0);
+        arow[t] = 16 * t + c16 < rows_g && qa < nq;
+        const int64_t grow = row0 + sm.s_row[min(qa, nq - 1)];
+        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + (t ? hh1 : hh0);
+#pragma unroll
+        for (int st = 0; st < KSM; ++st) bq[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
+        lse_v[t] = lse[hrow];
+        const int qb = c + 16 * t + c16;
+        aq[t] = 16 * t + c16 < qpw && qb < nq;
+        const int64_t irow = row0 + sm.s_row[min(qb, nq - 1)];
+#pragma unroll
+        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (irow * H_kv + r) * D + 32 * st + 8 * qd);
+      }
+      __syncthreads();                                // the previous pass is done with qit, pl, dl, kls, scalars
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        // index queries transposed: wave kq writes the k-steps st with st % 4 == kq
+#pragma unroll
+        for (int st = 0; st < KSI; ++st) {
+          if ((st & 3) != kq) continue;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) sm.qit[32 * st + 8 * qd + j][16 * t + c16] = raw_elem16(bi[t][st], j);
+        }
+        if (qd == 0 && kq == 0) {
+          sm.lse2[16 * t + c16] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
+          const int qb = c + 16 * t + c16;
+          if (aq[t]) {
+            const int64_t rl = sm.s_row[qb];
+            const int64_t pr = rl * H_kv + r;
+            sm.lsei2[16 * t + c16] = lse_idx[pr] * kLog2e;
+            sm.qpos[16 * t + c16] = pos_base + static_cast<int>(rl);
+            sm.incoff[16 * t + c16] = pr * topk + sm.s_slot[qb];
+          } else {
+            sm.lsei2[16 * t + c16] = INFINITY;
+            sm.qpos[16 * t + c16] = -1;
+            sm.incoff[16 * t + c16] = trash_inc;
+          }
+        }
+      }
+      __syncthreads();
+
+      // Main Branch P of this key quarter: lane holds key, rows 16t + 4qd + i
+      f32x4 acc_s[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        acc_s[t] = f32x4{};
+#pragma unroll
+        for (int st = 0; st < KSM; ++st)
+          acc_s[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
+                                  ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
+      }
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f32x4 pv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * t + 4 * qd + i;
+          const int qp = row < rows_g ? sm.qpos[row / G] : -1;
+          pv[i] = key <= qp ? exp2f(acc_s[t][i] * s_main_log2 - sm.lse2[row]) : 0.f;
+        }
+        *reinterpret_cast<f32x4*>(&sm.pl[16 * kq + c16][16 * t + 4 * qd]) = pv;
+      }
+      // index scores of this key quarter: lane holds key, queries 16t + 4qd + i
+      f32x4 acc_i[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        acc_i[t] = f32x4{};
+#pragma unroll
+        for (int st = 0; st < KSI; ++st)
+          acc_i[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bi[t][st]),
+                                  ld_bf16x8(&sm.ki[16 * kq + c16][32 * st + 8 * qd]), acc_i[t]);
+      }
+      __syncthreads();                                // P of every row in LDS
+
+      // teacher P (mean over the query's heads), student P_idx, Delta, KL term
+      f32x4 dlt[2];
+      float klq[2][4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int qi = 16 * t + 4 * qd + i;         // query within the pass
+          const bool on = qi < qpw && key <= sm.qpos[qi];
+          float pbar = 0.f;
+          if (qi < qpw)
+            for (int hh = 0; hh < G; ++hh) pbar += sm.pl[16 * kq + c16][qi * G + hh];
+          pbar *= inv_g;
+          const float lz = acc_i[t][i] * sidx_log2 - sm.lsei2[qi];   // log2 P_idx
+          const float pidx = on ? exp2f(lz) : 0.f;
+          dlt[t][i] = pidx - pbar;
+          klq[t][i] = (on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
+        }
+      // d k_idx += Delta^T q_idx over the pass's 32 queries (one k-step):
+      // k index 8qd + 4t + i = query 16t + 4qd + i
+      {
+        uint4 w;
+        w.x = pack_bf16x2(dlt[0][0], dlt[0][1]);
+        w.y = pack_bf16x2(dlt[0][2], dlt[0][3]);
+        w.z = pack_bf16x2(dlt[1][0], dlt[1][1]);
+        w.w = pack_bf16x2(dlt[1][2], dlt[1][3]);
+        const bf16x8 da = __builtin_bit_cast(bf16x8, w);
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          const uint16_t* qr = &sm.qit[16 * t + c16][4 * qd];
+          const uint2 lo = *reinterpret_cast<const uint2*>(qr), hi = *reinterpret_cast<const uint2*>(qr + 16);
+          acc_dk[t] = mfma16x16x32(da, __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y)), acc_dk[t]);
+        }
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            sm.dl[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(w[2 * t + (i >> 1)] >> (16 * (i & 1)));
+      }
+      // KL per query: sum over this wave's 16 keys, then over the 4 waves in LDS
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = klq[t][i];
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
+          if (c16 == 0) sm.kls[kq][16 * t + 4 * qd + i] = v;
+        }
+      __syncthreads();                                // Delta and KL terms of every key in LDS
+
+      // d q_idx of the pass's queries: dims 16n + c16 for n % 4 == kq, over the 64 keys
+#pragma unroll
+      for (int n = kq; n < NT; n += 4) {
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          f32x4 acc = f32x4{};
+#pragma unroll
+          for (int ks = 0; ks < kKlBK / 32; ++ks)
+            acc = mfma16x16x32(ld_bf16x8(&sm.dl[16 * t + c16][32 * ks + 8 * qd]),
+                               ld_bf16x8(&sm.kit[16 * n + c16][32 * ks + 8 * qd]), acc);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            dqp[sm.incoff[16 * t + 4 * qd + i] * D + 16 * n + c16] = acc[i];
+        }
+      }
+      if (kq == 0 && lane < 32)
+        klp[sm.incoff[lane]] = sm.kls[0][lane] + sm.kls[1][lane] + sm.kls[2][lane] + sm.kls[3][lane];
+    }
+
+    // item end: this wave's keys of d k_idx as the item's partial [kq][reg][lane]
+    float* dst = part + static_cast<int64_t>(item) * (kKlBK * D) + kq * (NT * 4 * 64) + lane;
+#pragma unroll
+    for (int reg = 0; reg < NT * 4; ++reg) dst[reg * 64] = acc_dk[reg >> 2][reg & 3];
+  }
+}
+
+// One CTA per key block: the items of the block's tiles of every group, in
+// group and item order, added to the fp32 accumulator of the block's keys.
+template <int D>
+__global__ __launch_bounds__(256) void kl_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
+                                                             const int32_t* __restrict__ item_off, int H_kv,
+                                                             int64_t nbcap, const float* __restrict__ part,
+                                                             float* __restrict__ dk_acc) {
+  constexpr int NT = D / 16;
+  const int64_t gb = blockIdx.x;
+  const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+  const SeqGeom g = seq_geom(sq, s);
+  const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+  bool any = false;
+  for (int r = 0; r < H_kv; ++r) any |= item_off[r * nbcap + gb] != item_off[r * nbcap + gb + 1];
+  if (!any) return;
+  for (int idx = threadIdx.x; idx < kKlBK * D; idx += 256) {
+    float acc = 0.f;
+    for (int r = 0; r < H_kv; ++r) {
+      const int64_t tile = r * nbcap + gb;
+      for (int32_t it = item_off[tile]; it < item_off[tile + 1]; ++it)
+        acc += part[static_cast<int64_t>(it) * (kKlBK * D) + idx];
+    }
+    const int kq = idx / (NT * 4 * 64);
+    const int reg = (idx / 64) % (NT * 4);
+    const int ln = idx & 63;
+    const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
+    const int dim = 16 * (reg >> 2) + (ln & 15);
+    if (key0 + key >= g.kv_len) continue;
+    dk_acc[(g.kv_start + key0 + key) * static_cast<int64_t>(D) + dim] += acc;
+  }
+}
+
+// One wave per (row, group) of the chunk: d q_idx = grad_scale x sum of the
+// valid slots' partials and KL = sum of their terms, in slot order.
+constexpr int kKlCombWaves = 4;
+
+template <int D>
+__global__ __launch_bounds__(64 * kKlCombWaves) void kl_combine_kernel(
+    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_kv, int topk,
+    int64_t row0, int64_t nrows, const float* __restrict__ dqp, const float* __restrict__ klp, float grad_scale,
+    uint16_t* __restrict__ d_index_q, float* __restrict__ kl) {
+  const int lane = lane_id();
+  const int64_t pr = static_cast<int64_t>(blockIdx.x) * kKlCombWaves + threadIdx.x / kWave;
+  if (pr >= nrows * H_kv) return;
+  const int64_t row = row0 + pr / H_kv;
+  const int r = static_cast<int>(pr % H_kv);
+  int s;
+  const int p = row_position(sq, row, &s);
+  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
+  constexpr int PER = D / 64;                         // dims per lane
+  float acc[PER];
+#pragma unroll
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+  float klsum = 0.f;
+  for (int j = 0; j < topk; ++j) {
+    if (!incidence_ok(ids[j], p, kKlBK, blk_base, s)) continue;
+    const int64_t inc = pr * topk + j;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] += dqp[inc * D + PER * lane + e];
+    klsum += klp[inc];
+  }
+  uint16_t* dst = d_index_q + (row * H_kv + r) * static_cast<int64_t>(D) + PER * lane;
+  if constexpr (PER == 1) {
+    dst[0] = f32_to_bf16_bits(acc[0] * grad_scale);
+  } else {
+    *reinterpret_cast<uint32_t*>(dst) = pack_bf16x2(acc[0] * grad_scale, acc[1] * grad_scale);
+  }
+  if (kl && lane == 0) kl[row * H_kv + r] = klsum;
+}
+
+__global__ __launch_bounds__(256) void kl_convert_kernel(const float* __restrict__ acc, int64_t n2, float scale,
+                                                         uint16_t* __restrict__ out) {
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n2;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    reinterpret_cast<uint32_t*>(out)[i] = pack_bf16x2(acc[2 * i] * scale, acc[2 * i + 1] * scale);
+}
+
+// ---------------------------------------------------------------- host plan
+struct KlPlan {
+  int64_t nbcap, ntile, chunk_rows, max_items;
+  int nscan;
+  size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_dk, off_handles, off_tpos, off_lsep,
+      off_lsei, off_dqp, off_klp, off_part, total;
+};
+
+constexpr size_t kDefaultKlBytes = size_t(16) << 30;
+
+void kl_layout(KlPlan& pl, const msa_seqs* seqs, int H_kv, int D, int topk) {
+  using msa_host::align_up;
+  size_t o = 0;
+  pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
+  pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
+  pl.off_dk = o;       o = align_up(o + sizeof(float) * static_cast<size_t>(seqs->total_kv_rows) * D, 256);
+  const size_t inc = static_cast<size_t>(pl.chunk_rows) * H_kv * topk;
+  pl.max_items = pl.ntile + static_cast<int64_t>((inc + kItemQueries - 1) / kItemQueries);
+  pl.off_handles = o;  o = align_up(o + sizeof(uint32_t) * inc, 256);
+  pl.off_tpos = o;     o = align_up(o + sizeof(int32_t) * inc, 256);
+  pl.off_lsep = o;     o = align_up(o + sizeof(float) * inc, 256);
+  pl.off_lsei = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.chunk_rows) * H_kv, 256);
+  pl.off_dqp = o;      o = align_up(o + sizeof(float) * (inc + 1) * D, 256);    // + trash slot
+  pl.off_klp = o;      o = align_up(o + sizeof(float) * (inc + 1), 256);
+  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * kKlBK * D, 256);
+  pl.total = o;
+}
+
+int make_kl_plan(const msa_seqs* seqs, int H_kv, int D, int topk, size_t budget, KlPlan* pl) {
+  const int64_t nb = (seqs->max_kv_len + kKlBK - 1) / kKlBK;
+  pl->nbcap = static_cast<int64_t>(seqs->num_seqs) * (nb > 0 ? nb : 1);
+  pl->ntile = static_cast<int64_t>(H_kv) * pl->nbcap;
+  if (pl->ntile >= (int64_t(1) << 31) - 1 || pl->nbcap >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  pl->nscan = static_cast<int>((pl->ntile + kScanPerBlock - 1) / kScanPerBlock);
+  if (pl->nscan > 1024 * 64) return MSA_ERR_UNSUPPORTED;
+  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  const int64_t all = std::max<int64_t>(1, seqs->total_q_rows);
+  pl->chunk_rows = std::min(all, max_rows);
+  kl_layout(*pl, seqs, H_kv, D, topk);
+  if (pl->total > budget) {
+    pl->chunk_rows = 1;
+    kl_layout(*pl, seqs, H_kv, D, topk);
+    const size_t one = pl->total;
+    if (one > budget) return MSA_ERR_WORKSPACE;
+    pl->chunk_rows = 2;
+    kl_layout(*pl, seqs, H_kv, D, topk);
+    const size_t per_row = pl->total - one + 1024;
+    pl->chunk_rows = std::min(std::min(all, max_rows), 1 + static_cast<int64_t>((budget - one) / per_row));
+    kl_layout(*pl, seqs, H_kv, D, topk);
+    while (pl->total > budget && pl->chunk_rows > 1) {
+      pl->chunk_rows = std::max<int64_t>(1, pl->chunk_rows * 7 / 8);
+      kl_layout(*pl, seqs, H_kv, D, topk);
+    }
+    if (pl->total > budget) return MSA_ERR_WORKSPACE;
+  }
+  return MSA_OK;
+}
+
+int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim, int BK, int topk) {
+  int st = msa_host::validate_seqs(seqs);
+  if (st != MSA_OK) return st;
+  if (H_q < 1 || H_kv < 1 || d_idx < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
+  if (H_q % H_kv != 0) return MSA_ERR_INVALID;
+  if (head_dim != kHeadDim || BK != kKlBK || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
+  if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
+  if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  return MSA_OK;
+}
+
+template <int D>
+int run_kl(const void* index_q, const void* index_k, const void* q, const void* k, const float* lse,
+           const int32_t* block_ids, const msa_seqs* seqs, int H_q, int H_kv, int topk, float softmax_scale,
+           float grad_scale, void* d_index_q, void* d_index_k, float* kl, const KlPlan& pl, char* ws,
+           hipStream_t stream) {
+  auto* blk_base = reinterpret_cast<int64_t*>(ws + pl.off_blk_base);
+  auto* cnt = reinterpret_cast<int32_t*>(ws + pl.off_cnt);
+  auto* tile_off = reinterpret_cast<int32_t*>(ws + pl.off_tile_off);
+  auto* item_off = reinterpret_cast<int32_t*>(ws + pl.off_item_off);
+  auto* blk_tot = reinterpret_cast<int32_t*>(ws + pl.off_blk_tot);
+  auto* dk_acc = reinterpret_cast<float*>(ws + pl.off_dk);
+  auto* handles = reinterpret_cast<uint32_t*>(ws + pl.off_handles);
+  auto* tpos = reinterpret_cast<int32_t*>(ws + pl.off_tpos);
+  auto* lsep = reinterpret_cast<float*>(ws + pl.off_lsep);
+  auto* lsei = reinterpret_cast<float*>(ws + pl.off_lsei);
+  auto* dqp = reinterpret_cast<float*>(ws + pl.off_dqp);
+  auto* klp = reinterpret_cast<float*>(ws + pl.off_klp);
+  auto* part = reinterpret_cast<float*>(ws + pl.off_part);
+  const msa_seqs sq = *seqs;
+  const int64_t kv_floats = seqs->total_kv_rows * static_cast<int64_t>(D);
+  const unsigned zero_blocks = static_cast<unsigned>(std::min<int64_t>((kv_floats + 255) / 256, 8192));
+  const float sidx = 1.f / std::sqrt(static_cast<float>(D));
+  const auto* iq = static_cast<const uint16_t*>(index_q);
+  const auto* ik = static_cast<const uint16_t*>(index_k);
+
+  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, kKlBK,
+                   blk_base);
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
+                   reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
+  static int ctas_lse = 0, ctas_grad = 0;
+  const int n_lse = persistent_ctas(kl_lse_kernel<D>, kKlThreads, &ctas_lse);
+  const int n_grad = persistent_ctas(kl_grad_kernel<D>, kKlThreads, &ctas_grad);
+  const int64_t trash_inc = pl.chunk_rows * H_kv * static_cast<int64_t>(topk);
+  for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
+    const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
+    const int64_t pairs = nr * H_kv;
+    build_reverse_index(block_ids, sq, blk_base, H_kv, kKlBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
+                        tile_off, item_off, blk_tot, tpos, handles, stream);
+    msa_prof::launch("kl_lse_kernel", kl_lse_kernel<D>, dim3(n_lse), dim3(kKlThreads), 0, stream, iq, ik, sq,
+                     static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
+                     static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,
+                     pl.nbcap, r0, sidx * kLog2e, lsep);
+    msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
+                     dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
+                     static_cast<const float*>(lsep), lsei);
+    msa_prof::launch("kl_grad_kernel", kl_grad_kernel<D>, dim3(n_grad), dim3(kKlThreads), 0, stream, iq, ik,
+                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
+                     static_cast<const float*>(lsei), sq, static_cast<const int64_t*>(blk_base),
+                     static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
+                     static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
+                     sidx, trash_inc, dqp, klp, part);
+    msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>, dim3(static_cast<unsigned>(pl.nbcap)),
+                     dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
+                     static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc);
+    msa_prof::launch("kl_combine_kernel", kl_combine_kernel<D>,
+                     dim3(static_cast<unsigned>((pairs + kKlCombWaves - 1) / kKlCombWaves)), dim3(64 * kKlCombWaves),
+                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
+                     static_cast<const float*>(dqp), static_cast<const float*>(klp), grad_scale * sidx,
+                     static_cast<uint16_t*>(d_index_q), kl);
+  }
+  if (kv_floats > 0)
+    msa_prof::launch("kl_convert_kernel", kl_convert_kernel, dim3(zero_blocks), dim3(256), 0, stream,
+                     static_cast<const float*>(dk_acc), kv_floats / 2, grad_scale * sidx,
+                     static_cast<uint16_t*>(d_index_k));
+  return msa_host::launch_status();
+}
+
+}  // namespace
+
+extern "C" size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                                       int d_idx, int head_dim, int block_size, int topk) {
+  if (validate_kl(seqs, num_q_heads, num_kv_heads, d_idx, head_dim, block_size, topk) != MSA_OK) return 0;
+  KlPlan pl;
+  if (make_kl_plan(seqs, num_kv_heads, d_idx, topk, kDefaultKlBytes, &pl) != MSA_OK) {
+    if (make_kl_plan(seqs, num_kv_heads, d_idx, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+    pl.chunk_rows = 1;
+    kl_layout(pl, seqs, num_kv_heads, d_idx, topk);
+  }
+  return pl.total;
+}
+
+extern "C" int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void* q, const void* k,
+                                      const float* lse, const int32_t* block_ids, const msa_seqs* seqs,
+                                      int num_q_heads, int num_kv_heads, int d_idx, int head_dim, int block_size,
+                                      int topk, float softmax_scale, float grad_scale, void* d_index_q,
+                                      void* d_index_k, float* kl, void* workspace, size_t workspace_bytes,
+                                      hipStream_t stream) {
+  int st = validate_kl(seqs, num_q_heads, num_kv_heads, d_idx, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (!index_q || !index_k || !q || !k || !lse || !block_ids || !d_index_q || !d_index_k) return MSA_ERR_INVALID;
+  if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
+  KlPlan pl;
+  st = make_kl_plan(seqs, num_kv_heads, d_idx, topk, workspace_bytes, &pl);
+  if (st != MSA_OK) return st;
+  if (!workspace || workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  if (d_idx == 64)
+    return run_kl<64>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk, softmax_scale,
+                      grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+  return run_kl<128>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk, softmax_scale,
+                     grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+}

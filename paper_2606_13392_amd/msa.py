@@ -27,6 +27,7 @@ EXPORTS = [
     "msa_sparse_attn_prefill_fp8", "msa_sparse_attn_decode_fp8",
     "msa_dense_attn_workspace_size", "msa_dense_attn",
     "msa_sparse_attn_backward_workspace_size", "msa_sparse_attn_backward",
+    "msa_sparse_kl_backward_workspace_size", "msa_sparse_kl_backward",
     "msa_profile_enable", "msa_profile_reset", "msa_profile_kernel_name", "msa_profile_read",
 ]
 
@@ -80,6 +81,10 @@ def lib() -> ctypes.CDLL:
         L.msa_sparse_attn_backward_workspace_size.restype = Z
         L.msa_sparse_attn_backward.argtypes = [P, P, P, P, P, P, P, S, I, I, I, I, I, F, P, P, P, P, Z, P]
         L.msa_sparse_attn_backward.restype = I
+        L.msa_sparse_kl_backward_workspace_size.argtypes = [S, I, I, I, I, I, I]
+        L.msa_sparse_kl_backward_workspace_size.restype = Z
+        L.msa_sparse_kl_backward.argtypes = [P, P, P, P, P, P, S, I, I, I, I, I, I, F, F, P, P, P, P, Z, P]
+        L.msa_sparse_kl_backward.restype = I
         L.msa_profile_enable.argtypes = [I]
         L.msa_profile_enable.restype = I
         L.msa_profile_reset.argtypes = []
@@ -338,6 +343,50 @@ def sparse_attn_backward(q, k, v, o, lse, d_o, block_ids, seqs: Seqs, block_size
                                     _stream())
     _check(st, "msa_sparse_attn_backward")
     return d_q, d_k, d_v
+
+
+def sparse_kl_backward_workspace_size(seqs: Seqs, num_q_heads, num_kv_heads, d_idx, head_dim, block_size,
+                                      topk) -> int:
+    return int(lib().msa_sparse_kl_backward_workspace_size(seqs.ref(), num_q_heads, num_kv_heads, d_idx, head_dim,
+                                                            block_size, topk))
+
+
+def sparse_kl_backward(index_q, index_k, q, k, lse, block_ids, seqs: Seqs, block_size: int, grad_scale: float = 1.0,
+                       softmax_scale=None, with_kl: bool = True, d_index_q=None, d_index_k=None, kl=None,
+                       workspace=None):
+    """Sparse KL loss of the Index Branch: (d_index_q [Tq, H_kv, d_idx] bf16,
+    d_index_k [Tkv, d_idx] bf16, kl [Tq, H_kv] fp32 or None); the gradients are
+    grad_scale times those of sum(kl)."""
+    Tq, H_kv, d_idx = index_q.shape
+    H_q, d_h = q.shape[1], q.shape[2]
+    topk = block_ids.shape[2]
+    dev = seqs.device
+    _need(index_q, "index_q", torch.bfloat16, (seqs.total_q_rows, H_kv, d_idx), dev)
+    _need(index_k, "index_k", torch.bfloat16, (seqs.total_kv_rows, d_idx), dev)
+    _need(q, "q", torch.bfloat16, (seqs.total_q_rows, H_q, d_h), dev)
+    _need(k, "k", torch.bfloat16, (seqs.total_kv_rows, H_kv, d_h), dev)
+    _need(lse, "lse", torch.float32, (Tq, H_q), dev)
+    _need(block_ids, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    if d_index_q is None:
+        d_index_q = torch.empty_like(index_q)
+    if d_index_k is None:
+        d_index_k = torch.empty_like(index_k)
+    if with_kl and kl is None:
+        kl = torch.empty((Tq, H_kv), dtype=torch.float32, device=dev)
+    _need(d_index_q, "d_index_q", torch.bfloat16, tuple(index_q.shape), dev)
+    _need(d_index_k, "d_index_k", torch.bfloat16, tuple(index_k.shape), dev)
+    if kl is not None:
+        _need(kl, "kl", torch.float32, (Tq, H_kv), dev)
+    scale = 1.0 / math.sqrt(d_h) if softmax_scale is None else float(softmax_scale)
+    L = lib()
+    nbytes = int(L.msa_sparse_kl_backward_workspace_size(seqs.ref(), H_q, H_kv, d_idx, d_h, block_size, topk))
+    ws = _workspace(nbytes, dev, workspace)
+    st = L.msa_sparse_kl_backward(_ptr(index_q), _ptr(index_k), _ptr(q), _ptr(k), _ptr(lse), _ptr(block_ids),
+                                  seqs.ref(), H_q, H_kv, d_idx, d_h, block_size, topk, scale, float(grad_scale),
+                                  _ptr(d_index_q), _ptr(d_index_k), _ptr(kl), _ptr(ws),
+                                  0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(st, "msa_sparse_kl_backward")
+    return d_index_q, d_index_k, kl
 
 
 def profile_enable(on: bool = True) -> None:
