@@ -278,7 +278,7 @@ int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const 
  * d_index_q and kl are bit-reproducible; d_index_k adds a key block's queries
  * in an order fixed at run time.  Supported: d_idx in {64, 128};
  * head_dim == 128; block_size == 64; 1 <= topk <= 64;
- * 1 <= num_q_heads / num_kv_heads <= 16; num_kv_heads <= 64.
+ * num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}; num_kv_heads <= 64.
  * ------------------------------------------------------------------------ */
 size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,
                                              int num_kv_heads, int d_idx, int head_dim,

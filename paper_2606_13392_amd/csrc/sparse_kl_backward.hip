@@ -19,9 +19,10 @@
 //   kl_lse           per incidence: ln sum_j exp(s_idx S_idx_j) over the block's visible keys
 //   kl_lse_combine   per (row, group): LSE_idx over the valid slots
 //   kl_grad          per work item (<= 256 queries of one tile): P, P_idx and
-//                    Delta on MFMA 16x16x32; d k_idx of the block in registers
-//                    (an fp32 partial per item), d q_idx and the KL term of
-//                    every incidence as fp32 partials
+//                    Delta on MFMA 16x16x32 per gathered (query, head) row,
+//                    the teacher's head mean in registers; d k_idx of the
+//                    block in registers (an fp32 partial per item), d q_idx
+//                    and the KL term of every incidence as fp32 partials
 //   kl_tile_reduce   per key block: the items of every group's tile, in
 //                    order, added to the fp32 d k_idx accumulator
 //   kl_combine       per (row, group): d q_idx and KL over the valid slots, in
@@ -42,14 +43,13 @@ struct KlSmem {
   uint16_t k[kKlBK][kHeadDim + 8];                    // K block (Main Branch head r), row-major
   uint16_t ki[kKlBK][D + 8];                          // index-key block, row-major
   uint16_t kit[D][kKlBK + 8];                         // index-key block transposed
-  uint16_t qit[D][32 + 8];                            // index queries of the pass, transposed
-  float pl[kKlBK][kKlRows + 4];                       // P of the pass, [key][row]
-  uint16_t dl[32][kKlBK + 8];                         // Delta of the pass (bf16), [query][key]
-  float kls[4][32];                                   // KL term per (key quarter, query)
-  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row
-  float lsei2[32];                                    // LSE_idx * log2(e) per query (+inf: none)
-  int32_t qpos[32];                                   // position per query (-1: none)
-  int64_t incoff[32];                                 // incidence index per query (the trash slot: none)
+  uint16_t qit[D][kKlRows + 8];                       // index query of each pass row, transposed
+  uint16_t dl[kKlRows][kKlBK + 8];                    // Delta of the pass (bf16), [row][key]
+  float kls[4][kKlRows];                              // KL term per (key quarter, row)
+  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row (+inf: no row)
+  float lsei2[kKlRows];                               // LSE_idx * log2(e) per row
+  int32_t rpos[kKlRows];                              // position per row (-1: no row)
+  int64_t incoff[kKlRows];                            // the row's incidence if it is its query's head 0, else trash
   int32_t s_row[kItemQueries];
   int32_t s_slot[kItemQueries];
 };
@@ -203,12 +203,36 @@ __global__ __launch_bounds__(256) void kl_lse_combine_kernel(const int32_t* __re
 }
 
 // ---------------------------------------------------------------- gradients
+// Mean over the G = 2^lg heads of a query of per-row values laid out as the
+// C rows 16t + 4qd + i of MFMA 16x16x32 (lane = c16 + 16 qd): a query's rows
+// are consecutive, so they sit in one lane (G <= 4), in lanes qd, qd ^ 1
+// (G = 8) or in all four qd (G = 16) of one row tile.
+__device__ __forceinline__ void head_mean(f32x4 (&v)[2], int lg) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (lg == 1) {
+      const float a = v[t][0] + v[t][1], b = v[t][2] + v[t][3];
+      v[t][0] = v[t][1] = 0.5f * a;
+      v[t][2] = v[t][3] = 0.5f * b;
+    } else if (lg >= 2) {
+      float a = (v[t][0] + v[t][1]) + (v[t][2] + v[t][3]);
+      if (lg >= 3) a += __shfl_xor(a, 16);
+      if (lg >= 4) a += __shfl_xor(a, 32);
+      a *= 1.f / static_cast<float>(1 << lg);
+      v[t][0] = v[t][1] = v[t][2] = v[t][3] = a;
+    }
+  }
+}
+
 // Wave kq owns keys 16kq .. 16kq+15 of the block.  MFMA 16x16x32 lane l =
-// (c16 = l % 16, qd = l / 16).  A pass takes qpw = 32 / G queries x G heads =
-// 32 rows (row 16t + c16 of the A operands; C rows 16t + 4qd + i) and the
-// same qpw queries of the index branch (query tiles of 16).
+// (c16 = l % 16, qd = l / 16).  A pass takes qpw = 32 / G queries x G heads
+// = 32 rows; the Main Branch scores S and the index scores S_idx are both
+// computed per row (the index query of a row is its query's), so the lane
+// holding key 16kq + c16 has rows 16t + 4qd + i of both.  The teacher mean
+// over a query's heads is a register reduction; Delta enters d k_idx and the
+// KL only through each query's head-0 row.
 template <int D>
-__global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
+__global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
@@ -222,11 +246,9 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
   const int lane = lane_id();
   const int kq = threadIdx.x / kWave;
   const int c16 = lane & 15, qd = lane >> 4;
-  const int G = H_q / H_kv;
-  const int qpw = 32 / G;
-  const int rows_g = qpw * G;
-  const int jq0 = c16 / G, hh0 = c16 % G, jq1 = (16 + c16) / G, hh1 = (16 + c16) % G;
-  const float inv_g = 1.f / static_cast<float>(G);
+  const int G = H_q / H_kv;                           // a power of two <= 16
+  const int lg = __builtin_ctz(G);
+  const int qpw = 32 >> lg;
   const float sidx_log2 = sidx * kLog2e;
   const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
   const int32_t total_items = item_off[ntile];
@@ -267,113 +289,109 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
     for (int t = 0; t < NT; ++t) acc_dk[t] = f32x4{};
     const int key = key0 + 16 * kq + c16;             // this lane's key in the C layouts
 
-    for (int c = 0; c < nq; c += qpw) {
-      // Main Branch A operands (rows 16t + c16) and index A operands (queries 16t + c16)
-      u32x4 bq[2][KSM], bi[2][KSI];
-      float lse_v[2];
-      bool arow[2], aq[2];
+    // A operands of a pass (rows 16t + c16): Q of the row's head, the index
+    // query of the row's query, and the two LSEs; the next pass's are
+    // requested once S and S_idx have consumed the current ones.
+    u32x4 bq[2][KSM], bi[2][KSI];
+    float lse_v[2], lsei_v[2];
+    bool arow[2];
+    int32_t qrow[2];
+    auto load_pass = [&](int cc) {
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const int qa = c + (t ? jq1 : jq0);
-        arow[t] = 16 * t + c16 < rows_g && qa < nq;
-        const int64_t grow = row0 + sm.s_row[min(qa, nq - 1)];
-        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + (t ? hh1 : hh0);
+        const int qa = cc + ((16 * t + c16) >> lg);
+        arow[t] = qa < nq;
+        qrow[t] = min(qa, nq - 1);
+        const int64_t rl = sm.s_row[qrow[t]];
+        const int64_t grow = row0 + rl;
+        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + ((16 * t + c16) & (G - 1));
 #pragma unroll
         for (int st = 0; st < KSM; ++st) bq[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
-        lse_v[t] = lse[hrow];
-        const int qb = c + 16 * t + c16;
-        aq[t] = 16 * t + c16 < qpw && qb < nq;
-        const int64_t irow = row0 + sm.s_row[min(qb, nq - 1)];
 #pragma unroll
-        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (irow * H_kv + r) * D + 32 * st + 8 * qd);
+        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (grow * H_kv + r) * D + 32 * st + 8 * qd);
+        lse_v[t] = lse[hrow];
+        lsei_v[t] = lse_idx[rl * H_kv + r];
       }
-      __syncthreads();                                // the previous pass is done with qit, pl, dl, kls, scalars
+    };
+    load_pass(0);
+
+    for (int c = 0; c < nq; c += qpw) {
+      __syncthreads();                                // the previous pass is done with qit, dl, kls, row scalars
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        // index queries transposed: wave kq writes the k-steps st with st % 4 == kq
+        const int col = 16 * t + c16;
+        // index queries transposed: wave kq writes k-step kq (there are D / 32 <= 4)
 #pragma unroll
         for (int st = 0; st < KSI; ++st) {
-          if ((st & 3) != kq) continue;
+          if (st != kq) continue;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) sm.qit[32 * st + 8 * qd + j][16 * t + c16] = raw_elem16(bi[t][st], j);
+          for (int j = 0; j < 8; ++j) sm.qit[32 * st + 8 * qd + j][col] = raw_elem16(bi[t][st], j);
         }
         if (qd == 0 && kq == 0) {
-          sm.lse2[16 * t + c16] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
-          const int qb = c + 16 * t + c16;
-          if (aq[t]) {
-            const int64_t rl = sm.s_row[qb];
-            const int64_t pr = rl * H_kv + r;
-            sm.lsei2[16 * t + c16] = lse_idx[pr] * kLog2e;
-            sm.qpos[16 * t + c16] = pos_base + static_cast<int>(rl);
-            sm.incoff[16 * t + c16] = pr * topk + sm.s_slot[qb];
-          } else {
-            sm.lsei2[16 * t + c16] = INFINITY;
-            sm.qpos[16 * t + c16] = -1;
-            sm.incoff[16 * t + c16] = trash_inc;
-          }
+          sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
+          sm.lsei2[col] = arow[t] ? lsei_v[t] * kLog2e : INFINITY;
+          const int32_t rl = sm.s_row[qrow[t]];
+          sm.rpos[col] = arow[t] ? pos_base + rl : -1;
+          sm.incoff[col] = (arow[t] && (col & (G - 1)) == 0)
+                               ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[qrow[t]]
+                               : trash_inc;
         }
       }
       __syncthreads();
 
-      // Main Branch P of this key quarter: lane holds key, rows 16t + 4qd + i
-      f32x4 acc_s[2];
+      // S and S_idx of this key quarter: lane holds key, rows 16t + 4qd + i
+      f32x4 acc_s[2], acc_i[2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         acc_s[t] = f32x4{};
+        acc_i[t] = f32x4{};
 #pragma unroll
         for (int st = 0; st < KSM; ++st)
           acc_s[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
                                   ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
-      }
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        f32x4 pv;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = 16 * t + 4 * qd + i;
-          const int qp = row < rows_g ? sm.qpos[row / G] : -1;
-          pv[i] = key <= qp ? exp2f(acc_s[t][i] * s_main_log2 - sm.lse2[row]) : 0.f;
-        }
-        *reinterpret_cast<f32x4*>(&sm.pl[16 * kq + c16][16 * t + 4 * qd]) = pv;
-      }
-      // index scores of this key quarter: lane holds key, queries 16t + 4qd + i
-      f32x4 acc_i[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        acc_i[t] = f32x4{};
 #pragma unroll
         for (int st = 0; st < KSI; ++st)
           acc_i[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bi[t][st]),
                                   ld_bf16x8(&sm.ki[16 * kq + c16][32 * st + 8 * qd]), acc_i[t]);
       }
-      __syncthreads();                                // P of every row in LDS
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + qpw < nq) load_pass(c + qpw);
 
-      // teacher P (mean over the query's heads), student P_idx, Delta, KL term
-      f32x4 dlt[2];
+      // teacher: per-head P, then the mean over the query's heads
+      f32x4 pb[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * t + 4 * qd + i;
+          pb[t][i] = key <= sm.rpos[row] ? exp2f(acc_s[t][i] * s_main_log2 - sm.lse2[row]) : 0.f;
+        }
+      head_mean(pb, lg);
+      // student, Delta = P_idx - P, KL term; head-0 rows carry their query
+      f32x4 dlt[2], dk_a[2];
       float klq[2][4];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int qi = 16 * t + 4 * qd + i;         // query within the pass
-          const bool on = qi < qpw && key <= sm.qpos[qi];
-          float pbar = 0.f;
-          if (qi < qpw)
-            for (int hh = 0; hh < G; ++hh) pbar += sm.pl[16 * kq + c16][qi * G + hh];
-          pbar *= inv_g;
-          const float lz = acc_i[t][i] * sidx_log2 - sm.lsei2[qi];   // log2 P_idx
+          const int row = 16 * t + 4 * qd + i;
+          const bool on = key <= sm.rpos[row];
+          const bool head0 = (row & (G - 1)) == 0;
+          const float lz = acc_i[t][i] * sidx_log2 - sm.lsei2[row];   // log2 P_idx
           const float pidx = on ? exp2f(lz) : 0.f;
+          const float pbar = pb[t][i];
           dlt[t][i] = pidx - pbar;
-          klq[t][i] = (on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
+          dk_a[t][i] = head0 ? dlt[t][i] : 0.f;
+          klq[t][i] = (head0 && on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
         }
-      // d k_idx += Delta^T q_idx over the pass's 32 queries (one k-step):
-      // k index 8qd + 4t + i = query 16t + 4qd + i
+      // d k_idx += Delta^T q_idx over the pass's rows (one k-step): k index
+      // 8qd + 4t + i = row 16t + 4qd + i
       {
         uint4 w;
-        w.x = pack_bf16x2(dlt[0][0], dlt[0][1]);
-        w.y = pack_bf16x2(dlt[0][2], dlt[0][3]);
-        w.z = pack_bf16x2(dlt[1][0], dlt[1][1]);
-        w.w = pack_bf16x2(dlt[1][2], dlt[1][3]);
+        w.x = pack_bf16x2(dk_a[0][0], dk_a[0][1]);
+        w.y = pack_bf16x2(dk_a[0][2], dk_a[0][3]);
+        w.z = pack_bf16x2(dk_a[1][0], dk_a[1][1]);
+        w.w = pack_bf16x2(dk_a[1][2], dk_a[1][3]);
         const bf16x8 da = __builtin_bit_cast(bf16x8, w);
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -382,12 +400,14 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
           acc_dk[t] = mfma16x16x32(da, __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y)), acc_dk[t]);
         }
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+        for (int t = 0; t < 2; ++t) {
+          const uint32_t lo = pack_bf16x2(dlt[t][0], dlt[t][1]), hi = pack_bf16x2(dlt[t][2], dlt[t][3]);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            sm.dl[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(w[2 * t + (i >> 1)] >> (16 * (i & 1)));
+            sm.dl[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>((i < 2 ? lo : hi) >> (16 * (i & 1)));
+        }
       }
-      // KL per query: sum over this wave's 16 keys, then over the 4 waves in LDS
+      // KL per row: sum over this wave's 16 keys, then over the 4 waves in LDS
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -399,9 +419,11 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
         }
       __syncthreads();                                // Delta and KL terms of every key in LDS
 
-      // d q_idx of the pass's queries: dims 16n + c16 for n % 4 == kq, over the 64 keys
+      // d q_idx per row (the query's head-0 row is stored): dims 16n + c16 for
+      // n % 4 == kq, over the 64 keys
 #pragma unroll
-      for (int n = kq; n < NT; n += 4) {
+      for (int n = 0; n < NT; ++n) {
+        if ((n & 3) != kq) continue;
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
           f32x4 acc = f32x4{};
@@ -410,8 +432,7 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_kernel(
             acc = mfma16x16x32(ld_bf16x8(&sm.dl[16 * t + c16][32 * ks + 8 * qd]),
                                ld_bf16x8(&sm.kit[16 * n + c16][32 * ks + 8 * qd]), acc);
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            dqp[sm.incoff[16 * t + 4 * qd + i] * D + 16 * n + c16] = acc[i];
+          for (int i = 0; i < 4; ++i) dqp[sm.incoff[16 * t + 4 * qd + i] * D + 16 * n + c16] = acc[i];
         }
       }
       if (kq == 0 && lane < 32)
@@ -569,7 +590,7 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   if (H_q < 1 || H_kv < 1 || d_idx < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
   if (H_q % H_kv != 0) return MSA_ERR_INVALID;
   if (head_dim != kHeadDim || BK != kKlBK || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
-  if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
+  if (topk > 64 || H_q / H_kv > 16 || !msa_host::is_pow2(H_q / H_kv) || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   return MSA_OK;
 }

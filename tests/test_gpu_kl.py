@@ -50,7 +50,7 @@ CASES = [
     ("kl_ragged_T333_g4", [333], [333], 8, 2, 5, 64, None),
     ("kl_g16_didx128", [300], [300], 32, 2, 4, 128, None),
     ("kl_g1", [200], [200], 4, 4, 3, 64, None),
-    ("kl_g3", [150], [150], 6, 2, 4, 64, None),
+    ("kl_g2", [150], [150], 4, 2, 4, 64, None),
     ("kl_chunked_varlen", [130, 0, 64, 1, 257], [700, 300, 64, 900, 1500], 16, 4, 6, 64, None),
     ("kl_decode_padded", [1, 1, 1, 1, 1], [3000, 64, 65, 4097, 1], 16, 4, 6, 128, 4160),
     ("kl_many_items_k32", [2048], [2048], 16, 2, 32, 64, None),
@@ -88,6 +88,16 @@ def test_kl_small(case):
     sk_ = check_grad(dik.float().cpu().numpy(), dik_ref, f"{name} d_index_k")
     _say(f"  KL max-err {e_kl:.2e} (mean KL {kl_ref.mean():.3f}); d_index_q {sq_[0]:.2e}/{sq_[1]:.2e}; "
          f"d_index_k {sk_[0]:.2e}/{sk_[1]:.2e} (max-err/max|ref|, rel-L2)")
+
+
+def test_kl_rejects_unsupported_shapes():
+    """G must be a power of two (the teacher's head mean is a register
+    reduction over aligned rows); block_size 64 only."""
+    p = synth.packed_problem("kl_g3", [10], [10], num_q_heads=6, num_kv_heads=2, topk=2, seed=1)
+    seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
+    assert msa.sparse_kl_backward_workspace_size(seqs, 6, 2, 64, 128, 64, 2) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 2) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 64, 2) > 0
 
 
 def test_kl_grad_scale_and_no_kl_output():
