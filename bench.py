@@ -8,7 +8,8 @@ workload is prefill at T = 1,048,576 tokens (64 query / 8 KV heads, head dim
 128, index dim 64, block 64, k = 64, planted blocks); ``value`` is its
 throughput in tokens/s.  A decode phase (64 sequences x 1 token at context
 131,072, k = 32: msa_index_topk + msa_sparse_attn_decode) is timed after it and
-reported under "decode".
+reported under "decode", and a training step of the attention at T = 32,768
+(forward, msa_sparse_attn_backward, msa_sparse_kl_backward) under "training".
 
 Inputs are drawn on the device before timing (synthetic, seeded) and stay
 resident in HBM.  Each library call is bracketed by HIP events on the stream
@@ -411,6 +412,94 @@ def run_decode(args, dev):
     return out
 
 
+def run_training(args, dev):
+    """One training step of an MSA layer's attention on the --train-workload
+    shape: the forward (msa_index_topk + msa_sparse_attn_prefill, keeping O
+    and LSE) and the backward (msa_sparse_attn_backward for an upstream dO,
+    msa_sparse_kl_backward for the Index Branch's KL loss with
+    grad_scale = 1 / (rows x H_kv))."""
+    import torch
+    from paper_2606_13392_amd import msa, synth
+    p = synth.workload(args.train_workload)
+    log(f"[bench] training step on {p.name}: {p.description}")
+    d = synth.generate_torch(p, dev, tensors=("index_q", "index_k", "q", "k", "v", "d_o"))
+    seqs = msa.Seqs.from_problem(p, dev)
+    H_q, H_kv, dh = p.num_q_heads, p.num_kv_heads, p.head_dim
+    rows = p.total_q_rows
+    ids = torch.empty((rows, H_kv, p.topk), dtype=torch.int32, device=dev)
+    o = torch.empty((rows, H_q, dh), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((rows, H_q), dtype=torch.float32, device=dev)
+    dq, dk, dv = (torch.empty_like(d[t]) for t in ("q", "k", "v"))
+    diq, dik = torch.empty_like(d["index_q"]), torch.empty_like(d["index_k"])
+    kl = torch.empty((rows, H_kv), dtype=torch.float32, device=dev)
+    ws = torch.empty(max(msa.index_topk_workspace_size(seqs, H_kv, p.d_idx, p.block_size, p.topk),
+                         msa.sparse_attn_prefill_workspace_size(seqs, H_q, H_kv, dh, p.block_size, p.topk),
+                         msa.sparse_attn_backward_workspace_size(seqs, H_q, H_kv, dh, p.block_size, p.topk),
+                         msa.sparse_kl_backward_workspace_size(seqs, H_q, H_kv, p.d_idx, dh, p.block_size, p.topk)),
+                     dtype=torch.uint8, device=dev)
+    gscale = 1.0 / (rows * H_kv)
+    timers = {n: CallTimer() for n in ("msa_index_topk", "msa_sparse_attn_prefill", "msa_sparse_attn_backward",
+                                       "msa_sparse_kl_backward")}
+    calls = {
+        "msa_index_topk": lambda: msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk,
+                                                 out=ids, workspace=ws),
+        "msa_sparse_attn_prefill": lambda: msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size,
+                                                                   out=o, lse=lse, workspace=ws),
+        "msa_sparse_attn_backward": lambda: msa.sparse_attn_backward(d["q"], d["k"], d["v"], o, lse, d["d_o"], ids,
+                                                                     seqs, p.block_size, d_q=dq, d_k=dk, d_v=dv,
+                                                                     workspace=ws),
+        "msa_sparse_kl_backward": lambda: msa.sparse_kl_backward(d["index_q"], d["index_k"], d["q"], d["k"], lse, ids,
+                                                                 seqs, p.block_size, grad_scale=gscale,
+                                                                 d_index_q=diq, d_index_k=dik, kl=kl, workspace=ws),
+    }
+    for _ in range(args.warmup):
+        for fn in calls.values():
+            fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.train_steps):
+        for fn in calls.values():
+            fn()
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.train_steps
+    msa.profile_reset()
+    msa.profile_enable(True)
+    for _ in range(args.train_steps):
+        for n, fn in calls.items():
+            timers[n].time(fn)
+    torch.cuda.synchronize()
+    prof = msa.profile_read()
+    msa.profile_enable(False)
+    loss = float(kl.double().mean())
+    G, D = p.group_size, p.d_idx
+    inc = int((ids >= 0).sum().item())
+    # per-incidence algorithmic bytes of the two dominant backward kernels
+    bwd_bytes = inc * (G * dh * 2 * 3 + G * 8)       # Q, dO gathers; bf16 dQ partial; LSE and D
+    kl_bytes = inc * (G * (dh * 2 + 4) + D * 2 + D * 4 + 8)   # Q gather + LSE; index query; d q_idx partial; LSE_idx, KL
+    kern = {n: {"launches_per_step": c / args.train_steps, "ms_per_step": ms / args.train_steps}
+            for n, (c, ms) in prof.items()}
+    out = {
+        "workload": f"{p.name}: {p.description}",
+        "value": rows / sec,
+        "unit": "tok/s",
+        "steps": args.train_steps,
+        "ms_per_step": sec * 1e3,
+        "calls": {n: {"ms_per_call": t.mean_ms()} for n, t in timers.items()},
+        "kernels": kern,
+        "incidences": inc,
+        "kl_loss_mean": loss,
+        "roofline": {},
+    }
+    for name, nbytes in (("bwd_kvo_kernel", bwd_bytes), ("kl_grad_kernel", kl_bytes)):
+        if name in kern and kern[name]["ms_per_step"] > 0:
+            gbs = nbytes / (kern[name]["ms_per_step"] * 1e-3) / 1e9
+            out["roofline"][name] = {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                     "frac": gbs / PEAK_HBM_GBS, "algorithmic_bytes_per_launch": nbytes}
+    del d, o, lse, dq, dk, dv, diq, dik, kl, ws, ids
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(pre, args):
     """The CPU oracle on a bounded random sample of query rows (host cores)."""
     import numpy as np
@@ -462,6 +551,10 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=20)
     ap.add_argument("--decode-warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--train-workload", default="prefill_32k",
+                    help="shape of the training step (forward + Main Branch backward + KL backward)")
+    ap.add_argument("--train-steps", type=int, default=3)
+    ap.add_argument("--no-train", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=160)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
@@ -538,6 +631,8 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_decode:
         line["decode"] = run_decode(args, dev)
+    if not args.no_train:
+        line["training"] = run_training(args, dev)
     print(json.dumps(line), flush=True)
 
 
