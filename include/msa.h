@@ -49,7 +49,20 @@
  * decode (one row per sequence; kv_starts may then point into a padded cache,
  * e.g. s * max_len).  Key block b of a sequence holds its keys
  * b*block_size .. min((b+1)*block_size, kv_len)-1 (Sec. 2.3, block equation);
- * the local block of position p is p / block_size.
+ * the local block of position p is p / block_size.  Rows of several tokens per
+ * sequence after a cached context (speculative / multi-token decode) are the
+ * chunked-prefill case with a few rows.
+ *
+ * Paged key side (optional): with block_table != NULL the key-side tensors
+ * (index_k, k, v) are a pool of pages of page_size rows, and key block b of
+ * sequence s lives in page block_table[s * block_table_stride + b], i.e. at
+ * rows page * page_size .. + page_size - 1 (kv_starts is then ignored and may
+ * be NULL).  page_size must equal the block_size of the call; kv_lens[s] <=
+ * block_table_stride * page_size.  Page ids outside [0, total_kv_rows /
+ * page_size) are clamped into it (results unspecified, memory safe).  This
+ * is a serving layout, not part of the paper.  msa_index_topk,
+ * msa_sparse_attn_prefill/_decode and their fp8 variants accept it; the
+ * other calls return MSA_ERR_UNSUPPORTED for a paged layout.
  */
 #ifndef MSA_H_
 #define MSA_H_
@@ -78,8 +91,12 @@ typedef struct msa_seqs {
   int32_t max_q_rows;        /* host: upper bound of q_offsets[s+1]-q_offsets[s] */
   int32_t max_kv_len;        /* host: upper bound of kv_lens[s] */
   const int32_t* q_offsets;  /* device [num_seqs+1], non-decreasing, q_offsets[0] == 0 */
-  const int64_t* kv_starts;  /* device [num_seqs], >= 0 */
+  const int64_t* kv_starts;  /* device [num_seqs], >= 0 (unused when paged) */
   const int32_t* kv_lens;    /* device [num_seqs], >= the sequence's query rows */
+  const int32_t* block_table;   /* device [num_seqs, block_table_stride] page ids, or NULL
+                                   (contiguous key side) */
+  int32_t block_table_stride;   /* host: entries per sequence of block_table */
+  int32_t page_size;            /* host: key rows per page (= the call's block_size) */
 } msa_seqs;
 
 /* Human-readable text of a status code (static storage). */

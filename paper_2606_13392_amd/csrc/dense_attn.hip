@@ -278,6 +278,7 @@ int validate_dense(const msa_seqs* seqs, int H_q, int H_kv, int head_dim) {
   if (head_dim != kHeadDim) return MSA_ERR_UNSUPPORTED;
   if (H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
   return MSA_OK;
 }
 

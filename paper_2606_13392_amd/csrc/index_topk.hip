@@ -142,15 +142,19 @@ struct IdxSmem {
 
 // Cooperative copy of one K_idx block (BK keys x D_IDX dims) through
 // registers: 256 threads x CH 16-byte pieces.
-template <int D_IDX, int BK, int CH>
-__device__ __forceinline__ void idx_load_block(const uint16_t* __restrict__ kseq, int kb, int tid,
-                                               u32x4 (&dst)[CH]) {
+// kseq: the sequence's first index-key row (contiguous), or the page pool (paged)
+template <int D_IDX, int BK, int CH, bool PAGED>
+__device__ __forceinline__ void idx_load_block(const uint16_t* __restrict__ kseq, const KeyBlocks& kbk, int kb,
+                                               int tid, u32x4 (&dst)[CH]) {
   constexpr int SEGS = D_IDX / 8;
 #pragma unroll
   for (int c = 0; c < CH; ++c) {
     const int idx = tid + 256 * c;
     const int key = idx / SEGS, seg = idx % SEGS;
-    dst[c] = *reinterpret_cast<const u32x4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
+    if constexpr (PAGED)
+      dst[c] = *reinterpret_cast<const u32x4*>(kseq + (kbk.template row_as<true>(kb) + key) * D_IDX + 8 * seg);
+    else
+      dst[c] = *reinterpret_cast<const u32x4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
   }
 }
 template <int D_IDX, int BK, int CH>
@@ -169,7 +173,7 @@ __device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_
 // row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
 // prunes with.  RW index rows per wave (64 or 128; a unit is 4 RW / 64 row
 // groups): with 128 every K_idx operand read from LDS feeds four MFMAs.
-template <int D_IDX, int BK, int RW>
+template <int D_IDX, int BK, int RW, bool PAGED>
 __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
@@ -214,7 +218,8 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
     cmax[sp] = -INFINITY;
   }
 
-  const uint16_t* kseq = index_k + ur.g.kv_start * D_IDX;
+  const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
+  const uint16_t* kseq = index_k + (PAGED ? 0 : ur.g.kv_start) * D_IDX;
   const int tid = threadIdx.x;
   auto compute = [&](int buf, int kb) {
     if (nvalid == 0) return;
@@ -268,18 +273,18 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
   // so no branch forces the compiler to wait on a prefetch it just issued.
   u32x4 ra[CH], rb[CH];
   const int klast = kb1 - 1;
-  idx_load_block<D_IDX, BK, CH>(kseq, kb0, tid, ra);
-  idx_load_block<D_IDX, BK, CH>(kseq, min(kb0 + 1, klast), tid, rb);
+  idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, kb0, tid, ra);
+  idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb0 + 1, klast), tid, rb);
   idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
   __syncthreads();
   // LDS buffer 0 holds block kb, register set rb holds kb+1
   for (int kb = kb0; kb < kb1; kb += 2) {
-    idx_load_block<D_IDX, BK, CH>(kseq, min(kb + 2, klast), tid, ra);
+    idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb + 2, klast), tid, ra);
     compute(0, kb);
     if (kb + 1 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[1], tid, rb);
     __syncthreads();
     if (kb + 1 >= kb1) break;
-    idx_load_block<D_IDX, BK, CH>(kseq, min(kb + 3, klast), tid, rb);
+    idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb + 3, klast), tid, rb);
     compute(1, kb + 1);
     if (kb + 2 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
     __syncthreads();
@@ -297,7 +302,7 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
 // registers and written as two 16-byte stores.
 constexpr int kSliceBlocks = 8;
 
-template <int D_IDX, int BK>
+template <int D_IDX, int BK, bool PAGED>
 __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
@@ -320,12 +325,14 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
   const int nvalid = ur.nq * H_kv;
   bf16x8 bq[2][KS];
   load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv) * D_IDX, nvalid, n, h, bq);
-  const uint16_t* kbase = index_k + ur.g.kv_start * D_IDX + h * (D_IDX / 2);
+  const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
+  const uint16_t* kbase = index_k + (PAGED ? 0 : ur.g.kv_start) * D_IDX + h * (D_IDX / 2);
 
   auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
+      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + 32 * i + n) * D_IDX
+                                 : kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
 #pragma unroll
       for (int st = 0; st < KS; ++st) a[i][st] = ld_bf16x8(kp + 8 * st);
     }
@@ -375,7 +382,7 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
 // per wave (clamped, unconditional loads) and more waves share each CU.
 // Lane (n, q4) supplies key 16i + n / row n and dims 32ks + 8q4 .. +8; C lane
 // (n, q4) holds row n, keys 16i + 4q4 + e.
-template <int D_IDX, int BK, int DEPTH>
+template <int D_IDX, int BK, int DEPTH, bool PAGED>
 __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
@@ -400,7 +407,8 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
   const uint16_t* qrow = index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv + n) * D_IDX + 8 * q4;
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) bq[ks] = n < nvalid ? ld_bf16x8(qrow + 32 * ks) : zero_bf16x8();
-  const uint16_t* kbase = index_k + (ur.g.kv_start + n) * D_IDX + 8 * q4;
+  const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
+  const uint16_t* kbase = index_k + ((PAGED ? 0 : ur.g.kv_start) + n) * D_IDX + 8 * q4;
 
   // blocks kb0 .. kb1-1 are entirely before every row's local block, hence
   // inside the sequence; loads past kb1 re-read block kb1-1
@@ -408,7 +416,8 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
     kb = min(kb, kb1 - 1);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = kbase + static_cast<int64_t>(kb * BK + 16 * i) * D_IDX;
+      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + 16 * i) * D_IDX
+                                 : kbase + static_cast<int64_t>(kb * BK + 16 * i) * D_IDX;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) a[i][ks] = ld_bf16x8(kp + 32 * ks);
     }
@@ -702,6 +711,7 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   if (d_idx != 64 && d_idx != 128) return MSA_ERR_UNSUPPORTED;
   if (BK != 64 && BK != 128) return MSA_ERR_UNSUPPORTED;
   if (topk > 64) return MSA_ERR_UNSUPPORTED;
+  if ((st = msa_host::check_paged(seqs, BK, true)) != MSA_OK) return st;
   pl->qr = 64 / H_kv;
   // sequences longer than two row groups take the LDS-shared kernel: units of
   // 4 row groups (one per wave), or 8 (two per wave) for d_idx 64 and
@@ -728,27 +738,40 @@ constexpr int64_t kSplitTopkRows = 4096;                 // fewer index rows: 4 
 template <int D, int B>
 constexpr int kNarrowDepth = D * B <= 64 * 64 ? 4 : 2;
 
-template <int D, int B>
-void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
-                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
-                   float* CM, int64_t cm_stride) {
+template <int D, int B, bool PAGED>
+void launch_scores_as(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
+                      const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
+                      float* CM, int64_t cm_stride) {
   if constexpr (D == 64 && B == 64) {
     if (pl.U == 2 * kWaves) {
-      msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 128>), grid, dim3(256), 0,
-                       stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
+      msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 128, PAGED>), grid, dim3(256),
+                       0, stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
                        cm_stride);
       return;
     }
   }
   if (pl.U == kWaves)
-    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 64>), grid, dim3(256), 0, stream,
-                     iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM, cm_stride);
+    msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 64, PAGED>), grid, dim3(256), 0,
+                     stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
+                     cm_stride);
   else if (pl.narrow)
-    msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>>), grid, dim3(256), 0, stream, iq,
-                       ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+    msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>, PAGED>),
+                     grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M,
+                     static_cast<int64_t>(pl.bcap));
   else
-    msa_prof::launch("index_block_max_wave_kernel", (index_block_max_wave_kernel<D, B>), grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv,
-                       pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+    msa_prof::launch("index_block_max_wave_kernel", (index_block_max_wave_kernel<D, B, PAGED>), grid, dim3(256), 0,
+                     stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap));
+}
+
+// A paged key side runs the kernels instantiated for it.
+template <int D, int B>
+void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
+                   const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
+                   float* CM, int64_t cm_stride) {
+  if (sq.block_table)
+    launch_scores_as<D, B, true>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride);
+  else
+    launch_scores_as<D, B, false>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride);
 }
 
 }  // namespace

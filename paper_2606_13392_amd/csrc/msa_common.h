@@ -231,15 +231,52 @@ __device__ __forceinline__ SeqGeom seq_geom(const msa_seqs& sq, int s) {
   SeqGeom g;
   g.q_begin = sq.q_offsets[s];
   g.q_rows = sq.q_offsets[s + 1] - g.q_begin;
-  int64_t st = sq.kv_starts[s];
   int64_t len = sq.kv_lens[s];
-  if (st < 0) st = 0;
-  if (st > sq.total_kv_rows) st = sq.total_kv_rows;
-  if (len > sq.total_kv_rows - st) len = sq.total_kv_rows - st;
+  int64_t st = 0;
+  if (sq.block_table) {
+    // paged: the block table bounds the sequence
+    const int64_t cap = static_cast<int64_t>(sq.block_table_stride) * sq.page_size;
+    if (len > cap) len = cap;
+  } else {
+    st = sq.kv_starts[s];
+    if (st < 0) st = 0;
+    if (st > sq.total_kv_rows) st = sq.total_kv_rows;
+    if (len > sq.total_kv_rows - st) len = sq.total_kv_rows - st;
+  }
   if (len < 0) len = 0;
   g.kv_start = st;
   g.kv_len = static_cast<int32_t>(len);
   return g;
+}
+
+// First key row of key block b (blocks of BK keys) of sequence s: kv_start +
+// b BK on a contiguous key side, else the page the block table lists (pages
+// of BK rows), clamped into the pool.
+struct KeyBlocks {
+  const int32_t* table;      // the sequence's block-table row, or null
+  int64_t base;              // kv_start
+  int64_t max_page;
+  int BK;
+  // PAGED fixes the layout at compile time (hot loops); row() decides at run time
+  template <bool PAGED>
+  __device__ __forceinline__ int64_t row_as(int b) const {
+    if constexpr (PAGED) {
+      int64_t page = table[b];
+      page = page < 0 ? 0 : (page > max_page ? max_page : page);
+      return page * BK;
+    } else {
+      return base + static_cast<int64_t>(b) * BK;
+    }
+  }
+  __device__ __forceinline__ int64_t row(int b) const { return table ? row_as<true>(b) : row_as<false>(b); }
+};
+__device__ __forceinline__ KeyBlocks key_blocks(const msa_seqs& sq, const SeqGeom& g, int s, int BK) {
+  KeyBlocks kb;
+  kb.table = sq.block_table ? sq.block_table + static_cast<int64_t>(s) * sq.block_table_stride : nullptr;
+  kb.base = g.kv_start;
+  kb.max_page = sq.total_kv_rows / BK - 1;
+  kb.BK = BK;
+  return kb;
 }
 
 }  // namespace msa
@@ -254,11 +291,26 @@ inline int validate_seqs(const msa_seqs* s) {
   if (s->num_seqs < 1 || s->total_q_rows < 0 || s->total_kv_rows < 0 || s->max_q_rows < 0 ||
       s->max_kv_len < 0)
     return MSA_ERR_INVALID;
-  if (!s->q_offsets || !s->kv_starts || !s->kv_lens) return MSA_ERR_INVALID;
+  if (!s->q_offsets || !s->kv_lens) return MSA_ERR_INVALID;
+  if (s->block_table) {
+    if (s->block_table_stride < 1 || s->page_size < 1) return MSA_ERR_INVALID;
+    if (s->max_kv_len > static_cast<int64_t>(s->block_table_stride) * s->page_size) return MSA_ERR_INVALID;
+    if (s->total_kv_rows < s->page_size) return MSA_ERR_INVALID;
+  } else if (!s->kv_starts) {
+    return MSA_ERR_INVALID;
+  }
   if (s->max_q_rows > s->max_kv_len) return MSA_ERR_INVALID;
   if (s->total_q_rows > (int64_t)s->num_seqs * s->max_q_rows) return MSA_ERR_INVALID;
   if (s->total_q_rows >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   return MSA_OK;
+}
+
+// A paged key side is accepted by calls that address keys per block; its
+// pages must hold exactly one key block.
+inline int check_paged(const msa_seqs* s, int block_size, bool supported) {
+  if (!s->block_table) return MSA_OK;
+  if (!supported) return MSA_ERR_UNSUPPORTED;
+  return s->page_size == block_size ? MSA_OK : MSA_ERR_INVALID;
 }
 
 inline int launch_status() {

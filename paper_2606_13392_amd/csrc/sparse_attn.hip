@@ -82,7 +82,7 @@ __device__ __forceinline__ void store_v_transposed(AttnSmem<BK>& sm, const R (&r
 
 // T: element type of Q, K and V (uint16_t = bf16 bits, uint8_t = e4m3 bits);
 // o_scale multiplies O (the V dequantisation scale for e4m3).
-template <int BK, typename T>
+template <int BK, typename T, bool PAGED>
 __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const int32_t* __restrict__ block_ids, msa_seqs sq, int H_q, int H_kv, int topk,
@@ -112,8 +112,10 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   for (int ks = 0; ks < kHeadDim / 32; ++ks) bq[ks] = widen_bf16x8(n < G ? load_raw(qrow + 32 * ks) : Raw<T>{});
 
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
-  const T* kbase = k + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
-  const T* vbase = v + g.kv_start * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+  const KeyBlocks kbk = key_blocks(sq, g, s, BK);
+  const int64_t seq0 = PAGED ? 0 : g.kv_start;           // contiguous: keys from kv_start
+  const T* kbase = k + seq0 * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
+  const T* vbase = v + seq0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;
   // without block ids (dense mode) slot b is key block b
   const int32_t* ids = block_ids ? block_ids + (row * H_kv + r) * topk : nullptr;
 
@@ -132,16 +134,21 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     const int key0 = b * BK;
     // K (A operands of S^T) and raw V of this block are requested together;
     // S^T and the softmax run while V is still in flight.
+    // paged: the block's page (keys addressed inside it); else keys from kv_start
+    const int64_t page_row = PAGED ? kbk.template row_as<true>(b) : 0;
     Raw<T> ka[BK / 16][kHeadDim / 32];
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i) {
       const int key = key0 + 16 * i + n;
-      const T* kp = kbase + static_cast<int64_t>(key) * kv_stride;
+      const T* kp = PAGED ? kbase + (page_row + 16 * i + n) * kv_stride : kbase + static_cast<int64_t>(key) * kv_stride;
 #pragma unroll
       for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? load_raw(kp + 32 * ks) : Raw<T>{};
     }
     Raw<T> vraw[BK / 16][4];
-    load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
+    if constexpr (PAGED)
+      load_v_raw<BK, T>(vbase + page_row * kv_stride, kv_stride, 0, g.kv_len - key0, vraw);
+    else
+      load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
 
     // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
     f32x4 st[BK / 16];
@@ -339,7 +346,7 @@ int validate_attn(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK,
   if (BK != 64 && BK != 128) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
-  return MSA_OK;
+  return msa_host::check_paged(seqs, BK, true);
 }
 
 struct SplitPlan {
@@ -393,10 +400,17 @@ int run_rows(const void* q, const void* k, const void* v, const int32_t* block_i
                      static_cast<const T*>(k), static_cast<const T*>(v), block_ids, sq, H_q, H_kv, topk,
                      sp.slots_per_wave, sl2, v_scale, op, lse, o_part, lse_part);
   };
-  if (BK == 64 && !fp8) launch(attn_rows_kernel<64, uint16_t>, uint16_t{});
-  else if (BK == 64) launch(attn_rows_kernel<64, uint8_t>, uint8_t{});
-  else if (!fp8) launch(attn_rows_kernel<128, uint16_t>, uint16_t{});
-  else launch(attn_rows_kernel<128, uint8_t>, uint8_t{});
+  if (sq.block_table) {
+    if (BK == 64 && !fp8) launch(attn_rows_kernel<64, uint16_t, true>, uint16_t{});
+    else if (BK == 64) launch(attn_rows_kernel<64, uint8_t, true>, uint8_t{});
+    else if (!fp8) launch(attn_rows_kernel<128, uint16_t, true>, uint16_t{});
+    else launch(attn_rows_kernel<128, uint8_t, true>, uint8_t{});
+  } else {
+    if (BK == 64 && !fp8) launch(attn_rows_kernel<64, uint16_t, false>, uint16_t{});
+    else if (BK == 64) launch(attn_rows_kernel<64, uint8_t, false>, uint8_t{});
+    else if (!fp8) launch(attn_rows_kernel<128, uint16_t, false>, uint16_t{});
+    else launch(attn_rows_kernel<128, uint8_t, false>, uint8_t{});
+  }
   if (sp.nsplit > 1) {
     const int64_t threads = hr * 16;
     msa_prof::launch("combine_kernel", combine_kernel, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream,

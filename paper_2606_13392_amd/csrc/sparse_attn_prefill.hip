@@ -89,8 +89,9 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
     }
     if (tile != staged) {
-      const T* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      const T* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const int64_t brow = key_blocks(sq, g, s, BK).row(static_cast<int>(gb - blk_base[s]));
+      const T* kb = k + brow * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const T* vb = v + brow * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const uint4 x = key0 + key < g.kv_len

@@ -592,6 +592,7 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   if (head_dim != kHeadDim || BK != kKlBK || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || !msa_host::is_pow2(H_q / H_kv) || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
+  if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
   return MSA_OK;
 }
 

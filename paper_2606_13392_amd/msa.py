@@ -42,6 +42,9 @@ class MsaSeqsC(ctypes.Structure):
         ("q_offsets", ctypes.c_void_p),
         ("kv_starts", ctypes.c_void_p),
         ("kv_lens", ctypes.c_void_p),
+        ("block_table", ctypes.c_void_p),
+        ("block_table_stride", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
     ]
 
 
@@ -123,10 +126,13 @@ def _need(t: torch.Tensor, name: str, dtype: torch.dtype, shape: Sequence[int], 
 
 
 class Seqs:
-    """Sequence layout (see include/msa.h): device arrays plus host totals."""
+    """Sequence layout (see include/msa.h): device arrays plus host totals.
+
+    ``block_table`` (int32 [num_seqs, max_blocks] on the device) makes the key
+    side paged with pages of ``page_size`` rows; ``kv_starts`` is then unused."""
 
     def __init__(self, q_rows: Sequence[int], kv_lens: Sequence[int], kv_starts: Sequence[int],
-                 total_kv_rows: int, device):
+                 total_kv_rows: int, device, block_table: Optional[torch.Tensor] = None, page_size: int = 0):
         assert len(q_rows) == len(kv_lens) == len(kv_starts) and len(q_rows) >= 1
         offs = [0]
         for r in q_rows:
@@ -143,9 +149,13 @@ class Seqs:
         self.total_kv_rows = int(total_kv_rows)
         self.max_q_rows = max(int(r) for r in q_rows)
         self.max_kv_len = max(int(x) for x in kv_lens)
+        self.block_table = block_table
+        if block_table is not None:
+            _need(block_table, "block_table", torch.int32, (self.num_seqs, block_table.shape[1]), self.device)
         self.c = MsaSeqsC(self.num_seqs, self.total_q_rows, self.total_kv_rows, self.max_q_rows,
                           self.max_kv_len, self.q_offsets.data_ptr(), self.kv_starts.data_ptr(),
-                          self.kv_lens.data_ptr())
+                          self.kv_lens.data_ptr(), None if block_table is None else block_table.data_ptr(),
+                          0 if block_table is None else int(block_table.shape[1]), int(page_size))
 
     @classmethod
     def from_problem(cls, p, device) -> "Seqs":

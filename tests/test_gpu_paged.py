@@ -1,0 +1,139 @@
+"""Paged key side (block table) and multi-token decode rows.
+
+A paged layout stores every key-side tensor (index_k, k, v) as a pool of
+pages of block_size rows in shuffled order, with spare pages in between;
+block b of sequence s is page block_table[s][b].  Kernels address keys one
+block at a time and compute in the same order, so every result must equal
+the contiguous layout's bit for bit; the contiguous results are checked
+against the oracle (here for multi-token "speculative" decode rows, whose
+positions are the chunked-prefill convention) and elsewhere.
+"""
+from __future__ import annotations
+
+import sys
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle.msa_oracle as O
+from paper_2606_13392_amd import msa, synth
+from tests.util import check_block_ids, check_outputs, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    msa.lib()
+    yield
+    torch.cuda.synchronize()
+
+
+def _paged_copy(p, x, dev, spare=7, seed=0):
+    """Page pool + block table for problem p's key-side tensors x (numpy bits)."""
+    B = p.block_size
+    nblk = [(L + B - 1) // B for L in p.kv_lens]
+    npages = sum(nblk) + spare
+    perm = np.random.default_rng(seed).permutation(npages)
+    table = np.zeros((p.num_seqs, max(nblk)), dtype=np.int32)
+    pool = {}
+    for name in ("index_k", "k", "v"):
+        shape = (npages * B,) + x[name].shape[1:]
+        pool[name] = np.zeros(shape, dtype=x[name].dtype)
+    used = 0
+    for s in range(p.num_seqs):
+        for b in range(nblk[s]):
+            page = int(perm[used])
+            used += 1
+            table[s, b] = page
+            r0 = p.kv_starts[s] + b * B
+            r1 = min(p.kv_starts[s] + p.kv_lens[s], r0 + B)
+            for name in pool:
+                pool[name][page * B:page * B + (r1 - r0)] = x[name][r0:r1]
+    seqs = msa.Seqs(p.q_rows, p.kv_lens, [0] * p.num_seqs, npages * B, dev,
+                    block_table=torch.from_numpy(table).to(dev), page_size=B)
+    return pool, seqs
+
+
+# name, q_rows, kv_lens, H_q, H_kv, block, topk, d_idx, kv_pad_to
+CASES = [
+    ("paged_decode", [1] * 6, [3000, 64, 65, 4097, 1, 900], 16, 4, 64, 6, 64, 4160),
+    ("paged_speculative_4", [4, 4, 4, 4], [5000, 4, 700, 2049], 16, 2, 64, 8, 64, 5120),
+    ("paged_speculative_mixed_bk128", [2, 8, 1, 3], [3000, 1500, 129, 4100], 32, 2, 128, 5, 128, 4224),
+    ("paged_chunked_prefill", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_paged_matches_contiguous(case):
+    name, q_rows, kv_lens, H_q, H_kv, bk, topk, d_idx, pad = case
+    _say(f"[case] {name}")
+    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, block_size=bk, topk=topk,
+                             d_idx=d_idx, seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
+    x = synth.generate_numpy(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {t: to_dev(v) for t, v in x.items()}
+    pool, pseqs = _paged_copy(p, x, dev)
+    pd = {t: to_dev(v) for t, v in pool.items()}
+    decode = p.max_q_rows <= 8
+    attn = msa.sparse_attn_decode if decode else msa.sparse_attn_prefill
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    pids = msa.index_topk(d["index_q"], pd["index_k"], pseqs, p.block_size, p.topk)
+    o, lse = attn(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    po, plse = attn(d["q"], pd["k"], pd["v"], pids, pseqs, p.block_size)
+    torch.cuda.synchronize()
+    assert torch.equal(ids, pids), "paged block ids differ from contiguous"
+    assert torch.equal(o.view(torch.int16), po.view(torch.int16)) and torch.equal(lse, plse), \
+        "paged attention differs from contiguous"
+    # the contiguous results against the oracle
+    lay = O.layout_of(p)
+    ids_h = ids.cpu().numpy()
+    ora_ids, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
+    exact, ties = check_block_ids(ids_h, ora_ids, gaps, x, lay, p.block_size, p.topk)
+    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_h, lay, p.block_size)
+    st = check_outputs(o.float().cpu().numpy(), lse.cpu().numpy(), o_ref, l_ref, name)
+    _say(f"  ids exact {exact} ties {ties}; O max-abs {st[0]:.2e} rel-L2 {st[1]:.2e}")
+
+
+def test_paged_fp8_decode_matches_contiguous():
+    name = "paged_fp8"
+    p = synth.packed_problem(name, [1] * 4, [2000, 70, 4096, 513], num_q_heads=16, num_kv_heads=4, topk=6,
+                             seed=31, kv_pad_to=4096)
+    x = synth.generate_fp8_numpy(p, synth.FP8_SCALES)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    pool, pseqs = _paged_copy(p, x, dev, seed=3)
+    iq, ik = to_dev(x["index_q"]), to_dev(x["index_k"])
+    ids = msa.index_topk(iq, ik, seqs, p.block_size, p.topk)
+    q8 = torch.from_numpy(x["q"]).to(dev)
+    o, lse = msa.sparse_attn_decode_fp8(q8, torch.from_numpy(x["k"]).to(dev), torch.from_numpy(x["v"]).to(dev),
+                                        synth.FP8_SCALES, ids, seqs, p.block_size)
+    po, plse = msa.sparse_attn_decode_fp8(q8, torch.from_numpy(pool["k"]).to(dev), torch.from_numpy(pool["v"]).to(dev),
+                                          synth.FP8_SCALES, ids, pseqs, p.block_size)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), po.view(torch.int16)) and torch.equal(lse, plse)
+
+
+def test_paged_rejections():
+    p = synth.packed_problem("paged_rej", [1, 1], [100, 200], num_q_heads=8, num_kv_heads=2, topk=2, seed=5)
+    x = synth.generate_numpy(p)
+    dev = torch.device("cuda")
+    pool, pseqs = _paged_copy(p, x, dev)
+    L = msa.lib()
+    # page size must equal the call's block size
+    assert L.msa_index_topk_workspace_size(pseqs.ref(), 2, 64, 128, 2) == 0
+    # calls that address keys as contiguous ranges reject a paged layout
+    assert L.msa_dense_attn_workspace_size(pseqs.ref(), 8, 2, 128) == 0
+    assert L.msa_sparse_attn_backward_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) == 0
+    assert L.msa_sparse_kl_backward_workspace_size(pseqs.ref(), 8, 2, 64, 128, 64, 2) == 0
+    assert L.msa_sparse_attn_prefill_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) > 0
