@@ -8,7 +8,8 @@ workload is prefill at T = 1,048,576 tokens (64 query / 8 KV heads, head dim
 128, index dim 64, block 64, k = 64, planted blocks); ``value`` is its
 throughput in tokens/s.  A decode phase (64 sequences x 1 token at context
 131,072, k = 32: msa_index_topk + msa_sparse_attn_decode) is timed after it and
-reported under "decode", and a training step of the attention at T = 32,768
+reported under "decode" (with the same step on a paged copy of the caches
+under "decode.paged"), and a training step of the attention at T = 32,768
 (forward, msa_sparse_attn_backward, msa_sparse_kl_backward) under "training".
 
 Inputs are drawn on the device before timing (synthetic, seeded) and stay
@@ -342,6 +343,7 @@ def run_decode(args, dev):
         t_idx.time(call_index)
         t_att.time(call_attn)
     torch.cuda.synchronize()
+    ref = (ids.clone(), o.clone(), lse.clone())      # the bf16 step's results (later legs reuse o / lse)
     fp8 = None
     if args.fp8:
         x8 = synth.generate_torch(p, dev, tensors=("q", "k", "v"), fp8_scales=synth.FP8_SCALES)
@@ -377,6 +379,9 @@ def run_decode(args, dev):
         dense = {"ms_per_step": dms, "kv_bytes": kv_bytes, "hbm_gbs": kv_bytes / (dms * 1e-3) / 1e9,
                  "msa_speedup": dms / (sec * 1e3)}
         del ws_d
+    paged = None
+    if not args.no_paged:
+        paged = run_decode_paged(p, d, seqs, *ref, args, dev)
     positions = torch.from_numpy(p.positions()).to(dev)
     toks = attended_tokens(ids, positions, p.block_size)
     scored = index_scored_keys(positions, p.block_size)
@@ -401,6 +406,10 @@ def run_decode(args, dev):
         "dense_baseline": dense,
         "paper_decode_speedup_h800": 7.6,
     }
+    if paged is not None:
+        paged["hbm_gbs"] = (idx_bytes + att_bytes) / (paged["ms_per_step"] * 1e-3) / 1e9
+        paged["hbm_frac"] = paged["hbm_gbs"] / PEAK_HBM_GBS
+        out["paged"] = paged
     if fp8 is not None:
         # bytes of the step with 1-byte Q, K, V (index tensors stay bf16)
         att8 = (float(toks.sum().item()) * dh * 2 + rows * H_q * dh * (1 + 2) + rows * H_q * 4
@@ -500,6 +509,66 @@ def run_training(args, dev):
     return out
 
 
+def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev):
+    """The decode step on a paged copy of the caches: every key-side tensor
+    becomes a pool of block_size-row pages in a seeded random order, read
+    through a block table; checks the step reproduces the contiguous
+    results bit for bit and times it the same way."""
+    import torch
+    from paper_2606_13392_amd import msa
+    B = p.block_size
+    nblk = [(L + B - 1) // B for L in p.kv_lens]
+    npages = sum(nblk)
+    g = torch.Generator(device="cpu")
+    g.manual_seed(p.seed + 77)
+    perm = torch.randperm(npages, generator=g).to(torch.int32)
+    table = torch.zeros((p.num_seqs, max(nblk)), dtype=torch.int32)
+    src_blocks = []
+    used = 0
+    for s_, n in enumerate(nblk):
+        table[s_, :n] = perm[used:used + n]
+        src_blocks.append(torch.arange(n, dtype=torch.int64) * B + p.kv_starts[s_])
+        used += n
+    src = torch.cat(src_blocks).to(dev)                      # first row of each source block
+    dst = perm.to(torch.int64).to(dev)                       # its page
+    pool = {}
+    for name in ("index_k", "k", "v"):
+        t = d[name]
+        out = torch.empty((npages * B,) + tuple(t.shape[1:]), dtype=t.dtype, device=dev)
+        rows = (src.view(-1, 1) + torch.arange(B, device=dev).view(1, -1)).clamp_max(t.shape[0] - 1)
+        out.view(npages, B, -1)[dst] = t[rows.view(-1)].view(npages, B, -1)
+        pool[name] = out
+    pseqs = msa.Seqs(p.q_rows, p.kv_lens, [0] * p.num_seqs, npages * B, dev, block_table=table.to(dev),
+                     page_size=B)
+    H_q, H_kv, dh = p.num_q_heads, p.num_kv_heads, p.head_dim
+    ids = torch.empty_like(ids_ref)
+    o = torch.empty_like(o_ref)
+    lse = torch.empty_like(lse_ref)
+    ws_i = torch.empty(msa.index_topk_workspace_size(pseqs, H_kv, p.d_idx, B, p.topk), dtype=torch.uint8,
+                       device=dev)
+    ws_a = torch.empty(max(1, msa.sparse_attn_decode_workspace_size(pseqs, H_q, H_kv, dh, B, p.topk)),
+                       dtype=torch.uint8, device=dev)
+
+    def step():
+        msa.index_topk(d["index_q"], pool["index_k"], pseqs, B, p.topk, out=ids, workspace=ws_i)
+        msa.sparse_attn_decode(d["q"], pool["k"], pool["v"], ids, pseqs, B, out=o, lse=lse, workspace=ws_a)
+
+    for _ in range(args.decode_warmup):
+        step()
+    torch.cuda.synchronize()
+    same = bool(torch.equal(ids, ids_ref) and torch.equal(o.view(torch.int16), o_ref.view(torch.int16))
+                and torch.equal(lse, lse_ref))
+    t0 = time.perf_counter()
+    for _ in range(args.decode_steps):
+        step()
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.decode_steps
+    del pool, ws_i, ws_a
+    torch.cuda.empty_cache()
+    return {"ms_per_step": sec * 1e3, "value": p.total_q_rows / sec, "unit": "tok/s", "pages": npages,
+            "page_rows": B, "bit_identical_to_contiguous": same}
+
+
 def cpu_baseline(pre, args):
     """The CPU oracle on a bounded random sample of query rows (host cores)."""
     import numpy as np
@@ -551,6 +620,7 @@ def main():
     ap.add_argument("--decode-steps", type=int, default=20)
     ap.add_argument("--decode-warmup", type=int, default=3)
     ap.add_argument("--no-decode", action="store_true")
+    ap.add_argument("--no-paged", action="store_true", help="skip the decode step on a paged KV cache")
     ap.add_argument("--train-workload", default="prefill_32k",
                     help="shape of the training step (forward + Main Branch backward + KL backward)")
     ap.add_argument("--train-steps", type=int, default=3)
