@@ -388,7 +388,8 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
     int64_t ldm) {
   constexpr int KS = D_IDX / 32;
-  constexpr int MT = BK / 16;
+  constexpr int HB = BK / 64;                         // 64-key sub-blocks per block
+  constexpr int MT = 4;                               // 16-key tiles per sub-block
   const int lane = lane_id();
   const int64_t uidx = u0 + blockIdx.y;
   const int slice = blockIdx.x * kWaves + threadIdx.x / kWave;
@@ -410,25 +411,27 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
   const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
   const uint16_t* kbase = index_k + ((PAGED ? 0 : ur.g.kv_start) + n) * D_IDX + 8 * q4;
 
-  // blocks kb0 .. kb1-1 are entirely before every row's local block, hence
-  // inside the sequence; loads past kb1 re-read block kb1-1
-  auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
-    kb = min(kb, kb1 - 1);
+  // sub-block j = keys 64 (j % HB) .. +63 of block kb0 + j / HB.  Blocks kb0
+  // .. kb1-1 are entirely before every row's local block, hence inside the
+  // sequence; loads past kb1 re-read block kb1-1
+  auto load_a = [&](int j, bf16x8 (&a)[MT][KS]) {
+    const int kb = min(kb0 + j / HB, kb1 - 1);
+    const int k0 = 64 * (j % HB);
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + 16 * i) * D_IDX
-                                 : kbase + static_cast<int64_t>(kb * BK + 16 * i) * D_IDX;
+      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + k0 + 16 * i) * D_IDX
+                                 : kbase + static_cast<int64_t>(kb * BK + k0 + 16 * i) * D_IDX;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) a[i][ks] = ld_bf16x8(kp + 32 * ks);
     }
   };
   bf16x8 buf[DEPTH][MT][KS];
 #pragma unroll
-  for (int d = 0; d < DEPTH; ++d) load_a(kb0 + d, buf[d]);
+  for (int d = 0; d < DEPTH; ++d) load_a(d, buf[d]);
   float mb[kSliceBlocks];
 #pragma unroll
-  for (int i = 0; i < kSliceBlocks; ++i) {
-    bf16x8 (&a)[MT][KS] = buf[i % DEPTH];
+  for (int j = 0; j < kSliceBlocks * HB; ++j) {
+    bf16x8 (&a)[MT][KS] = buf[j % DEPTH];
     f32x4 acc[MT];
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
@@ -443,8 +446,8 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
       for (int e = 0; e < 4; ++e) m = fmaxf(m, acc[t][e]);
     m = fmaxf(m, __uint_as_float(xor_lane_u32<16>(__float_as_uint(m))));
     m = fmaxf(m, __uint_as_float(xor_lane_u32<32>(__float_as_uint(m))));
-    mb[i] = m;
-    if (i + DEPTH < kSliceBlocks) load_a(kb0 + i + DEPTH, a);
+    mb[j / HB] = j % HB == 0 ? m : fmaxf(mb[j / HB], m);
+    if (j + DEPTH < kSliceBlocks * HB) load_a(j + DEPTH, a);
   }
   // values past kb1 are never read (they are >= every row's local block) and
   // stay inside this slice; quads start below ldm (a multiple of 4)
@@ -718,7 +721,7 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   // sequences longer than four row groups
   const int64_t mq = seqs->max_q_rows;
   pl->U = mq > 4 * pl->qr && d_idx == 64 && BK == 64 ? 2 * kWaves : (mq > 2 * pl->qr ? kWaves : 1);
-  pl->narrow = pl->U == 1 && std::min(pl->qr, seqs->max_q_rows) * H_kv <= 16 && !(d_idx == 128 && BK == 128);
+  pl->narrow = pl->U == 1 && std::min(pl->qr, seqs->max_q_rows) * H_kv <= 16;
   // at most one row group per sequence: unit s is sequence s, no unit table
   pl->seq_units = pl->U == 1 && seqs->max_q_rows <= pl->qr;
   const int64_t max_groups = seqs->total_q_rows / pl->qr + seqs->num_seqs;
@@ -734,9 +737,9 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
 constexpr int64_t kSplitTopkRows = 4096;                 // fewer index rows: 4 waves per row
 
-// Blocks in flight per wave of the narrow kernel: about 128 VGPRs of K_idx.
+// 64-key sub-blocks in flight per wave of the narrow kernel: about 128 VGPRs of K_idx.
 template <int D, int B>
-constexpr int kNarrowDepth = D * B <= 64 * 64 ? 4 : 2;
+constexpr int kNarrowDepth = D == 64 ? 4 : 2;
 
 template <int D, int B, bool PAGED>
 void launch_scores_as(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
