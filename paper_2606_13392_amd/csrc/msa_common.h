@@ -130,6 +130,26 @@ __device__ __forceinline__ uint64_t xor_lane_u64(uint64_t v) {
   const uint32_t hi = xor_lane_u32<J>(static_cast<uint32_t>(v >> 32));
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
+// Transposed store of 8 consecutive bf16 (w: elements 2k, 2k+1 in word k) of
+// row `col` into dst[d0 + e][col]: lanes l and l ^ 1 (rows col and col ^ 1)
+// trade two words so that each writes four 32-bit row pairs, the even lane
+// elements 0..3 and the odd lane elements 4..7.  Every lane must take part.
+template <int P>
+__device__ __forceinline__ void store_transposed_pairs(uint16_t (*dst)[P], int d0, int col, const u32x4& w) {
+  const bool odd = col & 1;
+  const uint32_t r0 = xor_lane_u32<1>(odd ? w[0] : w[2]);   // the neighbour's words of my half
+  const uint32_t r1 = xor_lane_u32<1>(odd ? w[1] : w[3]);
+  const uint32_t m0 = odd ? w[2] : w[0], m1 = odd ? w[3] : w[1];
+  const uint32_t ev0 = odd ? r0 : m0, od0 = odd ? m0 : r0;   // even row's / odd row's word
+  const uint32_t ev1 = odd ? r1 : m1, od1 = odd ? m1 : r1;
+  const int dd = d0 + (odd ? 4 : 0);
+  const int c0 = col & ~1;
+  *reinterpret_cast<uint32_t*>(&dst[dd + 0][c0]) = (ev0 & 0xFFFFu) | (od0 << 16);
+  *reinterpret_cast<uint32_t*>(&dst[dd + 1][c0]) = (ev0 >> 16) | (od0 & 0xFFFF0000u);
+  *reinterpret_cast<uint32_t*>(&dst[dd + 2][c0]) = (ev1 & 0xFFFFu) | (od1 << 16);
+  *reinterpret_cast<uint32_t*>(&dst[dd + 3][c0]) = (ev1 >> 16) | (od1 & 0xFFFF0000u);
+}
+
 // Value of lane - 1 (lane 0 receives `fill`): DPP wave shift right by one.
 __device__ __forceinline__ uint64_t lane_shr1_u64(uint64_t v, uint64_t fill) {
   const int lo = __builtin_amdgcn_update_dpp(static_cast<int>(static_cast<uint32_t>(fill)),

@@ -209,11 +209,8 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
         const int col = 32 * rg + 16 * t + c16;
         const u32x4 wq = kq == 0 ? bq[t][0] : kq == 1 ? bq[t][1] : kq == 2 ? bq[t][2] : bq[t][3];
         const u32x4 wd = kq == 0 ? bdo[t][0] : kq == 1 ? bdo[t][1] : kq == 2 ? bdo[t][2] : bdo[t][3];
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          sm.qt[32 * kq + 8 * qd + j][col] = raw_elem(wq, j);
-          sm.dot[32 * kq + 8 * qd + j][col] = raw_elem(wd, j);
-        }
+        store_transposed_pairs(sm.qt, 32 * kq + 8 * qd, col, wq);
+        store_transposed_pairs(sm.dot, 32 * kq + 8 * qd, col, wd);
         if (qd == 0 && kq == 0) {
           const int qa = c + rg * qpw + (t ? jq1 : jq0);
           sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
