@@ -382,6 +382,7 @@ def run_decode(args, dev):
     paged = None
     if not args.no_paged:
         paged = run_decode_paged(p, d, seqs, *ref, args, dev)
+        paged4 = run_decode_paged(p, d, seqs, *ref, args, dev, blocks_per_page=4)
     positions = torch.from_numpy(p.positions()).to(dev)
     toks = attended_tokens(ids, positions, p.block_size)
     scored = index_scored_keys(positions, p.block_size)
@@ -407,9 +408,11 @@ def run_decode(args, dev):
         "paper_decode_speedup_h800": 7.6,
     }
     if paged is not None:
-        paged["hbm_gbs"] = (idx_bytes + att_bytes) / (paged["ms_per_step"] * 1e-3) / 1e9
-        paged["hbm_frac"] = paged["hbm_gbs"] / PEAK_HBM_GBS
+        for rec in (paged, paged4):
+            rec["hbm_gbs"] = (idx_bytes + att_bytes) / (rec["ms_per_step"] * 1e-3) / 1e9
+            rec["hbm_frac"] = rec["hbm_gbs"] / PEAK_HBM_GBS
         out["paged"] = paged
+        out["paged_4_block_pages"] = paged4
     if fp8 is not None:
         # bytes of the step with 1-byte Q, K, V (index tensors stay bf16)
         att8 = (float(toks.sum().item()) * dh * 2 + rows * H_q * dh * (1 + 2) + rows * H_q * 4
@@ -509,14 +512,14 @@ def run_training(args, dev):
     return out
 
 
-def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev):
+def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev, blocks_per_page=1):
     """The decode step on a paged copy of the caches: every key-side tensor
-    becomes a pool of block_size-row pages in a seeded random order, read
-    through a block table; checks the step reproduces the contiguous
-    results bit for bit and times it the same way."""
+    becomes a pool of pages (blocks_per_page key blocks each) in a seeded
+    random order, read through a block table; checks the step reproduces the
+    contiguous results bit for bit and times it the same way."""
     import torch
     from paper_2606_13392_amd import msa
-    B = p.block_size
+    B = p.block_size * blocks_per_page                      # page rows
     nblk = [(L + B - 1) // B for L in p.kv_lens]
     npages = sum(nblk)
     g = torch.Generator(device="cpu")
@@ -540,6 +543,7 @@ def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev):
         pool[name] = out
     pseqs = msa.Seqs(p.q_rows, p.kv_lens, [0] * p.num_seqs, npages * B, dev, block_table=table.to(dev),
                      page_size=B)
+    B = p.block_size
     H_q, H_kv, dh = p.num_q_heads, p.num_kv_heads, p.head_dim
     ids = torch.empty_like(ids_ref)
     o = torch.empty_like(o_ref)
@@ -566,7 +570,7 @@ def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev):
     del pool, ws_i, ws_a
     torch.cuda.empty_cache()
     return {"ms_per_step": sec * 1e3, "value": p.total_q_rows / sec, "unit": "tok/s", "pages": npages,
-            "page_rows": B, "bit_identical_to_contiguous": same}
+            "page_rows": B * blocks_per_page, "bit_identical_to_contiguous": same}
 
 
 def cpu_baseline(pre, args):

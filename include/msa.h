@@ -54,11 +54,12 @@
  * chunked-prefill case with a few rows.
  *
  * Paged key side (optional): with block_table != NULL the key-side tensors
- * (index_k, k, v) are a pool of pages of page_size rows, and key block b of
- * sequence s lives in page block_table[s * block_table_stride + b], i.e. at
- * rows page * page_size .. + page_size - 1 (kv_starts is then ignored and may
- * be NULL).  page_size must equal the block_size of the call; kv_lens[s] <=
- * block_table_stride * page_size.  Page ids outside [0, total_kv_rows /
+ * (index_k, k, v) are a pool of pages of page_size rows; key j of sequence s
+ * is row page * page_size + j % page_size with
+ * page = block_table[s * block_table_stride + j / page_size] (kv_starts is
+ * then ignored and may be NULL).  page_size must be block_size times 1, 2, 4,
+ * ... or 64 for the call's block_size; kv_lens[s] <= block_table_stride *
+ * page_size.  Page ids outside [0, total_kv_rows /
  * page_size) are clamped into it (results unspecified, memory safe).  This
  * is a serving layout, not part of the paper.  msa_index_topk,
  * msa_sparse_attn_prefill/_decode and their fp8 variants accept it; the
@@ -95,8 +96,8 @@ typedef struct msa_seqs {
   const int32_t* kv_lens;    /* device [num_seqs], >= the sequence's query rows */
   const int32_t* block_table;   /* device [num_seqs, block_table_stride] page ids, or NULL
                                    (contiguous key side) */
-  int32_t block_table_stride;   /* host: entries per sequence of block_table */
-  int32_t page_size;            /* host: key rows per page (= the call's block_size) */
+  int32_t block_table_stride;   /* host: entries (pages) per sequence of block_table */
+  int32_t page_size;            /* host: key rows per page (block_size x 2^j, j <= 6) */
 } msa_seqs;
 
 /* Human-readable text of a status code (static storage). */

@@ -413,13 +413,16 @@ __global__ __launch_bounds__(256) void index_block_max_narrow_kernel(
 
   // sub-block j = keys 64 (j % HB) .. +63 of block kb0 + j / HB.  Blocks kb0
   // .. kb1-1 are entirely before every row's local block, hence inside the
-  // sequence; loads past kb1 re-read block kb1-1
+  // sequence; loads past kb1 re-read block kb1-1.  Paged: lane i holds the
+  // page of the slice's block i, fetched once.
+  const int64_t my_prow = PAGED ? kbk.template row_as<true>(min(kb0 + (lane % kSliceBlocks), kb1 - 1)) : 0;
   auto load_a = [&](int j, bf16x8 (&a)[MT][KS]) {
     const int kb = min(kb0 + j / HB, kb1 - 1);
     const int k0 = 64 * (j % HB);
+    const int64_t prow = PAGED ? static_cast<int64_t>(readlane_u64(static_cast<uint64_t>(my_prow), j / HB)) : 0;
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + k0 + 16 * i) * D_IDX
+      const uint16_t* kp = PAGED ? kbase + (prow + k0 + 16 * i) * D_IDX
                                  : kbase + static_cast<int64_t>(kb * BK + k0 + 16 * i) * D_IDX;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) a[i][ks] = ld_bf16x8(kp + 32 * ks);

@@ -270,20 +270,25 @@ __device__ __forceinline__ SeqGeom seq_geom(const msa_seqs& sq, int s) {
 }
 
 // First key row of key block b (blocks of BK keys) of sequence s: kv_start +
-// b BK on a contiguous key side, else the page the block table lists (pages
-// of BK rows), clamped into the pool.
+// b BK on a contiguous key side, else inside the page the block table lists
+// for it (pages of 2^lg_bpp blocks; page ids clamped into the pool).
 struct KeyBlocks {
   const int32_t* table;      // the sequence's block-table row, or null
   int64_t base;              // kv_start
   int64_t max_page;
   int BK;
+  int lg_bpp;                // log2 of key blocks per page
+  // first key row of block b, given the page id of its page
+  __device__ __forceinline__ int64_t block_row(int64_t page, int b) const {
+    page = page < 0 ? 0 : (page > max_page ? max_page : page);
+    return (page << lg_bpp) * BK + static_cast<int64_t>(b & ((1 << lg_bpp) - 1)) * BK;
+  }
+  __device__ __forceinline__ int page_index(int b) const { return b >> lg_bpp; }
   // PAGED fixes the layout at compile time (hot loops); row() decides at run time
   template <bool PAGED>
   __device__ __forceinline__ int64_t row_as(int b) const {
     if constexpr (PAGED) {
-      int64_t page = table[b];
-      page = page < 0 ? 0 : (page > max_page ? max_page : page);
-      return page * BK;
+      return block_row(table[page_index(b)], b);
     } else {
       return base + static_cast<int64_t>(b) * BK;
     }
@@ -294,8 +299,11 @@ __device__ __forceinline__ KeyBlocks key_blocks(const msa_seqs& sq, const SeqGeo
   KeyBlocks kb;
   kb.table = sq.block_table ? sq.block_table + static_cast<int64_t>(s) * sq.block_table_stride : nullptr;
   kb.base = g.kv_start;
-  kb.max_page = sq.total_kv_rows / BK - 1;
   kb.BK = BK;
+  kb.lg_bpp = 0;
+  if (sq.block_table)
+    while ((BK << kb.lg_bpp) < sq.page_size) ++kb.lg_bpp;
+  kb.max_page = sq.block_table ? sq.total_kv_rows / sq.page_size - 1 : 0;
   return kb;
 }
 
@@ -325,12 +333,15 @@ inline int validate_seqs(const msa_seqs* s) {
   return MSA_OK;
 }
 
-// A paged key side is accepted by calls that address keys per block; its
-// pages must hold exactly one key block.
+// A paged key side is accepted by calls that address keys per block; a page
+// holds 1, 2, 4, ... or 64 key blocks.
 inline int check_paged(const msa_seqs* s, int block_size, bool supported) {
   if (!s->block_table) return MSA_OK;
   if (!supported) return MSA_ERR_UNSUPPORTED;
-  return s->page_size == block_size ? MSA_OK : MSA_ERR_INVALID;
+  // pages of 2^j key blocks, j <= 6
+  for (int j = 0; j <= 6; ++j)
+    if (s->page_size == (block_size << j)) return MSA_OK;
+  return MSA_ERR_INVALID;
 }
 
 inline int launch_status() {

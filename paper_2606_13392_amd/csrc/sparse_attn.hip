@@ -128,6 +128,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   const int slot1 = min(topk, slot0 + slots_per_wave);
   // the wave's block ids, one per lane, fetched at once (slots_per_wave <= 64 with ids)
   const int my_b = ids && slot0 + lane < slot1 ? ids[slot0 + lane] : -1;
+  // paged: each lane fetches the page of its slot's block up front (no table
+  // read between a block's id and its loads)
+  int32_t my_pg = 0;
+  if constexpr (PAGED) {
+    const int bb = ids ? my_b : slot0 + lane;
+    if (p >= 0 && slot0 + lane < slot1 && bb >= 0 && bb <= p / BK) my_pg = kbk.table[kbk.page_index(bb)];
+  }
   for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
     const int b = ids ? __builtin_amdgcn_readlane(my_b, slot - slot0) : slot;
     if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
@@ -135,7 +142,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     // K (A operands of S^T) and raw V of this block are requested together;
     // S^T and the softmax run while V is still in flight.
     // paged: the block's page (keys addressed inside it); else keys from kv_start
-    const int64_t page_row = PAGED ? kbk.template row_as<true>(b) : 0;
+    const int64_t page_row = PAGED ? kbk.block_row(__builtin_amdgcn_readlane(my_pg, slot - slot0), b) : 0;
     Raw<T> ka[BK / 16][kHeadDim / 32];
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i) {

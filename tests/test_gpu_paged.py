@@ -1,8 +1,8 @@
 """Paged key side (block table) and multi-token decode rows.
 
 A paged layout stores every key-side tensor (index_k, k, v) as a pool of
-pages of block_size rows in shuffled order, with spare pages in between;
-block b of sequence s is page block_table[s][b].  Kernels address keys one
+pages of 1-8 key blocks in shuffled order, with spare pages in between; key
+j of sequence s sits in page block_table[s][j // page_size].  Kernels address keys one
 block at a time and compute in the same order, so every result must equal
 the contiguous layout's bit for bit; the contiguous results are checked
 against the oracle (here for multi-token "speculative" decode rows, whose
@@ -38,44 +38,47 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def _paged_copy(p, x, dev, spare=7, seed=0):
-    """Page pool + block table for problem p's key-side tensors x (numpy bits)."""
-    B = p.block_size
-    nblk = [(L + B - 1) // B for L in p.kv_lens]
-    npages = sum(nblk) + spare
+def _paged_copy(p, x, dev, spare=7, seed=0, blocks_per_page=1):
+    """Page pool + block table for problem p's key-side tensors x (numpy bits);
+    pages of blocks_per_page key blocks."""
+    P = p.block_size * blocks_per_page
+    npg = [(L + P - 1) // P for L in p.kv_lens]
+    npages = sum(npg) + spare
     perm = np.random.default_rng(seed).permutation(npages)
-    table = np.zeros((p.num_seqs, max(nblk)), dtype=np.int32)
+    table = np.zeros((p.num_seqs, max(npg)), dtype=np.int32)
     pool = {}
     for name in ("index_k", "k", "v"):
-        shape = (npages * B,) + x[name].shape[1:]
+        shape = (npages * P,) + x[name].shape[1:]
         pool[name] = np.zeros(shape, dtype=x[name].dtype)
     used = 0
     for s in range(p.num_seqs):
-        for b in range(nblk[s]):
+        for g in range(npg[s]):
             page = int(perm[used])
             used += 1
-            table[s, b] = page
-            r0 = p.kv_starts[s] + b * B
-            r1 = min(p.kv_starts[s] + p.kv_lens[s], r0 + B)
+            table[s, g] = page
+            r0 = p.kv_starts[s] + g * P
+            r1 = min(p.kv_starts[s] + p.kv_lens[s], r0 + P)
             for name in pool:
-                pool[name][page * B:page * B + (r1 - r0)] = x[name][r0:r1]
-    seqs = msa.Seqs(p.q_rows, p.kv_lens, [0] * p.num_seqs, npages * B, dev,
-                    block_table=torch.from_numpy(table).to(dev), page_size=B)
+                pool[name][page * P:page * P + (r1 - r0)] = x[name][r0:r1]
+    seqs = msa.Seqs(p.q_rows, p.kv_lens, [0] * p.num_seqs, npages * P, dev,
+                    block_table=torch.from_numpy(table).to(dev), page_size=P)
     return pool, seqs
 
 
-# name, q_rows, kv_lens, H_q, H_kv, block, topk, d_idx, kv_pad_to
+# name, q_rows, kv_lens, H_q, H_kv, block, topk, d_idx, kv_pad_to, blocks per page
 CASES = [
-    ("paged_decode", [1] * 6, [3000, 64, 65, 4097, 1, 900], 16, 4, 64, 6, 64, 4160),
-    ("paged_speculative_4", [4, 4, 4, 4], [5000, 4, 700, 2049], 16, 2, 64, 8, 64, 5120),
-    ("paged_speculative_mixed_bk128", [2, 8, 1, 3], [3000, 1500, 129, 4100], 32, 2, 128, 5, 128, 4224),
-    ("paged_chunked_prefill", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None),
+    ("paged_decode", [1] * 6, [3000, 64, 65, 4097, 1, 900], 16, 4, 64, 6, 64, 4160, 1),
+    ("paged_decode_4blk_pages", [1] * 6, [3000, 64, 65, 4097, 1, 900], 16, 4, 64, 6, 64, 4160, 4),
+    ("paged_speculative_4", [4, 4, 4, 4], [5000, 4, 700, 2049], 16, 2, 64, 8, 64, 5120, 1),
+    ("paged_speculative_mixed_bk128", [2, 8, 1, 3], [3000, 1500, 129, 4100], 32, 2, 128, 5, 128, 4224, 2),
+    ("paged_chunked_prefill", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None, 1),
+    ("paged_chunked_prefill_8blk_pages", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None, 8),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_paged_matches_contiguous(case):
-    name, q_rows, kv_lens, H_q, H_kv, bk, topk, d_idx, pad = case
+    name, q_rows, kv_lens, H_q, H_kv, bk, topk, d_idx, pad, bpp = case
     _say(f"[case] {name}")
     p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, block_size=bk, topk=topk,
                              d_idx=d_idx, seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
@@ -83,7 +86,7 @@ def test_paged_matches_contiguous(case):
     dev = torch.device("cuda")
     seqs = msa.Seqs.from_problem(p, dev)
     d = {t: to_dev(v) for t, v in x.items()}
-    pool, pseqs = _paged_copy(p, x, dev)
+    pool, pseqs = _paged_copy(p, x, dev, blocks_per_page=bpp)
     pd = {t: to_dev(v) for t, v in pool.items()}
     decode = p.max_q_rows <= 8
     attn = msa.sparse_attn_decode if decode else msa.sparse_attn_prefill
@@ -130,8 +133,11 @@ def test_paged_rejections():
     dev = torch.device("cuda")
     pool, pseqs = _paged_copy(p, x, dev)
     L = msa.lib()
-    # page size must equal the call's block size
+    # the page size must be the call's block size times a power of two
     assert L.msa_index_topk_workspace_size(pseqs.ref(), 2, 64, 128, 2) == 0
+    assert L.msa_index_topk_workspace_size(pseqs.ref(), 2, 64, 64, 2) > 0
+    pool3, pseqs3 = _paged_copy(p, x, dev, blocks_per_page=3)
+    assert L.msa_index_topk_workspace_size(pseqs3.ref(), 2, 64, 64, 2) == 0
     # calls that address keys as contiguous ranges reject a paged layout
     assert L.msa_dense_attn_workspace_size(pseqs.ref(), 8, 2, 128) == 0
     assert L.msa_sparse_attn_backward_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) == 0
