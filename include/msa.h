@@ -253,8 +253,9 @@ int msa_dense_attn(const void* q, const void* k, const void* v, const msa_seqs* 
  * a key block in an order fixed at run time, so their last bits can differ
  * between calls.  Workspace, stream and
  * error behaviour as for msa_sparse_attn_prefill.  Supported: head_dim == 128;
- * block_size == 64; 1 <= topk <= 64; 1 <= num_q_heads / num_kv_heads <= 16;
- * num_kv_heads <= 64 (block_size 128 returns MSA_ERR_UNSUPPORTED).
+ * block_size 64 with 1 <= topk <= 64, or block_size 128 with 1 <= topk <= 32
+ * (run as the blocks' 64-key halves); 1 <= num_q_heads / num_kv_heads <= 16;
+ * num_kv_heads <= 64.
  * ------------------------------------------------------------------------ */
 size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,
                                                int num_kv_heads, int head_dim, int block_size,
@@ -295,7 +296,8 @@ int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const 
  * Workspace, stream and error behaviour as for msa_sparse_attn_prefill.
  * d_index_q and kl are bit-reproducible; d_index_k adds a key block's queries
  * in an order fixed at run time.  Supported: d_idx in {64, 128};
- * head_dim == 128; block_size == 64; 1 <= topk <= 64;
+ * head_dim == 128; block_size 64 with 1 <= topk <= 64, or block_size 128 with
+ * 1 <= topk <= 32 (run as the blocks' 64-key halves);
  * num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}; num_kv_heads <= 64.
  * ------------------------------------------------------------------------ */
 size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,

@@ -270,6 +270,21 @@ int persistent_ctas(K kernel, int threads, int* cache) {
   }
   return *cache;
 }
+// Block ids of B_k = 64 f from ids of blocks of 64 f keys: block b becomes its
+// f sub-blocks f b .. f b + f - 1 (ascending order and -1 padding kept), so a
+// 64-key kernel covers exactly the same tokens.  One thread per (row, group).
+__global__ __launch_bounds__(256) void expand_block_ids_kernel(const int32_t* __restrict__ ids, int64_t pairs,
+                                                               int topk, int f, int32_t* __restrict__ out) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= pairs) return;
+  const int32_t* src = ids + i * topk;
+  int32_t* dst = out + i * topk * f;
+  for (int j = 0; j < topk; ++j) {
+    const int32_t b = src[j];
+    for (int e = 0; e < f; ++e) dst[j * f + e] = b >= 0 ? b * f + e : -1;
+  }
+}
+
 // Reverse index of query rows r0 .. r0 + nr - 1 (one chunk): counts, scans
 // and handle lists for every tile of H_kv x nbcap.
 void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int64_t* blk_base, int H_kv, int BK,

@@ -480,37 +480,26 @@ int validate_bwd(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, 
   if (st != MSA_OK) return st;
   if (H_q < 1 || H_kv < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
   if (H_q % H_kv != 0) return MSA_ERR_INVALID;
-  if (head_dim != kHeadDim || BK != kBwdBK) return MSA_ERR_UNSUPPORTED;
+  if (head_dim != kHeadDim || (BK != kBwdBK && BK != 2 * kBwdBK)) return MSA_ERR_UNSUPPORTED;
+  if (BK == 2 * kBwdBK && topk > 32) return MSA_ERR_UNSUPPORTED;   // its 64-key halves fill <= 64 slots
   if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
   return MSA_OK;
 }
 
-}  // namespace
-
-extern "C" size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
-                                                         int head_dim, int block_size, int topk) {
-  if (validate_bwd(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
-  BwdPlan pl;
-  if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk, kDefaultBwdBytes, &pl) != MSA_OK) {
-    if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
-    pl.chunk_rows = 1;
-    bwd_layout(pl, seqs, num_q_heads, num_kv_heads, topk);
-  }
-  return pl.total;
+// Block size 128: each id is expanded to its two 64-key halves in front of
+// the workspace and the 64-key path runs on 2 topk slots.
+size_t expanded_ids_bytes(const msa_seqs* seqs, int H_kv, int BK, int topk) {
+  if (BK == kBwdBK) return 0;
+  return msa_host::align_up(sizeof(int32_t) * static_cast<size_t>(seqs->total_q_rows) * H_kv * topk *
+                                (BK / kBwdBK), 256);
 }
 
-extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const void* o, const float* lse,
-                                        const void* d_o, const int32_t* block_ids, const msa_seqs* seqs,
-                                        int num_q_heads, int num_kv_heads, int head_dim, int block_size, int topk,
-                                        float softmax_scale, void* d_q, void* d_k, void* d_v, void* workspace,
-                                        size_t workspace_bytes, hipStream_t stream) {
-  const int H_q = num_q_heads, H_kv = num_kv_heads;
-  int st = validate_bwd(seqs, H_q, H_kv, head_dim, block_size, topk);
-  if (st != MSA_OK) return st;
-  if (!q || !k || !v || !o || !lse || !d_o || !block_ids || !d_q || !d_k || !d_v) return MSA_ERR_INVALID;
-  if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
+int run_backward(const void* q, const void* k, const void* v, const void* o, const float* lse, const void* d_o,
+                 const int32_t* block_ids, const msa_seqs* seqs, int H_q, int H_kv, int topk, float softmax_scale,
+                 void* d_q, void* d_k, void* d_v, void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  int st;
   BwdPlan pl;
   st = make_bwd_plan(seqs, H_q, H_kv, topk, workspace_bytes, &pl);
   if (st != MSA_OK) return st;
@@ -571,4 +560,45 @@ extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void
                      static_cast<const float*>(dk_acc), static_cast<const float*>(dv_acc), kv_floats / 4,
                      softmax_scale, static_cast<uint16_t*>(d_k), static_cast<uint16_t*>(d_v));
   return msa_host::launch_status();
+}
+
+}  // namespace
+
+extern "C" size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
+                                                         int head_dim, int block_size, int topk) {
+  if (validate_bwd(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
+  const int topk64 = topk * (block_size / kBwdBK);
+  BwdPlan pl;
+  if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk64, kDefaultBwdBytes, &pl) != MSA_OK) {
+    if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk64, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+    pl.chunk_rows = 1;
+    bwd_layout(pl, seqs, num_q_heads, num_kv_heads, topk64);
+  }
+  return expanded_ids_bytes(seqs, num_kv_heads, block_size, topk) + pl.total;
+}
+
+extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const void* o, const float* lse,
+                                        const void* d_o, const int32_t* block_ids, const msa_seqs* seqs,
+                                        int num_q_heads, int num_kv_heads, int head_dim, int block_size, int topk,
+                                        float softmax_scale, void* d_q, void* d_k, void* d_v, void* workspace,
+                                        size_t workspace_bytes, hipStream_t stream) {
+  const int H_q = num_q_heads, H_kv = num_kv_heads;
+  int st = validate_bwd(seqs, H_q, H_kv, head_dim, block_size, topk);
+  if (st != MSA_OK) return st;
+  if (!q || !k || !v || !o || !lse || !d_o || !block_ids || !d_q || !d_k || !d_v) return MSA_ERR_INVALID;
+  if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
+  const size_t xb = expanded_ids_bytes(seqs, H_kv, block_size, topk);
+  if (xb == 0)
+    return run_backward(q, k, v, o, lse, d_o, block_ids, seqs, H_q, H_kv, topk, softmax_scale, d_q, d_k, d_v,
+                        workspace, workspace_bytes, stream);
+  if (!workspace || workspace_bytes < xb) return MSA_ERR_WORKSPACE;
+  const int f = block_size / kBwdBK;
+  auto* ids64 = static_cast<int32_t*>(workspace);
+  const int64_t pairs = seqs->total_q_rows * H_kv;
+  if (pairs > 0)
+    msa_prof::launch("expand_block_ids_kernel", expand_block_ids_kernel,
+                     dim3(static_cast<unsigned>((pairs + 255) / 256)), dim3(256), 0, stream, block_ids, pairs, topk, f,
+                     ids64);
+  return run_backward(q, k, v, o, lse, d_o, ids64, seqs, H_q, H_kv, topk * f, softmax_scale, d_q, d_k, d_v,
+                      static_cast<char*>(workspace) + xb, workspace_bytes - xb, stream);
 }

@@ -589,7 +589,9 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   if (st != MSA_OK) return st;
   if (H_q < 1 || H_kv < 1 || d_idx < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
   if (H_q % H_kv != 0) return MSA_ERR_INVALID;
-  if (head_dim != kHeadDim || BK != kKlBK || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
+  if (head_dim != kHeadDim || (BK != kKlBK && BK != 2 * kKlBK) || (d_idx != 64 && d_idx != 128))
+    return MSA_ERR_UNSUPPORTED;
+  if (BK == 2 * kKlBK && topk > 32) return MSA_ERR_UNSUPPORTED;   // its 64-key halves fill <= 64 slots
   if (topk > 64 || H_q / H_kv > 16 || !msa_host::is_pow2(H_q / H_kv) || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
@@ -663,18 +665,27 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
   return msa_host::launch_status();
 }
 
+// Block size 128: each id is expanded to its two 64-key halves in front of
+// the workspace and the 64-key path runs on 2 topk slots.
+size_t kl_expanded_ids_bytes(const msa_seqs* seqs, int H_kv, int BK, int topk) {
+  if (BK == kKlBK) return 0;
+  return msa_host::align_up(sizeof(int32_t) * static_cast<size_t>(seqs->total_q_rows) * H_kv * topk * (BK / kKlBK),
+                            256);
+}
+
 }  // namespace
 
 extern "C" size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
                                                        int d_idx, int head_dim, int block_size, int topk) {
   if (validate_kl(seqs, num_q_heads, num_kv_heads, d_idx, head_dim, block_size, topk) != MSA_OK) return 0;
+  const int topk64 = topk * (block_size / kKlBK);
   KlPlan pl;
-  if (make_kl_plan(seqs, num_kv_heads, d_idx, topk, kDefaultKlBytes, &pl) != MSA_OK) {
-    if (make_kl_plan(seqs, num_kv_heads, d_idx, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+  if (make_kl_plan(seqs, num_kv_heads, d_idx, topk64, kDefaultKlBytes, &pl) != MSA_OK) {
+    if (make_kl_plan(seqs, num_kv_heads, d_idx, topk64, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
     pl.chunk_rows = 1;
-    kl_layout(pl, seqs, num_kv_heads, d_idx, topk);
+    kl_layout(pl, seqs, num_kv_heads, d_idx, topk64);
   }
-  return pl.total;
+  return kl_expanded_ids_bytes(seqs, num_kv_heads, block_size, topk) + pl.total;
 }
 
 extern "C" int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void* q, const void* k,
@@ -687,14 +698,28 @@ extern "C" int msa_sparse_kl_backward(const void* index_q, const void* index_k, 
   if (st != MSA_OK) return st;
   if (!index_q || !index_k || !q || !k || !lse || !block_ids || !d_index_q || !d_index_k) return MSA_ERR_INVALID;
   if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
+  const size_t xb = kl_expanded_ids_bytes(seqs, num_kv_heads, block_size, topk);
+  if (!workspace || workspace_bytes < xb) return MSA_ERR_WORKSPACE;
+  const int f = block_size / kKlBK;
+  const int32_t* ids = block_ids;
+  if (f > 1) {
+    auto* ids64 = static_cast<int32_t*>(workspace);
+    const int64_t pairs = seqs->total_q_rows * num_kv_heads;
+    if (pairs > 0)
+      msa_prof::launch("expand_block_ids_kernel", expand_block_ids_kernel,
+                       dim3(static_cast<unsigned>((pairs + 255) / 256)), dim3(256), 0, stream, block_ids, pairs, topk,
+                       f, ids64);
+    ids = ids64;
+  }
+  const int topk64 = topk * f;
   KlPlan pl;
-  st = make_kl_plan(seqs, num_kv_heads, d_idx, topk, workspace_bytes, &pl);
+  st = make_kl_plan(seqs, num_kv_heads, d_idx, topk64, workspace_bytes - xb, &pl);
   if (st != MSA_OK) return st;
-  if (!workspace || workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
-  char* ws = static_cast<char*>(workspace);
+  if (workspace_bytes - xb < pl.total) return MSA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace) + xb;
   if (d_idx == 64)
-    return run_kl<64>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk, softmax_scale,
+    return run_kl<64>(index_q, index_k, q, k, lse, ids, seqs, num_q_heads, num_kv_heads, topk64, softmax_scale,
                       grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
-  return run_kl<128>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk, softmax_scale,
+  return run_kl<128>(index_q, index_k, q, k, lse, ids, seqs, num_q_heads, num_kv_heads, topk64, softmax_scale,
                      grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
 }

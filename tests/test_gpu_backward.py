@@ -37,7 +37,7 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-# name, q_rows, kv_lens, H_q, H_kv, topk, kv_pad_to
+# name, q_rows, kv_lens, H_q, H_kv, topk, kv_pad_to[, block_size]
 CASES = [
     ("bwd_T1000_g8", [1000], [1000], 16, 2, 8, None),
     ("bwd_ragged_T333_g4", [333], [333], 8, 2, 5, None),
@@ -47,11 +47,13 @@ CASES = [
     ("bwd_chunked_varlen", [130, 0, 64, 1, 257], [700, 300, 64, 900, 1500], 16, 4, 6, None),
     ("bwd_decode_padded", [1, 1, 1, 1, 1], [3000, 64, 65, 4097, 1], 16, 4, 6, 4160),
     ("bwd_many_items_k32", [2048], [2048], 16, 2, 32, None),
+    ("bwd_bk128_g16", [900], [900], 32, 2, 5, None, 128),
+    ("bwd_bk128_chunked_varlen", [200, 1, 129], [1000, 700, 1500], 16, 2, 4, None, 128),
 ]
 
 
-def _setup(name, q_rows, kv_lens, H_q, H_kv, topk, pad):
-    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, topk=topk,
+def _setup(name, q_rows, kv_lens, H_q, H_kv, topk, pad, bk=64):
+    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, topk=topk, block_size=bk,
                              seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
     x = {k: v for k, v in synth.generate_numpy(p).items() if k in ("q", "k", "v")}
     x["d_o"] = synth.generate_grad_numpy(p)
@@ -126,10 +128,14 @@ def test_backward_chunked_workspace_and_reproducibility():
     assert np.array_equal(one[0], small[0]), "chunked dQ differs from the one-chunk dQ"
 
 
-def test_backward_rejects_block_128():
+def test_backward_block_128_limits():
+    """Block size 128 runs as its 64-key halves: topk <= 32 (the halves fill
+    <= 64 slots); other block sizes are rejected."""
     p = synth.packed_problem("bwd_bk128", [10], [10], num_q_heads=8, num_kv_heads=2, topk=2, seed=1)
     seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
-    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 2) == 0
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 32) > 0
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 33) == 0
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 256, 2) == 0
 
 
 def test_backward_workload_sampled():

@@ -54,6 +54,8 @@ CASES = [
     ("kl_chunked_varlen", [130, 0, 64, 1, 257], [700, 300, 64, 900, 1500], 16, 4, 6, 64, None),
     ("kl_decode_padded", [1, 1, 1, 1, 1], [3000, 64, 65, 4097, 1], 16, 4, 6, 128, 4160),
     ("kl_many_items_k32", [2048], [2048], 16, 2, 32, 64, None),
+    ("kl_bk128_g16_didx128", [900], [900], 32, 2, 5, 128, None, 128),
+    ("kl_bk128_chunked_varlen", [200, 1, 129], [1000, 700, 1500], 16, 2, 4, 64, None, 128),
 ]
 
 
@@ -67,10 +69,11 @@ def check_kl(got, ref, what):
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_kl_small(case):
-    name, q_rows, kv_lens, H_q, H_kv, topk, d_idx, pad = case
+    name, q_rows, kv_lens, H_q, H_kv, topk, d_idx, pad = case[:8]
+    bk = case[8] if len(case) > 8 else 64
     _say(f"[case] {name}")
     p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, topk=topk, d_idx=d_idx,
-                             seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
+                             block_size=bk, seed=zlib.crc32(name.encode()) % 10000, kv_pad_to=pad)
     x = synth.generate_numpy(p)
     ids = synth.random_block_ids(p)
     dev = torch.device("cuda")
@@ -92,11 +95,13 @@ def test_kl_small(case):
 
 def test_kl_rejects_unsupported_shapes():
     """G must be a power of two (the teacher's head mean is a register
-    reduction over aligned rows); block_size 64 only."""
+    reduction over aligned rows); block_size 128 runs as 64-key halves, so
+    topk <= 32 there."""
     p = synth.packed_problem("kl_g3", [10], [10], num_q_heads=6, num_kv_heads=2, topk=2, seed=1)
     seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
     assert msa.sparse_kl_backward_workspace_size(seqs, 6, 2, 64, 128, 64, 2) == 0
-    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 2) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 33) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 32) > 0
     assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 64, 2) > 0
 
 
