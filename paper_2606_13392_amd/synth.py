@@ -171,6 +171,11 @@ def workload(name: str) -> Problem:
                               block_size=128, topk=16, seed=1006, planted=8,
                               description="prefill T=1048576, 64q/4kv, d_idx 128, B_k 128, k=16, "
                                           "8 planted blocks/group (the paper's deployed shape)")
+    if name == "prefill_32k_bk128":
+        return packed_problem(name, [32768], [32768], num_q_heads=64, num_kv_heads=4, d_idx=128,
+                              block_size=128, topk=16, seed=1008, planted=8,
+                              description="prefill T=32768, 64q/4kv, d_idx 128, B_k 128, k=16, "
+                                          "8 planted blocks/group (the deployed shape at a training length)")
     if name == "decode_128k_bk128":
         return packed_problem(name, [1] * 64, [131072] * 64, num_q_heads=64, num_kv_heads=4, d_idx=128,
                               block_size=128, topk=16, seed=1007, kv_pad_to=131072,
@@ -186,7 +191,7 @@ def workload(name: str) -> Problem:
 
 WORKLOADS = ["prefill_4k", "prefill_32k", "decode_128k", "prefill_1m", "chunked_8x8k"]
 # the paper's deployed shape (B_k 128, k 16, GQA 16, d_idx 128)
-WORKLOADS_BK128 = ["prefill_1m_bk128", "decode_128k_bk128"]
+WORKLOADS_BK128 = ["prefill_1m_bk128", "decode_128k_bk128", "prefill_32k_bk128"]
 
 
 # --------------------------------------------------------------------------
