@@ -173,6 +173,10 @@ __device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_
 // row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
 // prunes with.  RW index rows per wave (64 or 128; a unit is 4 RW / 64 row
 // groups): with 128 every K_idx operand read from LDS feeds four MFMAs.
+// Keys are staged and scored 64 at a time whatever B_k is (a 128-key block is
+// two sub-blocks whose maxima are merged), which keeps the LDS buffers and the
+// register prefetch of the d_idx 128 / B_k 128 kernel small enough for two
+// CTAs per CU.
 template <int D_IDX, int BK, int RW, bool PAGED>
 __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
@@ -180,12 +184,12 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
     int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
   static_assert(kBlocksPerCta == kWave, "a CTA slice is one Top-k chunk");
   constexpr int KS = D_IDX / 16;                        // k-steps of the MFMA
-  constexpr int MT = BK / 32;                           // 32-key M tiles per block
   constexpr int SEGS = D_IDX / 8;                       // 16-byte segments per key row
-  constexpr int CH = BK * SEGS / 256;                   // 16-byte loads per thread per block
+  constexpr int SUB = BK / 64;                          // 64-key sub-blocks staged per block
+  constexpr int CH = 64 * SEGS / 256;                   // 16-byte loads per thread per sub-block
   constexpr int NJ = RW / 32;                           // 32-row column tiles per wave
   constexpr int NP = RW / 64;                           // row groups per wave
-  __shared__ IdxSmem<D_IDX, BK, RW> sm;
+  __shared__ IdxSmem<D_IDX, 64, RW> sm;
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int64_t uidx = u0 + blockIdx.x;
@@ -218,21 +222,21 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
     cmax[sp] = -INFINITY;
   }
 
-  const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
+  const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, 64);   // 64-key view of the blocks
   const uint16_t* kseq = index_k + (PAGED ? 0 : ur.g.kv_start) * D_IDX;
   const int tid = threadIdx.x;
-  auto compute = [&](int buf, int kb) {
+  float bm_sub[NP];
+  auto compute = [&](int buf, int sb) {
     if (nvalid == 0) return;
-    // 64 keys (two 32-key tiles) at a time keep 32 NJ accumulators live for any B_k
+    const int kb = sb / SUB;
     float bm[NP];
 #pragma unroll
     for (int sp = 0; sp < NP; ++sp) bm[sp] = -INFINITY;
-#pragma unroll
-    for (int hk = 0; hk < MT / 2; ++hk) {
+    {
       f32x16 acc[2][NJ];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const uint16_t* kr = &sm.k[buf][64 * hk + 32 * i + n][h * (D_IDX / 2)];
+        const uint16_t* kr = &sm.k[buf][32 * i + n][h * (D_IDX / 2)];
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16{};
 #pragma unroll
@@ -244,6 +248,15 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
       }
 #pragma unroll
       for (int sp = 0; sp < NP; ++sp) bm[sp] = fmaxf(bm[sp], block_max_rows<2, NJ>(acc, 2 * sp));
+    }
+    if constexpr (SUB > 1) {
+      if (sb % SUB != SUB - 1) {
+#pragma unroll
+        for (int sp = 0; sp < NP; ++sp) bm_sub[sp] = sb % SUB == 0 ? bm[sp] : fmaxf(bm_sub[sp], bm[sp]);
+        return;
+      }
+#pragma unroll
+      for (int sp = 0; sp < NP; ++sp) bm[sp] = fmaxf(bm[sp], bm_sub[sp]);
     }
 #pragma unroll
     for (int sp = 0; sp < NP; ++sp) {
@@ -272,21 +285,22 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
   // Loads are issued unconditionally (the index is clamped to the last block)
   // so no branch forces the compiler to wait on a prefetch it just issued.
   u32x4 ra[CH], rb[CH];
-  const int klast = kb1 - 1;
-  idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, kb0, tid, ra);
-  idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb0 + 1, klast), tid, rb);
-  idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
+  const int sb0 = kb0 * SUB, sb1 = kb1 * SUB;
+  const int slast = sb1 - 1;
+  idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, sb0, tid, ra);
+  idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb0 + 1, slast), tid, rb);
+  idx_store_block<D_IDX, 64, CH>(sm.k[0], tid, ra);
   __syncthreads();
-  // LDS buffer 0 holds block kb, register set rb holds kb+1
-  for (int kb = kb0; kb < kb1; kb += 2) {
-    idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb + 2, klast), tid, ra);
-    compute(0, kb);
-    if (kb + 1 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[1], tid, rb);
+  // LDS buffer 0 holds sub-block sb, register set rb holds sb+1
+  for (int sb = sb0; sb < sb1; sb += 2) {
+    idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb + 2, slast), tid, ra);
+    compute(0, sb);
+    if (sb + 1 < sb1) idx_store_block<D_IDX, 64, CH>(sm.k[1], tid, rb);
     __syncthreads();
-    if (kb + 1 >= kb1) break;
-    idx_load_block<D_IDX, BK, CH, PAGED>(kseq, kbk, min(kb + 3, klast), tid, rb);
-    compute(1, kb + 1);
-    if (kb + 2 < kb1) idx_store_block<D_IDX, BK, CH>(sm.k[0], tid, ra);
+    if (sb + 1 >= sb1) break;
+    idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb + 3, slast), tid, rb);
+    compute(1, sb + 1);
+    if (sb + 2 < sb1) idx_store_block<D_IDX, 64, CH>(sm.k[0], tid, ra);
     __syncthreads();
   }
   // rows whose local block is at or below kb0 never read this entry

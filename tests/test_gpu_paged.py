@@ -73,6 +73,9 @@ CASES = [
     ("paged_speculative_mixed_bk128", [2, 8, 1, 3], [3000, 1500, 129, 4100], 32, 2, 128, 5, 128, 4224, 2),
     ("paged_chunked_prefill", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None, 1),
     ("paged_chunked_prefill_8blk_pages", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, None, 8),
+    # 128-key blocks scored as two 64-key sub-blocks in the many-row score kernel
+    ("paged_chunked_prefill_bk128", [300, 1, 130], [2300, 800, 1500], 32, 2, 128, 5, 128, None, 2),
+    ("paged_chunked_prefill_bk128_didx64", [300, 1, 130], [2300, 800, 1500], 16, 2, 128, 6, 64, None, 1),
 ]
 
 
