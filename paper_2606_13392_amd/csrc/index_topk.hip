@@ -134,51 +134,36 @@ __device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][NJ], int
 // ---------------------------------------------------------------- scores, LDS
 constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
 
-template <int D_IDX, int BK, int RW>
+// One 16-byte piece per lane from global memory straight into LDS
+// (global_load_lds_dwordx4): lane l writes bytes [16 l, 16 l + 16) after the
+// wave-uniform LDS address dst.  Completion is counted by vmcnt.
+__device__ __forceinline__ void lds_dma16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+
+// A 64-key sub-block of K_idx in LDS, unpadded: key row r keeps its 16-byte
+// segment s in slot s ^ kswz(r), so the A-operand reads of 8 and of 16
+// consecutive lanes (16 consecutive rows, one segment) hit distinct banks.
+template <int D_IDX>
+__device__ __forceinline__ int kswz(int r) {
+  if constexpr (D_IDX == 64) return (r & 7) ^ ((r >> 3) & 1);
+  else return r & 15;
+}
+template <int D_IDX, int RW>
 struct IdxSmem {
-  uint16_t k[2][BK][D_IDX + 8];                   // K_idx blocks, row-major, +16 B pad per row
+  uint4 k[2][64 * D_IDX / 8];                      // two sub-blocks, swizzled rows
   float stage[kWaves][RW][kStageBlocks + 1];       // per wave: RW rows x 16 block maxima
 };
-
-// Cooperative copy of one K_idx block (BK keys x D_IDX dims) through
-// registers: 256 threads x CH 16-byte pieces.
-// kseq: the sequence's first index-key row (contiguous), or the page pool (paged)
-template <int D_IDX, int BK, int CH, bool PAGED>
-__device__ __forceinline__ void idx_load_block(const uint16_t* __restrict__ kseq, const KeyBlocks& kbk, int kb,
-                                               int tid, u32x4 (&dst)[CH]) {
-  constexpr int SEGS = D_IDX / 8;
-#pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    const int idx = tid + 256 * c;
-    const int key = idx / SEGS, seg = idx % SEGS;
-    if constexpr (PAGED)
-      dst[c] = *reinterpret_cast<const u32x4*>(kseq + (kbk.template row_as<true>(kb) + key) * D_IDX + 8 * seg);
-    else
-      dst[c] = *reinterpret_cast<const u32x4*>(kseq + static_cast<int64_t>(kb * BK + key) * D_IDX + 8 * seg);
-  }
-}
-template <int D_IDX, int BK, int CH>
-__device__ __forceinline__ void idx_store_block(uint16_t (*__restrict__ dstk)[D_IDX + 8], int tid,
-                                                const u32x4 (&src)[CH]) {
-  constexpr int SEGS = D_IDX / 8;
-#pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    const int idx = tid + 256 * c;
-    const int key = idx / SEGS, seg = idx % SEGS;
-    *reinterpret_cast<u32x4*>(&dstk[key][8 * seg]) = src[c];
-  }
-}
 
 // Besides M, each CTA writes its 64-block slice's maximum per row (over the
 // row's candidate blocks only) to CM[slice][row], the bound the Top-k kernel
 // prunes with.  RW index rows per wave (64 or 128; a unit is 4 RW / 64 row
 // groups): with 128 every K_idx operand read from LDS feeds four MFMAs.
 // Keys are staged and scored 64 at a time whatever B_k is (a 128-key block is
-// two sub-blocks whose maxima are merged), which keeps the LDS buffers and the
-// register prefetch of the d_idx 128 / B_k 128 kernel small enough for two
-// CTAs per CU.
+// two sub-blocks whose maxima are merged) and go from HBM to LDS without a
+// register copy, which lets the d_idx 128 / B_k 128 kernel run 3 CTAs per CU.
 template <int D_IDX, int BK, int RW, bool PAGED>
-__global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
+__global__ __launch_bounds__(256, (RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
     int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
@@ -189,7 +174,7 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
   constexpr int CH = 64 * SEGS / 256;                   // 16-byte loads per thread per sub-block
   constexpr int NJ = RW / 32;                           // 32-row column tiles per wave
   constexpr int NP = RW / 64;                           // row groups per wave
-  __shared__ IdxSmem<D_IDX, 64, RW> sm;
+  __shared__ IdxSmem<D_IDX, RW> sm;
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int64_t uidx = u0 + blockIdx.x;
@@ -236,12 +221,12 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
       f32x16 acc[2][NJ];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        const uint16_t* kr = &sm.k[buf][32 * i + n][h * (D_IDX / 2)];
+        const int row = 32 * i + n;
 #pragma unroll
         for (int j = 0; j < NJ; ++j) acc[i][j] = f32x16{};
 #pragma unroll
         for (int st = 0; st < KS; ++st) {
-          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 8 * st));
+          const bf16x8 a = __builtin_bit_cast(bf16x8, sm.k[buf][row * SEGS + ((h * (SEGS / 2) + st) ^ kswz<D_IDX>(row))]);
 #pragma unroll
           for (int j = 0; j < NJ; ++j) acc[i][j] = mfma32x32x16(a, bq[j][st], acc[i][j]);
         }
@@ -282,25 +267,36 @@ __global__ __launch_bounds__(256, (D_IDX == 64 && RW == 64) ? 3 : 2) void index_
     }
   };
 
-  // Loads are issued unconditionally (the index is clamped to the last block)
-  // so no branch forces the compiler to wait on a prefetch it just issued.
-  u32x4 ra[CH], rb[CH];
+  // Sub-blocks go from HBM straight into LDS (one 1 KiB piece per wave and
+  // load); sub-block sb + 1 is in flight while sb is scored.
   const int sb0 = kb0 * SUB, sb1 = kb1 * SUB;
-  const int slast = sb1 - 1;
-  idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, sb0, tid, ra);
-  idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb0 + 1, slast), tid, rb);
-  idx_store_block<D_IDX, 64, CH>(sm.k[0], tid, ra);
+  auto dma = [&](int buf, int sb) {
+#pragma unroll
+    for (int c = 0; c < CH; ++c) {
+      const int piece = w * CH + c;
+      const int q = piece * kWave + lane;
+      const int r = q / SEGS, slot = q % SEGS;
+      const int seg = slot ^ kswz<D_IDX>(r);
+      const uint16_t* src;
+      if constexpr (PAGED) src = kseq + (kbk.template row_as<true>(sb) + r) * D_IDX + 8 * seg;
+      else src = kseq + static_cast<int64_t>(sb * 64 + r) * D_IDX + 8 * seg;
+      lds_dma16(src, &sm.k[buf][piece * kWave]);
+    }
+  };
+  // s_waitcnt 0 before each barrier: this wave's pieces of the next
+  // sub-block have landed in LDS
+  dma(0, sb0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  // LDS buffer 0 holds sub-block sb, register set rb holds sb+1
   for (int sb = sb0; sb < sb1; sb += 2) {
-    idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb + 2, slast), tid, ra);
+    if (sb + 1 < sb1) dma(1, sb + 1);
     compute(0, sb);
-    if (sb + 1 < sb1) idx_store_block<D_IDX, 64, CH>(sm.k[1], tid, rb);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if (sb + 1 >= sb1) break;
-    idx_load_block<D_IDX, 64, CH, PAGED>(kseq, kbk, min(sb + 3, slast), tid, rb);
+    if (sb + 2 < sb1) dma(0, sb + 2);
     compute(1, sb + 1);
-    if (sb + 2 < sb1) idx_store_block<D_IDX, 64, CH>(sm.k[0], tid, ra);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
   // rows whose local block is at or below kb0 never read this entry
