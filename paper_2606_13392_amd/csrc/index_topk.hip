@@ -497,15 +497,62 @@ __device__ __forceinline__ uint64_t insert_keys(uint64_t v, uint64_t thr, int K1
   return readlane_u64(list, K1 - 1);
 }
 
+// Keys that beat the running threshold are appended to a per-wave LDS
+// buffer (128 entries) and merged into the sorted list 64 at a time: one
+// bitonic sort + merge per 64 candidates instead of one insertion each.  The
+// threshold only rises at a merge, so some extra keys are buffered; the list
+// after flush() is still exactly the best K1 (and more) of all pushed keys.
+struct KeyBatch {
+  uint64_t* pend;    // this wave's 128-entry LDS buffer
+  int cnt;           // buffered keys (wave-uniform, < 64 between calls)
+  int K1;
+  uint64_t list;     // sorted descending across the lanes; 0 marks an empty slot
+
+  __device__ __forceinline__ void merge(uint64_t v) {
+    const uint64_t vs = wave_sort_desc_u64(v);
+    const uint64_t rev = shfl_u64(vs, kWave - 1 - lane_id());
+    list = wave_bitonic_merge_desc_u64(list > rev ? list : rev);
+  }
+  // pushes the lanes' keys above thr; returns the new threshold (>= thr)
+  __device__ __forceinline__ uint64_t push(uint64_t v, uint64_t thr) {
+    const int lane = lane_id();
+    const bool take = v > thr;
+    const uint64_t pass = __ballot(take);
+    if (pass == 0) return thr;
+    const int pos = cnt + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(pass >> 32),
+                                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(pass), 0));
+    if (take) pend[pos] = v;
+    cnt += __popcll(pass);
+    if (cnt < kWave) return thr;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint64_t x = pend[lane];
+    const uint64_t y = pend[kWave + lane];
+    merge(x);
+    cnt -= kWave;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane < cnt) pend[lane] = y;
+    const uint64_t t = readlane_u64(list, K1 - 1);
+    return t > thr ? t : thr;
+  }
+  __device__ __forceinline__ void flush() {
+    if (cnt == 0) return;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int lane = lane_id();
+    merge(lane < cnt ? pend[lane] : 0ull);
+    cnt = 0;
+  }
+};
+
 // Streams chunks c_begin, c_begin + c_step, ... (64 scores each) of one row,
-// score b read as load(b); returns the row's best keys of those chunks,
-// sorted descending across the lanes (at least the best K1 are exact).
-template <typename Load>
-__device__ __forceinline__ uint64_t scan_row_chunks(Load load, int nscan, int K1, int c_begin, int c_step) {
+// score b read as load(b), and hands each chunk's keys to ins(v, tau) (which
+// returns the new threshold).
+template <typename Load, typename Ins>
+__device__ __forceinline__ void stream_chunks(Load load, int nscan, int c_begin, int c_step, Ins ins) {
   const int lane = lane_id();
-  uint64_t list = 0;   // sorted descending across lanes; 0 marks an empty slot
   uint64_t tau = 0;    // key of the K1-th best so far (0 while fewer are known)
-  if (K1 <= 0) return list;
   // block scores of the next kAhead chunks are in flight while one is ranked
   constexpr int kAhead = 4;
   float pf[kAhead];
@@ -524,9 +571,30 @@ __device__ __forceinline__ uint64_t scan_row_chunks(Load load, int nscan, int K1
       pf[kAhead - 1] = bn < nscan ? load(bn) : 0.f;
     }
     const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
-    tau = insert_keys(v, tau, K1, list);
+    tau = ins(v, tau);
   }
+}
+
+// The row's best keys of chunks c_begin, c_begin + c_step, ..., sorted
+// descending across the lanes (at least the best K1 are exact); keys are
+// inserted one chunk at a time.
+template <typename Load>
+__device__ __forceinline__ uint64_t scan_row_chunks(Load load, int nscan, int K1, int c_begin, int c_step) {
+  uint64_t list = 0;
+  if (K1 <= 0) return list;
+  stream_chunks(load, nscan, c_begin, c_step, [&](uint64_t v, uint64_t t) { return insert_keys(v, t, K1, list); });
   return list;
+}
+
+// The same selection through a KeyBatch.
+template <typename Load>
+__device__ __forceinline__ uint64_t scan_row_batched(Load load, int nscan, KeyBatch& kb) {
+  kb.list = 0;
+  kb.cnt = 0;
+  if (kb.K1 <= 0) return 0;
+  stream_chunks(load, nscan, 0, 1, [&](uint64_t v, uint64_t t) { return kb.push(v, t); });
+  kb.flush();
+  return kb.list;
 }
 
 // The same selection with chunk maxima: chunk c of the row (scores
@@ -535,11 +603,12 @@ __device__ __forceinline__ uint64_t scan_row_chunks(Load load, int nscan, int K1
 // score >= t0), so chunks with maximum below t0 are skipped and scores below
 // t0 are never ranked.
 template <typename Load, typename LoadCm>
-__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int nscan, int K1) {
+__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int nscan, KeyBatch& kb) {
   const int lane = lane_id();
+  const int K1 = kb.K1;
   const int nchunk = (nscan + kWave - 1) / kWave;
-  if (K1 <= 0 || nchunk <= K1) return scan_row_chunks(load, nscan, K1, 0, 1);
-  const uint64_t t0key = readlane_u64(scan_row_chunks(cm, nchunk, K1, 0, 1), K1 - 1);
+  if (K1 <= 0 || nchunk <= K1) return scan_row_batched(load, nscan, kb);
+  const uint64_t t0key = readlane_u64(scan_row_batched(cm, nchunk, kb), K1 - 1);
   const uint32_t o0 = static_cast<uint32_t>(t0key >> 32);     // ordered score of t0
   // keys above floor_key have scores >= t0 (o0 > 0 for every non-NaN score)
   const uint64_t floor_key = o0 > 0 ? (static_cast<uint64_t>(o0) << 32) - 1 : 0ull;
@@ -560,7 +629,8 @@ __device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int ns
     mask &= mask - 1;
     return kWave * (g - 1) + j;
   };
-  uint64_t list = 0;
+  kb.list = 0;
+  kb.cnt = 0;
   uint64_t tau = floor_key;
   constexpr int kAhead = 4;
   int cs[kAhead];
@@ -585,10 +655,10 @@ __device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int ns
       pf[kAhead - 1] = (cs[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
     }
     const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
-    tau = insert_keys(v, tau, K1, list);
-    if (tau < floor_key) tau = floor_key;
+    tau = kb.push(v, tau);
   }
-  return list;
+  kb.flush();
+  return kb.list;
 }
 
 // Local block + the K1 best keys of `list`, ids ascending, -1 padded.
@@ -647,6 +717,7 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
     const float* __restrict__ M, int64_t ldm, const float* __restrict__ CM, int64_t cm_stride, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int U, int rpu, int64_t u0, int64_t u1, int BK,
     int topk, int32_t* __restrict__ block_ids) {
+  __shared__ uint64_t s_pend[kWaves][2 * kWave];
   const int lane = lane_id();
   const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
   if (task >= (u1 - u0) * rpu) return;
@@ -658,13 +729,16 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   }
   const float* mrow = t.mrow;
   auto load = [=](int b) { return mrow[b]; };
+  KeyBatch kb;
+  kb.pend = s_pend[threadIdx.x / kWave];
+  kb.K1 = topk - 1;
   uint64_t list;
   if (CM) {
     const float* cmrow = CM + t.slot;
     auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
-    list = scan_row_pruned(load, cm, t.nscan, topk - 1);
+    list = scan_row_pruned(load, cm, t.nscan, kb);
   } else {
-    list = scan_row_chunks(load, t.nscan, topk - 1, 0, 1);
+    list = scan_row_batched(load, t.nscan, kb);
   }
   finish_row(list, topk - 1, t.lb, topk, t.out);
 }
