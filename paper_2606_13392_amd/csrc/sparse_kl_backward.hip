@@ -23,6 +23,9 @@
 //                    the teacher's head mean in registers; d k_idx of the
 //                    block in registers (an fp32 partial per item), d q_idx
 //                    and the KL term of every incidence as fp32 partials
+//                    (d_idx 64: kl_grad_wave, one wave per 32-row pass
+//                    against all 64 keys, no barrier between passes; d_idx
+//                    128: the four waves split the keys of each pass)
 //   kl_tile_reduce   per key block: the items of every group's tile, in
 //                    order, added to the fp32 d k_idx accumulator
 //   kl_combine       per (row, group): d q_idx and KL over the valid slots, in
@@ -446,6 +449,284 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
   }
 }
 
+// ---------------------------------------------------------------- gradients, one wave per pass
+// d_idx 64: a wave takes whole passes (32 rows against all 64 keys of the
+// block), so passes need no CTA barrier and each wave is its own stream of
+// gathers; the block's K, index keys and their transpose are shared by the
+// CTA per item.  d k_idx of all 64 keys stays in the wave's registers (64
+// VGPRs); at item end the four waves' partials are added in wave order.
+template <int D>
+struct KlwWave {
+  uint16_t qit[D][kKlRows + 8];                       // index query of each pass row, transposed
+  uint16_t dlc[kKlRows][kKlBK + 8];                   // Delta of each pass query (its head-0 row), [query][key]
+  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row (+inf: no row)
+  float lsei2[kKlRows];                               // LSE_idx * log2(e) per row
+  int32_t rpos[kKlRows];                              // position per row (-1: no row)
+  int64_t incq[kKlRows];                              // incidence of pass query j (the trash one past the item)
+};
+template <int D>
+struct KlwSmem {
+  union {
+    struct {
+      uint16_t k[kKlBK][kHeadDim + 8];                // K block (Main Branch head r), row-major
+      uint16_t ki[kKlBK][D + 8];                      // index-key block, row-major
+      uint16_t kit[D][kKlBK + 8];                     // index-key block transposed
+      KlwWave<D> wv[kKlThreads / kWave];
+    } m;
+    float red[kKlThreads / kWave][kKlBK * D];         // item end: each wave's d k_idx partial
+  } u;
+  int32_t s_row[kItemQueries];
+  int32_t s_slot[kItemQueries];
+};
+// two CTAs per CU
+static_assert(sizeof(KlwSmem<64>) <= 80 * 1024, "LDS of a one-wave-per-pass KL CTA");
+
+template <int D, int LG>
+__global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
+    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
+    const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
+    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
+    const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
+    float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
+    float* __restrict__ part) {
+  static_assert(D == 64, "d k_idx of 64 keys x 128 dims does not fit a wave's registers");
+  __shared__ KlwSmem<D> sm;
+  constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
+  constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
+  constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
+  constexpr int NW = kKlThreads / kWave;
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int c16 = lane & 15, qd = lane >> 4;
+  constexpr int G = 1 << LG;                          // H_q / H_kv
+  constexpr int lg = LG;
+  constexpr int qpw = 32 >> LG;                       // queries per pass
+  const float sidx_log2 = sidx * kLog2e;
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  KlwWave<D>& wv = sm.u.m.wv[w];
+
+  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int64_t gb = tile % nbcap;
+    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
+    const SeqGeom g = seq_geom(sq, s);
+    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+    const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
+
+    __syncthreads();                                  // the previous item is done with LDS
+    if (static_cast<int>(threadIdx.x) < nq) {
+      const uint32_t hd = handles[h0 + threadIdx.x];
+      sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
+      sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
+    }
+    {                                                 // staged every item: the item-end sum reuses this LDS
+      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      for (int c = threadIdx.x; c < kKlBK * (kHeadDim / 8); c += kKlThreads) {
+        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        *reinterpret_cast<u32x4*>(&sm.u.m.k[key][8 * dg]) =
+            key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
+      }
+      stage_index_keys<D>(sm.u.m, index_k + (g.kv_start + key0) * static_cast<int64_t>(D), g.kv_len - key0);
+    }
+    __syncthreads();
+
+    f32x4 acc_dk[4][NT];                              // [key tile][dim tile]: lane column = dim, rows = keys 4qd + i
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int n = 0; n < NT; ++n) acc_dk[kt][n] = f32x4{};
+
+    // A operands of a pass (rows 16t + c16), as in kl_grad_kernel
+    u32x4 bq[2][KSM], bi[2][KSI];
+    float lse_v[2], lsei_v[2];
+    bool arow[2];
+    int32_t qrow[2];
+    auto load_pass = [&](int cc) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int qa = cc + ((16 * t + c16) >> lg);
+        arow[t] = qa < nq;
+        qrow[t] = min(qa, nq - 1);
+        const int64_t rl = sm.s_row[qrow[t]];
+        const int64_t grow = row0 + rl;
+        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + ((16 * t + c16) & (G - 1));
+#pragma unroll
+        for (int st = 0; st < KSM; ++st) bq[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
+#pragma unroll
+        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (grow * H_kv + r) * D + 32 * st + 8 * qd);
+        lse_v[t] = lse[hrow];
+        lsei_v[t] = lse_idx[rl * H_kv + r];
+      }
+    };
+    const int npass = (nq + qpw - 1) / qpw;
+    int ps = w;
+    if (ps < npass) load_pass(ps * qpw);
+    for (; ps < npass; ps += NW) {
+      const int cq = ps * qpw;                        // the pass's first query in the item
+      // row scalars and the transposed index queries of the pass (wave-private)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int col = 16 * t + c16;
+#pragma unroll
+        for (int st = 0; st < KSI; ++st)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) wv.qit[32 * st + 8 * qd + j][col] = raw_elem16(bi[t][st], j);
+        if (qd == 0) {
+          const int32_t rl = sm.s_row[qrow[t]];
+          wv.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
+          wv.lsei2[col] = arow[t] ? lsei_v[t] * kLog2e : INFINITY;
+          wv.rpos[col] = arow[t] ? pos_base + rl : -1;
+          if ((col & (G - 1)) == 0)
+            wv.incq[col >> lg] = arow[t] ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[qrow[t]]
+                                         : trash_inc;
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+      // two halves of 32 keys keep the score registers small; key tile kt,
+      // row tile t: the lane holds key 16kt + c16 and rows 16t + 4qd + i
+      float klrow[2][4];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) klrow[t][i] = 0.f;
+#pragma unroll
+      for (int hk = 0; hk < 2; ++hk) {
+        // S and S_idx
+        f32x4 acc_s[2][2], acc_i[2][2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+          for (int t = 0; t < 2; ++t) {
+            const int kt = 2 * hk + u;
+            acc_s[u][t] = f32x4{};
+            acc_i[u][t] = f32x4{};
+#pragma unroll
+            for (int st = 0; st < KSM; ++st)
+              acc_s[u][t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
+                                         ld_bf16x8(&sm.u.m.k[16 * kt + c16][32 * st + 8 * qd]), acc_s[u][t]);
+#pragma unroll
+            for (int st = 0; st < KSI; ++st)
+              acc_i[u][t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bi[t][st]),
+                                         ld_bf16x8(&sm.u.m.ki[16 * kt + c16][32 * st + 8 * qd]), acc_i[u][t]);
+            __builtin_amdgcn_sched_barrier(0);      // bound how far LDS operand reads are hoisted
+          }
+        __builtin_amdgcn_sched_barrier(0);
+        if (hk == 1 && ps + NW < npass) load_pass((ps + NW) * qpw);
+
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int kt = 2 * hk + u;
+          const int key = key0 + 16 * kt + c16;
+          // teacher: per-head P, then the mean over the query's heads (in place)
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 16 * t + 4 * qd + i;
+              acc_s[u][t][i] = key <= wv.rpos[row] ? exp2f(acc_s[u][t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
+            }
+          head_mean(acc_s[u], lg);
+          // student, Delta = P_idx - P on head-0 rows (in place of S_idx), KL terms
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 16 * t + 4 * qd + i;
+              const bool on = key <= wv.rpos[row];
+              const bool head0 = (row & (G - 1)) == 0;
+              const float lz = acc_i[u][t][i] * sidx_log2 - wv.lsei2[row];   // log2 P_idx
+              const float pidx = on ? exp2f(lz) : 0.f;
+              const float pbar = acc_s[u][t][i];
+              klrow[t][i] += (head0 && on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
+              acc_i[u][t][i] = head0 ? pidx - pbar : 0.f;
+            }
+          // d k_idx += Delta^T q_idx over the pass's rows (one k-step): k
+          // index 8qd + 4t + i = row 16t + 4qd + i
+          uint4 dw;
+          dw.x = pack_bf16x2(acc_i[u][0][0], acc_i[u][0][1]);
+          dw.y = pack_bf16x2(acc_i[u][0][2], acc_i[u][0][3]);
+          dw.z = pack_bf16x2(acc_i[u][1][0], acc_i[u][1][1]);
+          dw.w = pack_bf16x2(acc_i[u][1][2], acc_i[u][1][3]);
+          const bf16x8 da = __builtin_bit_cast(bf16x8, dw);
+#pragma unroll
+          for (int n = 0; n < NT; ++n) {
+            const uint16_t* qr = &wv.qit[16 * n + c16][4 * qd];
+            const uint2 lo = *reinterpret_cast<const uint2*>(qr), hi = *reinterpret_cast<const uint2*>(qr + 16);
+            acc_dk[kt][n] = mfma16x16x32(da, __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y)),
+                                         acc_dk[kt][n]);
+            if (n & 1) __builtin_amdgcn_sched_barrier(0);
+          }
+          // the pass queries' Delta rows for d q_idx
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 16 * t + 4 * qd + i;
+              const uint32_t pr = t == 0 ? (i < 2 ? dw.x : dw.y) : (i < 2 ? dw.z : dw.w);
+              if ((row & (G - 1)) == 0) wv.dlc[row >> lg][16 * kt + c16] = static_cast<uint16_t>(pr >> (16 * (i & 1)));
+            }
+        }
+      }
+      // KL per head-0 row: sum over the 64 keys (registers, then the 16 lanes)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v = klrow[t][i];
+#pragma unroll
+          for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
+          const int row = 16 * t + 4 * qd + i;
+          if (c16 == 0 && (row & (G - 1)) == 0) klp[wv.incq[row >> lg]] = v;
+        }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+      // d q_idx of the pass queries (rows j = 16tq + 4qd + i of Delta), dims
+      // 16n + c16, over the 64 keys
+#pragma unroll
+      for (int tq = 0; tq < 2; ++tq) {
+        if (16 * tq >= qpw) break;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          f32x4 acc = f32x4{};
+#pragma unroll
+          for (int ks = 0; ks < kKlBK / 32; ++ks)
+            acc = mfma16x16x32(ld_bf16x8(&wv.dlc[16 * tq + c16][32 * ks + 8 * qd]),
+                               ld_bf16x8(&sm.u.m.kit[16 * n + c16][32 * ks + 8 * qd]), acc);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int j = 16 * tq + 4 * qd + i;
+            if (j < qpw) dqp[wv.incq[j] * D + 16 * n + c16] = acc[i];
+          }
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+
+    // item end: the four waves' d k_idx, added in wave order, as the item's
+    // partial in kl_grad_kernel's layout [key quarter][reg][lane]
+    __syncthreads();                                  // every pass is done: K and pass LDS are free
+#pragma unroll
+    for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sm.u.red[w][kt * (NT * 4 * 64) + (4 * n + i) * 64 + lane] = acc_dk[kt][n][i];
+    __syncthreads();
+    float* dst = part + static_cast<int64_t>(item) * (kKlBK * D);
+    for (int idx = threadIdx.x; idx < kKlBK * D; idx += kKlThreads)
+      dst[idx] = (sm.u.red[0][idx] + sm.u.red[1][idx]) + (sm.u.red[2][idx] + sm.u.red[3][idx]);
+  }
+}
+
 // One CTA per key block: the items of the block's tiles of every group, in
 // group and item order, added to the fp32 accumulator of the block's keys.
 template <int D>
@@ -598,6 +879,18 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   return MSA_OK;
 }
 
+// kl_grad_wave_kernel instance for G = 2^lg (lg <= 4, checked by validate_kl).
+template <typename... Args>
+void launch_kl_grad_wave(int lg, dim3 grid, hipStream_t stream, Args... args) {
+  switch (lg) {
+    case 0: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 0>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 1: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 1>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 2: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 2>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 3: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 3>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    default: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 4>, grid, dim3(kKlThreads), 0, stream, args...); break;
+  }
+}
+
 template <int D>
 int run_kl(const void* index_q, const void* index_k, const void* q, const void* k, const float* lse,
            const int32_t* block_ids, const msa_seqs* seqs, int H_q, int H_kv, int topk, float softmax_scale,
@@ -629,7 +922,9 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                    reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
   static int ctas_lse = 0, ctas_grad = 0;
   const int n_lse = persistent_ctas(kl_lse_kernel<D>, kKlThreads, &ctas_lse);
-  const int n_grad = persistent_ctas(kl_grad_kernel<D>, kKlThreads, &ctas_grad);
+  const int n_grad = D == 64 ? persistent_ctas(kl_grad_wave_kernel<64, 3>, kKlThreads, &ctas_grad)
+                            : persistent_ctas(kl_grad_kernel<D>, kKlThreads, &ctas_grad);
+  const int lg_g = __builtin_ctz(static_cast<unsigned>(H_q / H_kv));
   const int64_t trash_inc = pl.chunk_rows * H_kv * static_cast<int64_t>(topk);
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
@@ -643,12 +938,19 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
     msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
                      dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
                      static_cast<const float*>(lsep), lsei);
-    msa_prof::launch("kl_grad_kernel", kl_grad_kernel<D>, dim3(n_grad), dim3(kKlThreads), 0, stream, iq, ik,
-                     static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
-                     static_cast<const float*>(lsei), sq, static_cast<const int64_t*>(blk_base),
-                     static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
-                     static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
-                     sidx, trash_inc, dqp, klp, part);
+    if constexpr (D == 64)
+      launch_kl_grad_wave(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
+                          static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
+                          static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
+                          static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
+                          topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part);
+    else
+      msa_prof::launch("kl_grad_kernel", kl_grad_kernel<D>, dim3(n_grad), dim3(kKlThreads), 0, stream, iq, ik,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
+                       static_cast<const float*>(lsei), sq, static_cast<const int64_t*>(blk_base),
+                       static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
+                       static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
+                       sidx, trash_inc, dqp, klp, part);
     msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>, dim3(static_cast<unsigned>(pl.nbcap)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc);
