@@ -323,13 +323,16 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
   }
 }
 
-// One CTA per tile: sum of the tile's item partials (in item order) added to
-// the fp32 accumulators of the block's keys.
+// Per tile: the sum of its item partials, in item order, added to the fp32
+// accumulators of the block's keys.  kReduceSplit CTAs per tile, one float4
+// of the partial per thread, so every tile streams its partials with
+// independent loads.
+constexpr int kReduceSplit = kPartFloats / (4 * 256);
 __global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
                                                               const int32_t* __restrict__ item_off, int H_kv,
                                                               int64_t nbcap, const float* __restrict__ part,
                                                               float* __restrict__ dk_acc, float* __restrict__ dv_acc) {
-  const int64_t tile = blockIdx.x;
+  const int64_t tile = blockIdx.x / kReduceSplit;
   const int32_t i0 = item_off[tile], i1 = item_off[tile + 1];
   if (i0 == i1) return;
   const int r = static_cast<int>(tile / nbcap);
@@ -337,20 +340,34 @@ __global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const
   const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
   const SeqGeom g = seq_geom(sq, s);
   const int key0 = static_cast<int>(gb - blk_base[s]) * kBwdBK;
-  for (int idx = threadIdx.x; idx < kPartFloats; idx += 256) {
-    float acc = 0.f;
-    for (int32_t it = i0; it < i1; ++it) acc += part[static_cast<int64_t>(it) * kPartFloats + idx];
-    const int tensor = idx / (4 * 32 * 64);
-    const int kq = (idx / (32 * 64)) & 3;
-    const int reg = (idx / 64) & 31;
-    const int ln = idx & 63;
-    const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
-    const int dim = 16 * (reg >> 2) + (ln & 15);
-    if (key0 + key >= g.kv_len) continue;
-    float* dst = (tensor == 0 ? dv_acc : dk_acc) +
-                 ((g.kv_start + key0 + key) * H_kv + r) * static_cast<int64_t>(kHeadDim) + dim;
-    *dst += acc;
+  const int c4 = (blockIdx.x % kReduceSplit) * 256 + threadIdx.x;   // float4 of the partial
+  const float4* p4 = reinterpret_cast<const float4*>(part) + c4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 4
+  for (int32_t it = i0; it < i1; ++it) {
+    const float4 x = p4[static_cast<int64_t>(it) * (kPartFloats / 4)];
+    acc.x += x.x;
+    acc.y += x.y;
+    acc.z += x.z;
+    acc.w += x.w;
   }
+  // partial layout [tensor][kq][reg][lane]: 4 consecutive lanes = 4 consecutive dims
+  const int idx = 4 * c4;
+  const int tensor = idx / (4 * 32 * 64);
+  const int kq = (idx / (32 * 64)) & 3;
+  const int reg = (idx / 64) & 31;
+  const int ln = idx & 63;
+  const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
+  const int dim = 16 * (reg >> 2) + (ln & 15);
+  if (key0 + key >= g.kv_len) return;
+  float4* dst = reinterpret_cast<float4*>((tensor == 0 ? dv_acc : dk_acc) +
+                                          ((g.kv_start + key0 + key) * H_kv + r) * static_cast<int64_t>(kHeadDim) + dim);
+  float4 y = *dst;
+  y.x += acc.x;
+  y.y += acc.y;
+  y.z += acc.z;
+  y.w += acc.w;
+  *dst = y;
 }
 
 // One wave per (row, group) of the chunk: dQ = scale x sum of the valid slots'
@@ -546,7 +563,7 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
                      static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
                      static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf,
                      static_cast<int64_t>(pl.chunk_rows) * H_kv * topk * (H_q / H_kv) * kHeadDim, part);
-    msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile)),
+    msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile * kReduceSplit)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc,
                      dv_acc);

@@ -727,36 +727,54 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
   }
 }
 
-// One CTA per key block: the items of the block's tiles of every group, in
-// group and item order, added to the fp32 accumulator of the block's keys.
+// Per key block: the items of the block's tiles of every group, in group and
+// item order, added to the fp32 accumulator of the block's keys.
+// kKlReduceSplit CTAs per block, one float4 of the partial per thread.
+template <int D>
+constexpr int kKlReduceSplit = kKlBK * D / (4 * 256);
 template <int D>
 __global__ __launch_bounds__(256) void kl_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
                                                              const int32_t* __restrict__ item_off, int H_kv,
                                                              int64_t nbcap, const float* __restrict__ part,
                                                              float* __restrict__ dk_acc) {
   constexpr int NT = D / 16;
-  const int64_t gb = blockIdx.x;
+  constexpr int SPLIT = kKlReduceSplit<D>;
+  const int64_t gb = blockIdx.x / SPLIT;
   const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
   const SeqGeom g = seq_geom(sq, s);
   const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
   bool any = false;
   for (int r = 0; r < H_kv; ++r) any |= item_off[r * nbcap + gb] != item_off[r * nbcap + gb + 1];
   if (!any) return;
-  for (int idx = threadIdx.x; idx < kKlBK * D; idx += 256) {
-    float acc = 0.f;
-    for (int r = 0; r < H_kv; ++r) {
-      const int64_t tile = r * nbcap + gb;
-      for (int32_t it = item_off[tile]; it < item_off[tile + 1]; ++it)
-        acc += part[static_cast<int64_t>(it) * (kKlBK * D) + idx];
+  const int c4 = (blockIdx.x % SPLIT) * 256 + threadIdx.x;   // float4 of the partial
+  const float4* p4 = reinterpret_cast<const float4*>(part) + c4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int r = 0; r < H_kv; ++r) {
+    const int64_t tile = r * nbcap + gb;
+#pragma unroll 4
+    for (int32_t it = item_off[tile]; it < item_off[tile + 1]; ++it) {
+      const float4 x = p4[static_cast<int64_t>(it) * (kKlBK * D / 4)];
+      acc.x += x.x;
+      acc.y += x.y;
+      acc.z += x.z;
+      acc.w += x.w;
     }
-    const int kq = idx / (NT * 4 * 64);
-    const int reg = (idx / 64) % (NT * 4);
-    const int ln = idx & 63;
-    const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
-    const int dim = 16 * (reg >> 2) + (ln & 15);
-    if (key0 + key >= g.kv_len) continue;
-    dk_acc[(g.kv_start + key0 + key) * static_cast<int64_t>(D) + dim] += acc;
   }
+  // partial layout [kq][reg][lane]: 4 consecutive lanes = 4 consecutive dims
+  const int idx = 4 * c4;
+  const int kq = idx / (NT * 4 * 64);
+  const int reg = (idx / 64) % (NT * 4);
+  const int ln = idx & 63;
+  const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
+  const int dim = 16 * (reg >> 2) + (ln & 15);
+  if (key0 + key >= g.kv_len) return;
+  float4* dst = reinterpret_cast<float4*>(dk_acc + (g.kv_start + key0 + key) * static_cast<int64_t>(D) + dim);
+  float4 y = *dst;
+  y.x += acc.x;
+  y.y += acc.y;
+  y.z += acc.z;
+  y.w += acc.w;
+  *dst = y;
 }
 
 // One wave per (row, group) of the chunk: d q_idx = grad_scale x sum of the
@@ -951,7 +969,8 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                        static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
                        static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
                        sidx, trash_inc, dqp, klp, part);
-    msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>, dim3(static_cast<unsigned>(pl.nbcap)),
+    msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>,
+                     dim3(static_cast<unsigned>(pl.nbcap * kKlReduceSplit<D>)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc);
     msa_prof::launch("kl_combine_kernel", kl_combine_kernel<D>,
