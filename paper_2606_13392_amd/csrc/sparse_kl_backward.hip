@@ -795,17 +795,27 @@ __global__ __launch_bounds__(64 * kKlCombWaves) void kl_combine_kernel(
   const int p = row_position(sq, row, &s);
   const int32_t* ids = block_ids + (row * H_kv + r) * topk;
   constexpr int PER = D / 64;                         // dims per lane
+  // slot validity, one slot per lane; every slot has a partial row, so the
+  // loads below are unconditional and in flight together (unwritten partials
+  // of invalid slots are dropped by a select, never multiplied)
+  const bool mine = lane < topk && incidence_ok(ids[lane], p, kKlBK, blk_base, s);
+  const uint64_t valid = __ballot(mine);
+  const float* src = dqp + pr * topk * static_cast<int64_t>(D) + PER * lane;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  float klsum = 0.f;
+#pragma unroll 8
   for (int j = 0; j < topk; ++j) {
-    if (!incidence_ok(ids[j], p, kKlBK, blk_base, s)) continue;
-    const int64_t inc = pr * topk + j;
+    const bool ok = (valid >> j) & 1ull;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += dqp[inc * D + PER * lane + e];
-    klsum += klp[inc];
+    for (int e = 0; e < PER; ++e) {
+      const float x = src[static_cast<int64_t>(j) * D + e];
+      acc[e] += ok ? x : 0.f;
+    }
   }
+  float klsum = mine ? klp[pr * topk + lane] : 0.f;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) klsum += __shfl_xor(klsum, off);
   uint16_t* dst = d_index_q + (row * H_kv + r) * static_cast<int64_t>(D) + PER * lane;
   if constexpr (PER == 1) {
     dst[0] = f32_to_bf16_bits(acc[0] * grad_scale);
