@@ -391,15 +391,33 @@ __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
   const int E = G * kHeadDim;                         // elements of one slot
   const uint16_t* src = dq_buf + pr * topk * static_cast<int64_t>(E);
   uint16_t* dst = dq + (row * H_q + static_cast<int64_t>(r) * G) * kHeadDim;
+  // slot validity, one slot per lane; the valid slots' partials are then
+  // read 8 at a time (in slot order) so their loads are in flight together
+  const bool mine = lane < topk && incidence_ok(ids[lane], p, kBwdBK, blk_base, s);
+  const uint64_t valid = __ballot(mine);
   for (int c8 = lane; c8 < E / 8; c8 += kWave) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < topk; ++j) {
-      if (!incidence_ok(ids[j], p, kBwdBK, blk_base, s)) continue;
-      const u32x4 w = load_raw(src + static_cast<int64_t>(j) * E + 8 * c8);
+    uint64_t vm = valid;
+    while (vm != 0ull) {
+      constexpr int kBatch = 8;
+      int js[kBatch];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        acc[2 * e] += __uint_as_float(w[e] << 16);
-        acc[2 * e + 1] += __uint_as_float(w[e] & 0xFFFF0000u);
+      for (int u = 0; u < kBatch; ++u) {
+        js[u] = vm != 0ull ? __ffsll(static_cast<unsigned long long>(vm)) - 1 : -1;
+        vm &= vm - 1;
+      }
+      u32x4 w[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u)
+        w[u] = load_raw(src + static_cast<int64_t>(js[u] >= 0 ? js[u] : js[0]) * E + 8 * c8);
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        if (js[u] < 0) break;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          acc[2 * e] += __uint_as_float(w[u][e] << 16);
+          acc[2 * e + 1] += __uint_as_float(w[u][e] & 0xFFFF0000u);
+        }
       }
     }
     uint4 o;
