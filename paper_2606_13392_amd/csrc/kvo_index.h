@@ -285,15 +285,30 @@ __global__ __launch_bounds__(256) void expand_block_ids_kernel(const int32_t* __
   }
 }
 
+// Persistent work loops: a CTA's first item is blockIdx.x, later ones are
+// claimed from a global counter, so CTAs that drew cheap items take more
+// (the dynamic load balancing of Sec. 4.3).  The counters sit after the
+// ntile tile counts (cnt has ntile + kWorkCounters entries) and are zeroed
+// with them when the reverse index is built; each persistent launch that
+// follows uses its own one.
+constexpr int kWorkCounters = 2;
+__device__ __forceinline__ int32_t claim_next_item(int32_t* __restrict__ next_item, int32_t* s_claim) {
+  __syncthreads();                                    // every thread has read the previous claim
+  if (threadIdx.x == 0) *s_claim = static_cast<int32_t>(gridDim.x) + atomicAdd(next_item, 1);
+  __syncthreads();
+  return *s_claim;
+}
+
 // Reverse index of query rows r0 .. r0 + nr - 1 (one chunk): counts, scans
 // and handle lists for every tile of H_kv x nbcap.
 void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int64_t* blk_base, int H_kv, int BK,
                          int topk, int64_t nbcap, int64_t ntile, int nscan, int64_t r0, int64_t nr, int32_t* cnt,
                          int32_t* tile_off, int32_t* item_off, int32_t* blk_tot, int32_t* tpos, uint32_t* handles,
                          hipStream_t stream) {
-  const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((ntile + 255) / 256, 4096));
+  const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((ntile + kWorkCounters + 255) / 256, 4096));
   const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
-  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt, ntile, 0);
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt,
+                   ntile + kWorkCounters, 0);
   const dim3 hgrid(static_cast<unsigned>((nr + kHistRows - 1) / kHistRows), static_cast<unsigned>(H_kv));
   msa_prof::launch("kvo_count_kernel", kvo_count_kernel, hgrid, dim3(256), 0, stream, block_ids, sq, blk_base, H_kv,
                    BK, topk, nbcap, r0, nr, cnt, tpos);

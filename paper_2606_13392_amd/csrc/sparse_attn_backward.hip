@@ -103,8 +103,9 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
     const uint16_t* __restrict__ d_o, const float* __restrict__ lse, const float* __restrict__ delta, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0, float scale_log2,
-    uint16_t* __restrict__ dq_buf, int64_t dq_trash, float* __restrict__ part) {
+    uint16_t* __restrict__ dq_buf, int64_t dq_trash, float* __restrict__ part, int32_t* __restrict__ next_item) {
   __shared__ BwdSmem sm;
+  __shared__ int32_t s_claim;
   constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
 
-  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -460,7 +461,7 @@ void bwd_layout(BwdPlan& pl, const msa_seqs* seqs, int H_q, int H_kv, int topk) 
   using msa_host::align_up;
   size_t o = 0;
   pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
-  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * (pl.ntile + kWorkCounters), 256);
   pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
@@ -580,7 +581,8 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
                      static_cast<const float*>(delta), sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
                      static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf,
-                     static_cast<int64_t>(pl.chunk_rows) * H_kv * topk * (H_q / H_kv) * kHeadDim, part);
+                     static_cast<int64_t>(pl.chunk_rows) * H_kv * topk * (H_q / H_kv) * kHeadDim, part,
+                     cnt + pl.ntile);
     msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile * kReduceSplit)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
                      static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc,

@@ -50,8 +50,9 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off,
     const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk,
     int64_t nbcap, int64_t row0, float scale_log2, float o_scale, uint16_t* __restrict__ o_buf,
-    float* __restrict__ lse_buf) {
+    float* __restrict__ lse_buf, int32_t* __restrict__ next_item) {
   __shared__ KvoSmem<BK> sm;
+  __shared__ int32_t s_claim;
   __shared__ int32_t s_row[kItemQueries];     // query row inside the chunk
   __shared__ int32_t s_pos[kItemQueries];     // its absolute position
   __shared__ int32_t s_slot[kItemQueries];    // slot of this block in the row's id list
@@ -69,7 +70,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
 
-  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -388,7 +389,7 @@ size_t fixed_bytes(KvoPlan& pl, const msa_seqs* seqs) {
   using msa_host::align_up;
   size_t o = 0;
   pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
-  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * (pl.ntile + kWorkCounters), 256);
   pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
@@ -460,13 +461,13 @@ template <int BK, typename T>
 void launch_kvo_attn(const void* q, const void* k, const void* v, const msa_seqs& sq, const int64_t* blk_base,
                      const int32_t* tile_off, const int32_t* item_off, const uint32_t* handles, int H_q, int H_kv,
                      int topk, int64_t nbcap, int64_t r0, float sl2, float o_scale, uint16_t* o_buf, float* lse_buf,
-                     hipStream_t stream) {
+                     int32_t* next_item, hipStream_t stream) {
   static int ctas = 0;
   constexpr int threads = 64 * kvo_waves<BK>();
   msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<BK, T>,
                    dim3(persistent_ctas(kvo_attn_kernel<BK, T>, threads, &ctas)), dim3(threads), 0, stream,
                    static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v), sq, blk_base,
-                   tile_off, item_off, handles, H_q, H_kv, topk, nbcap, r0, sl2, o_scale, o_buf, lse_buf);
+                   tile_off, item_off, handles, H_q, H_kv, topk, nbcap, r0, sl2, o_scale, o_buf, lse_buf, next_item);
 }
 
 }  // namespace
@@ -502,16 +503,16 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
                         item_off, blk_tot, tpos, handles, stream);
     if (BK == 64 && !fp8)
       launch_kvo_attn<64, uint16_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0,
-                                    sl2, v_scale, o_buf, lse_buf, stream);
+                                    sl2, v_scale, o_buf, lse_buf, cnt + pl.ntile, stream);
     else if (BK == 64)
       launch_kvo_attn<64, uint8_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap, r0,
-                                   sl2, v_scale, o_buf, lse_buf, stream);
+                                   sl2, v_scale, o_buf, lse_buf, cnt + pl.ntile, stream);
     else if (!fp8)
       launch_kvo_attn<128, uint16_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap,
-                                     r0, sl2, v_scale, o_buf, lse_buf, stream);
+                                     r0, sl2, v_scale, o_buf, lse_buf, cnt + pl.ntile, stream);
     else
       launch_kvo_attn<128, uint8_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap,
-                                    r0, sl2, v_scale, o_buf, lse_buf, stream);
+                                    r0, sl2, v_scale, o_buf, lse_buf, cnt + pl.ntile, stream);
     const int64_t pairs = nr * H_kv;
     msa_prof::launch("kvo_combine_kernel", kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
                        dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,

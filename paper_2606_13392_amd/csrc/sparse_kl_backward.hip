@@ -101,8 +101,9 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_kv, int topk, int64_t nbcap, int64_t row0, float sidx_log2,
-    float* __restrict__ lse_part) {
+    float* __restrict__ lse_part, int32_t* __restrict__ next_item) {
   __shared__ KlLseSmem<D> sm;
+  __shared__ int32_t s_claim;
   constexpr int KS = D / 32;
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
@@ -110,7 +111,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
   const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
   const int32_t total_items = item_off[ntile];
   int64_t staged = -1;
-  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -241,8 +242,9 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
     float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
-    float* __restrict__ part) {
+    float* __restrict__ part, int32_t* __restrict__ next_item) {
   __shared__ KlSmem<D> sm;
+  __shared__ int32_t s_claim;
   constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
   constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
   constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
@@ -258,7 +260,7 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
 
-  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -488,9 +490,10 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
     float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
-    float* __restrict__ part) {
+    float* __restrict__ part, int32_t* __restrict__ next_item) {
   static_assert(D == 64, "d k_idx of 64 keys x 128 dims does not fit a wave's registers");
   __shared__ KlwSmem<D> sm;
+  __shared__ int32_t s_claim;
   constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
   constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
   constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
@@ -507,7 +510,7 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   KlwWave<D>& wv = sm.u.m.wv[w];
 
-  for (int32_t item = blockIdx.x; item < total_items; item += gridDim.x) {
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -846,7 +849,7 @@ void kl_layout(KlPlan& pl, const msa_seqs* seqs, int H_kv, int D, int topk) {
   using msa_host::align_up;
   size_t o = 0;
   pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
-  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * pl.ntile, 256);
+  pl.off_cnt = o;      o = align_up(o + sizeof(int32_t) * (pl.ntile + kWorkCounters), 256);
   pl.off_tile_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_item_off = o; o = align_up(o + sizeof(int32_t) * (pl.ntile + 1), 256);
   pl.off_blk_tot = o;  o = align_up(o + sizeof(int32_t) * 2 * pl.nscan, 256);
@@ -962,7 +965,7 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
     msa_prof::launch("kl_lse_kernel", kl_lse_kernel<D>, dim3(n_lse), dim3(kKlThreads), 0, stream, iq, ik, sq,
                      static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
                      static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,
-                     pl.nbcap, r0, sidx * kLog2e, lsep);
+                     pl.nbcap, r0, sidx * kLog2e, lsep, cnt + pl.ntile);
     msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
                      dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
                      static_cast<const float*>(lsep), lsei);
@@ -971,14 +974,15 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                           static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
                           static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
                           static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
-                          topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part);
+                          topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part,
+                          cnt + pl.ntile + 1);
     else
       msa_prof::launch("kl_grad_kernel", kl_grad_kernel<D>, dim3(n_grad), dim3(kKlThreads), 0, stream, iq, ik,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
                        static_cast<const float*>(lsei), sq, static_cast<const int64_t*>(blk_base),
                        static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
                        static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
-                       sidx, trash_inc, dqp, klp, part);
+                       sidx, trash_inc, dqp, klp, part, cnt + pl.ntile + 1);
     msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>,
                      dim3(static_cast<unsigned>(pl.nbcap * kKlReduceSplit<D>)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
