@@ -104,6 +104,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0, float scale_log2,
     uint16_t* __restrict__ dq_buf, int64_t dq_trash, float* __restrict__ part, int32_t* __restrict__ next_item) {
+  static_assert(kItemQueries <= kBwdThreads, "every thread loads at most one handle of an item");
   __shared__ BwdSmem sm;
   __shared__ int32_t s_claim;
   constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension

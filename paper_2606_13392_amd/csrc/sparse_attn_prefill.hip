@@ -51,6 +51,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
     const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk,
     int64_t nbcap, int64_t row0, float scale_log2, float o_scale, uint16_t* __restrict__ o_buf,
     float* __restrict__ lse_buf, int32_t* __restrict__ next_item) {
+  static_assert(kItemQueries <= 64 * kvo_waves<BK>(), "every thread loads at most one handle of an item");
   __shared__ KvoSmem<BK> sm;
   __shared__ int32_t s_claim;
   __shared__ int32_t s_row[kItemQueries];     // query row inside the chunk

@@ -102,6 +102,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_kv, int topk, int64_t nbcap, int64_t row0, float sidx_log2,
     float* __restrict__ lse_part, int32_t* __restrict__ next_item) {
+  static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
   __shared__ KlLseSmem<D> sm;
   __shared__ int32_t s_claim;
   constexpr int KS = D / 32;
@@ -243,6 +244,7 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
     float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
     float* __restrict__ part, int32_t* __restrict__ next_item) {
+  static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
   __shared__ KlSmem<D> sm;
   __shared__ int32_t s_claim;
   constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
@@ -492,6 +494,7 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
     float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
     float* __restrict__ part, int32_t* __restrict__ next_item) {
   static_assert(D == 64, "d k_idx of 64 keys x 128 dims does not fit a wave's registers");
+  static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
   __shared__ KlwSmem<D> sm;
   __shared__ int32_t s_claim;
   constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
