@@ -23,9 +23,8 @@
 //                    the teacher's head mean in registers; d k_idx of the
 //                    block in registers (an fp32 partial per item), d q_idx
 //                    and the KL term of every incidence as fp32 partials
-//                    (d_idx 64: kl_grad_wave, one wave per 32-row pass
-//                    against all 64 keys, no barrier between passes; d_idx
-//                    128: the four waves split the keys of each pass)
+//                    (kl_grad_wave: one wave per 32-row pass against all 64
+//                    keys, no barrier between passes)
 //   kl_tile_reduce   per key block: the items of every group's tile, in
 //                    order, added to the fp32 d k_idx accumulator
 //   kl_combine       per (row, group): d q_idx and KL over the valid slots, in
@@ -41,21 +40,6 @@ constexpr int kKlBK = 64;
 constexpr int kKlThreads = 256;                       // 4 waves: key quarters
 constexpr int kKlRows = 32;                           // gathered (query, head) rows per pass
 
-template <int D>
-struct KlSmem {
-  uint16_t k[kKlBK][kHeadDim + 8];                    // K block (Main Branch head r), row-major
-  uint16_t ki[kKlBK][D + 8];                          // index-key block, row-major
-  uint16_t kit[D][kKlBK + 8];                         // index-key block transposed
-  uint16_t qit[D][kKlRows + 8];                       // index query of each pass row, transposed
-  uint16_t dl[kKlRows][kKlBK + 8];                    // Delta of the pass (bf16), [row][key]
-  float kls[4][kKlRows];                              // KL term per (key quarter, row)
-  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row (+inf: no row)
-  float lsei2[kKlRows];                               // LSE_idx * log2(e) per row
-  int32_t rpos[kKlRows];                              // position per row (-1: no row)
-  int64_t incoff[kKlRows];                            // the row's incidence if it is its query's head 0, else trash
-  int32_t s_row[kItemQueries];
-  int32_t s_slot[kItemQueries];
-};
 
 __device__ __forceinline__ uint16_t raw_elem16(const u32x4& w, int j) {
   return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
@@ -229,236 +213,13 @@ __device__ __forceinline__ void head_mean(f32x4 (&v)[2], int lg) {
   }
 }
 
-// Wave kq owns keys 16kq .. 16kq+15 of the block.  MFMA 16x16x32 lane l =
-// (c16 = l % 16, qd = l / 16).  A pass takes qpw = 32 / G queries x G heads
-// = 32 rows; the Main Branch scores S and the index scores S_idx are both
-// computed per row (the index query of a row is its query's), so the lane
-// holding key 16kq + c16 has rows 16t + 4qd + i of both.  The teacher mean
-// over a query's heads is a register reduction; Delta enters d k_idx and the
-// KL only through each query's head-0 row.
-template <int D>
-__global__ __launch_bounds__(kKlThreads, D == 64 ? 3 : 2) void kl_grad_kernel(
-    const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
-    const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
-    const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
-    const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
-    float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
-    float* __restrict__ part, int32_t* __restrict__ next_item) {
-  static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
-  __shared__ KlSmem<D> sm;
-  __shared__ int32_t s_claim;
-  constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
-  constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
-  constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
-  const int lane = lane_id();
-  const int kq = threadIdx.x / kWave;
-  const int c16 = lane & 15, qd = lane >> 4;
-  const int G = H_q / H_kv;                           // a power of two <= 16
-  const int lg = __builtin_ctz(G);
-  const int qpw = 32 >> lg;
-  const float sidx_log2 = sidx * kLog2e;
-  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
-  const int32_t total_items = item_off[ntile];
-  const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
-  int64_t staged = -1;
-
-  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
-    const int64_t tile = upper_index(item_off, ntile + 1, item);
-    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
-    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
-    const int r = static_cast<int>(tile / nbcap);
-    const int64_t gb = tile % nbcap;
-    const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
-    const SeqGeom g = seq_geom(sq, s);
-    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
-    const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
-
-    __syncthreads();                                  // the previous item is done with LDS
-    if (static_cast<int>(threadIdx.x) < nq) {
-      const uint32_t hd = handles[h0 + threadIdx.x];
-      sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
-      sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
-    }
-    if (tile != staged) {
-      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      for (int c = threadIdx.x; c < kKlBK * (kHeadDim / 8); c += kKlThreads) {
-        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
-        *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) =
-            key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
-      }
-      stage_index_keys<D>(sm, index_k + (g.kv_start + key0) * static_cast<int64_t>(D), g.kv_len - key0);
-      staged = tile;
-    }
-    __syncthreads();
-
-    f32x4 acc_dk[NT];                                 // d k_idx: lane column = dim, rows = keys 4qd + i
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc_dk[t] = f32x4{};
-    const int key = key0 + 16 * kq + c16;             // this lane's key in the C layouts
-
-    // A operands of a pass (rows 16t + c16): Q of the row's head, the index
-    // query of the row's query, and the two LSEs; the next pass's are
-    // requested once S and S_idx have consumed the current ones.
-    u32x4 bq[2][KSM], bi[2][KSI];
-    float lse_v[2], lsei_v[2];
-    bool arow[2];
-    int32_t qrow[2];
-    auto load_pass = [&](int cc) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int qa = cc + ((16 * t + c16) >> lg);
-        arow[t] = qa < nq;
-        qrow[t] = min(qa, nq - 1);
-        const int64_t rl = sm.s_row[qrow[t]];
-        const int64_t grow = row0 + rl;
-        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + ((16 * t + c16) & (G - 1));
-#pragma unroll
-        for (int st = 0; st < KSM; ++st) bq[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
-#pragma unroll
-        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (grow * H_kv + r) * D + 32 * st + 8 * qd);
-        lse_v[t] = lse[hrow];
-        lsei_v[t] = lse_idx[rl * H_kv + r];
-      }
-    };
-    load_pass(0);
-
-    for (int c = 0; c < nq; c += qpw) {
-      __syncthreads();                                // the previous pass is done with qit, dl, kls, row scalars
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int col = 16 * t + c16;
-        // index queries transposed: wave kq writes k-step kq (there are D / 32 <= 4)
-#pragma unroll
-        for (int st = 0; st < KSI; ++st) {
-          if (st != kq) continue;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) sm.qit[32 * st + 8 * qd + j][col] = raw_elem16(bi[t][st], j);
-        }
-        if (qd == 0 && kq == 0) {
-          sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
-          sm.lsei2[col] = arow[t] ? lsei_v[t] * kLog2e : INFINITY;
-          const int32_t rl = sm.s_row[qrow[t]];
-          sm.rpos[col] = arow[t] ? pos_base + rl : -1;
-          sm.incoff[col] = (arow[t] && (col & (G - 1)) == 0)
-                               ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[qrow[t]]
-                               : trash_inc;
-        }
-      }
-      __syncthreads();
-
-      // S and S_idx of this key quarter: lane holds key, rows 16t + 4qd + i
-      f32x4 acc_s[2], acc_i[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        acc_s[t] = f32x4{};
-        acc_i[t] = f32x4{};
-#pragma unroll
-        for (int st = 0; st < KSM; ++st)
-          acc_s[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
-                                  ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
-#pragma unroll
-        for (int st = 0; st < KSI; ++st)
-          acc_i[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bi[t][st]),
-                                  ld_bf16x8(&sm.ki[16 * kq + c16][32 * st + 8 * qd]), acc_i[t]);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-      if (c + qpw < nq) load_pass(c + qpw);
-
-      // teacher: per-head P, then the mean over the query's heads
-      f32x4 pb[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = 16 * t + 4 * qd + i;
-          pb[t][i] = key <= sm.rpos[row] ? exp2f(acc_s[t][i] * s_main_log2 - sm.lse2[row]) : 0.f;
-        }
-      head_mean(pb, lg);
-      // student, Delta = P_idx - P, KL term; head-0 rows carry their query
-      f32x4 dlt[2], dk_a[2];
-      float klq[2][4];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = 16 * t + 4 * qd + i;
-          const bool on = key <= sm.rpos[row];
-          const bool head0 = (row & (G - 1)) == 0;
-          const float lz = acc_i[t][i] * sidx_log2 - sm.lsei2[row];   // log2 P_idx
-          const float pidx = on ? exp2f(lz) : 0.f;
-          const float pbar = pb[t][i];
-          dlt[t][i] = pidx - pbar;
-          dk_a[t][i] = head0 ? dlt[t][i] : 0.f;
-          klq[t][i] = (head0 && on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
-        }
-      // d k_idx += Delta^T q_idx over the pass's rows (one k-step): k index
-      // 8qd + 4t + i = row 16t + 4qd + i
-      {
-        uint4 w;
-        w.x = pack_bf16x2(dk_a[0][0], dk_a[0][1]);
-        w.y = pack_bf16x2(dk_a[0][2], dk_a[0][3]);
-        w.z = pack_bf16x2(dk_a[1][0], dk_a[1][1]);
-        w.w = pack_bf16x2(dk_a[1][2], dk_a[1][3]);
-        const bf16x8 da = __builtin_bit_cast(bf16x8, w);
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const uint16_t* qr = &sm.qit[16 * t + c16][4 * qd];
-          const uint2 lo = *reinterpret_cast<const uint2*>(qr), hi = *reinterpret_cast<const uint2*>(qr + 16);
-          acc_dk[t] = mfma16x16x32(da, __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y)), acc_dk[t]);
-        }
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const uint32_t lo = pack_bf16x2(dlt[t][0], dlt[t][1]), hi = pack_bf16x2(dlt[t][2], dlt[t][3]);
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            sm.dl[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>((i < 2 ? lo : hi) >> (16 * (i & 1)));
-        }
-      }
-      // KL per row: sum over this wave's 16 keys, then over the 4 waves in LDS
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v = klq[t][i];
-#pragma unroll
-          for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
-          if (c16 == 0) sm.kls[kq][16 * t + 4 * qd + i] = v;
-        }
-      __syncthreads();                                // Delta and KL terms of every key in LDS
-
-      // d q_idx per row (the query's head-0 row is stored): dims 16n + c16 for
-      // n % 4 == kq, over the 64 keys
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        if ((n & 3) != kq) continue;
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          f32x4 acc = f32x4{};
-#pragma unroll
-          for (int ks = 0; ks < kKlBK / 32; ++ks)
-            acc = mfma16x16x32(ld_bf16x8(&sm.dl[16 * t + c16][32 * ks + 8 * qd]),
-                               ld_bf16x8(&sm.kit[16 * n + c16][32 * ks + 8 * qd]), acc);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) dqp[sm.incoff[16 * t + 4 * qd + i] * D + 16 * n + c16] = acc[i];
-        }
-      }
-      if (kq == 0 && lane < 32)
-        klp[sm.incoff[lane]] = sm.kls[0][lane] + sm.kls[1][lane] + sm.kls[2][lane] + sm.kls[3][lane];
-    }
-
-    // item end: this wave's keys of d k_idx as the item's partial [kq][reg][lane]
-    float* dst = part + static_cast<int64_t>(item) * (kKlBK * D) + kq * (NT * 4 * 64) + lane;
-#pragma unroll
-    for (int reg = 0; reg < NT * 4; ++reg) dst[reg * 64] = acc_dk[reg >> 2][reg & 3];
-  }
-}
-
 // ---------------------------------------------------------------- gradients, one wave per pass
-// d_idx 64: a wave takes whole passes (32 rows against all 64 keys of the
-// block), so passes need no CTA barrier and each wave is its own stream of
-// gathers; the block's K, index keys and their transpose are shared by the
-// CTA per item.  d k_idx of all 64 keys stays in the wave's registers (64
-// VGPRs); at item end the four waves' partials are added in wave order.
+// A wave takes whole passes (32 rows against all 64 keys of the block), so
+// passes need no CTA barrier and each wave is its own stream of gathers; the
+// block's K, index keys and their transpose are shared by the CTA per item.
+// d k_idx of all 64 keys stays in the wave's registers (64 VGPRs at d_idx
+// 64, 128 at d_idx 128); at item end the four waves' partials are added in
+// wave order.
 template <int D>
 struct KlwWave {
   uint16_t qit[D][kKlRows + 8];                       // index query of each pass row, transposed
@@ -482,18 +243,19 @@ struct KlwSmem {
   int32_t s_row[kItemQueries];
   int32_t s_slot[kItemQueries];
 };
-// two CTAs per CU
-static_assert(sizeof(KlwSmem<64>) <= 80 * 1024, "LDS of a one-wave-per-pass KL CTA");
+// d_idx 64: two CTAs per CU (245 VGPRs at G = 8); d_idx 128: d k_idx alone
+// takes 128 VGPRs, so one CTA per CU with up to 512 registers per wave
+static_assert(sizeof(KlwSmem<64>) <= 80 * 1024, "LDS of a one-wave-per-pass KL CTA (two per CU)");
+static_assert(sizeof(KlwSmem<128>) <= 160 * 1024, "LDS of a one-wave-per-pass KL CTA (one per CU)");
 
 template <int D, int LG>
-__global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
+__global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
     float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
     float* __restrict__ part, int32_t* __restrict__ next_item) {
-  static_assert(D == 64, "d k_idx of 64 keys x 128 dims does not fit a wave's registers");
   static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
   __shared__ KlwSmem<D> sm;
   __shared__ int32_t s_claim;
@@ -547,7 +309,9 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
 #pragma unroll
       for (int n = 0; n < NT; ++n) acc_dk[kt][n] = f32x4{};
 
-    // A operands of a pass (rows 16t + c16), as in kl_grad_kernel
+    // A operands of a pass (rows 16t + c16): Q of the row's head, the index
+    // query of the row's query, and the two LSEs; the next pass's are
+    // requested once S and S_idx have consumed the current ones
     u32x4 bq[2][KSM], bi[2][KSI];
     float lse_v[2], lsei_v[2];
     bool arow[2];
@@ -718,7 +482,7 @@ __global__ __launch_bounds__(kKlThreads, 2) void kl_grad_wave_kernel(
     }
 
     // item end: the four waves' d k_idx, added in wave order, as the item's
-    // partial in kl_grad_kernel's layout [key quarter][reg][lane]
+    // partial, laid out [key quarter][reg][lane] as kl_tile_reduce_kernel reads it
     __syncthreads();                                  // every pass is done: K and pass LDS are free
 #pragma unroll
     for (int kt = 0; kt < 4; ++kt)
@@ -914,14 +678,14 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
 }
 
 // kl_grad_wave_kernel instance for G = 2^lg (lg <= 4, checked by validate_kl).
-template <typename... Args>
+template <int D, typename... Args>
 void launch_kl_grad_wave(int lg, dim3 grid, hipStream_t stream, Args... args) {
   switch (lg) {
-    case 0: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 0>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 1: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 1>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 2: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 2>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 3: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 3>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    default: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<64, 4>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 0: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 0>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 1: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 1>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 2: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 2>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 3: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 3>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    default: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 4>, grid, dim3(kKlThreads), 0, stream, args...); break;
   }
 }
 
@@ -956,8 +720,7 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                    reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
   static int ctas_lse = 0, ctas_grad = 0;
   const int n_lse = persistent_ctas(kl_lse_kernel<D>, kKlThreads, &ctas_lse);
-  const int n_grad = D == 64 ? persistent_ctas(kl_grad_wave_kernel<64, 3>, kKlThreads, &ctas_grad)
-                            : persistent_ctas(kl_grad_kernel<D>, kKlThreads, &ctas_grad);
+  const int n_grad = persistent_ctas(kl_grad_wave_kernel<D, 3>, kKlThreads, &ctas_grad);
   const int lg_g = __builtin_ctz(static_cast<unsigned>(H_q / H_kv));
   const int64_t trash_inc = pl.chunk_rows * H_kv * static_cast<int64_t>(topk);
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
@@ -972,20 +735,12 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
     msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
                      dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
                      static_cast<const float*>(lsep), lsei);
-    if constexpr (D == 64)
-      launch_kl_grad_wave(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
-                          static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
-                          static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
-                          static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
-                          topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part,
-                          cnt + pl.ntile + 1);
-    else
-      msa_prof::launch("kl_grad_kernel", kl_grad_kernel<D>, dim3(n_grad), dim3(kKlThreads), 0, stream, iq, ik,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
-                       static_cast<const float*>(lsei), sq, static_cast<const int64_t*>(blk_base),
-                       static_cast<const int32_t*>(tile_off), static_cast<const int32_t*>(item_off),
-                       static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, softmax_scale * kLog2e,
-                       sidx, trash_inc, dqp, klp, part, cnt + pl.ntile + 1);
+    launch_kl_grad_wave<D>(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
+                        static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
+                        static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
+                        static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
+                        topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part,
+                        cnt + pl.ntile + 1);
     msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>,
                      dim3(static_cast<unsigned>(pl.nbcap * kKlReduceSplit<D>)),
                      dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
