@@ -110,7 +110,9 @@ __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restric
     for (int i = threadIdx.x; i < kHistBins; i += 256) hist[i] = 0;
     __syncthreads();
   }
-  // pass 1: histogram (or, without LDS room, claim each position directly)
+  // pass 1: histogram (or, without LDS room, claim each position directly);
+  // one row per thread keeps 64 rows' id lookups in flight per wave (one row
+  // per wave, slot on lane, took twice as long)
   for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
     int s;
     const int p = row_position(sq, row, &s);
@@ -148,14 +150,16 @@ __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restric
   }
 }
 
-// One thread per (row, group) of the chunk: handle = (row in chunk << 6 | slot).
+// One wave per (row, group) of the chunk, slot j on lane j: handle =
+// (row in chunk << 6 | slot).
 __global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
                                                        const int64_t* __restrict__ blk_base, int H_kv, int BK,
                                                        int topk, int64_t nbcap, int64_t row0, int64_t nrows,
                                                        const int32_t* __restrict__ tile_off,
                                                        const int32_t* __restrict__ tpos,
                                                        uint32_t* __restrict__ handles) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int lane = lane_id();
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * (256 / kWave) + threadIdx.x / kWave;
   if (i >= nrows * H_kv) return;
   const int64_t rl = i / H_kv;
   const int64_t row = row0 + rl;
@@ -165,10 +169,10 @@ __global__ __launch_bounds__(256) void kvo_fill_kernel(const int32_t* __restrict
   const int32_t* ids = block_ids + (row * H_kv + r) * topk;
   const int32_t* tp = tpos + i * topk;
   const int64_t base = static_cast<int64_t>(r) * nbcap + blk_base[s];
-  for (int j = 0; j < topk; ++j) {
-    const int b = ids[j];
-    if (!incidence_ok(b, p, BK, blk_base, s)) continue;
-    handles[tile_off[base + b] + tp[j]] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(j);
+  if (lane < topk) {
+    const int b = ids[lane];
+    if (incidence_ok(b, p, BK, blk_base, s))
+      handles[tile_off[base + b] + tp[lane]] = (static_cast<uint32_t>(rl) << 6) | static_cast<uint32_t>(lane);
   }
 }
 
@@ -306,7 +310,7 @@ void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int
                          int32_t* tile_off, int32_t* item_off, int32_t* blk_tot, int32_t* tpos, uint32_t* handles,
                          hipStream_t stream) {
   const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((ntile + kWorkCounters + 255) / 256, 4096));
-  const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 255) / 256);
+  const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 256 / kWave - 1) / (256 / kWave));   // a wave per pair
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt,
                    ntile + kWorkCounters, 0);
   const dim3 hgrid(static_cast<unsigned>((nr + kHistRows - 1) / kHistRows), static_cast<unsigned>(H_kv));
