@@ -133,6 +133,7 @@ __device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][NJ], int
 
 // ---------------------------------------------------------------- scores, LDS
 constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
+constexpr int kPieceBlocks = 16;      // blocks per piece maximum (the Top-k's finer skip test)
 
 // One 16-byte piece per lane from global memory straight into LDS
 // (global_load_lds_dwordx4): lane l writes bytes [16 l, 16 l + 16) after the
@@ -166,8 +167,9 @@ template <int D_IDX, int BK, int RW, bool PAGED>
 __global__ __launch_bounds__(256, (RW == 64) ? 3 : 2) void index_block_max_lds_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int64_t u0, int64_t u1, float* __restrict__ M,
-    int64_t ldm, float* __restrict__ CM, int64_t cm_stride) {
+    int64_t ldm, float* __restrict__ CM, int64_t cm_stride, float* __restrict__ PM) {
   static_assert(kBlocksPerCta == kWave, "a CTA slice is one Top-k chunk");
+  static_assert(kStageBlocks == kPieceBlocks, "a piece ends where a store pass does");
   constexpr int KS = D_IDX / 16;                        // k-steps of the MFMA
   constexpr int SEGS = D_IDX / 8;                       // 16-byte segments per key row
   constexpr int SUB = BK / 64;                          // 64-key sub-blocks staged per block
@@ -200,11 +202,12 @@ __global__ __launch_bounds__(256, (RW == 64) ? 3 : 2) void index_block_max_lds_k
   float* mrow0 = M + slot0 * ldm;
   // lane holds rows 64 s + lane; their candidate blocks end at their local blocks
   int lb_lane[NP];
-  float cmax[NP];
+  float cmax[NP], pmax[NP];
 #pragma unroll
   for (int sp = 0; sp < NP; ++sp) {
     lb_lane[sp] = (ur.g.kv_len - ur.g.q_rows + ur.t0 + wq0 + (64 * sp + lane) / H_kv) / BK;
     cmax[sp] = -INFINITY;
+    pmax[sp] = -INFINITY;
   }
 
   const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, 64);   // 64-key view of the blocks
@@ -245,10 +248,19 @@ __global__ __launch_bounds__(256, (RW == 64) ? 3 : 2) void index_block_max_lds_k
     }
 #pragma unroll
     for (int sp = 0; sp < NP; ++sp) {
-      if (kb < lb_lane[sp]) cmax[sp] = fmaxf(cmax[sp], bm[sp]);
+      if (kb < lb_lane[sp]) {
+        cmax[sp] = fmaxf(cmax[sp], bm[sp]);
+        pmax[sp] = fmaxf(pmax[sp], bm[sp]);
+      }
       sm.stage[w][64 * sp + lane][kb & (kStageBlocks - 1)] = bm[sp];
     }
     if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
+      // the piece's maximum over each row's candidate blocks, PM[piece][row]
+#pragma unroll
+      for (int sp = 0; sp < NP; ++sp) {
+        if (64 * sp + lane < nvalid) PM[static_cast<int64_t>(kb / kPieceBlocks) * cm_stride + slot0 + 64 * sp + lane] = pmax[sp];
+        pmax[sp] = -INFINITY;
+      }
       // the wave writes 16 rows x 64 B per store pass (4 lanes per row, 16 B each)
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
@@ -597,13 +609,15 @@ __device__ __forceinline__ uint64_t scan_row_batched(Load load, int nscan, KeyBa
   return kb.list;
 }
 
-// The same selection with chunk maxima: chunk c of the row (scores
-// 64c .. 64c+63) has maximum cm(c).  The K1-th largest chunk maximum t0 is a
-// lower bound of the row's K1-th best score (K1 distinct chunks each hold a
-// score >= t0), so chunks with maximum below t0 are skipped and scores below
-// t0 are never ranked.
-template <typename Load, typename LoadCm>
-__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int nscan, KeyBatch& kb) {
+// The same selection with chunk and piece maxima: chunk c of the row
+// (scores 64c .. 64c+63) has maximum cm(c), piece q (scores 16q .. 16q+15)
+// maximum pm(q), both over candidate blocks only.  The K1-th largest chunk
+// maximum t0 is a lower bound of the row's K1-th best score (K1 distinct
+// chunks each hold a score >= t0), so pieces with maximum below t0 are
+// skipped and scores below t0 are never ranked.  Surviving pieces are read
+// four per wave load (lanes 16 k .. 16 k + 15 take the k-th).
+template <typename Load, typename LoadCm, typename LoadPm>
+__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, LoadPm pm, int nscan, KeyBatch& kb) {
   const int lane = lane_id();
   const int K1 = kb.K1;
   const int nchunk = (nscan + kWave - 1) / kWave;
@@ -613,48 +627,61 @@ __device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, int ns
   // keys above floor_key have scores >= t0 (o0 > 0 for every non-NaN score)
   const uint64_t floor_key = o0 > 0 ? (static_cast<uint64_t>(o0) << 32) - 1 : 0ull;
 
+  const int npiece = (nscan + kPieceBlocks - 1) / kPieceBlocks;
   int g = 0;
   uint64_t mask = 0;
   bool more = true;
-  // next chunk whose maximum reaches t0 (wave-uniform), or -1
-  auto next_chunk = [&]() -> int {
+  // next piece whose maximum reaches t0 (wave-uniform), or -1
+  auto next_piece = [&]() -> int {
     while (mask == 0) {
       if (!more) return -1;
       const int c = kWave * g + lane;
-      mask = __ballot(c < nchunk && ordered_u32(cm(c)) >= o0);
+      mask = __ballot(c < npiece && ordered_u32(pm(c)) >= o0);
       ++g;
-      more = kWave * g < nchunk;
+      more = kWave * g < npiece;
     }
     const int j = __ffsll(static_cast<unsigned long long>(mask)) - 1;
     mask &= mask - 1;
     return kWave * (g - 1) + j;
   };
+  // this lane's piece of the next four (-1 past the last)
+  auto next_quad = [&]() -> int {
+    int mine = -1;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int pc = next_piece();
+      if ((lane >> 4) == k) mine = pc;
+    }
+    return mine;
+  };
   kb.list = 0;
   kb.cnt = 0;
   uint64_t tau = floor_key;
   constexpr int kAhead = 4;
-  int cs[kAhead];
+  int lp[kAhead];
   float pf[kAhead];
 #pragma unroll
   for (int a = 0; a < kAhead; ++a) {
-    cs[a] = next_chunk();
-    const int b = cs[a] * kWave + lane;
-    pf[a] = (cs[a] >= 0 && b < nscan) ? load(b) : 0.f;
+    lp[a] = next_quad();
+    const int b = lp[a] * kPieceBlocks + (lane & 15);
+    pf[a] = (lp[a] >= 0 && b < nscan) ? load(b) : 0.f;
   }
-  while (cs[0] >= 0) {
-    const int b = cs[0] * kWave + lane;
+  // the quad's first piece is lane 0's: once it is -1 every piece is
+  while (__builtin_amdgcn_readfirstlane(lp[0]) >= 0) {
+    const int b = lp[0] * kPieceBlocks + (lane & 15);
+    const bool ok = lp[0] >= 0 && b < nscan;
     const float x = pf[0];
 #pragma unroll
     for (int a = 0; a + 1 < kAhead; ++a) {
-      cs[a] = cs[a + 1];
+      lp[a] = lp[a + 1];
       pf[a] = pf[a + 1];
     }
-    cs[kAhead - 1] = next_chunk();
+    lp[kAhead - 1] = next_quad();
     {
-      const int bn = cs[kAhead - 1] * kWave + lane;
-      pf[kAhead - 1] = (cs[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
+      const int bn = lp[kAhead - 1] * kPieceBlocks + (lane & 15);
+      pf[kAhead - 1] = (lp[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
     }
-    const uint64_t v = b < nscan ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
+    const uint64_t v = ok ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
     tau = kb.push(v, tau);
   }
   kb.flush();
@@ -714,7 +741,8 @@ __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64
 // One wave per index row.  With chunk maxima (CM[chunk][row], row stride
 // cm_stride) the row is ranked by the pruned scan.
 __global__ __launch_bounds__(256) void index_topk_kernel(
-    const float* __restrict__ M, int64_t ldm, const float* __restrict__ CM, int64_t cm_stride, msa_seqs sq,
+    const float* __restrict__ M, int64_t ldm, const float* __restrict__ CM, int64_t cm_stride,
+    const float* __restrict__ PM, msa_seqs sq,
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int U, int rpu, int64_t u0, int64_t u1, int BK,
     int topk, int32_t* __restrict__ block_ids) {
   __shared__ uint64_t s_pend[kWaves][2 * kWave];
@@ -736,7 +764,9 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   if (CM) {
     const float* cmrow = CM + t.slot;
     auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
-    list = scan_row_pruned(load, cm, t.nscan, kb);
+    const float* pmrow = PM + t.slot;
+    auto pm = [=](int q) { return pmrow[static_cast<int64_t>(q) * cm_stride]; };
+    list = scan_row_pruned(load, cm, pm, t.nscan, kb);
   } else {
     list = scan_row_batched(load, t.nscan, kb);
   }
@@ -789,6 +819,7 @@ struct IndexPlan {
   int64_t max_units;    // upper bound of the units over all sequences
   int bcap;             // M row length (key blocks, multiple of 4)
   int cmcap;            // chunk maxima per row (64-block Top-k chunks; U = 4 only, else 0)
+  int pcap;             // piece maxima per row (16-block pieces; with chunk maxima only)
   size_t hdr_bytes;
   size_t unit_bytes;    // M and chunk-maximum bytes per unit
 };
@@ -817,7 +848,8 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
   pl->cmcap = pl->U >= kWaves ? (pl->bcap + kWave - 1) / kWave : 0;
-  pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * (pl->bcap + pl->cmcap) * sizeof(float);
+  pl->pcap = pl->cmcap > 0 ? (pl->bcap + kPieceBlocks - 1) / kPieceBlocks : 0;
+  pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * (pl->bcap + pl->cmcap + pl->pcap) * sizeof(float);
   return MSA_OK;
 }
 
@@ -831,19 +863,19 @@ constexpr int kNarrowDepth = D == 64 ? 4 : 2;
 template <int D, int B, bool PAGED>
 void launch_scores_as(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
                       const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
-                      float* CM, int64_t cm_stride) {
+                      float* CM, int64_t cm_stride, float* PM) {
   if constexpr (D == 64 && B == 64) {
     if (pl.U == 2 * kWaves) {
       msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 128, PAGED>), grid, dim3(256),
                        0, stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
-                       cm_stride);
+                       cm_stride, PM);
       return;
     }
   }
   if (pl.U == kWaves)
     msa_prof::launch("index_block_max_lds_kernel", (index_block_max_lds_kernel<D, B, 64, PAGED>), grid, dim3(256), 0,
                      stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M, static_cast<int64_t>(pl.bcap), CM,
-                     cm_stride);
+                     cm_stride, PM);
   else if (pl.narrow)
     msa_prof::launch("index_block_max_narrow_kernel", (index_block_max_narrow_kernel<D, B, kNarrowDepth<D, B>, PAGED>),
                      grid, dim3(256), 0, stream, iq, ik, sq, unit_off, H_kv, pl.qr, u0, u1, M,
@@ -857,11 +889,11 @@ void launch_scores_as(const IndexPlan& pl, dim3 grid, hipStream_t stream, const 
 template <int D, int B>
 void launch_scores(const IndexPlan& pl, dim3 grid, hipStream_t stream, const uint16_t* iq, const uint16_t* ik,
                    const msa_seqs& sq, const int32_t* unit_off, int H_kv, int64_t u0, int64_t u1, float* M,
-                   float* CM, int64_t cm_stride) {
+                   float* CM, int64_t cm_stride, float* PM) {
   if (sq.block_table)
-    launch_scores_as<D, B, true>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride);
+    launch_scores_as<D, B, true>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride, PM);
   else
-    launch_scores_as<D, B, false>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride);
+    launch_scores_as<D, B, false>(pl, grid, stream, iq, ik, sq, unit_off, H_kv, u0, u1, M, CM, cm_stride, PM);
 }
 
 }  // namespace
@@ -894,6 +926,8 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   // chunk maxima CM[chunk][row] follow the chunk's score rows
   const int64_t cm_stride = chunk * pl.U * kWave;
   float* CM = pl.cmcap > 0 ? M + cm_stride * pl.bcap : nullptr;
+  // piece maxima PM[piece][row] follow the chunk maxima
+  float* PM = pl.cmcap > 0 ? CM + cm_stride * pl.cmcap : nullptr;
   const msa_seqs sq = *seqs;
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);
   const uint16_t* ik = static_cast<const uint16_t*>(index_k);
@@ -910,13 +944,13 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
                                      : dim3(static_cast<unsigned>((nslice + kWaves - 1) / kWaves),
                                             static_cast<unsigned>(u1 - u0));
     if (d_idx == 64 && block_size == 64)
-      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
+      launch_scores<64, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride, PM);
     else if (d_idx == 64)
-      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
+      launch_scores<64, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride, PM);
     else if (block_size == 64)
-      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
+      launch_scores<128, 64>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride, PM);
     else
-      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride);
+      launch_scores<128, 128>(pl, grid, stream, iq, ik, sq, unit_off, num_kv_heads, u0, u1, M, CM, cm_stride, PM);
     // index rows a unit can hold: its query rows (<= U * qr, <= max_q_rows) x H_kv
     const int rpu = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(pl.U) * pl.qr, seqs->max_q_rows)) *
                     num_kv_heads;
@@ -928,6 +962,7 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
     else
       msa_prof::launch("index_topk_kernel", index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)),
                        dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), static_cast<const float*>(CM), cm_stride,
+                       static_cast<const float*>(PM),
                        sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1, block_size, topk, block_ids);
   }
   return msa_host::launch_status();
