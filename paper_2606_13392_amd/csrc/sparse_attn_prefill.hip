@@ -70,8 +70,69 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
   const int32_t total_items = item_off[ntile];
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
+  constexpr int kThr = 64 * kvo_waves<BK>();
+  constexpr int KI = BK * (kHeadDim / 8) / kThr;          // K pieces per thread per block
+  static_assert(KI * kThr == BK * (kHeadDim / 8) && (BK / 4) * (kHeadDim / 8) == kThr, "staging map");
+  // B_k 64: the next item is claimed one ahead and its tile's K / V rows are
+  // loaded into registers while the current item is computed (B_k 128 has no
+  // registers to spare and stages after the barrier)
+  constexpr bool kPrefetch = BK == 64;
+  Raw<T> pk[KI], pv[4];
+  int64_t pf_tile = -1;
+  // K / V rows of `tl` into registers; keys at or past the sequence end read as zero
+  auto load_tile = [&](int64_t tl) {
+    const int r_ = static_cast<int>(tl / nbcap);
+    const int64_t gb_ = tl % nbcap;
+    const int s_ = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb_));
+    const SeqGeom g_ = seq_geom(sq, s_);
+    const int key0_ = static_cast<int>(gb_ - blk_base[s_]) * BK;
+    const int64_t brow = key_blocks(sq, g_, s_, BK).row(static_cast<int>(gb_ - blk_base[s_]));
+    const T* kb = k + brow * kv_stride + static_cast<int64_t>(r_) * kHeadDim;
+    const T* vb = v + brow * kv_stride + static_cast<int64_t>(r_) * kHeadDim;
+#pragma unroll
+    for (int i = 0; i < KI; ++i) {
+      const int c = threadIdx.x + kThr * i;
+      const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+      pk[i] = key0_ + key < g_.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : Raw<T>{};
+    }
+    {
+      const int key4 = threadIdx.x / (kHeadDim / 8), dg = threadIdx.x % (kHeadDim / 8);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key = 4 * key4 + j;
+        pv[j] = key0_ + key < g_.kv_len ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : Raw<T>{};
+      }
+    }
+  };
+  // registers to LDS: K row-major, V transposed
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int i = 0; i < KI; ++i) {
+      const int c = threadIdx.x + kThr * i;
+      const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+      *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = __builtin_bit_cast(uint4, widen(pk[i]));
+    }
+    const int key4 = threadIdx.x / (kHeadDim / 8), dg = threadIdx.x % (kHeadDim / 8);
+    uint4 rows[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) rows[j] = __builtin_bit_cast(uint4, widen(pv[j]));
+    const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
+    const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&rows[1]);
+    const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&rows[2]);
+    const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&rows[3]);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint2 w;
+      w.x = static_cast<uint32_t>(e0[e]) | (static_cast<uint32_t>(e1[e]) << 16);
+      w.y = static_cast<uint32_t>(e2[e]) | (static_cast<uint32_t>(e3[e]) << 16);
+      *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = w;
+    }
+  };
 
-  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
+  int32_t item = blockIdx.x;
+  int32_t nxt = 0;
+  if (kPrefetch && item < total_items) nxt = claim_next_item(next_item, &s_claim);
+  while (item < total_items) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
     const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
     const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
@@ -91,39 +152,19 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       s_pos[threadIdx.x] = g.kv_len - g.q_rows + static_cast<int>(row0 + rl - g.q_begin);
     }
     if (tile != staged) {
-      const int64_t brow = key_blocks(sq, g, s, BK).row(static_cast<int>(gb - blk_base[s]));
-      const T* kb = k + brow * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      const T* vb = v + brow * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
-        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
-        const uint4 x = key0 + key < g.kv_len
-                            ? __builtin_bit_cast(uint4, widen(load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg)))
-                            : make_uint4(0, 0, 0, 0);
-        *reinterpret_cast<uint4*>(&sm.k[key][8 * dg]) = x;
-      }
-      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += 64 * kvo_waves<BK>()) {
-        const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
-        uint4 rows[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int key = 4 * key4 + j;
-          rows[j] = key0 + key < g.kv_len
-                        ? __builtin_bit_cast(uint4, widen(load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg)))
-                        : make_uint4(0, 0, 0, 0);
-        }
-        const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&rows[0]);
-        const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&rows[1]);
-        const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&rows[2]);
-        const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&rows[3]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint2 w;
-          w.x = static_cast<uint32_t>(e0[e]) | (static_cast<uint32_t>(e1[e]) << 16);
-          w.y = static_cast<uint32_t>(e2[e]) | (static_cast<uint32_t>(e3[e]) << 16);
-          *reinterpret_cast<uint2*>(&sm.vt[8 * dg + e][4 * key4]) = w;
-        }
-      }
+      if (pf_tile != tile) load_tile(tile);
+      store_tile();
       staged = tile;
+    }
+    pf_tile = -1;
+    if constexpr (kPrefetch) {
+      if (nxt < total_items) {
+        const int64_t ntl = upper_index(item_off, ntile + 1, nxt);
+        if (ntl != tile) {
+          load_tile(ntl);
+          pf_tile = ntl;
+        }
+      }
     }
     __syncthreads();
 
@@ -260,6 +301,12 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       } else if (c + stride < nq) {
         load_q(c + stride, bq);
       }
+    }
+    if constexpr (kPrefetch) {
+      item = nxt;
+      if (item < total_items) nxt = claim_next_item(next_item, &s_claim);
+    } else {
+      item = claim_next_item(next_item, &s_claim);
     }
   }
 }
