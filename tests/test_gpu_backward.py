@@ -18,7 +18,7 @@ import torch
 
 import oracle.msa_oracle as O
 from paper_2606_13392_amd import msa, synth
-from tests.util import check_grad, from_dev_bits, to_dev
+from tests.util import check_grad, from_dev_bits, random_layouts, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -89,7 +89,12 @@ def _check_all(name, got, ref):
         _say(f"  {t} max-err/max|ref| {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+# seeded random batch layouts (sequence mix, head groups, block size, Top-k, key padding)
+RANDOM = [(c["name"], c["q_rows"], c["kv_lens"], c["H_q"], c["H_kv"], c["topk"], c["pad"], c["bk"])
+          for c in random_layouts(21, 8)]
+
+
+@pytest.mark.parametrize("case", CASES + RANDOM, ids=[c[0] for c in CASES + RANDOM])
 def test_backward_small(case):
     name = case[0]
     _say(f"[case] {name}")

@@ -22,7 +22,7 @@ import torch
 
 import oracle.msa_oracle as O
 from paper_2606_13392_amd import msa, synth
-from tests.util import check_grad, from_dev_bits, to_dev
+from tests.util import check_grad, from_dev_bits, random_layouts, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -67,7 +67,13 @@ def check_kl(got, ref, what):
     return float(err.max())
 
 
-@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+# seeded random batch layouts (sequence mix, power-of-two head groups, index
+# dimension, block size, Top-k, key padding)
+RANDOM = [(c["name"], c["q_rows"], c["kv_lens"], c["H_q"], c["H_kv"], c["topk"], c["d_idx"], c["pad"], c["bk"])
+          for c in random_layouts(31, 8, pow2_groups=True)]
+
+
+@pytest.mark.parametrize("case", CASES + RANDOM, ids=[c[0] for c in CASES + RANDOM])
 def test_kl_small(case):
     name, q_rows, kv_lens, H_q, H_kv, topk, d_idx, pad = case[:8]
     bk = case[8] if len(case) > 8 else 64

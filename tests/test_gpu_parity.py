@@ -16,7 +16,7 @@ import torch
 
 import oracle.msa_oracle as O
 from paper_2606_13392_amd import msa, synth
-from tests.util import check_block_ids, check_outputs, from_dev_bits, to_dev
+from tests.util import check_block_ids, check_outputs, from_dev_bits, random_layouts, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -71,7 +71,13 @@ def _problem(case):
     return p
 
 
-@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+# seeded random batch layouts: sequence counts and lengths, head groups,
+# index dimension, block size, Top-k and key padding drawn together
+RANDOM = [(c["name"], c["q_rows"], c["kv_lens"], c["H_q"], c["H_kv"], c["d_idx"], c["bk"], c["topk"], c["pad"], 0)
+          for c in random_layouts(11, 10)]
+
+
+@pytest.mark.parametrize("case", SMALL + RANDOM, ids=[c[0] for c in SMALL + RANDOM])
 def test_small_end_to_end(case):
     p = _problem(case)
     _say(f"[case] {p.name}")

@@ -82,3 +82,30 @@ def check_grad(got: np.ndarray, ref: np.ndarray, what=""):
         f"{what} error {err[worst]:.3e} > bound {bound[worst]:.3e} at {worst} (max|ref| {scale:.3e})"
     assert rel <= GRAD_REL_L2, f"{what} rel-L2 {rel:.3e}"
     return float(err.max() / scale), float(rel)
+
+
+def random_layouts(seed: int, n: int, *, max_seqs=4, max_kv=5000, max_q=300, pow2_groups=False):
+    """``n`` seeded batch layouts for parity sweeps beyond the hand-picked cases.
+
+    Each is a dict: per-sequence query rows and key lengths (queries are the
+    last rows of their sequence, an empty sequence allowed), head counts, index
+    dimension, block size, Top-k and, for about a third of them, a padded key
+    stride. Sizes stay where the oracle finishes in seconds."""
+    rng = np.random.default_rng(seed)
+    groups = (1, 2, 4, 8, 16) if pow2_groups else (1, 2, 3, 4, 6, 8, 16)
+    out = []
+    for i in range(n):
+        ns = int(rng.integers(1, max_seqs + 1))
+        kv = [int(v) for v in rng.integers(1, max_kv + 1, ns)]
+        q = [int(rng.integers(0, min(k, max_q) + 1)) for k in kv]
+        if sum(q) == 0:
+            q[0] = 1
+        h_kv = int(rng.choice([1, 2, 4]))
+        g = int(rng.choice(groups))
+        bk = int(rng.choice([64, 128]))
+        pad = None
+        if rng.random() < 0.35:
+            pad = ((max(kv) + 63) // 64 + int(rng.integers(0, 3))) * 64
+        out.append(dict(name=f"rand{seed}_{i}", q_rows=q, kv_lens=kv, H_q=h_kv * g, H_kv=h_kv,
+                        d_idx=int(rng.choice([64, 128])), bk=bk, topk=int(rng.integers(1, 33)), pad=pad))
+    return out
