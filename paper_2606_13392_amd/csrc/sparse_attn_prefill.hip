@@ -287,14 +287,17 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
           if (srow < qpw * G && sq_i < nq) {
             const int64_t prow_s =
                 ((static_cast<int64_t>(s_row[sq_i]) * H_kv + r) * topk + s_slot[sq_i]) * G + (srow % G);
-            *reinterpret_cast<uint4*>(o_buf + prow_s * kHeadDim + 64 * half + 8 * seg) =
-                *reinterpret_cast<const uint4*>(&sm.ost[wave][srow][(8 * seg) ^ ((srow & 7) << 3)]);
+            // nontemporal: the combine reads the partials only after the
+            // whole chunk, so caching them only evicts Q rows and K/V tiles
+            __builtin_nontemporal_store(
+                *reinterpret_cast<const u32x4*>(&sm.ost[wave][srow][(8 * seg) ^ ((srow & 7) << 3)]),
+                reinterpret_cast<u32x4*>(o_buf + prow_s * kHeadDim + 64 * half + 8 * seg));
           }
         }
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
       }
-      if (valid && h == 0) lse_buf[prow] = empty ? -INFINITY : (mm + __log2f(l)) * kLn2;
+      if (valid && h == 0) __builtin_nontemporal_store(empty ? -INFINITY : (mm + __log2f(l)) * kLn2, lse_buf + prow);
       if constexpr (BK == 64) {
 #pragma unroll
         for (int st = 0; st < KS; ++st) bq[st] = bq_next[st];
