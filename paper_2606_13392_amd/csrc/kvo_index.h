@@ -87,8 +87,10 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* __restrict__ p, 
 // segment's start) and hands out positions inside its segments with LDS
 // atomics.  A CTA whose sequences span more than kHistBins key blocks falls
 // back to one device atomic per incidence.  Positions are relative to the
-// tile; kvo_fill adds the tile offsets once the scan has run.
-constexpr int kHistRows = 4096;
+// tile; kvo_fill adds the tile offsets once the scan has run.  1024 rows per
+// CTA: a 32K-row chunk of 8 groups gives 256 CTAs (with 4096 rows, 64 CTAs
+// left most CUs idle and the kernel took 3.5x as long).
+constexpr int kHistRows = 1024;
 constexpr int kHistBins = 16384;
 
 __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
