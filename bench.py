@@ -282,8 +282,13 @@ def roofline_of(pre):
     kern = pre["kernels"]
     if not kern:
         return None
-    name = max(kern, key=lambda k: kern[k]["ms_per_step"])
-    k = kern[name]
+    return roofline_for(pre, max(kern, key=lambda k: kern[k]["ms_per_step"]))
+
+
+def roofline_for(pre, name):
+    """Roofline object of one prefill kernel: its algorithmic work per launch
+    over its event-timed launch duration, against the bound's peak."""
+    k = pre["kernels"][name]
     out = {"kernel": name, "ms_per_launch": k["ms_per_launch"], "launches_per_step": k["launches_per_step"],
            "traffic": measured_traffic(name, pre["workload"].name)}
     model = pre["models"].get(name)
@@ -689,6 +694,7 @@ def main():
                                         "tflops": att_tflops, "frac_of_bf16_peak": att_tflops / PEAK_BF16_TFLOPS},
         },
         "kernels": pre["kernels"],
+        "kernel_rooflines": {n: roofline_for(pre, n) for n in pre["kernels"] if n in pre["models"]},
         "fp8_attention": None if pre["fp8"] is None else dict(
             pre["fp8"], tflops=pre["eff_flops"] / (pre["fp8"]["ms_per_call"] * 1e-3) / 1e12,
             frac_of_bf16_peak=pre["eff_flops"] / (pre["fp8"]["ms_per_call"] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS),
