@@ -134,6 +134,7 @@ __device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][NJ], int
 // ---------------------------------------------------------------- scores, LDS
 constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
 constexpr int kPieceBlocks = 16;      // blocks per piece maximum (the Top-k's finer skip test)
+constexpr int kSurvivorCap = 1024;    // pieces per round of the Top-k's piece scan
 
 // One 16-byte piece per lane from global memory straight into LDS
 // (global_load_lds_dwordx4): lane l writes bytes [16 l, 16 l + 16) after the
@@ -617,7 +618,8 @@ __device__ __forceinline__ uint64_t scan_row_batched(Load load, int nscan, KeyBa
 // skipped and scores below t0 are never ranked.  Surviving pieces are read
 // four per wave load (lanes 16 k .. 16 k + 15 take the k-th).
 template <typename Load, typename LoadCm, typename LoadPm>
-__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, LoadPm pm, int nscan, KeyBatch& kb) {
+__device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, LoadPm pm, int nscan, KeyBatch& kb,
+                                                    int32_t* surv) {
   const int lane = lane_id();
   const int K1 = kb.K1;
   const int nchunk = (nscan + kWave - 1) / kWave;
@@ -628,61 +630,68 @@ __device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, LoadPm
   const uint64_t floor_key = o0 > 0 ? (static_cast<uint64_t>(o0) << 32) - 1 : 0ull;
 
   const int npiece = (nscan + kPieceBlocks - 1) / kPieceBlocks;
-  int g = 0;
-  uint64_t mask = 0;
-  bool more = true;
-  // next piece whose maximum reaches t0 (wave-uniform), or -1
-  auto next_piece = [&]() -> int {
-    while (mask == 0) {
-      if (!more) return -1;
-      const int c = kWave * g + lane;
-      mask = __ballot(c < npiece && ordered_u32(pm(c)) >= o0);
-      ++g;
-      more = kWave * g < npiece;
-    }
-    const int j = __ffsll(static_cast<unsigned long long>(mask)) - 1;
-    mask &= mask - 1;
-    return kWave * (g - 1) + j;
-  };
-  // this lane's piece of the next four (-1 past the last)
-  auto next_quad = [&]() -> int {
-    int mine = -1;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int pc = next_piece();
-      if ((lane >> 4) == k) mine = pc;
-    }
-    return mine;
-  };
   kb.list = 0;
   kb.cnt = 0;
   uint64_t tau = floor_key;
-  constexpr int kAhead = 4;
-  int lp[kAhead];
-  float pf[kAhead];
+  // pieces in rounds of kSurvivorCap: the round's piece maxima are loaded
+  // together, the indices of the pieces that reach t0 appended to the wave's
+  // LDS list in piece order, then their scores read four pieces per wave load
+  // (lanes 16 k .. 16 k + 15 take the k-th) with kAhead loads in flight
+  constexpr int kGroups = kSurvivorCap / kWave;
+  for (int r0 = 0; r0 < npiece; r0 += kSurvivorCap) {
+    float pv[kGroups];
 #pragma unroll
-  for (int a = 0; a < kAhead; ++a) {
-    lp[a] = next_quad();
-    const int b = lp[a] * kPieceBlocks + (lane & 15);
-    pf[a] = (lp[a] >= 0 && b < nscan) ? load(b) : 0.f;
-  }
-  // the quad's first piece is lane 0's: once it is -1 every piece is
-  while (__builtin_amdgcn_readfirstlane(lp[0]) >= 0) {
-    const int b = lp[0] * kPieceBlocks + (lane & 15);
-    const bool ok = lp[0] >= 0 && b < nscan;
-    const float x = pf[0];
+    for (int k = 0; k < kGroups; ++k) {
+      const int c = r0 + kWave * k + lane;
+      pv[k] = c < npiece ? pm(c) : 0.f;
+    }
+    int ns = 0;
 #pragma unroll
-    for (int a = 0; a + 1 < kAhead; ++a) {
-      lp[a] = lp[a + 1];
-      pf[a] = pf[a + 1];
+    for (int k = 0; k < kGroups; ++k) {
+      const int c = r0 + kWave * k + lane;
+      const bool ok = c < npiece && ordered_u32(pv[k]) >= o0;
+      const uint64_t m = __ballot(ok);
+      if (ok)
+        surv[ns + __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32),
+                                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0))] = c;
+      ns += __popcll(m);
     }
-    lp[kAhead - 1] = next_quad();
-    {
-      const int bn = lp[kAhead - 1] * kPieceBlocks + (lane & 15);
-      pf[kAhead - 1] = (lp[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const int nquad = (ns + 3) / 4;
+    auto quad_piece = [&](int i) -> int {
+      const int q = 4 * i + (lane >> 4);
+      return i < nquad && q < ns ? surv[q] : -1;
+    };
+    constexpr int kAhead = 4;
+    int lp[kAhead];
+    float pf[kAhead];
+#pragma unroll
+    for (int a = 0; a < kAhead; ++a) {
+      lp[a] = quad_piece(a);
+      const int b = lp[a] * kPieceBlocks + (lane & 15);
+      pf[a] = (lp[a] >= 0 && b < nscan) ? load(b) : 0.f;
     }
-    const uint64_t v = ok ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
-    tau = kb.push(v, tau);
+    for (int i = 0; i < nquad; ++i) {
+      const int b = lp[0] * kPieceBlocks + (lane & 15);
+      const bool ok = lp[0] >= 0 && b < nscan;
+      const float x = pf[0];
+#pragma unroll
+      for (int a = 0; a + 1 < kAhead; ++a) {
+        lp[a] = lp[a + 1];
+        pf[a] = pf[a + 1];
+      }
+      lp[kAhead - 1] = quad_piece(i + kAhead);
+      {
+        const int bn = lp[kAhead - 1] * kPieceBlocks + (lane & 15);
+        pf[kAhead - 1] = (lp[kAhead - 1] >= 0 && bn < nscan) ? load(bn) : 0.f;
+      }
+      const uint64_t v = ok ? rank_key(x, static_cast<uint32_t>(b)) : 0ull;
+      tau = kb.push(v, tau);
+    }
+    // the next round rewrites the list
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   kb.flush();
   return kb.list;
@@ -746,6 +755,7 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
     const int32_t* __restrict__ unit_off, int H_kv, int qr, int U, int rpu, int64_t u0, int64_t u1, int BK,
     int topk, int32_t* __restrict__ block_ids) {
   __shared__ uint64_t s_pend[kWaves][2 * kWave];
+  __shared__ int32_t s_surv[kWaves][kSurvivorCap];
   const int lane = lane_id();
   const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
   if (task >= (u1 - u0) * rpu) return;
@@ -766,7 +776,7 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
     auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
     const float* pmrow = PM + t.slot;
     auto pm = [=](int q) { return pmrow[static_cast<int64_t>(q) * cm_stride]; };
-    list = scan_row_pruned(load, cm, pm, t.nscan, kb);
+    list = scan_row_pruned(load, cm, pm, t.nscan, kb, s_surv[threadIdx.x / kWave]);
   } else {
     list = scan_row_batched(load, t.nscan, kb);
   }
