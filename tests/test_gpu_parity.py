@@ -74,7 +74,8 @@ def _problem(case):
 # seeded random batch layouts: sequence counts and lengths, head groups,
 # index dimension, block size, Top-k and key padding drawn together
 RANDOM = [(c["name"], c["q_rows"], c["kv_lens"], c["H_q"], c["H_kv"], c["d_idx"], c["bk"], c["topk"], c["pad"], 0)
-          for c in random_layouts(11, 10)]
+          for c in random_layouts(11, 10) + random_layouts(41, 5, max_seqs=2, max_kv=60000, max_q=120,
+                                                           topk_range=(33, 65))]
 
 
 @pytest.mark.parametrize("case", SMALL + RANDOM, ids=[c[0] for c in SMALL + RANDOM])

@@ -84,7 +84,7 @@ def check_grad(got: np.ndarray, ref: np.ndarray, what=""):
     return float(err.max() / scale), float(rel)
 
 
-def random_layouts(seed: int, n: int, *, max_seqs=4, max_kv=5000, max_q=300, pow2_groups=False):
+def random_layouts(seed: int, n: int, *, max_seqs=4, max_kv=5000, max_q=300, pow2_groups=False, topk_range=(1, 33)):
     """``n`` seeded batch layouts for parity sweeps beyond the hand-picked cases.
 
     Each is a dict: per-sequence query rows and key lengths (queries are the
@@ -107,5 +107,5 @@ def random_layouts(seed: int, n: int, *, max_seqs=4, max_kv=5000, max_q=300, pow
         if rng.random() < 0.35:
             pad = ((max(kv) + 63) // 64 + int(rng.integers(0, 3))) * 64
         out.append(dict(name=f"rand{seed}_{i}", q_rows=q, kv_lens=kv, H_q=h_kv * g, H_kv=h_kv,
-                        d_idx=int(rng.choice([64, 128])), bk=bk, topk=int(rng.integers(1, 33)), pad=pad))
+                        d_idx=int(rng.choice([64, 128])), bk=bk, topk=int(rng.integers(*topk_range)), pad=pad))
     return out
