@@ -140,14 +140,6 @@ def layout_of(problem) -> Layout:
 # --------------------------------------------------------------------------
 # Index Branch (Sec. 3.1)
 # --------------------------------------------------------------------------
-def index_dots(iq_row: np.ndarray, ik: np.ndarray) -> np.ndarray:
-    """Unscaled index dot products q_idx^(r)_i . k_idx_j for every group r.
-
-    iq_row: (H_kv, d_idx) float64, ik: (n, d_idx) float64 -> (H_kv, n) float64.
-    bf16 x bf16 products are exact in float64; the sum is float64."""
-    return iq_row @ ik.T
-
-
 def block_maxima(dots_row: np.ndarray, pos: int, block_size: int) -> np.ndarray:
     """Causal block max-pool of one (row, group): M_b over blocks
     b = 0 .. ceil(n / B_k) - 1 of the visible prefix j <= pos; blocks whose

@@ -151,6 +151,70 @@ def pin_selection_invariants(O, seed=3):
                 assert abs((min(sc[b] for b in nl) - max(sc[b] for b in un)) - gaps[i, g]) < 1e-5
 
 
+def pin_tie_rule_validator(O):
+    """The tie rule for selections that differ from the oracle's (Sec. 3.1
+    top-k equation; a set is correct when it keeps the local block, has
+    min(k, lb+1) distinct causal ids in ascending order with -1 padding, and
+    no unselected candidate beats a selected one by more than the tolerance).
+    Hand-built sets with known verdicts."""
+    B, tol = 4, 1e-3
+    pos = 6 * B + 2                    # lb = 6; candidates 0..5
+    # scaled block scores: ranking 1 > 3 > 5 > 0 > 4 > 2 (the local block 6 is
+    # forced; its score plays no part)
+    sc = np.array([4.0, 9.0, 1.0, 8.0, 3.0, 6.0, -50.0])
+    V = lambda ids, k=4, scores=sc, p=pos: O.selection_is_valid(np.array(ids, dtype=np.int32), scores, p, B, k, tol)
+    assert V([1, 3, 5, 6])                          # the oracle's own set
+    assert not V([1, 3, 5, -1])                     # local block missing, padded
+    assert not V([0, 1, 3, 5])                      # local block missing, full size, dominant
+    assert not V([1, 3, 6, -1])                     # too few
+    assert V([0, 1, 3, 5, 6], k=5)                  # k = 5 takes block 0 too
+    assert not V([1, 3, 5, 6, -1], k=5)             # ... and needs five ids
+    assert not V([1, 1, 3, 6])                      # duplicate id
+    assert not V([3, 1, 5, 6])                      # not ascending
+    assert not V([1, 3, 5, 7])                      # id past the local block (and no lb)
+    assert not V([1, 3, 6, 7])                      # id past the local block
+    assert not V([1, 3, 6, -2])                     # padding other than -1
+    assert not V([1, 2, 5, 6])                      # 2 (score 1) kept over 3 (score 8): beyond tol
+    # k = 3: scores 9, 8 pick {1, 3}; a swap 3 <-> 5 within the tolerance is accepted
+    near = sc.copy(); near[5] = 8.0 - 0.5 * tol
+    assert V([1, 5, 6], k=3, scores=near) and V([1, 3, 6], k=3, scores=near)
+    far = sc.copy(); far[5] = 8.0 - 2.0 * tol
+    assert V([1, 3, 6], k=3, scores=far) and not V([1, 5, 6], k=3, scores=far)
+    # fewer candidates than k - 1: everything is selected, padded
+    assert V([0, 1, 2, -1], k=4, p=2 * B + 1)
+    assert not V([0, 2, -1, -1], k=4, p=2 * B + 1)
+    assert not V([0, 1, 2, -2], k=4, p=2 * B + 1)    # padding other than -1, size right
+    # k = 1: the local block alone
+    assert V([6], k=1) and not V([5], k=1)
+
+
+def pin_row_block_scores(O, seed=43):
+    """Block scores the tie rule judges with, against a per-token loop
+    (chunked layout with a padded key side, ragged local block)."""
+    rng = np.random.default_rng(seed)
+    B, d, H_kv = 8, 16, 2
+    kv_lens, q_rows, starts = [45, 70], [5, 9], [0, 48]
+    ik = _bits(rng.standard_normal((120, d)))
+    iq = _bits(rng.standard_normal((sum(q_rows), H_kv, d)))
+    lay = O.Layout(q_rows, kv_lens, starts)
+    ikv, iqv = _vals(ik), _vals(iq)
+    for row in range(sum(q_rows)):
+        s = 0 if row < q_rows[0] else 1
+        pos = kv_lens[s] - q_rows[s] + (row - (0 if s == 0 else q_rows[0]))
+        for g in range(H_kv):
+            got = O.row_block_scores(iq, ik, lay, row, g, B)
+            for b in range(len(got)):
+                best = -math.inf
+                for j in range(b * B, min((b + 1) * B, pos + 1)):
+                    dot = 0.0
+                    for e in range(d):
+                        dot += iqv[row, g, e] * ikv[starts[s] + j, e]
+                    best = max(best, dot / math.sqrt(d))
+                assert (math.isinf(best) and math.isinf(got[b])) or abs(got[b] - best) < 1e-12, \
+                    (row, g, b, got[b], best)
+            assert len(got) == (pos + B) // B       # blocks up to the local one
+
+
 def pin_block_maxima_partial(O):
     """Partial last block (Sec. 2.3) and the causal cut inside the local block."""
     rng = np.random.default_rng(11)
@@ -546,7 +610,8 @@ def pin_kl_mixture_closed_form(O):
 
 
 ALL_PINS = [pin_flops_ratio, pin_effective_flops_dense, pin_brute_force_selection,
-            pin_planted_closed_form, pin_selection_invariants, pin_block_maxima_partial,
+            pin_planted_closed_form, pin_selection_invariants, pin_tie_rule_validator,
+            pin_row_block_scores, pin_block_maxima_partial,
             pin_dense_equality, pin_closed_forms, pin_combine,
             pin_decode_and_chunked_consistency, pin_head_permutation,
             pin_fp8_e4m3_codes, pin_fp8_attention_scales,

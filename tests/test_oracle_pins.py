@@ -47,6 +47,23 @@ MUTATIONS = {
     "kl_reverse_direction": ("kl = float(np.sum(p * (np.log(p) - np.log(p_idx))))",
                              "kl = float(np.sum(p_idx * (np.log(p_idx) - np.log(p))))"),
     "kl_dq_unscaled": ("d_iq = (ds @ ik_toks) * scale_idx", "d_iq = (ds @ ik_toks)"),
+    "tie_rule_dominance_flipped": (
+        "return min(block_scores[b] for b in nonlocal_sel) >= max(block_scores[b] for b in unsel) - tol",
+        "return max(block_scores[b] for b in unsel) >= min(block_scores[b] for b in nonlocal_sel) - tol"),
+    "tie_rule_tolerance_sign": (
+        "return min(block_scores[b] for b in nonlocal_sel) >= max(block_scores[b] for b in unsel) - tol",
+        "return min(block_scores[b] for b in nonlocal_sel) >= max(block_scores[b] for b in unsel) + tol"),
+    "tie_rule_local_not_checked": ("len(sel) != min(topk, lb + 1) or lb not in sel:",
+                                   "len(sel) != min(topk, lb + 1):"),
+    "tie_rule_padding_not_checked": ("or any(int(b) != -1 for b in ids[len(sel):])", "or False"),
+    "tie_rule_order_not_checked": ("if list(ids[:len(sel)]) != sorted(sel) or", "if"),
+    "tie_rule_past_local_allowed": ("if any(b < 0 or b > lb for b in sel):", "if any(b < 0 for b in sel):"),
+    "row_scores_unscaled": ("return block_maxima(d, pos, block_size) / math.sqrt(iq.shape[0])",
+                            "return block_maxima(d, pos, block_size)"),
+    "row_scores_causal_cut": ("ik = decode_bf16(index_k_bits[kv0:kv0 + pos + 1])\n    iq = decode_bf16(index_q_bits[row, group])",
+                              "ik = decode_bf16(index_k_bits[kv0:kv0 + pos])\n    iq = decode_bf16(index_q_bits[row, group])"),
+    "row_scores_no_kv_start": ("ik = decode_bf16(index_k_bits[kv0:kv0 + pos + 1])\n    iq = decode_bf16(index_q_bits[row, group])",
+                               "ik = decode_bf16(index_k_bits[0:pos + 1])\n    iq = decode_bf16(index_q_bits[row, group])"),
     "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
                              "O[i, g::H_kv], L[i, g::H_kv] = attend(\n                qf[g::H_kv], keys, vals, scale)"),
 }
