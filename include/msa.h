@@ -31,9 +31,12 @@
  *   matching *_workspace_size() query; the workspace is free again once the
  *   stream has executed the call.  Calls that share a workspace must be ordered
  *   on one stream.
- * - Apart from the opt-in kernel timing at the end of this header, the
- *   library keeps no global state; concurrent calls from several host threads
- *   are safe when they use distinct outputs and workspaces.
+ * - Global state: the opt-in kernel timing at the end of this header, the
+ *   grid size of each persistent kernel (derived from the device's occupancy
+ *   on first use and cached in an atomic), and the device-resident scratch of
+ *   msa_index_topk_noalloc.  Concurrent calls from several host threads are
+ *   safe when they use distinct outputs and workspaces (the no-allocation
+ *   entry point has its own rule).
  * - NaN or Inf inputs give unspecified (but memory-safe) results.
  *
  * Sequence layout (struct msa_seqs)
@@ -321,7 +324,8 @@ int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void*
  *   msa_profile_enable(on)   on != 0 starts recording for later calls, 0 stops.
  *   msa_profile_reset()      forgets the launches recorded so far.
  *   msa_profile_kernel_name(i)  name of the i-th kernel seen since load, or
- *                            NULL past the last one (static until unload).
+ *                            NULL past the last one; the string stays valid
+ *                            until the library is unloaded.
  *   msa_profile_read(name, &launches, &total_ms)  launches of `name` since the
  *                            last reset and their summed event-to-event time;
  *                            waits for those events; unknown names read 0.

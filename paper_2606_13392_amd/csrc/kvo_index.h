@@ -15,6 +15,7 @@
 #pragma once
 
 #include <algorithm>
+#include <atomic>
 
 #include "msa_common.h"
 #include "msa_profile.h"
@@ -25,6 +26,9 @@ using namespace msa;
 
 constexpr int kHeadDim = 128;
 constexpr int kItemQueries = 256;      // queries of one tile per work item
+// A handle packs (row in chunk << 6 | slot) into 32 bits, so a chunk holds at
+// most 2^26 query rows; the plans cap their chunks there.
+constexpr int64_t kMaxChunkRows = int64_t(1) << 26;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
@@ -262,19 +266,23 @@ __device__ __forceinline__ int64_t upper_index(const T* __restrict__ arr, int64_
   return lo;
 }
 
-// CTAs of a persistent kernel: every CU filled to the kernel's occupancy.
+// CTAs of a persistent kernel: every CU filled to the kernel's occupancy.  The
+// value is cached per kernel instance; concurrent first calls may both compute
+// it, and the atomic makes their stores and loads well defined.
 template <typename K>
-int persistent_ctas(K kernel, int threads, int* cache) {
-  if (*cache == 0) {
+int persistent_ctas(K kernel, int threads, std::atomic<int>* cache) {
+  int n = cache->load(std::memory_order_relaxed);
+  if (n == 0) {
     int dev = 0, cus = 256, per_cu = 1;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
       cus = 256;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess || per_cu < 1)
       per_cu = 1;
-    *cache = cus * per_cu;
+    n = cus * per_cu;
+    cache->store(n, std::memory_order_relaxed);
   }
-  return *cache;
+  return n;
 }
 // Block ids of B_k = 64 f from ids of blocks of 64 f keys: block b becomes its
 // f sub-blocks f b .. f b + f - 1 (ascending order and -1 padding kept), so a

@@ -3,6 +3,7 @@
 // touches it unless timing is enabled).
 #include <atomic>
 #include <cstring>
+#include <deque>
 #include <mutex>
 #include <string>
 #include <vector>
@@ -25,7 +26,9 @@ struct Entry {
 
 std::atomic<bool> g_enabled{false};
 std::mutex g_mu;
-std::vector<Entry> g_entries;
+// a deque never moves its elements when it grows, so the name pointers that
+// msa_profile_kernel_name hands out stay valid until the library is unloaded
+std::deque<Entry> g_entries;
 
 Entry* find(const char* name) {
   for (auto& e : g_entries)

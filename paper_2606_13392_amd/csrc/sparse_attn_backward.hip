@@ -486,7 +486,8 @@ int make_bwd_plan(const msa_seqs* seqs, int H_q, int H_kv, int topk, size_t budg
   if (pl->ntile >= (int64_t(1) << 31) - 1) return MSA_ERR_UNSUPPORTED;
   pl->nscan = static_cast<int>((pl->ntile + kScanPerBlock - 1) / kScanPerBlock);
   if (pl->nscan > 1024 * 64) return MSA_ERR_UNSUPPORTED;
-  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  const int64_t max_rows =
+      std::min(kMaxChunkRows, ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk));
   int64_t rows = std::max<int64_t>(1, seqs->total_q_rows);
   rows = std::min(rows, max_rows);
   pl->chunk_rows = rows;
@@ -569,7 +570,7 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
     msa_prof::launch("bwd_delta_kernel", bwd_delta_kernel, dim3(static_cast<unsigned>((pairs * 16 + 255) / 256)),
                      dim3(256), 0, stream, static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(d_o), pairs,
                      delta);
-  static int ctas = 0;
+  static std::atomic<int> ctas {0};
   const int nctas = persistent_ctas(bwd_kvo_kernel, kBwdThreads, &ctas);
   const float sl2 = softmax_scale * kLog2e;
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {

@@ -484,7 +484,8 @@ int make_kvo_plan(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk, siz
     rows = 0;
   }
   // incidences of a chunk must fit the int32 offsets
-  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  const int64_t max_rows =
+      std::min(kMaxChunkRows, ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk));
   if (rows > max_rows) rows = max_rows;
   if (rows < 1) return MSA_ERR_WORKSPACE;
   pl->chunk_rows = rows;
@@ -513,7 +514,7 @@ void launch_kvo_attn(const void* q, const void* k, const void* v, const msa_seqs
                      const int32_t* tile_off, const int32_t* item_off, const uint32_t* handles, int H_q, int H_kv,
                      int topk, int64_t nbcap, int64_t r0, float sl2, float o_scale, uint16_t* o_buf, float* lse_buf,
                      int32_t* next_item, hipStream_t stream) {
-  static int ctas = 0;
+  static std::atomic<int> ctas {0};
   constexpr int threads = 64 * kvo_waves<BK>();
   msa_prof::launch("kvo_attn_kernel", kvo_attn_kernel<BK, T>,
                    dim3(persistent_ctas(kvo_attn_kernel<BK, T>, threads, &ctas)), dim3(threads), 0, stream,

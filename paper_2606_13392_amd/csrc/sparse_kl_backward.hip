@@ -640,7 +640,8 @@ int make_kl_plan(const msa_seqs* seqs, int H_kv, int D, int topk, size_t budget,
   if (pl->ntile >= (int64_t(1) << 31) - 1 || pl->nbcap >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   pl->nscan = static_cast<int>((pl->ntile + kScanPerBlock - 1) / kScanPerBlock);
   if (pl->nscan > 1024 * 64) return MSA_ERR_UNSUPPORTED;
-  const int64_t max_rows = ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk);
+  const int64_t max_rows =
+      std::min(kMaxChunkRows, ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk));
   const int64_t all = std::max<int64_t>(1, seqs->total_q_rows);
   pl->chunk_rows = std::min(all, max_rows);
   kl_layout(*pl, seqs, H_kv, D, topk);
@@ -718,7 +719,7 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                    blk_base);
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
                    reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
-  static int ctas_lse = 0, ctas_grad = 0;
+  static std::atomic<int> ctas_lse {0}, ctas_grad {0};
   const int n_lse = persistent_ctas(kl_lse_kernel<D>, kKlThreads, &ctas_lse);
   const int n_grad = persistent_ctas(kl_grad_wave_kernel<D, 3>, kKlThreads, &ctas_grad);
   const int lg_g = __builtin_ctz(static_cast<unsigned>(H_q / H_kv));

@@ -131,3 +131,71 @@ def test_profile_api_without_launches():
     assert L.msa_profile_read(b"no_such_kernel", None, ctypes.byref(ms)) != 0
     assert L.msa_profile_enable(0) == 0
     assert msa.profile_read() == {} or all(v[0] > 0 for v in msa.profile_read().values())
+
+
+def _all_queries(L, s):
+    r = ctypes.byref(s)
+    return (L.msa_index_topk_workspace_size(r, 2, 64, 64, 8),
+            L.msa_index_topk_workspace_size(r, 4, 128, 128, 16),
+            L.msa_sparse_attn_prefill_workspace_size(r, 8, 2, 128, 64, 8),
+            L.msa_sparse_attn_decode_workspace_size(r, 8, 2, 128, 64, 8),
+            L.msa_dense_attn_workspace_size(r, 8, 2, 128),
+            L.msa_sparse_attn_backward_workspace_size(r, 8, 2, 128, 64, 8),
+            L.msa_sparse_kl_backward_workspace_size(r, 8, 2, 64, 128, 64, 8))
+
+
+def _all_rejections(L, s):
+    r = ctypes.byref(s)
+    return (L.msa_index_topk(8, 8, r, 3, 64, 64, 8, 8, 8, 1 << 20, None),
+            L.msa_index_topk(8, 8, r, 2, 64, 64, 8, None, 8, 1 << 20, None),
+            L.msa_index_topk(8, 8, r, 2, 64, 64, 8, 8, 8, 8, None),
+            L.msa_sparse_attn_prefill(8, 8, 8, 8, r, 6, 4, 128, 64, 8, 0.1, 8, 8, 8, 1 << 30, None),
+            L.msa_sparse_attn_decode(8, 8, 8, 8, r, 8, 2, 64, 64, 8, 0.1, 8, 8, 8, 1 << 30, None),
+            L.msa_strerror(msa.MSA_ERR_HIP))
+
+
+def test_host_calls_from_many_threads():
+    """Workspace queries and host-side rejections give the same answers when
+    8 host threads make them at once (ctypes drops the GIL around each call)."""
+    import threading
+    L = msa.lib()
+    layouts = [_seqs(), _seqs(num_seqs=4, total_q_rows=4, max_q_rows=1),
+               _seqs(total_q_rows=5000, total_kv_rows=5000, max_q_rows=5000, max_kv_len=5000)]
+    want = [(_all_queries(L, s), _all_rejections(L, s)) for s in layouts]
+    errors = []
+
+    def work(t):
+        try:
+            for it in range(300):
+                i = (t + it) % len(layouts)
+                got = (_all_queries(L, layouts[i]), _all_rejections(L, layouts[i]))
+                if got != want[i]:
+                    errors.append((t, it, got, want[i]))
+                    return
+        except Exception as e:   # surfaced below
+            errors.append((t, repr(e)))
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(8)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    assert not errors, errors[:2]
+
+
+def test_chunks_stay_within_the_handle_row_field():
+    """A reverse-index handle keeps the row inside its chunk in 26 bits, so a
+    chunk never exceeds 2^26 rows even where the workspace would allow more
+    (one KV head, Top-k 1: H_kv * topk < 32).  Twice the rows then need no
+    more workspace, since both plans use chunks of 2^26 rows (the backward
+    also keeps D = dO . O for every row: 4 bytes per row and head)."""
+    L = msa.lib()
+    big = 1 << 27
+    a = _seqs(total_q_rows=1 << 26, total_kv_rows=big, max_q_rows=1 << 26, max_kv_len=big)
+    b = _seqs(total_q_rows=big, total_kv_rows=big, max_q_rows=big, max_kv_len=big)
+    for fn, args, per_row in ((L.msa_sparse_attn_prefill_workspace_size, (1, 1, 128, 64, 1), 0),
+                              (L.msa_sparse_attn_backward_workspace_size, (1, 1, 128, 64, 1), 4),
+                              (L.msa_sparse_kl_backward_workspace_size, (1, 1, 64, 128, 64, 1), 0)):
+        na, nb = fn(ctypes.byref(a), *args), fn(ctypes.byref(b), *args)
+        assert na > 0 and nb > 0
+        assert nb - na == per_row * (big - (1 << 26)), (fn.__name__, na, nb)
