@@ -33,10 +33,8 @@
  *   on one stream.
  * - Global state: the opt-in kernel timing at the end of this header, the
  *   grid size of each persistent kernel (derived from the device's occupancy
- *   on first use and cached in an atomic), and the device-resident scratch of
- *   msa_index_topk_noalloc.  Concurrent calls from several host threads are
- *   safe when they use distinct outputs and workspaces (the no-allocation
- *   entry point has its own rule).
+ *   on first use and cached in an atomic).  Concurrent calls from several host
+ *   threads are safe when they use distinct outputs and workspaces.
  * - NaN or Inf inputs give unspecified (but memory-safe) results.
  *
  * Sequence layout (struct msa_seqs)
