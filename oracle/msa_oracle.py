@@ -192,24 +192,32 @@ def select_blocks(index_q_bits: np.ndarray, index_k_bits: np.ndarray, layout: La
     inv_sqrt = 1.0 / math.sqrt(d_idx)
     ids = np.full((len(rows), H_kv, topk), -1, dtype=np.int32)
     gaps = np.full((len(rows), H_kv), math.inf)
-    # group the requested rows by sequence so each batch shares its keys
+    # group the requested rows by sequence so each batch shares its keys, in
+    # order of position so a batch's rows need keys up to similar depths
     by_seq = {}
     for i, r in enumerate(rows):
         s, pos = layout.locate(r)
         by_seq.setdefault(s, []).append((i, r, pos))
     for s, items in by_seq.items():
+        items.sort(key=lambda it: it[2])
         kv0, kvl = layout.kv_starts[s], layout.kv_lens[s]
-        for b0 in range(0, len(items), batch_rows):
-            batch = items[b0:b0 + batch_rows]
+        b0 = 0
+        while b0 < len(items):
+            # at most ~2 GiB of float64 dot products per batch
+            n_keys = min(kvl, items[min(len(items), b0 + batch_rows) - 1][2] + 1)
+            nb = max(1, min(batch_rows, (1 << 31) // max(1, 8 * H_kv * n_keys)))
+            batch = items[b0:b0 + nb]
+            b0 += nb
             pmax = max(pos for _, _, pos in batch)
             ik = decode_bf16(index_k_bits[kv0:kv0 + min(kvl, pmax + 1)])
             iq = decode_bf16(index_q_bits[[r for _, r, _ in batch]])      # (B, H_kv, d)
-            dots = np.einsum("bhd,nd->bhn", iq, ik, optimize=True)        # float64
+            # float64 dot products of every (row, group) with every key
+            dots = (iq.reshape(-1, d_idx) @ ik.T).reshape(len(batch), H_kv, -1)
+            dots32 = dots.astype(np.float32)
             for j, (i, r, pos) in enumerate(batch):
                 for g in range(H_kv):
-                    d = dots[j, g]
-                    m_rank = block_maxima(d.astype(np.float32), pos, block_size)
-                    m_scaled = block_maxima(d, pos, block_size) * inv_sqrt
+                    m_rank = block_maxima(dots32[j, g], pos, block_size)
+                    m_scaled = block_maxima(dots[j, g], pos, block_size) * inv_sqrt
                     ids[i, g], gaps[i, g] = select_row(m_rank, m_scaled, pos, block_size, topk)
     return ids, gaps
 
