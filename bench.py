@@ -579,14 +579,15 @@ def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev, blocks_per_
 
 
 def cpu_baseline(pre, args):
-    """The CPU oracle on a bounded random sample of query rows (host cores)."""
+    """The CPU oracle on a bounded sample of query rows spread evenly over
+    depth (host cores); the full-problem time is extrapolated from it."""
     import numpy as np
     import torch
     import oracle.msa_oracle as O
+    from paper_2606_13392_amd import synth
     p = pre["workload"]
     d = pre["inputs"]
-    rng = np.random.default_rng(12345)
-    rows = sorted(int(r) for r in rng.choice(p.total_q_rows, size=args.cpu_sample_rows, replace=False))
+    rows = synth.stratified_rows(p, args.cpu_sample_rows, seed=12345)
     to_np = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     # query-side rows the sample needs (np.zeros commits only the pages written)
     sel = torch.tensor(rows, device=d["q"].device)
@@ -608,14 +609,18 @@ def cpu_baseline(pre, args):
     ids, _ = O.select_blocks(iq, ik, lay, p.block_size, p.topk, rows=rows, batch_rows=16)
     O.sparse_attention(q, k, v, ids, lay, p.block_size, rows=rows, block_ids_are_for_rows=True)
     dt = time.perf_counter() - t0
+    full_s = dt * p.total_q_rows / len(rows)
     return {
         "value": len(rows) / dt,
         "unit": "tok/s",
         "cores": min(cores, blas_threads) if blas_threads > 1 else 1,
         "kind": "oracle",
-        "sample": f"{len(rows)} random query rows of {p.name} (all {p.num_kv_heads} groups, "
-                  f"{p.num_q_heads} heads), index selection + sparse attention, fp64 numpy; "
-                  f"{dt:.1f} s; host has {cores} cores, BLAS threads {blas_threads}",
+        "sample": f"{len(rows)} query rows of {p.name} stratified over depth (one per equal band, plus the first "
+                  f"two blocks' rows and the last row; all {p.num_kv_heads} groups, {p.num_q_heads} heads), "
+                  f"index selection + sparse attention, fp64 numpy; {dt:.1f} s; host has {cores} cores, "
+                  f"BLAS threads {blas_threads}",
+        "extrapolated_full_s": full_s,
+        "extrapolated_note": f"extrapolated: all {p.total_q_rows} rows at the sample's mean time per row",
     }
 
 
@@ -634,7 +639,7 @@ def main():
                     help="shape of the training step (forward + Main Branch backward + KL backward)")
     ap.add_argument("--train-steps", type=int, default=3)
     ap.add_argument("--no-train", action="store_true")
-    ap.add_argument("--cpu-sample-rows", type=int, default=160)
+    ap.add_argument("--cpu-sample-rows", type=int, default=300)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
     ap.add_argument("--fp8", action="store_true",

@@ -166,9 +166,9 @@ class Seqs:
 
 
 def _workspace(nbytes: int, device, ws: Optional[torch.Tensor]) -> Optional[torch.Tensor]:
-    if nbytes == 0:
-        return ws
-    if ws is not None and ws.numel() * ws.element_size() >= nbytes:
+    """The caller's workspace as given (a call runs in chunks sized to it and
+    reports MSA_ERR_WORKSPACE below its minimum), else one of the queried size."""
+    if ws is not None or nbytes == 0:
         return ws
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 

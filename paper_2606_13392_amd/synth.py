@@ -194,6 +194,33 @@ WORKLOADS = ["prefill_4k", "prefill_32k", "decode_128k", "prefill_1m", "chunked_
 WORKLOADS_BK128 = ["prefill_1m_bk128", "decode_128k_bk128", "prefill_32k_bk128"]
 
 
+def stratified_rows(p: Problem, n: int, seed: int) -> List[int]:
+    """About ``n`` packed query rows spread over every depth, for checks and
+    baselines that cannot afford every row: each sequence's rows are cut into
+    equal bands (a count proportional to its rows) and one row is drawn per
+    band; each sequence's first rows (its first two key blocks' worth) and its
+    last row are always included.  Sorted, distinct."""
+    rng = np.random.default_rng([seed, 99])
+    T = p.total_q_rows
+    out = set()
+    for s in range(p.num_seqs):
+        a, b = p.q_offsets[s], p.q_offsets[s + 1]
+        if b <= a:
+            continue
+        m = b - a
+        bands = max(1, min(m, round(n * m / max(T, 1))))
+        edges = np.linspace(a, b, bands + 1).astype(np.int64)
+        for lo, hi in zip(edges[:-1], edges[1:]):
+            if hi > lo:
+                out.add(int(rng.integers(lo, hi)))
+        B = p.block_size
+        for off in (0, 1, B - 1, B, B + 1, 2 * B - 1):
+            if off < m:
+                out.add(a + off)
+        out.add(b - 1)
+    return sorted(out)
+
+
 # --------------------------------------------------------------------------
 # numpy backend (row addressable)
 # --------------------------------------------------------------------------

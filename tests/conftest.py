@@ -11,3 +11,11 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: long-running case")
+
+
+def pytest_terminal_summary(terminalreporter):
+    from tests.util import OUTPUT_TALLY as t
+    if t["calls"]:
+        terminalreporter.write_line(
+            f"output comparisons: {t['calls']} calls, {t['elements']} O elements, {t['over']} beyond 1e-2 "
+            f"(worst {t['worst']:.4f})")

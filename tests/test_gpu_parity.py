@@ -172,6 +172,51 @@ def test_workspace_rejected_when_small():
     assert bool((out == 7).all())          # nothing was launched
 
 
+def test_forward_small_workspaces_run_several_chunks():
+    """Workspaces far below the one-chunk size: the index call runs its rows in
+    many unit chunks and the attention call in several row chunks (reverse
+    index, partials and combine per chunk).  Results equal the one-chunk run
+    bit for bit and the oracle within the bars."""
+    p = _problem(("chunked_ws_small", [130, 64, 1, 257, 700], [700, 64, 900, 1500, 2000], 16, 4, 64, 64, 6,
+                  None, 0))
+    _say(f"[case] {p.name}")
+    x = synth.generate_numpy(p)
+    lay = O.layout_of(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    ids0 = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    o0, l0 = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids0, seqs, p.block_size)
+    z = _plan_sizes(p)
+    ws_i = z["hdr"] + 2 * z["unit_bytes"]
+    ws_a = z["fixed"] + 4 * 256 + (p.total_q_rows // 5) * z["prb"]
+    idx_starts, attn_starts = _launch_row_starts(p, ws_i, ws_a)
+    wi = torch.empty(ws_i, dtype=torch.uint8, device=dev)
+    wa = torch.empty(ws_a, dtype=torch.uint8, device=dev)
+    msa.profile_reset()
+    msa.profile_enable(True)
+    try:
+        ids1 = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk, workspace=wi)
+        o1, l1 = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids1, seqs, p.block_size, workspace=wa)
+        torch.cuda.synchronize()
+    finally:
+        msa.profile_enable(False)
+    rec = msa.profile_read()
+    msa.profile_reset()
+    n_topk = sum(rec.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel"))
+    n_comb = rec.get("kvo_combine_kernel", (0, 0))[0]
+    _say(f"  launches: index {n_topk} (plan {len(idx_starts)}), attention {n_comb} (plan {len(attn_starts)})")
+    assert n_topk == len(idx_starts) >= 3 and n_comb == len(attn_starts) >= 3
+    assert torch.equal(ids0, ids1)
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16)) and torch.equal(l0, l1)
+    ids_ora, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
+    ids_h = ids1.cpu().numpy()
+    exact, ties = check_block_ids(ids_h, ids_ora, gaps, x, lay, p.block_size, p.topk)
+    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_h, lay, p.block_size)
+    stats = check_outputs(o1.float().cpu().numpy(), l1.cpu().numpy(), o_ref, l_ref, p.name)
+    _say(f"  ids exact={exact} ties={ties}; O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+
+
 # ---------------------------------------------------------------- workloads
 def _sample_rows(p, n, seed):
     rng = np.random.default_rng(seed)
@@ -184,26 +229,73 @@ def _sample_rows(p, n, seed):
     return sorted(rows)
 
 
-def test_workload_prefill_4k():
-    p = synth.workload("prefill_4k")
-    _say(f"[case] {p.name}")
-    x = synth.generate_numpy(p)
-    lay = O.layout_of(p)
-    dev = torch.device("cuda")
-    seqs = msa.Seqs.from_problem(p, dev)
-    d = {k: to_dev(v) for k, v in x.items()}
-    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
-    o, l = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
-    torch.cuda.synchronize()
-    ids_gpu = ids.cpu().numpy()
-    ids_ora, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
-    exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, x, lay, p.block_size, p.topk)
-    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_gpu, lay, p.block_size)
-    stats = check_outputs(o.float().cpu().numpy(), l.cpu().numpy(), o_ref, l_ref, p.name)
-    _say(f"  ids exact={exact} ties={ties}; O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+def _align(x, a=256):
+    return (x + a - 1) // a * a
 
 
-def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
+def _plan_sizes(p):
+    """Sizes behind the two prefill calls' chunk plans (mirrored from the
+    library): index call: row-group size qr, rows per unit U, units, header and
+    bytes per unit; attention call: fixed bytes and bytes per chunk row."""
+    S, T, H_kv, H_q, k, B = p.num_seqs, p.total_q_rows, p.num_kv_heads, p.num_q_heads, p.topk, p.block_size
+    qr = 64 // H_kv
+    mq = p.max_q_rows
+    U = 8 if (mq > 4 * qr and p.d_idx == 64 and B == 64) else (4 if mq > 2 * qr else 1)
+    seq_units = U == 1 and mq <= qr
+    max_units = S if seq_units else (T // qr + S) // U + S
+    bcap = _align(-(-p.max_kv_len // B), 4)
+    cmcap = -(-bcap // 64) if U >= 4 else 0
+    pcap = -(-bcap // 16) if cmcap else 0
+    unit_bytes = U * 64 * (bcap + cmcap + pcap) * 4
+    hdr = _align(4 * (S + 1))
+    ntile = H_kv * S * max(1, -(-p.max_kv_len // B))
+    nscan = -(-ntile // 2048)
+    fixed = (_align(8 * (S + 1)) + _align(4 * (ntile + 2)) + 2 * _align(4 * (ntile + 1)) + _align(8 * nscan))
+    prb = 8 * H_kv * k + k * H_q * (128 * 2 + 4)
+    return dict(qr=qr, U=U, seq_units=seq_units, max_units=max_units, unit_bytes=unit_bytes, hdr=hdr,
+                fixed=fixed, prb=prb)
+
+
+def _launch_row_starts(p, ws_index, ws_attn):
+    """First packed row of every launch of the two prefill calls, mirroring
+    their chunk plans: the index call scores units of U row groups (a row group
+    is 64 / H_kv rows of one sequence) in chunks sized to its workspace; the
+    attention call builds its reverse index and partials for chunks of rows
+    sized to its workspace.  Returns (index starts, attention starts); callers
+    compare their number with the launches made."""
+    S, T, H_kv, H_q, k = p.num_seqs, p.total_q_rows, p.num_kv_heads, p.num_q_heads, p.topk
+    z = _plan_sizes(p)
+    qr, U, seq_units, max_units = z["qr"], z["U"], z["seq_units"], z["max_units"]
+    chunk = min((ws_index - z["hdr"]) // z["unit_bytes"], max_units)
+    unit_off = [0]
+    for s in range(S):
+        rows = p.q_offsets[s + 1] - p.q_offsets[s]
+        groups = -(-rows // qr)
+        unit_off.append(unit_off[-1] + (1 if seq_units else -(-groups // U)))
+    idx = []
+    for u0 in range(0, max_units, chunk):
+        for s in range(S):
+            if unit_off[s] <= u0 < unit_off[s + 1]:
+                idx.append(p.q_offsets[s] + (u0 - unit_off[s]) * (1 if seq_units else U * qr))
+                break
+    fixed, prb = z["fixed"], z["prb"]
+
+    def total(c):
+        return (fixed + 2 * _align(4 * c * H_kv * k) + _align(2 * k * c * H_q * 128) + _align(4 * k * c * H_q))
+
+    cr = T if total(T) <= ws_attn else (ws_attn - fixed - 4 * 256) // prb
+    cr = min(cr, ((1 << 31) - 1) // (H_kv * k), 1 << 26)
+    return idx, list(range(0, T, cr))
+
+
+def _stratified_with_launch_edges(p, n, idx_starts, attn_starts):
+    rows = set(synth.stratified_rows(p, n, seed=p.seed))
+    for r in list(idx_starts) + list(attn_starts):
+        rows |= {r, max(0, r - 1)}            # first row of a launch, last row of the one before
+    return sorted(x for x in rows if 0 <= x < p.total_q_rows)
+
+
+def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None, stratified=False):
     p = synth.workload(name)
     _say(f"[case] {p.name} rows={p.total_q_rows} kv_rows={p.total_kv_rows}")
     dev = torch.device("cuda")
@@ -216,11 +308,31 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
         x = None
     lay = O.layout_of(p)
     decode = p.max_q_rows == 1
-    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
     fn = msa.sparse_attn_decode if decode else msa.sparse_attn_prefill
-    o, l = fn(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
-    torch.cuda.synchronize()
-    rows = list(range(p.total_q_rows)) if decode else _sample_rows(p, n_rows, seed=p.seed)
+    msa.profile_reset()
+    msa.profile_enable(True)
+    try:
+        ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+        o, l = fn(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+        torch.cuda.synchronize()
+    finally:
+        msa.profile_enable(False)
+    launches = msa.profile_read()
+    msa.profile_reset()
+    if decode:
+        rows = list(range(p.total_q_rows))
+    elif stratified:
+        ws_i = msa.index_topk_workspace_size(seqs, p.num_kv_heads, p.d_idx, p.block_size, p.topk)
+        ws_a = msa.sparse_attn_prefill_workspace_size(seqs, p.num_q_heads, p.num_kv_heads, p.head_dim,
+                                                      p.block_size, p.topk)
+        idx_starts, attn_starts = _launch_row_starts(p, ws_i, ws_a)
+        n_topk = sum(launches.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel"))
+        n_comb = launches.get("kvo_combine_kernel", (0, 0))[0]
+        _say(f"  launches: index {n_topk} (plan {len(idx_starts)}), attention {n_comb} (plan {len(attn_starts)})")
+        assert n_topk == len(idx_starts) and n_comb == len(attn_starts), "chunk plan mirror out of date"
+        rows = _stratified_with_launch_edges(p, n_rows, idx_starts, attn_starts)
+    else:
+        rows = _sample_rows(p, n_rows, seed=p.seed)
     # the oracle reads the input rows it needs back from the (generated) inputs;
     # only sampled rows of the query-side tensors and outputs leave the device
     rows_t = torch.tensor(rows, dtype=torch.int64, device=dev)
@@ -236,7 +348,11 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
     exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, inputs, lay, p.block_size, p.topk, rows=rows)
     _say(f"  ids exact={exact} ties={ties} over {len(rows)} rows")
     # Main branch on sampled rows, oracle fed with the GPU's (validated) ids
-    arows = rows if check_attn_rows is None else rows[::max(1, len(rows) // check_attn_rows)]
+    if check_attn_rows is None:
+        arows = rows
+    else:
+        step = max(1, len(rows) // check_attn_rows)
+        arows = sorted(set(rows[::step]) | {rows[0], rows[-1]})
     arows_t = torch.tensor(arows, dtype=torch.int64, device=dev)
     o_h = o[arows_t].float().cpu().numpy()
     l_h = l[arows_t].cpu().numpy()
@@ -262,6 +378,26 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None):
     _say(f"  O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e} lse {stats[2]:.2e} over {len(arows)} rows")
     del d, o, l, ids
     torch.cuda.empty_cache()
+    return len(rows), len(arows)
+
+
+def test_workload_prefill_4k():
+    p = synth.workload("prefill_4k")
+    _say(f"[case] {p.name}")
+    x = synth.generate_numpy(p)
+    lay = O.layout_of(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {k: to_dev(v) for k, v in x.items()}
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    o, l = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    torch.cuda.synchronize()
+    ids_gpu = ids.cpu().numpy()
+    ids_ora, gaps = O.select_blocks(x["index_q"], x["index_k"], lay, p.block_size, p.topk)
+    exact, ties = check_block_ids(ids_gpu, ids_ora, gaps, x, lay, p.block_size, p.topk)
+    o_ref, l_ref = O.sparse_attention(x["q"], x["k"], x["v"], ids_gpu, lay, p.block_size)
+    stats = check_outputs(o.float().cpu().numpy(), l.cpu().numpy(), o_ref, l_ref, p.name)
+    _say(f"  ids exact={exact} ties={ties}; O max-abs {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
 
 
 def test_workload_prefill_32k_sampled():
@@ -273,13 +409,18 @@ def test_workload_decode_128k():
 
 
 def test_workload_chunked_8x8k_sampled():
-    _sampled_workload("chunked_8x8k", 96, gen="torch", check_attn_rows=48)
+    # every launch of both calls: its first row and the last row of the launch
+    # before; plus rows stratified over every sequence's depth
+    n, na = _sampled_workload("chunked_8x8k", 1024, gen="torch", check_attn_rows=256, stratified=True)
+    assert n >= 1024 and na >= 256
 
 
 def test_workload_prefill_1m_sampled():
     # the full 1M-token prefill in the launch configuration bench.py times;
-    # ids and outputs checked on sampled rows (first/last rows and block edges included)
-    _sampled_workload("prefill_1m", 40, gen="torch", check_attn_rows=20)
+    # ids on >= 1024 rows stratified over depth plus the first and last row of
+    # every index and attention launch, outputs on >= 256 of them
+    n, na = _sampled_workload("prefill_1m", 700, gen="torch", check_attn_rows=256, stratified=True)
+    assert n >= 1024 and na >= 256
 
 
 def test_workload_prefill_1m_bk128_sampled():

@@ -10,12 +10,29 @@ import torch
 import oracle.msa_oracle as O
 
 GAP_TOL = 1e-3          # score gap below which several selections are correct
-O_MAX_ABS = 1e-2        # outputs vs the fp64 oracle, on top of the output format's rounding
+O_MAX_ABS = 1e-2        # outputs vs the fp64 oracle (the stated max-abs bar)
 O_REL_L2 = 5e-3
-# O is returned in bf16, which keeps 8 significant bits: rounding the exact
-# result to the output format alone moves it by up to 2^-9 |O| (0.0078 at
-# |O| = 4), so the element-wise bound is O_MAX_ABS + 2^-9 |O_ref|.
 BF16_HALF_ULP_REL = 2.0 ** -9
+
+# Tally over a test session of output elements compared against the oracle
+# and of those whose raw difference exceeds O_MAX_ABS (reported at the end of
+# the session by tests/conftest.py).
+OUTPUT_TALLY = {"elements": 0, "over": 0, "worst": 0.0, "calls": 0}
+
+
+def bf16_rounding_interval(y: np.ndarray):
+    """[lo, hi]: the real values that round (to nearest) to the bf16 values y
+    (float32 arrays holding bf16 values exactly)."""
+    y = np.ascontiguousarray(y, dtype=np.float32)
+    b = (y.view(np.uint32) >> np.uint32(16)).astype(np.uint32)
+    up = ((b + np.uint32(1)) << np.uint32(16)).view(np.float32).astype(np.float64)
+    dn = ((b - np.uint32(1)) << np.uint32(16)).view(np.float32).astype(np.float64)
+    yv = y.astype(np.float64)
+    nb_lo, nb_hi = np.minimum(up, dn), np.maximum(up, dn)
+    zero = (b & np.uint32(0x7FFF)) == 0
+    lo = np.where(zero, 0.0, yv - (yv - nb_lo) / 2)
+    hi = np.where(zero, 0.0, yv + (nb_hi - yv) / 2)
+    return lo, hi
 
 
 def to_dev(bits: np.ndarray, device="cuda") -> torch.Tensor:
@@ -47,17 +64,37 @@ def check_block_ids(gpu_ids, ora_ids, gaps, inputs, layout, block_size, topk, ro
 
 
 def check_outputs(o_gpu: np.ndarray, lse_gpu: np.ndarray, o_ref: np.ndarray, lse_ref: np.ndarray, what=""):
-    o_gpu = o_gpu.astype(np.float64)
-    err = np.abs(o_gpu - o_ref)
-    rel = np.linalg.norm(o_gpu - o_ref) / max(np.linalg.norm(o_ref), 1e-30)
+    """O within O_MAX_ABS of the oracle before the bf16 output rounding (the
+    oracle's value lies within O_MAX_ABS of the set of reals that round to the
+    kernel's bf16 output), relative L2 within O_REL_L2, LSE within O_MAX_ABS.
+    The elements whose raw difference exceeds O_MAX_ABS (possible only where
+    half a bf16 step adds to the arithmetic error) are counted and printed.
+    Returns (max-abs, rel-L2, LSE max-abs, elements beyond
+    O_MAX_ABS, their worst difference)."""
+    o32 = np.asarray(o_gpu, dtype=np.float32)
+    o64 = o32.astype(np.float64)
+    err = np.abs(o64 - o_ref)
+    rel = np.linalg.norm(o64 - o_ref) / max(np.linalg.norm(o_ref), 1e-30)
     lerr = np.abs(lse_gpu.astype(np.float64) - lse_ref)
-    bound = O_MAX_ABS + BF16_HALF_ULP_REL * np.abs(o_ref)
-    worst = np.unravel_index(np.argmax(err - bound), err.shape)
-    assert (err <= bound).all(), \
-        f"{what} O error {err[worst]:.3e} > bound {bound[worst]:.3e} at {worst} (max-abs {err.max():.3e})"
+    lo, hi = bf16_rounding_interval(o32)
+    pre = np.maximum(np.maximum(lo - o_ref, o_ref - hi), 0.0)   # distance to the rounding interval
+    worst = np.unravel_index(np.argmax(pre), pre.shape)
+    assert (pre <= O_MAX_ABS).all(), \
+        f"{what} O error before output rounding {pre[worst]:.3e} > {O_MAX_ABS} at {worst} " \
+        f"(got {o64[worst]:.6f}, oracle {o_ref[worst]:.6f})"
+    over = err > O_MAX_ABS
+    n_over = int(over.sum())
+    worst_over = float(err[over].max()) if n_over else 0.0
+    if n_over:
+        print(f"  {what}: {n_over} of {err.size} O elements beyond {O_MAX_ABS} (worst {worst_over:.4f}, "
+              f"smallest |O| among them {float(np.abs(o_ref[over]).min()):.3f})", flush=True)
     assert rel <= O_REL_L2, f"{what} O rel-L2 {rel:.3e}"
     assert lerr.max() <= O_MAX_ABS, f"{what} LSE max-abs {lerr.max():.3e}"
-    return float(err.max()), float(rel), float(lerr.max())
+    OUTPUT_TALLY["elements"] += int(err.size)
+    OUTPUT_TALLY["over"] += n_over
+    OUTPUT_TALLY["worst"] = max(OUTPUT_TALLY["worst"], worst_over)
+    OUTPUT_TALLY["calls"] += 1
+    return float(err.max()), float(rel), float(lerr.max()), n_over, worst_over
 
 
 # Gradients of the training backward: each element is a sum of products in
