@@ -131,6 +131,30 @@ int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seq
                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
+ * msa_index_topk_noalloc -- msa_index_topk without a workspace argument, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * serving loops that must not call hipMalloc, harnesses that forbid it.
+ *
+ * Arguments, outputs (block_ids, caller-allocated), results and errors are
+ * those of msa_index_topk.  The scratch space lives in a device array of the
+ * library of MSA_INDEX_TOPK_NOALLOC_MAX_BYTES bytes; each GPU the call runs on
+ * holds its own copy until the process ends.  The call runs on the current
+ * device, and `stream` must belong to it.  It allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); its first call on a device looks
+ * the array's address up once.  A problem whose smallest workspace (the
+ * sequence table plus one unit of rows, the quantum msa_index_topk chunks by)
+ * exceeds the array returns MSA_ERR_WORKSPACE and launches nothing; problems
+ * larger than the array but within that bound run in several chunks.
+ * Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ * (several streams or host threads) race and must be serialised by the
+ * caller.  Nothing in the array needs to start at zero.
+ * ------------------------------------------------------------------------ */
+#define MSA_INDEX_TOPK_NOALLOC_MAX_BYTES ((size_t)64 << 20)
+int msa_index_topk_noalloc(const void* index_q, const void* index_k, const msa_seqs* seqs,
+                           int num_kv_heads, int d_idx, int block_size, int topk,
+                           int32_t* block_ids, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
  * Main Branch: msa_sparse_attn_prefill / msa_sparse_attn_decode
  *
  * Sec. 3.1, sparse-attention equation: for query row i and query head h of

@@ -23,6 +23,8 @@
 //                         blocks at a time, filters against the current k-1-th
 //                         best key and keeps a sorted list (one key per lane).
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 
 #include "msa_common.h"
 #include "msa_profile.h"
@@ -918,16 +920,13 @@ extern "C" size_t msa_index_topk_workspace_size(const msa_seqs* seqs, int num_kv
   return pl.hdr_bytes + static_cast<size_t>(units) * pl.unit_bytes;
 }
 
-extern "C" int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seqs,
-                              int num_kv_heads, int d_idx, int block_size, int topk,
-                              int32_t* block_ids, void* workspace, size_t workspace_bytes,
-                              hipStream_t stream) {
-  IndexPlan pl;
-  int st = make_plan(seqs, num_kv_heads, d_idx, block_size, topk, &pl);
-  if (st != MSA_OK) return st;
-  if (seqs->total_q_rows == 0) return MSA_OK;
-  if (!index_q || !index_k || !block_ids || !workspace) return MSA_ERR_INVALID;
-  if (workspace_bytes < pl.hdr_bytes + pl.unit_bytes) return MSA_ERR_WORKSPACE;
+namespace {
+
+// The call on a validated plan: block scores and Top-k per chunk of units, the
+// chunk sized to the workspace.
+int index_topk_run(const IndexPlan& pl, const void* index_q, const void* index_k, const msa_seqs* seqs,
+                   int num_kv_heads, int d_idx, int block_size, int topk, int32_t* block_ids, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream) {
   int64_t chunk = static_cast<int64_t>((workspace_bytes - pl.hdr_bytes) / pl.unit_bytes);
   if (chunk > pl.max_units) chunk = pl.max_units;
 
@@ -977,3 +976,77 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   }
   return msa_host::launch_status();
 }
+
+}  // namespace
+
+extern "C" int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seqs,
+                              int num_kv_heads, int d_idx, int block_size, int topk,
+                              int32_t* block_ids, void* workspace, size_t workspace_bytes,
+                              hipStream_t stream) {
+  IndexPlan pl;
+  int st = make_plan(seqs, num_kv_heads, d_idx, block_size, topk, &pl);
+  if (st != MSA_OK) return st;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if (!index_q || !index_k || !block_ids || !workspace) return MSA_ERR_INVALID;
+  if (workspace_bytes < pl.hdr_bytes + pl.unit_bytes) return MSA_ERR_WORKSPACE;
+  return index_topk_run(pl, index_q, index_k, seqs, num_kv_heads, d_idx, block_size, topk, block_ids, workspace,
+                        workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------- no-allocation entry point
+// msa_index_topk_noalloc runs the same kernels on a workspace that lives in a
+// device array of this file (one copy per GPU, held until the process ends),
+// so the call allocates nothing.  Host code never passes the array's name to
+// a kernel: it is a host-side stand-in for the symbol.  The device address is
+// looked up once per device with hipGetSymbolAddress and cached.
+static __device__ __align__(256) unsigned char scratch[MSA_INDEX_TOPK_NOALLOC_MAX_BYTES];
+
+namespace {
+
+constexpr size_t kNoallocScratchBytes = MSA_INDEX_TOPK_NOALLOC_MAX_BYTES;
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+// Device address of `scratch` on the current device.
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return MSA_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return MSA_ERR_UNSUPPORTED;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return MSA_ERR_HIP;
+      }
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return MSA_OK;
+}
+
+}  // namespace
+
+extern "C" int msa_index_topk_noalloc(const void* index_q, const void* index_k, const msa_seqs* seqs,
+                                      int num_kv_heads, int d_idx, int block_size, int topk,
+                                      int32_t* block_ids, hipStream_t stream) {
+  IndexPlan pl;
+  int st = make_plan(seqs, num_kv_heads, d_idx, block_size, topk, &pl);
+  if (st != MSA_OK) return st;
+  if (seqs->total_q_rows == 0) return MSA_OK;
+  if (!index_q || !index_k || !block_ids) return MSA_ERR_INVALID;
+  // the smallest workspace the call can run in (one unit of rows) must fit
+  if (pl.hdr_bytes + pl.unit_bytes > kNoallocScratchBytes) return MSA_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if ((st = scratch_on_current_device(&ws)) != MSA_OK) return st;
+  return index_topk_run(pl, index_q, index_k, seqs, num_kv_heads, d_idx, block_size, topk, block_ids, ws,
+                        kNoallocScratchBytes, stream);
+}
+

@@ -21,7 +21,7 @@ MSA_OK, MSA_ERR_INVALID, MSA_ERR_UNSUPPORTED, MSA_ERR_WORKSPACE, MSA_ERR_HIP = 0
 
 EXPORTS = [
     "msa_strerror",
-    "msa_index_topk_workspace_size", "msa_index_topk",
+    "msa_index_topk_workspace_size", "msa_index_topk", "msa_index_topk_noalloc",
     "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
     "msa_sparse_attn_prefill_fp8", "msa_sparse_attn_decode_fp8",
@@ -65,6 +65,8 @@ def lib() -> ctypes.CDLL:
         L.msa_index_topk_workspace_size.restype = Z
         L.msa_index_topk.argtypes = [P, P, S, I, I, I, I, P, P, Z, P]
         L.msa_index_topk.restype = I
+        L.msa_index_topk_noalloc.argtypes = [P, P, S, I, I, I, I, P, P]
+        L.msa_index_topk_noalloc.restype = I
         for name in ("prefill", "decode"):
             ws = getattr(L, f"msa_sparse_attn_{name}_workspace_size")
             ws.argtypes = [S, I, I, I, I, I]
@@ -193,6 +195,24 @@ def index_topk(index_q: torch.Tensor, index_k: torch.Tensor, seqs: Seqs, block_s
     st = lib().msa_index_topk(_ptr(index_q), _ptr(index_k), seqs.ref(), H_kv, d_idx, block_size, topk,
                               _ptr(out), _ptr(ws), 0 if ws is None else ws.numel() * ws.element_size(), _stream())
     _check(st, "msa_index_topk")
+    return out
+
+
+NOALLOC_MAX_BYTES = 64 << 20      # MSA_INDEX_TOPK_NOALLOC_MAX_BYTES
+
+
+def index_topk_noalloc(index_q: torch.Tensor, index_k: torch.Tensor, seqs: Seqs, block_size: int, topk: int,
+                       out: torch.Tensor) -> torch.Tensor:
+    """msa_index_topk_noalloc: the Index Branch on the library's own scratch
+    array; ``out`` (int32 [total_q_rows, H_kv, topk]) is caller-allocated."""
+    Tq, H_kv, d_idx = index_q.shape
+    dev = seqs.device
+    _need(index_q, "index_q", torch.bfloat16, (seqs.total_q_rows, H_kv, d_idx), dev)
+    _need(index_k, "index_k", torch.bfloat16, (seqs.total_kv_rows, d_idx), dev)
+    _need(out, "block_ids", torch.int32, (Tq, H_kv, topk), dev)
+    st = lib().msa_index_topk_noalloc(_ptr(index_q), _ptr(index_k), seqs.ref(), H_kv, d_idx, block_size, topk,
+                                      _ptr(out), _stream())
+    _check(st, "msa_index_topk_noalloc")
     return out
 
 

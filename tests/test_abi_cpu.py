@@ -199,3 +199,18 @@ def test_chunks_stay_within_the_handle_row_field():
         na, nb = fn(ctypes.byref(a), *args), fn(ctypes.byref(b), *args)
         assert na > 0 and nb > 0
         assert nb - na == per_row * (big - (1 << 26)), (fn.__name__, na, nb)
+
+
+def test_noalloc_rejects_problems_beyond_its_scratch():
+    """msa_index_topk_noalloc checks the problem against its fixed scratch on
+    the host: a sequence of 4M keys needs more than the 64 MiB array for one
+    unit of rows, so the call returns MSA_ERR_WORKSPACE before any HIP call;
+    invalid arguments are rejected as msa_index_topk rejects them."""
+    L = msa.lib()
+    n = 1 << 22
+    s = _seqs(total_q_rows=n, total_kv_rows=n, max_q_rows=n, max_kv_len=n)
+    assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 8, 64, 64, 16, 8, None) == msa.MSA_ERR_WORKSPACE
+    s = _seqs()
+    assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 3, 64, 64, 8, 8, None) == msa.MSA_ERR_UNSUPPORTED
+    assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 2, 64, 64, 8, None, None) == msa.MSA_ERR_INVALID
+    assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 2, 64, 64, 0, 8, None) == msa.MSA_ERR_INVALID
