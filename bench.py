@@ -642,8 +642,8 @@ def main():
     ap.add_argument("--cpu-sample-rows", type=int, default=300)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
-    ap.add_argument("--fp8", action="store_true",
-                    help="also time the Main Branch on E4M3 Q/K/V (msa_sparse_attn_*_fp8)")
+    ap.add_argument("--no-fp8", dest="fp8", action="store_false",
+                    help="skip the Main Branch on E4M3 Q/K/V (msa_sparse_attn_*_fp8), timed by default")
     ap.add_argument("--calib-copy-gib", type=float, default=0.0,
                     help="first run one in-place int32 add over this many GiB (reads and writes exactly "
                          "that much): the reference kernel for scaling HBM byte counters")
@@ -692,6 +692,9 @@ def main():
                    "num_q_heads": p.num_q_heads, "num_kv_heads": p.num_kv_heads, "head_dim": p.head_dim,
                    "d_idx": p.d_idx, "block_size": p.block_size, "topk": p.topk},
         "roofline": roofline_of(pre),
+        # the Main Branch call (msa_sparse_attn_prefill, incl. its reverse index and combine) on
+        # selected-block FLOPs, against the dense bf16 MFMA peak
+        "main_branch_frac_of_bf16_peak": att_tflops / PEAK_BF16_TFLOPS,
         "calls": {
             "msa_index_topk": {"ms_per_call": pre["ms_idx"], "algorithmic_flops": pre["idx_flops"],
                                "tflops": idx_tflops, "frac_of_bf16_peak": idx_tflops / PEAK_BF16_TFLOPS},
