@@ -273,10 +273,10 @@ int msa_dense_attn(const void* q, const void* k, const void* v, const msa_seqs* 
  *   d_k, d_v   bf16 [total_kv_rows, num_kv_heads, head_dim] OUTPUT; every row is
  *              written, key rows no query attended get 0
  *
- * Work runs key-block-outer with fp32 accumulation.  d_q is bit-reproducible
- * (its partials are added in slot order); d_k and d_v add the contributions of
- * a key block in an order fixed at run time, so their last bits can differ
- * between calls.  Workspace, stream and
+ * Work runs key-block-outer with fp32 accumulation.  Every output is
+ * bit-reproducible: d_q adds its partials in slot order, and d_k and d_v add a
+ * key block's contributions in ascending (query row, slot) order (the
+ * reverse index is sorted into that order).  Workspace, stream and
  * error behaviour as for msa_sparse_attn_prefill.  Supported: head_dim == 128;
  * block_size 64 with 1 <= topk <= 64, or block_size 128 with 1 <= topk <= 32
  * (run as the blocks' 64-key halves); 1 <= num_q_heads / num_kv_heads <= 16;
@@ -319,8 +319,8 @@ int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const 
  *   kl         fp32 [total_q_rows, num_kv_heads]          OUTPUT, or NULL to skip
  *
  * Workspace, stream and error behaviour as for msa_sparse_attn_prefill.
- * d_index_q and kl are bit-reproducible; d_index_k adds a key block's queries
- * in an order fixed at run time.  Supported: d_idx in {64, 128};
+ * d_index_q, d_index_k and kl are bit-reproducible (d_index_k adds a key
+ * block's queries in ascending (row, slot) order).  Supported: d_idx in {64, 128};
  * head_dim == 128; block_size 64 with 1 <= topk <= 64, or block_size 128 with
  * 1 <= topk <= 32 (run as the blocks' 64-key halves);
  * num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}; num_kv_heads <= 64.

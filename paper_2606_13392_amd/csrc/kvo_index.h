@@ -313,12 +313,83 @@ __device__ __forceinline__ int32_t claim_next_item(int32_t* __restrict__ next_it
   return *s_claim;
 }
 
+// ---------------------------------------------------------------- canonical handle order
+// The reverse index hands out positions inside a tile with atomics, so a
+// tile's handle list comes out in a run-dependent order.  Kernels whose sums
+// run over a tile's handles (the training backward's dK / dV and d k_idx)
+// sort each list into ascending handle order -- row, then slot -- which makes
+// their results bit-reproducible.  One CTA per tile: runs of kSortRun handles
+// are sorted in LDS (bitonic), then merged pairwise through `tmp` (each
+// element's place in the merged run is its rank in its own run plus its rank
+// among the other run's elements; the handles of a tile are distinct).
+constexpr int kSortRun = 2048;
+
+__device__ __forceinline__ int32_t count_below(const uint32_t* __restrict__ a, int32_t n, uint32_t x) {
+  int32_t lo = 0, hi = n;                      // first index with a[i] >= x
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (a[mid] < x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+__global__ __launch_bounds__(256) void sort_tile_handles_kernel(uint32_t* __restrict__ handles,
+                                                                uint32_t* __restrict__ tmp,
+                                                                const int32_t* __restrict__ tile_off) {
+  __shared__ uint32_t sh[kSortRun];
+  const int64_t t = blockIdx.x;
+  const int32_t beg = tile_off[t];
+  const int32_t n = tile_off[t + 1] - beg;
+  if (n <= 1) return;                                 // uniform over the CTA
+  const int tid = threadIdx.x;
+  uint32_t* a = handles + beg;
+  uint32_t* b = tmp + beg;
+  for (int32_t r0 = 0; r0 < n; r0 += kSortRun) {
+    const int32_t m = min(kSortRun, n - r0);
+    int32_t P = 1;
+    while (P < m) P <<= 1;
+    for (int32_t i = tid; i < P; i += 256) sh[i] = i < m ? a[r0 + i] : 0xFFFFFFFFu;
+    __syncthreads();
+    for (int32_t kk = 2; kk <= P; kk <<= 1)
+      for (int32_t j = kk >> 1; j > 0; j >>= 1) {
+        for (int32_t i = tid; i < P; i += 256) {
+          const int32_t ixj = i ^ j;
+          if (ixj > i) {
+            const uint32_t x = sh[i], y = sh[ixj];
+            const bool up = (i & kk) == 0;
+            if ((x > y) == up) { sh[i] = y; sh[ixj] = x; }
+          }
+        }
+        __syncthreads();
+      }
+    for (int32_t i = tid; i < m; i += 256) a[r0 + i] = sh[i];
+    __syncthreads();
+  }
+  uint32_t* src = a;
+  uint32_t* dst = b;
+  for (int32_t w = kSortRun; w < n; w <<= 1) {
+    for (int32_t i = tid; i < n; i += 256) {
+      const int32_t lo = (i / (2 * w)) * (2 * w);     // the pair of runs holding i
+      const int32_t mid = min(lo + w, n), hi = min(lo + 2 * w, n);
+      const uint32_t x = src[i];
+      const int32_t pos = i < mid ? lo + (i - lo) + count_below(src + mid, hi - mid, x)
+                                  : lo + (i - mid) + count_below(src + lo, mid - lo, x);
+      dst[pos] = x;
+    }
+    __syncthreads();
+    uint32_t* sw = src; src = dst; dst = sw;
+  }
+  if (src != a) {
+    for (int32_t i = tid; i < n; i += 256) a[i] = src[i];
+  }
+}
+
 // Reverse index of query rows r0 .. r0 + nr - 1 (one chunk): counts, scans
-// and handle lists for every tile of H_kv x nbcap.
+// and handle lists for every tile of H_kv x nbcap; `canonical` sorts each list.
 void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int64_t* blk_base, int H_kv, int BK,
                          int topk, int64_t nbcap, int64_t ntile, int nscan, int64_t r0, int64_t nr, int32_t* cnt,
                          int32_t* tile_off, int32_t* item_off, int32_t* blk_tot, int32_t* tpos, uint32_t* handles,
-                         hipStream_t stream) {
+                         hipStream_t stream, bool canonical = false) {
   const unsigned fill_blocks = static_cast<unsigned>(std::min<int64_t>((ntile + kWorkCounters + 255) / 256, 4096));
   const unsigned gthreads = static_cast<unsigned>((nr * H_kv + 256 / kWave - 1) / (256 / kWave));   // a wave per pair
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(fill_blocks), dim3(256), 0, stream, cnt,
@@ -334,6 +405,11 @@ void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int
                    dim3(256), 0, stream, blk_tot, ntile, tile_off, item_off);
   msa_prof::launch("kvo_fill_kernel", kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base,
                    H_kv, BK, topk, nbcap, r0, nr, tile_off, tpos, handles);
+  // positions are no longer needed: tpos is the sort's merge buffer
+  if (canonical)
+    msa_prof::launch("sort_tile_handles_kernel", sort_tile_handles_kernel, dim3(static_cast<unsigned>(ntile)),
+                     dim3(256), 0, stream, handles, reinterpret_cast<uint32_t*>(tpos),
+                     static_cast<const int32_t*>(tile_off));
 }
 
 }  // namespace

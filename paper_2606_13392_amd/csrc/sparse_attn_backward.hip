@@ -576,7 +576,7 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
     build_reverse_index(block_ids, sq, blk_base, H_kv, kBwdBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
-                        tile_off, item_off, blk_tot, tpos, handles, stream);
+                        tile_off, item_off, blk_tot, tpos, handles, stream, true);
     msa_prof::launch("bwd_kvo_kernel", bwd_kvo_kernel, dim3(nctas), dim3(kBwdThreads), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(d_o), lse,

@@ -728,7 +728,7 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
     const int64_t pairs = nr * H_kv;
     build_reverse_index(block_ids, sq, blk_base, H_kv, kKlBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
-                        tile_off, item_off, blk_tot, tpos, handles, stream);
+                        tile_off, item_off, blk_tot, tpos, handles, stream, true);
     msa_prof::launch("kl_lse_kernel", kl_lse_kernel<D>, dim3(n_lse), dim3(kKlThreads), 0, stream, iq, ik, sq,
                      static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
                      static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,

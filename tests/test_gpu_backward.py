@@ -116,7 +116,8 @@ def test_backward_chunked_workspace_and_reproducibility():
     """A workspace below the one-chunk size runs several row chunks and meets
     the same bar.  dQ sums its slot partials in slot order, so it is equal bit
     for bit across runs and chunkings; dK and dV add a block's queries in the
-    run-time order of the reverse index, so only the bar applies to them."""
+    ascending (row, slot) order the reverse index is sorted into, so they are
+    equal bit for bit across runs with the same chunking."""
     case = ("bwd_chunks", [700, 900], [700, 1200], 16, 2, 6, None)
     _say("[case] bwd_chunks")
     p, x, ids = _setup(*case)
@@ -126,11 +127,33 @@ def test_backward_chunked_workspace_and_reproducibility():
     one = list(_run(p, x, ids))
     again = list(_run(p, x, ids))
     assert np.array_equal(one[0], again[0]), "dQ is not reproducible"
+    assert np.array_equal(one[1], again[1]) and np.array_equal(one[2], again[2]), "dK / dV are not reproducible"
     small = list(_run(p, x, ids, workspace_bytes=int(full * 0.4)))
     ref = O.sparse_attention_backward(x["q"], x["k"], x["v"], x["d_o"], ids, O.layout_of(p), p.block_size)
     _check_all("bwd_chunks (one chunk)", one, ref)
     _check_all("bwd_chunks (small workspace)", small, ref)
     assert np.array_equal(one[0], small[0]), "chunked dQ differs from the one-chunk dQ"
+
+
+def test_backward_reproducible_on_crowded_tiles():
+    """Tiles of thousands of queries (every row of a 4096-row sequence picks
+    the same hot blocks): the reverse index's atomics hand out positions in a
+    different order on every run, and the sorted handle lists still give dK
+    and dV equal bit for bit over three runs."""
+    case = ("bwd_crowded", [4096], [4096], 16, 2, 8, None)
+    _say("[case] bwd_crowded")
+    p, x, ids = _setup(*case)
+    ids[:, :, 0] = np.where(ids[:, :, 0] >= 0, 0, ids[:, :, 0])      # block 0 in every row that sees it
+    for r in range(ids.shape[0]):
+        for g in range(ids.shape[1]):
+            sel = sorted(set(int(b) for b in ids[r, g] if b >= 0))
+            ids[r, g, :] = -1
+            ids[r, g, :len(sel)] = sel
+    runs = [list(_run(p, x, ids)) for _ in range(3)]
+    for t in range(3):
+        assert all(np.array_equal(runs[0][t], rr[t]) for rr in runs[1:]), f"output {t} differs between runs"
+    ref = O.sparse_attention_backward(x["q"], x["k"], x["v"], x["d_o"], ids, O.layout_of(p), p.block_size)
+    _check_all("bwd_crowded", runs[0], ref)
 
 
 def test_backward_block_128_limits():

@@ -186,3 +186,27 @@ def test_kl_workload_sampled(name, n_rows):
     assert ratio < 1e-2
     del d, lse, diq, dik, kl, ids
     torch.cuda.empty_cache()
+
+
+def test_kl_reproducible():
+    """d_index_k adds a key block's queries in the sorted (row, slot) order of
+    the reverse index: three runs agree bit for bit (as d_index_q and KL do)."""
+    name = "kl_repro"
+    p = synth.packed_problem(name, [3000], [3000], num_q_heads=16, num_kv_heads=2, topk=16, d_idx=64,
+                             seed=zlib.crc32(name.encode()) % 10000)
+    x = synth.generate_numpy(p)
+    ids = synth.random_block_ids(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {t: to_dev(v) for t, v in x.items()}
+    ids_d = torch.from_numpy(ids).to(dev)
+    _, lse = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids_d, seqs, p.block_size)
+    outs = []
+    for _ in range(3):
+        diq, dik, kl = msa.sparse_kl_backward(d["index_q"], d["index_k"], d["q"], d["k"], lse, ids_d, seqs,
+                                              p.block_size)
+        torch.cuda.synchronize()
+        outs.append((from_dev_bits(diq), from_dev_bits(dik), kl.cpu().numpy()))
+    for o in outs[1:]:
+        assert np.array_equal(outs[0][0], o[0]) and np.array_equal(outs[0][1], o[1])
+        assert np.array_equal(outs[0][2].view(np.uint32), o[2].view(np.uint32))
