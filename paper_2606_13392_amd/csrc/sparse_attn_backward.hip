@@ -11,10 +11,10 @@
 // dK and dV of a block stay in registers while the queries that selected it
 // stream past, each incidence costs a gather of its Q and dO rows, and its dQ
 // contribution goes as a bf16 partial into the incidence's slot.  No
-// atomics touch a gradient: dQ sums its slot partials in slot order (bit-
-// reproducible); dK and dV sum a block's queries in the order of its handle
-// list, which the reverse index fills with atomics, so their last bits can
-// differ between runs.
+// atomics touch a gradient: dQ sums its slot partials in slot order, and dK
+// and dV sum a block's queries in the order of its handle list, which is
+// sorted into ascending (row, slot) order after the reverse index is built,
+// so every gradient is bit-reproducible.
 //
 //   bwd_delta        D per (row, head)
 //   per chunk of query rows:
