@@ -278,9 +278,8 @@ int msa_dense_attn(const void* q, const void* k, const void* v, const msa_seqs* 
  * key block's contributions in ascending (query row, slot) order (the
  * reverse index is sorted into that order).  Workspace, stream and
  * error behaviour as for msa_sparse_attn_prefill.  Supported: head_dim == 128;
- * block_size 64 with 1 <= topk <= 64, or block_size 128 with 1 <= topk <= 32
- * (run as the blocks' 64-key halves); 1 <= num_q_heads / num_kv_heads <= 16;
- * num_kv_heads <= 64.
+ * block_size 64 or 128 with 1 <= topk <= 64; 1 <= num_q_heads / num_kv_heads
+ * <= 16; num_kv_heads <= 64.
  * ------------------------------------------------------------------------ */
 size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,
                                                int num_kv_heads, int head_dim, int block_size,

@@ -38,21 +38,23 @@
 
 namespace {
 
-constexpr int kBwdBK = 64;
-constexpr int kBwdRowGroups = 1;                      // 32-row groups per CTA pass
-constexpr int kBwdWaves = 4 * kBwdRowGroups;          // 4 key quarters
-constexpr int kBwdThreads = 64 * kBwdWaves;
-constexpr int kBwdPassRows = 32 * kBwdRowGroups;      // gathered (query, head) rows per CTA pass
-static_assert(kBwdRowGroups == 1, "dK / dV of a key quarter live in one wave");
-constexpr int kPartFloats = 2 * kBwdBK * kHeadDim;    // dK and dV of one work item
+// Key blocks of 64 or 128 keys: one wave per 16 keys (4 or 8 waves per CTA).
+template <int BK>
+constexpr int bwd_waves() { return BK / 16; }
+template <int BK>
+constexpr int bwd_threads() { return 64 * bwd_waves<BK>(); }
+constexpr int kBwdPassRows = 32;                      // gathered (query, head) rows per CTA pass
+template <int BK>
+constexpr int bwd_part_floats() { return 2 * BK * kHeadDim; }   // dK and dV of one work item
 
+template <int BK>
 struct BwdSmem {
-  uint16_t k[kBwdBK][kHeadDim + 8];                   // K block, row-major
-  uint16_t v[kBwdBK][kHeadDim + 8];                   // V block, row-major
-  uint16_t kt[kHeadDim][kBwdBK + 8];                  // K block transposed
+  uint16_t k[BK][kHeadDim + 8];                       // K block, row-major
+  uint16_t v[BK][kHeadDim + 8];                       // V block, row-major
+  uint16_t kt[kHeadDim][BK + 8];                      // K block transposed
   uint16_t qt[kHeadDim][kBwdPassRows + 8];            // Q rows of the pass, transposed
   uint16_t dot[kHeadDim][kBwdPassRows + 8];           // dO rows of the pass, transposed
-  uint16_t ds[kBwdRowGroups][32][kBwdBK + 8];         // dS of the pass, [row][key] per row group
+  uint16_t ds[32][BK + 8];                            // dS of the pass, [row][key]
   float lse2[kBwdPassRows];                           // LSE * log2(e) per pass row (+inf: no row)
   float dlt[kBwdPassRows];                            // D per pass row
   int32_t rpos[kBwdPassRows];                         // absolute position per pass row (-1: no row)
@@ -60,8 +62,9 @@ struct BwdSmem {
   int32_t s_row[kItemQueries];                        // query row inside the chunk
   int32_t s_slot[kItemQueries];                       // slot of this block in the row's id list
 };
-// two CTAs per CU
-static_assert(sizeof(BwdSmem) <= 80 * 1024, "LDS of a backward CTA");
+// B_k 64: two CTAs per CU; B_k 128: one CTA of 8 waves
+static_assert(sizeof(BwdSmem<64>) <= 80 * 1024, "LDS of a B_k 64 backward CTA");
+static_assert(sizeof(BwdSmem<128>) <= 160 * 1024, "LDS of a B_k 128 backward CTA");
 
 __device__ __forceinline__ uint16_t raw_elem(const u32x4& w, int j) {
   return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
@@ -98,19 +101,23 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restri
 // t, rows 16t + 4qd + i (i = 0..3).  Those 8 rows are the k-slice the lane
 // supplies to dV += P^T dO and dK += dS^T Q (k index 8qd + 4t + i), and
 // the B operands read the same rows from the transposed Q / dO copies.
-__global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
+template <int BK>
+__global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ d_o, const float* __restrict__ lse, const float* __restrict__ delta, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0, float scale_log2,
     uint16_t* __restrict__ dq_buf, int64_t dq_trash, float* __restrict__ part, int32_t* __restrict__ next_item) {
-  static_assert(kItemQueries <= kBwdThreads, "every thread loads at most one handle of an item");
-  __shared__ BwdSmem sm;
+  constexpr int NKW = bwd_waves<BK>();                // waves = 16-key slices of the block
+  constexpr int kThreads = bwd_threads<BK>();
+  static_assert(kItemQueries <= kThreads, "every thread loads at most one handle of an item");
+  __shared__ BwdSmem<BK> sm;
   __shared__ int32_t s_claim;
   constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension
+  constexpr int DQU = 8 / NKW;                        // 16-dim tiles of dQ per wave
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int kq = wave & 3, rg = wave >> 2;
+  const int kq = wave, rg = 0;
   const int c16 = lane & 15, qd = lane >> 4;
   const int G = H_q / H_kv;
   const int qpw = 32 / G;                             // queries per row group and pass
@@ -130,7 +137,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
     const int64_t gb = tile % nbcap;
     const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
     const SeqGeom g = seq_geom(sq, s);
-    const int key0 = static_cast<int>(gb - blk_base[s]) * kBwdBK;
+    const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
 
     __syncthreads();                                  // the previous item is done with LDS
     if (static_cast<int>(threadIdx.x) < nq) {
@@ -144,7 +151,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
       const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       // K row-major and transposed: a thread takes 4 keys x 8 dims
-      for (int c = threadIdx.x; c < (kBwdBK / 4) * (kHeadDim / 8); c += kBwdThreads) {
+      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += kThreads) {
         const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         u32x4 rows[4];
 #pragma unroll
@@ -161,7 +168,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
           *reinterpret_cast<uint2*>(&sm.kt[8 * dg + e][4 * key4]) = w;
         }
       }
-      for (int c = threadIdx.x; c < kBwdBK * (kHeadDim / 8); c += kBwdThreads) {
+      for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kThreads) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         *reinterpret_cast<u32x4*>(&sm.v[key][8 * dg]) =
             key0 + key < g.kv_len ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
@@ -203,17 +210,20 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
     };
     load_pass(0);
 
-    for (int c = 0; c < nq; c += kBwdRowGroups * qpw) {
+    for (int c = 0; c < nq; c += qpw) {
       __syncthreads();                                // the previous pass is done with qt, dot, ds, row scalars
-      // transposed copies: key quarter kq writes the dims of k-step kq
+      // transposed copies: wave kq writes the dims of k-step kq % 4 (both
+      // row tiles with 4 waves; row tile kq / 4 with 8)
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
-        const int col = 32 * rg + 16 * t + c16;
-        const u32x4 wq = kq == 0 ? bq[t][0] : kq == 1 ? bq[t][1] : kq == 2 ? bq[t][2] : bq[t][3];
-        const u32x4 wd = kq == 0 ? bdo[t][0] : kq == 1 ? bdo[t][1] : kq == 2 ? bdo[t][2] : bdo[t][3];
-        store_transposed_pairs(sm.qt, 32 * kq + 8 * qd, col, wq);
-        store_transposed_pairs(sm.dot, 32 * kq + 8 * qd, col, wd);
-        if (qd == 0 && kq == 0) {
+        if (NKW == 8 && t != (kq >> 2)) continue;
+        const int ksw = kq & 3;
+        const int col = 16 * t + c16;
+        const u32x4 wq = ksw == 0 ? bq[t][0] : ksw == 1 ? bq[t][1] : ksw == 2 ? bq[t][2] : bq[t][3];
+        const u32x4 wd = ksw == 0 ? bdo[t][0] : ksw == 1 ? bdo[t][1] : ksw == 2 ? bdo[t][2] : bdo[t][3];
+        store_transposed_pairs(sm.qt, 32 * ksw + 8 * qd, col, wq);
+        store_transposed_pairs(sm.dot, 32 * ksw + 8 * qd, col, wd);
+        if (qd == 0 && ksw == 0) {
           const int qa = c + rg * qpw + (t ? jq1 : jq0);
           sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
           sm.dlt[col] = arow[t] ? dlt_v[t] : 0.f;
@@ -240,13 +250,13 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
         }
       }
       __builtin_amdgcn_sched_barrier(0);
-      if (c + kBwdRowGroups * qpw < nq) load_pass(c + kBwdRowGroups * qpw);
+      if (c + qpw < nq) load_pass(c + qpw);
       // P and dS in place: lane holds rows 16t + 4qd + i
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int prow = 32 * rg + 16 * t + 4 * qd + i;
+          const int prow = 16 * t + 4 * qd + i;
           const float l2 = sm.lse2[prow];
           const bool vis = key <= sm.rpos[prow] && l2 > -INFINITY;
           const float p = vis ? exp2f(acc_s[t][i] * scale_log2 - l2) : 0.f;
@@ -270,47 +280,56 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          sm.ds[rg][16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(sw[2 * t + (i >> 1)] >> (16 * (i & 1)));
+          sm.ds[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(sw[2 * t + (i >> 1)] >> (16 * (i & 1)));
       __builtin_amdgcn_sched_barrier(0);
       // dV += P^T dO, dK += dS^T Q over the 32 rows (one k-step), 8 dim tiles
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
-        const uint16_t* dr = &sm.dot[16 * t + c16][32 * rg + 4 * qd];
-        const uint16_t* qr = &sm.qt[16 * t + c16][32 * rg + 4 * qd];
+        const uint16_t* dr = &sm.dot[16 * t + c16][4 * qd];
+        const uint16_t* qr = &sm.qt[16 * t + c16][4 * qd];
         acc_dv[t] = mfma16x16x32(pa, lds_pair_bf16x8(dr, dr + 16), acc_dv[t]);
         acc_dk[t] = mfma16x16x32(sa, lds_pair_bf16x8(qr, qr + 16), acc_dk[t]);
         if (t & 1) __builtin_amdgcn_sched_barrier(0);   // bound the operand reads in flight
       }
-      __syncthreads();                                // dS of all 4 key quarters in LDS
+      __syncthreads();                                // dS of every key slice in LDS
 
-      // dQ of this row group, dims 32kq + 16u + c16, over the 64 keys
-      f32x4 acc_q[2][2];
+      // dQ of the pass, dims (128 / NKW) kq + 16u + c16, over the block's keys
+      f32x4 acc_q[2][DQU];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int u = 0; u < 2; ++u) {
+        for (int u = 0; u < DQU; ++u) {
           acc_q[t][u] = f32x4{};
 #pragma unroll
-          for (int ks = 0; ks < kBwdBK / 32; ++ks)
-            acc_q[t][u] = mfma16x16x32(ld_bf16x8(&sm.ds[rg][16 * t + c16][32 * ks + 8 * qd]),
-                                       ld_bf16x8(&sm.kt[32 * kq + 16 * u + c16][32 * ks + 8 * qd]), acc_q[t][u]);
+          for (int ks = 0; ks < BK / 32; ++ks)
+            acc_q[t][u] = mfma16x16x32(ld_bf16x8(&sm.ds[16 * t + c16][32 * ks + 8 * qd]),
+                                       ld_bf16x8(&sm.kt[(kHeadDim / NKW) * kq + 16 * u + c16][32 * ks + 8 * qd]),
+                                       acc_q[t][u]);
         }
       __builtin_amdgcn_sched_barrier(0);
-      // bf16 partial of each row into its incidence's slot: lanes c16 and
-      // c16 ^ 1 swap values so that each stores one bf16 pair (even lanes
-      // dims c16, c16 + 1; odd lanes dims 15 + c16, 16 + c16); rows without a
-      // query write the trash row (no branch around the stores)
+      // bf16 partial of each row into its incidence's slot; rows without a
+      // query write the trash row (no branch around the stores).  Two dQ tiles
+      // (4 waves): lanes c16 and c16 ^ 1 swap values so that each stores one
+      // bf16 pair (even lanes dims c16, c16 + 1 of tile 0; odd lanes dims
+      // 15 + c16, 16 + c16, i.e. c16 - 1, c16 of tile 1).  One tile (8
+      // waves): even lanes store dims c16, c16 + 1 with the odd neighbour's value.
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float v0 = acc_q[t][0][i], v1 = acc_q[t][1][i];
           const bool odd = c16 & 1;
-          const float mine = odd ? v1 : v0;
-          const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(odd ? v0 : v1)));
-          const uint32_t pair = odd ? pack_bf16x2(other, mine) : pack_bf16x2(mine, other);
-          uint16_t* dst = dq_buf + sm.dqoff[32 * rg + 16 * t + 4 * qd + i] + 32 * kq + (odd ? 15 + c16 : c16);
-          *reinterpret_cast<uint32_t*>(dst) = pair;
+          uint16_t* base = dq_buf + sm.dqoff[16 * t + 4 * qd + i] + (kHeadDim / NKW) * kq;
+          if constexpr (DQU == 2) {
+            const float v0 = acc_q[t][0][i], v1 = acc_q[t][1][i];
+            const float mine = odd ? v1 : v0;
+            const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(odd ? v0 : v1)));
+            const uint32_t pair = odd ? pack_bf16x2(other, mine) : pack_bf16x2(mine, other);
+            *reinterpret_cast<uint32_t*>(base + (odd ? 15 + c16 : c16)) = pair;
+          } else {
+            const float mine = acc_q[t][0][i];
+            const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(mine)));
+            if (!odd) *reinterpret_cast<uint32_t*>(base + c16) = pack_bf16x2(mine, other);
+          }
         }
     }
 
@@ -318,7 +337,7 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
 #pragma unroll
     for (int tensor = 0; tensor < 2; ++tensor) {
       const f32x4* acc = tensor == 0 ? acc_dv : acc_dk;
-      float* dst = part + (static_cast<int64_t>(item) * 2 + tensor) * (4 * 32 * 64) + kq * (32 * 64) + lane;
+      float* dst = part + (static_cast<int64_t>(item) * 2 + tensor) * (NKW * 32 * 64) + kq * (32 * 64) + lane;
 #pragma unroll
       for (int reg = 0; reg < 32; ++reg) dst[reg * 64] = acc[reg >> 2][reg & 3];
     }
@@ -326,28 +345,32 @@ __global__ __launch_bounds__(kBwdThreads, 2) void bwd_kvo_kernel(
 }
 
 // Per tile: the sum of its item partials, in item order, added to the fp32
-// accumulators of the block's keys.  kReduceSplit CTAs per tile, one float4
-// of the partial per thread, so every tile streams its partials with
-// independent loads.
-constexpr int kReduceSplit = kPartFloats / (4 * 256);
+// accumulators of the block's keys.  bwd_reduce_split<BK>() CTAs per tile,
+// one float4 of the partial per thread, so every tile streams its partials
+// with independent loads.
+template <int BK>
+constexpr int bwd_reduce_split() { return bwd_part_floats<BK>() / (4 * 256); }
+template <int BK>
 __global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
                                                               const int32_t* __restrict__ item_off, int H_kv,
                                                               int64_t nbcap, const float* __restrict__ part,
                                                               float* __restrict__ dk_acc, float* __restrict__ dv_acc) {
-  const int64_t tile = blockIdx.x / kReduceSplit;
+  constexpr int NKW = bwd_waves<BK>();
+  constexpr int kSplit = bwd_reduce_split<BK>();
+  const int64_t tile = blockIdx.x / kSplit;
   const int32_t i0 = item_off[tile], i1 = item_off[tile + 1];
   if (i0 == i1) return;
   const int r = static_cast<int>(tile / nbcap);
   const int64_t gb = tile % nbcap;
   const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
   const SeqGeom g = seq_geom(sq, s);
-  const int key0 = static_cast<int>(gb - blk_base[s]) * kBwdBK;
-  const int c4 = (blockIdx.x % kReduceSplit) * 256 + threadIdx.x;   // float4 of the partial
+  const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
+  const int c4 = (blockIdx.x % kSplit) * 256 + threadIdx.x;   // float4 of the partial
   const float4* p4 = reinterpret_cast<const float4*>(part) + c4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll 4
   for (int32_t it = i0; it < i1; ++it) {
-    const float4 x = p4[static_cast<int64_t>(it) * (kPartFloats / 4)];
+    const float4 x = p4[static_cast<int64_t>(it) * (bwd_part_floats<BK>() / 4)];
     acc.x += x.x;
     acc.y += x.y;
     acc.z += x.z;
@@ -355,8 +378,8 @@ __global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const
   }
   // partial layout [tensor][kq][reg][lane]: 4 consecutive lanes = 4 consecutive dims
   const int idx = 4 * c4;
-  const int tensor = idx / (4 * 32 * 64);
-  const int kq = (idx / (32 * 64)) & 3;
+  const int tensor = idx / (NKW * 32 * 64);
+  const int kq = (idx / (32 * 64)) % NKW;
   const int reg = (idx / 64) & 31;
   const int ln = idx & 63;
   const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
@@ -378,7 +401,7 @@ constexpr int kCombWaves = 4;
 
 __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
     const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_q, int H_kv,
-    int topk, int64_t row0, int64_t nrows, const uint16_t* __restrict__ dq_buf, float scale,
+    int BK, int topk, int64_t row0, int64_t nrows, const uint16_t* __restrict__ dq_buf, float scale,
     uint16_t* __restrict__ dq) {
   const int lane = lane_id();
   const int64_t pr = static_cast<int64_t>(blockIdx.x) * kCombWaves + threadIdx.x / kWave;
@@ -395,7 +418,7 @@ __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
   uint16_t* dst = dq + (row * H_q + static_cast<int64_t>(r) * G) * kHeadDim;
   // slot validity, one slot per lane; the valid slots' partials are then
   // read 8 at a time (in slot order) so their loads are in flight together
-  const bool mine = lane < topk && incidence_ok(ids[lane], p, kBwdBK, blk_base, s);
+  const bool mine = lane < topk && incidence_ok(ids[lane], p, BK, blk_base, s);
   const uint64_t valid = __ballot(mine);
   for (int c8 = lane; c8 < E / 8; c8 += kWave) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -450,6 +473,7 @@ __global__ __launch_bounds__(256) void bwd_kv_convert_kernel(const float* __rest
 
 // ---------------------------------------------------------------- host plan
 struct BwdPlan {
+  int BK;                                             // key block size (64 or 128)
   int64_t nbcap, ntile, chunk_rows, max_items;
   int nscan;
   size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_delta, off_dk, off_dv, off_handles,
@@ -475,12 +499,13 @@ void bwd_layout(BwdPlan& pl, const msa_seqs* seqs, int H_q, int H_kv, int topk) 
   pl.off_handles = o;  o = align_up(o + sizeof(uint32_t) * inc, 256);
   pl.off_tpos = o;     o = align_up(o + sizeof(int32_t) * inc, 256);
   pl.off_dq = o;       o = align_up(o + sizeof(uint16_t) * (inc * (H_q / H_kv) + 1) * kHeadDim, 256);   // + trash row
-  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * kPartFloats, 256);
+  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * 2 * pl.BK * kHeadDim, 256);
   pl.total = o;
 }
 
-int make_bwd_plan(const msa_seqs* seqs, int H_q, int H_kv, int topk, size_t budget, BwdPlan* pl) {
-  const int64_t nb = (seqs->max_kv_len + kBwdBK - 1) / kBwdBK;
+int make_bwd_plan(const msa_seqs* seqs, int H_q, int H_kv, int BK, int topk, size_t budget, BwdPlan* pl) {
+  pl->BK = BK;
+  const int64_t nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->nbcap = static_cast<int64_t>(seqs->num_seqs) * (nb > 0 ? nb : 1);
   pl->ntile = static_cast<int64_t>(H_kv) * pl->nbcap;
   if (pl->ntile >= (int64_t(1) << 31) - 1) return MSA_ERR_UNSUPPORTED;
@@ -518,28 +543,20 @@ int validate_bwd(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, 
   if (st != MSA_OK) return st;
   if (H_q < 1 || H_kv < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
   if (H_q % H_kv != 0) return MSA_ERR_INVALID;
-  if (head_dim != kHeadDim || (BK != kBwdBK && BK != 2 * kBwdBK)) return MSA_ERR_UNSUPPORTED;
-  if (BK == 2 * kBwdBK && topk > 32) return MSA_ERR_UNSUPPORTED;   // its 64-key halves fill <= 64 slots
+  if (head_dim != kHeadDim || (BK != 64 && BK != 128)) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
   return MSA_OK;
 }
 
-// Block size 128: each id is expanded to its two 64-key halves in front of
-// the workspace and the 64-key path runs on 2 topk slots.
-size_t expanded_ids_bytes(const msa_seqs* seqs, int H_kv, int BK, int topk) {
-  if (BK == kBwdBK) return 0;
-  return msa_host::align_up(sizeof(int32_t) * static_cast<size_t>(seqs->total_q_rows) * H_kv * topk *
-                                (BK / kBwdBK), 256);
-}
-
+template <int BK>
 int run_backward(const void* q, const void* k, const void* v, const void* o, const float* lse, const void* d_o,
                  const int32_t* block_ids, const msa_seqs* seqs, int H_q, int H_kv, int topk, float softmax_scale,
                  void* d_q, void* d_k, void* d_v, void* workspace, size_t workspace_bytes, hipStream_t stream) {
   int st;
   BwdPlan pl;
-  st = make_bwd_plan(seqs, H_q, H_kv, topk, workspace_bytes, &pl);
+  st = make_bwd_plan(seqs, H_q, H_kv, BK, topk, workspace_bytes, &pl);
   if (st != MSA_OK) return st;
   if (!workspace || workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
   char* ws = static_cast<char*>(workspace);
@@ -559,8 +576,7 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
   const int64_t kv_floats = seqs->total_kv_rows * H_kv * static_cast<int64_t>(kHeadDim);
   const unsigned zero_blocks = static_cast<unsigned>(std::min<int64_t>((kv_floats + 255) / 256, 8192));
 
-  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, kBwdBK,
-                   blk_base);
+  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK, blk_base);
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
                    reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
@@ -571,13 +587,13 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
                      dim3(256), 0, stream, static_cast<const uint16_t*>(o), static_cast<const uint16_t*>(d_o), pairs,
                      delta);
   static std::atomic<int> ctas {0};
-  const int nctas = persistent_ctas(bwd_kvo_kernel, kBwdThreads, &ctas);
+  const int nctas = persistent_ctas(bwd_kvo_kernel<BK>, bwd_threads<BK>(), &ctas);
   const float sl2 = softmax_scale * kLog2e;
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
-    build_reverse_index(block_ids, sq, blk_base, H_kv, kBwdBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
+    build_reverse_index(block_ids, sq, blk_base, H_kv, BK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
                         tile_off, item_off, blk_tot, tpos, handles, stream, true);
-    msa_prof::launch("bwd_kvo_kernel", bwd_kvo_kernel, dim3(nctas), dim3(kBwdThreads), 0, stream,
+    msa_prof::launch("bwd_kvo_kernel", bwd_kvo_kernel<BK>, dim3(nctas), dim3(bwd_threads<BK>()), 0, stream,
                      static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                      static_cast<const uint16_t*>(v), static_cast<const uint16_t*>(d_o), lse,
                      static_cast<const float*>(delta), sq, static_cast<const int64_t*>(blk_base),
@@ -585,13 +601,13 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
                      static_cast<const uint32_t*>(handles), H_q, H_kv, topk, pl.nbcap, r0, sl2, dq_buf,
                      static_cast<int64_t>(pl.chunk_rows) * H_kv * topk * (H_q / H_kv) * kHeadDim, part,
                      cnt + pl.ntile);
-    msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel, dim3(static_cast<unsigned>(pl.ntile * kReduceSplit)),
-                     dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
-                     static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc,
-                     dv_acc);
+    msa_prof::launch("bwd_tile_reduce_kernel", bwd_tile_reduce_kernel<BK>,
+                     dim3(static_cast<unsigned>(pl.ntile * bwd_reduce_split<BK>())), dim3(256), 0, stream, sq,
+                     static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(item_off), H_kv, pl.nbcap,
+                     static_cast<const float*>(part), dk_acc, dv_acc);
     msa_prof::launch("bwd_dq_combine_kernel", bwd_dq_combine_kernel,
                      dim3(static_cast<unsigned>((nr * H_kv + kCombWaves - 1) / kCombWaves)), dim3(64 * kCombWaves),
-                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_q, H_kv, topk, r0, nr,
+                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_q, H_kv, BK, topk, r0, nr,
                      static_cast<const uint16_t*>(dq_buf), softmax_scale, static_cast<uint16_t*>(d_q));
   }
   if (kv_floats > 0)
@@ -606,14 +622,13 @@ int run_backward(const void* q, const void* k, const void* v, const void* o, con
 extern "C" size_t msa_sparse_attn_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
                                                          int head_dim, int block_size, int topk) {
   if (validate_bwd(seqs, num_q_heads, num_kv_heads, head_dim, block_size, topk) != MSA_OK) return 0;
-  const int topk64 = topk * (block_size / kBwdBK);
   BwdPlan pl;
-  if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk64, kDefaultBwdBytes, &pl) != MSA_OK) {
-    if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, topk64, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+  if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, block_size, topk, kDefaultBwdBytes, &pl) != MSA_OK) {
+    if (make_bwd_plan(seqs, num_q_heads, num_kv_heads, block_size, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
     pl.chunk_rows = 1;
-    bwd_layout(pl, seqs, num_q_heads, num_kv_heads, topk64);
+    bwd_layout(pl, seqs, num_q_heads, num_kv_heads, topk);
   }
-  return expanded_ids_bytes(seqs, num_kv_heads, block_size, topk) + pl.total;
+  return pl.total;
 }
 
 extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const void* o, const float* lse,
@@ -626,18 +641,9 @@ extern "C" int msa_sparse_attn_backward(const void* q, const void* k, const void
   if (st != MSA_OK) return st;
   if (!q || !k || !v || !o || !lse || !d_o || !block_ids || !d_q || !d_k || !d_v) return MSA_ERR_INVALID;
   if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
-  const size_t xb = expanded_ids_bytes(seqs, H_kv, block_size, topk);
-  if (xb == 0)
-    return run_backward(q, k, v, o, lse, d_o, block_ids, seqs, H_q, H_kv, topk, softmax_scale, d_q, d_k, d_v,
-                        workspace, workspace_bytes, stream);
-  if (!workspace || workspace_bytes < xb) return MSA_ERR_WORKSPACE;
-  const int f = block_size / kBwdBK;
-  auto* ids64 = static_cast<int32_t*>(workspace);
-  const int64_t pairs = seqs->total_q_rows * H_kv;
-  if (pairs > 0)
-    msa_prof::launch("expand_block_ids_kernel", expand_block_ids_kernel,
-                     dim3(static_cast<unsigned>((pairs + 255) / 256)), dim3(256), 0, stream, block_ids, pairs, topk, f,
-                     ids64);
-  return run_backward(q, k, v, o, lse, d_o, ids64, seqs, H_q, H_kv, topk * f, softmax_scale, d_q, d_k, d_v,
-                      static_cast<char*>(workspace) + xb, workspace_bytes - xb, stream);
+  if (block_size == 64)
+    return run_backward<64>(q, k, v, o, lse, d_o, block_ids, seqs, H_q, H_kv, topk, softmax_scale, d_q, d_k, d_v,
+                            workspace, workspace_bytes, stream);
+  return run_backward<128>(q, k, v, o, lse, d_o, block_ids, seqs, H_q, H_kv, topk, softmax_scale, d_q, d_k, d_v,
+                           workspace, workspace_bytes, stream);
 }

@@ -49,6 +49,8 @@ CASES = [
     ("bwd_many_items_k32", [2048], [2048], 16, 2, 32, None),
     ("bwd_bk128_g16", [900], [900], 32, 2, 5, None, 128),
     ("bwd_bk128_chunked_varlen", [200, 1, 129], [1000, 700, 1500], 16, 2, 4, None, 128),
+    ("bwd_bk128_k48_g8", [3000], [3000], 32, 4, 24, None, 128),
+    ("bwd_bk128_decode_padded", [1, 1, 1], [3000, 129, 4097], 16, 2, 6, 4224, 128),
 ]
 
 
@@ -157,12 +159,12 @@ def test_backward_reproducible_on_crowded_tiles():
 
 
 def test_backward_block_128_limits():
-    """Block size 128 runs as its 64-key halves: topk <= 32 (the halves fill
-    <= 64 slots); other block sizes are rejected."""
+    """Block size 128 runs its own kernel (8 waves of 16 keys) with up to 64
+    slots, like block size 64; other block sizes are rejected."""
     p = synth.packed_problem("bwd_bk128", [10], [10], num_q_heads=8, num_kv_heads=2, topk=2, seed=1)
     seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
-    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 32) > 0
-    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 33) == 0
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 64) > 0
+    assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 128, 65) == 0
     assert msa.sparse_attn_backward_workspace_size(seqs, 8, 2, 128, 256, 2) == 0
 
 
