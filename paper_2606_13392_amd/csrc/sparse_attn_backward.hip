@@ -19,15 +19,19 @@
 //   bwd_delta        D per (row, head)
 //   per chunk of query rows:
 //     reverse index  (kvo_index.h)
-//     bwd_kvo        persistent CTAs of 4 waves, two per CU, over the work
-//                    items (<= 256 queries of one tile).  K, V and K^T of the
-//                    block sit in LDS.  A CTA pass takes 32 gathered (query,
-//                    head) rows; wave kq owns keys 16kq .. 16kq+15: S = Q K^T
+//     bwd_kvo        persistent CTAs of B_k / 16 waves (two CTAs per CU at
+//                    B_k 64, one at 128) over the work items (<= 256 queries
+//                    of one tile).  K and V of the block sit in LDS row-major.
+//                    A pass takes 32 gathered (query, head) rows, whose Q and
+//                    dO rows are copied from HBM straight into LDS (DMA) one
+//                    pass ahead; wave kq owns keys 16kq .. 16kq+15: S = Q K^T
 //                    and dP = dO V^T (MFMA 16x16x32, one key per lane column),
-//                    then dV += P^T dO and dK += dS^T Q from transposed copies
-//                    of the pass's Q and dO rows, then dQ over all 64 keys
-//                    for dims 32kq .. 32kq+31 from dS staged in LDS.  At the
-//                    end of an item each wave writes its keys' dK / dV as the
+//                    then dV += P^T dO and dK += dS^T Q, their B operands read
+//                    down the columns of the row-major Q / dO rows with
+//                    transposing LDS reads, then dQ over the block's keys for
+//                    the wave's dims from dS staged in LDS (K read the same
+//                    way); dQ partials are stored one pass late.  At the end
+//                    of an item each wave writes its keys' dK / dV as the
 //                    item's partial.
 //     bwd_tile_reduce  per tile: its items' partials, in order, added to fp32
 //                    dK / dV accumulators
@@ -49,22 +53,49 @@ constexpr int bwd_part_floats() { return 2 * BK * kHeadDim; }   // dK and dV of 
 
 template <int BK>
 struct BwdSmem {
-  uint16_t k[BK][kHeadDim + 8];                       // K block, row-major
+  uint16_t k[BK][kHeadDim + 16];                      // K block, row-major (+32 B: transposing reads of 4 rows
+                                                      // x 32 B hit distinct banks)
   uint16_t v[BK][kHeadDim + 8];                       // V block, row-major
-  uint16_t kt[kHeadDim][BK + 8];                      // K block transposed
-  uint16_t qt[kHeadDim][kBwdPassRows + 8];            // Q rows of the pass, transposed
-  uint16_t dot[kHeadDim][kBwdPassRows + 8];           // dO rows of the pass, transposed
+  // Q and dO rows of a pass (double-buffered), row-major with 16-byte
+  // segments XOR-swizzled by row (bwd_qrow_off); filled by DMA
+  uint16_t qdo[2][2][kBwdPassRows][kHeadDim];
   uint16_t ds[32][BK + 8];                            // dS of the pass, [row][key]
-  float lse2[kBwdPassRows];                           // LSE * log2(e) per pass row (+inf: no row)
-  float dlt[kBwdPassRows];                            // D per pass row
-  int32_t rpos[kBwdPassRows];                         // absolute position per pass row (-1: no row)
-  int64_t dqoff[kBwdPassRows];                        // element offset of the row's dQ partial (the trash row: no row)
+  float lse2[2][kBwdPassRows];                        // LSE * log2(e) per pass row (+inf: no row)
+  float dlt[2][kBwdPassRows];                         // D per pass row
+  int32_t rpos[2][kBwdPassRows];                      // absolute position per pass row (-1: no row)
+  int64_t dqoff[2][kBwdPassRows];                     // element offset of the row's dQ partial (the trash row: no row)
   int32_t s_row[kItemQueries];                        // query row inside the chunk
   int32_t s_slot[kItemQueries];                       // slot of this block in the row's id list
 };
 // B_k 64: two CTAs per CU; B_k 128: one CTA of 8 waves
 static_assert(sizeof(BwdSmem<64>) <= 80 * 1024, "LDS of a B_k 64 backward CTA");
 static_assert(sizeof(BwdSmem<128>) <= 160 * 1024, "LDS of a B_k 128 backward CTA");
+
+// Byte offset of element (row, col) in a pass buffer: 256-byte rows whose
+// 16-byte segments are XOR-swizzled by the row's low 4 bits, so that the
+// 16-byte operand reads of 16 rows and the transposing reads of 4 rows both
+// spread over the banks.
+__device__ __forceinline__ int bwd_qrow_off(int row, int col) {
+  return row * (kHeadDim * 2) + 16 * ((col >> 3) ^ (row & 15)) + 2 * (col & 7);
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+// Transposing LDS read (ds_read_b64_tr_b16): within each 16-lane group, lane
+// j supplies the address of 4 consecutive bf16 elements, and lane 4a + b
+// receives element b of the loads of lanes a, a + 4, a + 8, a + 12.  With lane
+// j pointing at row k0 + j / 4, columns n0 + 4 (j % 4) .. + 3 of a row-major
+// tile, lane n receives rows k0 .. k0 + 3 of column n0 + n: a 4-element slice
+// of an MFMA B operand that runs down a column.
+__device__ __forceinline__ uint2 lds_tr4(const void* p) {
+  const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(v4i16*)(const_cast<void*>(p)));
+  return __builtin_bit_cast(uint2, x);
+}
+// One 16-byte piece per lane from global memory into LDS (global_load_lds):
+// lane l writes bytes [16 l, 16 l + 16) after the wave-uniform LDS address dst.
+__device__ __forceinline__ void bwd_dma16(const void* src, void* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
 
 __device__ __forceinline__ uint16_t raw_elem(const u32x4& w, int j) {
   return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
@@ -95,12 +126,15 @@ __global__ __launch_bounds__(256) void bwd_delta_kernel(const uint16_t* __restri
   if (pair < pairs && part == 0) delta[pair] = acc;
 }
 
-// Wave (kq, rg): keys 16kq .. 16kq+15 of the block, rows 32rg .. 32rg+31 of
-// each CTA pass.  MFMA 16x16x32: lane l = (c = l % 16, quarter qd = l / 16).
-// In S = Q K^T and dP = dO V^T the lane holds key 16kq + c and, of row tile
-// t, rows 16t + 4qd + i (i = 0..3).  Those 8 rows are the k-slice the lane
-// supplies to dV += P^T dO and dK += dS^T Q (k index 8qd + 4t + i), and
-// the B operands read the same rows from the transposed Q / dO copies.
+// Wave kq owns keys 16kq .. 16kq+15 of the block.  MFMA 16x16x32: lane
+// l = (c = l % 16, quarter qd = l / 16).  In S = Q K^T and dP = dO V^T the
+// lane holds key 16kq + c and, of row tile t, rows 16t + 4qd + i (i = 0..3).
+// Those 8 rows are the k-slice the lane supplies to dV += P^T dO and
+// dK += dS^T Q (k index 8qd + 4t + i); the B operands read the same rows down
+// each column of the row-major Q / dO pass buffers with transposing LDS
+// reads, and dQ's B operand reads K the same way.  A pass's Q and dO rows are
+// gathered straight into LDS (DMA) one pass ahead; its dQ partials are
+// stored at the start of the next pass, so neither waits on memory.
 template <int BK>
 __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
@@ -111,23 +145,24 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
   constexpr int NKW = bwd_waves<BK>();                // waves = 16-key slices of the block
   constexpr int kThreads = bwd_threads<BK>();
   static_assert(kItemQueries <= kThreads, "every thread loads at most one handle of an item");
+  static_assert(2 * (kBwdPassRows / 4) % NKW == 0, "DMA pieces split evenly over the waves");
   __shared__ BwdSmem<BK> sm;
   __shared__ int32_t s_claim;
   constexpr int KS = kHeadDim / 32;                   // k-steps of S and dP over the head dimension
   constexpr int DQU = 8 / NKW;                        // 16-dim tiles of dQ per wave
+  constexpr int kDma = 2 * (kBwdPassRows / 4) / NKW;  // 1 KiB DMA pieces per wave and pass
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int kq = wave, rg = 0;
+  const int kq = wave;
   const int c16 = lane & 15, qd = lane >> 4;
   const int G = H_q / H_kv;
-  const int qpw = 32 / G;                             // queries per row group and pass
-  // this lane's A-operand rows 16t + c16: (query within the pass, head)
-  const int jq0 = c16 / G, hh0 = c16 % G, jq1 = (16 + c16) / G, hh1 = (16 + c16) % G;
-  const int rows_g = qpw * G;                         // used rows of a row group
+  const int qpw = 32 / G;                             // queries per pass
+  const int rows_g = qpw * G;                         // used rows of a pass
   const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
   const int32_t total_items = item_off[ntile];
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
+  const uint8_t* kbytes = reinterpret_cast<const uint8_t*>(&sm.k[0][0]);
 
   for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
@@ -142,126 +177,142 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
     __syncthreads();                                  // the previous item is done with LDS
     if (static_cast<int>(threadIdx.x) < nq) {
       const uint32_t hd = handles[h0 + threadIdx.x];
-      const int32_t rl = static_cast<int32_t>(hd >> 6);
-      sm.s_row[threadIdx.x] = rl;
+      sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
       sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
     }
     const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);   // + row in chunk
     if (tile != staged) {
       const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      // K row-major and transposed: a thread takes 4 keys x 8 dims
-      for (int c = threadIdx.x; c < (BK / 4) * (kHeadDim / 8); c += kThreads) {
-        const int key4 = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
-        u32x4 rows[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int key = 4 * key4 + j;
-          rows[j] = key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
-          *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) = rows[j];
-        }
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          uint2 w;
-          w.x = static_cast<uint32_t>(raw_elem(rows[0], e)) | (static_cast<uint32_t>(raw_elem(rows[1], e)) << 16);
-          w.y = static_cast<uint32_t>(raw_elem(rows[2], e)) | (static_cast<uint32_t>(raw_elem(rows[3], e)) << 16);
-          *reinterpret_cast<uint2*>(&sm.kt[8 * dg + e][4 * key4]) = w;
-        }
-      }
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kThreads) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
+        const bool in = key0 + key < g.kv_len;
+        *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) =
+            in ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
         *reinterpret_cast<u32x4*>(&sm.v[key][8 * dg]) =
-            key0 + key < g.kv_len ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
+            in ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
       }
       staged = tile;
     }
-    __syncthreads();
+    __syncthreads();                                  // handles (and K / V) in LDS
+
+    // pass row ra of the pass at item query cc: (query cc + ra / G, head ra % G);
+    // rows past the pass's queries read a valid row (their P and dS are zero)
+    auto pass_row = [&](int cc, int ra, bool& ok) -> int64_t {
+      const int qa = cc + ra / G;
+      ok = ra < rows_g && qa < nq;
+      const int ro = ok ? ra : 0;
+      const int64_t grow = row0 + sm.s_row[ok ? qa : min(cc, nq - 1)];
+      return grow * H_q + static_cast<int64_t>(r) * G + ro % G;
+    };
+    // Q and dO rows of the pass at cc into buffer b: wave kq issues kDma 1 KiB
+    // pieces (4 rows each); lane l of a piece writes slot l % 16 of row
+    // 4 piece + l / 16, which holds the row's segment (slot ^ row) % 16
+    auto issue_dma = [&](int cc, int b) {
+#pragma unroll
+      for (int i = 0; i < kDma; ++i) {
+        const int piece = kq * kDma + i;              // 0 .. 15: tensor piece / 8, rows 4 (piece % 8) ..
+        const int tensor = piece >> 3;
+        const int ra = 4 * (piece & 7) + (lane >> 4);
+        bool ok;
+        const int64_t hr = pass_row(cc, ra, ok);
+        const int seg = (lane & 15) ^ (ra & 15);
+        const uint16_t* src = (tensor == 0 ? q : d_o) + hr * kHeadDim + 8 * seg;
+        bwd_dma16(src, &sm.qdo[b][tensor][4 * (piece & 7)][0]);
+      }
+    };
+    // the pass's row scalars: lanes 0..31 of wave 0 load them ...
+    float nl = 0.f, nd = 0.f;
+    int32_t npos = -1;
+    int64_t noff = dq_trash;
+    auto load_scalars = [&](int cc) {
+      if (kq == 0 && lane < kBwdPassRows) {
+        bool ok;
+        const int64_t hr = pass_row(cc, lane, ok);
+        nl = lse[hr];
+        nd = delta[hr];
+        const int qa = cc + lane / G;
+        npos = ok ? pos_base + sm.s_row[qa] : -1;
+        noff = ok ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G + lane % G) *
+                        kHeadDim
+                  : dq_trash;
+        if (!ok) nl = INFINITY;
+      }
+    };
+    // ... and store them into the other buffer once every wave has stored the
+    // previous pass's dQ (which reads that buffer's offsets)
+    auto store_scalars = [&](int b) {
+      if (kq == 0 && lane < kBwdPassRows) {
+        sm.lse2[b][lane] = nl == INFINITY ? INFINITY : nl * kLog2e;
+        sm.dlt[b][lane] = nd;
+        sm.rpos[b][lane] = npos;
+        sm.dqoff[b][lane] = noff;
+      }
+    };
 
     f32x4 acc_dv[8], acc_dk[8];                       // [dim tile]: lane column = dim, rows = keys 4qd + i
 #pragma unroll
     for (int t = 0; t < 8; ++t) { acc_dv[t] = f32x4{}; acc_dk[t] = f32x4{}; }
     const int key = key0 + 16 * kq + c16;             // this lane's key in the C layout of S
-
-    // A operands of a pass: Q and dO of rows 16t + c16 of this row group, dims
-    // 32ks + 8qd .. +8, plus the rows' LSE and D.  The next pass's are
-    // requested as soon as S and dP have consumed the current ones.
-    u32x4 bq[2][KS], bdo[2][KS];
-    int64_t hrow[2];
-    bool arow[2];
-    float lse_v[2], dlt_v[2];
-    auto load_pass = [&](int cc) {
+    // dQ values of the previous pass, stored one pass late
+    uint32_t dq_pend[2][4];
+    int pend_buf = -1;
+    auto store_dq = [&](int b) {
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int ra = 16 * t + c16;
-        const int qa = cc + rg * qpw + (t ? jq1 : jq0);
-        arow[t] = ra < rows_g && qa < nq;
-        // rows without a query load a valid row of the item: their P and dS
-        // are zero, so any finite operand values give zero contributions
-        const int64_t grow = row0 + sm.s_row[min(qa, nq - 1)];
-        hrow[t] = grow * H_q + static_cast<int64_t>(r) * G + (t ? hh1 : hh0);
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int st = 0; st < KS; ++st) {
-          bq[t][st] = load_raw(q + hrow[t] * kHeadDim + 32 * st + 8 * qd);
-          bdo[t][st] = load_raw(d_o + hrow[t] * kHeadDim + 32 * st + 8 * qd);
+        for (int i = 0; i < 4; ++i) {
+          const bool odd = c16 & 1;
+          uint16_t* base = dq_buf + sm.dqoff[b][16 * t + 4 * qd + i] + (kHeadDim / NKW) * kq;
+          if constexpr (DQU == 2) *reinterpret_cast<uint32_t*>(base + (odd ? 15 + c16 : c16)) = dq_pend[t][i];
+          else if (!odd) *reinterpret_cast<uint32_t*>(base + c16) = dq_pend[t][i];
         }
-        lse_v[t] = lse[hrow[t]];
-        dlt_v[t] = delta[hrow[t]];
-      }
     };
-    load_pass(0);
 
-    for (int c = 0; c < nq; c += qpw) {
-      __syncthreads();                                // the previous pass is done with qt, dot, ds, row scalars
-      // transposed copies: wave kq writes the dims of k-step kq % 4 (both
-      // row tiles with 4 waves; row tile kq / 4 with 8)
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        if (NKW == 8 && t != (kq >> 2)) continue;
-        const int ksw = kq & 3;
-        const int col = 16 * t + c16;
-        const u32x4 wq = ksw == 0 ? bq[t][0] : ksw == 1 ? bq[t][1] : ksw == 2 ? bq[t][2] : bq[t][3];
-        const u32x4 wd = ksw == 0 ? bdo[t][0] : ksw == 1 ? bdo[t][1] : ksw == 2 ? bdo[t][2] : bdo[t][3];
-        store_transposed_pairs(sm.qt, 32 * ksw + 8 * qd, col, wq);
-        store_transposed_pairs(sm.dot, 32 * ksw + 8 * qd, col, wd);
-        if (qd == 0 && ksw == 0) {
-          const int qa = c + rg * qpw + (t ? jq1 : jq0);
-          sm.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
-          sm.dlt[col] = arow[t] ? dlt_v[t] : 0.f;
-          sm.rpos[col] = arow[t] ? pos_base + sm.s_row[qa] : -1;
-          sm.dqoff[col] = arow[t] ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G +
-                                     (t ? hh1 : hh0)) * kHeadDim
-                                  : dq_trash;
-        }
+    issue_dma(0, 0);
+    load_scalars(0);
+    store_scalars(0);
+    int buf = 0;
+    for (int c = 0; c < nq; c += qpw, buf ^= 1) {
+      __builtin_amdgcn_s_waitcnt(0);                  // this wave's DMA pieces of the pass have landed
+      __syncthreads();                                // every wave's pieces, the pass's scalars; the
+                                                      // previous pass is done with ds and the other buffer
+      if (pend_buf >= 0) store_dq(pend_buf);
+      const bool more = c + qpw < nq;
+      if (more) {
+        issue_dma(c + qpw, buf ^ 1);
+        load_scalars(c + qpw);
       }
-      __syncthreads();
+      const uint8_t* qb = reinterpret_cast<const uint8_t*>(&sm.qdo[buf][0][0][0]);
+      const uint8_t* dob = reinterpret_cast<const uint8_t*>(&sm.qdo[buf][1][0][0]);
 
-      // S = Q K^T, dP = dO V^T for this row group x this key quarter
+      // S = Q K^T, dP = dO V^T for this key slice
       f32x4 acc_s[2], acc_dp[2];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         acc_s[t] = f32x4{};
         acc_dp[t] = f32x4{};
+        const int ra = 16 * t + c16;
 #pragma unroll
         for (int st = 0; st < KS; ++st) {
-          acc_s[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
+          const int off = bwd_qrow_off(ra, 32 * st + 8 * qd);
+          acc_s[t] = mfma16x16x32(*reinterpret_cast<const bf16x8*>(qb + off),
                                   ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
-          acc_dp[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bdo[t][st]),
+          acc_dp[t] = mfma16x16x32(*reinterpret_cast<const bf16x8*>(dob + off),
                                    ld_bf16x8(&sm.v[16 * kq + c16][32 * st + 8 * qd]), acc_dp[t]);
         }
       }
-      __builtin_amdgcn_sched_barrier(0);
-      if (c + qpw < nq) load_pass(c + qpw);
       // P and dS in place: lane holds rows 16t + 4qd + i
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int prow = 16 * t + 4 * qd + i;
-          const float l2 = sm.lse2[prow];
-          const bool vis = key <= sm.rpos[prow] && l2 > -INFINITY;
+          const float l2 = sm.lse2[buf][prow];
+          const bool vis = key <= sm.rpos[buf][prow] && l2 > -INFINITY;
           const float p = vis ? exp2f(acc_s[t][i] * scale_log2 - l2) : 0.f;
           acc_s[t][i] = p;
-          acc_dp[t][i] = p * (acc_dp[t][i] - sm.dlt[prow]);
+          acc_dp[t][i] = p * (acc_dp[t][i] - sm.dlt[buf][prow]);
         }
       // A operands of dV and dK: k index 8qd + 4t + i = row 16t + 4qd + i
       uint4 pw, sw;
@@ -282,56 +333,71 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
         for (int i = 0; i < 4; ++i)
           sm.ds[16 * t + 4 * qd + i][16 * kq + c16] = static_cast<uint16_t>(sw[2 * t + (i >> 1)] >> (16 * (i & 1)));
       __builtin_amdgcn_sched_barrier(0);
-      // dV += P^T dO, dK += dS^T Q over the 32 rows (one k-step), 8 dim tiles
+      // dV += P^T dO, dK += dS^T Q over the 32 rows (one k-step), 8 dim tiles;
+      // B: rows 4qd .. 4qd + 3 and 16 + 4qd .. 16 + 4qd + 3 of dim 16t + c16
+      // (lane j of a quarter points at row 4qd (+ 16) + j / 4, dims 16t + 4 (j % 4) ..)
+      const int tr_row = 4 * qd + (c16 >> 2);
+      const int tr_col = 4 * (c16 & 3);
 #pragma unroll
       for (int t = 0; t < 8; ++t) {
-        const uint16_t* dr = &sm.dot[16 * t + c16][4 * qd];
-        const uint16_t* qr = &sm.qt[16 * t + c16][4 * qd];
-        acc_dv[t] = mfma16x16x32(pa, lds_pair_bf16x8(dr, dr + 16), acc_dv[t]);
-        acc_dk[t] = mfma16x16x32(sa, lds_pair_bf16x8(qr, qr + 16), acc_dk[t]);
+        const int o0 = bwd_qrow_off(tr_row, 16 * t + tr_col), o1 = bwd_qrow_off(16 + tr_row, 16 * t + tr_col);
+        const uint2 d0 = lds_tr4(dob + o0), d1 = lds_tr4(dob + o1);
+        const uint2 q0 = lds_tr4(qb + o0), q1 = lds_tr4(qb + o1);
+        acc_dv[t] = mfma16x16x32(pa, __builtin_bit_cast(bf16x8, make_uint4(d0.x, d0.y, d1.x, d1.y)), acc_dv[t]);
+        acc_dk[t] = mfma16x16x32(sa, __builtin_bit_cast(bf16x8, make_uint4(q0.x, q0.y, q1.x, q1.y)), acc_dk[t]);
         if (t & 1) __builtin_amdgcn_sched_barrier(0);   // bound the operand reads in flight
       }
-      __syncthreads();                                // dS of every key slice in LDS
+      __syncthreads();                                // dS of every key slice in LDS; every wave's
+                                                      // store_dq of this pass has read the other buffer
+      if (more) store_scalars(buf ^ 1);               // the next pass's scalars (their loads have landed)
 
-      // dQ of the pass, dims (128 / NKW) kq + 16u + c16, over the block's keys
+      // dQ of the pass, dims (128 / NKW) kq + 16u + c16, over the block's keys;
+      // B: keys 32ks + 8qd .. + 7 of that dim, read down K's column
       f32x4 acc_q[2][DQU];
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
-        for (int u = 0; u < DQU; ++u) {
-          acc_q[t][u] = f32x4{};
+        for (int u = 0; u < DQU; ++u) acc_q[t][u] = f32x4{};
 #pragma unroll
-          for (int ks = 0; ks < BK / 32; ++ks)
-            acc_q[t][u] = mfma16x16x32(ld_bf16x8(&sm.ds[16 * t + c16][32 * ks + 8 * qd]),
-                                       ld_bf16x8(&sm.kt[(kHeadDim / NKW) * kq + 16 * u + c16][32 * ks + 8 * qd]),
-                                       acc_q[t][u]);
+      for (int u = 0; u < DQU; ++u) {
+        const int n0 = (kHeadDim / NKW) * kq + 16 * u;
+#pragma unroll
+        for (int ks = 0; ks < BK / 32; ++ks) {
+          const int krow = 32 * ks + 8 * qd + (c16 >> 2);
+          const uint2 k0v = lds_tr4(kbytes + (krow * (kHeadDim + 16) + n0 + tr_col) * 2);
+          const uint2 k1v = lds_tr4(kbytes + ((krow + 4) * (kHeadDim + 16) + n0 + tr_col) * 2);
+          const bf16x8 kb8 = __builtin_bit_cast(bf16x8, make_uint4(k0v.x, k0v.y, k1v.x, k1v.y));
+#pragma unroll
+          for (int t = 0; t < 2; ++t)
+            acc_q[t][u] = mfma16x16x32(ld_bf16x8(&sm.ds[16 * t + c16][32 * ks + 8 * qd]), kb8, acc_q[t][u]);
         }
+      }
       __builtin_amdgcn_sched_barrier(0);
-      // bf16 partial of each row into its incidence's slot; rows without a
-      // query write the trash row (no branch around the stores).  Two dQ tiles
-      // (4 waves): lanes c16 and c16 ^ 1 swap values so that each stores one
-      // bf16 pair (even lanes dims c16, c16 + 1 of tile 0; odd lanes dims
-      // 15 + c16, 16 + c16, i.e. c16 - 1, c16 of tile 1).  One tile (8
-      // waves): even lanes store dims c16, c16 + 1 with the odd neighbour's value.
+      // bf16 partials of the pass's rows, stored at the start of the next pass
+      // (rows without a query go to the trash row).  Two dQ tiles (4 waves):
+      // lanes c16 and c16 ^ 1 swap values so that each stores one bf16 pair
+      // (even lanes dims c16, c16 + 1 of tile 0; odd lanes dims c16 - 1, c16
+      // of tile 1).  One tile (8 waves): even lanes store dims c16, c16 + 1.
 #pragma unroll
       for (int t = 0; t < 2; ++t)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const bool odd = c16 & 1;
-          uint16_t* base = dq_buf + sm.dqoff[16 * t + 4 * qd + i] + (kHeadDim / NKW) * kq;
           if constexpr (DQU == 2) {
             const float v0 = acc_q[t][0][i], v1 = acc_q[t][1][i];
             const float mine = odd ? v1 : v0;
             const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(odd ? v0 : v1)));
-            const uint32_t pair = odd ? pack_bf16x2(other, mine) : pack_bf16x2(mine, other);
-            *reinterpret_cast<uint32_t*>(base + (odd ? 15 + c16 : c16)) = pair;
+            dq_pend[t][i] = odd ? pack_bf16x2(other, mine) : pack_bf16x2(mine, other);
           } else {
             const float mine = acc_q[t][0][i];
             const float other = __uint_as_float(xor_lane_u32<1>(__float_as_uint(mine)));
-            if (!odd) *reinterpret_cast<uint32_t*>(base + c16) = pack_bf16x2(mine, other);
+            dq_pend[t][i] = pack_bf16x2(mine, other);
           }
         }
+      pend_buf = buf;
     }
+    // the last pass's dQ: its scalars stay valid until the next item's barrier
+    if (pend_buf >= 0) store_dq(pend_buf);
 
     // item end: the item's dV / dK partial, [tensor][kq][reg][lane]
 #pragma unroll
