@@ -6,15 +6,20 @@
 //
 // Prefill (dense_prefill_kernel), FlashAttention-2 order: a CTA owns one KV
 // group and a tile of consecutive query rows whose G heads share the group's
-// K and V; its 4 waves hold 32 (query row, head) rows each.  Key blocks of 64
-// are streamed through a double-buffered LDS ring (K row-major, V transposed)
-// fed by register prefetch one block ahead; per block each wave computes
-// S^T = K Q^T and O^T += V^T P^T with MFMA 32x32x16 and keeps the online
-// softmax (running max and sum per row) in registers.
+// K and V; its 8 waves hold 32 (query row, head) rows each, one CTA per CU.
+// Key blocks of 64 are copied into a double-buffered LDS ring by DMA
+// (global_load_lds, one block ahead, rows stored with a bank-conflict-free
+// segment permutation); per block each wave computes S^T = K Q^T and
+// O^T += V^T P^T with MFMA 32x32x16, the V^T operand read down V's columns
+// with transposing LDS reads.  The O MFMAs of block b are interleaved by
+// hand with the online softmax of block b+1 (running max and sum per row in
+// registers, raw hardware exp2, row sums by bf16 dot products over the same
+// rounded weights that multiply V).
 //
 // Decode (at most four query rows per sequence) runs the row kernel of the
 // sparse decode call over every key block (msa_rows_dense).
 #include <algorithm>
+#include <type_traits>
 
 #include "msa_common.h"
 #include "msa_profile.h"
@@ -30,15 +35,26 @@ using namespace msa;
 
 constexpr int kHeadDim = 128;
 constexpr int kBK = 64;                  // keys per streamed block
-constexpr int kThreads = 256;            // 4 waves
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kDecodeRows = 4;           // sequences with at most this many query rows take the row kernel
+constexpr int kWaves = 8;                // waves per CTA (32 MFMA rows each), one CTA per CU
+constexpr int kThreads = kWaves * kWave;
+constexpr int kAhead = 3;                // LDS operand reads issued this many MFMA slots ahead
 
-struct DenseSmem {
-  uint16_t k[2][kBK][kHeadDim + 8];      // K blocks, row-major (+16 B pad per row)
-  uint16_t vt[2][kHeadDim][kBK + 4];     // V blocks transposed (+8 B pad per row)
+// Key blocks in LDS, row-major, 16-byte segments permuted per row (an XOR
+// with a row-dependent mask) so that every read pattern is free of bank
+// conflicts whether the LDS serves 16 or 32 lanes of a wave per cycle:
+//   K (16 bytes per lane: 32 consecutive rows x the two segments of a k-step)
+//     segment s of row r at s ^ (2 (r & 7) + ((r >> 3) & 1));
+//   V (ds_read_tr16_b64: 4 consecutive rows x 4 adjacent segments per 32
+//     lanes) segment s of row r at s ^ 4 (r & 3).
+struct DenseRing {
+  uint16_t k[2][kBK * kHeadDim];
+  uint16_t v[2][kBK * kHeadDim];
 };
+__device__ __forceinline__ int k_seg(int r, int s) { return s ^ (((r & 7) << 1) | ((r >> 3) & 1)); }
+__device__ __forceinline__ int v_seg(int r, int s) { return s ^ ((r & 3) << 2); }
 
 // tile_off[s] = query tiles before sequence s (tiles of qt rows).
 __global__ __launch_bounds__(256) void dense_tile_offsets_kernel(msa_seqs sq, int qt, int32_t* __restrict__ tile_off) {
@@ -65,74 +81,58 @@ __global__ __launch_bounds__(256) void dense_tile_offsets_kernel(msa_seqs sq, in
   for (int s = s0; s < s1; ++s) { tile_off[s] = acc; acc += tiles(s); }
 }
 
-// V staging map: thread tid takes 4-key group tid & 15 and 8-dim group
-// 4 (tid / 64) + {0, 2, 1, 3}[(tid / 16) & 3], so each 32-lane half of a wave
-// writes dim groups d and d + 2 of Vt, whose rows start 32 banks apart: the
-// 8-byte transposed stores hit 64 distinct banks.
-__device__ __forceinline__ void dense_v_map(int tid, int& key4, int& dg) {
-  key4 = tid & 15;
-  const int q = (tid >> 4) & 3;
-  dg = 4 * (tid >> 6) + ((q & 1) << 1) + (q >> 1);
+// Raw hardware 2^x (v_exp_f32): results below the fp32 normal range come out
+// as zero, which an online softmax whose largest weight is 1 cannot notice.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+// lsum + lo + hi of a packed bf16 pair (v_dot2c_f32_bf16 against (1, 1)):
+// the row sum is taken over the same rounded weights that multiply V.
+__device__ __forceinline__ float add_bf16_pair(float lsum, uint32_t pair) {
+  typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2v;
+  const bf16x2v ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, pair), ones, lsum, false);
+}
+__device__ __forceinline__ float xor32f(float x) {
+  return __builtin_bit_cast(float, xor_lane_u32<32>(__builtin_bit_cast(uint32_t, x)));
+}
+__device__ __forceinline__ uint2 lds_tr4(const uint16_t* p) {
+  typedef __attribute__((__vector_size__(4 * sizeof(short)))) short v4i16;
+  const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) v4i16*)(v4i16*)(const_cast<uint16_t*>(p)));
+  return __builtin_bit_cast(uint2, x);
+}
+// global_load_lds: lane l's 16 bytes land at dst + 16 l (dst wave-uniform).
+__device__ __forceinline__ void dma16(const uint16_t* src, uint16_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
 }
 
-// One key block of group r: thread tid loads 4 K pieces (key, 16-byte
-// segment) and 4 V rows of one (4-key group, 8-dim group); keys at or past
-// kv_len read as zero.
-__device__ __forceinline__ void dense_load_block(const uint16_t* __restrict__ kb, const uint16_t* __restrict__ vb,
-                                                 int64_t stride, int key0, int kv_len, int tid, u32x4 (&rk)[4],
-                                                 u32x4 (&rv)[4]) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int idx = tid + kThreads * c;
-    const int key = idx / (kHeadDim / 8), seg = idx % (kHeadDim / 8);
-    rk[c] = key0 + key < kv_len ? *reinterpret_cast<const u32x4*>(kb + static_cast<int64_t>(key0 + key) * stride + 8 * seg)
-                                : u32x4{0, 0, 0, 0};
-  }
-  int key4, dg;
-  dense_v_map(tid, key4, dg);
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int key = key0 + 4 * key4 + j;
-    rv[j] = key < kv_len ? *reinterpret_cast<const u32x4*>(vb + static_cast<int64_t>(key) * stride + 8 * dg)
-                         : u32x4{0, 0, 0, 0};
-  }
-}
-__device__ __forceinline__ void dense_store_block(DenseSmem& sm, int buf, int tid, const u32x4 (&rk)[4],
-                                                  const u32x4 (&rv)[4]) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int idx = tid + kThreads * c;
-    const int key = idx / (kHeadDim / 8), seg = idx % (kHeadDim / 8);
-    *reinterpret_cast<u32x4*>(&sm.k[buf][key][8 * seg]) = rk[c];
-  }
-  int key4, dg;
-  dense_v_map(tid, key4, dg);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    const int w = e >> 1, sh = (e & 1) * 16;
-    uint2 x;
-    x.x = ((rv[0][w] >> sh) & 0xFFFFu) | (((rv[1][w] >> sh) & 0xFFFFu) << 16);
-    x.y = ((rv[2][w] >> sh) & 0xFFFFu) | (((rv[3][w] >> sh) & 0xFFFFu) << 16);
-    *reinterpret_cast<uint2*>(&sm.vt[buf][8 * dg + e][4 * key4]) = x;
-  }
-}
+// Per-lane byte offsets of one key block's DMA (global side, relative to
+// the block's first key row) and of the MFMA operand reads (LDS side,
+// relative to a ring buffer), fixed for the whole kernel.
+struct DenseLaneOffsets {
+  uint32_t kg[kBK / 4 / kWaves], vg[kBK / 4 / kWaves];   // DMA sources: row * stride + 16-byte segment
+  uint32_t ks[kHeadDim / 16];                            // K operand, k-step st (rows 32i add 8 KiB)
+  uint32_t vs[kHeadDim / 32];                            // V^T operand, dim tile td (row offsets are immediates)
+};
 
 // grid: (tiles, H_kv); tiles are taken last-first so the longest causal
-// ranges start first.
-__global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
+// ranges start first.  Per iteration b (one barrier): the DMA for K_{b+2}
+// and V_{b+1} is issued, S^T_{b+1} = K_{b+1} Q^T and O^T += V_b^T P_b^T are
+// issued on the MFMA pipe, and the softmax of S_{b+1} runs on the VALU while
+// the O MFMAs drain.
+__global__ __launch_bounds__(kThreads, 1) void dense_prefill_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v, msa_seqs sq,
     const int32_t* __restrict__ tile_off, int H_q, int H_kv, int ntile_grid, float scale_log2,
     uint16_t* __restrict__ o, float* __restrict__ lse) {
-  __shared__ __align__(16) DenseSmem sm;
+  __shared__ __align__(16) DenseRing ring;
   constexpr int MT = kBK / 32;             // 32-key tiles of S^T
   constexpr int KS = kHeadDim / 16;        // k-steps of S^T = K Q^T
+  constexpr int NDMA = kBK / 4 / kWaves;   // DMA instructions per wave per block and tensor
   const int lane = lane_id();
   const int wave = threadIdx.x / kWave;
-  const int tid = threadIdx.x;
   const int n = lane & 31, h = lane >> 5;
   const int G = H_q / H_kv;
   const int qpw = 32 / G;                  // query rows per wave
-  const int qt = 4 * qpw;                  // query rows per CTA
+  const int qt = kWaves * qpw;             // query rows per CTA
   const int jq = n / G, hh = n % G;
   const int r = blockIdx.y;
   const int tile = ntile_grid - 1 - static_cast<int>(blockIdx.x);
@@ -148,9 +148,63 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
   const int t = t0 + wave * qpw + jq;                     // this lane's query row in the sequence
   const bool valid = n < qpw * G && t < t_end;
   const int p = valid ? g.kv_len - g.q_rows + t : -1;
-  // smallest position among the wave's rows (invalid lanes see every key masked anyway)
+  // smallest position among the wave's rows (invalid lanes see every key masked anyway);
+  // blocks below nfree are visible to every row of the wave and need no mask
   const int p_wave = g.kv_len - g.q_rows + min(t0 + wave * qpw, t_end - 1);
+  const int nfree = (p_wave + 1) / kBK;
   const int64_t head_row = (static_cast<int64_t>(g.q_begin) + (valid ? t : t0)) * H_q + static_cast<int64_t>(r) * G + hh;
+
+  const int64_t stride = static_cast<int64_t>(H_kv) * kHeadDim;
+  const char* kb = reinterpret_cast<const char*>(k + g.kv_start * stride + static_cast<int64_t>(r) * kHeadDim);
+  const char* vb = reinterpret_cast<const char*>(v + g.kv_start * stride + static_cast<int64_t>(r) * kHeadDim);
+  const uint32_t stride_b = static_cast<uint32_t>(stride) * 2;
+
+  DenseLaneOffsets lo;
+  {
+    const int gq = lane >> 4, jj = lane & 15;
+#pragma unroll
+    for (int c = 0; c < NDMA; ++c) {
+      const int ra = 4 * (c * kWaves + wave) + gq;
+      lo.kg[c] = ra * stride_b + 16 * k_seg(ra, jj);        // the permutations are involutions
+      lo.vg[c] = ra * stride_b + 16 * v_seg(ra, jj);
+    }
+#pragma unroll
+    for (int st = 0; st < KS; ++st) lo.ks[st] = 2 * (n * kHeadDim + 8 * k_seg(n, 2 * st + h));
+    // V^T operand: in each 16-lane group, lane j addresses row k0 + j/4, dims
+    // n0 + 4(j%4) .. +3 of V and receives rows k0 .. k0+3 of dim n0 + j
+    // (ds_read_tr16_b64); row r_l = 4h + j/4 within each 16-key k-step (rows
+    // 16u + r_l and + 8 share the permutation)
+    const int rl = 4 * h + (jj >> 2);
+#pragma unroll
+    for (int td = 0; td < kHeadDim / 32; ++td) {
+      const int col = 32 * td + 16 * (gq & 1) + 4 * (jj & 3);
+      lo.vs[td] = 2 * (rl * kHeadDim + 8 * v_seg(rl, col >> 3) + (col & 7));
+    }
+  }
+  // One key block (K and / or V) into LDS by DMA: each wave instruction fills
+  // 4 rows (1 KiB); lane l takes row 4 piece + l / 16 and the logical segment
+  // that the row's permutation stores at physical segment l % 16.  In a block
+  // running past kv_len the missing rows re-read the last key (finite values
+  // whose scores are masked).
+  auto dma = [&](const char* base, const uint32_t (&go)[NDMA], bool is_v, int key0, uint16_t* dst) {
+    const char* blk = base + static_cast<int64_t>(key0) * stride_b;
+    if (key0 + kBK <= g.kv_len) {
+#pragma unroll
+      for (int c = 0; c < NDMA; ++c)
+        dma16(reinterpret_cast<const uint16_t*>(blk + go[c]), dst + 4 * (c * kWaves + wave) * kHeadDim);
+    } else {
+#pragma unroll
+      for (int c = 0; c < NDMA; ++c) {
+        const int ra = 4 * (c * kWaves + wave) + (lane >> 4);
+        const int rr = min(ra, g.kv_len - 1 - key0);
+        const uint32_t off = rr * stride_b + 16 * (is_v ? v_seg(ra, lane & 15) : k_seg(ra, lane & 15));
+        dma16(reinterpret_cast<const uint16_t*>(blk + off), dst + 4 * (c * kWaves + wave) * kHeadDim);
+      }
+    }
+  };
+  dma(kb, lo.kg, false, 0, ring.k[0]);
+  dma(vb, lo.vg, true, 0, ring.v[0]);
+  if (nblk > 1) dma(kb, lo.kg, false, kBK, ring.k[1]);
 
   bf16x8 bq[KS];
   {
@@ -158,42 +212,33 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
 #pragma unroll
     for (int st = 0; st < KS; ++st) bq[st] = valid ? ld_bf16x8(qrow + 16 * st) : zero_bf16x8();
   }
-  const int64_t stride = static_cast<int64_t>(H_kv) * kHeadDim;
-  const uint16_t* kb = k + g.kv_start * stride + static_cast<int64_t>(r) * kHeadDim;
-  const uint16_t* vb = v + g.kv_start * stride + static_cast<int64_t>(r) * kHeadDim;
+
+  // S^T = K Q^T on one key block: lane (n, h) gets keys 32i + 8(e/4) + 4h + e%4 of row n
+  auto scores = [&](const uint16_t* kbuf, f32x16 (&acc_s)[MT]) {
+    const char* kbb = reinterpret_cast<const char*>(kbuf);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) {
+      acc_s[i] = f32x16{};
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+        acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(
+                                    kbb + lo.ks[st] + 2 * 32 * i * kHeadDim)),
+                                bq[st], acc_s[i]);
+    }
+  };
 
   f32x16 acc_o[kHeadDim / 32];
 #pragma unroll
   for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] = f32x16{};
   float m_run = -INFINITY, l_run = 0.f;
+  // P of the pending block in bf16, as the B operand of O^T = V^T P^T: k-step
+  // u covers keys 32(u/2) + 16(u%2) + {4h + e, 8 + 4h + e}, e = 0..3
+  bf16x8 bp[kBK / 16];
 
-  u32x4 rk[4], rv[4];
-  dense_load_block(kb, vb, stride, 0, g.kv_len, tid, rk, rv);
-  dense_store_block(sm, 0, tid, rk, rv);
-  dense_load_block(kb, vb, stride, min(1, nblk - 1) * kBK, g.kv_len, tid, rk, rv);
-  __syncthreads();
-  for (int b = 0; b < nblk; ++b) {
-    const int buf = b & 1;
-    // block b+1 goes to the other buffer (its readers passed the last barrier);
-    // block b+2 is requested before block b is computed
-    if (b + 1 < nblk) dense_store_block(sm, buf ^ 1, tid, rk, rv);
-    dense_load_block(kb, vb, stride, min(b + 2, nblk - 1) * kBK, g.kv_len, tid, rk, rv);
-
-    // S^T = K Q^T: lane (n, h) holds keys 32i + 8(e/4) + 4h + e%4 of row n
-    f32x16 acc_s[MT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      acc_s[i] = f32x16{};
-      const uint16_t* kr = &sm.k[buf][32 * i + n][8 * h];
-#pragma unroll
-      for (int st = 0; st < KS; ++st)
-        acc_s[i] = mfma32x32x16(__builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kr + 16 * st)), bq[st],
-                                acc_s[i]);
-    }
-    const int key0 = b * kBK;
-    // running max in raw score units (scale_log2 > 0 keeps the order);
-    // only blocks reaching past the wave's first row need the causal mask
-    if (key0 + kBK - 1 > p_wave) {
+  // online softmax of one block's scores (raw units; scale_log2 > 0 keeps
+  // the order): updates m_run / l_run, leaves P in bp, returns alpha
+  auto softmax = [&](f32x16 (&acc_s)[MT], int key0, auto masked) -> float {
+    if constexpr (decltype(masked)::value) {
 #pragma unroll
       for (int i = 0; i < MT; ++i)
 #pragma unroll
@@ -207,30 +252,16 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
     for (int i = 0; i < MT; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) bmax = fmaxf(bmax, acc_s[i][e]);
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+    bmax = fmaxf(bmax, xor32f(bmax));
     const float m_new = fmaxf(m_run, bmax);
     const float mm = m_new == -INFINITY ? 0.f : m_new;     // rows with nothing visible yet
-    const float alpha = exp2f((m_run - mm) * scale_log2);
+    const float alpha = exp2_hw((m_run - mm) * scale_log2);
     const float neg = -mm * scale_log2;
-    float lsum = 0.f;
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float pe = exp2f(fmaf(acc_s[i][e], scale_log2, neg));
-        acc_s[i][e] = pe;
-        lsum += pe;
-      }
-    lsum += __shfl_xor(lsum, 32);
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-    if (__ballot(alpha != 1.f)) {                        // some row's maximum moved
-#pragma unroll
-      for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] *= alpha;
-    }
-
-    // P in bf16 as the B operand of O^T = V^T P^T: k-step u covers keys
-    // 32(u/2) + 16(u%2) + {4h + e, 8 + 4h + e}, the lane's acc_s[u/2][8(u%2) ..].
+      for (int e = 0; e < 16; ++e) acc_s[i][e] = exp2_hw(fmaf(acc_s[i][e], scale_log2, neg));
+    float lsum = 0.f;
 #pragma unroll
     for (int u = 0; u < kBK / 16; ++u) {
       uint4 pw;
@@ -239,20 +270,156 @@ __global__ __launch_bounds__(kThreads, 2) void dense_prefill_kernel(
       pw.y = pack_bf16x2(acc_s[i][e0 + 2], acc_s[i][e0 + 3]);
       pw.z = pack_bf16x2(acc_s[i][e0 + 4], acc_s[i][e0 + 5]);
       pw.w = pack_bf16x2(acc_s[i][e0 + 6], acc_s[i][e0 + 7]);
-      const bf16x8 bp = __builtin_bit_cast(bf16x8, pw);
-      const int kbase = 32 * (u >> 1) + 16 * (u & 1) + 4 * h;
+      lsum = add_bf16_pair(add_bf16_pair(add_bf16_pair(add_bf16_pair(lsum, pw.x), pw.y), pw.z), pw.w);
+      bp[u] = __builtin_bit_cast(bf16x8, pw);
+    }
+    lsum += xor32f(lsum);
+    l_run = l_run * alpha + lsum;
+    m_run = m_new;
+    return alpha;
+  };
+
+  // O^T += V^T P^T from one value block (A operand read down V's columns)
+  auto pv = [&](const uint16_t* vbuf) {
+    const char* vbb = reinterpret_cast<const char*>(vbuf);
+#pragma unroll
+    for (int u = 0; u < kBK / 16; ++u) {
+      const int row0 = 32 * (u >> 1) + 16 * (u & 1);
 #pragma unroll
       for (int td = 0; td < kHeadDim / 32; ++td) {
-        const uint16_t* vr = &sm.vt[buf][32 * td + n][kbase];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 8);
-        uint4 w;
-        w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
-        acc_o[td] = mfma32x32x16(__builtin_bit_cast(bf16x8, w), bp, acc_o[td]);
+        const char* a0 = vbb + lo.vs[td] + 2 * row0 * kHeadDim;
+        const uint2 x0 = lds_tr4(reinterpret_cast<const uint16_t*>(a0));
+        const uint2 x1 = lds_tr4(reinterpret_cast<const uint16_t*>(a0 + 2 * 8 * kHeadDim));  // rows +8: same permutation
+        acc_o[td] = mfma32x32x16(__builtin_bit_cast(bf16x8, make_uint4(x0.x, x0.y, x1.x, x1.y)), bp[u], acc_o[td]);
       }
     }
-    __syncthreads();                                      // buffer buf is free again
+  };
+
+  // iteration b: K_{b+1} is in k[(b+1)&1], V_b in v[b&1]
+  // Iteration b (K_{b+1} in k[(b+1)&1], V_b in v[b&1]), laid out by hand as
+  // 32 MFMA slots, each fenced off from the next so that the compiler keeps
+  // the order: O is first rescaled by block b's alpha (only when some row's
+  // maximum moved); slots 0..15 issue S^T_{b+1} = K_{b+1} Q^T, slots 16..31
+  // O^T += V_b^T P_b^T with one sixteenth of block b+1's softmax after each
+  // MFMA, so the VALU works while the MFMA pipe drains; LDS operands are read
+  // kAhead slots before their MFMA.
+  float alpha_pend = 0.f;                 // alpha of the block whose P is in bp
+  auto step = [&](int b, auto masked) {
+    __builtin_amdgcn_s_waitcnt(0);        // this thread's copies of K_{b+1} and V_b have landed
+    __syncthreads();                      // everyone's have, and block b-1's readers are done
+    if (b + 2 < nblk) dma(kb, lo.kg, false, (b + 2) * kBK, ring.k[b & 1]);
+    dma(vb, lo.vg, true, (b + 1) * kBK, ring.v[(b + 1) & 1]);
+    const char* kbb = reinterpret_cast<const char*>(ring.k[(b + 1) & 1]);
+    const char* vbb = reinterpret_cast<const char*>(ring.v[b & 1]);
+    if (__ballot(alpha_pend != 1.f)) {    // some row's maximum moved with block b
+#pragma unroll
+      for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] *= alpha_pend;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+
+    constexpr int NS = MT * KS;           // S^T slots
+    auto kread = [&](int j) -> bf16x8 {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(kbb + lo.ks[j % KS] + 2 * 32 * (j / KS) * kHeadDim));
+    };
+    f32x16 acc_s[MT];
+#pragma unroll
+    for (int i = 0; i < MT; ++i) acc_s[i] = f32x16{};
+    bf16x8 kr[NS];
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) kr[j] = kread(j);
+#pragma unroll
+    for (int j = 0; j < NS; ++j) {
+      if (j + kAhead < NS) kr[j + kAhead] = kread(j + kAhead);
+      acc_s[j / KS] = mfma32x32x16(kr[j], bq[j % KS], acc_s[j / KS]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+
+    constexpr int NO = (kBK / 16) * (kHeadDim / 32);   // O^T slots
+    auto vread = [&](int j) -> bf16x8 {
+      const int u = j / (kHeadDim / 32), td = j % (kHeadDim / 32);
+      const char* a0 = vbb + lo.vs[td] + 2 * (32 * (u >> 1) + 16 * (u & 1)) * kHeadDim;
+      const uint2 x0 = lds_tr4(reinterpret_cast<const uint16_t*>(a0));
+      const uint2 x1 = lds_tr4(reinterpret_cast<const uint16_t*>(a0 + 2 * 8 * kHeadDim));
+      return __builtin_bit_cast(bf16x8, make_uint4(x0.x, x0.y, x1.x, x1.y));
+    };
+    bf16x8 vr[NO];
+    bf16x8 bp_next[kBK / 16];
+#pragma unroll
+    for (int j = 0; j < kAhead; ++j) vr[j] = vread(j);
+    const int key0 = (b + 1) * kBK;
+    float m0 = -INFINITY, m_new = 0.f, alpha = 0.f, neg = 0.f, lsum = 0.f;
+#pragma unroll
+    for (int j = 0; j < NO; ++j) {
+      if (j + kAhead < NO) vr[j + kAhead] = vread(j + kAhead);
+      acc_o[j % (kHeadDim / 32)] = mfma32x32x16(vr[j], bp[j / (kHeadDim / 32)], acc_o[j % (kHeadDim / 32)]);
+      if (j == 0) {
+        if constexpr (decltype(masked)::value) {
+#pragma unroll
+          for (int i = 0; i < MT; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+              const int key = key0 + 32 * i + 8 * (e >> 2) + 4 * h + (e & 3);
+              acc_s[i][e] = key <= p ? acc_s[i][e] : -INFINITY;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < 16; ++e) m0 = fmaxf(m0, acc_s[0][e]);
+      } else if (j == 1) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) m0 = fmaxf(m0, acc_s[1][e]);
+        m0 = fmaxf(m0, xor32f(m0));
+        m_new = fmaxf(m_run, m0);
+        const float mm = m_new == -INFINITY ? 0.f : m_new;   // rows with nothing visible yet
+        alpha = exp2_hw((m_run - mm) * scale_log2);
+        neg = -mm * scale_log2;
+      } else if (j < 14) {
+#pragma unroll
+        for (int x = 0; x < 32; ++x) {
+          if (2 + (3 * x) / 8 != j) continue;
+          acc_s[x >> 4][x & 15] = exp2_hw(fmaf(acc_s[x >> 4][x & 15], scale_log2, neg));
+        }
+      } else {
+#pragma unroll
+        for (int u = 2 * (j - 14); u < 2 * (j - 14) + 2; ++u) {
+          uint4 pw;
+          const int i = u >> 1, e0 = 8 * (u & 1);
+          pw.x = pack_bf16x2(acc_s[i][e0 + 0], acc_s[i][e0 + 1]);
+          pw.y = pack_bf16x2(acc_s[i][e0 + 2], acc_s[i][e0 + 3]);
+          pw.z = pack_bf16x2(acc_s[i][e0 + 4], acc_s[i][e0 + 5]);
+          pw.w = pack_bf16x2(acc_s[i][e0 + 6], acc_s[i][e0 + 7]);
+          lsum = add_bf16_pair(add_bf16_pair(add_bf16_pair(add_bf16_pair(lsum, pw.x), pw.y), pw.z), pw.w);
+          bp_next[u] = __builtin_bit_cast(bf16x8, pw);
+        }
+        if (j == 15) {
+          lsum += xor32f(lsum);
+          l_run = l_run * alpha + lsum;
+          m_run = m_new;
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int u = 0; u < kBK / 16; ++u) bp[u] = bp_next[u];
+    alpha_pend = alpha;
+  };
+
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  {
+    f32x16 acc_s[MT];
+    scores(ring.k[0], acc_s);
+    alpha_pend = nfree > 0 ? softmax(acc_s, 0, std::false_type{}) : softmax(acc_s, 0, std::true_type{});
   }
+  int b = 0;
+  for (; b + 1 < min(nfree, nblk); ++b) step(b, std::false_type{});
+  for (; b + 1 < nblk; ++b) step(b, std::true_type{});
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (__ballot(alpha_pend != 1.f)) {
+#pragma unroll
+    for (int i = 0; i < kHeadDim / 32; ++i) acc_o[i] *= alpha_pend;
+  }
+  pv(ring.v[b & 1]);
 
   if (!valid) return;
   const bool empty = !(l_run > 0.f);
@@ -307,7 +474,7 @@ extern "C" int msa_dense_attn(const void* q, const void* k, const void* v, const
   const size_t need = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
   if (!workspace || workspace_bytes < need) return MSA_ERR_WORKSPACE;
   const int G = num_q_heads / num_kv_heads;
-  const int qt = 4 * (32 / G);
+  const int qt = kWaves * (32 / G);
   // every sequence contributes at most q_rows / qt + 1 tiles
   const int64_t ntile = seqs->total_q_rows / qt + seqs->num_seqs;
   if (ntile >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
