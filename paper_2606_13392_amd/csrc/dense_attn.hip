@@ -81,9 +81,6 @@ __global__ __launch_bounds__(256) void dense_tile_offsets_kernel(msa_seqs sq, in
   for (int s = s0; s < s1; ++s) { tile_off[s] = acc; acc += tiles(s); }
 }
 
-// Raw hardware 2^x (v_exp_f32): results below the fp32 normal range come out
-// as zero, which an online softmax whose largest weight is 1 cannot notice.
-__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
 // lsum + lo + hi of a packed bf16 pair (v_dot2c_f32_bf16 against (1, 1)):
 // the row sum is taken over the same rounded weights that multiply V.
 __device__ __forceinline__ float add_bf16_pair(float lsum, uint32_t pair) {

@@ -48,6 +48,12 @@ __device__ __forceinline__ u32x4 widen(u32x2 r) {
 template <typename R>
 __device__ __forceinline__ bf16x8 widen_bf16x8(R r) { return __builtin_bit_cast(bf16x8, widen(r)); }
 
+// Raw hardware 2^x (v_exp_f32, half rate on gfx950): results below the fp32
+// normal range come out as zero, which a softmax weight relative to its
+// row's maximum (at most 1) cannot notice; exp2f adds a range reduction of
+// five more instructions for those results.
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // MFMA 32x32x16 bf16 -> f32.  Lane l supplies row (A) / column (B) l%32 and
 // eight consecutive k of the half l/32; C lane l holds column l%32, rows
 // 8*(r/4) + 4*(l/32) + r%4 for r = 0..15.

@@ -180,13 +180,13 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
     const float m_new = fmaxf(m_run, bmax);
-    const float alpha = exp2f(m_run - m_new);
+    const float alpha = exp2_hw(m_run - m_new);
     float lsum = 0.f;
 #pragma unroll
     for (int i = 0; i < BK / 16; ++i)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float pe = exp2f(st[i][e] - m_new);
+        const float pe = exp2_hw(st[i][e] - m_new);
         st[i][e] = pe;
         lsum += pe;
       }

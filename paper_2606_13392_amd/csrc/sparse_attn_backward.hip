@@ -310,7 +310,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
           const int prow = 16 * t + 4 * qd + i;
           const float l2 = sm.lse2[buf][prow];
           const bool vis = key <= sm.rpos[buf][prow] && l2 > -INFINITY;
-          const float p = vis ? exp2f(acc_s[t][i] * scale_log2 - l2) : 0.f;
+          const float p = vis ? exp2_hw(acc_s[t][i] * scale_log2 - l2) : 0.f;
           acc_s[t][i] = p;
           acc_dp[t][i] = p * (acc_dp[t][i] - sm.dlt[buf][prow]);
         }

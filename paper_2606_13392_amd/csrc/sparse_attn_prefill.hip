@@ -222,7 +222,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
       for (int i = 0; i < MT; ++i)
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const float pe = exp2f(acc_s[i][e] - mm);
+          const float pe = exp2_hw(acc_s[i][e] - mm);
           acc_s[i][e] = pe;
           l += pe;
         }

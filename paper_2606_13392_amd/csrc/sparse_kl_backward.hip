@@ -400,7 +400,7 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kern
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int row = 16 * t + 4 * qd + i;
-              acc_s[u][t][i] = key <= wv.rpos[row] ? exp2f(acc_s[u][t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
+              acc_s[u][t][i] = key <= wv.rpos[row] ? exp2_hw(acc_s[u][t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
             }
           head_mean(acc_s[u], lg);
           // student, Delta = P_idx - P on head-0 rows (in place of S_idx), KL terms
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kern
               const bool on = key <= wv.rpos[row];
               const bool head0 = (row & (G - 1)) == 0;
               const float lz = acc_i[u][t][i] * sidx_log2 - wv.lsei2[row];   // log2 P_idx
-              const float pidx = on ? exp2f(lz) : 0.f;
+              const float pidx = on ? exp2_hw(lz) : 0.f;
               const float pbar = acc_s[u][t][i];
               klrow[t][i] += (head0 && on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
               acc_i[u][t][i] = head0 ? pidx - pbar : 0.f;
