@@ -507,7 +507,7 @@ def run_training(args, dev):
         "kl_loss_mean": loss,
         "roofline": {},
     }
-    for name, nbytes in (("bwd_kvo_kernel", bwd_bytes), ("kl_grad_wave_kernel", kl_bytes)):
+    for name, nbytes in (("bwd_kvo_kernel", bwd_bytes), ("kl_grad_kernel", kl_bytes)):
         if name in kern and kern[name]["ms_per_step"] > 0:
             gbs = nbytes / (kern[name]["ms_per_step"] * 1e-3) / 1e9
             out["roofline"][name] = {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -320,8 +320,7 @@ int msa_sparse_attn_backward(const void* q, const void* k, const void* v, const 
  * Workspace, stream and error behaviour as for msa_sparse_attn_prefill.
  * d_index_q, d_index_k and kl are bit-reproducible (d_index_k adds a key
  * block's queries in ascending (row, slot) order).  Supported: d_idx in {64, 128};
- * head_dim == 128; block_size 64 with 1 <= topk <= 64, or block_size 128 with
- * 1 <= topk <= 32 (run as the blocks' 64-key halves);
+ * head_dim == 128; block_size 64 or 128 with 1 <= topk <= 64;
  * num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}; num_kv_heads <= 64.
  * ------------------------------------------------------------------------ */
 size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads,

@@ -14,80 +14,56 @@
 // The teacher's per-head normalisers are the forward's LSE (Sec. 4.3, "LSE
 // fusion"); the student's LSE_idx is reduced over the selected blocks from
 // per-block log-sum-exps (Sec. 4.3) computed in a first key-block-outer
-// sweep.  Both sweeps use the reverse index of kvo_index.h, per chunk of
-// query rows:
+// sweep.  The sweeps use the reverse index of kvo_index.h on the call's own
+// key blocks (B_k = 64 or 128), per chunk of query rows:
 //   kl_lse           per incidence: ln sum_j exp(s_idx S_idx_j) over the block's visible keys
 //   kl_lse_combine   per (row, group): LSE_idx over the valid slots
-//   kl_grad          per work item (<= 256 queries of one tile): P, P_idx and
-//                    Delta on MFMA 16x16x32 per gathered (query, head) row,
-//                    the teacher's head mean in registers; d k_idx of the
-//                    block in registers (an fp32 partial per item), d q_idx
-//                    and the KL term of every incidence as fp32 partials
-//                    (kl_grad_wave: one wave per 32-row pass against all 64
-//                    keys, no barrier between passes)
+//   kl_grad          per work item (<= 256 queries of one tile), one wave per
+//                    pass of 16 queries: the teacher on MFMA 16x16x32 over the
+//                    pass's 16 G (query, head) rows in sub-passes of 32, its
+//                    head mean into an LDS tile; the student on the 16 query
+//                    rows only: P_idx, Delta, the KL terms, d q_idx
+//                    (Delta k_idx) as fp32 partials per incidence, and Delta
+//                    in bf16 per incidence for the next kernel
+//   kl_dk            per work item: d k_idx of the block = Delta^T q_idx over
+//                    the item's queries (MFMA, both operands read down
+//                    columns with transposing LDS reads), an fp32 partial
 //   kl_tile_reduce   per key block: the items of every group's tile, in
 //                    order, added to the fp32 d k_idx accumulator
 //   kl_combine       per (row, group): d q_idx and KL over the valid slots, in
 //                    slot order
 // and at the end kl_convert (accumulator times grad_scale to bf16).  No
-// atomics touch a result except the reverse index's handle order, which
-// fixes the order in which a block's queries add into d k_idx.
+// atomics touch a result except the reverse index's handle order, which the
+// index sorts per tile, so every output is bit-reproducible.
 #include "kvo_index.h"
 
 namespace {
 
-constexpr int kKlBK = 64;
-constexpr int kKlThreads = 256;                       // 4 waves: key quarters
-constexpr int kKlRows = 32;                           // gathered (query, head) rows per pass
+constexpr int kKlThreads = 256;                       // LSE sweep: 4 waves
+constexpr int kK2Waves = 8;                           // gradient and d k_idx kernels: 8 waves
+constexpr int kK2Threads = kK2Waves * kWave;
+constexpr int kK2Q = 16;                              // student queries per pass
 
-
-__device__ __forceinline__ uint16_t raw_elem16(const u32x4& w, int j) {
-  return static_cast<uint16_t>(w[j >> 1] >> (16 * (j & 1)));
-}
-
-// Stage the index-key block (row-major and transposed) of keys key0 .. key0+63.
-template <int D, typename Smem>
-__device__ __forceinline__ void stage_index_keys(Smem& sm, const uint16_t* __restrict__ ikb, int nkeys) {
-  for (int c = threadIdx.x; c < (kKlBK / 4) * (D / 8); c += kKlThreads) {
-    const int key4 = c / (D / 8), dg = c % (D / 8);
-    u32x4 rows[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int key = 4 * key4 + j;
-      rows[j] = key < nkeys ? load_raw(ikb + static_cast<int64_t>(key) * D + 8 * dg) : u32x4{};
-      *reinterpret_cast<u32x4*>(&sm.ki[key][8 * dg]) = rows[j];
-    }
-    if constexpr (sizeof(sm.kit) > 0) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        uint2 w;
-        w.x = static_cast<uint32_t>(raw_elem16(rows[0], e)) | (static_cast<uint32_t>(raw_elem16(rows[1], e)) << 16);
-        w.y = static_cast<uint32_t>(raw_elem16(rows[2], e)) | (static_cast<uint32_t>(raw_elem16(rows[3], e)) << 16);
-        *reinterpret_cast<uint2*>(&sm.kit[8 * dg + e][4 * key4]) = w;
-      }
-    }
-  }
-}
 
 // ---------------------------------------------------------------- LSE_idx
-template <int D>
+template <int BK, int D>
 struct KlLseSmem {
-  uint16_t ki[kKlBK][D + 8];
+  uint16_t ki[BK][D + 8];
   int32_t s_row[kItemQueries];
   int32_t s_slot[kItemQueries];
 };
 
-// Per work item: each wave takes 16 queries at a time; S_idx (16 queries x 64
+// Per work item: each wave takes 16 queries at a time; S_idx (16 queries x BK
 // keys) on MFMA 16x16x32, masked to the visible keys, reduced to the block's
 // log-sum-exp per query.
-template <int D>
+template <int BK, int D>
 __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_kv, int topk, int64_t nbcap, int64_t row0, float sidx_log2,
     float* __restrict__ lse_part, int32_t* __restrict__ next_item) {
   static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
-  __shared__ KlLseSmem<D> sm;
+  __shared__ KlLseSmem<BK, D> sm;
   __shared__ int32_t s_claim;
   constexpr int KS = D / 32;
   const int lane = lane_id();
@@ -104,7 +80,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
     const int64_t gb = tile % nbcap;
     const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
     const SeqGeom g = seq_geom(sq, s);
-    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+    const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
     const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
     __syncthreads();
     if (static_cast<int>(threadIdx.x) < nq) {
@@ -114,7 +90,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
     }
     if (tile != staged) {
       const uint16_t* ikb = index_k + (g.kv_start + key0) * static_cast<int64_t>(D);
-      for (int c = threadIdx.x; c < kKlBK * (D / 8); c += kKlThreads) {
+      for (int c = threadIdx.x; c < BK * (D / 8); c += kKlThreads) {
         const int key = c / (D / 8), dg = c % (D / 8);
         *reinterpret_cast<u32x4*>(&sm.ki[key][8 * dg]) =
             key0 + key < g.kv_len ? load_raw(ikb + static_cast<int64_t>(key) * D + 8 * dg) : u32x4{};
@@ -128,9 +104,10 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
       u32x4 a[KS];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) a[ks] = load_raw(index_q + (grow * H_kv + r) * D + 32 * ks + 8 * qd);
-      f32x4 acc[4];
+      constexpr int KT = BK / 16;
+      f32x4 acc[KT];
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt) {
+      for (int kt = 0; kt < KT; ++kt) {
         acc[kt] = f32x4{};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
@@ -144,7 +121,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
         const int pos = qi < nq ? pos_base + sm.s_row[qi] : -1;
         float m = -INFINITY;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) {
+        for (int kt = 0; kt < KT; ++kt) {
           const float z = key0 + 16 * kt + c16 <= pos ? acc[kt][i] * sidx_log2 : -INFINITY;
           acc[kt][i] = z;
           m = fmaxf(m, z);
@@ -154,7 +131,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
         const float mm = m == -INFINITY ? 0.f : m;
         float l = 0.f;
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt) l += exp2f(acc[kt][i] - mm);
+        for (int kt = 0; kt < KT; ++kt) l += exp2f(acc[kt][i] - mm);
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) l += __shfl_xor(l, off);
         if (c16 == 0 && qi < nq) {
@@ -169,7 +146,8 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
 // One thread per (row, group) of the chunk: LSE_idx = ln sum over the valid
 // slots of exp(partial).
 __global__ __launch_bounds__(256) void kl_lse_combine_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
-                                                             const int64_t* __restrict__ blk_base, int H_kv, int topk,
+                                                             const int64_t* __restrict__ blk_base, int BK, int H_kv,
+                                                             int topk,
                                                              int64_t row0, int64_t nrows,
                                                              const float* __restrict__ lse_part,
                                                              float* __restrict__ lse_idx) {
@@ -183,12 +161,64 @@ __global__ __launch_bounds__(256) void kl_lse_combine_kernel(const int32_t* __re
   const float* lp = lse_part + pr * topk;
   float m = -INFINITY;
   for (int j = 0; j < topk; ++j)
-    if (incidence_ok(ids[j], p, kKlBK, blk_base, s)) m = fmaxf(m, lp[j]);
+    if (incidence_ok(ids[j], p, BK, blk_base, s)) m = fmaxf(m, lp[j]);
   float l = 0.f;
   if (m > -INFINITY)
     for (int j = 0; j < topk; ++j)
-      if (incidence_ok(ids[j], p, kKlBK, blk_base, s)) l += __expf(lp[j] - m);
+      if (incidence_ok(ids[j], p, BK, blk_base, s)) l += __expf(lp[j] - m);
   lse_idx[pr] = m > -INFINITY ? m + __logf(l) : -INFINITY;
+}
+
+// ---------------------------------------------------------------- LDS staging
+// Staged rows of W bf16 (W = 64 or 128) have their 16-byte segments permuted
+// (an XOR with a row-dependent mask) so that both read patterns below are
+// free of bank conflicts: 16 consecutive rows at one segment (16 bytes per
+// lane) and, for the transposing reads, 4 consecutive rows x 2 adjacent
+// segments per 16 lanes.  A 128-element row fills the 64 banks, two
+// 64-element rows share them.
+template <int W>
+__device__ __forceinline__ int kl_seg(int r, int s) {
+  if constexpr (W == 128) return s ^ (((r & 7) << 1) | ((r >> 3) & 1));
+  else return s ^ ((((r >> 1) & 1) << 2) | ((r >> 2) & 3));
+}
+// element offset of (row, col) in a permuted block; col % 8 is 0 or 4
+template <int W>
+__device__ __forceinline__ int kl_off(int r, int col) {
+  return r * W + 8 * kl_seg<W>(r, col >> 3) + (col & 7);
+}
+// global_load_lds: lane l's 16 bytes land at dst + 16 l (dst wave-uniform)
+__device__ __forceinline__ void kl_dma16(const uint16_t* src, uint16_t* dst) {
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+}
+// transposing LDS read: in each 16-lane group, lane j addresses row k0 + j/4,
+// columns n0 + 4(j%4) .. +3 and receives rows k0 .. k0+3 of column n0 + j
+typedef __attribute__((__vector_size__(4 * sizeof(short)))) short kl_v4i16;
+__device__ __forceinline__ uint2 kl_tr4(const uint16_t* p) {
+  const kl_v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) kl_v4i16*)(kl_v4i16*)(const_cast<uint16_t*>(p)));
+  return __builtin_bit_cast(uint2, x);
+}
+// B operand (8 consecutive rows k0 .. k0+7 of column n0 + lane % 16) of
+// MFMA 16x16x32 from a permuted block, by two transposing reads
+template <int W>
+__device__ __forceinline__ bf16x8 kl_col8(const uint16_t* blk, int k0, int n0, int c16) {
+  const int col = n0 + 4 * (c16 & 3);
+  const uint2 a = kl_tr4(blk + kl_off<W>(k0 + (c16 >> 2), col));
+  const uint2 b = kl_tr4(blk + kl_off<W>(k0 + 4 + (c16 >> 2), col));
+  return __builtin_bit_cast(bf16x8, make_uint4(a.x, a.y, b.x, b.y));
+}
+// Rows 0 .. rows-1 of a block of row width W into LDS by DMA, by all NT
+// threads: wave instruction `piece` fills 1 KiB = 64 / (W / 8) rows; a lane's
+// source row comes from row_src (rows past the data re-read a valid row).
+template <int W, int NT, typename RowSrc>
+__device__ __forceinline__ void kl_stage(int rows, RowSrc row_src, uint16_t* dst) {
+  constexpr int SEGS = W / 8;
+  constexpr int RPI = 64 / SEGS;
+  const int lane = lane_id(), wave = threadIdx.x / kWave;
+  for (int piece = wave; piece * RPI < rows; piece += NT / kWave) {
+    const int row = piece * RPI + lane / SEGS;
+    kl_dma16(row_src(row) + 8 * kl_seg<W>(row, lane % SEGS), dst + piece * RPI * W);
+  }
 }
 
 // ---------------------------------------------------------------- gradients
@@ -213,67 +243,59 @@ __device__ __forceinline__ void head_mean(f32x4 (&v)[2], int lg) {
   }
 }
 
-// ---------------------------------------------------------------- gradients, one wave per pass
-// A wave takes whole passes (32 rows against all 64 keys of the block), so
-// passes need no CTA barrier and each wave is its own stream of gathers; the
-// block's K, index keys and their transpose are shared by the CTA per item.
-// d k_idx of all 64 keys stays in the wave's registers (64 VGPRs at d_idx
-// 64, 128 at d_idx 128); at item end the four waves' partials are added in
-// wave order.
-template <int D>
-struct KlwWave {
-  uint16_t qit[D][kKlRows + 8];                       // index query of each pass row, transposed
-  uint16_t dlc[kKlRows][kKlBK + 8];                   // Delta of each pass query (its head-0 row), [query][key]
-  float lse2[kKlRows];                                // Main Branch LSE * log2(e) per row (+inf: no row)
-  float lsei2[kKlRows];                               // LSE_idx * log2(e) per row
-  int32_t rpos[kKlRows];                              // position per row (-1: no row)
-  int64_t incq[kKlRows];                              // incidence of pass query j (the trash one past the item)
+template <int BK, int D>
+struct Kl2Wave {
+  float pbar[kK2Q][BK + 4];                           // teacher head mean per (pass query, key); Delta in
+                                                      // bf16 then overwrites each row's front half
+  float lse2[32];                                     // teacher rows of a sub-pass: LSE * log2(e) (+inf: none)
+  int32_t pos[kK2Q];                                  // position of each pass query (-1: none)
+  float lsei2[kK2Q];                                  // LSE_idx * log2(e) of each pass query
+  int64_t inc[kK2Q];                                  // incidence of each pass query (the trash one for none)
 };
-template <int D>
-struct KlwSmem {
-  union {
-    struct {
-      uint16_t k[kKlBK][kHeadDim + 8];                // K block (Main Branch head r), row-major
-      uint16_t ki[kKlBK][D + 8];                      // index-key block, row-major
-      uint16_t kit[D][kKlBK + 8];                     // index-key block transposed
-      KlwWave<D> wv[kKlThreads / kWave];
-    } m;
-    float red[kKlThreads / kWave][kKlBK * D];         // item end: each wave's d k_idx partial
-  } u;
+template <int BK, int D>
+struct Kl2Smem {
+  uint16_t k[BK * kHeadDim];                          // K block of head group r, permuted rows
+  uint16_t ki[BK * D];                                // index-key block, permuted rows
+  Kl2Wave<BK, D> wv[kK2Waves];
   int32_t s_row[kItemQueries];
   int32_t s_slot[kItemQueries];
 };
-// d_idx 64: two CTAs per CU (245 VGPRs at G = 8); d_idx 128: d k_idx alone
-// takes 128 VGPRs, so one CTA per CU with up to 512 registers per wave
-static_assert(sizeof(KlwSmem<64>) <= 80 * 1024, "LDS of a one-wave-per-pass KL CTA (two per CU)");
-static_assert(sizeof(KlwSmem<128>) <= 160 * 1024, "LDS of a one-wave-per-pass KL CTA (one per CU)");
+static_assert(sizeof(Kl2Smem<128, 128>) <= 160 * 1024, "LDS of the KL gradient CTA");
 
-template <int D, int LG>
-__global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kernel(
+// One CTA of 8 waves per work item; wave w takes passes w, w + 8, ... of 16
+// queries.  Teacher: the pass's 16 G (query, head) rows in sub-passes of 32
+// (16 for G = 1), Q gathered one sub-pass ahead; S = Q K^T on MFMA 16x16x32,
+// P = exp2(s S log2 e - LSE log2 e) on the visible keys, the head mean over
+// each query's G rows (registers and lane swaps), stored per (query, key).
+// Student, on the 16 query rows: S_idx, P_idx = exp2(s_idx S_idx log2 e -
+// LSE_idx log2 e), Delta = P_idx - P, the KL terms (summed per query over the
+// block's keys), d q_idx = Delta k_idx over the block's keys.
+template <int BK, int D, int LG>
+__global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
     const uint16_t* __restrict__ index_q, const uint16_t* __restrict__ index_k, const uint16_t* __restrict__ q,
     const uint16_t* __restrict__ k, const float* __restrict__ lse, const float* __restrict__ lse_idx, msa_seqs sq,
     const int64_t* __restrict__ blk_base, const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off,
     const uint32_t* __restrict__ handles, int H_q, int H_kv, int topk, int64_t nbcap, int64_t row0,
-    float s_main_log2, float sidx, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
-    float* __restrict__ part, int32_t* __restrict__ next_item) {
-  static_assert(kItemQueries <= kKlThreads, "every thread loads at most one handle of an item");
-  __shared__ KlwSmem<D> sm;
+    float s_main_log2, float sidx_log2, int64_t trash_inc, float* __restrict__ dqp, float* __restrict__ klp,
+    uint16_t* __restrict__ dlt, int32_t* __restrict__ next_item) {
+  static_assert(kItemQueries <= kK2Threads, "every thread loads at most one handle of an item");
+  __shared__ __align__(16) Kl2Smem<BK, D> sm;
   __shared__ int32_t s_claim;
-  constexpr int KSM = kHeadDim / 32;                  // k-steps of S over the head dimension
-  constexpr int KSI = D / 32;                         // k-steps of S_idx over d_idx
-  constexpr int NT = D / 16;                          // dim tiles of d k_idx / d q_idx
-  constexpr int NW = kKlThreads / kWave;
+  constexpr int G = 1 << LG;
+  constexpr int R = G >= 2 ? 32 : 16;                 // teacher rows per sub-pass
+  constexpr int NTT = R / 16;                         // teacher row tiles
+  constexpr int NSP = kK2Q * G / R;                   // sub-passes per pass
+  constexpr int KT = BK / 16;                         // key tiles
+  constexpr int KSM = kHeadDim / 32;                  // k-steps over the head dimension
+  constexpr int KSI = D / 32;                         // k-steps over d_idx
   const int lane = lane_id();
   const int w = threadIdx.x / kWave;
   const int c16 = lane & 15, qd = lane >> 4;
-  constexpr int G = 1 << LG;                          // H_q / H_kv
-  constexpr int lg = LG;
-  constexpr int qpw = 32 >> LG;                       // queries per pass
-  const float sidx_log2 = sidx * kLog2e;
   const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
   const int32_t total_items = item_off[ntile];
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
-  KlwWave<D>& wv = sm.u.m.wv[w];
+  Kl2Wave<BK, D>& wv = sm.wv[w];
+  int64_t staged = -1;
 
   for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
@@ -283,7 +305,8 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kern
     const int64_t gb = tile % nbcap;
     const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
     const SeqGeom g = seq_geom(sq, s);
-    const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+    const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
+    const int nkey = g.kv_len - key0;                 // >= 1: a tile with queries has a visible key
     const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);
 
     __syncthreads();                                  // the previous item is done with LDS
@@ -292,227 +315,268 @@ __global__ __launch_bounds__(kKlThreads, D == 64 ? 2 : 1) void kl_grad_wave_kern
       sm.s_row[threadIdx.x] = static_cast<int32_t>(hd >> 6);
       sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
     }
-    {                                                 // staged every item: the item-end sum reuses this LDS
+    if (tile != staged) {
       const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      for (int c = threadIdx.x; c < kKlBK * (kHeadDim / 8); c += kKlThreads) {
-        const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
-        *reinterpret_cast<u32x4*>(&sm.u.m.k[key][8 * dg]) =
-            key0 + key < g.kv_len ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
-      }
-      stage_index_keys<D>(sm.u.m, index_k + (g.kv_start + key0) * static_cast<int64_t>(D), g.kv_len - key0);
+      const uint16_t* ikb = index_k + (g.kv_start + key0) * static_cast<int64_t>(D);
+      kl_stage<kHeadDim, kK2Threads>(BK, [&](int row) { return kb + min(row, nkey - 1) * kv_stride; }, sm.k);
+      kl_stage<D, kK2Threads>(BK, [&](int row) { return ikb + min(row, nkey - 1) * static_cast<int64_t>(D); }, sm.ki);
+      staged = tile;
     }
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 
-    f32x4 acc_dk[4][NT];                              // [key tile][dim tile]: lane column = dim, rows = keys 4qd + i
+    const int npass = (nq + kK2Q - 1) / kK2Q;
+    // teacher sub-pass (pass, sp): A operands (Q rows 16t + c16) and their LSEs
+    u32x4 aq[NTT][KSM], an[NTT][KSM];                // this sub-pass's, the next one's
+    float al[NTT], aln[NTT];
+    auto load_sub = [&](int ps, int sp, u32x4 (&a)[NTT][KSM], float (&l)[NTT]) {
 #pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
+      for (int t = 0; t < NTT; ++t) {
+        const int x = sp * R + 16 * t + c16;          // teacher row of the pass
+        const int jq = ps * kK2Q + (x >> LG);         // its query in the item
+        const int j = min(jq, nq - 1);
+        const int64_t hrow = (row0 + sm.s_row[j]) * H_q + static_cast<int64_t>(r) * G + (x & (G - 1));
 #pragma unroll
-      for (int n = 0; n < NT; ++n) acc_dk[kt][n] = f32x4{};
-
-    // A operands of a pass (rows 16t + c16): Q of the row's head, the index
-    // query of the row's query, and the two LSEs; the next pass's are
-    // requested once S and S_idx have consumed the current ones
-    u32x4 bq[2][KSM], bi[2][KSI];
-    float lse_v[2], lsei_v[2];
-    bool arow[2];
-    int32_t qrow[2];
-    auto load_pass = [&](int cc) {
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int qa = cc + ((16 * t + c16) >> lg);
-        arow[t] = qa < nq;
-        qrow[t] = min(qa, nq - 1);
-        const int64_t rl = sm.s_row[qrow[t]];
-        const int64_t grow = row0 + rl;
-        const int64_t hrow = grow * H_q + static_cast<int64_t>(r) * G + ((16 * t + c16) & (G - 1));
-#pragma unroll
-        for (int st = 0; st < KSM; ++st) bq[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
-#pragma unroll
-        for (int st = 0; st < KSI; ++st) bi[t][st] = load_raw(index_q + (grow * H_kv + r) * D + 32 * st + 8 * qd);
-        lse_v[t] = lse[hrow];
-        lsei_v[t] = lse_idx[rl * H_kv + r];
+        for (int st = 0; st < KSM; ++st) a[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
+        l[t] = jq < nq ? lse[hrow] * kLog2e : INFINITY;
       }
     };
-    const int npass = (nq + qpw - 1) / qpw;
     int ps = w;
-    if (ps < npass) load_pass(ps * qpw);
-    for (; ps < npass; ps += NW) {
-      const int cq = ps * qpw;                        // the pass's first query in the item
-      // row scalars and the transposed index queries of the pass (wave-private)
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int col = 16 * t + c16;
-#pragma unroll
-        for (int st = 0; st < KSI; ++st)
-#pragma unroll
-          for (int j = 0; j < 8; ++j) wv.qit[32 * st + 8 * qd + j][col] = raw_elem16(bi[t][st], j);
+    if (ps < npass) load_sub(ps, 0, aq, al);
+    for (; ps < npass; ps += kK2Waves) {
+      const int cq = ps * kK2Q;
+      if (lane < kK2Q) {
+        const bool ok = cq + lane < nq;
+        const int j = min(cq + lane, nq - 1);
+        const int32_t rl = sm.s_row[j];
+        wv.pos[lane] = ok ? pos_base + rl : -1;
+        wv.lsei2[lane] = ok ? lse_idx[static_cast<int64_t>(rl) * H_kv + r] * kLog2e : INFINITY;
+        wv.inc[lane] = ok ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[j] : trash_inc;
+      }
+      // ---- teacher
+#pragma unroll 1
+      for (int sp = 0; sp < NSP; ++sp) {
+        // the next sub-pass's gathers go out before this one's MFMAs
+        if (sp + 1 < NSP) load_sub(ps, sp + 1, an, aln);
+        else if (ps + kK2Waves < npass) load_sub(ps + kK2Waves, 0, an, aln);
         if (qd == 0) {
-          const int32_t rl = sm.s_row[qrow[t]];
-          wv.lse2[col] = arow[t] ? lse_v[t] * kLog2e : INFINITY;
-          wv.lsei2[col] = arow[t] ? lsei_v[t] * kLog2e : INFINITY;
-          wv.rpos[col] = arow[t] ? pos_base + rl : -1;
-          if ((col & (G - 1)) == 0)
-            wv.incq[col >> lg] = arow[t] ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[qrow[t]]
-                                         : trash_inc;
+#pragma unroll
+          for (int t = 0; t < NTT; ++t) wv.lse2[16 * t + c16] = al[t];
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+          f32x4 acc[2];
+#pragma unroll
+          for (int t = 0; t < 2; ++t) acc[t] = f32x4{};
+#pragma unroll
+          for (int st = 0; st < KSM; ++st) {
+            const bf16x8 kb8 = ld_bf16x8(sm.k + kl_off<kHeadDim>(16 * kt + c16, 32 * st + 8 * qd));
+#pragma unroll
+            for (int t = 0; t < NTT; ++t) acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, aq[t][st]), kb8, acc[t]);
+          }
+          const int key = key0 + 16 * kt + c16;
+#pragma unroll
+          for (int t = 0; t < NTT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 16 * t + 4 * qd + i;
+              const int xq = (sp * R + row) >> LG;
+              acc[t][i] = key <= wv.pos[xq] ? exp2_hw(acc[t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
+            }
+          if constexpr (LG > 0) head_mean(acc, LG);
+#pragma unroll
+          for (int t = 0; t < NTT; ++t)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int row = 16 * t + 4 * qd + i;
+              if ((row & (G - 1)) == 0) wv.pbar[(sp * R + row) >> LG][16 * kt + c16] = acc[t][i];
+            }
+        }
+#pragma unroll
+        for (int t = 0; t < NTT; ++t) {
+          al[t] = aln[t];
+#pragma unroll
+          for (int st = 0; st < KSM; ++st) aq[t][st] = an[t][st];
         }
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-      // two halves of 32 keys keep the score registers small; key tile kt,
-      // row tile t: the lane holds key 16kt + c16 and rows 16t + 4qd + i
-      float klrow[2][4];
+      // ---- student: rows = the pass's 16 queries (lane c16 supplies query c16)
+      u32x4 ai[KSI];
+      {
+        const int j = min(cq + c16, nq - 1);
+        const int64_t grow = row0 + sm.s_row[j];
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) klrow[t][i] = 0.f;
-#pragma unroll
-      for (int hk = 0; hk < 2; ++hk) {
-        // S and S_idx
-        f32x4 acc_s[2][2], acc_i[2][2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int t = 0; t < 2; ++t) {
-            const int kt = 2 * hk + u;
-            acc_s[u][t] = f32x4{};
-            acc_i[u][t] = f32x4{};
-#pragma unroll
-            for (int st = 0; st < KSM; ++st)
-              acc_s[u][t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bq[t][st]),
-                                         ld_bf16x8(&sm.u.m.k[16 * kt + c16][32 * st + 8 * qd]), acc_s[u][t]);
-#pragma unroll
-            for (int st = 0; st < KSI; ++st)
-              acc_i[u][t] = mfma16x16x32(__builtin_bit_cast(bf16x8, bi[t][st]),
-                                         ld_bf16x8(&sm.u.m.ki[16 * kt + c16][32 * st + 8 * qd]), acc_i[u][t]);
-            __builtin_amdgcn_sched_barrier(0);      // bound how far LDS operand reads are hoisted
-          }
-        __builtin_amdgcn_sched_barrier(0);
-        if (hk == 1 && ps + NW < npass) load_pass((ps + NW) * qpw);
-
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int kt = 2 * hk + u;
-          const int key = key0 + 16 * kt + c16;
-          // teacher: per-head P, then the mean over the query's heads (in place)
-#pragma unroll
-          for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = 16 * t + 4 * qd + i;
-              acc_s[u][t][i] = key <= wv.rpos[row] ? exp2_hw(acc_s[u][t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
-            }
-          head_mean(acc_s[u], lg);
-          // student, Delta = P_idx - P on head-0 rows (in place of S_idx), KL terms
-#pragma unroll
-          for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = 16 * t + 4 * qd + i;
-              const bool on = key <= wv.rpos[row];
-              const bool head0 = (row & (G - 1)) == 0;
-              const float lz = acc_i[u][t][i] * sidx_log2 - wv.lsei2[row];   // log2 P_idx
-              const float pidx = on ? exp2_hw(lz) : 0.f;
-              const float pbar = acc_s[u][t][i];
-              klrow[t][i] += (head0 && on && pbar > 0.f) ? pbar * (__log2f(pbar) - lz) * kLn2 : 0.f;
-              acc_i[u][t][i] = head0 ? pidx - pbar : 0.f;
-            }
-          // d k_idx += Delta^T q_idx over the pass's rows (one k-step): k
-          // index 8qd + 4t + i = row 16t + 4qd + i
-          uint4 dw;
-          dw.x = pack_bf16x2(acc_i[u][0][0], acc_i[u][0][1]);
-          dw.y = pack_bf16x2(acc_i[u][0][2], acc_i[u][0][3]);
-          dw.z = pack_bf16x2(acc_i[u][1][0], acc_i[u][1][1]);
-          dw.w = pack_bf16x2(acc_i[u][1][2], acc_i[u][1][3]);
-          const bf16x8 da = __builtin_bit_cast(bf16x8, dw);
-#pragma unroll
-          for (int n = 0; n < NT; ++n) {
-            const uint16_t* qr = &wv.qit[16 * n + c16][4 * qd];
-            const uint2 lo = *reinterpret_cast<const uint2*>(qr), hi = *reinterpret_cast<const uint2*>(qr + 16);
-            acc_dk[kt][n] = mfma16x16x32(da, __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y)),
-                                         acc_dk[kt][n]);
-            if (n & 1) __builtin_amdgcn_sched_barrier(0);
-          }
-          // the pass queries' Delta rows for d q_idx
-#pragma unroll
-          for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = 16 * t + 4 * qd + i;
-              const uint32_t pr = t == 0 ? (i < 2 ? dw.x : dw.y) : (i < 2 ? dw.z : dw.w);
-              if ((row & (G - 1)) == 0) wv.dlc[row >> lg][16 * kt + c16] = static_cast<uint16_t>(pr >> (16 * (i & 1)));
-            }
-        }
+        for (int ks = 0; ks < KSI; ++ks) ai[ks] = load_raw(index_q + (grow * H_kv + r) * D + 32 * ks + 8 * qd);
       }
-      // KL per head-0 row: sum over the 64 keys (registers, then the 16 lanes)
+      float klq[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
+      for (int kt = 0; kt < KT; ++kt) {
+        f32x4 acc = f32x4{};
+#pragma unroll
+        for (int ks = 0; ks < KSI; ++ks)
+          acc = mfma16x16x32(__builtin_bit_cast(bf16x8, ai[ks]), ld_bf16x8(sm.ki + kl_off<D>(16 * kt + c16, 32 * ks + 8 * qd)),
+                             acc);
+        // lane (key 16kt + c16, queries 4qd + i)
+        const int key = key0 + 16 * kt + c16;
+        float pb[4], dl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pb[i] = wv.pbar[4 * qd + i][16 * kt + c16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          float v = klrow[t][i];
-#pragma unroll
-          for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
-          const int row = 16 * t + 4 * qd + i;
-          if (c16 == 0 && (row & (G - 1)) == 0) klp[wv.incq[row >> lg]] = v;
+          const int qq = 4 * qd + i;
+          const bool on = key <= wv.pos[qq];
+          const float lz = acc[i] * sidx_log2 - wv.lsei2[qq];     // log2 P_idx
+          const float pidx = on ? exp2_hw(lz) : 0.f;
+          klq[i] += (on && pb[i] > 0.f) ? pb[i] * (__log2f(pb[i]) - lz) * kLn2 : 0.f;
+          dl[i] = on ? pidx - pb[i] : 0.f;
         }
+        // Delta in bf16 over the front of the row: bytes [32kt, 32kt + 32)
+        // hold P of keys 8kt .. 8kt+7, read at key tile kt/2 <= kt
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          reinterpret_cast<uint16_t*>(wv.pbar[4 * qd + i])[16 * kt + c16] = f32_to_bf16_bits(dl[i]);
+      }
+      // KL per query: the 16 key lanes
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v = klq[i];
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) v += __shfl_xor(v, off);
+        if (c16 == 0) klp[wv.inc[4 * qd + i]] = v;
+      }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-      // d q_idx of the pass queries (rows j = 16tq + 4qd + i of Delta), dims
-      // 16n + c16, over the 64 keys
+      // Delta rows of the pass to the incidence-major buffer (d k_idx pass)
 #pragma unroll
-      for (int tq = 0; tq < 2; ++tq) {
-        if (16 * tq >= qpw) break;
+      for (int c = lane; c < kK2Q * (BK / 8); c += kWave) {
+        const int row = c / (BK / 8), seg = c % (BK / 8);
+        *reinterpret_cast<uint4*>(dlt + wv.inc[row] * BK + 8 * seg) =
+            *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(wv.pbar[row]) + 8 * seg);
+      }
+      // d q_idx = Delta (16 queries x BK keys) k_idx (BK x D): A = Delta rows,
+      // B = k_idx columns by transposing reads
 #pragma unroll
-        for (int n = 0; n < NT; ++n) {
-          f32x4 acc = f32x4{};
+      for (int n = 0; n < D / 16; ++n) {
+        f32x4 acc = f32x4{};
 #pragma unroll
-          for (int ks = 0; ks < kKlBK / 32; ++ks)
-            acc = mfma16x16x32(ld_bf16x8(&wv.dlc[16 * tq + c16][32 * ks + 8 * qd]),
-                               ld_bf16x8(&sm.u.m.kit[16 * n + c16][32 * ks + 8 * qd]), acc);
+        for (int ks = 0; ks < BK / 32; ++ks)
+          acc = mfma16x16x32(ld_bf16x8(reinterpret_cast<const uint16_t*>(wv.pbar[c16]) + 32 * ks + 8 * qd),
+                             kl_col8<D>(sm.ki, 32 * ks + 8 * qd, 16 * n, c16), acc);
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int j = 16 * tq + 4 * qd + i;
-            if (j < qpw) dqp[wv.incq[j] * D + 16 * n + c16] = acc[i];
-          }
-        }
+        for (int i = 0; i < 4; ++i) dqp[wv.inc[4 * qd + i] * D + 16 * n + c16] = acc[i];
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+  }
+}
 
-    // item end: the four waves' d k_idx, added in wave order, as the item's
-    // partial, laid out [key quarter][reg][lane] as kl_tile_reduce_kernel reads it
-    __syncthreads();                                  // every pass is done: K and pass LDS are free
-#pragma unroll
-    for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sm.u.red[w][kt * (NT * 4 * 64) + (4 * n + i) * 64 + lane] = acc_dk[kt][n][i];
+// ---------------------------------------------------------------- d k_idx
+template <int BK, int D>
+struct Kl2DkSmem {
+  uint16_t dl[kItemQueries * BK];                     // Delta row of each item query (permuted rows)
+  uint16_t qi[kItemQueries * D];                      // index query row of each item query (permuted rows)
+};
+static_assert(sizeof(Kl2DkSmem<128, 128>) <= 160 * 1024, "LDS of the d k_idx CTA");
+
+// One CTA of 8 waves per work item: d k_idx (BK x D) = sum over the item's
+// queries (handle order) of Delta_q^T q_idx_q on MFMA 16x16x32, both
+// operands read down columns with transposing reads; the item's fp32
+// partial, row-major.  Query slots past the item read the trash incidence's
+// Delta row, which is zero.
+template <int BK, int D>
+__global__ __launch_bounds__(kK2Threads, 1) void kl_dk_kernel(
+    const uint16_t* __restrict__ index_q, msa_seqs sq, const int64_t* __restrict__ blk_base,
+    const int32_t* __restrict__ tile_off, const int32_t* __restrict__ item_off, const uint32_t* __restrict__ handles,
+    int H_kv, int topk, int64_t nbcap, int64_t row0, int64_t trash_inc, const uint16_t* __restrict__ dlt,
+    float* __restrict__ part, int32_t* __restrict__ next_item) {
+  __shared__ __align__(16) Kl2DkSmem<BK, D> sm;
+  __shared__ int32_t s_claim;
+  __shared__ int64_t s_inc[kItemQueries];
+  __shared__ int64_t s_qrow[kItemQueries];
+  constexpr int NTO = (BK / 16) * (D / 16);           // output tiles
+  constexpr int PER = (NTO + kK2Waves - 1) / kK2Waves;
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int c16 = lane & 15, qd = lane >> 4;
+  const int64_t ntile = static_cast<int64_t>(H_kv) * nbcap;
+  const int32_t total_items = item_off[ntile];
+  (void)sq;
+  (void)blk_base;
+  for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
+    const int64_t tile = upper_index(item_off, ntile + 1, item);
+    const int32_t h0 = tile_off[tile] + (item - item_off[tile]) * kItemQueries;
+    const int32_t nq = min(tile_off[tile + 1] - h0, kItemQueries);
+    const int r = static_cast<int>(tile / nbcap);
+    const int nq32 = (nq + 31) & ~31;
+    __syncthreads();                                  // the previous item is done with LDS
+    if (static_cast<int>(threadIdx.x) < nq32) {
+      const int j = threadIdx.x;
+      if (j < nq) {
+        const uint32_t hd = handles[h0 + j];
+        const int64_t rl = static_cast<int64_t>(hd >> 6);
+        s_inc[j] = (rl * H_kv + r) * topk + static_cast<int64_t>(hd & 63u);
+        s_qrow[j] = (row0 + rl) * H_kv + r;
+      } else {
+        s_inc[j] = trash_inc;
+        s_qrow[j] = -1;
+      }
+    }
     __syncthreads();
-    float* dst = part + static_cast<int64_t>(item) * (kKlBK * D);
-    for (int idx = threadIdx.x; idx < kKlBK * D; idx += kKlThreads)
-      dst[idx] = (sm.u.red[0][idx] + sm.u.red[1][idx]) + (sm.u.red[2][idx] + sm.u.red[3][idx]);
+    if (static_cast<int>(threadIdx.x) < nq32 && s_qrow[threadIdx.x] < 0) s_qrow[threadIdx.x] = s_qrow[0];
+    __syncthreads();
+    kl_stage<BK, kK2Threads>(nq32, [&](int row) { return dlt + s_inc[row] * BK; }, sm.dl);
+    kl_stage<D, kK2Threads>(nq32, [&](int row) { return index_q + s_qrow[row] * D; }, sm.qi);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    f32x4 acc[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) acc[u] = f32x4{};
+    for (int kk = 0; kk < nq32 / 32; ++kk) {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int ot = w + kK2Waves * u;
+        if (ot < NTO) {
+          const int kt = ot / (D / 16), n = ot % (D / 16);
+          // A: Delta^T rows = keys 16kt + c16, k = queries; B: q_idx columns
+          acc[u] = mfma16x16x32(kl_col8<BK>(sm.dl, 32 * kk + 8 * qd, 16 * kt, c16),
+                                kl_col8<D>(sm.qi, 32 * kk + 8 * qd, 16 * n, c16), acc[u]);
+        }
+      }
+    }
+    // C: lane (dim 16n + c16, keys 16kt + 4qd + i)
+    float* dst = part + static_cast<int64_t>(item) * (BK * D);
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int ot = w + kK2Waves * u;
+      if (ot < NTO) {
+        const int kt = ot / (D / 16), n = ot % (D / 16);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dst[(16 * kt + 4 * qd + i) * D + 16 * n + c16] = acc[u][i];
+      }
+    }
   }
 }
 
 // Per key block: the items of the block's tiles of every group, in group and
 // item order, added to the fp32 accumulator of the block's keys.
-// kKlReduceSplit CTAs per block, one float4 of the partial per thread.
-template <int D>
-constexpr int kKlReduceSplit = kKlBK * D / (4 * 256);
-template <int D>
+// BK D / 1024 CTAs per block, one float4 of the row-major partial per thread.
+template <int BK, int D>
+constexpr int kKlReduceSplit = BK * D / (4 * 256);
+template <int BK, int D>
 __global__ __launch_bounds__(256) void kl_tile_reduce_kernel(msa_seqs sq, const int64_t* __restrict__ blk_base,
                                                              const int32_t* __restrict__ item_off, int H_kv,
                                                              int64_t nbcap, const float* __restrict__ part,
                                                              float* __restrict__ dk_acc) {
-  constexpr int NT = D / 16;
-  constexpr int SPLIT = kKlReduceSplit<D>;
+  constexpr int SPLIT = kKlReduceSplit<BK, D>;
   const int64_t gb = blockIdx.x / SPLIT;
   const int s = static_cast<int>(upper_index(blk_base, sq.num_seqs + 1, gb));
   const SeqGeom g = seq_geom(sq, s);
-  const int key0 = static_cast<int>(gb - blk_base[s]) * kKlBK;
+  const int key0 = static_cast<int>(gb - blk_base[s]) * BK;
   bool any = false;
   for (int r = 0; r < H_kv; ++r) any |= item_off[r * nbcap + gb] != item_off[r * nbcap + gb + 1];
   if (!any) return;
@@ -523,20 +587,14 @@ __global__ __launch_bounds__(256) void kl_tile_reduce_kernel(msa_seqs sq, const 
     const int64_t tile = r * nbcap + gb;
 #pragma unroll 4
     for (int32_t it = item_off[tile]; it < item_off[tile + 1]; ++it) {
-      const float4 x = p4[static_cast<int64_t>(it) * (kKlBK * D / 4)];
+      const float4 x = p4[static_cast<int64_t>(it) * (BK * D / 4)];
       acc.x += x.x;
       acc.y += x.y;
       acc.z += x.z;
       acc.w += x.w;
     }
   }
-  // partial layout [kq][reg][lane]: 4 consecutive lanes = 4 consecutive dims
-  const int idx = 4 * c4;
-  const int kq = idx / (NT * 4 * 64);
-  const int reg = (idx / 64) % (NT * 4);
-  const int ln = idx & 63;
-  const int key = 16 * kq + 4 * (ln >> 4) + (reg & 3);
-  const int dim = 16 * (reg >> 2) + (ln & 15);
+  const int key = (4 * c4) / D, dim = (4 * c4) % D;
   if (key0 + key >= g.kv_len) return;
   float4* dst = reinterpret_cast<float4*>(dk_acc + (g.kv_start + key0 + key) * static_cast<int64_t>(D) + dim);
   float4 y = *dst;
@@ -553,8 +611,8 @@ constexpr int kKlCombWaves = 4;
 
 template <int D>
 __global__ __launch_bounds__(64 * kKlCombWaves) void kl_combine_kernel(
-    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_kv, int topk,
-    int64_t row0, int64_t nrows, const float* __restrict__ dqp, const float* __restrict__ klp, float grad_scale,
+    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int BK, int H_kv,
+    int topk, int64_t row0, int64_t nrows, const float* __restrict__ dqp, const float* __restrict__ klp, float grad_scale,
     uint16_t* __restrict__ d_index_q, float* __restrict__ kl) {
   const int lane = lane_id();
   const int64_t pr = static_cast<int64_t>(blockIdx.x) * kKlCombWaves + threadIdx.x / kWave;
@@ -568,7 +626,7 @@ __global__ __launch_bounds__(64 * kKlCombWaves) void kl_combine_kernel(
   // slot validity, one slot per lane; every slot has a partial row, so the
   // loads below are unconditional and in flight together (unwritten partials
   // of invalid slots are dropped by a select, never multiplied)
-  const bool mine = lane < topk && incidence_ok(ids[lane], p, kKlBK, blk_base, s);
+  const bool mine = lane < topk && incidence_ok(ids[lane], p, BK, blk_base, s);
   const uint64_t valid = __ballot(mine);
   const float* src = dqp + pr * topk * static_cast<int64_t>(D) + PER * lane;
   float acc[PER];
@@ -607,12 +665,12 @@ struct KlPlan {
   int64_t nbcap, ntile, chunk_rows, max_items;
   int nscan;
   size_t off_blk_base, off_cnt, off_tile_off, off_item_off, off_blk_tot, off_dk, off_handles, off_tpos, off_lsep,
-      off_lsei, off_dqp, off_klp, off_part, total;
+      off_lsei, off_dqp, off_klp, off_dlt, off_part, total;
 };
 
 constexpr size_t kDefaultKlBytes = size_t(16) << 30;
 
-void kl_layout(KlPlan& pl, const msa_seqs* seqs, int H_kv, int D, int topk) {
+void kl_layout(KlPlan& pl, const msa_seqs* seqs, int H_kv, int BK, int D, int topk) {
   using msa_host::align_up;
   size_t o = 0;
   pl.off_blk_base = o; o = align_up(o + sizeof(int64_t) * (seqs->num_seqs + 1), 256);
@@ -627,14 +685,15 @@ void kl_layout(KlPlan& pl, const msa_seqs* seqs, int H_kv, int D, int topk) {
   pl.off_tpos = o;     o = align_up(o + sizeof(int32_t) * inc, 256);
   pl.off_lsep = o;     o = align_up(o + sizeof(float) * inc, 256);
   pl.off_lsei = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.chunk_rows) * H_kv, 256);
-  pl.off_dqp = o;      o = align_up(o + sizeof(float) * (inc + 1) * D, 256);    // + trash slot
+  pl.off_dqp = o;      o = align_up(o + sizeof(float) * (inc + 1) * D, 256);        // + trash incidence
   pl.off_klp = o;      o = align_up(o + sizeof(float) * (inc + 1), 256);
-  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * kKlBK * D, 256);
+  pl.off_dlt = o;      o = align_up(o + sizeof(uint16_t) * (inc + 1) * BK, 256);
+  pl.off_part = o;     o = align_up(o + sizeof(float) * static_cast<size_t>(pl.max_items) * BK * D, 256);
   pl.total = o;
 }
 
-int make_kl_plan(const msa_seqs* seqs, int H_kv, int D, int topk, size_t budget, KlPlan* pl) {
-  const int64_t nb = (seqs->max_kv_len + kKlBK - 1) / kKlBK;
+int make_kl_plan(const msa_seqs* seqs, int H_kv, int BK, int D, int topk, size_t budget, KlPlan* pl) {
+  const int64_t nb = (seqs->max_kv_len + BK - 1) / BK;
   pl->nbcap = static_cast<int64_t>(seqs->num_seqs) * (nb > 0 ? nb : 1);
   pl->ntile = static_cast<int64_t>(H_kv) * pl->nbcap;
   if (pl->ntile >= (int64_t(1) << 31) - 1 || pl->nbcap >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
@@ -644,20 +703,20 @@ int make_kl_plan(const msa_seqs* seqs, int H_kv, int D, int topk, size_t budget,
       std::min(kMaxChunkRows, ((int64_t(1) << 31) - 1) / (static_cast<int64_t>(H_kv) * topk));
   const int64_t all = std::max<int64_t>(1, seqs->total_q_rows);
   pl->chunk_rows = std::min(all, max_rows);
-  kl_layout(*pl, seqs, H_kv, D, topk);
+  kl_layout(*pl, seqs, H_kv, BK, D, topk);
   if (pl->total > budget) {
     pl->chunk_rows = 1;
-    kl_layout(*pl, seqs, H_kv, D, topk);
+    kl_layout(*pl, seqs, H_kv, BK, D, topk);
     const size_t one = pl->total;
     if (one > budget) return MSA_ERR_WORKSPACE;
     pl->chunk_rows = 2;
-    kl_layout(*pl, seqs, H_kv, D, topk);
+    kl_layout(*pl, seqs, H_kv, BK, D, topk);
     const size_t per_row = pl->total - one + 1024;
     pl->chunk_rows = std::min(std::min(all, max_rows), 1 + static_cast<int64_t>((budget - one) / per_row));
-    kl_layout(*pl, seqs, H_kv, D, topk);
+    kl_layout(*pl, seqs, H_kv, BK, D, topk);
     while (pl->total > budget && pl->chunk_rows > 1) {
       pl->chunk_rows = std::max<int64_t>(1, pl->chunk_rows * 7 / 8);
-      kl_layout(*pl, seqs, H_kv, D, topk);
+      kl_layout(*pl, seqs, H_kv, BK, D, topk);
     }
     if (pl->total > budget) return MSA_ERR_WORKSPACE;
   }
@@ -669,28 +728,26 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   if (st != MSA_OK) return st;
   if (H_q < 1 || H_kv < 1 || d_idx < 1 || head_dim < 1 || BK < 1 || topk < 1) return MSA_ERR_INVALID;
   if (H_q % H_kv != 0) return MSA_ERR_INVALID;
-  if (head_dim != kHeadDim || (BK != kKlBK && BK != 2 * kKlBK) || (d_idx != 64 && d_idx != 128))
-    return MSA_ERR_UNSUPPORTED;
-  if (BK == 2 * kKlBK && topk > 32) return MSA_ERR_UNSUPPORTED;   // its 64-key halves fill <= 64 slots
+  if (head_dim != kHeadDim || (BK != 64 && BK != 128) || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || !msa_host::is_pow2(H_q / H_kv) || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
   if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
   return MSA_OK;
 }
 
-// kl_grad_wave_kernel instance for G = 2^lg (lg <= 4, checked by validate_kl).
-template <int D, typename... Args>
-void launch_kl_grad_wave(int lg, dim3 grid, hipStream_t stream, Args... args) {
+// kl_grad_kernel instance for G = 2^lg (lg <= 4, checked by validate_kl).
+template <int BK, int D, typename... Args>
+void launch_kl_grad(int lg, dim3 grid, hipStream_t stream, Args... args) {
   switch (lg) {
-    case 0: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 0>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 1: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 1>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 2: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 2>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    case 3: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 3>, grid, dim3(kKlThreads), 0, stream, args...); break;
-    default: msa_prof::launch("kl_grad_wave_kernel", kl_grad_wave_kernel<D, 4>, grid, dim3(kKlThreads), 0, stream, args...); break;
+    case 0: msa_prof::launch("kl_grad_kernel", kl_grad_kernel<BK, D, 0>, grid, dim3(kK2Threads), 0, stream, args...); break;
+    case 1: msa_prof::launch("kl_grad_kernel", kl_grad_kernel<BK, D, 1>, grid, dim3(kK2Threads), 0, stream, args...); break;
+    case 2: msa_prof::launch("kl_grad_kernel", kl_grad_kernel<BK, D, 2>, grid, dim3(kK2Threads), 0, stream, args...); break;
+    case 3: msa_prof::launch("kl_grad_kernel", kl_grad_kernel<BK, D, 3>, grid, dim3(kK2Threads), 0, stream, args...); break;
+    default: msa_prof::launch("kl_grad_kernel", kl_grad_kernel<BK, D, 4>, grid, dim3(kK2Threads), 0, stream, args...); break;
   }
 }
 
-template <int D>
+template <int BK, int D>
 int run_kl(const void* index_q, const void* index_k, const void* q, const void* k, const float* lse,
            const int32_t* block_ids, const msa_seqs* seqs, int H_q, int H_kv, int topk, float softmax_scale,
            float grad_scale, void* d_index_q, void* d_index_k, float* kl, const KlPlan& pl, char* ws,
@@ -707,6 +764,7 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
   auto* lsei = reinterpret_cast<float*>(ws + pl.off_lsei);
   auto* dqp = reinterpret_cast<float*>(ws + pl.off_dqp);
   auto* klp = reinterpret_cast<float*>(ws + pl.off_klp);
+  auto* dlt = reinterpret_cast<uint16_t*>(ws + pl.off_dlt);
   auto* part = reinterpret_cast<float*>(ws + pl.off_part);
   const msa_seqs sq = *seqs;
   const int64_t kv_floats = seqs->total_kv_rows * static_cast<int64_t>(D);
@@ -714,41 +772,52 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
   const float sidx = 1.f / std::sqrt(static_cast<float>(D));
   const auto* iq = static_cast<const uint16_t*>(index_q);
   const auto* ik = static_cast<const uint16_t*>(index_k);
+  const int64_t trash_inc = pl.chunk_rows * H_kv * static_cast<int64_t>(topk);
 
-  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, kKlBK,
+  msa_prof::launch("kvo_block_base_kernel", kvo_block_base_kernel, dim3(1), dim3(256), 0, stream, sq, BK,
                    blk_base);
   msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(zero_blocks), dim3(256), 0, stream,
                    reinterpret_cast<int32_t*>(dk_acc), kv_floats, 0);
-  static std::atomic<int> ctas_lse {0}, ctas_grad {0};
-  const int n_lse = persistent_ctas(kl_lse_kernel<D>, kKlThreads, &ctas_lse);
-  const int n_grad = persistent_ctas(kl_grad_wave_kernel<D, 3>, kKlThreads, &ctas_grad);
+  // the trash incidence's Delta row stands in for the query slots past an item: zero
+  msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(1), dim3(256), 0, stream,
+                   reinterpret_cast<int32_t*>(dlt + trash_inc * BK), static_cast<int64_t>(BK / 2), 0);
+  static std::atomic<int> ctas_lse {0}, ctas_grad {0}, ctas_dk {0};
+  const int n_lse = persistent_ctas(kl_lse_kernel<BK, D>, kKlThreads, &ctas_lse);
+  const int n_grad = persistent_ctas(kl_grad_kernel<BK, D, 3>, kK2Threads, &ctas_grad);
+  const int n_dk = persistent_ctas(kl_dk_kernel<BK, D>, kK2Threads, &ctas_dk);
   const int lg_g = __builtin_ctz(static_cast<unsigned>(H_q / H_kv));
-  const int64_t trash_inc = pl.chunk_rows * H_kv * static_cast<int64_t>(topk);
   for (int64_t r0 = 0; r0 < seqs->total_q_rows; r0 += pl.chunk_rows) {
     const int64_t nr = std::min<int64_t>(pl.chunk_rows, seqs->total_q_rows - r0);
     const int64_t pairs = nr * H_kv;
-    build_reverse_index(block_ids, sq, blk_base, H_kv, kKlBK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
+    build_reverse_index(block_ids, sq, blk_base, H_kv, BK, topk, pl.nbcap, pl.ntile, pl.nscan, r0, nr, cnt,
                         tile_off, item_off, blk_tot, tpos, handles, stream, true);
-    msa_prof::launch("kl_lse_kernel", kl_lse_kernel<D>, dim3(n_lse), dim3(kKlThreads), 0, stream, iq, ik, sq,
+    msa_prof::launch("kl_lse_kernel", kl_lse_kernel<BK, D>, dim3(n_lse), dim3(kKlThreads), 0, stream, iq, ik, sq,
                      static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
                      static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,
                      pl.nbcap, r0, sidx * kLog2e, lsep, cnt + pl.ntile);
     msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
-                     dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
-                     static_cast<const float*>(lsep), lsei);
-    launch_kl_grad_wave<D>(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
-                        static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
-                        static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
-                        static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
-                        topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx, trash_inc, dqp, klp, part,
-                        cnt + pl.ntile + 1);
-    msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<D>,
-                     dim3(static_cast<unsigned>(pl.nbcap * kKlReduceSplit<D>)),
-                     dim3(256), 0, stream, sq, static_cast<const int64_t*>(blk_base),
-                     static_cast<const int32_t*>(item_off), H_kv, pl.nbcap, static_cast<const float*>(part), dk_acc);
+                     dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), BK, H_kv, topk, r0,
+                     nr, static_cast<const float*>(lsep), lsei);
+    launch_kl_grad<BK, D>(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
+                          static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
+                          static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
+                          static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_q, H_kv,
+                          topk, pl.nbcap, r0, softmax_scale * kLog2e, sidx * kLog2e, trash_inc, dqp, klp, dlt,
+                          cnt + pl.ntile + 1);
+    // d k_idx's persistent loop reuses the LSE sweep's work counter, reset
+    msa_prof::launch("fill_i32_kernel", fill_i32_kernel, dim3(1), dim3(256), 0, stream, cnt + pl.ntile,
+                     static_cast<int64_t>(1), 0);
+    msa_prof::launch("kl_dk_kernel", kl_dk_kernel<BK, D>, dim3(n_dk), dim3(kK2Threads), 0, stream, iq, sq,
+                     static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
+                     static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,
+                     pl.nbcap, r0, trash_inc, static_cast<const uint16_t*>(dlt), part, cnt + pl.ntile);
+    msa_prof::launch("kl_tile_reduce_kernel", kl_tile_reduce_kernel<BK, D>,
+                     dim3(static_cast<unsigned>(pl.nbcap * kKlReduceSplit<BK, D>)), dim3(256), 0, stream, sq,
+                     static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(item_off), H_kv, pl.nbcap,
+                     static_cast<const float*>(part), dk_acc);
     msa_prof::launch("kl_combine_kernel", kl_combine_kernel<D>,
                      dim3(static_cast<unsigned>((pairs + kKlCombWaves - 1) / kKlCombWaves)), dim3(64 * kKlCombWaves),
-                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), H_kv, topk, r0, nr,
+                     0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), BK, H_kv, topk, r0, nr,
                      static_cast<const float*>(dqp), static_cast<const float*>(klp), grad_scale * sidx,
                      static_cast<uint16_t*>(d_index_q), kl);
   }
@@ -759,27 +828,18 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
   return msa_host::launch_status();
 }
 
-// Block size 128: each id is expanded to its two 64-key halves in front of
-// the workspace and the 64-key path runs on 2 topk slots.
-size_t kl_expanded_ids_bytes(const msa_seqs* seqs, int H_kv, int BK, int topk) {
-  if (BK == kKlBK) return 0;
-  return msa_host::align_up(sizeof(int32_t) * static_cast<size_t>(seqs->total_q_rows) * H_kv * topk * (BK / kKlBK),
-                            256);
-}
-
 }  // namespace
 
 extern "C" size_t msa_sparse_kl_backward_workspace_size(const msa_seqs* seqs, int num_q_heads, int num_kv_heads,
                                                        int d_idx, int head_dim, int block_size, int topk) {
   if (validate_kl(seqs, num_q_heads, num_kv_heads, d_idx, head_dim, block_size, topk) != MSA_OK) return 0;
-  const int topk64 = topk * (block_size / kKlBK);
   KlPlan pl;
-  if (make_kl_plan(seqs, num_kv_heads, d_idx, topk64, kDefaultKlBytes, &pl) != MSA_OK) {
-    if (make_kl_plan(seqs, num_kv_heads, d_idx, topk64, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
+  if (make_kl_plan(seqs, num_kv_heads, block_size, d_idx, topk, kDefaultKlBytes, &pl) != MSA_OK) {
+    if (make_kl_plan(seqs, num_kv_heads, block_size, d_idx, topk, ~size_t(0) >> 1, &pl) != MSA_OK) return 0;
     pl.chunk_rows = 1;
-    kl_layout(pl, seqs, num_kv_heads, d_idx, topk64);
+    kl_layout(pl, seqs, num_kv_heads, block_size, d_idx, topk);
   }
-  return kl_expanded_ids_bytes(seqs, num_kv_heads, block_size, topk) + pl.total;
+  return pl.total;
 }
 
 extern "C" int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void* q, const void* k,
@@ -792,28 +852,22 @@ extern "C" int msa_sparse_kl_backward(const void* index_q, const void* index_k, 
   if (st != MSA_OK) return st;
   if (!index_q || !index_k || !q || !k || !lse || !block_ids || !d_index_q || !d_index_k) return MSA_ERR_INVALID;
   if (seqs->total_q_rows == 0 && seqs->total_kv_rows == 0) return MSA_OK;
-  const size_t xb = kl_expanded_ids_bytes(seqs, num_kv_heads, block_size, topk);
-  if (!workspace || workspace_bytes < xb) return MSA_ERR_WORKSPACE;
-  const int f = block_size / kKlBK;
-  const int32_t* ids = block_ids;
-  if (f > 1) {
-    auto* ids64 = static_cast<int32_t*>(workspace);
-    const int64_t pairs = seqs->total_q_rows * num_kv_heads;
-    if (pairs > 0)
-      msa_prof::launch("expand_block_ids_kernel", expand_block_ids_kernel,
-                       dim3(static_cast<unsigned>((pairs + 255) / 256)), dim3(256), 0, stream, block_ids, pairs, topk,
-                       f, ids64);
-    ids = ids64;
-  }
-  const int topk64 = topk * f;
+  if (!workspace) return MSA_ERR_WORKSPACE;
   KlPlan pl;
-  st = make_kl_plan(seqs, num_kv_heads, d_idx, topk64, workspace_bytes - xb, &pl);
+  st = make_kl_plan(seqs, num_kv_heads, block_size, d_idx, topk, workspace_bytes, &pl);
   if (st != MSA_OK) return st;
-  if (workspace_bytes - xb < pl.total) return MSA_ERR_WORKSPACE;
-  char* ws = static_cast<char*>(workspace) + xb;
+  if (workspace_bytes < pl.total) return MSA_ERR_WORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  if (block_size == 64) {
+    if (d_idx == 64)
+      return run_kl<64, 64>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk,
+                            softmax_scale, grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+    return run_kl<64, 128>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk,
+                           softmax_scale, grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+  }
   if (d_idx == 64)
-    return run_kl<64>(index_q, index_k, q, k, lse, ids, seqs, num_q_heads, num_kv_heads, topk64, softmax_scale,
-                      grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
-  return run_kl<128>(index_q, index_k, q, k, lse, ids, seqs, num_q_heads, num_kv_heads, topk64, softmax_scale,
-                     grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+    return run_kl<128, 64>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk,
+                           softmax_scale, grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
+  return run_kl<128, 128>(index_q, index_k, q, k, lse, block_ids, seqs, num_q_heads, num_kv_heads, topk,
+                          softmax_scale, grad_scale, d_index_q, d_index_k, kl, pl, ws, stream);
 }

@@ -56,6 +56,11 @@ CASES = [
     ("kl_many_items_k32", [2048], [2048], 16, 2, 32, 64, None),
     ("kl_bk128_g16_didx128", [900], [900], 32, 2, 5, 128, None, 128),
     ("kl_bk128_chunked_varlen", [200, 1, 129], [1000, 700, 1500], 16, 2, 4, 64, None, 128),
+    # native 128-key blocks: more than 32 slots, every head-group size
+    ("kl_bk128_k48_g8", [2000], [6500], 16, 2, 48, 128, None, 128),
+    ("kl_bk128_g1_didx64", [260], [900], 2, 2, 7, 64, None, 128),
+    ("kl_bk128_g2", [300], [1300], 4, 2, 9, 128, None, 128),
+    ("kl_bk128_g4_decode_padded", [1, 1, 1, 1], [3000, 128, 129, 1], 16, 4, 6, 64, 3072, 128),
 ]
 
 
@@ -101,13 +106,15 @@ def test_kl_small(case):
 
 def test_kl_rejects_unsupported_shapes():
     """G must be a power of two (the teacher's head mean is a register
-    reduction over aligned rows); block_size 128 runs as 64-key halves, so
-    topk <= 32 there."""
+    reduction over aligned rows); block_size 64 or 128 (both native), at most
+    64 slots (the reverse index's handle field), d_idx 64 or 128."""
     p = synth.packed_problem("kl_g3", [10], [10], num_q_heads=6, num_kv_heads=2, topk=2, seed=1)
     seqs = msa.Seqs.from_problem(p, torch.device("cuda"))
     assert msa.sparse_kl_backward_workspace_size(seqs, 6, 2, 64, 128, 64, 2) == 0
-    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 33) == 0
-    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 32) > 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 65) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 256, 2) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 96, 128, 64, 2) == 0
+    assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 128, 64) > 0
     assert msa.sparse_kl_backward_workspace_size(seqs, 8, 2, 64, 128, 64, 2) > 0
 
 
@@ -188,12 +195,13 @@ def test_kl_workload_sampled(name, n_rows):
     torch.cuda.empty_cache()
 
 
-def test_kl_reproducible():
+@pytest.mark.parametrize("bk,d_idx,H_q", [(64, 64, 16), (128, 128, 32)])
+def test_kl_reproducible(bk, d_idx, H_q):
     """d_index_k adds a key block's queries in the sorted (row, slot) order of
     the reverse index: three runs agree bit for bit (as d_index_q and KL do)."""
-    name = "kl_repro"
-    p = synth.packed_problem(name, [3000], [3000], num_q_heads=16, num_kv_heads=2, topk=16, d_idx=64,
-                             seed=zlib.crc32(name.encode()) % 10000)
+    name = f"kl_repro_{bk}"
+    p = synth.packed_problem(name, [3000], [3000], num_q_heads=H_q, num_kv_heads=2, topk=16, d_idx=d_idx,
+                             block_size=bk, seed=zlib.crc32(name.encode()) % 10000)
     x = synth.generate_numpy(p)
     ids = synth.random_block_ids(p)
     dev = torch.device("cuda")
