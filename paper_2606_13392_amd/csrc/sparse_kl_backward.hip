@@ -143,30 +143,28 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
   }
 }
 
-// One thread per (row, group) of the chunk: LSE_idx = ln sum over the valid
-// slots of exp(partial).
-__global__ __launch_bounds__(256) void kl_lse_combine_kernel(const int32_t* __restrict__ block_ids, msa_seqs sq,
-                                                             const int64_t* __restrict__ blk_base, int BK, int H_kv,
-                                                             int topk,
-                                                             int64_t row0, int64_t nrows,
-                                                             const float* __restrict__ lse_part,
-                                                             float* __restrict__ lse_idx) {
-  const int64_t pr = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+// One wave per (row, group) of the chunk, slot j on lane j: LSE_idx = ln sum
+// over the valid slots of exp(partial) (a fixed butterfly order).
+constexpr int kLseCombWaves = 4;
+__global__ __launch_bounds__(64 * kLseCombWaves) void kl_lse_combine_kernel(
+    const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int BK, int H_kv,
+    int topk, int64_t row0, int64_t nrows, const float* __restrict__ lse_part, float* __restrict__ lse_idx) {
+  const int lane = lane_id();
+  const int64_t pr = static_cast<int64_t>(blockIdx.x) * kLseCombWaves + threadIdx.x / kWave;
   if (pr >= nrows * H_kv) return;
   const int64_t row = row0 + pr / H_kv;
   const int r = static_cast<int>(pr % H_kv);
   int s;
   const int p = row_position(sq, row, &s);
-  const int32_t* ids = block_ids + (row * H_kv + r) * topk;
-  const float* lp = lse_part + pr * topk;
-  float m = -INFINITY;
-  for (int j = 0; j < topk; ++j)
-    if (incidence_ok(ids[j], p, BK, blk_base, s)) m = fmaxf(m, lp[j]);
-  float l = 0.f;
-  if (m > -INFINITY)
-    for (int j = 0; j < topk; ++j)
-      if (incidence_ok(ids[j], p, BK, blk_base, s)) l += __expf(lp[j] - m);
-  lse_idx[pr] = m > -INFINITY ? m + __logf(l) : -INFINITY;
+  const bool ok = lane < topk && incidence_ok(block_ids[(row * H_kv + r) * topk + lane], p, BK, blk_base, s);
+  const float x = ok ? lse_part[pr * topk + lane] : -INFINITY;
+  float m = x;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  float l = m > -INFINITY && ok ? __expf(x - m) : 0.f;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) l += __shfl_xor(l, off);
+  if (lane == 0) lse_idx[pr] = m > -INFINITY ? m + __logf(l) : -INFINITY;
 }
 
 // ---------------------------------------------------------------- LDS staging
@@ -795,8 +793,9 @@ int run_kl(const void* index_q, const void* index_k, const void* q, const void* 
                      static_cast<const int64_t*>(blk_base), static_cast<const int32_t*>(tile_off),
                      static_cast<const int32_t*>(item_off), static_cast<const uint32_t*>(handles), H_kv, topk,
                      pl.nbcap, r0, sidx * kLog2e, lsep, cnt + pl.ntile);
-    msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel, dim3(static_cast<unsigned>((pairs + 255) / 256)),
-                     dim3(256), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), BK, H_kv, topk, r0,
+    msa_prof::launch("kl_lse_combine_kernel", kl_lse_combine_kernel,
+                     dim3(static_cast<unsigned>((pairs + kLseCombWaves - 1) / kLseCombWaves)),
+                     dim3(64 * kLseCombWaves), 0, stream, block_ids, sq, static_cast<const int64_t*>(blk_base), BK, H_kv, topk, r0,
                      nr, static_cast<const float*>(lsep), lsei);
     launch_kl_grad<BK, D>(lg_g, dim3(n_grad), stream, iq, ik, static_cast<const uint16_t*>(q),
                           static_cast<const uint16_t*>(k), lse, static_cast<const float*>(lsei), sq,
