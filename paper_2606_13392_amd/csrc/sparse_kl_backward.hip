@@ -325,9 +325,11 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
 
     const int npass = (nq + kK2Q - 1) / kK2Q;
     // teacher sub-pass (pass, sp): A operands (Q rows 16t + c16) and their LSEs
+    // (loads only: their values are first used a sub-pass later)
     u32x4 aq[NTT][KSM], an[NTT][KSM];                // this sub-pass's, the next one's
-    float al[NTT], aln[NTT];
-    auto load_sub = [&](int ps, int sp, u32x4 (&a)[NTT][KSM], float (&l)[NTT]) {
+    float al[NTT], aln[NTT];                         // raw LSEs
+    bool av[NTT], avn[NTT];                          // row has a query
+    auto load_sub = [&](int ps, int sp, u32x4 (&a)[NTT][KSM], float (&l)[NTT], bool (&v)[NTT]) {
 #pragma unroll
       for (int t = 0; t < NTT; ++t) {
         const int x = sp * R + 16 * t + c16;          // teacher row of the pass
@@ -336,11 +338,58 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
         const int64_t hrow = (row0 + sm.s_row[j]) * H_q + static_cast<int64_t>(r) * G + (x & (G - 1));
 #pragma unroll
         for (int st = 0; st < KSM; ++st) a[t][st] = load_raw(q + hrow * kHeadDim + 32 * st + 8 * qd);
-        l[t] = jq < nq ? lse[hrow] * kLog2e : INFINITY;
+        l[t] = lse[hrow];
+        v[t] = jq < nq;
+      }
+    };
+    // one teacher sub-pass on operands (a, l, v); the next sub-pass's
+    // gathers (the wave's last one reloads a valid row) go out first into
+    // (na, nl, nv), unconditionally, so that no copy waits on them
+    auto sub = [&](int ps, int sp, u32x4 (&a)[NTT][KSM], float (&l)[NTT], bool (&v)[NTT],
+                   u32x4 (&na)[NTT][KSM], float (&nl)[NTT], bool (&nv)[NTT]) {
+      int nps = ps, nsp = sp + 1;
+      if (nsp == NSP) { nps = min(ps + kK2Waves, npass - 1); nsp = 0; }
+      load_sub(nps, nsp, na, nl, nv);
+      asm volatile("" ::: "memory");                  // the gathers stay ahead of this sub-pass's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
+      if (qd == 0) {
+#pragma unroll
+        for (int t = 0; t < NTT; ++t) wv.lse2[16 * t + c16] = v[t] ? l[t] * kLog2e : INFINITY;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt) {
+        f32x4 acc[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) acc[t] = f32x4{};
+#pragma unroll
+        for (int st = 0; st < KSM; ++st) {
+          const bf16x8 kb8 = ld_bf16x8(sm.k + kl_off<kHeadDim>(16 * kt + c16, 32 * st + 8 * qd));
+#pragma unroll
+          for (int t = 0; t < NTT; ++t) acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, a[t][st]), kb8, acc[t]);
+        }
+        const int key = key0 + 16 * kt + c16;
+#pragma unroll
+        for (int t = 0; t < NTT; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = 16 * t + 4 * qd + i;
+            const int xq = (sp * R + row) >> LG;
+            acc[t][i] = key <= wv.pos[xq] ? exp2_hw(acc[t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
+          }
+        if constexpr (LG > 0) head_mean(acc, LG);
+#pragma unroll
+        for (int t = 0; t < NTT; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = 16 * t + 4 * qd + i;
+            if ((row & (G - 1)) == 0) wv.pbar[(sp * R + row) >> LG][16 * kt + c16] = acc[t][i];
+          }
       }
     };
     int ps = w;
-    if (ps < npass) load_sub(ps, 0, aq, al);
+    if (ps < npass) load_sub(ps, 0, aq, al, av);
     for (; ps < npass; ps += kK2Waves) {
       const int cq = ps * kK2Q;
       if (lane < kK2Q) {
@@ -351,50 +400,28 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
         wv.lsei2[lane] = ok ? lse_idx[static_cast<int64_t>(rl) * H_kv + r] * kLog2e : INFINITY;
         wv.inc[lane] = ok ? (static_cast<int64_t>(rl) * H_kv + r) * topk + sm.s_slot[j] : trash_inc;
       }
-      // ---- teacher
+      // the student's index-query rows (lane c16 supplies query c16), in
+      // flight during the teacher
+      u32x4 ai[KSI];
+      {
+        const int j = min(cq + c16, nq - 1);
+        const int64_t grow = row0 + sm.s_row[j];
+#pragma unroll
+        for (int ks = 0; ks < KSI; ++ks) ai[ks] = load_raw(index_q + (grow * H_kv + r) * D + 32 * ks + 8 * qd);
+      }
+      // ---- teacher: sub-passes in pairs, the two operand sets trading roles
+      if constexpr (NSP % 2 == 0) {
 #pragma unroll 1
-      for (int sp = 0; sp < NSP; ++sp) {
-        // the next sub-pass's gathers go out before this one's MFMAs
-        if (sp + 1 < NSP) load_sub(ps, sp + 1, an, aln);
-        else if (ps + kK2Waves < npass) load_sub(ps + kK2Waves, 0, an, aln);
-        if (qd == 0) {
-#pragma unroll
-          for (int t = 0; t < NTT; ++t) wv.lse2[16 * t + c16] = al[t];
+        for (int sp = 0; sp < NSP; sp += 2) {
+          sub(ps, sp, aq, al, av, an, aln, avn);
+          sub(ps, sp + 1, an, aln, avn, aq, al, av);
         }
-        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-#pragma unroll
-        for (int kt = 0; kt < KT; ++kt) {
-          f32x4 acc[2];
-#pragma unroll
-          for (int t = 0; t < 2; ++t) acc[t] = f32x4{};
-#pragma unroll
-          for (int st = 0; st < KSM; ++st) {
-            const bf16x8 kb8 = ld_bf16x8(sm.k + kl_off<kHeadDim>(16 * kt + c16, 32 * st + 8 * qd));
-#pragma unroll
-            for (int t = 0; t < NTT; ++t) acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, aq[t][st]), kb8, acc[t]);
-          }
-          const int key = key0 + 16 * kt + c16;
-#pragma unroll
-          for (int t = 0; t < NTT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = 16 * t + 4 * qd + i;
-              const int xq = (sp * R + row) >> LG;
-              acc[t][i] = key <= wv.pos[xq] ? exp2_hw(acc[t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
-            }
-          if constexpr (LG > 0) head_mean(acc, LG);
-#pragma unroll
-          for (int t = 0; t < NTT; ++t)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int row = 16 * t + 4 * qd + i;
-              if ((row & (G - 1)) == 0) wv.pbar[(sp * R + row) >> LG][16 * kt + c16] = acc[t][i];
-            }
-        }
+      } else {
+        sub(ps, 0, aq, al, av, an, aln, avn);
 #pragma unroll
         for (int t = 0; t < NTT; ++t) {
           al[t] = aln[t];
+          av[t] = avn[t];
 #pragma unroll
           for (int st = 0; st < KSM; ++st) aq[t][st] = an[t][st];
         }
@@ -403,13 +430,6 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
       // ---- student: rows = the pass's 16 queries (lane c16 supplies query c16)
-      u32x4 ai[KSI];
-      {
-        const int j = min(cq + c16, nq - 1);
-        const int64_t grow = row0 + sm.s_row[j];
-#pragma unroll
-        for (int ks = 0; ks < KSI; ++ks) ai[ks] = load_raw(index_q + (grow * H_kv + r) * D + 32 * ks + 8 * qd);
-      }
       float klq[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
