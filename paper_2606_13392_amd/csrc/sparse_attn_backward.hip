@@ -60,8 +60,9 @@ struct BwdSmem {
   // segments XOR-swizzled by row (bwd_qrow_off); filled by DMA
   uint16_t qdo[2][2][kBwdPassRows][kHeadDim];
   uint16_t ds[32][BK + 8];                            // dS of the pass, [row][key]
-  float lse2[2][kBwdPassRows];                        // LSE * log2(e) per pass row (+inf: no row)
-  float dlt[2][kBwdPassRows];                         // D per pass row
+  float lse[2][kBwdPassRows];                         // forward LSE per pass row (copied by DMA; a valid
+                                                      // row's for rows without a query)
+  float dlt[2][kBwdPassRows];                         // D per pass row (likewise)
   int32_t rpos[2][kBwdPassRows];                      // absolute position per pass row (-1: no row)
   int64_t dqoff[2][kBwdPassRows];                     // element offset of the row's dQ partial (the trash row: no row)
   int32_t s_row[kItemQueries];                        // query row inside the chunk
@@ -91,10 +92,24 @@ __device__ __forceinline__ uint2 lds_tr4(const void* p) {
       (__attribute__((address_space(3))) v4i16*)(v4i16*)(const_cast<void*>(p)));
   return __builtin_bit_cast(uint2, x);
 }
-// One 16-byte piece per lane from global memory into LDS (global_load_lds):
-// lane l writes bytes [16 l, 16 l + 16) after the wave-uniform LDS address dst.
+// One 16-byte (or 4-byte) piece per lane from global memory into LDS
+// (global_load_lds): lane l writes bytes [16 l, 16 l + 16) (or [4 l, 4 l + 4))
+// after the wave-uniform LDS address dst.  Issued from inline assembly so
+// that the compiler, which cannot tell the buffers apart, does not wait for
+// these copies before every later LDS read: the pass loop waits for them
+// itself (s_waitcnt before the barrier that publishes them).  M0 holds the
+// LDS address; one wait state separates its write from the copy.
+__device__ __forceinline__ uint32_t bwd_lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<size_t>((__attribute__((address_space(3))) const void*)(p))));
+}
 __device__ __forceinline__ void bwd_dma16(const void* src, void* dst) {
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :: "v"(src), "s"(bwd_lds_addr(dst)) : "m0");
+}
+__device__ __forceinline__ void bwd_dma4(const void* src, void* dst) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :: "v"(src), "s"(bwd_lds_addr(dst)) : "m0");
 }
 
 __device__ __forceinline__ uint16_t raw_elem(const u32x4& w, int j) {
@@ -221,30 +236,27 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
         bwd_dma16(src, &sm.qdo[b][tensor][4 * (piece & 7)][0]);
       }
     };
-    // the pass's row scalars: lanes 0..31 of wave 0 load them ...
-    float nl = 0.f, nd = 0.f;
+    // the pass's row scalars: lanes 0..31 of wave 0 copy LSE and D into
+    // buffer b by DMA and work out the position and dQ offset ...
     int32_t npos = -1;
     int64_t noff = dq_trash;
-    auto load_scalars = [&](int cc) {
+    auto load_scalars = [&](int cc, int b) {
       if (kq == 0 && lane < kBwdPassRows) {
         bool ok;
         const int64_t hr = pass_row(cc, lane, ok);
-        nl = lse[hr];
-        nd = delta[hr];
+        bwd_dma4(lse + hr, &sm.lse[b][0]);
+        bwd_dma4(delta + hr, &sm.dlt[b][0]);
         const int qa = cc + lane / G;
         npos = ok ? pos_base + sm.s_row[qa] : -1;
         noff = ok ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G + lane % G) *
                         kHeadDim
                   : dq_trash;
-        if (!ok) nl = INFINITY;
       }
     };
-    // ... and store them into the other buffer once every wave has stored the
-    // previous pass's dQ (which reads that buffer's offsets)
+    // ... and store those two into the other buffer once every wave has
+    // stored the previous pass's dQ (which reads that buffer's offsets)
     auto store_scalars = [&](int b) {
       if (kq == 0 && lane < kBwdPassRows) {
-        sm.lse2[b][lane] = nl == INFINITY ? INFINITY : nl * kLog2e;
-        sm.dlt[b][lane] = nd;
         sm.rpos[b][lane] = npos;
         sm.dqoff[b][lane] = noff;
       }
@@ -270,18 +282,18 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
     };
 
     issue_dma(0, 0);
-    load_scalars(0);
+    load_scalars(0, 0);
     store_scalars(0);
     int buf = 0;
     for (int c = 0; c < nq; c += qpw, buf ^= 1) {
-      __builtin_amdgcn_s_waitcnt(0);                  // this wave's DMA pieces of the pass have landed
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's copies for the pass have landed
       __syncthreads();                                // every wave's pieces, the pass's scalars; the
                                                       // previous pass is done with ds and the other buffer
       if (pend_buf >= 0) store_dq(pend_buf);
       const bool more = c + qpw < nq;
       if (more) {
         issue_dma(c + qpw, buf ^ 1);
-        load_scalars(c + qpw);
+        load_scalars(c + qpw, buf ^ 1);
       }
       const uint8_t* qb = reinterpret_cast<const uint8_t*>(&sm.qdo[buf][0][0][0]);
       const uint8_t* dob = reinterpret_cast<const uint8_t*>(&sm.qdo[buf][1][0][0]);
@@ -308,7 +320,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int prow = 16 * t + 4 * qd + i;
-          const float l2 = sm.lse2[buf][prow];
+          const float l2 = sm.lse[buf][prow] * kLog2e;
           const bool vis = key <= sm.rpos[buf][prow] && l2 > -INFINITY;
           const float p = vis ? exp2_hw(acc_s[t][i] * scale_log2 - l2) : 0.f;
           acc_s[t][i] = p;
@@ -349,7 +361,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
       }
       __syncthreads();                                // dS of every key slice in LDS; every wave's
                                                       // store_dq of this pass has read the other buffer
-      if (more) store_scalars(buf ^ 1);               // the next pass's scalars (their loads have landed)
+      if (more) store_scalars(buf ^ 1);               // the next pass's positions and dQ offsets
 
       // dQ of the pass, dims (128 / NKW) kq + 16u + c16, over the block's keys;
       // B: keys 32ks + 8qd .. + 7 of that dim, read down K's column
