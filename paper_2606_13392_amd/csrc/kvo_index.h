@@ -318,11 +318,23 @@ __device__ __forceinline__ int32_t claim_next_item(int32_t* __restrict__ next_it
 // tile's handle list comes out in a run-dependent order.  Kernels whose sums
 // run over a tile's handles (the training backward's dK / dV and d k_idx)
 // sort each list into ascending handle order -- row, then slot -- which makes
-// their results bit-reproducible.  One CTA per tile: runs of kSortRun handles
-// are sorted in LDS (bitonic), then merged pairwise through `tmp` (each
-// element's place in the merged run is its rank in its own run plus its rank
-// among the other run's elements; the handles of a tile are distinct).
+// their results bit-reproducible.  A row selects a block once, so a tile's
+// handles have distinct rows and the order is the rows' order.  One CTA per
+// tile, two launches:
+//   sort_tile_handles_kernel   tiles of at most kSortRun handles: bitonic
+//                              sort in LDS;
+//   rank_tile_handles_kernel   longer tiles: the rows are marked in an LDS
+//                              bitmap over the tile's row span, and each
+//                              handle's place is the number of marked rows
+//                              below its own (popcounts; a prefix per 32
+//                              words); spans of more than kRankMapWords * 32
+//                              rows (or a row listed twice) fall back to
+//                              merging sorted runs pairwise through `tmp` (a
+//                              handle's place in a merged run is its rank in
+//                              its own run plus its rank among the other
+//                              run's handles).
 constexpr int kSortRun = 2048;
+constexpr int kRankMapWords = 32768;                  // 1M rows of span, 128 KiB of LDS
 
 __device__ __forceinline__ int32_t count_below(const uint32_t* __restrict__ a, int32_t n, uint32_t x) {
   int32_t lo = 0, hi = n;                      // first index with a[i] >= x
@@ -333,55 +345,153 @@ __device__ __forceinline__ int32_t count_below(const uint32_t* __restrict__ a, i
   return lo;
 }
 
+// Bitonic sort of a[0 .. m) (m <= kSortRun) through the LDS array sh.
+__device__ __forceinline__ void sort_run_lds(uint32_t* __restrict__ a, int32_t m, uint32_t* sh) {
+  const int tid = threadIdx.x;
+  int32_t P = 1;
+  while (P < m) P <<= 1;
+  for (int32_t i = tid; i < P; i += 256) sh[i] = i < m ? a[i] : 0xFFFFFFFFu;
+  __syncthreads();
+  for (int32_t kk = 2; kk <= P; kk <<= 1)
+    for (int32_t j = kk >> 1; j > 0; j >>= 1) {
+      for (int32_t i = tid; i < P; i += 256) {
+        const int32_t ixj = i ^ j;
+        if (ixj > i) {
+          const uint32_t x = sh[i], y = sh[ixj];
+          const bool up = (i & kk) == 0;
+          if ((x > y) == up) { sh[i] = y; sh[ixj] = x; }
+        }
+      }
+      __syncthreads();
+    }
+  for (int32_t i = tid; i < m; i += 256) a[i] = sh[i];
+  __syncthreads();
+}
+
 __global__ __launch_bounds__(256) void sort_tile_handles_kernel(uint32_t* __restrict__ handles,
-                                                                uint32_t* __restrict__ tmp,
                                                                 const int32_t* __restrict__ tile_off) {
   __shared__ uint32_t sh[kSortRun];
   const int64_t t = blockIdx.x;
   const int32_t beg = tile_off[t];
   const int32_t n = tile_off[t + 1] - beg;
-  if (n <= 1) return;                                 // uniform over the CTA
+  if (n <= 1 || n > kSortRun) return;                // uniform over the CTA
+  sort_run_lds(handles + beg, n, sh);
+}
+
+// a[0 .. n) sorted as runs of kSortRun (through sh), then merged pairwise
+// through b; the result ends in a.
+__device__ __forceinline__ void sort_by_merging(uint32_t* __restrict__ a, uint32_t* __restrict__ b, int32_t n,
+                                                uint32_t* sh) {
   const int tid = threadIdx.x;
-  uint32_t* a = handles + beg;
-  uint32_t* b = tmp + beg;
-  for (int32_t r0 = 0; r0 < n; r0 += kSortRun) {
-    const int32_t m = min(kSortRun, n - r0);
-    int32_t P = 1;
-    while (P < m) P <<= 1;
-    for (int32_t i = tid; i < P; i += 256) sh[i] = i < m ? a[r0 + i] : 0xFFFFFFFFu;
-    __syncthreads();
-    for (int32_t kk = 2; kk <= P; kk <<= 1)
-      for (int32_t j = kk >> 1; j > 0; j >>= 1) {
-        for (int32_t i = tid; i < P; i += 256) {
-          const int32_t ixj = i ^ j;
-          if (ixj > i) {
-            const uint32_t x = sh[i], y = sh[ixj];
-            const bool up = (i & kk) == 0;
-            if ((x > y) == up) { sh[i] = y; sh[ixj] = x; }
-          }
-        }
-        __syncthreads();
-      }
-    for (int32_t i = tid; i < m; i += 256) a[r0 + i] = sh[i];
-    __syncthreads();
-  }
+  for (int32_t r0 = 0; r0 < n; r0 += kSortRun) sort_run_lds(a + r0, min(kSortRun, n - r0), sh);
   uint32_t* src = a;
   uint32_t* dst = b;
   for (int32_t w = kSortRun; w < n; w <<= 1) {
     for (int32_t i = tid; i < n; i += 256) {
-      const int32_t lo = (i / (2 * w)) * (2 * w);     // the pair of runs holding i
-      const int32_t mid = min(lo + w, n), hi = min(lo + 2 * w, n);
+      const int32_t l0 = (i / (2 * w)) * (2 * w);     // the pair of runs holding i
+      const int32_t mid = min(l0 + w, n), h1 = min(l0 + 2 * w, n);
       const uint32_t x = src[i];
-      const int32_t pos = i < mid ? lo + (i - lo) + count_below(src + mid, hi - mid, x)
-                                  : lo + (i - mid) + count_below(src + lo, mid - lo, x);
+      const int32_t pos = i < mid ? l0 + (i - l0) + count_below(src + mid, h1 - mid, x)
+                                  : l0 + (i - mid) + count_below(src + l0, mid - l0, x);
       dst[pos] = x;
     }
     __syncthreads();
     uint32_t* sw = src; src = dst; dst = sw;
   }
-  if (src != a) {
+  if (src != a)
     for (int32_t i = tid; i < n; i += 256) a[i] = src[i];
+}
+
+__global__ __launch_bounds__(256) void rank_tile_handles_kernel(uint32_t* __restrict__ handles,
+                                                                uint32_t* __restrict__ tmp,
+                                                                const int32_t* __restrict__ tile_off) {
+  __shared__ uint32_t map[kRankMapWords];
+  __shared__ int32_t grp[kRankMapWords / 32];         // marked rows before each 32-word group
+  __shared__ uint32_t red[2][256 / kWave];
+  __shared__ int32_t scan[256];
+  const int64_t t = blockIdx.x;
+  const int32_t beg = tile_off[t];
+  const int32_t n = tile_off[t + 1] - beg;
+  if (n <= kSortRun) return;                          // uniform over the CTA
+  const int tid = threadIdx.x, lane = lane_id(), wave = tid / kWave;
+  uint32_t* a = handles + beg;
+  uint32_t* b = tmp + beg;
+  // the tile's row span
+  uint32_t lo = 0xFFFFFFFFu, hi = 0;
+  for (int32_t i = tid; i < n; i += 256) {
+    const uint32_t r = a[i] >> 6;
+    lo = min(lo, r);
+    hi = max(hi, r);
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    lo = min(lo, static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), off)));
+    hi = max(hi, static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), off)));
+  }
+  if (lane == 0) { red[0][wave] = lo; red[1][wave] = hi; }
+  __syncthreads();
+  lo = red[0][0];
+  hi = red[1][0];
+#pragma unroll
+  for (int w = 1; w < 256 / kWave; ++w) { lo = min(lo, red[0][w]); hi = max(hi, red[1][w]); }
+  const int64_t words = (static_cast<int64_t>(hi) - lo + 32) / 32;
+  if (words > kRankMapWords) {                        // span too wide for the bitmap
+    sort_by_merging(a, b, n, map);
+    return;
+  }
+  const int nw = static_cast<int>(words);
+  const int ng = (nw + 31) / 32;
+  for (int i = tid; i < nw; i += 256) map[i] = 0;
+  __syncthreads();
+  for (int32_t i = tid; i < n; i += 256) {
+    const uint32_t r = (a[i] >> 6) - lo;
+    atomicOr(&map[r >> 5], 1u << (r & 31));
+  }
+  __syncthreads();
+  // marked rows per 32-word group, exclusive prefix over the groups (each
+  // thread owns up to 4 consecutive groups)
+  int32_t cnt[4];
+  int32_t own = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int g = 4 * tid + q;
+    int32_t c = 0;
+    if (g < ng)
+      for (int w = 32 * g; w < min(32 * g + 32, nw); ++w) c += __popc(map[w]);
+    cnt[q] = c;
+    own += c;
+  }
+  scan[tid] = own;
+  __syncthreads();
+  for (int off = 1; off < 256; off <<= 1) {
+    const int32_t v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  if (scan[255] != n) {                               // a row listed twice (not a valid selection):
+    __syncthreads();                                  // order by (row, slot) all the same
+    sort_by_merging(a, b, n, map);
+    return;
+  }
+  int32_t run = scan[tid] - own;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int g = 4 * tid + q;
+    if (g < ng) grp[g] = run;
+    run += cnt[q];
+  }
+  __syncthreads();
+  for (int32_t i = tid; i < n; i += 256) {
+    const uint32_t h = a[i];
+    const uint32_t r = (h >> 6) - lo;
+    const int w = static_cast<int>(r >> 5);
+    int32_t rank = grp[w >> 5] + __popc(map[w] & ((1u << (r & 31)) - 1u));
+    for (int v = w & ~31; v < w; ++v) rank += __popc(map[v]);
+    b[rank] = h;
+  }
+  __syncthreads();
+  for (int32_t i = tid; i < n; i += 256) a[i] = b[i];
 }
 
 // Reverse index of query rows r0 .. r0 + nr - 1 (one chunk): counts, scans
@@ -405,11 +515,14 @@ void build_reverse_index(const int32_t* block_ids, const msa_seqs& sq, const int
                    dim3(256), 0, stream, blk_tot, ntile, tile_off, item_off);
   msa_prof::launch("kvo_fill_kernel", kvo_fill_kernel, dim3(gthreads), dim3(256), 0, stream, block_ids, sq, blk_base,
                    H_kv, BK, topk, nbcap, r0, nr, tile_off, tpos, handles);
-  // positions are no longer needed: tpos is the sort's merge buffer
-  if (canonical)
+  // positions are no longer needed: tpos is the long tiles' scatter buffer
+  if (canonical) {
     msa_prof::launch("sort_tile_handles_kernel", sort_tile_handles_kernel, dim3(static_cast<unsigned>(ntile)),
+                     dim3(256), 0, stream, handles, static_cast<const int32_t*>(tile_off));
+    msa_prof::launch("rank_tile_handles_kernel", rank_tile_handles_kernel, dim3(static_cast<unsigned>(ntile)),
                      dim3(256), 0, stream, handles, reinterpret_cast<uint32_t*>(tpos),
                      static_cast<const int32_t*>(tile_off));
+  }
 }
 
 }  // namespace
