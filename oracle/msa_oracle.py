@@ -15,7 +15,8 @@ What it computes, in the paper's order and notation:
   with no visible token score -inf), and Top-k block selection with the local
   block always included (Sec. 3.1 last paragraph of "Index Branch"; Sec. 3.2
   "Local Block"; Appendix C.2 final recipe: only the incomplete self block is
-  forced, no sink).
+  forced, no sink); and the Top-k operator alone on a given score matrix
+  (Sec. 4.1 latency table).
 * Main Branch (Sec. 3.1, sparse-attention equation): exact softmax attention of
   each query head of group r over the causally visible tokens of the selected
   blocks, using key/value head r; also the natural-log log-sum-exp.
@@ -252,6 +253,23 @@ def selection_is_valid(ids: np.ndarray, block_scores: np.ndarray, pos: int, bloc
     if not nonlocal_sel or not unsel:
         return True
     return min(block_scores[b] for b in nonlocal_sel) >= max(block_scores[b] for b in unsel) - tol
+
+
+def row_topk(scores: np.ndarray, k: int) -> np.ndarray:
+    """The Top-k operator on its own: for each row of an (N, B) score matrix,
+    the min(k, B) columns of largest score, equal scores keeping the lower
+    column (R3), listed ascending and padded with -1 to ``k`` (Sec. 3.1 top-k
+    equation without the forced local block; Sec. 4.1 latency table: fp32
+    inputs of shape (N, B), rows processed independently).  -0 equals +0."""
+    scores = np.asarray(scores)
+    n, B = scores.shape
+    out = np.full((n, k), -1, dtype=np.int32)
+    cols = np.arange(B)
+    for i in range(n):
+        order = np.lexsort((cols, -scores[i].astype(np.float64)))
+        sel = np.sort(cols[order[:k]])
+        out[i, :sel.shape[0]] = sel
+    return out
 
 
 # --------------------------------------------------------------------------

@@ -215,6 +215,35 @@ def pin_row_block_scores(O, seed=43):
             assert len(got) == (pos + B) // B       # blocks up to the local one
 
 
+def pin_row_topk(O, seed=47):
+    """Top-k of each row against its definition by counting: column c is
+    selected iff fewer than k columns beat it (a larger score, or an equal
+    score and a lower column); -0 and +0 tie, -inf ranks like any value.
+    Also k = 1 against numpy's argmax (first maximum), k >= B (every column),
+    and tie-free rows against torch.topk's index set."""
+    rng = np.random.default_rng(seed)
+    pool = np.array([-np.inf, -2.5, -1.0, -0.0, 0.0, 0.5, 1.0, 3.0], dtype=np.float32)
+    for n_cols, k in ((13, 4), (9, 9), (5, 8), (16, 1), (31, 7)):
+        x = rng.choice(pool, size=(20, n_cols))
+        got = O.row_topk(x, k)
+        assert got.shape == (20, k) and got.dtype == np.int32
+        for i in range(20):
+            sel = []
+            for c in range(n_cols):
+                beats = sum(1 for d in range(n_cols)
+                            if x[i, d] > x[i, c] or (x[i, d] == x[i, c] and d < c))
+                if beats < k:
+                    sel.append(c)
+            want = sel + [-1] * (k - len(sel))
+            assert list(got[i]) == want, (i, list(got[i]), want)
+    x = rng.choice(pool, size=(40, 11))
+    assert np.array_equal(O.row_topk(x, 1)[:, 0], np.argmax(x, axis=1))
+    assert np.array_equal(O.row_topk(x, 11), np.tile(np.arange(11, dtype=np.int32), (40, 1)))
+    y = rng.standard_normal((30, 500)).astype(np.float32)
+    want = np.sort(torch.topk(torch.from_numpy(y), 24, dim=1).indices.numpy(), axis=1)
+    assert np.array_equal(O.row_topk(y, 24), want)
+
+
 def pin_block_maxima_partial(O):
     """Partial last block (Sec. 2.3) and the causal cut inside the local block."""
     rng = np.random.default_rng(11)
@@ -611,7 +640,7 @@ def pin_kl_mixture_closed_form(O):
 
 ALL_PINS = [pin_flops_ratio, pin_effective_flops_dense, pin_brute_force_selection,
             pin_planted_closed_form, pin_selection_invariants, pin_tie_rule_validator,
-            pin_row_block_scores, pin_block_maxima_partial,
+            pin_row_block_scores, pin_row_topk, pin_block_maxima_partial,
             pin_dense_equality, pin_closed_forms, pin_combine,
             pin_decode_and_chunked_consistency, pin_head_permutation,
             pin_fp8_e4m3_codes, pin_fp8_attention_scales,

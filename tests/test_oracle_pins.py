@@ -64,6 +64,12 @@ MUTATIONS = {
                               "ik = decode_bf16(index_k_bits[kv0:kv0 + pos])\n    iq = decode_bf16(index_q_bits[row, group])"),
     "row_scores_no_kv_start": ("ik = decode_bf16(index_k_bits[kv0:kv0 + pos + 1])\n    iq = decode_bf16(index_q_bits[row, group])",
                                "ik = decode_bf16(index_k_bits[0:pos + 1])\n    iq = decode_bf16(index_q_bits[row, group])"),
+    "row_topk_smallest": ("order = np.lexsort((cols, -scores[i].astype(np.float64)))",
+                          "order = np.lexsort((cols, scores[i].astype(np.float64)))"),
+    "row_topk_tie_higher_column": ("order = np.lexsort((cols, -scores[i].astype(np.float64)))",
+                                   "order = np.lexsort((-cols, -scores[i].astype(np.float64)))"),
+    "row_topk_rank_order_output": ("sel = np.sort(cols[order[:k]])", "sel = cols[order[:k]]"),
+    "row_topk_one_short": ("sel = np.sort(cols[order[:k]])", "sel = np.sort(cols[order[:k - 1]])"),
     "head_to_group_modulo": ("O[i, g * G:(g + 1) * G], L[i, g * G:(g + 1) * G] = attend(\n                qf[g * G:(g + 1) * G], keys, vals, scale)",
                              "O[i, g::H_kv], L[i, g::H_kv] = attend(\n                qf[g::H_kv], keys, vals, scale)"),
 }
