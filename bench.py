@@ -578,6 +578,50 @@ def run_decode_paged(p, d, seqs, ids_ref, o_ref, lse_ref, args, dev, blocks_per_
             "page_rows": B * blocks_per_page, "bit_identical_to_contiguous": same}
 
 
+# The paper's Top-k latency table (Sec. 4.1; H800, fp32 (N, B) inputs, unsorted
+# outputs, median of 50 iterations): (N, B, k) -> torch.topk, TileLang, theirs, in us
+PAPER_TOPK_US_H800 = {(131072, 1024, 16): (3970, 2864, 779), (131072, 2048, 32): (5378, 3630, 1991),
+                      (524288, 4096, 16): (33810, 17779, 7880), (524288, 8192, 32): (57659, 26100, 21326)}
+
+
+def run_topk_latency(args, dev):
+    """msa_block_topk (the Top-k operator on its own) and torch.topk on the
+    paper's table shapes, median of 50 individually event-timed calls after
+    warm-up, as the paper measures."""
+    import torch
+    from paper_2606_13392_amd import msa, synth
+
+    def median_us(fn, iters=50, warm=5):
+        for _ in range(warm):
+            fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) * 1e3 for a, b in ev)
+        return t[len(t) // 2]
+
+    rows = []
+    for (N, B, k) in synth.TOPK_SHAPES:
+        x = synth.topk_scores(N, B, seed=N + B + k, device=dev)
+        out = torch.empty((N, k), dtype=torch.int32, device=dev)
+        ours = median_us(lambda: msa.block_topk(x, k, out=out))
+        ref = median_us(lambda: torch.topk(x, k, dim=1, sorted=False))
+        p_torch, p_tl, p_ours = PAPER_TOPK_US_H800[(N, B, k)]
+        rows.append({"N": N, "B": B, "k": k, "us": ours, "torch_topk_us": ref, "vs_torch_topk": ref / ours,
+                     "score_read_gbs": N * B * 4 / (ours * 1e-6) / 1e9,
+                     "hbm_frac": N * B * 4 / (ours * 1e-6) / 1e9 / PEAK_HBM_GBS,
+                     "paper_h800_us": p_ours, "paper_h800_vs_torch": p_torch / p_ours,
+                     "paper_h800_vs_tilelang": p_tl / p_ours})
+        log(f"[bench] top-k N {N} B {B} k {k}: {ours:.1f} us (torch.topk {ref:.1f} us; paper H800 {p_ours} us)")
+        del x, out
+        torch.cuda.empty_cache()
+    return {"inputs": "i.i.d. N(0,1) fp32 score rows (seeded, on the device)", "timing": "median of 50",
+            "shapes": rows}
+
+
 def cpu_baseline(pre, args):
     """The CPU oracle on a bounded sample of query rows spread evenly over
     depth (host cores); the full-problem time is extrapolated from it."""
@@ -639,6 +683,8 @@ def main():
                     help="shape of the training step (forward + Main Branch backward + KL backward)")
     ap.add_argument("--train-steps", type=int, default=3)
     ap.add_argument("--no-train", action="store_true")
+    ap.add_argument("--no-topk", action="store_true",
+                    help="skip the Top-k operator on the paper's latency-table shapes")
     ap.add_argument("--cpu-sample-rows", type=int, default=300)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-dense", action="store_true", help="skip the dense causal GQA baseline")
@@ -721,6 +767,8 @@ def main():
         line["decode"] = run_decode(args, dev)
     if not args.no_train:
         line["training"] = run_training(args, dev)
+    if not args.no_topk:
+        line["topk_latency"] = run_topk_latency(args, dev)
     print(json.dumps(line), flush=True)
 
 

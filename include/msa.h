@@ -10,6 +10,7 @@
  * stage and per inference phase:
  *
  *   msa_index_topk           Index Branch: block scores + Top-k (prefill and decode)
+ *   msa_block_topk           the Top-k operator alone, on a score matrix the caller holds
  *   msa_sparse_attn_prefill  Main Branch for many query rows per sequence
  *   msa_sparse_attn_decode   Main Branch for one query row per sequence
  *   msa_sparse_attn_*_fp8    Main Branch on e4m3 queries and KV cache
@@ -153,6 +154,28 @@ int msa_index_topk(const void* index_q, const void* index_k, const msa_seqs* seq
 int msa_index_topk_noalloc(const void* index_q, const void* index_k, const msa_seqs* seqs,
                            int num_kv_heads, int d_idx, int block_size, int topk,
                            int32_t* block_ids, hipStream_t stream);
+
+/* ------------------------------------------------------------------------
+ * msa_block_topk -- the Top-k operator of the Index Branch on its own, for a
+ * score matrix the caller already holds (Sec. 3.1 top-k equation; Sec. 4.1
+ * "Per-thread register top-k" and its latency table, which times this
+ * operator on fp32 inputs of shape (N, B) with rows processed independently).
+ *
+ *   scores  fp32 [n_rows, ld]: columns 0 .. n_cols-1 of each row are ranked;
+ *           the buffer spans n_rows * ld floats.
+ *   ids     int32 [n_rows, k]  OUTPUT: the min(k, n_cols) columns of largest
+ *           score of each row in ascending order, then -1 padding.  Equal
+ *           scores keep the lower column; -0 equals +0; -inf ranks below
+ *           every finite score like any other value.
+ *
+ * No block is forced and no causal limit applies (msa_index_topk adds both).
+ * Supported: 1 <= k <= 64; 0 <= n_cols <= 2^30; ld >= n_cols.  NaN
+ * scores give unspecified (memory-safe) ids.  No workspace.  Rows that are
+ * 16-byte aligned (scores aligned, ld % 4 == 0) are read four columns per
+ * lane and load; others one column per lane.
+ * ------------------------------------------------------------------------ */
+int msa_block_topk(const float* scores, int64_t n_rows, int n_cols, int64_t ld, int k,
+                   int32_t* ids, hipStream_t stream);
 
 /* ------------------------------------------------------------------------
  * Main Branch: msa_sparse_attn_prefill / msa_sparse_attn_decode

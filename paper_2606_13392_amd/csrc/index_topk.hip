@@ -699,6 +699,154 @@ __device__ __forceinline__ uint64_t scan_row_pruned(Load load, LoadCm cm, LoadPm
   return kb.list;
 }
 
+// ---------------------------------------------------------------- radix selection
+// The largest t such that at least K of the wave's values x[0 .. V) (all
+// lanes; absent values are 0) are >= t: the K-th largest value when at least K
+// are present.  Bit by bit from the top, one compare per value and bit; the
+// counts are wave-uniform (ballot + popcount), so no value moves between lanes.
+// With LOBIT > 0 only bits 31 .. LOBIT are decided (the lower ones stay 0):
+// a lower bound of that value, within 2^LOBIT of it.
+template <int V, int LOBIT = 0>
+__device__ __forceinline__ uint32_t kth_largest_u32(const uint32_t* x, int K) {
+  uint32_t t = 0;
+  for (int bit = 31; bit >= LOBIT; --bit) {
+    const uint32_t c = t | (1u << bit);
+    int n = 0;
+#pragma unroll
+    for (int v = 0; v < V; ++v) n += __popcll(__ballot(x[v] >= c));
+    if (n >= K) t = c;
+  }
+  return t;
+}
+
+// A lower bound of the K-th largest of up to 16 values per lane (nv used),
+// exact in its top 16 bits (for an ordered float: sign, exponent and 7
+// mantissa bits).
+__device__ __forceinline__ uint32_t kth_largest_bound(const uint32_t* x, int nv, int K) {
+  if (nv <= 2) return kth_largest_u32<2, 16>(x, K);
+  if (nv <= 4) return kth_largest_u32<4, 16>(x, K);
+  if (nv <= 8) return kth_largest_u32<8, 16>(x, K);
+  return kth_largest_u32<16, 16>(x, K);
+}
+
+__device__ __forceinline__ int lanes_below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0));
+}
+
+// Exact selection of a row through radix searches instead of sorting
+// networks.  A bound t1 <= the row's K1-th best score -- the K1-th largest
+// piece maximum (K1 distinct pieces each hold a score >= it), or for rows of
+// at most K1 pieces the K1-th largest score itself, either to 16 bits from
+// below -- leaves few candidates: the scores >= t1 (of the pieces that reach
+// t1) are appended as keys to `buf` (2 kWave entries) and the K1-th largest
+// key among them is found by a radix search on the score half, and on the id
+// half among equal scores at the boundary.  On return lanes 0 .. K1-1 of
+// `list` hold the K1 best keys (in no order).  Returns false, deciding
+// nothing, when the candidates overflow `buf` (rows with many equal scores)
+// or the row has more than kSurvivorCap pieces; the caller then ranks the row
+// by the pruned scan.  M rows are 16-byte aligned with a multiple of 4 floats.
+template <typename LoadPm>
+__device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow, LoadPm pm, int nscan, int K1,
+                                                 uint64_t* buf, int32_t* surv, uint64_t& list) {
+  const int lane = lane_id();
+  if (K1 <= 0) return false;
+  if (nscan <= K1) {                                      // every candidate block is selected
+    list = lane < nscan ? rank_key(0.f, static_cast<uint32_t>(lane)) : 0ull;
+    return true;
+  }
+  const int npiece = (nscan + kPieceBlocks - 1) / kPieceBlocks;
+  if (npiece > kSurvivorCap) return false;
+  const bool direct = npiece <= K1;                       // rank the scores themselves
+  const int nval = direct ? nscan : npiece;               // <= kSurvivorCap either way
+  constexpr int kGroups = kSurvivorCap / kWave;
+  const int nv = (nval + kWave - 1) / kWave;
+  uint32_t pv[kGroups];
+#pragma unroll
+  for (int k = 0; k < kGroups; ++k) {
+    const int c = kWave * k + lane;
+    pv[k] = k < nv && c < nval ? ordered_u32(direct ? mrow[c] : pm(c)) : 0u;
+  }
+  const uint32_t t1 = kth_largest_bound(pv, nv, K1);
+  if (t1 == 0) return false;
+  // the float with ordered value t1 (scores compare against it directly)
+  const float t1f = __uint_as_float((t1 & 0x80000000u) ? (t1 & 0x7FFFFFFFu) : ~t1);
+  constexpr int kBuf = 2 * kWave;
+  int cnt = 0;
+  auto append = [&](bool take, float x, int b) {
+    const uint64_t m = __ballot(take);
+    const int pos = cnt + lanes_below(m);
+    if (take && pos < kBuf) buf[pos] = rank_key(x, static_cast<uint32_t>(b));
+    cnt += __popcll(m);
+  };
+  if (direct) {
+#pragma unroll
+    for (int k = 0; k < kGroups; ++k)
+      if (k < nv) {
+        const int c = kWave * k + lane;
+        append(pv[k] >= t1, __uint_as_float((pv[k] & 0x80000000u) ? (pv[k] & 0x7FFFFFFFu) : ~pv[k]), c);
+      }
+  } else {
+    int ns = 0;
+#pragma unroll
+    for (int k = 0; k < kGroups; ++k)
+      if (k < nv) {
+        const bool ok = pv[k] >= t1;
+        const uint64_t m = __ballot(ok);
+        if (ok) surv[ns + lanes_below(m)] = kWave * k + lane;
+        ns += __popcll(m);
+      }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // scores of the surviving pieces, 16 pieces per wave load: lane l reads
+    // blocks 4 (l & 3) .. + 3 of piece surv[16 i + (l >> 2)] as one float4;
+    // rounds of 8 loads, all in flight together
+    constexpr int kLoads = 8;
+    for (int r0 = 0; r0 < ns; r0 += 16 * kLoads) {
+      f32x4 x[kLoads];
+      int bb[kLoads];
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        const int q = r0 + 16 * i + (lane >> 2);
+        bb[i] = q < ns ? kPieceBlocks * surv[q] + 4 * (lane & 3) : nscan;
+        x[i] = bb[i] < nscan ? *reinterpret_cast<const f32x4*>(mrow + bb[i]) : f32x4{};
+      }
+#pragma unroll
+      for (int i = 0; i < kLoads; ++i) {
+        if (r0 + 16 * i >= ns) break;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) append(bb[i] + e < nscan && x[i][e] >= t1f, x[i][e], bb[i] + e);
+      }
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  if (cnt > kBuf || cnt < K1) return false;
+  const uint64_t c0 = lane < cnt ? buf[lane] : 0ull;
+  const uint64_t c1 = kWave + lane < cnt ? buf[kWave + lane] : 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  uint32_t h[2] = {static_cast<uint32_t>(c0 >> 32), static_cast<uint32_t>(c1 >> 32)};
+  const uint32_t tv = kth_largest_u32<2>(h, K1);         // >= t1 > 0, so absent entries never match
+  const int n_gt = __popcll(__ballot(h[0] > tv)) + __popcll(__ballot(h[1] > tv));
+  const int n_eq = __popcll(__ballot(h[0] == tv)) + __popcll(__ballot(h[1] == tv));
+  const int need = K1 - n_gt;                             // 1 <= need <= n_eq
+  uint64_t kk = static_cast<uint64_t>(tv) << 32;
+  if (n_eq != need) {
+    uint32_t l[2] = {h[0] == tv ? static_cast<uint32_t>(c0) : 0u, h[1] == tv ? static_cast<uint32_t>(c1) : 0u};
+    kk |= kth_largest_u32<2>(l, need);
+  }
+  const bool s0 = c0 >= kk && c0 != 0ull, s1 = c1 >= kk && c1 != 0ull;
+  const uint64_t m0 = __ballot(s0), m1 = __ballot(s1);
+  if (s0) buf[lanes_below(m0)] = c0;
+  if (s1) buf[__popcll(m0) + lanes_below(m1)] = c1;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  list = lane < K1 ? buf[lane] : 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return true;
+}
+
 // Local block + the K1 best keys of `list`, ids ascending, -1 padded.
 __device__ __forceinline__ void finish_row(uint64_t list, int K1, int lb, int topk, int32_t* __restrict__ out) {
   const int lane = lane_id();
@@ -728,13 +876,17 @@ __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64
   RowTask t;
   t.ok = false;
   t.no_position = false;
-  const int64_t uidx = u0 + task / rpu;
-  const int L = static_cast<int>(task % rpu);          // index row inside the unit
+  // task is wave-uniform and below 2^32 (the host checks), H_kv and BK are
+  // powers of two: the arithmetic stays scalar and 32-bit
+  const uint32_t tk = static_cast<uint32_t>(task);
+  const uint32_t uq = tk / static_cast<uint32_t>(rpu);
+  const int64_t uidx = u0 + uq;
+  const int L = static_cast<int>(tk - uq * static_cast<uint32_t>(rpu));   // index row inside the unit
   const int64_t slot = (uidx - u0) * (static_cast<int64_t>(U) * kWave) + L;
   UnitRows ur = locate_unit(sq, unit_off, uidx, qr, U);
   if (!ur.ok || L >= ur.nq * H_kv) return t;
-  const int row = ur.t0 + L / H_kv;
-  const int r = L % H_kv;
+  const int row = ur.t0 + (L >> __builtin_ctz(H_kv));
+  const int r = L & (H_kv - 1);
   t.out = block_ids + (static_cast<int64_t>(ur.g.q_begin + row) * H_kv + r) * topk;
   const int p = ur.g.kv_len - ur.g.q_rows + row;
   t.ok = true;
@@ -742,7 +894,7 @@ __device__ __forceinline__ RowTask locate_row(const float* __restrict__ M, int64
     t.no_position = true;
     return t;
   }
-  t.lb = p / BK;
+  t.lb = p >> __builtin_ctz(BK);
   t.nscan = min(t.lb, static_cast<int>(ldm));      // == lb whenever kv_lens respect max_kv_len
   t.mrow = M + slot * ldm;
   t.slot = slot;
@@ -759,7 +911,7 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   __shared__ uint64_t s_pend[kWaves][2 * kWave];
   __shared__ int32_t s_surv[kWaves][kSurvivorCap];
   const int lane = lane_id();
-  const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + threadIdx.x / kWave;
+  const int64_t task = static_cast<int64_t>(blockIdx.x) * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x) / kWave;
   if (task >= (u1 - u0) * rpu) return;
   const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, rpu, u0, task, BK, topk, block_ids);
   if (!t.ok) return;
@@ -778,7 +930,8 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
     auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
     const float* pmrow = PM + t.slot;
     auto pm = [=](int q) { return pmrow[static_cast<int64_t>(q) * cm_stride]; };
-    list = scan_row_pruned(load, cm, pm, t.nscan, kb, s_surv[threadIdx.x / kWave]);
+    if (!select_row_radix(mrow, pm, t.nscan, topk - 1, kb.pend, s_surv[threadIdx.x / kWave], list))
+      list = scan_row_pruned(load, cm, pm, t.nscan, kb, s_surv[threadIdx.x / kWave]);
   } else {
     list = scan_row_batched(load, t.nscan, kb);
   }
@@ -820,6 +973,65 @@ __global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
     }
   }
   if (w == 0) finish_row(list, K1, t.lb, topk, t.out);
+}
+
+// ---------------------------------------------------------------- row Top-k
+// The Top-k operator on its own (msa_block_topk): the k best columns of each
+// row of an fp32 score matrix, one wave per row.  The row is streamed once
+// (VEC: four columns per lane and load, kRowAhead wave loads in flight) and
+// its keys pushed through a KeyBatch against the running k-th best.
+constexpr int kRowWaves = 4;
+constexpr int kRowAhead = 4;
+
+template <bool VEC>
+__global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float* __restrict__ scores,
+                                                                     int64_t n_rows, int n_cols, int64_t ld, int k,
+                                                                     int32_t* __restrict__ ids) {
+  __shared__ uint64_t s_pend[kRowWaves][2 * kWave];
+  const int lane = lane_id();
+  const int w = threadIdx.x / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kRowWaves + w;
+  if (row >= n_rows) return;
+  const float* srow = scores + row * ld;
+  KeyBatch kb;
+  kb.pend = s_pend[w];
+  kb.K1 = k;
+  kb.list = 0;
+  kb.cnt = 0;
+  uint64_t tau = 0;
+  if constexpr (VEC) {
+    // wave load i covers columns 256 i .. 256 i + 255; lane l holds 4l .. 4l + 3
+    // (rows are 16-byte aligned and ld % 4 == 0, so a load that starts below
+    // n_cols stays inside the row's ld columns)
+    const int nload = (n_cols + 4 * kWave - 1) / (4 * kWave);
+    auto load = [&](int i) -> f32x4 {
+      const int c0 = 4 * kWave * i + 4 * lane;
+      return c0 < n_cols ? *reinterpret_cast<const f32x4*>(srow + c0) : f32x4{};
+    };
+    f32x4 pf[kRowAhead];
+#pragma unroll
+    for (int a = 0; a < kRowAhead; ++a) pf[a] = load(a);
+    for (int i0 = 0; i0 < nload; i0 += kRowAhead) {
+#pragma unroll
+      for (int a = 0; a < kRowAhead; ++a) {
+        const f32x4 x = pf[a];
+        pf[a] = load(i0 + a + kRowAhead);
+        const int c0 = 4 * kWave * (i0 + a) + 4 * lane;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const uint64_t v = c0 + e < n_cols ? rank_key(x[e], static_cast<uint32_t>(c0 + e)) : 0ull;
+          tau = kb.push(v, tau);
+        }
+      }
+    }
+  } else {
+    stream_chunks([=](int b) { return srow[b]; }, n_cols, 0, 1, [&](uint64_t v, uint64_t t) { return kb.push(v, t); });
+  }
+  kb.flush();
+  const int cnt = __popcll(__ballot(lane < k && kb.list != 0ull));
+  uint32_t id = lane < cnt ? key_block(kb.list) : 0xFFFFFFFFu;
+  id = wave_sort_asc_u32(id);
+  if (lane < k) ids[row * k + lane] = lane < cnt ? static_cast<int32_t>(id) : -1;
 }
 
 // ---------------------------------------------------------------- host side
@@ -964,6 +1176,7 @@ int index_topk_run(const IndexPlan& pl, const void* index_q, const void* index_k
     const int rpu = static_cast<int>(std::min<int64_t>(static_cast<int64_t>(pl.U) * pl.qr, seqs->max_q_rows)) *
                     num_kv_heads;
     const int64_t rows = (u1 - u0) * rpu;
+    if (rows >= (int64_t(1) << 32)) return MSA_ERR_UNSUPPORTED;      // tasks are 32-bit in the kernels
     if (rows <= kSplitTopkRows)
       msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(64 * kSplitWaves), 0, stream, M,
                          static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
@@ -991,6 +1204,25 @@ extern "C" int msa_index_topk(const void* index_q, const void* index_k, const ms
   if (workspace_bytes < pl.hdr_bytes + pl.unit_bytes) return MSA_ERR_WORKSPACE;
   return index_topk_run(pl, index_q, index_k, seqs, num_kv_heads, d_idx, block_size, topk, block_ids, workspace,
                         workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------- row Top-k (host)
+extern "C" int msa_block_topk(const float* scores, int64_t n_rows, int n_cols, int64_t ld, int k, int32_t* ids,
+                              hipStream_t stream) {
+  if (n_rows < 0 || n_cols < 0 || ld < n_cols || k < 1) return MSA_ERR_INVALID;
+  if (k > kWave || n_cols > (1 << 30)) return MSA_ERR_UNSUPPORTED;
+  if (n_rows == 0) return MSA_OK;
+  if (!ids || (n_cols > 0 && !scores)) return MSA_ERR_INVALID;
+  const int64_t grid = (n_rows + kRowWaves - 1) / kRowWaves;
+  if (grid > 0x7FFFFFFF) return MSA_ERR_UNSUPPORTED;
+  const bool vec = reinterpret_cast<uintptr_t>(scores) % 16 == 0 && ld % 4 == 0;
+  if (vec)
+    msa_prof::launch("row_topk_kernel", row_topk_kernel<true>, dim3(static_cast<unsigned>(grid)),
+                     dim3(kRowWaves * kWave), 0, stream, scores, n_rows, n_cols, ld, k, ids);
+  else
+    msa_prof::launch("row_topk_kernel", row_topk_kernel<false>, dim3(static_cast<unsigned>(grid)),
+                     dim3(kRowWaves * kWave), 0, stream, scores, n_rows, n_cols, ld, k, ids);
+  return msa_host::launch_status();
 }
 
 // ---------------------------------------------------------------- no-allocation entry point

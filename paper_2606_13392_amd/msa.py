@@ -21,7 +21,7 @@ MSA_OK, MSA_ERR_INVALID, MSA_ERR_UNSUPPORTED, MSA_ERR_WORKSPACE, MSA_ERR_HIP = 0
 
 EXPORTS = [
     "msa_strerror",
-    "msa_index_topk_workspace_size", "msa_index_topk", "msa_index_topk_noalloc",
+    "msa_index_topk_workspace_size", "msa_index_topk", "msa_index_topk_noalloc", "msa_block_topk",
     "msa_sparse_attn_prefill_workspace_size", "msa_sparse_attn_prefill",
     "msa_sparse_attn_decode_workspace_size", "msa_sparse_attn_decode",
     "msa_sparse_attn_prefill_fp8", "msa_sparse_attn_decode_fp8",
@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
         L.msa_index_topk.restype = I
         L.msa_index_topk_noalloc.argtypes = [P, P, S, I, I, I, I, P, P]
         L.msa_index_topk_noalloc.restype = I
+        L.msa_block_topk.argtypes = [P, ctypes.c_int64, I, ctypes.c_int64, I, P, P]
+        L.msa_block_topk.restype = I
         for name in ("prefill", "decode"):
             ws = getattr(L, f"msa_sparse_attn_{name}_workspace_size")
             ws.argtypes = [S, I, I, I, I, I]
@@ -213,6 +215,27 @@ def index_topk_noalloc(index_q: torch.Tensor, index_k: torch.Tensor, seqs: Seqs,
     st = lib().msa_index_topk_noalloc(_ptr(index_q), _ptr(index_k), seqs.ref(), H_kv, d_idx, block_size, topk,
                                       _ptr(out), _stream())
     _check(st, "msa_index_topk_noalloc")
+    return out
+
+
+def block_topk(scores: torch.Tensor, k: int, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """msa_block_topk: the k best columns of each row of an fp32 [n_rows, n_cols]
+    matrix (row stride taken from the tensor; unit column stride), int32
+    [n_rows, k], ascending, -1 padded."""
+    if scores.dim() != 2:
+        raise ValueError("scores: expected a 2-d tensor")
+    if scores.dtype != torch.float32:
+        raise TypeError(f"scores: expected torch.float32, got {scores.dtype}")
+    n_rows, n_cols = scores.shape
+    if n_cols > 1 and scores.stride(1) != 1:
+        raise ValueError("scores: columns must be contiguous")
+    ld = scores.stride(0) if n_rows > 1 else max(n_cols, 1)
+    dev = scores.device
+    if out is None:
+        out = torch.empty((n_rows, k), dtype=torch.int32, device=dev)
+    _need(out, "ids", torch.int32, (n_rows, k), dev)
+    st = lib().msa_block_topk(_ptr(scores), n_rows, n_cols, ld, k, _ptr(out), _stream())
+    _check(st, "msa_block_topk")
     return out
 
 

@@ -422,3 +422,32 @@ def random_block_ids(p: Problem, pad_slots: int = 0) -> np.ndarray:
             sel = np.sort(np.concatenate([others, [lb]]))
             ids[row, g, :sel.shape[0]] = sel
     return ids
+
+
+# --------------------------------------------------------------------------
+# score matrices for the Top-k operator on its own
+# --------------------------------------------------------------------------
+# (N, B, k) of the paper's Top-k latency table (Sec. 4.1): N rows of B block
+# scores each, k kept per row.  The paper does not state its score values;
+# rows of i.i.d. N(0, 1) floats stand in (for i.i.d. continuous scores the
+# rank pattern of a row, which is all a comparison-based Top-k sees, does not
+# depend on the distribution).
+TOPK_SHAPES = [(131072, 1024, 16), (131072, 2048, 32), (524288, 4096, 16), (524288, 8192, 32)]
+TID_TOPK = 9
+
+
+def topk_scores(n_rows: int, n_cols: int, seed: int, device, ld: Optional[int] = None,
+                pool: Optional[List[float]] = None):
+    """fp32 [n_rows, n_cols] score matrix: i.i.d. N(0, 1), or drawn uniformly
+    from ``pool`` (to force ties, signed zeros, -inf).  With ``ld`` > n_cols
+    it is a view of the first n_cols columns of an [n_rows, ld] matrix."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed) * 1000003 + TID_TOPK)
+    width = n_cols if ld is None else int(ld)
+    if pool is None:
+        full = torch.randn((n_rows, width), generator=g, device=device, dtype=torch.float32)
+    else:
+        vals = torch.tensor(pool, dtype=torch.float32, device=device)
+        full = vals[torch.randint(0, len(pool), (n_rows, width), generator=g, device=device)]
+    return full[:, :n_cols]

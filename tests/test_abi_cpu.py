@@ -214,3 +214,16 @@ def test_noalloc_rejects_problems_beyond_its_scratch():
     assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 3, 64, 64, 8, 8, None) == msa.MSA_ERR_UNSUPPORTED
     assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 2, 64, 64, 8, None, None) == msa.MSA_ERR_INVALID
     assert L.msa_index_topk_noalloc(8, 8, ctypes.byref(s), 2, 64, 64, 0, 8, None) == msa.MSA_ERR_INVALID
+
+
+def test_block_topk_rejects_on_the_host():
+    L = msa.lib()
+    assert L.msa_block_topk(8, 0, 100, 100, 16, 8, None) == msa.MSA_OK          # no rows: nothing to do
+    assert L.msa_block_topk(8, 4, 100, 100, 0, 8, None) == msa.MSA_ERR_INVALID  # k < 1
+    assert L.msa_block_topk(8, 4, 100, 100, 65, 8, None) == msa.MSA_ERR_UNSUPPORTED
+    assert L.msa_block_topk(8, 4, 100, 99, 16, 8, None) == msa.MSA_ERR_INVALID  # ld < n_cols
+    assert L.msa_block_topk(8, -1, 100, 100, 16, 8, None) == msa.MSA_ERR_INVALID
+    assert L.msa_block_topk(8, 4, -1, 100, 16, 8, None) == msa.MSA_ERR_INVALID
+    assert L.msa_block_topk(8, 4, 100, 100, 16, None, None) == msa.MSA_ERR_INVALID
+    assert L.msa_block_topk(None, 4, 100, 100, 16, 8, None) == msa.MSA_ERR_INVALID
+    assert L.msa_block_topk(8, 4, (1 << 30) + 1, 1 << 31, 16, 8, None) == msa.MSA_ERR_UNSUPPORTED

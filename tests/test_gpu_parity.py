@@ -429,3 +429,47 @@ def test_workload_prefill_1m_bk128_sampled():
 
 def test_workload_decode_128k_bk128():
     _sampled_workload("decode_128k_bk128", 64, gen="torch")
+
+
+# Exact score ties: the key blocks of the index repeat a few patterns (each
+# row sees every block maximum many times over), or the index queries are
+# zero (every score ties).  Equal scores keep the lower block id on both
+# sides, so the ids must equal the oracle's exactly.  The cases reach every
+# selection path of the Top-k: rows with at most k-1 candidates, rows ranked
+# on their scores directly, rows pruned by piece maxima with a tie at the
+# boundary, and rows whose tied candidates overflow the radix buffer (ranked
+# by the pruned scan instead).
+TIE_CASES = [
+    # name, T, H_kv, topk, repeat period of the key blocks (0: zero index queries)
+    ("ties_period5_k8", 16384, 2, 8, 5),
+    ("ties_period40_k16", 30000, 2, 16, 40),
+    ("ties_period3_k64", 80000, 1, 64, 3),
+    ("ties_all_equal_k16", 20000, 2, 16, 0),
+]
+
+
+@pytest.mark.parametrize("case", TIE_CASES, ids=[c[0] for c in TIE_CASES])
+def test_index_exact_ties(case):
+    name, T, H_kv, topk, period = case
+    _say(f"[ties] {name}")
+    p = synth.packed_problem(name, [T], [T], num_q_heads=2 * H_kv, num_kv_heads=H_kv, d_idx=64, block_size=64,
+                             topk=topk, seed=zlib.crc32(name.encode()) % 10000)
+    x = synth.generate_numpy(p)
+    iq, ik = x["index_q"].copy(), x["index_k"].copy()
+    B = p.block_size
+    if period:
+        for b in range(period, T // B):
+            ik[b * B:(b + 1) * B] = ik[(b % period) * B:(b % period + 1) * B]
+    else:
+        iq[:] = 0
+    lay = O.layout_of(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    ids = msa.index_topk(to_dev(iq), to_dev(ik), seqs, B, topk)
+    torch.cuda.synchronize()
+    rows = synth.stratified_rows(p, 160, seed=3)
+    ids_ora, _ = O.select_blocks(iq, ik, lay, B, topk, rows=rows)
+    got = ids.cpu().numpy()[rows]
+    bad = [(r, g) for i, r in enumerate(rows) for g in range(H_kv) if not np.array_equal(got[i, g], ids_ora[i, g])]
+    _say(f"  {len(rows)} rows x {H_kv} groups, {len(bad)} differ")
+    assert not bad, f"first differing (row, group) {bad[0]}: {got[rows.index(bad[0][0]), bad[0][1]]} vs oracle"
