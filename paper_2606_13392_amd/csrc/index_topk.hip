@@ -733,6 +733,46 @@ __device__ __forceinline__ int lanes_below(uint64_t m) {
   return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(m >> 32), __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0));
 }
 
+// The K best of the cnt (<= 2 kWave) distinct non-zero keys in the wave's
+// LDS buffer `buf`: the K-th largest key kk is found by a radix search on the
+// score half, and on the id half among equal scores at the boundary; the keys
+// >= kk (all of them when cnt <= K) are compacted to the front of `buf` and
+// returned one per lane in lanes 0 .. min(cnt, K)-1 (in no order; other
+// lanes 0).  With `kth` non-null, *kth receives kk (0 when cnt <= K).
+__device__ __forceinline__ uint64_t best_keys(uint64_t* buf, int cnt, int K, uint64_t* kth) {
+  const int lane = lane_id();
+  const uint64_t c0 = lane < cnt ? buf[lane] : 0ull;
+  const uint64_t c1 = kWave + lane < cnt ? buf[kWave + lane] : 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  uint64_t kk = 0;
+  if (cnt > K) {
+    uint32_t h[2] = {static_cast<uint32_t>(c0 >> 32), static_cast<uint32_t>(c1 >> 32)};
+    const uint32_t tv = kth_largest_u32<2>(h, K);
+    const int n_gt = __popcll(__ballot(h[0] > tv)) + __popcll(__ballot(h[1] > tv));
+    const int n_eq = __popcll(__ballot(h[0] == tv && c0 != 0ull)) + __popcll(__ballot(h[1] == tv && c1 != 0ull));
+    const int need = K - n_gt;                              // 1 <= need <= n_eq
+    kk = static_cast<uint64_t>(tv) << 32;
+    if (n_eq != need) {
+      uint32_t l[2] = {h[0] == tv && c0 != 0ull ? static_cast<uint32_t>(c0) : 0u,
+                       h[1] == tv && c1 != 0ull ? static_cast<uint32_t>(c1) : 0u};
+      kk |= kth_largest_u32<2>(l, need);
+    }
+  }
+  if (kth) *kth = kk;
+  const bool s0 = c0 != 0ull && c0 >= kk, s1 = c1 != 0ull && c1 >= kk;
+  const uint64_t m0 = __ballot(s0), m1 = __ballot(s1);
+  if (s0) buf[lanes_below(m0)] = c0;
+  if (s1) buf[__popcll(m0) + lanes_below(m1)] = c1;
+  const int nsel = __popcll(m0) + __popcll(m1);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  const uint64_t list = lane < nsel && lane < K ? buf[lane] : 0ull;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  return list;
+}
+
 // Exact selection of a row through radix searches instead of sorting
 // networks.  A bound t1 <= the row's K1-th best score -- the K1-th largest
 // piece maximum (K1 distinct pieces each hold a score >= it), or for rows of
@@ -821,29 +861,7 @@ __device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow,
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   if (cnt > kBuf || cnt < K1) return false;
-  const uint64_t c0 = lane < cnt ? buf[lane] : 0ull;
-  const uint64_t c1 = kWave + lane < cnt ? buf[kWave + lane] : 0ull;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  uint32_t h[2] = {static_cast<uint32_t>(c0 >> 32), static_cast<uint32_t>(c1 >> 32)};
-  const uint32_t tv = kth_largest_u32<2>(h, K1);         // >= t1 > 0, so absent entries never match
-  const int n_gt = __popcll(__ballot(h[0] > tv)) + __popcll(__ballot(h[1] > tv));
-  const int n_eq = __popcll(__ballot(h[0] == tv)) + __popcll(__ballot(h[1] == tv));
-  const int need = K1 - n_gt;                             // 1 <= need <= n_eq
-  uint64_t kk = static_cast<uint64_t>(tv) << 32;
-  if (n_eq != need) {
-    uint32_t l[2] = {h[0] == tv ? static_cast<uint32_t>(c0) : 0u, h[1] == tv ? static_cast<uint32_t>(c1) : 0u};
-    kk |= kth_largest_u32<2>(l, need);
-  }
-  const bool s0 = c0 >= kk && c0 != 0ull, s1 = c1 >= kk && c1 != 0ull;
-  const uint64_t m0 = __ballot(s0), m1 = __ballot(s1);
-  if (s0) buf[lanes_below(m0)] = c0;
-  if (s1) buf[__popcll(m0) + lanes_below(m1)] = c1;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  list = lane < K1 ? buf[lane] : 0ull;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  list = best_keys(buf, cnt, K1, nullptr);
   return true;
 }
 
@@ -977,61 +995,100 @@ __global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
 
 // ---------------------------------------------------------------- row Top-k
 // The Top-k operator on its own (msa_block_topk): the k best columns of each
-// row of an fp32 score matrix, one wave per row.  The row is streamed once
-// (VEC: four columns per lane and load, kRowAhead wave loads in flight) and
-// its keys pushed through a KeyBatch against the running k-th best.
+// row of an fp32 score matrix, one wave per row.  The row is read in rounds
+// of kRowPer values per lane (VEC: float4 loads).  A round's bound is the k-th
+// largest of the lanes' maxima (k distinct lanes hold a score at least that
+// large), raised to the running bound; the round's scores at or above it are
+// appended as keys to the wave's LDS buffer.  A buffer more than half full is
+// cut to its k best, whose k-th key raises the bound.  The k best keys of the
+// buffer are the row's.  A row whose candidates still overflow the buffer
+// (many equal scores) is streamed again through a key batch.
 constexpr int kRowWaves = 4;
+constexpr int kRowPer = 32;
 constexpr int kRowAhead = 4;
 
 template <bool VEC>
 __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float* __restrict__ scores,
                                                                      int64_t n_rows, int n_cols, int64_t ld, int k,
                                                                      int32_t* __restrict__ ids) {
-  __shared__ uint64_t s_pend[kRowWaves][2 * kWave];
+  __shared__ uint64_t s_buf[kRowWaves][2 * kWave];
   const int lane = lane_id();
-  const int w = threadIdx.x / kWave;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x) / kWave;
   const int64_t row = static_cast<int64_t>(blockIdx.x) * kRowWaves + w;
   if (row >= n_rows) return;
   const float* srow = scores + row * ld;
-  KeyBatch kb;
-  kb.pend = s_pend[w];
-  kb.K1 = k;
-  kb.list = 0;
-  kb.cnt = 0;
-  uint64_t tau = 0;
-  if constexpr (VEC) {
-    // wave load i covers columns 256 i .. 256 i + 255; lane l holds 4l .. 4l + 3
-    // (rows are 16-byte aligned and ld % 4 == 0, so a load that starts below
-    // n_cols stays inside the row's ld columns)
-    const int nload = (n_cols + 4 * kWave - 1) / (4 * kWave);
-    auto load = [&](int i) -> f32x4 {
-      const int c0 = 4 * kWave * i + 4 * lane;
-      return c0 < n_cols ? *reinterpret_cast<const f32x4*>(srow + c0) : f32x4{};
-    };
-    f32x4 pf[kRowAhead];
+  uint64_t* buf = s_buf[w];
+  constexpr int kBuf = 2 * kWave;
+  uint32_t t = 0;                  // ordered bound: the row's k-th best score is >= it
+  int cnt = 0;
+  bool fits = true;
+  for (int c0 = 0; c0 < n_cols; c0 += kWave * kRowPer) {
+    // column of value v of this lane: VEC c0 + 256 (v / 4) + 4 lane + v % 4, else c0 + 64 v + lane
+    auto col_of = [&](int v) { return VEC ? c0 + 4 * kWave * (v / 4) + 4 * lane + v % 4 : c0 + kWave * v + lane; };
+    float x[kRowPer];
+    if constexpr (VEC) {
+      // rows are 16-byte aligned and ld % 4 == 0: a load that starts below
+      // n_cols stays inside the row's ld columns
 #pragma unroll
-    for (int a = 0; a < kRowAhead; ++a) pf[a] = load(a);
-    for (int i0 = 0; i0 < nload; i0 += kRowAhead) {
+      for (int i = 0; i < kRowPer / 4; ++i) {
+        const int c = col_of(4 * i);
+        const f32x4 q = c < n_cols ? *reinterpret_cast<const f32x4*>(srow + c) : f32x4{};
 #pragma unroll
-      for (int a = 0; a < kRowAhead; ++a) {
-        const f32x4 x = pf[a];
-        pf[a] = load(i0 + a + kRowAhead);
-        const int c0 = 4 * kWave * (i0 + a) + 4 * lane;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const uint64_t v = c0 + e < n_cols ? rank_key(x[e], static_cast<uint32_t>(c0 + e)) : 0ull;
-          tau = kb.push(v, tau);
-        }
+        for (int e = 0; e < 4; ++e) x[4 * i + e] = q[e];
       }
+    } else {
+#pragma unroll
+      for (int v = 0; v < kRowPer; ++v) x[v] = col_of(v) < n_cols ? srow[col_of(v)] : 0.f;
     }
-  } else {
-    stream_chunks([=](int b) { return srow[b]; }, n_cols, 0, 1, [&](uint64_t v, uint64_t t) { return kb.push(v, t); });
+    uint32_t lm = 0;
+#pragma unroll
+    for (int v = 0; v < kRowPer; ++v) {
+      const uint32_t o = col_of(v) < n_cols ? ordered_u32(x[v]) : 0u;
+      lm = o > lm ? o : lm;
+    }
+    const uint32_t tr = kth_largest_u32<1>(&lm, k);
+    t = tr > t ? tr : t;
+#pragma unroll
+    for (int v = 0; v < kRowPer; ++v) {
+      const int c = col_of(v);
+      const bool take = c < n_cols && ordered_u32(x[v]) >= t;
+      const uint64_t m = __ballot(take);
+      if (m == 0) continue;
+      const int pos = cnt + lanes_below(m);
+      if (take && pos < kBuf) buf[pos] = rank_key(x[v], static_cast<uint32_t>(c));
+      cnt += __popcll(m);
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (cnt > kBuf) {
+      fits = false;
+      break;
+    }
+    if (cnt > kBuf / 2 && cnt > k) {
+      uint64_t kk;
+      best_keys(buf, cnt, k, &kk);
+      cnt = k;
+      const uint32_t tk = static_cast<uint32_t>(kk >> 32);
+      t = tk > t ? tk : t;
+    }
   }
-  kb.flush();
-  const int cnt = __popcll(__ballot(lane < k && kb.list != 0ull));
-  uint32_t id = lane < cnt ? key_block(kb.list) : 0xFFFFFFFFu;
+  uint64_t list;
+  if (fits) {
+    list = best_keys(buf, cnt, k, nullptr);
+  } else {
+    KeyBatch kb;
+    kb.pend = buf;
+    kb.K1 = k;
+    kb.list = 0;
+    kb.cnt = 0;
+    stream_chunks([=](int b) { return srow[b]; }, n_cols, 0, 1, [&](uint64_t v, uint64_t th) { return kb.push(v, th); });
+    kb.flush();
+    list = kb.list;
+  }
+  const int nsel = __popcll(__ballot(lane < k && list != 0ull));
+  uint32_t id = lane < nsel ? key_block(list) : 0xFFFFFFFFu;
   id = wave_sort_asc_u32(id);
-  if (lane < k) ids[row * k + lane] = lane < cnt ? static_cast<int32_t>(id) : -1;
+  if (lane < k) ids[row * k + lane] = lane < nsel ? static_cast<int32_t>(id) : -1;
 }
 
 // ---------------------------------------------------------------- host side
