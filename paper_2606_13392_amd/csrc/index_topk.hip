@@ -996,7 +996,8 @@ __global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
 // ---------------------------------------------------------------- row Top-k
 // The Top-k operator on its own (msa_block_topk): the k best columns of each
 // row of an fp32 score matrix, one wave per row.  The row is read in rounds
-// of kRowPer values per lane (VEC: float4 loads).  A round's bound is the k-th
+// of RP values per lane (16 for rows of at most 1024 columns, else 32; VEC:
+// float4 loads).  A round's bound is the k-th
 // largest of the lanes' maxima (k distinct lanes hold a score at least that
 // large), raised to the running bound; the round's scores at or above it are
 // appended as keys to the wave's LDS buffer.  A buffer more than half full is
@@ -1004,10 +1005,9 @@ __global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
 // buffer are the row's.  A row whose candidates still overflow the buffer
 // (many equal scores) is streamed again through a key batch.
 constexpr int kRowWaves = 4;
-constexpr int kRowPer = 32;
 constexpr int kRowAhead = 4;
 
-template <bool VEC>
+template <bool VEC, int RP>
 __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float* __restrict__ scores,
                                                                      int64_t n_rows, int n_cols, int64_t ld, int k,
                                                                      int32_t* __restrict__ ids) {
@@ -1022,15 +1022,15 @@ __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float
   uint32_t t = 0;                  // ordered bound: the row's k-th best score is >= it
   int cnt = 0;
   bool fits = true;
-  for (int c0 = 0; c0 < n_cols; c0 += kWave * kRowPer) {
+  for (int c0 = 0; c0 < n_cols; c0 += kWave * RP) {
     // column of value v of this lane: VEC c0 + 256 (v / 4) + 4 lane + v % 4, else c0 + 64 v + lane
     auto col_of = [&](int v) { return VEC ? c0 + 4 * kWave * (v / 4) + 4 * lane + v % 4 : c0 + kWave * v + lane; };
-    float x[kRowPer];
+    float x[RP];
     if constexpr (VEC) {
       // rows are 16-byte aligned and ld % 4 == 0: a load that starts below
       // n_cols stays inside the row's ld columns
 #pragma unroll
-      for (int i = 0; i < kRowPer / 4; ++i) {
+      for (int i = 0; i < RP / 4; ++i) {
         const int c = col_of(4 * i);
         const f32x4 q = c < n_cols ? *reinterpret_cast<const f32x4*>(srow + c) : f32x4{};
 #pragma unroll
@@ -1038,18 +1038,18 @@ __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float
       }
     } else {
 #pragma unroll
-      for (int v = 0; v < kRowPer; ++v) x[v] = col_of(v) < n_cols ? srow[col_of(v)] : 0.f;
+      for (int v = 0; v < RP; ++v) x[v] = col_of(v) < n_cols ? srow[col_of(v)] : 0.f;
     }
     uint32_t lm = 0;
 #pragma unroll
-    for (int v = 0; v < kRowPer; ++v) {
+    for (int v = 0; v < RP; ++v) {
       const uint32_t o = col_of(v) < n_cols ? ordered_u32(x[v]) : 0u;
       lm = o > lm ? o : lm;
     }
     const uint32_t tr = kth_largest_u32<1>(&lm, k);
     t = tr > t ? tr : t;
 #pragma unroll
-    for (int v = 0; v < kRowPer; ++v) {
+    for (int v = 0; v < RP; ++v) {
       const int c = col_of(v);
       const bool take = c < n_cols && ordered_u32(x[v]) >= t;
       const uint64_t m = __ballot(take);
@@ -1273,12 +1273,17 @@ extern "C" int msa_block_topk(const float* scores, int64_t n_rows, int n_cols, i
   const int64_t grid = (n_rows + kRowWaves - 1) / kRowWaves;
   if (grid > 0x7FFFFFFF) return MSA_ERR_UNSUPPORTED;
   const bool vec = reinterpret_cast<uintptr_t>(scores) % 16 == 0 && ld % 4 == 0;
+  auto launch_row_topk = [&](auto k16, auto k32) {
+    const dim3 g(static_cast<unsigned>(grid)), b(kRowWaves * kWave);
+    if (n_cols <= 16 * kWave)
+      msa_prof::launch("row_topk_kernel", k16, g, b, 0, stream, scores, n_rows, n_cols, ld, k, ids);
+    else
+      msa_prof::launch("row_topk_kernel", k32, g, b, 0, stream, scores, n_rows, n_cols, ld, k, ids);
+  };
   if (vec)
-    msa_prof::launch("row_topk_kernel", row_topk_kernel<true>, dim3(static_cast<unsigned>(grid)),
-                     dim3(kRowWaves * kWave), 0, stream, scores, n_rows, n_cols, ld, k, ids);
+    launch_row_topk(row_topk_kernel<true, 16>, row_topk_kernel<true, 32>);
   else
-    msa_prof::launch("row_topk_kernel", row_topk_kernel<false>, dim3(static_cast<unsigned>(grid)),
-                     dim3(kRowWaves * kWave), 0, stream, scores, n_rows, n_cols, ld, k, ids);
+    launch_row_topk(row_topk_kernel<false, 16>, row_topk_kernel<false, 32>);
   return msa_host::launch_status();
 }
 
