@@ -240,3 +240,51 @@ def test_backward_workload_sampled():
     assert ratio < 1e-2
     del d, o, lse, dq, dk, dv, ids
     torch.cuda.empty_cache()
+
+
+def test_backward_tile_wider_than_the_rank_bitmap():
+    """One tile whose handles span more rows than the ordering kernel's LDS
+    row bitmap covers (2^20): every row of a 1.2M-row sequence (one head, one
+    group, k 2) selects block 0 besides its local block, so block 0's tile
+    holds 1.2M handles over rows 0 .. 1.2M-1 and is put in canonical order by
+    the merge fallback.  dK / dV must be equal bit for bit over three runs,
+    dQ of sampled rows must match the oracle, and over all keys
+    sum_j dV_j = sum_i dO_i and sum_j dK_j = 0 (every handle counted once)."""
+    T, B = 1_200_000, 64
+    p = synth.packed_problem("bwd_wide_tile", [T], [T], num_q_heads=1, num_kv_heads=1, topk=2, seed=77)
+    _say("[case] bwd_wide_tile (1.2M rows, tile of block 0 spans every row)")
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = synth.generate_torch(p, dev, tensors=("q", "k", "v", "d_o"))
+    lb = torch.arange(T, device=dev, dtype=torch.int32) // B
+    ids = torch.stack([torch.zeros_like(lb), torch.where(lb > 0, lb, torch.full_like(lb, -1))], dim=1)
+    ids = ids.view(T, 1, 2).contiguous()
+    o, lse = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, B)
+    runs = []
+    for _ in range(3):
+        runs.append(msa.sparse_attn_backward(d["q"], d["k"], d["v"], o, lse, d["d_o"], ids, seqs, B))
+        torch.cuda.synchronize()
+    for t in range(3):
+        a = runs[0][t].view(torch.int16)
+        assert all(torch.equal(a, r[t].view(torch.int16)) for r in runs[1:]), f"output {t} differs between runs"
+    dq, dk, dv = runs[0]
+    # dQ of sampled rows against the oracle
+    lay = O.layout_of(p)
+    ids_h = ids.cpu().numpy()
+    scale = 1.0 / math.sqrt(p.head_dim)
+    rows = [0, 63, 64, 1000, 524288, 1048575, 1048576, T - 1]
+    dq_ref = np.zeros((len(rows), 1, p.head_dim))
+    for i, r in enumerate(rows):
+        s, pos = lay.locate(r)
+        toks = O.selected_tokens(ids_h[r, 0], pos, B)
+        tt = torch.from_numpy(toks).to(dev)
+        dq_ref[i] = O.attend_backward(O.decode_bf16(from_dev_bits(d["q"][r])), O.decode_bf16(from_dev_bits(d["k"][tt, 0])),
+                                      O.decode_bf16(from_dev_bits(d["v"][tt, 0])),
+                                      O.decode_bf16(from_dev_bits(d["d_o"][r])), scale)[0]
+    rows_t = torch.tensor(rows, dtype=torch.int64, device=dev)
+    stats = check_grad(dq[rows_t].float().cpu().numpy(), dq_ref, "dQ sampled rows")
+    _say(f"  dQ ({len(rows)} rows) max-err/max|ref| {stats[0]:.2e} rel-L2 {stats[1]:.2e}")
+    rel = float((dv.double().sum(dim=0) - d["d_o"].double().sum(dim=0)).norm() / d["d_o"].double().sum(dim=0).norm())
+    ratio = float(dk.double().sum(dim=0).norm() / dk.double().abs().sum(dim=0).norm())
+    _say(f"  sum dV vs sum dO rel {rel:.2e}; |sum dK| / |sum |dK|| {ratio:.2e}")
+    assert rel < 1e-2 and ratio < 1e-2
