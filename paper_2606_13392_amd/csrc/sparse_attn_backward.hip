@@ -21,7 +21,8 @@
 //     reverse index  (kvo_index.h)
 //     bwd_kvo        persistent CTAs of B_k / 16 waves (two CTAs per CU at
 //                    B_k 64, one at 128) over the work items (<= 256 queries
-//                    of one tile).  K and V of the block sit in LDS row-major.
+//                    of one tile).  K and V of the block sit in LDS row-major
+//                    (K's 16-byte segments permuted per row).
 //                    A pass takes 32 gathered (query, head) rows, whose Q and
 //                    dO rows are copied from HBM straight into LDS (DMA) one
 //                    pass ahead; wave kq owns keys 16kq .. 16kq+15: S = Q K^T
@@ -53,8 +54,7 @@ constexpr int bwd_part_floats() { return 2 * BK * kHeadDim; }   // dK and dV of 
 
 template <int BK>
 struct BwdSmem {
-  uint16_t k[BK][kHeadDim + 16];                      // K block, row-major (+32 B: transposing reads of 4 rows
-                                                      // x 32 B hit distinct banks)
+  uint16_t k[BK][kHeadDim];                           // K block, 256-byte rows, segments swizzled (bwd_swz)
   uint16_t v[BK][kHeadDim + 8];                       // V block, row-major
   // Q and dO rows of a pass (double-buffered), row-major with 16-byte
   // segments XOR-swizzled by row (bwd_qrow_off); filled by DMA
@@ -72,12 +72,17 @@ struct BwdSmem {
 static_assert(sizeof(BwdSmem<64>) <= 80 * 1024, "LDS of a B_k 64 backward CTA");
 static_assert(sizeof(BwdSmem<128>) <= 160 * 1024, "LDS of a B_k 128 backward CTA");
 
-// Byte offset of element (row, col) in a pass buffer: 256-byte rows whose
-// 16-byte segments are XOR-swizzled by the row's low 4 bits, so that the
-// 16-byte operand reads of 16 rows and the transposing reads of 4 rows both
-// spread over the banks.
+// 256-byte rows (a pass buffer's Q / dO rows, the K block) keep their 16-byte
+// segment s in slot s ^ bwd_swz(row).  The permutation moves segment pairs
+// (2p, 2p + 1) as pairs, by (row & 7), and flips the low bit by bit 3 of the
+// row, so that both read shapes are free of bank conflicts: 16-byte operand
+// reads of 16 consecutive rows at one segment (16 distinct slots), and
+// transposing reads of 4 consecutive rows x 16 columns (one segment pair per
+// row, the four pairs distinct).
+__device__ __forceinline__ int bwd_swz(int row) { return ((row & 7) << 1) | ((row >> 3) & 1); }
+// Byte offset of element (row, col) in such a buffer.
 __device__ __forceinline__ int bwd_qrow_off(int row, int col) {
-  return row * (kHeadDim * 2) + 16 * ((col >> 3) ^ (row & 15)) + 2 * (col & 7);
+  return row * (kHeadDim * 2) + 16 * ((col >> 3) ^ bwd_swz(row)) + 2 * (col & 7);
 }
 
 typedef short v4i16 __attribute__((ext_vector_type(4)));
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kThreads) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const bool in = key0 + key < g.kv_len;
-        *reinterpret_cast<u32x4*>(&sm.k[key][8 * dg]) =
+        *reinterpret_cast<u32x4*>(&sm.k[key][8 * (dg ^ bwd_swz(key))]) =
             in ? load_raw(kb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
         *reinterpret_cast<u32x4*>(&sm.v[key][8 * dg]) =
             in ? load_raw(vb + static_cast<int64_t>(key) * kv_stride + 8 * dg) : u32x4{};
@@ -222,7 +227,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
     };
     // Q and dO rows of the pass at cc into buffer b: wave kq issues kDma 1 KiB
     // pieces (4 rows each); lane l of a piece writes slot l % 16 of row
-    // 4 piece + l / 16, which holds the row's segment (slot ^ row) % 16
+    // 4 piece + l / 16, which holds the row's segment slot ^ bwd_swz(row)
     auto issue_dma = [&](int cc, int b) {
 #pragma unroll
       for (int i = 0; i < kDma; ++i) {
@@ -231,7 +236,7 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
         const int ra = 4 * (piece & 7) + (lane >> 4);
         bool ok;
         const int64_t hr = pass_row(cc, ra, ok);
-        const int seg = (lane & 15) ^ (ra & 15);
+        const int seg = (lane & 15) ^ bwd_swz(ra);
         const uint16_t* src = (tensor == 0 ? q : d_o) + hr * kHeadDim + 8 * seg;
         bwd_dma16(src, &sm.qdo[b][tensor][4 * (piece & 7)][0]);
       }
@@ -309,7 +314,8 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
         for (int st = 0; st < KS; ++st) {
           const int off = bwd_qrow_off(ra, 32 * st + 8 * qd);
           acc_s[t] = mfma16x16x32(*reinterpret_cast<const bf16x8*>(qb + off),
-                                  ld_bf16x8(&sm.k[16 * kq + c16][32 * st + 8 * qd]), acc_s[t]);
+                                  *reinterpret_cast<const bf16x8*>(kbytes + bwd_qrow_off(16 * kq + c16, 32 * st + 8 * qd)),
+                                  acc_s[t]);
           acc_dp[t] = mfma16x16x32(*reinterpret_cast<const bf16x8*>(dob + off),
                                    ld_bf16x8(&sm.v[16 * kq + c16][32 * st + 8 * qd]), acc_dp[t]);
         }
@@ -376,8 +382,8 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
 #pragma unroll
         for (int ks = 0; ks < BK / 32; ++ks) {
           const int krow = 32 * ks + 8 * qd + (c16 >> 2);
-          const uint2 k0v = lds_tr4(kbytes + (krow * (kHeadDim + 16) + n0 + tr_col) * 2);
-          const uint2 k1v = lds_tr4(kbytes + ((krow + 4) * (kHeadDim + 16) + n0 + tr_col) * 2);
+          const uint2 k0v = lds_tr4(kbytes + bwd_qrow_off(krow, n0 + tr_col));
+          const uint2 k1v = lds_tr4(kbytes + bwd_qrow_off(krow + 4, n0 + tr_col));
           const bf16x8 kb8 = __builtin_bit_cast(bf16x8, make_uint4(k0v.x, k0v.y, k1v.x, k1v.y));
 #pragma unroll
           for (int t = 0; t < 2; ++t)
