@@ -183,6 +183,16 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
   const int64_t kv_stride = static_cast<int64_t>(H_kv) * kHeadDim;
   int64_t staged = -1;
   const uint8_t* kbytes = reinterpret_cast<const uint8_t*>(&sm.k[0][0]);
+  // pass-invariant splits of pass rows into (query, head): G need not be a
+  // power of two, so the divisions are taken once here, not in every pass
+  int dma_rq[kDma], dma_rh[kDma];
+#pragma unroll
+  for (int i = 0; i < kDma; ++i) {
+    const int ra = 4 * ((kq * kDma + i) & 7) + (lane >> 4);
+    dma_rq[i] = ra / G;
+    dma_rh[i] = ra % G;
+  }
+  const int lane_rq = lane / G, lane_rh = lane % G;
 
   for (int32_t item = blockIdx.x; item < total_items; item = claim_next_item(next_item, &s_claim)) {
     const int64_t tile = upper_index(item_off, ntile + 1, item);
@@ -218,27 +228,34 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
 
     // pass row ra of the pass at item query cc: (query cc + ra / G, head ra % G);
     // rows past the pass's queries read a valid row (their P and dS are zero)
-    auto pass_row = [&](int cc, int ra, bool& ok) -> int64_t {
-      const int qa = cc + ra / G;
+    // (rq, rh = ra / G, ra % G, precomputed)
+    auto pass_row = [&](int cc, int ra, int rq, int rh, bool& ok) -> int64_t {
+      const int qa = cc + rq;
       ok = ra < rows_g && qa < nq;
-      const int ro = ok ? ra : 0;
       const int64_t grow = row0 + sm.s_row[ok ? qa : min(cc, nq - 1)];
-      return grow * H_q + static_cast<int64_t>(r) * G + ro % G;
+      return grow * H_q + static_cast<int64_t>(r) * G + (ok ? rh : 0);
     };
     // Q and dO rows of the pass at cc into buffer b: wave kq issues kDma 1 KiB
     // pieces (4 rows each); lane l of a piece writes slot l % 16 of row
     // 4 piece + l / 16, which holds the row's segment slot ^ bwd_swz(row)
+    // (a row past the pass's queries reads head r G + ra % G of a valid query
+    // row: any valid row serves, its P and dS are zero)
+    const uint16_t* dma_base[kDma];
+#pragma unroll
+    for (int i = 0; i < kDma; ++i) {
+      const int piece = kq * kDma + i;                // 0 .. 15: tensor piece / 8, rows 4 (piece % 8) ..
+      const int ra = 4 * (piece & 7) + (lane >> 4);
+      dma_base[i] = ((piece >> 3) == 0 ? q : d_o) + (static_cast<int64_t>(r) * G + dma_rh[i]) * kHeadDim +
+                    8 * ((lane & 15) ^ bwd_swz(ra));
+    }
+    const int64_t row_elems = static_cast<int64_t>(H_q) * kHeadDim;
     auto issue_dma = [&](int cc, int b) {
 #pragma unroll
       for (int i = 0; i < kDma; ++i) {
-        const int piece = kq * kDma + i;              // 0 .. 15: tensor piece / 8, rows 4 (piece % 8) ..
-        const int tensor = piece >> 3;
-        const int ra = 4 * (piece & 7) + (lane >> 4);
-        bool ok;
-        const int64_t hr = pass_row(cc, ra, ok);
-        const int seg = (lane & 15) ^ bwd_swz(ra);
-        const uint16_t* src = (tensor == 0 ? q : d_o) + hr * kHeadDim + 8 * seg;
-        bwd_dma16(src, &sm.qdo[b][tensor][4 * (piece & 7)][0]);
+        const int piece = kq * kDma + i;
+        const int qa = cc + dma_rq[i];
+        const int64_t grow = row0 + sm.s_row[qa < nq ? qa : min(cc, nq - 1)];
+        bwd_dma16(dma_base[i] + grow * row_elems, &sm.qdo[b][piece >> 3][4 * (piece & 7)][0]);
       }
     };
     // the pass's row scalars: lanes 0..31 of wave 0 copy LSE and D into
@@ -248,12 +265,12 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
     auto load_scalars = [&](int cc, int b) {
       if (kq == 0 && lane < kBwdPassRows) {
         bool ok;
-        const int64_t hr = pass_row(cc, lane, ok);
+        const int64_t hr = pass_row(cc, lane, lane_rq, lane_rh, ok);
         bwd_dma4(lse + hr, &sm.lse[b][0]);
         bwd_dma4(delta + hr, &sm.dlt[b][0]);
-        const int qa = cc + lane / G;
+        const int qa = cc + lane_rq;
         npos = ok ? pos_base + sm.s_row[qa] : -1;
-        noff = ok ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G + lane % G) *
+        noff = ok ? (((static_cast<int64_t>(sm.s_row[qa]) * H_kv + r) * topk + sm.s_slot[qa]) * G + lane_rh) *
                         kHeadDim
                   : dq_trash;
       }
