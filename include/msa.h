@@ -63,9 +63,11 @@
  * ... or 64 for the call's block_size; kv_lens[s] <= block_table_stride *
  * page_size.  Page ids outside [0, total_kv_rows /
  * page_size) are clamped into it (results unspecified, memory safe).  This
- * is a serving layout, not part of the paper.  msa_index_topk,
- * msa_sparse_attn_prefill/_decode and their fp8 variants accept it; the
- * other calls return MSA_ERR_UNSUPPORTED for a paged layout.
+ * is a serving layout, not part of the paper.  Every call accepts it except
+ * msa_dense_attn, which returns MSA_ERR_UNSUPPORTED for a paged layout; the
+ * training calls then write dK, dV and d index_k in the pool's rows (rows of
+ * pages no sequence lists get zero; keys in pages shared by several
+ * sequences get the sum of their gradients).
  */
 #ifndef MSA_H_
 #define MSA_H_

@@ -212,8 +212,10 @@ __global__ __launch_bounds__(bwd_threads<BK>(), BK == 64 ? 2 : 1) void bwd_kvo_k
     }
     const int pos_base = g.kv_len - g.q_rows + static_cast<int>(row0 - g.q_begin);   // + row in chunk
     if (tile != staged) {
-      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      const uint16_t* vb = v + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      // the block's first key row (contiguous, or inside its page)
+      const int64_t krow0 = key_blocks(sq, g, s, BK).row(key0 / BK);
+      const uint16_t* kb = k + krow0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const uint16_t* vb = v + krow0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;
       for (int c = threadIdx.x; c < BK * (kHeadDim / 8); c += kThreads) {
         const int key = c / (kHeadDim / 8), dg = c % (kHeadDim / 8);
         const bool in = key0 + key < g.kv_len;
@@ -487,7 +489,8 @@ __global__ __launch_bounds__(256) void bwd_tile_reduce_kernel(msa_seqs sq, const
   const int dim = 16 * (reg >> 2) + (ln & 15);
   if (key0 + key >= g.kv_len) return;
   float4* dst = reinterpret_cast<float4*>((tensor == 0 ? dv_acc : dk_acc) +
-                                          ((g.kv_start + key0 + key) * H_kv + r) * static_cast<int64_t>(kHeadDim) + dim);
+                                          ((key_blocks(sq, g, s, BK).row(key0 / BK) + key) * H_kv + r) *
+                                              static_cast<int64_t>(kHeadDim) + dim);
   float4 y = *dst;
   y.x += acc.x;
   y.y += acc.y;
@@ -647,8 +650,7 @@ int validate_bwd(const msa_seqs* seqs, int H_q, int H_kv, int head_dim, int BK, 
   if (head_dim != kHeadDim || (BK != 64 && BK != 128)) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
-  if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
-  return MSA_OK;
+  return msa_host::check_paged(seqs, BK, true);
 }
 
 template <int BK>

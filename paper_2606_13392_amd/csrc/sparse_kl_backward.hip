@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kKlThreads) void kl_lse_kernel(
       sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
     }
     if (tile != staged) {
-      const uint16_t* ikb = index_k + (g.kv_start + key0) * static_cast<int64_t>(D);
+      const uint16_t* ikb = index_k + key_blocks(sq, g, s, BK).row(key0 / BK) * static_cast<int64_t>(D);
       for (int c = threadIdx.x; c < BK * (D / 8); c += kKlThreads) {
         const int key = c / (D / 8), dg = c % (D / 8);
         *reinterpret_cast<u32x4*>(&sm.ki[key][8 * dg]) =
@@ -314,8 +314,9 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
       sm.s_slot[threadIdx.x] = static_cast<int32_t>(hd & 63u);
     }
     if (tile != staged) {
-      const uint16_t* kb = k + (g.kv_start + key0) * kv_stride + static_cast<int64_t>(r) * kHeadDim;
-      const uint16_t* ikb = index_k + (g.kv_start + key0) * static_cast<int64_t>(D);
+      const int64_t krow0 = key_blocks(sq, g, s, BK).row(key0 / BK);   // contiguous, or inside its page
+      const uint16_t* kb = k + krow0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;
+      const uint16_t* ikb = index_k + krow0 * static_cast<int64_t>(D);
       kl_stage<kHeadDim, kK2Threads>(BK, [&](int row) { return kb + min(row, nkey - 1) * kv_stride; }, sm.k);
       kl_stage<D, kK2Threads>(BK, [&](int row) { return ikb + min(row, nkey - 1) * static_cast<int64_t>(D); }, sm.ki);
       staged = tile;
@@ -614,7 +615,8 @@ __global__ __launch_bounds__(256) void kl_tile_reduce_kernel(msa_seqs sq, const 
   }
   const int key = (4 * c4) / D, dim = (4 * c4) % D;
   if (key0 + key >= g.kv_len) return;
-  float4* dst = reinterpret_cast<float4*>(dk_acc + (g.kv_start + key0 + key) * static_cast<int64_t>(D) + dim);
+  float4* dst = reinterpret_cast<float4*>(dk_acc + (key_blocks(sq, g, s, BK).row(key0 / BK) + key) *
+                                                       static_cast<int64_t>(D) + dim);
   float4 y = *dst;
   y.x += acc.x;
   y.y += acc.y;
@@ -749,8 +751,7 @@ int validate_kl(const msa_seqs* seqs, int H_q, int H_kv, int d_idx, int head_dim
   if (head_dim != kHeadDim || (BK != 64 && BK != 128) || (d_idx != 64 && d_idx != 128)) return MSA_ERR_UNSUPPORTED;
   if (topk > 64 || H_q / H_kv > 16 || !msa_host::is_pow2(H_q / H_kv) || H_kv > 64) return MSA_ERR_UNSUPPORTED;
   if (seqs->total_q_rows * H_kv >= (int64_t(1) << 31)) return MSA_ERR_UNSUPPORTED;
-  if (seqs->block_table) return MSA_ERR_UNSUPPORTED;   // contiguous key side only
-  return MSA_OK;
+  return msa_host::check_paged(seqs, BK, true);
 }
 
 // kl_grad_kernel instance for G = 2^lg (lg <= 4, checked by validate_kl).

@@ -141,8 +141,64 @@ def test_paged_rejections():
     assert L.msa_index_topk_workspace_size(pseqs.ref(), 2, 64, 64, 2) > 0
     pool3, pseqs3 = _paged_copy(p, x, dev, blocks_per_page=3)
     assert L.msa_index_topk_workspace_size(pseqs3.ref(), 2, 64, 64, 2) == 0
-    # calls that address keys as contiguous ranges reject a paged layout
+    # the dense baseline addresses keys as contiguous ranges and rejects a paged layout
     assert L.msa_dense_attn_workspace_size(pseqs.ref(), 8, 2, 128) == 0
-    assert L.msa_sparse_attn_backward_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) == 0
-    assert L.msa_sparse_kl_backward_workspace_size(pseqs.ref(), 8, 2, 64, 128, 64, 2) == 0
+    assert L.msa_sparse_attn_backward_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) > 0
+    assert L.msa_sparse_kl_backward_workspace_size(pseqs.ref(), 8, 2, 64, 128, 64, 2) > 0
+    assert L.msa_sparse_kl_backward_workspace_size(pseqs3.ref(), 8, 2, 64, 128, 64, 2) == 0
     assert L.msa_sparse_attn_prefill_workspace_size(pseqs.ref(), 8, 2, 128, 64, 2) > 0
+
+
+# name, q_rows, kv_lens, H_q, H_kv, block, topk, d_idx, blocks per page
+TRAIN_CASES = [
+    ("paged_train_chunked", [300, 1, 130], [2300, 800, 1500], 16, 2, 64, 8, 64, 1),
+    ("paged_train_4blk_pages", [700, 200], [700, 1900], 16, 4, 64, 6, 64, 4),
+    ("paged_train_bk128", [300, 129], [2300, 1500], 32, 2, 128, 5, 128, 2),
+]
+
+
+@pytest.mark.parametrize("case", TRAIN_CASES, ids=[c[0] for c in TRAIN_CASES])
+def test_paged_training_matches_contiguous(case):
+    """The training calls on a paged key side: dQ, d index_q and the KL equal
+    the contiguous layout's bit for bit, dK, dV and d index_k equal it row for
+    row through the block table, and pool rows no sequence uses stay zero."""
+    name, q_rows, kv_lens, H_q, H_kv, bk, topk, d_idx, bpp = case
+    _say(f"[case] {name}")
+    p = synth.packed_problem(name, q_rows, kv_lens, num_q_heads=H_q, num_kv_heads=H_kv, block_size=bk, topk=topk,
+                             d_idx=d_idx, seed=zlib.crc32(name.encode()) % 10000)
+    x = synth.generate_numpy(p)
+    x_do = synth.generate_grad_numpy(p)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    d = {t: to_dev(v) for t, v in x.items()}
+    d_o = to_dev(x_do)
+    pool, pseqs = _paged_copy(p, x, dev, blocks_per_page=bpp, seed=11)
+    pd = {t: to_dev(v) for t, v in pool.items()}
+    ids = msa.index_topk(d["index_q"], d["index_k"], seqs, p.block_size, p.topk)
+    o, lse = msa.sparse_attn_prefill(d["q"], d["k"], d["v"], ids, seqs, p.block_size)
+    dq, dk, dv = msa.sparse_attn_backward(d["q"], d["k"], d["v"], o, lse, d_o, ids, seqs, p.block_size)
+    pdq, pdk, pdv = msa.sparse_attn_backward(d["q"], pd["k"], pd["v"], o, lse, d_o, ids, pseqs, p.block_size)
+    diq, dik, kl = msa.sparse_kl_backward(d["index_q"], d["index_k"], d["q"], d["k"], lse, ids, seqs, p.block_size)
+    pdiq, pdik, pkl = msa.sparse_kl_backward(d["index_q"], pd["index_k"], d["q"], pd["k"], lse, ids, pseqs,
+                                             p.block_size)
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16) if t.dtype == torch.bfloat16 else t
+    assert torch.equal(bits(dq), bits(pdq)), "paged dQ differs"
+    assert torch.equal(bits(diq), bits(pdiq)) and torch.equal(kl, pkl), "paged d index_q / KL differ"
+    # key-side gradients: contiguous row kv_start + j <-> pool row of key j
+    P = p.block_size * bpp
+    table = pseqs.block_table.cpu().numpy()
+    used = np.zeros(pool["k"].shape[0], dtype=bool)
+    for s in range(p.num_seqs):
+        for j0 in range(0, p.kv_lens[s], P):
+            n = min(P, p.kv_lens[s] - j0)
+            prow = int(table[s, j0 // P]) * P
+            crow = p.kv_starts[s] + j0
+            used[prow:prow + n] = True
+            for a, b in ((dk, pdk), (dv, pdv), (dik, pdik)):
+                assert torch.equal(bits(a[crow:crow + n]), bits(b[prow:prow + n])), f"paged key gradient differs, seq {s}"
+    unused = torch.from_numpy(~used).to(dev)
+    if bool(unused.any()):
+        for t in (pdk, pdv, pdik):
+            assert float(t[unused].float().abs().max()) == 0.0, "an unused pool row has a gradient"
+    _say(f"  equal bit for bit; {int((~used).sum())} unused pool rows zero")
