@@ -133,6 +133,7 @@ def run_prefill(args, dev):
     pos3 = positions.view(-1, 1, 1)
     incidences = float(((ids >= 0) & (ids.to(torch.int64) * p.block_size <= pos3)).sum().item())
     scored_keys = float(index_scored_keys(positions, p.block_size).sum().item())
+    topk_bytes = topk_read_bytes(positions, p)
     eff_flops = 4.0 * dh * (H_q // H_kv) * float(toks.sum().item())
     idx_flops = 2.0 * p.d_idx * H_kv * scored_keys
     paper_main = 4.0 * H_q * dh * p.total_q_rows * p.topk * p.block_size
@@ -150,7 +151,7 @@ def run_prefill(args, dev):
         "paper_main_flops": paper_main,
         "kernels": {k: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps,
                         "ms_per_launch": ms / n} for k, (n, ms) in kernels.items()},
-        "models": kernel_models(p, incidences, scored_keys, eff_flops, idx_flops),
+        "models": kernel_models(p, incidences, scored_keys, eff_flops, idx_flops, topk_bytes),
         "inputs": d,
         "ids": ids,
     }
@@ -226,7 +227,18 @@ def dense_prefill_baseline(args, p, d, dev):
             "full_is": "measured" if S == T else "extrapolated from the timed rows at the same TFLOP/s"}
 
 
-def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
+def topk_read_bytes(positions, p):
+    """The least a pruned Top-k must move per step: per (row, group) the
+    piece maxima (one per 16 candidate blocks), the scores of the k-1 pieces
+    that at least reach the bound (all candidates when there are fewer), and
+    the k ids written."""
+    import torch
+    lb = torch.clamp(torch.div(positions, p.block_size, rounding_mode="floor"), min=0).to(torch.int64)
+    per_row = (lb + 15) // 16 + torch.clamp(lb, max=16 * (p.topk - 1))
+    return float(4 * p.num_kv_heads * (per_row.sum().item() + p.topk * positions.numel()))
+
+
+def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops, topk_bytes):
     """Algorithmic work per step of the prefill kernels: (bound, amount, unit).
 
     An incidence is one valid (query row, group, selected block).  The
@@ -235,7 +247,8 @@ def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
     fp32 LSE (Sec. 4.2 IO analysis, KV-outer): its intensity, about 2/3 B_k
     FLOP/B, sits far below MI355X's bf16 ridge (2.5 PFLOP/s / 8 TB/s = 312), so
     it is HBM-bound.  The combine reads every partial and writes O and LSE.
-    Index scoring is an MFMA contraction; Top-k streams the block scores."""
+    Index scoring is an MFMA contraction; Top-k reads the piece maxima and the
+    pieces that reach its bound (topk_read_bytes)."""
     G = p.num_q_heads // p.num_kv_heads
     d, T, H_kv, H_q = p.head_dim, p.total_q_rows, p.num_kv_heads, p.num_q_heads
     kv_bytes = 4.0 * H_kv * float(sum(p.kv_lens)) * d
@@ -247,7 +260,7 @@ def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops):
         "kvo_combine_kernel": ("hbm", comb_bytes, "bytes"),
         "index_block_max_lds_kernel": ("mfma", idx_flops, "flops"),
         "index_block_max_wave_kernel": ("mfma", idx_flops, "flops"),
-        "index_topk_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
+        "index_topk_kernel": ("hbm", topk_bytes, "bytes"),
         "index_topk_split_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
     }
 
