@@ -359,6 +359,17 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // this lane's rows' LSE and query position, read once for all key tiles
+      float l2r[NTT][4];
+      int posr[NTT][4];
+#pragma unroll
+      for (int t = 0; t < NTT; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = 16 * t + 4 * qd + i;
+          l2r[t][i] = wv.lse2[row];
+          posr[t][i] = wv.pos[(sp * R + row) >> LG];
+        }
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
         f32x4 acc[2];
@@ -374,11 +385,8 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
 #pragma unroll
         for (int t = 0; t < NTT; ++t)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = 16 * t + 4 * qd + i;
-            const int xq = (sp * R + row) >> LG;
-            acc[t][i] = key <= wv.pos[xq] ? exp2_hw(acc[t][i] * s_main_log2 - wv.lse2[row]) : 0.f;
-          }
+          for (int i = 0; i < 4; ++i)
+            acc[t][i] = key <= posr[t][i] ? exp2_hw(acc[t][i] * s_main_log2 - l2r[t][i]) : 0.f;
         if constexpr (LG > 0) head_mean(acc, LG);
 #pragma unroll
         for (int t = 0; t < NTT; ++t)
