@@ -440,6 +440,13 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
 
       // ---- student: rows = the pass's 16 queries (lane c16 supplies query c16)
       float klq[4] = {0.f, 0.f, 0.f, 0.f};
+      int qpos[4];
+      float ql2[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        qpos[i] = wv.pos[4 * qd + i];
+        ql2[i] = wv.lsei2[4 * qd + i];
+      }
 #pragma unroll
       for (int kt = 0; kt < KT; ++kt) {
         f32x4 acc = f32x4{};
@@ -454,9 +461,8 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
         for (int i = 0; i < 4; ++i) pb[i] = wv.pbar[4 * qd + i][16 * kt + c16];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int qq = 4 * qd + i;
-          const bool on = key <= wv.pos[qq];
-          const float lz = acc[i] * sidx_log2 - wv.lsei2[qq];     // log2 P_idx
+          const bool on = key <= qpos[i];
+          const float lz = acc[i] * sidx_log2 - ql2[i];            // log2 P_idx
           const float pidx = on ? exp2_hw(lz) : 0.f;
           klq[i] += (on && pb[i] > 0.f) ? pb[i] * (__log2f(pb[i]) - lz) * kLn2 : 0.f;
           dl[i] = on ? pidx - pb[i] : 0.f;
@@ -486,6 +492,9 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
       }
       // d q_idx = Delta (16 queries x BK keys) k_idx (BK x D): A = Delta rows,
       // B = k_idx columns by transposing reads
+      int64_t incq[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) incq[i] = wv.inc[4 * qd + i] * D;
 #pragma unroll
       for (int n = 0; n < D / 16; ++n) {
         f32x4 acc = f32x4{};
@@ -494,7 +503,7 @@ __global__ __launch_bounds__(kK2Threads, 1) void kl_grad_kernel(
           acc = mfma16x16x32(ld_bf16x8(reinterpret_cast<const uint16_t*>(wv.pbar[c16]) + 32 * ks + 8 * qd),
                              kl_col8<D>(sm.ki, 32 * ks + 8 * qd, 16 * n, c16), acc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) dqp[wv.inc[4 * qd + i] * D + 16 * n + c16] = acc[i];
+        for (int i = 0; i < 4; ++i) dqp[incq[i] + 16 * n + c16] = acc[i];
       }
       __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
       __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
