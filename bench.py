@@ -262,6 +262,7 @@ def kernel_models(p, incidences, scored_keys, eff_flops, idx_flops, topk_bytes):
         "index_block_max_wave_kernel": ("mfma", idx_flops, "flops"),
         "index_topk_kernel": ("hbm", topk_bytes, "bytes"),
         "index_topk_split_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
+        "index_topk_rows_kernel": ("hbm", score_blocks * 4.0 + T * H_kv * p.topk * 4.0, "bytes"),
     }
 
 

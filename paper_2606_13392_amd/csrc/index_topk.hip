@@ -994,56 +994,44 @@ __global__ __launch_bounds__(64 * kSplitWaves) void index_topk_split_kernel(
 }
 
 // ---------------------------------------------------------------- row Top-k
-// The Top-k operator on its own (msa_block_topk): the k best columns of each
-// row of an fp32 score matrix, one wave per row.  The row is read in rounds
-// of RP values per lane (16 for rows of at most 1024 columns, else 32; VEC:
-// float4 loads).  A round's bound is the k-th
-// largest of the lanes' maxima (k distinct lanes hold a score at least that
-// large), raised to the running bound; the round's scores at or above it are
-// appended as keys to the wave's LDS buffer.  A buffer more than half full is
-// cut to its k best, whose k-th key raises the bound.  The k best keys of the
-// buffer are the row's.  A row whose candidates still overflow the buffer
-// (many equal scores) is streamed again through a key batch.
-constexpr int kRowWaves = 4;
-constexpr int kRowAhead = 4;
-
+// The k best (score, column) keys of one row of n fp32 scores, for one wave
+// (k <= 64): lanes 0 .. min(n, k)-1 of the result hold them, in no order.
+// The row is read in rounds of RP values per lane (VEC: float4 loads; the
+// row is 16-byte aligned and a load that starts below n stays inside its
+// allocation).  A round's bound is the k-th largest of the lanes' maxima (k
+// distinct lanes hold a score at least that large), raised to the running
+// bound; the round's scores at or above it are appended as keys to the
+// wave's LDS buffer `buf` (2 kWave entries).  A buffer more than half full
+// is cut to its k best, whose k-th key raises the bound.  The k best keys of
+// the buffer are the row's.  A row whose candidates still overflow the
+// buffer (many equal scores) is streamed again through a key batch.
 template <bool VEC, int RP>
-__global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float* __restrict__ scores,
-                                                                     int64_t n_rows, int n_cols, int64_t ld, int k,
-                                                                     int32_t* __restrict__ ids) {
-  __shared__ uint64_t s_buf[kRowWaves][2 * kWave];
+__device__ __forceinline__ uint64_t row_best_keys(const float* __restrict__ srow, int n, int k, uint64_t* buf) {
   const int lane = lane_id();
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x) / kWave;
-  const int64_t row = static_cast<int64_t>(blockIdx.x) * kRowWaves + w;
-  if (row >= n_rows) return;
-  const float* srow = scores + row * ld;
-  uint64_t* buf = s_buf[w];
   constexpr int kBuf = 2 * kWave;
   uint32_t t = 0;                  // ordered bound: the row's k-th best score is >= it
   int cnt = 0;
   bool fits = true;
-  for (int c0 = 0; c0 < n_cols; c0 += kWave * RP) {
+  for (int c0 = 0; c0 < n; c0 += kWave * RP) {
     // column of value v of this lane: VEC c0 + 256 (v / 4) + 4 lane + v % 4, else c0 + 64 v + lane
     auto col_of = [&](int v) { return VEC ? c0 + 4 * kWave * (v / 4) + 4 * lane + v % 4 : c0 + kWave * v + lane; };
     float x[RP];
     if constexpr (VEC) {
-      // rows are 16-byte aligned and ld % 4 == 0: a load that starts below
-      // n_cols stays inside the row's ld columns
 #pragma unroll
       for (int i = 0; i < RP / 4; ++i) {
         const int c = col_of(4 * i);
-        const f32x4 q = c < n_cols ? *reinterpret_cast<const f32x4*>(srow + c) : f32x4{};
+        const f32x4 q = c < n ? *reinterpret_cast<const f32x4*>(srow + c) : f32x4{};
 #pragma unroll
         for (int e = 0; e < 4; ++e) x[4 * i + e] = q[e];
       }
     } else {
 #pragma unroll
-      for (int v = 0; v < RP; ++v) x[v] = col_of(v) < n_cols ? srow[col_of(v)] : 0.f;
+      for (int v = 0; v < RP; ++v) x[v] = col_of(v) < n ? srow[col_of(v)] : 0.f;
     }
     uint32_t lm = 0;
 #pragma unroll
     for (int v = 0; v < RP; ++v) {
-      const uint32_t o = col_of(v) < n_cols ? ordered_u32(x[v]) : 0u;
+      const uint32_t o = col_of(v) < n ? ordered_u32(x[v]) : 0u;
       lm = o > lm ? o : lm;
     }
     const uint32_t tr = kth_largest_u32<1>(&lm, k);
@@ -1051,7 +1039,7 @@ __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float
 #pragma unroll
     for (int v = 0; v < RP; ++v) {
       const int c = col_of(v);
-      const bool take = c < n_cols && ordered_u32(x[v]) >= t;
+      const bool take = c < n && ordered_u32(x[v]) >= t;
       const uint64_t m = __ballot(take);
       if (m == 0) continue;
       const int pos = cnt + lanes_below(m);
@@ -1072,19 +1060,55 @@ __global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float
       t = tk > t ? tk : t;
     }
   }
-  uint64_t list;
-  if (fits) {
-    list = best_keys(buf, cnt, k, nullptr);
-  } else {
-    KeyBatch kb;
-    kb.pend = buf;
-    kb.K1 = k;
-    kb.list = 0;
-    kb.cnt = 0;
-    stream_chunks([=](int b) { return srow[b]; }, n_cols, 0, 1, [&](uint64_t v, uint64_t th) { return kb.push(v, th); });
-    kb.flush();
-    list = kb.list;
+  if (fits) return best_keys(buf, cnt, k, nullptr);
+  KeyBatch kb;
+  kb.pend = buf;
+  kb.K1 = k;
+  kb.list = 0;
+  kb.cnt = 0;
+  stream_chunks([=](int b) { return srow[b]; }, n, 0, 1, [&](uint64_t v, uint64_t th) { return kb.push(v, th); });
+  kb.flush();
+  return kb.list;
+}
+
+// One wave per index row of a chunk without chunk or piece maxima (few rows,
+// e.g. decode): the K1 best of the row's candidate blocks by row_best_keys,
+// then the local block.
+constexpr int kRowWaves = 4;
+
+__global__ __launch_bounds__(kRowWaves * kWave) void index_topk_rows_kernel(
+    const float* __restrict__ M, int64_t ldm, msa_seqs sq, const int32_t* __restrict__ unit_off, int H_kv, int qr,
+    int U, int rpu, int64_t u0, int64_t u1, int BK, int topk, int32_t* __restrict__ block_ids) {
+  __shared__ uint64_t s_buf[kRowWaves][2 * kWave];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x) / kWave;
+  const int64_t task = static_cast<int64_t>(blockIdx.x) * kRowWaves + w;
+  if (task >= (u1 - u0) * rpu) return;
+  const RowTask t = locate_row(M, ldm, sq, unit_off, H_kv, qr, U, rpu, u0, task, BK, topk, block_ids);
+  if (!t.ok) return;
+  if (t.no_position) {
+    if (lane < topk) t.out[lane] = -1;
+    return;
   }
+  const int K1 = topk - 1;
+  // M rows are 16-byte aligned and hold a multiple of 4 floats
+  const uint64_t list = K1 > 0 ? row_best_keys<true, 32>(t.mrow, t.nscan, K1, s_buf[w]) : 0ull;
+  finish_row(list, K1, t.lb, topk, t.out);
+}
+
+// The Top-k operator on its own (msa_block_topk): the k best columns of each
+// row of an fp32 score matrix, one wave per row, by row_best_keys with
+// rounds of 16 values per lane for rows of at most 1024 columns, else 32.
+template <bool VEC, int RP>
+__global__ __launch_bounds__(kRowWaves * kWave) void row_topk_kernel(const float* __restrict__ scores,
+                                                                     int64_t n_rows, int n_cols, int64_t ld, int k,
+                                                                     int32_t* __restrict__ ids) {
+  __shared__ uint64_t s_buf[kRowWaves][2 * kWave];
+  const int lane = lane_id();
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x) / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kRowWaves + w;
+  if (row >= n_rows) return;
+  const uint64_t list = row_best_keys<VEC, RP>(scores + row * ld, n_cols, k, s_buf[w]);
   const int nsel = __popcll(__ballot(lane < k && list != 0ull));
   uint32_t id = lane < nsel ? key_block(list) : 0xFFFFFFFFu;
   id = wave_sort_asc_u32(id);
@@ -1135,7 +1159,15 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
 }
 
 constexpr size_t kDefaultScoreBytes = size_t(4) << 30;   // block-score staging per call
-constexpr int64_t kSplitTopkRows = 4096;                 // fewer index rows: 4 waves per row
+constexpr int64_t kSplitTopkRows = 4096;                 // fewer index rows: no chunk / piece maxima
+// Few rows go one wave per row (index_topk_rows_kernel) when the rows are
+// short (at most 4 rounds of 2048 blocks), numerous enough to spread and the
+// Top-k small enough for the lane-maximum bound to keep a round's candidates
+// within the wave's buffer; otherwise 16 waves share each row
+// (index_topk_split_kernel).
+constexpr int kRowTopkMaxK = 33;
+constexpr int64_t kRowTopkMinRows = 64;
+constexpr int kRowTopkMaxBlocks = 4 * 2048;
 
 // 64-key sub-blocks in flight per wave of the narrow kernel: about 128 VGPRs of K_idx.
 template <int D, int B>
@@ -1234,10 +1266,15 @@ int index_topk_run(const IndexPlan& pl, const void* index_q, const void* index_k
                     num_kv_heads;
     const int64_t rows = (u1 - u0) * rpu;
     if (rows >= (int64_t(1) << 32)) return MSA_ERR_UNSUPPORTED;      // tasks are 32-bit in the kernels
-    if (rows <= kSplitTopkRows)
-      msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)), dim3(64 * kSplitWaves), 0, stream, M,
-                         static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
-                         block_size, topk, block_ids);
+    if (rows <= kSplitTopkRows && topk <= kRowTopkMaxK && rows >= kRowTopkMinRows && pl.bcap <= kRowTopkMaxBlocks)
+      msa_prof::launch("index_topk_rows_kernel", index_topk_rows_kernel,
+                       dim3(static_cast<unsigned>((rows + kRowWaves - 1) / kRowWaves)), dim3(kRowWaves * kWave), 0,
+                       stream, M, static_cast<int64_t>(pl.bcap), sq, unit_off, num_kv_heads, pl.qr, pl.U, rpu, u0, u1,
+                       block_size, topk, block_ids);
+    else if (rows <= kSplitTopkRows)
+      msa_prof::launch("index_topk_split_kernel", index_topk_split_kernel, dim3(static_cast<unsigned>(rows)),
+                       dim3(64 * kSplitWaves), 0, stream, M, static_cast<int64_t>(pl.bcap), sq, unit_off,
+                       num_kv_heads, pl.qr, pl.U, rpu, u0, u1, block_size, topk, block_ids);
     else
       msa_prof::launch("index_topk_kernel", index_topk_kernel, dim3(static_cast<unsigned>((rows + kWaves - 1) / kWaves)),
                        dim3(256), 0, stream, M, static_cast<int64_t>(pl.bcap), static_cast<const float*>(CM), cm_stride,

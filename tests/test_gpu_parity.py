@@ -203,7 +203,7 @@ def test_forward_small_workspaces_run_several_chunks():
         msa.profile_enable(False)
     rec = msa.profile_read()
     msa.profile_reset()
-    n_topk = sum(rec.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel"))
+    n_topk = sum(rec.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel", "index_topk_rows_kernel"))
     n_comb = rec.get("kvo_combine_kernel", (0, 0))[0]
     _say(f"  launches: index {n_topk} (plan {len(idx_starts)}), attention {n_comb} (plan {len(attn_starts)})")
     assert n_topk == len(idx_starts) >= 3 and n_comb == len(attn_starts) >= 3
@@ -326,7 +326,7 @@ def _sampled_workload(name, n_rows, gen="numpy", check_attn_rows=None, stratifie
         ws_a = msa.sparse_attn_prefill_workspace_size(seqs, p.num_q_heads, p.num_kv_heads, p.head_dim,
                                                       p.block_size, p.topk)
         idx_starts, attn_starts = _launch_row_starts(p, ws_i, ws_a)
-        n_topk = sum(launches.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel"))
+        n_topk = sum(launches.get(kn, (0, 0))[0] for kn in ("index_topk_kernel", "index_topk_split_kernel", "index_topk_rows_kernel"))
         n_comb = launches.get("kvo_combine_kernel", (0, 0))[0]
         _say(f"  launches: index {n_topk} (plan {len(idx_starts)}), attention {n_comb} (plan {len(attn_starts)})")
         assert n_topk == len(idx_starts) and n_comb == len(attn_starts), "chunk plan mirror out of date"
@@ -473,3 +473,49 @@ def test_index_exact_ties(case):
     bad = [(r, g) for i, r in enumerate(rows) for g in range(H_kv) if not np.array_equal(got[i, g], ids_ora[i, g])]
     _say(f"  {len(rows)} rows x {H_kv} groups, {len(bad)} differ")
     assert not bad, f"first differing (row, group) {bad[0]}: {got[rows.index(bad[0][0]), bad[0][1]]} vs oracle"
+
+
+# Decode-shaped batches (one query row per sequence) with exact score ties
+# among key blocks: name, sequences, context, H_kv, topk, repeat period of
+# each sequence's key blocks (0: zero index queries, every score equal).
+# The first three go one wave per index row (a Top-k of at most 33 over at
+# most 8192 blocks, >= 64 rows); the all-equal rows overflow that wave's
+# candidate buffer and are ranked again through the key batch.  The last
+# shares each row among 16 waves (k 64).
+DECODE_TIE_CASES = [
+    ("dec_ties_period7_k16", 64, 8192, 1, 16, 7),
+    ("dec_ties_period5_k32", 32, 65536 - 100, 2, 32, 5),
+    ("dec_ties_all_equal_k32", 16, 135000, 4, 32, 0),
+    ("dec_ties_period3_k64", 16, 100000, 2, 64, 3),
+]
+
+
+@pytest.mark.parametrize("case", DECODE_TIE_CASES, ids=[c[0] for c in DECODE_TIE_CASES])
+def test_decode_index_exact_ties(case):
+    name, nseq, ctx, H_kv, topk, period = case
+    _say(f"[decode ties] {name}: {nseq} x 1 row at {ctx}, H_kv {H_kv}, k {topk}")
+    p = synth.packed_problem(name, [1] * nseq, [ctx] * nseq, num_q_heads=2 * H_kv, num_kv_heads=H_kv, d_idx=64,
+                             block_size=64, topk=topk, seed=zlib.crc32(name.encode()) % 10000)
+    B = p.block_size
+    rng = np.random.default_rng(p.seed)
+    iq = rng.standard_normal((nseq, H_kv, 64), dtype=np.float32)
+    ik = rng.standard_normal((nseq * ctx, 64), dtype=np.float32)
+    if period:
+        for s in range(nseq):
+            seq = ik[s * ctx:(s + 1) * ctx]
+            pat = seq[:period * B].copy()
+            reps = -(-ctx // (period * B))
+            seq[:] = np.tile(pat, (reps, 1))[:ctx]
+    else:
+        iq[:] = 0
+    iq, ik = synth.bf16_bits_from_f32(iq), synth.bf16_bits_from_f32(ik)
+    dev = torch.device("cuda")
+    seqs = msa.Seqs.from_problem(p, dev)
+    ids = msa.index_topk(to_dev(iq), to_dev(ik), seqs, B, topk)
+    torch.cuda.synchronize()
+    lay = O.layout_of(p)
+    ids_ora, _ = O.select_blocks(iq, ik, lay, B, topk, rows=list(range(nseq)))
+    got = ids.cpu().numpy()
+    bad = [(r, g) for r in range(nseq) for g in range(H_kv) if not np.array_equal(got[r, g], ids_ora[r, g])]
+    _say(f"  {nseq} rows x {H_kv} groups, {len(bad)} differ")
+    assert not bad, f"first differing (row, group) {bad[0]}: {got[bad[0][0], bad[0][1]]} vs oracle"
