@@ -320,6 +320,7 @@ __global__ __launch_bounds__(64 * kvo_waves<BK>(), BK == 128 ? 1 : 2) void kvo_a
 // dims of one of the group's G heads over the valid slots.
 constexpr int kCombineWaves = 4;
 
+template <int PER>
 __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
     const int32_t* __restrict__ block_ids, msa_seqs sq, const int64_t* __restrict__ blk_base, int H_q, int H_kv,
     int BK, int topk, int64_t row0, int64_t nrows, const uint16_t* __restrict__ o_buf,
@@ -358,57 +359,71 @@ __global__ __launch_bounds__(64 * kCombineWaves) void kvo_combine_kernel(
     s_w[wave][lane][hh] = (valid && x > -INFINITY && t > -INFINITY) ? exp2f((x - t) * kLog2e) : 0.f;
   }
   __syncthreads();
-  // dims per lane: 8 for G <= 4, 16 for G <= 8, 32 for G <= 16 (a multiple of
-  // the 16-byte loads); lane covers head hh, dims [dd, dd + per); lanes past
-  // G * 128 / per idle.
-  const int per = G <= 4 ? 8 : (G <= 8 ? 16 : 32);
-  const int lanes_per_head = kHeadDim / per;
+  // PER dims per lane: 8 for G <= 4, 16 for G <= 8, 32 for G <= 16 (a
+  // multiple of the 16-byte loads); lane covers head hh, dims [dd, dd + PER);
+  // lanes past G * 128 / PER idle.
+  constexpr int E8 = PER / 8;                        // 16-byte loads per slot
+  constexpr int NB = PER == 32 ? 2 : 4;              // slots per batch
+  const int lanes_per_head = kHeadDim / PER;
   const bool lane_on = lane < G * lanes_per_head;
   const int hh = lane_on ? lane / lanes_per_head : 0;
-  const int dd = (lane % lanes_per_head) * per;
-  float acc[32];
+  const int dd = (lane % lanes_per_head) * PER;
+  float acc[PER];
 #pragma unroll
-  for (int e = 0; e < 32; ++e) acc[e] = 0.f;
+  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
   const uint16_t* obase = o_buf + ((rl * H_kv + r) * static_cast<int64_t>(topk)) * G * kHeadDim +
                           static_cast<int64_t>(hh) * kHeadDim + dd;
-  // valid slots, 4 at a time: their partial loads are in flight together
+  // valid slots in batches of NB, ascending; batch n + 1's partial loads are
+  // issued before batch n is accumulated (two batches in flight)
   uint64_t vmask = __ballot(valid);
-  while (vmask != 0ull && lane_on) {
-    int js[4];
+  auto take = [&](int (&js)[NB]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < NB; ++u) {
       js[u] = vmask != 0ull ? __ffsll(static_cast<unsigned long long>(vmask)) - 1 : -1;
       vmask &= vmask - 1;
     }
-    u32x4 x[4][4];
-    float w[4];
+  };
+  auto issue = [&](const int (&js)[NB], u32x4 (&x)[NB][E8]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int j = js[u] >= 0 ? js[u] : js[0];
-      w[u] = js[u] >= 0 ? s_w[wave][j][hh] : 0.f;
-      const uint16_t* src = obase + static_cast<int64_t>(j) * G * kHeadDim;
+    for (int u = 0; u < NB; ++u) {
+      const uint16_t* src = obase + static_cast<int64_t>(js[u] >= 0 ? js[u] : js[0]) * G * kHeadDim;
 #pragma unroll
-      for (int e8 = 0; e8 < 4; ++e8)
-        if (8 * e8 < per) x[u][e8] = *reinterpret_cast<const u32x4*>(src + 8 * e8);
+      for (int e8 = 0; e8 < E8; ++e8) x[u][e8] = *reinterpret_cast<const u32x4*>(src + 8 * e8);
     }
+  };
+  auto accumulate = [&](const int (&js)[NB], const u32x4 (&x)[NB][E8]) {
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
+    for (int u = 0; u < NB; ++u) {
+      const float w = js[u] >= 0 ? s_w[wave][js[u]][hh] : 0.f;
 #pragma unroll
-      for (int e8 = 0; e8 < 4; ++e8) {
-        if (8 * e8 >= per) break;
+      for (int e8 = 0; e8 < E8; ++e8)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          acc[8 * e8 + 2 * e] += w[u] * __uint_as_float(x[u][e8][e] << 16);
-          acc[8 * e8 + 2 * e + 1] += w[u] * __uint_as_float(x[u][e8][e] & 0xFFFF0000u);
+          acc[8 * e8 + 2 * e] += w * __uint_as_float(x[u][e8][e] << 16);
+          acc[8 * e8 + 2 * e + 1] += w * __uint_as_float(x[u][e8][e] & 0xFFFF0000u);
         }
-      }
+    }
+  };
+  if (lane_on) {
+    int ja[NB], jb[NB];
+    u32x4 xa[NB][E8], xb[NB][E8];
+    take(ja);
+    if (ja[0] >= 0) issue(ja, xa);
+    while (ja[0] >= 0) {
+      take(jb);
+      if (jb[0] >= 0) issue(jb, xb);
+      accumulate(ja, xa);
+      if (jb[0] < 0) break;
+      take(ja);
+      if (ja[0] >= 0) issue(ja, xa);
+      accumulate(jb, xb);
+    }
   }
   if (!active || !lane_on) return;
   const int head = r * G + hh;
   uint16_t* dst = o + (row * H_q + head) * kHeadDim + dd;
 #pragma unroll
-  for (int e8 = 0; e8 < 4; ++e8) {
-    if (8 * e8 >= per) break;
+  for (int e8 = 0; e8 < E8; ++e8) {
     uint4 wv;
     wv.x = pack_bf16x2(acc[8 * e8 + 0], acc[8 * e8 + 1]);
     wv.y = pack_bf16x2(acc[8 * e8 + 2], acc[8 * e8 + 3]);
@@ -566,9 +581,11 @@ int msa_kvo_prefill(const void* q, const void* k, const void* v, const int32_t* 
       launch_kvo_attn<128, uint8_t>(q, k, v, sq, blk_base, tile_off, item_off, handles, H_q, H_kv, topk, pl.nbcap,
                                     r0, sl2, v_scale, o_buf, lse_buf, cnt + pl.ntile, stream);
     const int64_t pairs = nr * H_kv;
-    msa_prof::launch("kvo_combine_kernel", kvo_combine_kernel, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
-                       dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,
-                       o_buf, lse_buf, op, lse);
+    const int G = H_q / H_kv;
+    auto combine = G <= 4 ? kvo_combine_kernel<8> : (G <= 8 ? kvo_combine_kernel<16> : kvo_combine_kernel<32>);
+    msa_prof::launch("kvo_combine_kernel", combine, dim3(static_cast<unsigned>((pairs + kCombineWaves - 1) / kCombineWaves)),
+                     dim3(64 * kCombineWaves), 0, stream, block_ids, sq, blk_base, H_q, H_kv, BK, topk, r0, nr,
+                     o_buf, lse_buf, op, lse);
   }
   return msa_host::launch_status();
 }
