@@ -137,6 +137,7 @@ __device__ __forceinline__ float block_max_rows(const f32x16 (&acc)[MT][NJ], int
 constexpr int kStageBlocks = 16;      // block maxima staged per row before a 64-byte store
 constexpr int kPieceBlocks = 16;      // blocks per piece maximum (the Top-k's finer skip test)
 constexpr int kSurvivorCap = 1024;    // pieces per round of the Top-k's piece scan
+constexpr int kSlicePieces = 4;       // pieces per 64-block CTA slice: PM[slice][row][4]
 
 // One 16-byte piece per lane from global memory straight into LDS
 // (global_load_lds_dwordx4): lane l writes bytes [16 l, 16 l + 16) after the
@@ -258,10 +259,14 @@ __global__ __launch_bounds__(256, (RW == 64) ? 3 : 2) void index_block_max_lds_k
       sm.stage[w][64 * sp + lane][kb & (kStageBlocks - 1)] = bm[sp];
     }
     if ((kb & (kStageBlocks - 1)) == kStageBlocks - 1 || kb + 1 == kb1) {
-      // the piece's maximum over each row's candidate blocks, PM[piece][row]
+      // the piece's maximum over each row's candidate blocks: the 4 pieces of
+      // the CTA's slice sit together per row, PM[slice][row][4], so that the
+      // Top-k kernel reads a row's piece maxima four per 16-byte load
 #pragma unroll
       for (int sp = 0; sp < NP; ++sp) {
-        if (64 * sp + lane < nvalid) PM[static_cast<int64_t>(kb / kPieceBlocks) * cm_stride + slot0 + 64 * sp + lane] = pmax[sp];
+        if (64 * sp + lane < nvalid)
+          PM[(static_cast<int64_t>(blockIdx.y) * cm_stride + slot0 + 64 * sp + lane) * kSlicePieces +
+             (kb / kPieceBlocks) % kSlicePieces] = pmax[sp];
         pmax[sp] = -INFINITY;
       }
       // the wave writes 16 rows x 64 B per store pass (4 lanes per row, 16 B each)
@@ -785,8 +790,8 @@ __device__ __forceinline__ uint64_t best_keys(uint64_t* buf, int cnt, int K, uin
 // nothing, when the candidates overflow `buf` (rows with many equal scores)
 // or the row has more than kSurvivorCap pieces; the caller then ranks the row
 // by the pruned scan.  M rows are 16-byte aligned with a multiple of 4 floats.
-template <typename LoadPm>
-__device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow, LoadPm pm, int nscan, int K1,
+template <typename LoadPm4>
+__device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow, LoadPm4 pm4, int nscan, int K1,
                                                  uint64_t* buf, int32_t* surv, uint64_t& list) {
   const int lane = lane_id();
   if (K1 <= 0) return false;
@@ -799,12 +804,26 @@ __device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow,
   const bool direct = npiece <= K1;                       // rank the scores themselves
   const int nval = direct ? nscan : npiece;               // <= kSurvivorCap either way
   constexpr int kGroups = kSurvivorCap / kWave;
-  const int nv = (nval + kWave - 1) / kWave;
+  // value k of this lane: score 64 k + lane (direct), else piece
+  // 4 (64 (k / 4) + lane) + k % 4 (the lane's slices, four pieces per load)
+  const int nv = direct ? (nval + kWave - 1) / kWave : kSlicePieces * ((nval + kSlicePieces * kWave - 1) / (kSlicePieces * kWave));
+  auto value_id = [&](int k) { return direct ? kWave * k + lane : kSlicePieces * (kWave * (k / kSlicePieces) + lane) + k % kSlicePieces; };
   uint32_t pv[kGroups];
+  if (direct) {
 #pragma unroll
-  for (int k = 0; k < kGroups; ++k) {
-    const int c = kWave * k + lane;
-    pv[k] = k < nv && c < nval ? ordered_u32(direct ? mrow[c] : pm(c)) : 0u;
+    for (int k = 0; k < kGroups; ++k) {
+      const int c = kWave * k + lane;
+      pv[k] = k < nv && c < nval ? ordered_u32(mrow[c]) : 0u;
+    }
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < kGroups / kSlicePieces; ++kk) {
+      const int ch = kWave * kk + lane;
+      const f32x4 x = kSlicePieces * kk < nv && kSlicePieces * ch < nval ? pm4(ch) : f32x4{};
+#pragma unroll
+      for (int e = 0; e < kSlicePieces; ++e)
+        pv[kSlicePieces * kk + e] = kSlicePieces * ch + e < nval ? ordered_u32(x[e]) : 0u;
+    }
   }
   const uint32_t t1 = kth_largest_bound(pv, nv, K1);
   if (t1 == 0) return false;
@@ -832,7 +851,7 @@ __device__ __forceinline__ bool select_row_radix(const float* __restrict__ mrow,
       if (k < nv) {
         const bool ok = pv[k] >= t1;
         const uint64_t m = __ballot(ok);
-        if (ok) surv[ns + lanes_below(m)] = kWave * k + lane;
+        if (ok) surv[ns + lanes_below(m)] = value_id(k);
         ns += __popcll(m);
       }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -946,9 +965,10 @@ __global__ __launch_bounds__(256) void index_topk_kernel(
   if (CM) {
     const float* cmrow = CM + t.slot;
     auto cm = [=](int c) { return cmrow[static_cast<int64_t>(c) * cm_stride]; };
-    const float* pmrow = PM + t.slot;
-    auto pm = [=](int q) { return pmrow[static_cast<int64_t>(q) * cm_stride]; };
-    if (!select_row_radix(mrow, pm, t.nscan, topk - 1, kb.pend, s_surv[threadIdx.x / kWave], list))
+    const float* pmrow = PM + t.slot * kSlicePieces;
+    auto pm = [=](int q) { return pmrow[static_cast<int64_t>(q / kSlicePieces) * cm_stride * kSlicePieces + q % kSlicePieces]; };
+    auto pm4 = [=](int ch) { return *reinterpret_cast<const f32x4*>(pmrow + static_cast<int64_t>(ch) * cm_stride * kSlicePieces); };
+    if (!select_row_radix(mrow, pm4, t.nscan, topk - 1, kb.pend, s_surv[threadIdx.x / kWave], list))
       list = scan_row_pruned(load, cm, pm, t.nscan, kb, s_surv[threadIdx.x / kWave]);
   } else {
     list = scan_row_batched(load, t.nscan, kb);
@@ -1153,7 +1173,7 @@ int make_plan(const msa_seqs* seqs, int H_kv, int d_idx, int BK, int topk, Index
   pl->bcap = static_cast<int>(msa_host::align_up(static_cast<size_t>(nb > 0 ? nb : 1), 4));
   pl->hdr_bytes = msa_host::align_up(sizeof(int32_t) * (seqs->num_seqs + 1), 256);
   pl->cmcap = pl->U >= kWaves ? (pl->bcap + kWave - 1) / kWave : 0;
-  pl->pcap = pl->cmcap > 0 ? (pl->bcap + kPieceBlocks - 1) / kPieceBlocks : 0;
+  pl->pcap = pl->cmcap * kSlicePieces;
   pl->unit_bytes = static_cast<size_t>(pl->U) * kWave * (pl->bcap + pl->cmcap + pl->pcap) * sizeof(float);
   return MSA_OK;
 }
@@ -1236,7 +1256,7 @@ int index_topk_run(const IndexPlan& pl, const void* index_q, const void* index_k
   // chunk maxima CM[chunk][row] follow the chunk's score rows
   const int64_t cm_stride = chunk * pl.U * kWave;
   float* CM = pl.cmcap > 0 ? M + cm_stride * pl.bcap : nullptr;
-  // piece maxima PM[piece][row] follow the chunk maxima
+  // piece maxima PM[slice][row][4] follow the chunk maxima
   float* PM = pl.cmcap > 0 ? CM + cm_stride * pl.cmcap : nullptr;
   const msa_seqs sq = *seqs;
   const uint16_t* iq = static_cast<const uint16_t*>(index_q);

@@ -52,10 +52,11 @@ def test_workspace_queries_are_host_only():
     # row groups of 64 / H_kv = 32 query rows; sequences longer than two groups
     # take units of 4 groups.  Each unit holds 4 x 64 index rows of
     # ceil(100/64) = 2 block scores rounded up to 4, one 64-block chunk
-    # maximum and one 16-block piece maximum, fp32; plus the unit table.
+    # maximum and the four 16-block piece maxima of that chunk, fp32; plus the
+    # unit table.
     groups = 100 // 32 + 1
     units = groups // 4 + 1
-    assert n == 256 + units * 4 * 64 * (4 + 1 + 1) * 4
+    assert n == 256 + units * 4 * 64 * (4 + 1 + 4) * 4
     # at most one row group per sequence: one unit per sequence, no chunk maxima
     s1 = _seqs(num_seqs=4, total_q_rows=4, max_q_rows=1)
     n1 = L.msa_index_topk_workspace_size(ctypes.byref(s1), 2, 64, 64, 8)

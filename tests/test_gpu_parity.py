@@ -245,7 +245,7 @@ def _plan_sizes(p):
     max_units = S if seq_units else (T // qr + S) // U + S
     bcap = _align(-(-p.max_kv_len // B), 4)
     cmcap = -(-bcap // 64) if U >= 4 else 0
-    pcap = -(-bcap // 16) if cmcap else 0
+    pcap = 4 * cmcap                      # the four 16-block piece maxima of each 64-block chunk
     unit_bytes = U * 64 * (bcap + cmcap + pcap) * 4
     hdr = _align(4 * (S + 1))
     ntile = H_kv * S * max(1, -(-p.max_kv_len // B))
