@@ -222,9 +222,51 @@ def dense_prefill_baseline(args, p, d, dev):
     tflops = slice_flops / (ms * 1e-3) / 1e12
     del o, lse, ws
     log(f"[bench] dense baseline: {S} rows in {ms:.1f} ms ({tflops:.0f} TFLOP/s)")
+    k0 = p.kv_starts[0]
+    sdpa = torch_sdpa_reference(q, d["k"][k0:], d["v"][k0:], L, slice_flops)
     return {"rows_timed": S, "ms_timed": ms, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS,
             "flops_full": full_flops, "ms_full": ms * full_flops / slice_flops,
-            "full_is": "measured" if S == T else "extrapolated from the timed rows at the same TFLOP/s"}
+            "full_is": "measured" if S == T else "extrapolated from the timed rows at the same TFLOP/s",
+            "torch_sdpa_flash": sdpa}
+
+
+def torch_sdpa_reference(q, k, v, L, flops):
+    """torch's own flash attention (scaled_dot_product_attention restricted to
+    its FLASH_ATTENTION backend, GQA) on the same dense rows, for context: the
+    S query rows at the end of an L-key context as a non-causal pass over the
+    keys before them plus a causal S x S square (the same FLOPs as the dense
+    kernel's causal rows).  Timing only; None values and the error when the
+    backend cannot run the shapes."""
+    import torch
+    import torch.nn.functional as F
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    S = q.shape[0]
+    try:
+        qh = q.permute(1, 0, 2).unsqueeze(0).contiguous()
+        kh = k[:L].permute(1, 0, 2).unsqueeze(0).contiguous()
+        vh = v[:L].permute(1, 0, 2).unsqueeze(0).contiguous()
+        kp, vp, ks, vs = kh[:, :, :L - S], vh[:, :, :L - S], kh[:, :, L - S:], vh[:, :, L - S:]
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            def run():
+                F.scaled_dot_product_attention(qh, kp, vp, enable_gqa=True)
+                F.scaled_dot_product_attention(qh, ks, vs, is_causal=True, enable_gqa=True)
+            run()
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            run()
+            b.record()
+            torch.cuda.synchronize()
+        ms = a.elapsed_time(b)
+        del qh, kh, vh, kp, vp, ks, vs
+        torch.cuda.empty_cache()
+        tflops = flops / (ms * 1e-3) / 1e12
+        log(f"[bench] torch SDPA (flash backend) on the same rows: {ms:.1f} ms ({tflops:.0f} TFLOP/s)")
+        return {"ms_timed": ms, "tflops": tflops, "frac_of_bf16_peak": tflops / PEAK_BF16_TFLOPS}
+    except Exception as e:                      # a context figure only: never fails the bench
+        torch.cuda.empty_cache()
+        return {"ms_timed": None, "tflops": None, "error": f"{type(e).__name__}: {str(e)[:200]}"}
 
 
 def topk_read_bytes(positions, p):
