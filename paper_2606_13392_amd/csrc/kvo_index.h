@@ -118,13 +118,25 @@ __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restric
   }
   // pass 1: histogram (or, without LDS room, claim each position directly);
   // one row per thread keeps 64 rows' id lookups in flight per wave (one row
-  // per wave, slot on lane, took twice as long)
+  // per wave, slot on lane, took twice as long); a row's ids are read four per
+  // 16-byte load when topk % 4 == 0 and the id array is 16-byte aligned
+  const bool vec = topk % 4 == 0 && (reinterpret_cast<uintptr_t>(block_ids) & 15) == 0;
   for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
     int s;
     const int p = row_position(sq, row, &s);
     const int32_t* ids = block_ids + (row * H_kv + r) * topk;
     int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
     const int64_t gb0 = blk_base[s];
+    if (vec && in_lds) {
+      for (int j = 0; j < topk; j += 4) {
+        const int4 b4 = *reinterpret_cast<const int4*>(ids + j);
+        const int bb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (incidence_ok(bb[e], p, BK, blk_base, s)) atomicAdd(&hist[gb0 + bb[e] - g_lo], 1);
+      }
+      continue;
+    }
     for (int j = 0; j < topk; ++j) {
       const int b = ids[j];
       if (!incidence_ok(b, p, BK, blk_base, s)) continue;
@@ -141,13 +153,27 @@ __global__ __launch_bounds__(256) void kvo_count_kernel(const int32_t* __restric
     if (c > 0) hist[i] = atomicAdd(&cnt[tile_base + g_lo + i], c);
   }
   __syncthreads();
-  // pass 2: positions inside the claimed segments
+  // pass 2: positions inside the claimed segments (16-byte loads and stores
+  // of four slots on the same condition; slots that are no incidence get
+  // position 0, which nothing reads)
   for (int64_t row = rb0 + threadIdx.x; row < rb1; row += 256) {
     int s;
     const int p = row_position(sq, row, &s);
     const int32_t* ids = block_ids + (row * H_kv + r) * topk;
     int32_t* tp = tpos + ((row - row0) * H_kv + r) * topk;
     const int64_t gb0 = blk_base[s];
+    if (vec) {
+      for (int j = 0; j < topk; j += 4) {
+        const int4 b4 = *reinterpret_cast<const int4*>(ids + j);
+        const int bb[4] = {b4.x, b4.y, b4.z, b4.w};
+        int t4[4] = {0, 0, 0, 0};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (incidence_ok(bb[e], p, BK, blk_base, s)) t4[e] = atomicAdd(&hist[gb0 + bb[e] - g_lo], 1);
+        *reinterpret_cast<int4*>(tp + j) = make_int4(t4[0], t4[1], t4[2], t4[3]);
+      }
+      continue;
+    }
     for (int j = 0; j < topk; ++j) {
       const int b = ids[j];
       if (!incidence_ok(b, p, BK, blk_base, s)) continue;
