@@ -26,11 +26,19 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr int kAttnWaves = 4;                 // waves per CTA, each with its own block share
 constexpr int kRedStride = kHeadDim + 4;      // fp32 row stride of the merge buffer
 
+constexpr int kKRowPad = kHeadDim + 8;       // bf16 K rows staged with 16 bytes of padding
+
 template <int BK>
 struct AttnSmem {
-  // V of one block, transposed: vt[d][key]; +4 keys of padding per row.  After
-  // the block loop the same bytes hold the wave's scaled O (16 x kRedStride fp32).
-  uint16_t vt[kHeadDim][BK + 4];
+  union {                                        // kr: 64-key bf16 blocks only
+    // bf16 K of one block, row-major kr[key][d]: the rows arrive as whole
+    // 256-byte rows (16 lanes per row) and are read back as MFMA operands
+    uint16_t kr[BK == 64 ? BK : 1][kKRowPad];
+    // V of one block, transposed: vt[d][key]; +4 keys of padding per row.
+    // After the block loop the same bytes hold the wave's scaled O (16 x
+    // kRedStride fp32).
+    uint16_t vt[kHeadDim][BK + 4];
+  };
 };
 static_assert(sizeof(AttnSmem<64>) >= 16 * kRedStride * sizeof(float), "merge buffer does not fit");
 
@@ -115,6 +123,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
   const KeyBlocks kbk = key_blocks(sq, g, s, BK);
   const int64_t seq0 = PAGED ? 0 : g.kv_start;           // contiguous: keys from kv_start
   const T* kbase = k + seq0 * kv_stride + static_cast<int64_t>(r) * kHeadDim + 8 * q4;
+  const T* krow_base = k + seq0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;   // row starts
   const T* vbase = v + seq0 * kv_stride + static_cast<int64_t>(r) * kHeadDim;
   // without block ids (dense mode) slot b is key block b
   const int32_t* ids = block_ids ? block_ids + (row * H_kv + r) * topk : nullptr;
@@ -143,13 +152,32 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     // S^T and the softmax run while V is still in flight.
     // paged: the block's page (keys addressed inside it); else keys from kv_start
     const int64_t page_row = PAGED ? kbk.block_row(__builtin_amdgcn_readlane(my_pg, slot - slot0), b) : 0;
+    // bf16, 64-key blocks: each load instruction takes 4 whole 256-byte K rows
+    // (16 lanes per row; the rows are scattered at the cache's token stride,
+    // and whole rows per instruction are served faster than 64-byte pieces of
+    // 16 rows) and the block goes through LDS into the MFMA operand layout
+    // (111 -> 107 us per 128K decode step).  E4M3 (128-byte rows) and 128-key
+    // blocks (equal or slower staged) load the operands directly.
+    constexpr bool kStageK = sizeof(T) == 2 && BK == 64;
     Raw<T> ka[BK / 16][kHeadDim / 32];
+    if constexpr (kStageK) {
 #pragma unroll
-    for (int i = 0; i < BK / 16; ++i) {
-      const int key = key0 + 16 * i + n;
-      const T* kp = PAGED ? kbase + (page_row + 16 * i + n) * kv_stride : kbase + static_cast<int64_t>(key) * kv_stride;
+      for (int i = 0; i < BK / 16; ++i)
 #pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? load_raw(kp + 32 * ks) : Raw<T>{};
+        for (int j = 0; j < 4; ++j) {
+          const int kr = 16 * i + 4 * j + q4;            // key row of this lane: lanes 16 q4 .. + 15
+          const int key = key0 + kr;
+          const T* kp = (PAGED ? krow_base + (page_row + kr) * kv_stride : krow_base + static_cast<int64_t>(key) * kv_stride) + 8 * n;
+          ka[i][j] = key < g.kv_len ? load_raw(kp) : Raw<T>{};
+        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < BK / 16; ++i) {
+        const int key = key0 + 16 * i + n;
+        const T* kp = PAGED ? kbase + (page_row + 16 * i + n) * kv_stride : kbase + static_cast<int64_t>(key) * kv_stride;
+#pragma unroll
+        for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? load_raw(kp + 32 * ks) : Raw<T>{};
+      }
     }
     Raw<T> vraw[BK / 16][4];
     if constexpr (PAGED)
@@ -157,6 +185,20 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     else
       load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
 
+    if constexpr (kStageK) {
+      wave_lds_order();                               // the previous block's V^T reads are done
+#pragma unroll
+      for (int i = 0; i < BK / 16; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<Raw<T>*>(&sm.kr[16 * i + 4 * j + q4][8 * n]) = ka[i][j];
+      wave_lds_order();                               // K staged
+#pragma unroll
+      for (int i = 0; i < BK / 16; ++i)
+#pragma unroll
+        for (int ks = 0; ks < kHeadDim / 32; ++ks)
+          ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr[16 * i + n][32 * ks + 8 * q4]);
+    }
     // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
     f32x4 st[BK / 16];
 #pragma unroll
