@@ -34,6 +34,8 @@ struct AttnSmem {
     // bf16 K of one block, row-major kr[key][d]: the rows arrive as whole
     // 256-byte rows (16 lanes per row) and are read back as MFMA operands
     uint16_t kr[BK == 64 ? BK : 1][kKRowPad];
+    // E4M3 K of one 64-key block, row-major kr8[key][d] (+16 B pad per row)
+    uint8_t kr8[BK == 64 ? BK : 1][kHeadDim + 16];
     // V of one block, transposed: vt[d][key]; +4 keys of padding per row.
     // After the block loop the same bytes hold the wave's scaled O (16 x
     // kRedStride fp32).
@@ -152,15 +154,34 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     // S^T and the softmax run while V is still in flight.
     // paged: the block's page (keys addressed inside it); else keys from kv_start
     const int64_t page_row = PAGED ? kbk.block_row(__builtin_amdgcn_readlane(my_pg, slot - slot0), b) : 0;
-    // bf16, 64-key blocks: each load instruction takes 4 whole 256-byte K rows
-    // (16 lanes per row; the rows are scattered at the cache's token stride,
-    // and whole rows per instruction are served faster than 64-byte pieces of
-    // 16 rows) and the block goes through LDS into the MFMA operand layout
-    // (111 -> 107 us per 128K decode step).  E4M3 (128-byte rows) and 128-key
-    // blocks (equal or slower staged) load the operands directly.
-    constexpr bool kStageK = sizeof(T) == 2 && BK == 64;
+    // 64-key blocks: each load instruction takes whole K rows (bf16: 4 rows
+    // of 256 bytes, 16 lanes per row; E4M3: 8 rows of 128 bytes) -- the rows
+    // are scattered at the cache's token stride, and whole rows per
+    // instruction are served faster than 64- or 32-byte pieces of 16 rows --
+    // and the block goes through LDS into the MFMA operand layout (bf16: 111
+    // -> 107 us per 128K decode step).  128-key blocks (equal or slower
+    // staged) load the operands directly.
+    constexpr bool kStageK = BK == 64;
     Raw<T> ka[BK / 16][kHeadDim / 32];
-    if constexpr (kStageK) {
+    if constexpr (kStageK && sizeof(T) == 1) {
+      u32x4 kw[BK / 8];
+#pragma unroll
+      for (int i = 0; i < BK / 8; ++i) {
+        const int kr = 8 * i + (lane >> 3);                 // key row of this lane: lanes 8 (lane / 8) .. + 7
+        const int key = key0 + kr;
+        const T* kp = (PAGED ? krow_base + (page_row + kr) * kv_stride : krow_base + static_cast<int64_t>(key) * kv_stride) + 16 * (lane & 7);
+        kw[i] = key < g.kv_len ? *reinterpret_cast<const u32x4*>(kp) : u32x4{};
+      }
+      wave_lds_order();                               // the previous block's V^T reads are done
+#pragma unroll
+      for (int i = 0; i < BK / 8; ++i) *reinterpret_cast<u32x4*>(&sm.kr8[8 * i + (lane >> 3)][16 * (lane & 7)]) = kw[i];
+      wave_lds_order();                               // K staged
+#pragma unroll
+      for (int i = 0; i < BK / 16; ++i)
+#pragma unroll
+        for (int ks = 0; ks < kHeadDim / 32; ++ks)
+          ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr8[16 * i + n][32 * ks + 8 * q4]);
+    } else if constexpr (kStageK) {
 #pragma unroll
       for (int i = 0; i < BK / 16; ++i)
 #pragma unroll
@@ -185,7 +206,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     else
       load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
 
-    if constexpr (kStageK) {
+    if constexpr (kStageK && sizeof(T) == 2) {
       wave_lds_order();                               // the previous block's V^T reads are done
 #pragma unroll
       for (int i = 0; i < BK / 16; ++i)
