@@ -356,16 +356,49 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
   bf16x8 bq[2][KS];
   load_index_rows<D_IDX>(index_q + (static_cast<int64_t>(ur.g.q_begin + ur.t0) * H_kv) * D_IDX, nvalid, n, h, bq);
   const KeyBlocks kbk = key_blocks(sq, ur.g, ur.s, BK);
+  // Lane (n, h) takes key row 32 i + n, dims h d_idx / 2 + 8 st .. +8 at
+  // k-step st.  d_idx 64 / B_k 64: a block (64 contiguous keys) is loaded as
+  // whole rows, lane l taking 16-byte unit 64 c + l of load c (1 KiB per
+  // load), and goes through the wave's LDS rows into the operand layout
+  // (214 -> 204 us for 64 sequences x 4 rows at 128K); the wider variants
+  // load the operands directly (staged, they spill or lose occupancy).
+  constexpr bool kWhole = D_IDX == 64 && BK == 64;
   const uint16_t* kbase = index_k + (PAGED ? 0 : ur.g.kv_start) * D_IDX + h * (D_IDX / 2);
-
   auto load_a = [&](int kb, bf16x8 (&a)[MT][KS]) {
+    if constexpr (kWhole) {
+      const uint16_t* sb = index_k + (PAGED ? kbk.template row_as<true>(kb) : ur.g.kv_start + static_cast<int64_t>(kb) * BK) * D_IDX;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + 32 * i + n) * D_IDX
-                                 : kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
+      for (int c = 0; c < MT * KS; ++c) a[c / KS][c % KS] = ld_bf16x8(sb + 8 * (kWave * c + lane));
+    } else {
 #pragma unroll
-      for (int st = 0; st < KS; ++st) a[i][st] = ld_bf16x8(kp + 8 * st);
+      for (int i = 0; i < MT; ++i) {
+        const uint16_t* kp = PAGED ? kbase + (kbk.template row_as<true>(kb) + 32 * i + n) * D_IDX
+                                   : kbase + static_cast<int64_t>(kb * BK + 32 * i + n) * D_IDX;
+#pragma unroll
+        for (int st = 0; st < KS; ++st) a[i][st] = ld_bf16x8(kp + 8 * st);
+      }
     }
+  };
+  // rows padded by 16 bytes: the operand reads (16 rows, one column) are
+  // free of bank conflicts
+  __shared__ __align__(16) uint16_t ks_lds[kWhole ? kWaves : 1][kWhole ? BK : 1][D_IDX + 8];
+  auto to_operands = [&](bf16x8 (&a)[MT][KS]) {
+    if constexpr (!kWhole) return;
+    auto& rows = ks_lds[threadIdx.x / kWave];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");     // the previous block's reads are done
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int c = 0; c < MT * KS; ++c) {
+      const int u = kWave * c + lane;
+      *reinterpret_cast<bf16x8*>(&rows[u / (D_IDX / 8)][8 * (u % (D_IDX / 8))]) = a[c / KS][c % KS];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int st = 0; st < KS; ++st)
+        a[i][st] = *reinterpret_cast<const bf16x8*>(&rows[32 * i + n][h * (D_IDX / 2) + 8 * st]);
   };
   bf16x8 a[MT][KS], an[MT][KS];
   float mb[kSliceBlocks];
@@ -377,6 +410,7 @@ __global__ __launch_bounds__(256) void index_block_max_wave_kernel(
     if (kb < kb1) {                                   // uniform
       // next block in flight during this one (clamped, unconditional load)
       load_a(kb + 1 < kb1 ? kb + 1 : kb, an);
+      to_operands(a);
       f32x16 acc[MT][2];
 #pragma unroll
       for (int t = 0; t < MT; ++t) {
