@@ -477,22 +477,27 @@ def test_index_exact_ties(case):
 
 # Decode-shaped batches (one query row per sequence) with exact score ties
 # among key blocks: name, sequences, context, H_kv, topk, repeat period of
-# each sequence's key blocks (0: zero index queries, every score equal).
-# The first three go one wave per index row (a Top-k of at most 33 over at
-# most 8192 blocks, >= 64 rows); the all-equal rows overflow that wave's
-# candidate buffer and are ranked again through the key batch.  The last
-# shares each row among 16 waves (k 64).
-DECODE_TIE_CASES = [
-    ("dec_ties_period7_k16", 64, 8192, 1, 16, 7),
-    ("dec_ties_period5_k32", 32, 65536 - 100, 2, 32, 5),
-    ("dec_ties_all_equal_k32", 16, 135000, 4, 32, 0),
-    ("dec_ties_period3_k64", 16, 100000, 2, 64, 3),
+# each sequence's key blocks (0: zero index queries, every score equal; -1:
+# no repeats, the boundary cases of the kernel choice).  One wave per index
+# row takes a Top-k of at most 33 over at most 8192 blocks with >= 64 rows;
+# the all-equal rows overflow that wave's candidate buffer and are ranked
+# again through the key batch.  16 waves share each row otherwise (k 34 and
+# 64, fewer rows, longer rows).
+DECODE_TIE_CASES = [                           # ..., the Top-k kernel the call must launch
+    ("dec_ties_period7_k16", 64, 8192, 1, 16, 7, "rows"),
+    ("dec_ties_period5_k32", 32, 65536 - 100, 2, 32, 5, "rows"),
+    ("dec_ties_all_equal_k32", 16, 135000, 4, 32, 0, "rows"),
+    ("dec_ties_period3_k64", 16, 100000, 2, 64, 3, "split"),
+    ("dec_rows_k33_64rows", 32, 30000, 2, 33, -1, "rows"),
+    ("dec_split_k34_64rows", 32, 30000, 2, 34, -1, "split"),
+    ("dec_split_k33_32rows", 16, 30000, 2, 33, -1, "split"),
+    ("dec_rows_8192_blocks", 8, 8192 * 64, 8, 16, -1, "rows"),
 ]
 
 
 @pytest.mark.parametrize("case", DECODE_TIE_CASES, ids=[c[0] for c in DECODE_TIE_CASES])
 def test_decode_index_exact_ties(case):
-    name, nseq, ctx, H_kv, topk, period = case
+    name, nseq, ctx, H_kv, topk, period, kernel = case
     _say(f"[decode ties] {name}: {nseq} x 1 row at {ctx}, H_kv {H_kv}, k {topk}")
     p = synth.packed_problem(name, [1] * nseq, [ctx] * nseq, num_q_heads=2 * H_kv, num_kv_heads=H_kv, d_idx=64,
                              block_size=64, topk=topk, seed=zlib.crc32(name.encode()) % 10000)
@@ -500,22 +505,34 @@ def test_decode_index_exact_ties(case):
     rng = np.random.default_rng(p.seed)
     iq = rng.standard_normal((nseq, H_kv, 64), dtype=np.float32)
     ik = rng.standard_normal((nseq * ctx, 64), dtype=np.float32)
-    if period:
+    if period > 0:
         for s in range(nseq):
             seq = ik[s * ctx:(s + 1) * ctx]
             pat = seq[:period * B].copy()
             reps = -(-ctx // (period * B))
             seq[:] = np.tile(pat, (reps, 1))[:ctx]
-    else:
+    elif period == 0:
         iq[:] = 0
     iq, ik = synth.bf16_bits_from_f32(iq), synth.bf16_bits_from_f32(ik)
     dev = torch.device("cuda")
     seqs = msa.Seqs.from_problem(p, dev)
-    ids = msa.index_topk(to_dev(iq), to_dev(ik), seqs, B, topk)
-    torch.cuda.synchronize()
+    msa.profile_reset()
+    msa.profile_enable(True)
+    try:
+        ids = msa.index_topk(to_dev(iq), to_dev(ik), seqs, B, topk)
+        torch.cuda.synchronize()
+    finally:
+        msa.profile_enable(False)
+    launched = msa.profile_read()
+    msa.profile_reset()
+    assert f"index_topk_{kernel}_kernel" in launched, f"expected the {kernel} Top-k kernel, launched {sorted(launched)}"
     lay = O.layout_of(p)
-    ids_ora, _ = O.select_blocks(iq, ik, lay, B, topk, rows=list(range(nseq)))
+    ids_ora, gaps = O.select_blocks(iq, ik, lay, B, topk, rows=list(range(nseq)))
     got = ids.cpu().numpy()
+    if period < 0:                   # random scores: the oracle's gap rule decides near-ties
+        check_block_ids(got, ids_ora, gaps, {"index_q": iq, "index_k": ik}, lay, B, topk, list(range(nseq)))
+        _say(f"  {nseq} rows x {H_kv} groups checked")
+        return
     bad = [(r, g) for r in range(nseq) for g in range(H_kv) if not np.array_equal(got[r, g], ids_ora[r, g])]
     _say(f"  {nseq} rows x {H_kv} groups, {len(bad)} differ")
     assert not bad, f"first differing (row, group) {bad[0]}: {got[bad[0][0], bad[0][1]]} vs oracle"
