@@ -146,25 +146,30 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
     const int bb = ids ? my_b : slot0 + lane;
     if (p >= 0 && slot0 + lane < slot1 && bb >= 0 && bb <= p / BK) my_pg = kbk.table[kbk.page_index(bb)];
   }
-  for (int slot = slot0; slot < slot1 && p >= 0; ++slot) {
-    const int b = ids ? __builtin_amdgcn_readlane(my_b, slot - slot0) : slot;
-    if (b < 0 || b > p / BK) continue;               // padding, or a block with no visible token
+  // 64-key blocks: each load instruction takes whole K rows (bf16: 4 rows of
+  // 256 bytes, 16 lanes per row; E4M3: 8 rows of 128 bytes) -- the rows are
+  // scattered at the cache's token stride, and whole rows per instruction are
+  // served faster than 64- or 32-byte pieces of 16 rows -- and the block goes
+  // through LDS into the MFMA operand layout (bf16: 111 -> 107 us per 128K
+  // decode step).  128-key blocks (equal or slower staged) load the operands
+  // directly.
+  constexpr bool kStageK = BK == 64;
+  Raw<T> ka[BK / 16][kHeadDim / 32];
+  u32x4 kw[sizeof(T) == 1 && kStageK ? BK / 8 : 1];     // E4M3 whole rows before staging
+  Raw<T> vraw[BK / 16][4];
+  // K and raw V of slot j (a valid slot of the current window) are requested;
+  // the next valid slot's loads go out as soon as these registers are free
+  // (K after the S^T MFMAs, V after its LDS staging), so they fly under this
+  // block's softmax and O^T MFMAs.
+  auto block_of = [&](int slot) { return ids ? __builtin_amdgcn_readlane(my_b, slot - slot0) : slot; };
+  auto row_of = [&](int slot, int b) -> int64_t {
+    return PAGED ? kbk.block_row(__builtin_amdgcn_readlane(my_pg, slot - slot0), b) : 0;
+  };
+  auto load_k = [&](int slot) {
+    const int b = block_of(slot);
     const int key0 = b * BK;
-    // K (A operands of S^T) and raw V of this block are requested together;
-    // S^T and the softmax run while V is still in flight.
-    // paged: the block's page (keys addressed inside it); else keys from kv_start
-    const int64_t page_row = PAGED ? kbk.block_row(__builtin_amdgcn_readlane(my_pg, slot - slot0), b) : 0;
-    // 64-key blocks: each load instruction takes whole K rows (bf16: 4 rows
-    // of 256 bytes, 16 lanes per row; E4M3: 8 rows of 128 bytes) -- the rows
-    // are scattered at the cache's token stride, and whole rows per
-    // instruction are served faster than 64- or 32-byte pieces of 16 rows --
-    // and the block goes through LDS into the MFMA operand layout (bf16: 111
-    // -> 107 us per 128K decode step).  128-key blocks (equal or slower
-    // staged) load the operands directly.
-    constexpr bool kStageK = BK == 64;
-    Raw<T> ka[BK / 16][kHeadDim / 32];
+    const int64_t page_row = row_of(slot, b);
     if constexpr (kStageK && sizeof(T) == 1) {
-      u32x4 kw[BK / 8];
 #pragma unroll
       for (int i = 0; i < BK / 8; ++i) {
         const int kr = 8 * i + (lane >> 3);                 // key row of this lane: lanes 8 (lane / 8) .. + 7
@@ -172,15 +177,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
         const T* kp = (PAGED ? krow_base + (page_row + kr) * kv_stride : krow_base + static_cast<int64_t>(key) * kv_stride) + 16 * (lane & 7);
         kw[i] = key < g.kv_len ? *reinterpret_cast<const u32x4*>(kp) : u32x4{};
       }
-      wave_lds_order();                               // the previous block's V^T reads are done
-#pragma unroll
-      for (int i = 0; i < BK / 8; ++i) *reinterpret_cast<u32x4*>(&sm.kr8[8 * i + (lane >> 3)][16 * (lane & 7)]) = kw[i];
-      wave_lds_order();                               // K staged
-#pragma unroll
-      for (int i = 0; i < BK / 16; ++i)
-#pragma unroll
-        for (int ks = 0; ks < kHeadDim / 32; ++ks)
-          ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr8[16 * i + n][32 * ks + 8 * q4]);
     } else if constexpr (kStageK) {
 #pragma unroll
       for (int i = 0; i < BK / 16; ++i)
@@ -200,93 +196,125 @@ __global__ __launch_bounds__(64 * kAttnWaves) void attn_rows_kernel(
         for (int ks = 0; ks < kHeadDim / 32; ++ks) ka[i][ks] = key < g.kv_len ? load_raw(kp + 32 * ks) : Raw<T>{};
       }
     }
-    Raw<T> vraw[BK / 16][4];
+  };
+  auto load_v = [&](int slot) {
+    const int b = block_of(slot);
     if constexpr (PAGED)
-      load_v_raw<BK, T>(vbase + page_row * kv_stride, kv_stride, 0, g.kv_len - key0, vraw);
+      load_v_raw<BK, T>(vbase + row_of(slot, b) * kv_stride, kv_stride, 0, g.kv_len - b * BK, vraw);
     else
-      load_v_raw<BK, T>(vbase, kv_stride, key0, g.kv_len, vraw);
-
-    if constexpr (kStageK && sizeof(T) == 2) {
-      wave_lds_order();                               // the previous block's V^T reads are done
-#pragma unroll
-      for (int i = 0; i < BK / 16; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          *reinterpret_cast<Raw<T>*>(&sm.kr[16 * i + 4 * j + q4][8 * n]) = ka[i][j];
-      wave_lds_order();                               // K staged
-#pragma unroll
-      for (int i = 0; i < BK / 16; ++i)
-#pragma unroll
-        for (int ks = 0; ks < kHeadDim / 32; ++ks)
-          ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr[16 * i + n][32 * ks + 8 * q4]);
+      load_v_raw<BK, T>(vbase, kv_stride, b * BK, g.kv_len, vraw);
+  };
+  // windows of 64 slots (one slot per lane in the validity ballot)
+  for (int w0 = slot0; w0 < slot1 && p >= 0; w0 += kWave) {
+    const int bl = ids ? my_b : w0 + lane;
+    const bool vl = w0 + lane < slot1 && bl >= 0 && bl <= p / BK;
+    uint64_t pend = __ballot(vl);
+    int slot = pend != 0ull ? w0 + __ffsll(static_cast<unsigned long long>(pend)) - 1 : -1;
+    if (slot >= 0) {
+      load_k(slot);
+      load_v(slot);
     }
-    // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
-    f32x4 st[BK / 16];
-#pragma unroll
-    for (int i = 0; i < BK / 16; ++i) {
-      st[i] = f32x4{};
-#pragma unroll
-      for (int ks = 0; ks < kHeadDim / 32; ++ks) st[i] = mfma16x16x32(widen_bf16x8(ka[i][ks]), bq[ks], st[i]);
-    }
-    // lane (n, q4) holds keys 16i + 4*q4 + e of head n
-    float bmax = -INFINITY;
-#pragma unroll
-    for (int i = 0; i < BK / 16; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = key0 + 16 * i + 4 * q4 + e;
-        float z = st[i][e] * scale_log2;
-        z = key <= p ? z : -INFINITY;
-        st[i][e] = z;
-        bmax = fmaxf(bmax, z);
+    while (slot >= 0) {
+      pend &= pend - 1;
+      const int next = pend != 0ull ? w0 + __ffsll(static_cast<unsigned long long>(pend)) - 1 : -1;
+      const int b = block_of(slot);
+      const int key0 = b * BK;
+      if constexpr (kStageK && sizeof(T) == 1) {
+        wave_lds_order();                               // the previous block's V^T reads are done
+  #pragma unroll
+        for (int i = 0; i < BK / 8; ++i) *reinterpret_cast<u32x4*>(&sm.kr8[8 * i + (lane >> 3)][16 * (lane & 7)]) = kw[i];
+        wave_lds_order();                               // K staged
+  #pragma unroll
+        for (int i = 0; i < BK / 16; ++i)
+  #pragma unroll
+          for (int ks = 0; ks < kHeadDim / 32; ++ks)
+            ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr8[16 * i + n][32 * ks + 8 * q4]);
       }
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
-    const float m_new = fmaxf(m_run, bmax);
-    const float alpha = exp2_hw(m_run - m_new);
-    float lsum = 0.f;
-#pragma unroll
-    for (int i = 0; i < BK / 16; ++i)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const float pe = exp2_hw(st[i][e] - m_new);
-        st[i][e] = pe;
-        lsum += pe;
+      if constexpr (kStageK && sizeof(T) == 2) {
+        wave_lds_order();                               // the previous block's V^T reads are done
+  #pragma unroll
+        for (int i = 0; i < BK / 16; ++i)
+  #pragma unroll
+          for (int j = 0; j < 4; ++j)
+            *reinterpret_cast<Raw<T>*>(&sm.kr[16 * i + 4 * j + q4][8 * n]) = ka[i][j];
+        wave_lds_order();                               // K staged
+  #pragma unroll
+        for (int i = 0; i < BK / 16; ++i)
+  #pragma unroll
+          for (int ks = 0; ks < kHeadDim / 32; ++ks)
+            ka[i][ks] = *reinterpret_cast<const Raw<T>*>(&sm.kr[16 * i + n][32 * ks + 8 * q4]);
       }
-    lsum += __shfl_xor(lsum, 16);
-    lsum += __shfl_xor(lsum, 32);
-    l_run = l_run * alpha + lsum;
-    m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < kHeadDim / 16; ++t) acc[t] *= alpha;
+      // S^T tiles: keys 16i..16i+15 (rows) x heads (columns)
+      f32x4 st[BK / 16];
+  #pragma unroll
+      for (int i = 0; i < BK / 16; ++i) {
+        st[i] = f32x4{};
+  #pragma unroll
+        for (int ks = 0; ks < kHeadDim / 32; ++ks) st[i] = mfma16x16x32(widen_bf16x8(ka[i][ks]), bq[ks], st[i]);
+      }
+      if (next >= 0) load_k(next);
+      // lane (n, q4) holds keys 16i + 4*q4 + e of head n
+      float bmax = -INFINITY;
+  #pragma unroll
+      for (int i = 0; i < BK / 16; ++i)
+  #pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = key0 + 16 * i + 4 * q4 + e;
+          float z = st[i][e] * scale_log2;
+          z = key <= p ? z : -INFINITY;
+          st[i][e] = z;
+          bmax = fmaxf(bmax, z);
+        }
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 16));
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 32));
+      const float m_new = fmaxf(m_run, bmax);
+      const float alpha = exp2_hw(m_run - m_new);
+      float lsum = 0.f;
+  #pragma unroll
+      for (int i = 0; i < BK / 16; ++i)
+  #pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float pe = exp2_hw(st[i][e] - m_new);
+          st[i][e] = pe;
+          lsum += pe;
+        }
+      lsum += __shfl_xor(lsum, 16);
+      lsum += __shfl_xor(lsum, 32);
+      l_run = l_run * alpha + lsum;
+      m_run = m_new;
+  #pragma unroll
+      for (int t = 0; t < kHeadDim / 16; ++t) acc[t] *= alpha;
 
-    wave_lds_order();                                 // the previous block's V^T reads are done
-    store_v_transposed<BK>(sm, vraw);
-    // P^T as the B operand: k-step u covers keys 32u..32u+31; lane (n, q4)
-    // supplies logical k = 8*q4 + e <-> key 32u + 4*q4 + e (e < 4) and
-    // 32u + 16 + 4*q4 + e - 4 (e >= 4), exactly the keys its S^T tiles hold.
-    wave_lds_order();                                 // V staged
-#pragma unroll
-    for (int u = 0; u < BK / 32; ++u) {
-      bf16x8 bp;
-      {
-        uint4 w;
-        w.x = pack_bf16x2(st[2 * u][0], st[2 * u][1]);
-        w.y = pack_bf16x2(st[2 * u][2], st[2 * u][3]);
-        w.z = pack_bf16x2(st[2 * u + 1][0], st[2 * u + 1][1]);
-        w.w = pack_bf16x2(st[2 * u + 1][2], st[2 * u + 1][3]);
-        bp = __builtin_bit_cast(bf16x8, w);
+      wave_lds_order();                                 // the previous block's V^T reads are done
+      store_v_transposed<BK>(sm, vraw);
+      if (next >= 0) load_v(next);
+      // P^T as the B operand: k-step u covers keys 32u..32u+31; lane (n, q4)
+      // supplies logical k = 8*q4 + e <-> key 32u + 4*q4 + e (e < 4) and
+      // 32u + 16 + 4*q4 + e - 4 (e >= 4), exactly the keys its S^T tiles hold.
+      wave_lds_order();                                 // V staged
+  #pragma unroll
+      for (int u = 0; u < BK / 32; ++u) {
+        bf16x8 bp;
+        {
+          uint4 w;
+          w.x = pack_bf16x2(st[2 * u][0], st[2 * u][1]);
+          w.y = pack_bf16x2(st[2 * u][2], st[2 * u][3]);
+          w.z = pack_bf16x2(st[2 * u + 1][0], st[2 * u + 1][1]);
+          w.w = pack_bf16x2(st[2 * u + 1][2], st[2 * u + 1][3]);
+          bp = __builtin_bit_cast(bf16x8, w);
+        }
+  #pragma unroll
+        for (int t = 0; t < kHeadDim / 16; ++t) {
+          // A operand V^T: row d = 16t + n (lane's m), the same key mapping.
+          const uint16_t* vr = &sm.vt[16 * t + n][32 * u + 4 * q4];
+          uint4 w;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+          w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
+          acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, w), bp, acc[t]);
+        }
       }
-#pragma unroll
-      for (int t = 0; t < kHeadDim / 16; ++t) {
-        // A operand V^T: row d = 16t + n (lane's m), the same key mapping.
-        const uint16_t* vr = &sm.vt[16 * t + n][32 * u + 4 * q4];
-        uint4 w;
-        const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-        w.x = lo.x; w.y = lo.y; w.z = hi.x; w.w = hi.y;
-        acc[t] = mfma16x16x32(__builtin_bit_cast(bf16x8, w), bp, acc[t]);
-      }
+      slot = next;
     }
   }
 
