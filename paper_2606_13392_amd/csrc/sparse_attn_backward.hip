@@ -527,18 +527,22 @@ __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
   for (int c8 = lane; c8 < E / 8; c8 += kWave) {
     float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     uint64_t vm = valid;
-    while (vm != 0ull) {
-      constexpr int kBatch = 8;
-      int js[kBatch];
+    // batches of 8 valid slots in slot order; batch n + 1's loads are issued
+    // before batch n is accumulated (two in flight; the sum order is unchanged)
+    constexpr int kBatch = 8;
+    auto take = [&](int (&js)[kBatch]) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         js[u] = vm != 0ull ? __ffsll(static_cast<unsigned long long>(vm)) - 1 : -1;
         vm &= vm - 1;
       }
-      u32x4 w[kBatch];
+    };
+    auto issue = [&](const int (&js)[kBatch], u32x4 (&w)[kBatch]) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u)
         w[u] = load_raw(src + static_cast<int64_t>(js[u] >= 0 ? js[u] : js[0]) * E + 8 * c8);
+    };
+    auto accumulate = [&](const int (&js)[kBatch], const u32x4 (&w)[kBatch]) {
 #pragma unroll
       for (int u = 0; u < kBatch; ++u) {
         if (js[u] < 0) break;
@@ -548,6 +552,19 @@ __global__ __launch_bounds__(64 * kCombWaves) void bwd_dq_combine_kernel(
           acc[2 * e + 1] += __uint_as_float(w[u][e] & 0xFFFF0000u);
         }
       }
+    };
+    int ja[kBatch], jb[kBatch];
+    u32x4 wa[kBatch], wb[kBatch];
+    take(ja);
+    if (ja[0] >= 0) issue(ja, wa);
+    while (ja[0] >= 0) {
+      take(jb);
+      if (jb[0] >= 0) issue(jb, wb);
+      accumulate(ja, wa);
+      if (jb[0] < 0) break;
+      take(ja);
+      if (ja[0] >= 0) issue(ja, wa);
+      accumulate(jb, wb);
     }
     uint4 o;
     o.x = pack_bf16x2(acc[0] * scale, acc[1] * scale);
