@@ -753,8 +753,8 @@ def main():
                     help="prefill rows the dense baseline runs (the last ones; 0 = all)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py: this build runs the MSA hot path on one GPU only; --gpus must be 1 "
-              "(the multi-GPU sharding is a design note, not an implementation)", file=sys.stderr)
+        print("bench.py: the library runs the MSA hot path on one GPU; --gpus must be 1 "
+              "(sharding across GPUs is not implemented)", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2606_13392_amd import msa

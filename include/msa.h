@@ -84,7 +84,7 @@ extern "C" {
 /* Status codes returned by every int-valued call. */
 #define MSA_OK 0
 #define MSA_ERR_INVALID (-1)     /* null pointer, negative or inconsistent size, H_q % H_kv != 0 ... */
-#define MSA_ERR_UNSUPPORTED (-2) /* a valid shape this build has no kernel for */
+#define MSA_ERR_UNSUPPORTED (-2) /* a valid shape the library has no kernel for */
 #define MSA_ERR_WORKSPACE (-3)   /* workspace smaller than the *_workspace_size() value */
 #define MSA_ERR_HIP (-4)         /* a HIP launch failed (the HIP error is consumed) */
 

@@ -61,3 +61,17 @@ def test_traffic_records_are_well_formed_and_read_by_bench():
         got = bench.measured_traffic(r["kernel"], r["workload"])
         # current sources: the record's bytes; changed sources: no traffic figure
         assert got == (float(r["bytes_per_launch"]) if h.hexdigest() == r["sources_sha256"] else None)
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py runs one GPU: --gpus N > 1 exits with status 2 and a message,
+    before touching a GPU."""
+    import subprocess
+    import sys
+    from pathlib import Path
+    root = Path(__file__).resolve().parents[1]
+    res = subprocess.run([sys.executable, str(root / "bench.py"), "--gpus", "2"], capture_output=True, text=True,
+                         timeout=120)
+    assert res.returncode == 2
+    assert "--gpus must be 1" in res.stderr
+    assert res.stdout == ""
