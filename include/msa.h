@@ -34,8 +34,11 @@
  *   on one stream.
  * - Global state: the opt-in kernel timing at the end of this header, the
  *   grid size of each persistent kernel (derived from the device's occupancy
- *   on first use and cached in an atomic).  Concurrent calls from several host
- *   threads are safe when they use distinct outputs and workspaces.
+ *   on first use and cached in an atomic), and msa_index_topk_noalloc's
+ *   file-scope device scratch array with its per-device address table.
+ *   Concurrent calls from several host threads are safe when they use
+ *   distinct outputs and workspaces (msa_index_topk_noalloc calls on one GPU
+ *   share its scratch array and must not overlap).
  * - NaN or Inf inputs give unspecified (but memory-safe) results.
  *
  * Sequence layout (struct msa_seqs)
@@ -364,7 +367,7 @@ int msa_sparse_kl_backward(const void* index_q, const void* index_k, const void*
  * While enabled, every kernel a call launches is bracketed by a pair of HIP
  * events recorded on the call's stream, filed under the kernel's name (e.g.
  * "kvo_attn_kernel", "index_block_max_lds_kernel").  The events are created
- * on first use and kept for reuse; they are the library's only global state.
+ * on first use and kept for reuse (global state of the timer alone).
  *
  *   msa_profile_enable(on)   on != 0 starts recording for later calls, 0 stops.
  *   msa_profile_reset()      forgets the launches recorded so far.
