@@ -27,11 +27,12 @@
  *   their arguments on the host, launch kernels and return.  Results are
  *   valid once the stream has reached them.  Nothing is launched when a call
  *   returns an error.  No call synchronises the host with the device.
- * - The library allocates no device memory.  Calls that need scratch space take
- *   a caller-provided `workspace` of at least the size returned by the
- *   matching *_workspace_size() query; the workspace is free again once the
- *   stream has executed the call.  Calls that share a workspace must be ordered
- *   on one stream.
+ * - No call allocates device memory.  Calls that need scratch space take a
+ *   caller-provided `workspace` of at least the size returned by the matching
+ *   *_workspace_size() query; the workspace is free again once the stream has
+ *   executed the call.  Calls that share a workspace must be ordered on one
+ *   stream.  (msa_index_topk_noalloc uses the library's static device array
+ *   instead, see below.)
  * - Global state: the opt-in kernel timing at the end of this header, the
  *   grid size of each persistent kernel (derived from the device's occupancy
  *   on first use and cached in an atomic), and msa_index_topk_noalloc's
